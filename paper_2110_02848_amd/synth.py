@@ -1,0 +1,333 @@
+"""Seeded synthetic transducers in the structure-of-arrays / CSR layout.
+
+This module only *builds inputs*.  It holds none of the composition's
+arithmetic, so both the GPU path and the CPU oracle may consume its arrays.
+
+Graph format (a plain dict of numpy arrays), following the structure-of-arrays
+description of Section 3.2 of the paper (start/accept arrays of V booleans,
+five E-arrays of arc data, an out-arc offset array of V+1 entries):
+
+    num_states : int                V >= 0
+    arc_offset : int32[V+1]         arcs of state v are [arc_offset[v], arc_offset[v+1])
+    src, dst   : int32[E]           source / destination state of each arc
+    ilabel     : int32[E]           input label, 0 is epsilon, real labels >= 1
+    olabel     : int32[E]           output label, 0 is epsilon
+    weight     : float32[E]         log-semiring weight
+    start      : uint8[V]           1 = start state
+    accept     : uint8[V]           1 = accepting state
+
+Arcs are stored grouped by source state ("consecutive by node"); inside a state
+they keep the order in which they were generated.
+
+Workloads (Section 4 of the paper; the paper's LibriSpeech lexicon is not
+available, so uniform random spellings stand in for it):
+
+* random FST pairs (Section 4.1 recipe, with epsilon labels and several
+  accepting states): ``random_pair_config(i, seed)`` for i in 1..3;
+* emissions (A) and lexicon (B) graphs (Section 4.2 recipe):
+  ``emissions_lexicon_config(i, seed)`` for i in 4..5.
+"""
+from __future__ import annotations
+
+import hashlib
+from dataclasses import dataclass
+
+import numpy as np
+
+EPS = 0
+
+GRAPH_KEYS = ("arc_offset", "src", "dst", "ilabel", "olabel", "weight", "start", "accept")
+
+
+# --------------------------------------------------------------------------
+# construction helpers
+# --------------------------------------------------------------------------
+
+def from_arcs(num_states, arcs, start=(0,), accept=()):
+    """Build a graph dict from a list of ``(src, dst, ilabel, olabel, weight)``.
+
+    Arcs are grouped by source state with a stable sort, so arcs that share a
+    source keep their relative order.  ``start`` and ``accept`` are iterables of
+    state ids.
+    """
+    V = int(num_states)
+    arcs = list(arcs)
+    E = len(arcs)
+    src = np.array([a[0] for a in arcs], dtype=np.int32).reshape(E)
+    order = np.argsort(src, kind="stable")
+    src = src[order]
+    dst = np.array([a[1] for a in arcs], dtype=np.int32).reshape(E)[order]
+    il = np.array([a[2] for a in arcs], dtype=np.int32).reshape(E)[order]
+    ol = np.array([a[3] for a in arcs], dtype=np.int32).reshape(E)[order]
+    w = np.array([a[4] for a in arcs], dtype=np.float32).reshape(E)[order]
+    st = np.zeros(V, dtype=np.uint8)
+    ac = np.zeros(V, dtype=np.uint8)
+    for s in start:
+        st[s] = 1
+    for s in accept:
+        ac[s] = 1
+    return _finish(V, src, dst, il, ol, w, st, ac)
+
+
+def _finish(V, src, dst, il, ol, w, st, ac):
+    counts = np.bincount(src, minlength=V).astype(np.int64) if len(src) else np.zeros(V, np.int64)
+    off = np.zeros(V + 1, dtype=np.int32)
+    if V:
+        off[1:] = np.cumsum(counts)
+    g = dict(
+        num_states=int(V),
+        arc_offset=off,
+        src=np.ascontiguousarray(src, dtype=np.int32),
+        dst=np.ascontiguousarray(dst, dtype=np.int32),
+        ilabel=np.ascontiguousarray(il, dtype=np.int32),
+        olabel=np.ascontiguousarray(ol, dtype=np.int32),
+        weight=np.ascontiguousarray(w, dtype=np.float32),
+        start=np.ascontiguousarray(st, dtype=np.uint8),
+        accept=np.ascontiguousarray(ac, dtype=np.uint8),
+    )
+    check_graph(g)
+    return g
+
+
+def check_graph(g):
+    """Raise ValueError unless ``g`` is a well-formed graph dict."""
+    V = g["num_states"]
+    off = g["arc_offset"]
+    E = len(g["src"])
+    if V < 0 or off.shape != (V + 1,):
+        raise ValueError("arc_offset must have V+1 entries")
+    if off[0] != 0 or off[-1] != E or np.any(np.diff(off.astype(np.int64)) < 0):
+        raise ValueError("arc_offset must be monotone from 0 to E")
+    for k in ("dst", "ilabel", "olabel", "weight"):
+        if len(g[k]) != E:
+            raise ValueError(f"{k} must have E entries")
+    if E:
+        expect_src = np.repeat(np.arange(V, dtype=np.int32), np.diff(off))
+        if not np.array_equal(expect_src, g["src"]):
+            raise ValueError("src inconsistent with arc_offset")
+        if g["dst"].min() < 0 or g["dst"].max() >= V:
+            raise ValueError("dst out of range")
+        if g["ilabel"].min() < 0 or g["olabel"].min() < 0:
+            raise ValueError("negative label")
+    for k in ("start", "accept"):
+        if g[k].shape != (V,) or (V and g[k].max() > 1):
+            raise ValueError(f"{k} must hold V entries of 0/1")
+
+
+def graph_sha256(g):
+    h = hashlib.sha256()
+    h.update(np.int64(g["num_states"]).tobytes())
+    for k in GRAPH_KEYS:
+        h.update(np.ascontiguousarray(g[k]).tobytes())
+    return h.hexdigest()
+
+
+def num_arcs(g):
+    return int(len(g["src"]))
+
+
+# --------------------------------------------------------------------------
+# random transducers (Section 4.1)
+# --------------------------------------------------------------------------
+
+def random_fst(rng, V, degree, n_sym, p_eps, p_accept, start=(0,)):
+    """Every state gets exactly ``degree`` out-arcs.
+
+    Destinations are uniform over all states (self-loops allowed).  Input and
+    output labels are drawn independently: epsilon with probability ``p_eps``,
+    otherwise uniform over ``1..n_sym``.  Weights are N(0,1) drawn in float64
+    and rounded to float32.  Each state accepts independently with
+    probability ``p_accept``.
+    """
+    E = V * degree
+    src = np.repeat(np.arange(V, dtype=np.int32), degree)
+    dst = rng.integers(0, V, size=E, dtype=np.int64).astype(np.int32)
+    il_eps = rng.random(E) < p_eps
+    il_sym = rng.integers(1, n_sym + 1, size=E, dtype=np.int64)
+    ol_eps = rng.random(E) < p_eps
+    ol_sym = rng.integers(1, n_sym + 1, size=E, dtype=np.int64)
+    il = np.where(il_eps, EPS, il_sym).astype(np.int32)
+    ol = np.where(ol_eps, EPS, ol_sym).astype(np.int32)
+    w = rng.standard_normal(E).astype(np.float32)
+    ac = (rng.random(V) < p_accept).astype(np.uint8)
+    st = np.zeros(V, dtype=np.uint8)
+    for s in start:
+        if V:
+            st[s] = 1
+    return _finish(V, src, dst, il, ol, w, st, ac)
+
+
+@dataclass(frozen=True)
+class RandomSpec:
+    V: int
+    degree: int
+    n_sym: int
+    p_eps: float
+    p_accept: float
+
+
+RANDOM_SPECS = {
+    1: RandomSpec(64, 4, 16, 0.10, 0.10),
+    2: RandomSpec(1000, 8, 32, 0.05, 0.10),
+    3: RandomSpec(5000, 4, 64, 0.05, 0.05),
+}
+
+
+def _rngs(cfg, seed):
+    ss = np.random.SeedSequence([int(cfg), int(seed)])
+    return [np.random.default_rng(s) for s in ss.spawn(2)]
+
+
+def random_pair_config(cfg, seed=0):
+    spec = RANDOM_SPECS[cfg]
+    ra, rb = _rngs(cfg, seed)
+    A = random_fst(ra, spec.V, spec.degree, spec.n_sym, spec.p_eps, spec.p_accept)
+    B = random_fst(rb, spec.V, spec.degree, spec.n_sym, spec.p_eps, spec.p_accept)
+    return A, B
+
+
+# --------------------------------------------------------------------------
+# emissions and lexicon (Section 4.2)
+# --------------------------------------------------------------------------
+
+def emissions(rng, T, C):
+    """Linear acceptor with T frames and C token arcs per frame.
+
+    State t has arcs t -> t+1 labelled c:c for c = 1..C, in label order, with
+    weight float32(log_softmax(z_t)[c]) for logits z_t ~ N(0,1)^C drawn in
+    float64.  State 0 is the start state and state T the only accepting state.
+    Returns the graph and the float32 [T, C] emission table.
+    """
+    z = rng.standard_normal((T, C))
+    m = z.max(axis=1, keepdims=True)
+    logp = z - m - np.log(np.exp(z - m).sum(axis=1, keepdims=True))
+    table = logp.astype(np.float32)
+    V = T + 1
+    src = np.repeat(np.arange(T, dtype=np.int32), C)
+    dst = src + 1
+    lab = np.tile(np.arange(1, C + 1, dtype=np.int32), T)
+    st = np.zeros(V, np.uint8)
+    st[0] = 1
+    ac = np.zeros(V, np.uint8)
+    ac[T] = 1
+    g = _finish(V, src, dst, lab, lab.copy(), table.reshape(-1).copy(), st, ac)
+    return g, table
+
+
+def lexicon(rng, W, C, len_lo, len_hi):
+    """Lexicon transducer over C tokens with W words (word ids 1..W).
+
+    Word lengths are uniform over ``len_lo..len_hi`` and spellings uniform over
+    ``1..C``.  Each word w is a path out of the root (state 0): an arc with
+    epsilon input and output w into p_1, then token arcs tok_j:epsilon from p_j
+    to p_{j+1}, then an epsilon:epsilon arc from p_{L+1} back to the root.  All
+    weights are 0.  The root is the start state and the only accepting state.
+    Returns the graph and the list of spellings.
+    """
+    lens = rng.integers(len_lo, len_hi + 1, size=W, dtype=np.int64)
+    spell = [rng.integers(1, C + 1, size=int(L), dtype=np.int64).astype(np.int32) for L in lens]
+    V = 1 + int(np.sum(lens + 1))
+    E = int(np.sum(lens + 2))
+    src = np.empty(E, np.int32)
+    dst = np.empty(E, np.int32)
+    il = np.empty(E, np.int32)
+    ol = np.empty(E, np.int32)
+    # root arcs first (CSR order): one entry arc per word
+    first_state = 1 + np.concatenate([[0], np.cumsum(lens + 1)[:-1]]).astype(np.int64)
+    src[:W] = 0
+    dst[:W] = first_state
+    il[:W] = EPS
+    ol[:W] = np.arange(1, W + 1)
+    pos = W
+    for w in range(W):
+        L = int(lens[w])
+        p1 = int(first_state[w])
+        s = np.arange(p1, p1 + L, dtype=np.int32)
+        src[pos:pos + L] = s
+        dst[pos:pos + L] = s + 1
+        il[pos:pos + L] = spell[w]
+        ol[pos:pos + L] = EPS
+        pos += L
+        src[pos] = p1 + L
+        dst[pos] = 0
+        il[pos] = EPS
+        ol[pos] = EPS
+        pos += 1
+    order = np.argsort(src, kind="stable")
+    w0 = np.zeros(E, np.float32)
+    st = np.zeros(V, np.uint8)
+    st[0] = 1
+    ac = np.zeros(V, np.uint8)
+    ac[0] = 1
+    g = _finish(V, src[order], dst[order], il[order], ol[order], w0, st, ac)
+    return g, spell
+
+
+@dataclass(frozen=True)
+class LexSpec:
+    T: int
+    C: int
+    W: int
+    len_lo: int
+    len_hi: int
+
+
+LEX_SPECS = {
+    4: LexSpec(100, 28, 1000, 3, 8),
+    5: LexSpec(500, 64, 10000, 3, 10),
+}
+
+
+def emissions_lexicon_config(cfg, seed=0, spec=None):
+    """A = emissions, B = lexicon (so A o B maps token strings to word strings)."""
+    spec = spec or LEX_SPECS[cfg]
+    ra, rb = _rngs(cfg, seed)
+    A, table = emissions(ra, spec.T, spec.C)
+    B, spell = lexicon(rb, spec.W, spec.C, spec.len_lo, spec.len_hi)
+    return A, B, dict(table=table, spellings=spell, spec=spec)
+
+
+def config(cfg, seed=0):
+    """Inputs ``(A, B)`` of workload ``cfg`` (1..5) for a given seed."""
+    if cfg in RANDOM_SPECS:
+        return random_pair_config(cfg, seed)
+    A, B, _ = emissions_lexicon_config(cfg, seed)
+    return A, B
+
+
+CONFIG_NAMES = {
+    1: "random pair V=64 d=4 K=16 p_eps=0.1 p_acc=0.1",
+    2: "random pair V=1000 d=8 K=32 p_eps=0.05 p_acc=0.1",
+    3: "random pair V=5000 d=4 K=64 p_eps=0.05 p_acc=0.05",
+    4: "emissions(T=100,C=28) o lexicon(W=1000,L=3..8)",
+    5: "emissions(T=500,C=64) o lexicon(W=10000,L=3..10)",
+}
+
+
+# --------------------------------------------------------------------------
+# small graphs for tests
+# --------------------------------------------------------------------------
+
+def tiny_random(rng, V, max_degree, n_sym, p_eps, p_accept=0.4, n_start=1):
+    """Tiny random transducer with variable out-degree (0..max_degree)."""
+    arcs = []
+    for s in range(V):
+        d = int(rng.integers(0, max_degree + 1))
+        for _ in range(d):
+            t = int(rng.integers(0, V))
+            il = 0 if rng.random() < p_eps else int(rng.integers(1, n_sym + 1))
+            ol = 0 if rng.random() < p_eps else int(rng.integers(1, n_sym + 1))
+            w = float(np.float32(rng.standard_normal()))
+            arcs.append((s, t, il, ol, w))
+    starts = sorted(set(int(x) for x in rng.integers(0, V, size=n_start)))
+    acc = [s for s in range(V) if rng.random() < p_accept]
+    return from_arcs(V, arcs, start=starts, accept=acc)
+
+
+def identity_fst(n_sym):
+    """One state, start and accepting, with a loop s:s of weight 0 per symbol."""
+    return from_arcs(1, [(0, 0, s, s, 0.0) for s in range(1, n_sym + 1)], start=[0], accept=[0])
+
+
+def empty_graph():
+    return from_arcs(0, [], start=[], accept=[])

@@ -1,0 +1,299 @@
+"""Test helpers: golden-file parsing, structural invariants of a composed graph,
+closed forms for the emissions-lexicon workload, and result comparison.
+
+Everything here reads only the input graphs and a composed graph's arrays; it
+does not call the oracle or the GPU library.
+"""
+from __future__ import annotations
+
+import math
+import os
+from collections import deque
+
+import numpy as np
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+RESULT_KEYS = ("arc_offset", "src", "dst", "ilabel", "olabel", "weight", "arc_a", "arc_b",
+               "start", "accept", "key_a", "key_b", "key_f")
+
+
+def read_golden(name):
+    """Parse ``key: values`` lines (``#`` starts a comment); repeated keys
+    accumulate into a list."""
+    out = {}
+    with open(os.path.join(GOLDEN, name)) as fh:
+        for line in fh:
+            line = line.split("#", 1)[0].strip()
+            if not line:
+                continue
+            k, v = line.split(":", 1)
+            out.setdefault(k.strip(), []).append(v.split())
+    return out
+
+
+def eps_out(A):
+    e = np.zeros(A["num_states"], bool)
+    if len(A["src"]):
+        e[A["src"][A["olabel"] == 0]] = True
+    return e
+
+
+def _bits(x):
+    return np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+
+
+def check_invariants(A, B, C):
+    """Return a list of violated invariants of a canonical composed graph."""
+    errs = []
+    VA, VB = A["num_states"], B["num_states"]
+    V, E = int(C["num_states"]), int(C["num_arcs"])
+    ka = C["key_a"].astype(np.int64)
+    kb = C["key_b"].astype(np.int64)
+    kf = C["key_f"].astype(np.int64)
+    epsA = eps_out(A)
+    if V == 0:
+        if E != 0:
+            errs.append("arcs without states")
+        return errs
+    if ka.min() < 0 or ka.max() >= VA or kb.min() < 0 or kb.max() >= VB:
+        return ["key out of range"]
+    key = (ka * VB + kb) * 2 + kf
+    if np.any(np.diff(key) <= 0):
+        errs.append("states not in strictly ascending key order")
+    if np.any((kf == 1) & ~epsA[ka]):
+        errs.append("filter bit set on a state of A without epsilon output")
+    if len(np.unique(ka * VB + kb)) > VA * VB:
+        errs.append("more (qa, qb) pairs than VA*VB")
+    if V > VB * (VA + int(epsA.sum())):
+        errs.append("more states than VB*(VA + #epsOutA)")
+    st_exp = ((kf == 0) & (A["start"][ka] == 1) & (B["start"][kb] == 1)).astype(np.uint8)
+    ac_exp = ((A["accept"][ka] == 1) & (B["accept"][kb] == 1)).astype(np.uint8)
+    if not np.array_equal(st_exp, C["start"]):
+        errs.append("start flags differ from keys")
+    if not np.array_equal(ac_exp, C["accept"]):
+        errs.append("accept flags differ from keys")
+    off = C["arc_offset"].astype(np.int64)
+    src = C["src"].astype(np.int64)
+    dst = C["dst"].astype(np.int64)
+    if off[0] != 0 or off[-1] != E or np.any(np.diff(off) < 0):
+        errs.append("bad arc_offset")
+    elif not np.array_equal(np.repeat(np.arange(V), np.diff(off)), src):
+        errs.append("src inconsistent with arc_offset")
+    if E:
+        if dst.min() < 0 or dst.max() >= V:
+            return errs + ["dst out of range"]
+        a = C["arc_a"].astype(np.int64)
+        b = C["arc_b"].astype(np.int64)
+        M = (a >= 0) & (b >= 0)
+        EA = (a >= 0) & (b < 0)
+        EB = (a < 0) & (b >= 0)
+        if np.any(~(M | EA | EB)):
+            errs.append("arc without provenance")
+        w = _bits(C["weight"])
+        aa, bb = np.maximum(a, 0), np.maximum(b, 0)
+        # matching moves
+        m = M
+        ok = ((A["olabel"][aa] == B["ilabel"][bb]) & (A["olabel"][aa] != 0)
+              & (ka[src] == A["src"][aa]) & (kb[src] == B["src"][bb])
+              & (ka[dst] == A["dst"][aa]) & (kb[dst] == B["dst"][bb]) & (kf[dst] == 0)
+              & (C["ilabel"] == A["ilabel"][aa]) & (C["olabel"] == B["olabel"][bb])
+              & (w == _bits(A["weight"][aa] + B["weight"][bb])))
+        if np.any(m & ~ok):
+            errs.append("matching arc inconsistent with its provenance")
+        ok = ((A["olabel"][aa] == 0) & (kf[src] == 0) & (ka[src] == A["src"][aa])
+              & (kb[src] == kb[dst]) & (ka[dst] == A["dst"][aa])
+              & (kf[dst] == 0)
+              & (C["ilabel"] == A["ilabel"][aa]) & (C["olabel"] == 0)
+              & (w == _bits(A["weight"][aa])))
+        if np.any(EA & ~ok):
+            errs.append("A-epsilon arc inconsistent with its provenance")
+        ok = ((B["ilabel"][bb] == 0) & (ka[src] == ka[dst]) & (kb[src] == B["src"][bb])
+              & (kb[dst] == B["dst"][bb]) & (kf[dst] == epsA[ka[dst]].astype(np.int64))
+              & (C["ilabel"] == 0) & (C["olabel"] == B["olabel"][bb])
+              & (w == _bits(B["weight"][bb])))
+        if np.any(EB & ~ok):
+            errs.append("B-epsilon arc inconsistent with its provenance")
+        trip = np.stack([src, a, b], axis=1)
+        if len(np.unique(trip, axis=0)) != E:
+            errs.append("duplicate (src, arc_a, arc_b)")
+        lab = np.where(M, A["olabel"][aa].astype(np.int64), 0)
+        big = np.int64(1) << 40
+        order = np.lexsort((np.where(b >= 0, b, big), np.where(a >= 0, a, big), lab, src))
+        if not np.array_equal(order, np.arange(E)):
+            errs.append("arcs not in canonical order")
+    # trim: every state reachable from a start state and reaching an accept state
+    fwd = _reach(V, src, dst, np.flatnonzero(C["start"]))
+    bwd = _reach(V, dst, src, np.flatnonzero(C["accept"]))
+    if not fwd.all():
+        errs.append("inaccessible state")
+    if not bwd.all():
+        errs.append("non-coaccessible state")
+    return errs
+
+
+def _reach(V, frm, to, seeds):
+    seen = np.zeros(V, bool)
+    seen[seeds] = True
+    if len(frm) == 0:
+        return seen
+    order = np.argsort(frm, kind="stable")
+    frm_s, to_s = frm[order], to[order]
+    off = np.searchsorted(frm_s, np.arange(V + 1))
+    frontier = np.asarray(seeds, dtype=np.int64)
+    while len(frontier):
+        lo, hi = off[frontier], off[frontier + 1]
+        cnt = hi - lo
+        if cnt.sum() == 0:
+            break
+        idx = np.repeat(lo - np.concatenate([[0], np.cumsum(cnt)[:-1]]), cnt) + np.arange(cnt.sum())
+        nxt = np.unique(to_s[idx])
+        nxt = nxt[~seen[nxt]]
+        seen[nxt] = True
+        frontier = nxt
+    return seen
+
+
+def compare_results(got, ref, keys=RESULT_KEYS):
+    """Element-wise, bit-exact comparison; returns a list of mismatches."""
+    errs = []
+    if int(got["num_states"]) != int(ref["num_states"]):
+        errs.append(f"num_states {got['num_states']} != {ref['num_states']}")
+    if int(got["num_arcs"]) != int(ref["num_arcs"]):
+        errs.append(f"num_arcs {got['num_arcs']} != {ref['num_arcs']}")
+    if errs:
+        return errs
+    for k in keys:
+        g, r = np.asarray(got[k]), np.asarray(ref[k])
+        if k == "weight":
+            g, r = _bits(g), _bits(r)
+        else:
+            g, r = g.astype(np.int64), r.astype(np.int64)
+        if g.shape != r.shape:
+            errs.append(f"{k}: shape {g.shape} != {r.shape}")
+            continue
+        bad = np.flatnonzero(g != r)
+        if len(bad):
+            i = int(bad[0])
+            errs.append(f"{k}: {len(bad)} mismatches, first at {i}: {g[i]} != {r[i]}")
+    return errs
+
+
+# --------------------------------------------------------------------------
+# emissions o lexicon closed forms
+# --------------------------------------------------------------------------
+
+def lexicon_closed_form(T, spellings):
+    """|V_C| and |E_C| of trim(emissions o lexicon) from the word lengths.
+
+    Root keys (t, root) are accessible iff t is a sum of word lengths and
+    co-accessible iff T - t is; a word instance starting at frame t0 is in C
+    iff (t0, root) is accessible and (t0 + L, root) co-accessible, and then it
+    contributes L + 1 states (p_1 .. p_{L+1}) and L + 2 arcs."""
+    lens = np.array([len(s) for s in spellings], dtype=np.int64)
+    Ls = sorted(set(lens.tolist()))
+    acc = np.zeros(T + 1, bool)
+    acc[0] = True
+    for t in range(1, T + 1):
+        acc[t] = any(t - L >= 0 and acc[t - L] for L in Ls)
+    co = np.zeros(T + 1, bool)
+    co[T] = True
+    for t in range(T - 1, -1, -1):
+        co[t] = any(t + L <= T and co[t + L] for L in Ls)
+    n_by_len = {}
+    for L in Ls:
+        n_by_len[L] = sum(1 for t0 in range(0, T - L + 1) if acc[t0] and co[t0 + L])
+    n = np.array([n_by_len[L] for L in lens], dtype=np.int64)
+    V = int(np.sum((lens + 1) * n)) + int(np.sum(acc & co))
+    E = int(np.sum((lens + 2) * n))
+    return V, E
+
+
+def lexicon_total_score(table, spellings):
+    """Log of the total path sum of emissions o lexicon by a frame recursion
+    (float64): alpha(t) = LSE over words w of alpha(t - L_w) + sum_k E[t-L_w+k,
+    spell_w[k]]; the answer is alpha(T)."""
+    T = table.shape[0]
+    tab = table.astype(np.float64)
+    alpha = np.full(T + 1, -np.inf)
+    alpha[0] = 0.0
+    by_len = {}
+    for w, s in enumerate(spellings):
+        by_len.setdefault(len(s), []).append(np.asarray(s, dtype=np.int64) - 1)
+    for t in range(1, T + 1):
+        terms = []
+        for L, words in by_len.items():
+            if L > t or alpha[t - L] == -np.inf:
+                continue
+            S = np.stack(words)  # [n, L]
+            sc = tab[np.arange(t - L, t)[None, :], S].sum(axis=1)
+            terms.append(alpha[t - L] + sc)
+        if terms:
+            x = np.concatenate(terms)
+            m = x.max()
+            alpha[t] = m + math.log(np.exp(x - m).sum())
+    return alpha[T]
+
+
+def dag_total_score(C):
+    """Log of the total weight of all accepting paths of an acyclic composed
+    graph (float64 forward recursion in topological order)."""
+    V = int(C["num_states"])
+    src = C["src"].astype(np.int64)
+    dst = C["dst"].astype(np.int64)
+    w = C["weight"].astype(np.float64)
+    indeg = np.bincount(dst, minlength=V)
+    order = np.argsort(src, kind="stable")
+    off = np.searchsorted(src[order], np.arange(V + 1))
+    alpha = np.full(V, -np.inf)
+    alpha[C["start"] == 1] = 0.0
+    frontier = np.flatnonzero(indeg == 0)
+    done = 0
+    while len(frontier):
+        done += len(frontier)
+        lo, hi = off[frontier], off[frontier + 1]
+        cnt = hi - lo
+        tot = int(cnt.sum())
+        if tot == 0:
+            break
+        idx = order[np.repeat(lo - np.concatenate([[0], np.cumsum(cnt)[:-1]]), cnt) + np.arange(tot)]
+        np.logaddexp.at(alpha, dst[idx], alpha[src[idx]] + w[idx])
+        dec = np.bincount(dst[idx], minlength=V)
+        before = indeg.copy()
+        indeg -= dec
+        frontier = np.flatnonzero((indeg == 0) & (before > 0))
+    if done != V:
+        raise ValueError("graph is not acyclic")
+    acc = alpha[C["accept"] == 1]
+    m = acc.max()
+    return m + math.log(np.exp(acc - m).sum())
+
+
+def trim_graph(g):
+    """Trim a single transducer (states reachable from a start state and
+    reaching an accept state).  Returns (kept state ids ascending, kept arc ids
+    ascending)."""
+    V = g["num_states"]
+    src = g["src"].astype(np.int64)
+    dst = g["dst"].astype(np.int64)
+    fwd = _reach(V, src, dst, np.flatnonzero(g["start"]))
+    bwd = _reach(V, dst, src, np.flatnonzero(g["accept"]))
+    keep = fwd & bwd
+    arcs = np.flatnonzero(keep[src] & keep[dst]) if len(src) else np.zeros(0, np.int64)
+    return np.flatnonzero(keep), arcs
+
+
+def bfs_levels(n, adj, seeds):
+    """Plain BFS levels (used for small trace checks)."""
+    lvl = [-1] * n
+    q = deque()
+    for s in seeds:
+        lvl[s] = 0
+        q.append(s)
+    while q:
+        u = q.popleft()
+        for v in adj[u]:
+            if lvl[v] < 0:
+                lvl[v] = lvl[u] + 1
+                q.append(v)
+    return lvl

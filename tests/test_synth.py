@@ -1,0 +1,78 @@
+"""Seeded input generators: determinism, layout and workload recipes (CPU)."""
+import numpy as np
+import pytest
+
+from paper_2110_02848_amd import synth
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4])
+def test_deterministic_per_seed(cfg):
+    A1, B1 = synth.config(cfg, 5)
+    A2, B2 = synth.config(cfg, 5)
+    A3, B3 = synth.config(cfg, 6)
+    assert synth.graph_sha256(A1) == synth.graph_sha256(A2)
+    assert synth.graph_sha256(B1) == synth.graph_sha256(B2)
+    assert synth.graph_sha256(A1) != synth.graph_sha256(A3)
+    assert synth.graph_sha256(A1) != synth.graph_sha256(B1)
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_random_recipe(cfg):
+    spec = synth.RANDOM_SPECS[cfg]
+    A, B = synth.config(cfg, 0)
+    for g in (A, B):
+        assert g["num_states"] == spec.V
+        assert np.all(np.diff(g["arc_offset"]) == spec.degree)
+        assert g["start"].tolist() == [1] + [0] * (spec.V - 1)
+        for lab in (g["ilabel"], g["olabel"]):
+            assert lab.min() >= 0 and lab.max() <= spec.n_sym
+            assert abs(np.mean(lab == 0) - spec.p_eps) < 0.05 + 3 / np.sqrt(len(lab))
+        assert g["weight"].dtype == np.float32
+
+
+@pytest.mark.parametrize("cfg", [4, 5])
+def test_lexicon_recipe(cfg):
+    spec = synth.LEX_SPECS[cfg]
+    A, B, meta = synth.emissions_lexicon_config(cfg, 0)
+    T, C, W = spec.T, spec.C, spec.W
+    assert A["num_states"] == T + 1 and len(A["src"]) == T * C
+    assert np.array_equal(A["ilabel"], A["olabel"])
+    # each frame is a log-softmax: probabilities sum to one
+    p = np.exp(meta["table"].astype(np.float64)).sum(axis=1)
+    assert np.allclose(p, 1.0, atol=1e-5)
+    lens = np.array([len(s) for s in meta["spellings"]])
+    assert lens.min() >= spec.len_lo and lens.max() <= spec.len_hi
+    assert B["num_states"] == 1 + int(np.sum(lens + 1))
+    assert len(B["src"]) == int(np.sum(lens + 2))
+    # root: W entry arcs eps:w, start and accept
+    root = slice(B["arc_offset"][0], B["arc_offset"][1])
+    assert np.all(B["ilabel"][root] == 0)
+    assert B["olabel"][root].tolist() == list(range(1, W + 1))
+    assert B["start"][0] == 1 and B["accept"][0] == 1 and B["accept"].sum() == 1
+    assert not np.any(B["weight"])
+
+
+def test_from_arcs_groups_by_source_stably():
+    g = synth.from_arcs(3, [(2, 0, 1, 1, 0.0), (0, 1, 2, 2, 0.0), (2, 1, 3, 3, 0.0),
+                            (0, 2, 4, 4, 0.0)], start=[0], accept=[2])
+    assert g["arc_offset"].tolist() == [0, 2, 2, 4]
+    assert g["ilabel"].tolist() == [2, 4, 1, 3]
+    assert g["src"].tolist() == [0, 0, 2, 2]
+
+
+@pytest.mark.parametrize("bad", ["offset", "dst", "label", "flag", "src"])
+def test_check_graph_rejects(bad):
+    g = synth.from_arcs(2, [(0, 1, 1, 1, 0.0), (1, 0, 1, 1, 0.0)], start=[0], accept=[1])
+    g = {k: (v.copy() if hasattr(v, "copy") else v) for k, v in g.items()}
+    if bad == "offset":
+        g["arc_offset"][1] = 3
+    elif bad == "dst":
+        g["dst"][0] = 2
+    elif bad == "label":
+        g["ilabel"][0] = -1
+    elif bad == "flag":
+        g["start"][0] = 2
+    else:
+        g["src"][0] = 1
+    with pytest.raises(ValueError):
+        synth.check_graph(g)
