@@ -178,7 +178,9 @@ def canonicalize(raw, A):
     a, b = raw["arc_a"].astype(np.int64), raw["arc_b"].astype(np.int64)
     big = np.int64(1) << 40
     olA = np.asarray(A["olabel"], dtype=np.int64)
-    lab = np.where((a >= 0) & (b >= 0), olA[np.maximum(a, 0)] if E else 0, 0)
+    match = (a >= 0) & (b >= 0)
+    lab = np.zeros(E, np.int64)
+    lab[match] = olA[a[match]]
     ak = np.where(a >= 0, a, big)
     bk = np.where(b >= 0, b, big)
     aorder = np.lexsort((bk, ak, lab, src))

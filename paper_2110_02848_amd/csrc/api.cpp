@@ -1,0 +1,487 @@
+// Host orchestration and the C ABI of libfstcompose.so (include/fst_compose.h).
+//
+// fst_compose_run drives the phases of the parallel composition (paper
+// Section 3.3) on one HIP stream:
+//   1. validate A and B, build label-sorted out- and in-views;
+//   2. forward frontier search from the start keys (accessible keys);
+//   3. backward frontier search from the accessible accepting keys over the
+//      in-arcs (co-accessible keys); the trim set is what both reach;
+//   4. number the trim keys in key order and count each state's kept arcs
+//      (the paper's first pass), scan the counts into arc offsets;
+// fst_compose_fill then writes the arcs (the paper's second pass).
+#include <stdlib.h>
+#include <string.h>
+
+#include <new>
+
+#include "internal.h"
+
+using namespace fstc;
+
+namespace {
+
+struct DevBuf {
+  void *p = nullptr;
+  size_t cap = 0;
+};
+
+constexpr int NEV = 7;
+
+}  // namespace
+
+struct fst_ctx {
+  int device = 0;
+  int64_t max_ws = 0;
+  size_t ws_total = 0;
+  bool timing = false;
+  bool have_times = false;
+  bool timed_run = false;
+
+  DevBuf scal, lists;
+  DevBuf k0, k1, v0, v1, sort_tmp, scan_tmp;
+  DevBuf aOutPerm, aOutLab, aOutNeps, bOutPerm, bOutLab, bOutNeps;
+  DevBuf aInOff, aInPerm, aInLab, aInNeps, bInOff, bInPerm, bInLab, bInNeps;
+  DevBuf vis, coacc, wbase, fq, bq, cnt;
+  Scalars *h_sc = nullptr;
+  hipEvent_t ev[NEV] = {};
+
+  bool ready = false;
+  Problem P = {};
+  uint32_t nstates = 0, narcs = 0, nheavy = 0;
+  fst_stats stats = {};
+};
+
+namespace {
+
+struct DeviceGuard {
+  int prev = -1;
+  bool ok = false;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+    ok = hipSetDevice(dev) == hipSuccess;
+  }
+  ~DeviceGuard() {
+    if (prev >= 0) (void)hipSetDevice(prev);
+  }
+};
+
+#define HIP_TRY(expr)                        \
+  do {                                       \
+    if ((expr) != hipSuccess) return FST_ERR_HIP; \
+  } while (0)
+
+#define FST_TRY(expr)             \
+  do {                            \
+    int rc_ = (expr);             \
+    if (rc_ != FST_OK) return rc_; \
+  } while (0)
+
+size_t round_up(size_t x) { return (x + 255) & ~(size_t)255; }
+
+int ensure(fst_ctx *c, DevBuf &b, size_t bytes) {
+  bytes = round_up(bytes ? bytes : 1);
+  if (b.cap >= bytes) return FST_OK;
+  size_t next = c->ws_total - b.cap + bytes;
+  if (c->max_ws > 0 && next > (size_t)c->max_ws) return FST_ERR_NOMEM;
+  if (b.p) {
+    // earlier queued work may still read the old buffer
+    if (hipDeviceSynchronize() != hipSuccess) return FST_ERR_HIP;
+    (void)hipFree(b.p);
+    c->ws_total -= b.cap;
+    b.p = nullptr;
+    b.cap = 0;
+  }
+  if (hipMalloc(&b.p, bytes) != hipSuccess) {
+    (void)hipGetLastError();
+    b.p = nullptr;
+    return FST_ERR_NOMEM;
+  }
+  b.cap = bytes;
+  c->ws_total += bytes;
+  return FST_OK;
+}
+
+void release(DevBuf &b) {
+  if (b.p) (void)hipFree(b.p);
+  b.p = nullptr;
+  b.cap = 0;
+}
+
+template <typename T>
+T *as(DevBuf &b) {
+  return reinterpret_cast<T *>(b.p);
+}
+
+int readback(fst_ctx *c, hipStream_t s) {
+  HIP_TRY(hipMemcpyAsync(c->h_sc, c->scal.p, sizeof(Scalars), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  return FST_OK;
+}
+
+int bitlen(unsigned long long x) { return x ? 64 - __builtin_clzll(x) : 0; }
+
+int check_graph_args(const fst_graph *g) {
+  if (g->num_states < 0 || g->num_arcs < 0) return FST_ERR_INVALID_ARG;
+  if (g->num_states == 0) return g->num_arcs == 0 ? FST_OK : FST_ERR_INVALID_GRAPH;
+  if (!g->arc_offset || !g->start || !g->accept) return FST_ERR_INVALID_ARG;
+  if (g->num_arcs > 0 &&
+      (!g->src || !g->dst || !g->ilabel || !g->olabel || !g->weight))
+    return FST_ERR_INVALID_ARG;
+  return FST_OK;
+}
+
+DevGraph dev_graph(const fst_graph *g) {
+  DevGraph d;
+  d.V = g->num_states;
+  d.E = g->num_arcs;
+  d.off = g->arc_offset;
+  d.src = g->src;
+  d.dst = g->dst;
+  d.il = g->ilabel;
+  d.ol = g->olabel;
+  d.w = g->weight;
+  d.start = g->start;
+  d.accept = g->accept;
+  return d;
+}
+
+void mark(fst_ctx *c, int i, hipStream_t s) {
+  if (c->timing) (void)hipEventRecord(c->ev[i], s);
+}
+
+int finish_empty(fst_ctx *c, int64_t *V_C, int64_t *E_C) {
+  c->P = Problem{};
+  c->nstates = 0;
+  c->narcs = 0;
+  c->nheavy = 0;
+  c->ready = true;
+  *V_C = 0;
+  *E_C = 0;
+  return FST_OK;
+}
+
+// Frontier loop: expand [lo, hi) level by level until no new key appears.
+int search(fst_ctx *c, bool forward, uint32_t *q, uint32_t cap, uint32_t hi,
+           int64_t *levels, hipStream_t s) {
+  Scalars *d_sc = as<Scalars>(c->scal);
+  uint32_t lo = 0;
+  *levels = 0;
+  while (lo < hi) {
+    HIP_TRY(launch_expand(c->P, forward, q, lo, hi, q, cap, d_sc, s));
+    FST_TRY(readback(c, s));
+    lo = hi;
+    hi = c->h_sc->tail;
+    ++*levels;
+    if (c->h_sc->overflow) return FST_ERR_TOO_LARGE;
+  }
+  return FST_OK;
+}
+
+int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, int64_t *V_C,
+             int64_t *E_C) {
+  FST_TRY(check_graph_args(A));
+  FST_TRY(check_graph_args(B));
+  const DevGraph dA = dev_graph(A), dB = dev_graph(B);
+  const int32_t VA = dA.V, VB = dB.V, EA = dA.E, EB = dB.E;
+
+  FST_TRY(ensure(c, c->scal, sizeof(Scalars)));
+  Scalars *d_sc = as<Scalars>(c->scal);
+  mark(c, 0, s);
+  HIP_TRY(hipMemsetAsync(d_sc, 0, sizeof(Scalars), s));
+  if (VA) HIP_TRY(launch_validate(dA, 0, &d_sc->errA, &d_sc->maxLabA, s));
+  if (VB) HIP_TRY(launch_validate(dB, 1, &d_sc->errB, &d_sc->maxLabB, s));
+  FST_TRY(readback(c, s));
+  if (c->h_sc->errA || c->h_sc->errB) return FST_ERR_INVALID_GRAPH;
+  c->stats = fst_stats{};
+  if (VA == 0 || VB == 0) return finish_empty(c, V_C, E_C);
+
+  const uint32_t shiftB = (uint32_t)bitlen((unsigned long long)(VB - 1));
+  const unsigned long long nkeys = (unsigned long long)VA << (shiftB + 1);
+  if (nkeys >= (1ull << 32)) return FST_ERR_TOO_LARGE;
+  c->stats.key_space = (int64_t)nkeys;
+  const int labA = bitlen(c->h_sc->maxLabA), labB = bitlen(c->h_sc->maxLabB);
+
+  // ---- label-sorted views ----
+  const size_t Emax = (size_t)(EA > EB ? EA : EB);
+  FST_TRY(ensure(c, c->k0, Emax * 8));
+  FST_TRY(ensure(c, c->k1, Emax * 8));
+  FST_TRY(ensure(c, c->v0, Emax * 4));
+  FST_TRY(ensure(c, c->v1, Emax * 4));
+  FST_TRY(ensure(c, c->sort_tmp, sort_temp_bytes(Emax)));
+  FST_TRY(ensure(c, c->aOutPerm, (size_t)EA * 4));
+  FST_TRY(ensure(c, c->aOutLab, (size_t)EA * 4));
+  FST_TRY(ensure(c, c->aOutNeps, (size_t)VA * 4));
+  FST_TRY(ensure(c, c->bOutPerm, (size_t)EB * 4));
+  FST_TRY(ensure(c, c->bOutLab, (size_t)EB * 4));
+  FST_TRY(ensure(c, c->bOutNeps, (size_t)VB * 4));
+  FST_TRY(ensure(c, c->aInOff, ((size_t)VA + 1) * 4));
+  FST_TRY(ensure(c, c->aInPerm, (size_t)EA * 4));
+  FST_TRY(ensure(c, c->aInLab, (size_t)EA * 4));
+  FST_TRY(ensure(c, c->aInNeps, (size_t)VA * 4));
+  FST_TRY(ensure(c, c->bInOff, ((size_t)VB + 1) * 4));
+  FST_TRY(ensure(c, c->bInPerm, (size_t)EB * 4));
+  FST_TRY(ensure(c, c->bInLab, (size_t)EB * 4));
+  FST_TRY(ensure(c, c->bInNeps, (size_t)VB * 4));
+  unsigned long long *k0 = as<unsigned long long>(c->k0), *k1 = as<unsigned long long>(c->k1);
+  int32_t *v0 = as<int32_t>(c->v0), *v1 = as<int32_t>(c->v1);
+  HIP_TRY(build_view(dA, 0, false, labA, as<int32_t>(c->aOutPerm), as<int32_t>(c->aOutLab),
+                     as<int32_t>(c->aOutNeps), nullptr, k0, v0, k1, v1, c->sort_tmp.p,
+                     &d_sc->nEpsStatesA, s));
+  HIP_TRY(build_view(dB, 1, false, labB, as<int32_t>(c->bOutPerm), as<int32_t>(c->bOutLab),
+                     as<int32_t>(c->bOutNeps), nullptr, k0, v0, k1, v1, c->sort_tmp.p, nullptr,
+                     s));
+  HIP_TRY(build_view(dA, 0, true, labA, as<int32_t>(c->aInPerm), as<int32_t>(c->aInLab),
+                     as<int32_t>(c->aInNeps), as<int32_t>(c->aInOff), k0, v0, k1, v1,
+                     c->sort_tmp.p, nullptr, s));
+  HIP_TRY(build_view(dB, 1, true, labB, as<int32_t>(c->bInPerm), as<int32_t>(c->bInLab),
+                     as<int32_t>(c->bInNeps), as<int32_t>(c->bInOff), k0, v0, k1, v1,
+                     c->sort_tmp.p, nullptr, s));
+  FST_TRY(readback(c, s));
+
+  // ---- search state ----
+  const unsigned long long capll =
+      (unsigned long long)VB * ((unsigned long long)VA + c->h_sc->nEpsStatesA);
+  const uint32_t cap = (uint32_t)capll;  // <= nkeys < 2^32
+  const size_t nwords = (size_t)((nkeys + 31) / 32);
+  FST_TRY(ensure(c, c->vis, nwords * 4));
+  FST_TRY(ensure(c, c->coacc, nwords * 4));
+  FST_TRY(ensure(c, c->wbase, nwords * 4));
+  FST_TRY(ensure(c, c->fq, (size_t)cap * 4));
+  FST_TRY(ensure(c, c->bq, (size_t)cap * 4));
+  FST_TRY(ensure(c, c->lists, ((size_t)VA + VB + 2) * 4));
+  size_t scan_n = nwords > (size_t)cap + 1 ? nwords : (size_t)cap + 1;
+  FST_TRY(ensure(c, c->scan_tmp, scan_temp_bytes(scan_n)));
+  HIP_TRY(hipMemsetAsync(c->vis.p, 0, nwords * 4, s));
+  HIP_TRY(hipMemsetAsync(c->coacc.p, 0, nwords * 4, s));
+
+  Problem &P = c->P;
+  P = Problem{};
+  P.A = dA;
+  P.B = dB;
+  P.aOut = View{dA.off, as<int32_t>(c->aOutPerm), as<int32_t>(c->aOutLab), as<int32_t>(c->aOutNeps)};
+  P.bOut = View{dB.off, as<int32_t>(c->bOutPerm), as<int32_t>(c->bOutLab), as<int32_t>(c->bOutNeps)};
+  P.aIn = View{as<int32_t>(c->aInOff), as<int32_t>(c->aInPerm), as<int32_t>(c->aInLab),
+               as<int32_t>(c->aInNeps)};
+  P.bIn = View{as<int32_t>(c->bInOff), as<int32_t>(c->bInPerm), as<int32_t>(c->bInLab),
+               as<int32_t>(c->bInNeps)};
+  P.shiftB = shiftB;
+  P.vis = as<uint32_t>(c->vis);
+  P.coacc = as<uint32_t>(c->coacc);
+  P.wbase = as<uint32_t>(c->wbase);
+
+  // ---- forward search ----
+  mark(c, 1, s);
+  int32_t *la = as<int32_t>(c->lists), *lb = la + VA;
+  uint32_t *cnts = reinterpret_cast<uint32_t *>(lb + VB);
+  HIP_TRY(hipMemsetAsync(cnts, 0, 8, s));
+  uint32_t *fq = as<uint32_t>(c->fq), *bq = as<uint32_t>(c->bq);
+  HIP_TRY(launch_seed_lists(P, la, cnts, lb, cnts + 1, fq, cap, d_sc, s));
+  FST_TRY(readback(c, s));
+  FST_TRY(search(c, true, fq, cap, c->h_sc->tail, &c->stats.fwd_levels, s));
+  const uint32_t nacc = c->h_sc->tail;
+  c->stats.accessible = nacc;
+  c->stats.generated = (int64_t)c->h_sc->generated;
+
+  // ---- backward search ----
+  mark(c, 2, s);
+  HIP_TRY(hipMemsetAsync(&d_sc->tail, 0, sizeof(uint32_t), s));
+  HIP_TRY(launch_bwd_seed(P, fq, nacc, bq, cap, d_sc, s));
+  FST_TRY(readback(c, s));
+  FST_TRY(search(c, false, bq, cap, c->h_sc->tail, &c->stats.bwd_levels, s));
+
+  // ---- numbering and arc counts ----
+  mark(c, 3, s);
+  uint32_t *wbase = as<uint32_t>(c->wbase);
+  HIP_TRY(launch_popc_words(P.coacc, wbase, nwords, s));
+  HIP_TRY(scan_u32(wbase, wbase, nwords, false, &d_sc->total, c->scan_tmp.p, s));
+  FST_TRY(readback(c, s));
+  const unsigned long long nst = c->h_sc->total;
+  if (nst > (unsigned long long)INT32_MAX) return FST_ERR_TOO_LARGE;
+  const uint32_t nstates = (uint32_t)nst;
+  uint32_t *key_of = fq;   // the forward queue is free now (nstates <= nacc)
+  uint32_t *heavy = bq;    // so is the backward queue
+  HIP_TRY(launch_key_of_id(P.coacc, wbase, nwords, key_of, s));
+  FST_TRY(ensure(c, c->cnt, ((size_t)nstates + 1) * 4));
+  uint32_t *cnt = as<uint32_t>(c->cnt);
+  HIP_TRY(hipMemsetAsync(&d_sc->heavy, 0, sizeof(uint32_t), s));
+  HIP_TRY(launch_count(P, key_of, nstates, cnt, heavy, d_sc, s));
+  HIP_TRY(launch_count_heavy(P, key_of, heavy, &d_sc->heavy, cnt, s));
+  HIP_TRY(scan_u32(cnt, cnt, nstates, false, &d_sc->total, c->scan_tmp.p, s));
+  mark(c, 4, s);
+  FST_TRY(readback(c, s));
+  const unsigned long long narcs = c->h_sc->total;
+  if (narcs > (unsigned long long)INT32_MAX) return FST_ERR_TOO_LARGE;
+
+  c->nstates = nstates;
+  c->narcs = (uint32_t)narcs;
+  c->nheavy = c->h_sc->heavy;
+  c->stats.coaccessible = nstates;
+  c->stats.heavy_states = c->nheavy;
+  c->stats.num_states = nstates;
+  c->stats.num_arcs = (int64_t)narcs;
+  c->timed_run = c->timing;
+  c->ready = true;
+  *V_C = nstates;
+  *E_C = (int64_t)narcs;
+  return FST_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int fst_ctx_create(int device, fst_ctx **ctx) {
+  if (!ctx) return FST_ERR_INVALID_ARG;
+  *ctx = nullptr;
+  int ndev = 0;
+  if (hipGetDeviceCount(&ndev) != hipSuccess || device < 0 || device >= ndev) {
+    (void)hipGetLastError();
+    return FST_ERR_INVALID_ARG;
+  }
+  fst_ctx *c = new (std::nothrow) fst_ctx();
+  if (!c) return FST_ERR_NOMEM;
+  c->device = device;
+  DeviceGuard g(device);
+  if (!g.ok) {
+    delete c;
+    return FST_ERR_HIP;
+  }
+  if (hipHostMalloc(reinterpret_cast<void **>(&c->h_sc), sizeof(Scalars), 0) != hipSuccess) {
+    delete c;
+    return FST_ERR_NOMEM;
+  }
+  memset(c->h_sc, 0, sizeof(Scalars));
+  for (int i = 0; i < NEV; ++i) {
+    if (hipEventCreate(&c->ev[i]) != hipSuccess) {
+      fst_ctx_destroy(c);
+      return FST_ERR_HIP;
+    }
+  }
+  *ctx = c;
+  return FST_OK;
+}
+
+void fst_ctx_destroy(fst_ctx *c) {
+  if (!c) return;
+  DeviceGuard g(c->device);
+  (void)hipDeviceSynchronize();
+  DevBuf *bufs[] = {&c->scal, &c->lists, &c->k0, &c->k1, &c->v0, &c->v1, &c->sort_tmp,
+                    &c->scan_tmp, &c->aOutPerm, &c->aOutLab, &c->aOutNeps, &c->bOutPerm,
+                    &c->bOutLab, &c->bOutNeps, &c->aInOff, &c->aInPerm, &c->aInLab,
+                    &c->aInNeps, &c->bInOff, &c->bInPerm, &c->bInLab, &c->bInNeps, &c->vis,
+                    &c->coacc, &c->wbase, &c->fq, &c->bq, &c->cnt};
+  for (DevBuf *b : bufs) release(*b);
+  for (int i = 0; i < NEV; ++i)
+    if (c->ev[i]) (void)hipEventDestroy(c->ev[i]);
+  if (c->h_sc) (void)hipHostFree(c->h_sc);
+  delete c;
+}
+
+int fst_ctx_set_option(fst_ctx *c, int option, int64_t value) {
+  if (!c) return FST_ERR_INVALID_ARG;
+  switch (option) {
+    case FST_OPT_MAX_WORKSPACE:
+      if (value < 0) return FST_ERR_INVALID_ARG;
+      c->max_ws = value;
+      return FST_OK;
+    case FST_OPT_TIMING:
+      c->timing = value != 0;
+      c->have_times = false;
+      return FST_OK;
+    default:
+      return FST_ERR_INVALID_ARG;
+  }
+}
+
+int fst_compose_run(fst_ctx *c, const fst_graph *A, const fst_graph *B, void *stream,
+                    int64_t *num_states, int64_t *num_arcs) {
+  if (!c || !A || !B || !num_states || !num_arcs) return FST_ERR_INVALID_ARG;
+  DeviceGuard g(c->device);
+  if (!g.ok) return FST_ERR_HIP;
+  c->ready = false;
+  c->have_times = false;
+  c->timed_run = false;
+  *num_states = 0;
+  *num_arcs = 0;
+  int rc = run_impl(c, A, B, reinterpret_cast<hipStream_t>(stream), num_states, num_arcs);
+  if (rc != FST_OK) {
+    c->ready = false;
+    *num_states = 0;
+    *num_arcs = 0;
+    (void)hipGetLastError();
+  }
+  return rc;
+}
+
+int fst_compose_fill(fst_ctx *c, const fst_graph_out *C, void *stream) {
+  if (!c || !C) return FST_ERR_INVALID_ARG;
+  if (!c->ready) return FST_ERR_STATE;
+  if (!C->arc_offset) return FST_ERR_INVALID_ARG;
+  if (c->nstates && (!C->start || !C->accept)) return FST_ERR_INVALID_ARG;
+  if (c->narcs && (!C->src || !C->dst || !C->ilabel || !C->olabel || !C->weight))
+    return FST_ERR_INVALID_ARG;
+  DeviceGuard g(c->device);
+  if (!g.ok) return FST_ERR_HIP;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  OutGraph O;
+  O.arc_offset = C->arc_offset;
+  O.src = C->src;
+  O.dst = C->dst;
+  O.il = C->ilabel;
+  O.ol = C->olabel;
+  O.w = C->weight;
+  O.start = C->start;
+  O.accept = C->accept;
+  O.key_a = C->key_a;
+  O.key_b = C->key_b;
+  O.key_f = C->key_f;
+  O.arc_a = C->arc_a;
+  O.arc_b = C->arc_b;
+  mark(c, 5, s);
+  hipError_t e = launch_fill(c->P, as<uint32_t>(c->fq), c->nstates, as<uint32_t>(c->cnt),
+                             as<uint32_t>(c->bq), c->nheavy, c->narcs, O, s);
+  mark(c, 6, s);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return FST_ERR_HIP;
+  }
+  c->have_times = c->timed_run;
+  return FST_OK;
+}
+
+int fst_compose_stats(const fst_ctx *c, fst_stats *out) {
+  if (!c || !out) return FST_ERR_INVALID_ARG;
+  if (!c->ready) return FST_ERR_STATE;
+  *out = c->stats;
+  return FST_OK;
+}
+
+int fst_compose_phase_times(const fst_ctx *c, float *ms, int n) {
+  if (!c || !ms || n < 0) return FST_ERR_INVALID_ARG;
+  if (!c->have_times) return FST_ERR_STATE;
+  DeviceGuard g(c->device);
+  if (hipEventSynchronize(c->ev[6]) != hipSuccess) return FST_ERR_HIP;
+  const int pairs[5][2] = {{0, 1}, {1, 2}, {2, 3}, {3, 4}, {5, 6}};
+  for (int i = 0; i < n && i < 5; ++i) {
+    float t = 0.f;
+    if (hipEventElapsedTime(&t, c->ev[pairs[i][0]], c->ev[pairs[i][1]]) != hipSuccess)
+      return FST_ERR_HIP;
+    ms[i] = t;
+  }
+  return FST_OK;
+}
+
+const char *fst_strerror(int code) {
+  switch (code) {
+    case FST_OK: return "ok";
+    case FST_ERR_INVALID_ARG: return "invalid argument";
+    case FST_ERR_INVALID_GRAPH: return "invalid graph";
+    case FST_ERR_TOO_LARGE: return "problem too large (key space or output size)";
+    case FST_ERR_NOMEM: return "out of device memory or over the workspace cap";
+    case FST_ERR_HIP: return "HIP runtime error";
+    case FST_ERR_STATE: return "no successful fst_compose_run to fill from";
+    default: return "unknown error";
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,236 @@
+"""Python binding of libfstcompose.so (argument marshalling only).
+
+Every step of the composition runs in the library's HIP kernels; this module
+only passes device pointers and the current HIP stream across the C ABI
+declared in ``include/fst_compose.h``.  PyTorch supplies device memory and
+streams.  There is no fallback: if the library is missing or cannot be loaded
+the calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libfstcompose.so")
+
+FST_OK = 0
+FST_ERR_INVALID_ARG = 1
+FST_ERR_INVALID_GRAPH = 2
+FST_ERR_TOO_LARGE = 3
+FST_ERR_NOMEM = 4
+FST_ERR_HIP = 5
+FST_ERR_STATE = 6
+
+FST_OPT_MAX_WORKSPACE = 1
+FST_OPT_TIMING = 2
+
+PHASES = ("preprocess", "forward", "backward", "count", "fill")
+
+
+class FstError(RuntimeError):
+    def __init__(self, code, where):
+        self.code = code
+        super().__init__(f"{where}: {_strerror(code)} (code {code})")
+
+
+class _Graph(ctypes.Structure):
+    _fields_ = [("num_states", ctypes.c_int32), ("num_arcs", ctypes.c_int32),
+                ("arc_offset", ctypes.c_void_p), ("src", ctypes.c_void_p),
+                ("dst", ctypes.c_void_p), ("ilabel", ctypes.c_void_p),
+                ("olabel", ctypes.c_void_p), ("weight", ctypes.c_void_p),
+                ("start", ctypes.c_void_p), ("accept", ctypes.c_void_p)]
+
+
+class _GraphOut(ctypes.Structure):
+    _fields_ = [("arc_offset", ctypes.c_void_p), ("src", ctypes.c_void_p),
+                ("dst", ctypes.c_void_p), ("ilabel", ctypes.c_void_p),
+                ("olabel", ctypes.c_void_p), ("weight", ctypes.c_void_p),
+                ("start", ctypes.c_void_p), ("accept", ctypes.c_void_p),
+                ("key_a", ctypes.c_void_p), ("key_b", ctypes.c_void_p),
+                ("key_f", ctypes.c_void_p), ("arc_a", ctypes.c_void_p),
+                ("arc_b", ctypes.c_void_p)]
+
+
+class _Stats(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int64) for n in (
+        "key_space", "accessible", "coaccessible", "generated", "fwd_levels",
+        "bwd_levels", "heavy_states", "num_states", "num_arcs")]
+
+
+_lib = None
+
+
+def load():
+    """Load the HIP library (raises if it was not built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                           "or python -m paper_2110_02848_amd.build")
+    lib = ctypes.CDLL(LIB_PATH)
+    lib.fst_ctx_create.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_void_p)]
+    lib.fst_ctx_create.restype = ctypes.c_int
+    lib.fst_ctx_destroy.argtypes = [ctypes.c_void_p]
+    lib.fst_ctx_destroy.restype = None
+    lib.fst_ctx_set_option.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int64]
+    lib.fst_ctx_set_option.restype = ctypes.c_int
+    lib.fst_compose_run.argtypes = [ctypes.c_void_p, ctypes.POINTER(_Graph),
+                                    ctypes.POINTER(_Graph), ctypes.c_void_p,
+                                    ctypes.POINTER(ctypes.c_int64),
+                                    ctypes.POINTER(ctypes.c_int64)]
+    lib.fst_compose_run.restype = ctypes.c_int
+    lib.fst_compose_fill.argtypes = [ctypes.c_void_p, ctypes.POINTER(_GraphOut), ctypes.c_void_p]
+    lib.fst_compose_fill.restype = ctypes.c_int
+    lib.fst_compose_stats.argtypes = [ctypes.c_void_p, ctypes.POINTER(_Stats)]
+    lib.fst_compose_stats.restype = ctypes.c_int
+    lib.fst_compose_phase_times.argtypes = [ctypes.c_void_p, ctypes.POINTER(ctypes.c_float),
+                                            ctypes.c_int]
+    lib.fst_compose_phase_times.restype = ctypes.c_int
+    lib.fst_strerror.argtypes = [ctypes.c_int]
+    lib.fst_strerror.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def _strerror(code):
+    try:
+        return load().fst_strerror(code).decode()
+    except Exception:  # pragma: no cover - message only
+        return "error"
+
+
+def _check(rc, where):
+    if rc != FST_OK:
+        raise FstError(rc, where)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr() if t is not None and t.numel() else None)
+
+
+def _stream_handle(stream):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+GRAPH_DTYPES = dict(arc_offset=np.int32, src=np.int32, dst=np.int32, ilabel=np.int32,
+                    olabel=np.int32, weight=np.float32, start=np.uint8, accept=np.uint8)
+
+
+def to_device(g, device="cuda:0"):
+    """Copy a numpy graph dict to device tensors (dict with the same keys)."""
+    import torch
+    out = {"num_states": int(g["num_states"])}
+    for k, dt in GRAPH_DTYPES.items():
+        out[k] = torch.from_numpy(np.ascontiguousarray(g[k], dtype=dt)).to(device)
+    return out
+
+
+def _graph_struct(g):
+    s = _Graph()
+    s.num_states = int(g["num_states"])
+    s.num_arcs = int(g["src"].numel())
+    for k in GRAPH_DTYPES:
+        setattr(s, k, _ptr(g[k]))
+    return s
+
+
+class Composer:
+    """Owns one library context on one device (reuse it across calls)."""
+
+    def __init__(self, device=0):
+        self._lib = load()
+        self.device = int(device)
+        h = ctypes.c_void_p()
+        _check(self._lib.fst_ctx_create(self.device, ctypes.byref(h)), "fst_ctx_create")
+        self._h = h
+
+    def close(self):
+        if getattr(self, "_h", None):
+            self._lib.fst_ctx_destroy(self._h)
+            self._h = None
+
+    def __del__(self):  # pragma: no cover - interpreter shutdown order
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def set_option(self, option, value):
+        _check(self._lib.fst_ctx_set_option(self._h, option, int(value)), "fst_ctx_set_option")
+
+    def run(self, A, B, stream=None):
+        """Phase 1: search, trim, number and count.  Returns (V_C, E_C)."""
+        ga, gb = _graph_struct(A), _graph_struct(B)
+        nv, ne = ctypes.c_int64(), ctypes.c_int64()
+        rc = self._lib.fst_compose_run(self._h, ctypes.byref(ga), ctypes.byref(gb),
+                                       _stream_handle(stream), ctypes.byref(nv), ctypes.byref(ne))
+        _check(rc, "fst_compose_run")
+        return int(nv.value), int(ne.value)
+
+    def alloc_output(self, nv, ne, provenance=True, keys=True):
+        import torch
+        dev = f"cuda:{self.device}"
+        i32 = dict(dtype=torch.int32, device=dev)
+        u8 = dict(dtype=torch.uint8, device=dev)
+        C = dict(num_states=nv, num_arcs=ne,
+                 arc_offset=torch.empty(nv + 1, **i32),
+                 src=torch.empty(ne, **i32), dst=torch.empty(ne, **i32),
+                 ilabel=torch.empty(ne, **i32), olabel=torch.empty(ne, **i32),
+                 weight=torch.empty(ne, dtype=torch.float32, device=dev),
+                 start=torch.empty(nv, **u8), accept=torch.empty(nv, **u8))
+        if keys:
+            C.update(key_a=torch.empty(nv, **i32), key_b=torch.empty(nv, **i32),
+                     key_f=torch.empty(nv, **u8))
+        if provenance:
+            C.update(arc_a=torch.empty(ne, **i32), arc_b=torch.empty(ne, **i32))
+        return C
+
+    def fill(self, C, stream=None):
+        """Phase 2: write C into the tensors of ``alloc_output`` (async)."""
+        o = _GraphOut()
+        o.arc_offset = ctypes.c_void_p(C["arc_offset"].data_ptr())
+        for k in ("src", "dst", "ilabel", "olabel", "weight", "start", "accept",
+                  "key_a", "key_b", "key_f", "arc_a", "arc_b"):
+            setattr(o, k, _ptr(C.get(k)))
+        _check(self._lib.fst_compose_fill(self._h, ctypes.byref(o), _stream_handle(stream)),
+               "fst_compose_fill")
+        return C
+
+    def compose(self, A, B, provenance=True, keys=True, stream=None):
+        """C = A o B as a dict of device tensors (asynchronous fill)."""
+        nv, ne = self.run(A, B, stream)
+        C = self.alloc_output(nv, ne, provenance, keys)
+        return self.fill(C, stream)
+
+    def stats(self):
+        st = _Stats()
+        _check(self._lib.fst_compose_stats(self._h, ctypes.byref(st)), "fst_compose_stats")
+        return {n: int(getattr(st, n)) for n, _ in _Stats._fields_}
+
+    def phase_times(self):
+        buf = (ctypes.c_float * len(PHASES))()
+        _check(self._lib.fst_compose_phase_times(self._h, buf, len(PHASES)),
+               "fst_compose_phase_times")
+        return dict(zip(PHASES, [float(x) for x in buf]))
+
+
+def to_numpy(C):
+    """Device result dict -> numpy dict (synchronises)."""
+    out = {}
+    for k, v in C.items():
+        out[k] = v.cpu().numpy() if hasattr(v, "cpu") else v
+    return out
+
+
+def compose_numpy(A, B, device=0, composer=None):
+    """Convenience: numpy graphs in, numpy canonical C out (via the GPU)."""
+    comp = composer or Composer(device)
+    dev = f"cuda:{comp.device}"
+    C = comp.compose(to_device(A, dev), to_device(B, dev))
+    return to_numpy(C)

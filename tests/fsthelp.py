@@ -43,6 +43,16 @@ def _bits(x):
     return np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
 
 
+def _padded(g):
+    """Arc arrays with one dummy trailing arc, so that masked-out lookups with
+    index 0 stay in range for graphs without arcs."""
+    out = dict(g)
+    for k, dt in (("src", np.int32), ("dst", np.int32), ("ilabel", np.int32),
+                  ("olabel", np.int32), ("weight", np.float32)):
+        out[k] = np.concatenate([np.asarray(g[k], dtype=dt), np.zeros(1, dt)])
+    return out
+
+
 def check_invariants(A, B, C):
     """Return a list of violated invariants of a canonical composed graph."""
     errs = []
@@ -92,6 +102,8 @@ def check_invariants(A, B, C):
             errs.append("arc without provenance")
         w = _bits(C["weight"])
         aa, bb = np.maximum(a, 0), np.maximum(b, 0)
+        A = _padded(A)
+        B = _padded(B)
         # matching moves
         m = M
         ok = ((A["olabel"][aa] == B["ilabel"][bb]) & (A["olabel"][aa] != 0)

@@ -345,3 +345,15 @@ def test_canonical_arc_order():
     s0 = C["src"] == 0
     got = list(zip(C["arc_a"][s0].tolist(), C["arc_b"][s0].tolist()))
     assert got == [(1, -1), (-1, 1), (2, 0), (0, 2)]
+
+
+def test_arcless_side_with_epsilon_moves():
+    # A has no arcs (start and accepting); only B's epsilon-input arcs move
+    A = synth.from_arcs(2, [], start=[0, 1], accept=[0, 1])
+    B = synth.from_arcs(3, [(0, 1, 0, 4, 0.5), (1, 2, 0, 0, 0.25), (0, 2, 3, 1, 1.0)],
+                        start=[0], accept=[2])
+    for order in (oracle.ORDER_PAPER, oracle.ORDER_FORWARD):
+        C = oracle.compose(A, B, order)
+        assert C["num_states"] == 6 and C["num_arcs"] == 4
+        assert not fsthelp.check_invariants(A, B, C)
+        assert not brute.check(A, B, C, 3)
