@@ -34,14 +34,18 @@ struct fst_ctx {
   int64_t max_ws = 0;
   size_t ws_total = 0;
   bool timing = false;
+  bool buckets = true;
+  int chain_depth = CHAIN_MAX;
   bool have_times = false;
   bool timed_run = false;
 
   DevBuf scal, lists;
   DevBuf k0, k1, v0, v1, sort_tmp, scan_tmp;
-  DevBuf aOutPerm, aOutLab, aOutNeps, bOutPerm, bOutLab, bOutNeps;
-  DevBuf aInOff, aInPerm, aInLab, aInNeps, bInOff, bInPerm, bInLab, bInNeps;
-  DevBuf vis, coacc, wbase, fq, bq, cnt;
+  DevBuf aOutPerm, aOutLab, aOutNbr, aOutNeps, aOutLut, bOutPerm, bOutLab, bOutNbr, bOutNeps,
+      bOutLut;
+  DevBuf aInOff, aInPerm, aInLab, aInNbr, aInNeps, aInLut, bInOff, bInPerm, bInLab, bInNbr,
+      bInNeps, bInLut;
+  DevBuf vis, coacc, wbase, fq, bq, heavy, hoff, cnt;
   Scalars *h_sc = nullptr;
   hipEvent_t ev[NEV] = {};
 
@@ -160,21 +164,33 @@ int finish_empty(fst_ctx *c, int64_t *V_C, int64_t *E_C) {
   return FST_OK;
 }
 
-// Frontier loop: expand [lo, hi) level by level until no new key appears.
-int search(fst_ctx *c, bool forward, uint32_t *q, uint32_t cap, uint32_t hi,
-           int64_t *levels, hipStream_t s) {
+// Frontier search from the keys already in q[0, tail): generations are queued
+// in batches without host round trips; the host only checks after each
+// batch whether the frontier has emptied (extra generations are no-ops).
+int search(fst_ctx *c, bool forward, uint32_t *q, uint32_t cap, int64_t *levels,
+           hipStream_t s) {
   Scalars *d_sc = as<Scalars>(c->scal);
-  uint32_t lo = 0;
-  *levels = 0;
-  while (lo < hi) {
-    HIP_TRY(launch_expand(c->P, forward, q, lo, hi, q, cap, d_sc, s));
+  HIP_TRY(launch_gen_init(d_sc, cap, s));
+  int g = 0, batch = 4;
+  for (;;) {
+    for (int b = 0; b < batch; ++b, ++g)
+      HIP_TRY(launch_generation(c->P, forward, q, as<uint32_t>(c->bq), cap,
+                                as<uint32_t>(c->heavy), as<uint32_t>(c->hoff), g, d_sc, s));
     FST_TRY(readback(c, s));
-    lo = hi;
-    hi = c->h_sc->tail;
-    ++*levels;
     if (c->h_sc->overflow) return FST_ERR_TOO_LARGE;
+    const GenDesc d = c->h_sc->D[g & 1];
+    if (d.qlo == d.qhi) break;
+    if (batch < 64) batch *= 2;
   }
+  *levels = c->h_sc->gens;
   return FST_OK;
+}
+
+// Label buckets are kept when the table is at most this large.
+constexpr size_t LUT_BUDGET = (size_t)256 << 20;
+
+size_t lut_bytes(int32_t V, uint32_t lab_max) {
+  return (size_t)V * ((size_t)lab_max + 2) * sizeof(int32_t);
 }
 
 int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, int64_t *V_C,
@@ -208,34 +224,41 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   FST_TRY(ensure(c, c->v0, Emax * 4));
   FST_TRY(ensure(c, c->v1, Emax * 4));
   FST_TRY(ensure(c, c->sort_tmp, sort_temp_bytes(Emax)));
-  FST_TRY(ensure(c, c->aOutPerm, (size_t)EA * 4));
-  FST_TRY(ensure(c, c->aOutLab, (size_t)EA * 4));
-  FST_TRY(ensure(c, c->aOutNeps, (size_t)VA * 4));
-  FST_TRY(ensure(c, c->bOutPerm, (size_t)EB * 4));
-  FST_TRY(ensure(c, c->bOutLab, (size_t)EB * 4));
-  FST_TRY(ensure(c, c->bOutNeps, (size_t)VB * 4));
-  FST_TRY(ensure(c, c->aInOff, ((size_t)VA + 1) * 4));
-  FST_TRY(ensure(c, c->aInPerm, (size_t)EA * 4));
-  FST_TRY(ensure(c, c->aInLab, (size_t)EA * 4));
-  FST_TRY(ensure(c, c->aInNeps, (size_t)VA * 4));
-  FST_TRY(ensure(c, c->bInOff, ((size_t)VB + 1) * 4));
-  FST_TRY(ensure(c, c->bInPerm, (size_t)EB * 4));
-  FST_TRY(ensure(c, c->bInLab, (size_t)EB * 4));
-  FST_TRY(ensure(c, c->bInNeps, (size_t)VB * 4));
+  const uint32_t maxA = c->h_sc->maxLabA, maxB = c->h_sc->maxLabB;
+  const bool lutA = c->buckets && lut_bytes(VA, maxA) <= LUT_BUDGET;
+  const bool lutB = c->buckets && lut_bytes(VB, maxB) <= LUT_BUDGET;
+  struct ViewBufs {
+    DevBuf *perm, *lab, *nbr, *neps, *lut, *off;
+  };
+  const ViewBufs vb[4] = {
+      {&c->aOutPerm, &c->aOutLab, &c->aOutNbr, &c->aOutNeps, &c->aOutLut, nullptr},
+      {&c->bOutPerm, &c->bOutLab, &c->bOutNbr, &c->bOutNeps, &c->bOutLut, nullptr},
+      {&c->aInPerm, &c->aInLab, &c->aInNbr, &c->aInNeps, &c->aInLut, &c->aInOff},
+      {&c->bInPerm, &c->bInLab, &c->bInNbr, &c->bInNeps, &c->bInLut, &c->bInOff}};
   unsigned long long *k0 = as<unsigned long long>(c->k0), *k1 = as<unsigned long long>(c->k1);
   int32_t *v0 = as<int32_t>(c->v0), *v1 = as<int32_t>(c->v1);
-  HIP_TRY(build_view(dA, 0, false, labA, as<int32_t>(c->aOutPerm), as<int32_t>(c->aOutLab),
-                     as<int32_t>(c->aOutNeps), nullptr, k0, v0, k1, v1, c->sort_tmp.p,
-                     &d_sc->nEpsStatesA, s));
-  HIP_TRY(build_view(dB, 1, false, labB, as<int32_t>(c->bOutPerm), as<int32_t>(c->bOutLab),
-                     as<int32_t>(c->bOutNeps), nullptr, k0, v0, k1, v1, c->sort_tmp.p, nullptr,
-                     s));
-  HIP_TRY(build_view(dA, 0, true, labA, as<int32_t>(c->aInPerm), as<int32_t>(c->aInLab),
-                     as<int32_t>(c->aInNeps), as<int32_t>(c->aInOff), k0, v0, k1, v1,
-                     c->sort_tmp.p, nullptr, s));
-  HIP_TRY(build_view(dB, 1, true, labB, as<int32_t>(c->bInPerm), as<int32_t>(c->bInLab),
-                     as<int32_t>(c->bInNeps), as<int32_t>(c->bInOff), k0, v0, k1, v1,
-                     c->sort_tmp.p, nullptr, s));
+  View views[4];
+  for (int i = 0; i < 4; ++i) {
+    const bool isA = (i % 2) == 0, in = i >= 2;
+    const DevGraph &g = isA ? dA : dB;
+    const bool lut = isA ? lutA : lutB;
+    const uint32_t lmax = isA ? maxA : maxB;
+    FST_TRY(ensure(c, *vb[i].perm, (size_t)g.E * 4));
+    FST_TRY(ensure(c, *vb[i].lab, (size_t)g.E * 4));
+    FST_TRY(ensure(c, *vb[i].nbr, (size_t)g.E * 4));
+    FST_TRY(ensure(c, *vb[i].neps, (size_t)g.V * 4));
+    if (lut) FST_TRY(ensure(c, *vb[i].lut, lut_bytes(g.V, lmax)));
+    if (in) FST_TRY(ensure(c, *vb[i].off, ((size_t)g.V + 1) * 4));
+    int32_t *off = in ? as<int32_t>(*vb[i].off) : nullptr;
+    int32_t *lutp = lut ? as<int32_t>(*vb[i].lut) : nullptr;
+    HIP_TRY(build_view(g, isA ? 0 : 1, in, isA ? labA : labB, (int32_t)lmax,
+                       as<int32_t>(*vb[i].perm), as<int32_t>(*vb[i].lab), as<int32_t>(*vb[i].nbr),
+                       as<int32_t>(*vb[i].neps), lutp, off, k0, v0, k1, v1, c->sort_tmp.p,
+                       i == 0 ? &d_sc->nEpsStatesA : nullptr, s));
+    views[i] = View{in ? off : g.off, as<int32_t>(*vb[i].perm), as<int32_t>(*vb[i].lab),
+                    as<int32_t>(*vb[i].nbr), as<int32_t>(*vb[i].neps), lutp,
+                    (int32_t)lmax + 2};
+  }
   FST_TRY(readback(c, s));
 
   // ---- search state ----
@@ -248,6 +271,8 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   FST_TRY(ensure(c, c->wbase, nwords * 4));
   FST_TRY(ensure(c, c->fq, (size_t)cap * 4));
   FST_TRY(ensure(c, c->bq, (size_t)cap * 4));
+  FST_TRY(ensure(c, c->heavy, (size_t)cap * 4));
+  FST_TRY(ensure(c, c->hoff, (size_t)cap * 4));
   FST_TRY(ensure(c, c->lists, ((size_t)VA + VB + 2) * 4));
   size_t scan_n = nwords > (size_t)cap + 1 ? nwords : (size_t)cap + 1;
   FST_TRY(ensure(c, c->scan_tmp, scan_temp_bytes(scan_n)));
@@ -258,13 +283,12 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   P = Problem{};
   P.A = dA;
   P.B = dB;
-  P.aOut = View{dA.off, as<int32_t>(c->aOutPerm), as<int32_t>(c->aOutLab), as<int32_t>(c->aOutNeps)};
-  P.bOut = View{dB.off, as<int32_t>(c->bOutPerm), as<int32_t>(c->bOutLab), as<int32_t>(c->bOutNeps)};
-  P.aIn = View{as<int32_t>(c->aInOff), as<int32_t>(c->aInPerm), as<int32_t>(c->aInLab),
-               as<int32_t>(c->aInNeps)};
-  P.bIn = View{as<int32_t>(c->bInOff), as<int32_t>(c->bInPerm), as<int32_t>(c->bInLab),
-               as<int32_t>(c->bInNeps)};
+  P.aOut = views[0];
+  P.bOut = views[1];
+  P.aIn = views[2];
+  P.bIn = views[3];
   P.shiftB = shiftB;
+  P.chain_max = c->chain_depth;
   P.vis = as<uint32_t>(c->vis);
   P.coacc = as<uint32_t>(c->coacc);
   P.wbase = as<uint32_t>(c->wbase);
@@ -275,19 +299,16 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   uint32_t *cnts = reinterpret_cast<uint32_t *>(lb + VB);
   HIP_TRY(hipMemsetAsync(cnts, 0, 8, s));
   uint32_t *fq = as<uint32_t>(c->fq), *bq = as<uint32_t>(c->bq);
-  HIP_TRY(launch_seed_lists(P, la, cnts, lb, cnts + 1, fq, cap, d_sc, s));
-  FST_TRY(readback(c, s));
-  FST_TRY(search(c, true, fq, cap, c->h_sc->tail, &c->stats.fwd_levels, s));
-  const uint32_t nacc = c->h_sc->tail;
-  c->stats.accessible = nacc;
+  HIP_TRY(launch_seed_lists(P, la, cnts, lb, cnts + 1, fq, bq, cap, d_sc, s));
+  FST_TRY(search(c, true, fq, cap, &c->stats.fwd_levels, s));
+  c->stats.accessible = c->h_sc->naccessible;
   c->stats.generated = (int64_t)c->h_sc->generated;
 
   // ---- backward search ----
   mark(c, 2, s);
-  HIP_TRY(hipMemsetAsync(&d_sc->tail, 0, sizeof(uint32_t), s));
-  HIP_TRY(launch_bwd_seed(P, fq, nacc, bq, cap, d_sc, s));
-  FST_TRY(readback(c, s));
-  FST_TRY(search(c, false, bq, cap, c->h_sc->tail, &c->stats.bwd_levels, s));
+  // the accepting keys listed in bq by the forward search seed it
+  HIP_TRY(hipMemcpyAsync(&d_sc->tail, &d_sc->tail2, sizeof(uint32_t), hipMemcpyDeviceToDevice, s));
+  FST_TRY(search(c, false, bq, cap, &c->stats.bwd_levels, s));
 
   // ---- numbering and arc counts ----
   mark(c, 3, s);
@@ -298,7 +319,7 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   const unsigned long long nst = c->h_sc->total;
   if (nst > (unsigned long long)INT32_MAX) return FST_ERR_TOO_LARGE;
   const uint32_t nstates = (uint32_t)nst;
-  uint32_t *key_of = fq;   // the forward queue is free now (nstates <= nacc)
+  uint32_t *key_of = fq;   // the forward queue is free now (nstates <= cap)
   uint32_t *heavy = bq;    // so is the backward queue
   HIP_TRY(launch_key_of_id(P.coacc, wbase, nwords, key_of, s));
   FST_TRY(ensure(c, c->cnt, ((size_t)nstates + 1) * 4));
@@ -365,11 +386,14 @@ void fst_ctx_destroy(fst_ctx *c) {
   if (!c) return;
   DeviceGuard g(c->device);
   (void)hipDeviceSynchronize();
-  DevBuf *bufs[] = {&c->scal, &c->lists, &c->k0, &c->k1, &c->v0, &c->v1, &c->sort_tmp,
-                    &c->scan_tmp, &c->aOutPerm, &c->aOutLab, &c->aOutNeps, &c->bOutPerm,
-                    &c->bOutLab, &c->bOutNeps, &c->aInOff, &c->aInPerm, &c->aInLab,
-                    &c->aInNeps, &c->bInOff, &c->bInPerm, &c->bInLab, &c->bInNeps, &c->vis,
-                    &c->coacc, &c->wbase, &c->fq, &c->bq, &c->cnt};
+  DevBuf *bufs[] = {&c->scal,    &c->lists,    &c->k0,       &c->k1,       &c->v0,
+                    &c->v1,      &c->sort_tmp, &c->scan_tmp, &c->aOutPerm, &c->aOutLab,
+                    &c->aOutNbr, &c->aOutNeps, &c->aOutLut,  &c->bOutPerm, &c->bOutLab,
+                    &c->bOutNbr, &c->bOutNeps, &c->bOutLut,  &c->aInOff,   &c->aInPerm,
+                    &c->aInLab,  &c->aInNbr,   &c->aInNeps,  &c->aInLut,   &c->bInOff,
+                    &c->bInPerm, &c->bInLab,   &c->bInNbr,   &c->bInNeps,  &c->bInLut,
+                    &c->vis,     &c->coacc,    &c->wbase,    &c->fq,       &c->bq,
+                    &c->heavy,   &c->hoff,     &c->cnt};
   for (DevBuf *b : bufs) release(*b);
   for (int i = 0; i < NEV; ++i)
     if (c->ev[i]) (void)hipEventDestroy(c->ev[i]);
@@ -387,6 +411,13 @@ int fst_ctx_set_option(fst_ctx *c, int option, int64_t value) {
     case FST_OPT_TIMING:
       c->timing = value != 0;
       c->have_times = false;
+      return FST_OK;
+    case FST_OPT_LABEL_BUCKETS:
+      c->buckets = value != 0;
+      return FST_OK;
+    case FST_OPT_CHAIN_DEPTH:
+      if (value < 0 || value > (1 << 20)) return FST_ERR_INVALID_ARG;
+      c->chain_depth = (int)value;
       return FST_OK;
     default:
       return FST_ERR_INVALID_ARG;

@@ -94,15 +94,30 @@ __global__ __launch_bounds__(NT) void k_make_keys(DevGraph g, int side, int by_d
   }
 }
 
-__global__ __launch_bounds__(NT) void k_split(const ull *__restrict__ k,
+__global__ __launch_bounds__(NT) void k_split(DevGraph g, int by_dst, const ull *__restrict__ k,
                                               const int32_t *__restrict__ v, long long n,
                                               int lab_bits, int32_t *__restrict__ perm,
-                                              int32_t *__restrict__ lab) {
+                                              int32_t *__restrict__ lab,
+                                              int32_t *__restrict__ nbr) {
   const ull mask = (lab_bits >= 64) ? ~0ull : ((1ull << lab_bits) - 1ull);
   for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n;
        i += (long long)gridDim.x * NT) {
-    perm[i] = v[i];
+    const int32_t e = v[i];
+    perm[i] = e;
     lab[i] = (int32_t)(k[i] & mask);
+    nbr[i] = by_dst ? g.src[e] : g.dst[e];
+  }
+}
+
+// Label buckets: lut[v * S + l] = first position of label >= l in group v.
+__global__ __launch_bounds__(NT) void k_build_lut(const int32_t *__restrict__ off,
+                                                  const int32_t *__restrict__ lab, int V, int S,
+                                                  int32_t *__restrict__ lut) {
+  const long long n = (long long)V * S;
+  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n;
+       i += (long long)gridDim.x * NT) {
+    const int32_t v = (int32_t)(i / S), l = (int32_t)(i % S);
+    lut[i] = lower_bound_i32(lab, off[v], off[v + 1], l);
   }
 }
 
@@ -143,6 +158,25 @@ __global__ __launch_bounds__(NT) void k_neps(const int32_t *__restrict__ off,
 // search helpers
 // ---------------------------------------------------------------------------
 
+// Positions of label `lab` inside group q of a view, whose non-epsilon part
+// is [lo, hi): one bucket lookup when the view has buckets, else a binary
+// search.
+__device__ __forceinline__ void label_range(const View &v, uint32_t q, int32_t lo, int32_t hi,
+                                            int32_t lab, int32_t &r0, int32_t &r1) {
+  if (v.lut) {
+    if ((uint32_t)lab < (uint32_t)(v.lstride - 1)) {
+      const int32_t *b = v.lut + (size_t)q * (uint32_t)v.lstride + lab;
+      r0 = b[0];
+      r1 = b[1];
+    } else {
+      r0 = r1 = hi;
+    }
+    return;
+  }
+  r0 = lower_bound_i32(v.lab, lo, hi, lab);
+  r1 = upper_bound_i32(v.lab, r0, hi, lab);
+}
+
 // Claim key k in bitmap bm; true for exactly one caller per key.
 __device__ __forceinline__ bool claim(uint32_t *bm, uint32_t k) {
   const uint32_t bit = 1u << (k & 31u);
@@ -151,23 +185,43 @@ __device__ __forceinline__ bool claim(uint32_t *bm, uint32_t k) {
   return (atomicOr(w, bit) & bit) == 0;
 }
 
+// An append-only key list with a device counter.
+struct Pusher {
+  uint32_t *Q;
+  uint32_t cap;
+  uint32_t *count;
+  Scalars *sc;
+};
+
 // Append `key` for every lane with `want`, one atomic per wavefront.
-__device__ __forceinline__ void wave_push(bool want, uint32_t key, uint32_t *q, uint32_t cap,
-                                          Scalars *sc) {
+__device__ __forceinline__ void wave_push(bool want, uint32_t key, const Pusher &pu) {
   unsigned long long m = __ballot(want);
   if (m == 0) return;
   const int leader = __ffsll(m) - 1;
   uint32_t base = 0;
-  if ((int)__lane_id() == leader) base = atomicAdd(&sc->tail, (uint32_t)__popcll(m));
+  if ((int)__lane_id() == leader) base = atomicAdd(pu.count, (uint32_t)__popcll(m));
   base = __shfl(base, leader, WAVE);
   if (want) {
     uint32_t pos = base + (uint32_t)__popcll(m & __lanemask_lt());
-    if (pos < cap) q[pos] = key;
-    else atomicOr(&sc->overflow, 1u);
+    if (pos < pu.cap) pu.Q[pos] = key;
+    else atomicOr(&pu.sc->overflow, 1u);
   }
 }
 
-// Per-key move structure of a forward key (also used by compaction).
+// A key the forward search reached for the first time: count it, and if it
+// accepts, mark it co-accessible and list it as a seed of the backward search.
+__device__ __forceinline__ void note_accessible(const Problem &P, bool fresh, uint32_t v,
+                                                const Pusher &acc, uint32_t &nacc) {
+  bool accepting = false;
+  if (fresh) {
+    ++nacc;
+    accepting = P.A.accept[key_qa(v, P.shiftB)] && P.B.accept[key_qb(v, P.shiftB)];
+    if (accepting) atomicOr(P.coacc + (v >> 5), 1u << (v & 31u));
+  }
+  wave_push(accepting, v, acc);
+}
+
+// Move structure of a key (forward direction; also used by compaction).
 struct Fwd {
   uint32_t qa, qb, f;
   int32_t aS, ae, aE, bS, be, bE;
@@ -192,51 +246,32 @@ __device__ __forceinline__ Fwd fwd_info(const Problem &P, uint32_t key) {
   return s;
 }
 
-__device__ __forceinline__ uint32_t fwd_units(const Problem &P, uint32_t key) {
-  Fwd s = fwd_info(P, key);
-  return s.eA + (uint32_t)s.be + s.mU;
-}
+// Work units of a key: its A-epsilon arcs, its B-epsilon arcs, and the
+// non-epsilon arcs of the smaller side (each joined with the other side's
+// bucket of its label).
+__device__ __forceinline__ uint32_t fwd_units(const Fwd &s) { return s.eA + (uint32_t)s.be + s.mU; }
 
-// One forward work unit: an A-epsilon arc, a B-epsilon arc, or one arc of the
-// smaller non-epsilon side joined against the other side's label bucket.
-__device__ __forceinline__ void fwd_unit(const Problem &P, uint32_t key, uint32_t local,
-                                         uint32_t *q, uint32_t cap, Scalars *sc, ull &gen) {
-  const Fwd s = fwd_info(P, key);
+// Calls f(dst key) for the moves of unit `u` of key s.
+template <class F>
+__device__ __forceinline__ void fwd_unit(const Problem &P, const Fwd &s, uint32_t u, F &&f) {
   const uint32_t sh = P.shiftB;
-  if (local < s.eA) {
-    int32_t ea = P.aOut.perm[s.aS + (int32_t)local];
-    uint32_t d = make_key((uint32_t)P.A.dst[ea], s.qb, 0u, sh);
-    ++gen;
-    wave_push(claim(P.vis, d), d, q, cap, sc);
-  } else if (local < s.eA + (uint32_t)s.be) {
-    int32_t eb = P.bOut.perm[s.bS + (int32_t)(local - s.eA)];
-    uint32_t d = make_key(s.qa, (uint32_t)P.B.dst[eb], s.ae > 0 ? 1u : 0u, sh);
-    ++gen;
-    wave_push(claim(P.vis, d), d, q, cap, sc);
+  if (u < s.eA) {
+    f(make_key((uint32_t)P.aOut.nbr[s.aS + (int32_t)u], s.qb, 0u, sh));
+  } else if (u < s.eA + (uint32_t)s.be) {
+    f(make_key(s.qa, (uint32_t)P.bOut.nbr[s.bS + (int32_t)(u - s.eA)], s.ae > 0 ? 1u : 0u, sh));
   } else {
-    const uint32_t j = local - s.eA - (uint32_t)s.be;
+    const uint32_t j = u - s.eA - (uint32_t)s.be;
+    int32_t lo, hi;
     if (s.nA <= s.nB) {
       const int32_t pa = s.aS + s.ae + (int32_t)j;
-      const int32_t lab = P.aOut.lab[pa];
-      const uint32_t da = (uint32_t)P.A.dst[P.aOut.perm[pa]];
-      const int32_t lo = lower_bound_i32(P.bOut.lab, s.bS + s.be, s.bE, lab);
-      const int32_t hi = upper_bound_i32(P.bOut.lab, lo, s.bE, lab);
-      for (int32_t p = lo; p < hi; ++p) {
-        uint32_t d = make_key(da, (uint32_t)P.B.dst[P.bOut.perm[p]], 0u, sh);
-        ++gen;
-        wave_push(claim(P.vis, d), d, q, cap, sc);
-      }
+      const uint32_t da = (uint32_t)P.aOut.nbr[pa];
+      label_range(P.bOut, s.qb, s.bS + s.be, s.bE, P.aOut.lab[pa], lo, hi);
+      for (int32_t p = lo; p < hi; ++p) f(make_key(da, (uint32_t)P.bOut.nbr[p], 0u, sh));
     } else {
       const int32_t pb = s.bS + s.be + (int32_t)j;
-      const int32_t lab = P.bOut.lab[pb];
-      const uint32_t db = (uint32_t)P.B.dst[P.bOut.perm[pb]];
-      const int32_t lo = lower_bound_i32(P.aOut.lab, s.aS + s.ae, s.aE, lab);
-      const int32_t hi = upper_bound_i32(P.aOut.lab, lo, s.aE, lab);
-      for (int32_t p = lo; p < hi; ++p) {
-        uint32_t d = make_key((uint32_t)P.A.dst[P.aOut.perm[p]], db, 0u, sh);
-        ++gen;
-        wave_push(claim(P.vis, d), d, q, cap, sc);
-      }
+      const uint32_t db = (uint32_t)P.bOut.nbr[pb];
+      label_range(P.aOut, s.qa, s.aS + s.ae, s.aE, P.bOut.lab[pb], lo, hi);
+      for (int32_t p = lo; p < hi; ++p) f(make_key((uint32_t)P.aOut.nbr[p], db, 0u, sh));
     }
   }
 }
@@ -269,104 +304,217 @@ __device__ __forceinline__ Bwd bwd_info(const Problem &P, uint32_t key) {
   return s;
 }
 
-__device__ __forceinline__ uint32_t bwd_units(const Problem &P, uint32_t key) {
-  Bwd s = bwd_info(P, key);
-  return s.eA + s.eB + s.mU;
-}
+__device__ __forceinline__ uint32_t bwd_units(const Bwd &s) { return s.eA + s.eB + s.mU; }
 
-__device__ __forceinline__ void bwd_try(const Problem &P, uint32_t p, uint32_t *q, uint32_t cap,
-                                        Scalars *sc) {
-  bool want = test_bit(P.vis, p) && claim(P.coacc, p);
-  wave_push(want, p, q, cap, sc);
-}
-
-__device__ __forceinline__ void bwd_unit(const Problem &P, uint32_t key, uint32_t local,
-                                         uint32_t *q, uint32_t cap, Scalars *sc) {
-  const Bwd s = bwd_info(P, key);
+// Calls f(predecessor key) for the predecessors of unit `u` of key s.
+template <class F>
+__device__ __forceinline__ void bwd_unit(const Problem &P, const Bwd &s, uint32_t u, F &&f) {
   const uint32_t sh = P.shiftB;
-  if (local < s.eA) {
-    int32_t ea = P.aIn.perm[s.aS + (int32_t)local];
-    bwd_try(P, make_key((uint32_t)P.A.src[ea], s.vb, 0u, sh), q, cap, sc);
-  } else if (local < s.eA + s.eB) {
-    int32_t eb = P.bIn.perm[s.bS + (int32_t)(local - s.eA)];
-    uint32_t ub = (uint32_t)P.B.src[eb];
-    bwd_try(P, make_key(s.va, ub, 0u, sh), q, cap, sc);
-    if (s.epsV) bwd_try(P, make_key(s.va, ub, 1u, sh), q, cap, sc);
+  if (u < s.eA) {
+    f(make_key((uint32_t)P.aIn.nbr[s.aS + (int32_t)u], s.vb, 0u, sh));
+  } else if (u < s.eA + s.eB) {
+    const uint32_t ub = (uint32_t)P.bIn.nbr[s.bS + (int32_t)(u - s.eA)];
+    f(make_key(s.va, ub, 0u, sh));
+    if (s.epsV) f(make_key(s.va, ub, 1u, sh));
   } else {
-    const uint32_t j = local - s.eA - s.eB;
+    const uint32_t j = u - s.eA - s.eB;
+    int32_t lo, hi;
     if (s.nA <= s.nB) {
       const int32_t pa = s.aS + s.ae + (int32_t)j;
-      const int32_t lab = P.aIn.lab[pa];
-      const uint32_t ua = (uint32_t)P.A.src[P.aIn.perm[pa]];
+      const uint32_t ua = (uint32_t)P.aIn.nbr[pa];
       const bool fa = P.aOut.neps[ua] > 0;
-      const int32_t lo = lower_bound_i32(P.bIn.lab, s.bS + s.be, s.bE, lab);
-      const int32_t hi = upper_bound_i32(P.bIn.lab, lo, s.bE, lab);
+      label_range(P.bIn, s.vb, s.bS + s.be, s.bE, P.aIn.lab[pa], lo, hi);
       for (int32_t p = lo; p < hi; ++p) {
-        uint32_t ub = (uint32_t)P.B.src[P.bIn.perm[p]];
-        bwd_try(P, make_key(ua, ub, 0u, sh), q, cap, sc);
-        if (fa) bwd_try(P, make_key(ua, ub, 1u, sh), q, cap, sc);
+        const uint32_t ub = (uint32_t)P.bIn.nbr[p];
+        f(make_key(ua, ub, 0u, sh));
+        if (fa) f(make_key(ua, ub, 1u, sh));
       }
     } else {
       const int32_t pb = s.bS + s.be + (int32_t)j;
-      const int32_t lab = P.bIn.lab[pb];
-      const uint32_t ub = (uint32_t)P.B.src[P.bIn.perm[pb]];
-      const int32_t lo = lower_bound_i32(P.aIn.lab, s.aS + s.ae, s.aE, lab);
-      const int32_t hi = upper_bound_i32(P.aIn.lab, lo, s.aE, lab);
+      const uint32_t ub = (uint32_t)P.bIn.nbr[pb];
+      label_range(P.aIn, s.va, s.aS + s.ae, s.aE, P.bIn.lab[pb], lo, hi);
       for (int32_t p = lo; p < hi; ++p) {
-        uint32_t ua = (uint32_t)P.A.src[P.aIn.perm[p]];
-        bwd_try(P, make_key(ua, ub, 0u, sh), q, cap, sc);
-        if (P.aOut.neps[ua] > 0) bwd_try(P, make_key(ua, ub, 1u, sh), q, cap, sc);
+        const uint32_t ua = (uint32_t)P.aIn.nbr[p];
+        f(make_key(ua, ub, 0u, sh));
+        if (P.aOut.neps[ua] > 0) f(make_key(ua, ub, 1u, sh));
       }
     }
   }
 }
 
-// Level expansion over qin[lo, hi).  Each workgroup takes NT keys, computes
-// their work units, scans them in LDS and deals the units to its threads in
-// rounds of NT, so a key with thousands of epsilon arcs is split across the
-// whole workgroup.
 template <bool FWD>
-__global__ __launch_bounds__(NT) void k_expand(Problem P, const uint32_t *__restrict__ qin,
-                                               uint32_t lo, uint32_t hi, uint32_t *qout,
-                                               uint32_t cap, Scalars *sc) {
-  __shared__ uint32_t s_key[NT];
-  __shared__ ull s_off[NT + 1];
-  __shared__ ull s_w[NWAVES];
-  ull gen = 0;
-  for (ull base = (ull)lo + (ull)blockIdx.x * NT; base < hi; base += (ull)gridDim.x * NT) {
-    const ull i = base + threadIdx.x;
-    uint32_t key = 0;
-    ull units = 0;
-    if (i < hi) {
-      key = qin[i];
-      units = FWD ? fwd_units(P, key) : bwd_units(P, key);
+__device__ __forceinline__ uint32_t units_of(const Problem &P, uint32_t key) {
+  if (FWD) return fwd_units(fwd_info(P, key));
+  return bwd_units(bwd_info(P, key));
+}
+
+// A key reached for the first time: forward = newly accessible; backward =
+// accessible and newly co-accessible.
+template <bool FWD>
+__device__ __forceinline__ bool first_visit(const Problem &P, uint32_t k) {
+  if (FWD) return claim(P.vis, k);
+  return test_bit(P.vis, k) && claim(P.coacc, k);
+}
+
+// A newly claimed key either becomes this thread's next key (depth-first
+// continuation, only for light keys) or is appended to the next frontier.
+template <bool FWD>
+__device__ __forceinline__ void offer(const Problem &P, bool fresh, uint32_t v, uint32_t &cont,
+                                      int depth, const Pusher &pu) {
+  bool take = false;
+  if (fresh && cont == NO_KEY && depth < P.chain_max) take = units_of<FWD>(P, v) <= LIGHT_SEARCH;
+  if (take) cont = v;
+  wave_push(fresh && !take, v, pu);
+}
+
+// Per-thread search counters, summed per wavefront at kernel end.
+struct Tally {
+  ull gen = 0;        // moves generated (forward)
+  uint32_t nacc = 0;  // keys reached for the first time (forward)
+};
+
+__device__ __forceinline__ void flush_tally(Tally &t, Scalars *sc) {
+  const ull gen = wave_sum(t.gen);
+  const uint32_t nacc = wave_sum(t.nacc);
+  if (__lane_id() == 0) {
+    if (gen) atomicAdd(&sc->generated, gen);
+    if (nacc) atomicAdd(&sc->naccessible, nacc);
+  }
+}
+
+// Visit one move target (forward) or predecessor (backward) v.
+template <bool FWD>
+__device__ __forceinline__ void visit(const Problem &P, uint32_t v, uint32_t &cont, int depth,
+                                      const Pusher &pu, const Pusher &acc, Tally &t) {
+  const bool fresh = first_visit<FWD>(P, v);
+  if (FWD) {
+    ++t.gen;
+    note_accessible(P, fresh, v, acc, t.nacc);
+  }
+  offer<FWD>(P, fresh, v, cont, depth, pu);
+}
+
+// Expand `key` and then, depth-first, the light keys it discovers, until a
+// key discovers nothing new or the depth budget is spent.
+template <bool FWD>
+__device__ void run_chain(const Problem &P, uint32_t key, int depth, const Pusher &pu,
+                          const Pusher &acc, Tally &t) {
+  while (key != NO_KEY) {
+    uint32_t cont = NO_KEY;
+    auto f = [&](uint32_t v) { visit<FWD>(P, v, cont, depth, pu, acc, t); };
+    if (FWD) {
+      const Fwd s = fwd_info(P, key);
+      const uint32_t n = fwd_units(s);
+      for (uint32_t u = 0; u < n; ++u) fwd_unit(P, s, u, f);
+    } else {
+      const Bwd s = bwd_info(P, key);
+      const uint32_t n = bwd_units(s);
+      for (uint32_t u = 0; u < n; ++u) bwd_unit(P, s, u, f);
     }
-    ull total;
-    ull ex = block_excl_scan<ull>(units, s_w, total);
-    s_key[threadIdx.x] = key;
-    s_off[threadIdx.x] = ex;
-    if (threadIdx.x == 0) s_off[NT] = total;
-    __syncthreads();
-    for (ull r = 0; r < total; r += NT) {
-      const ull u = r + threadIdx.x;
-      if (u < total) {
-        // owner = largest o with s_off[o] <= u (it has units > 0)
-        int a = 0, b = NT - 1;
-        while (a < b) {
-          int mid = (a + b + 1) >> 1;
-          if (s_off[mid] <= u) a = mid; else b = mid - 1;
+    key = cont;
+    ++depth;
+  }
+}
+
+// Generation step 1: every frontier key Q[qlo, qhi).  Light keys are expanded
+// by their thread (with continuation); heavy keys are listed with the prefix
+// of their unit counts (one packed 64-bit atomic per wavefront keeps list
+// positions and unit offsets consistent) for step 2.
+template <bool FWD>
+__global__ __launch_bounds__(NT) void k_gen_expand(Problem P, Pusher pu, Pusher acc,
+                                                   uint32_t *heavy, uint32_t *hoff, int g) {
+  Scalars *sc = pu.sc;
+  if (sc->overflow) return;
+  const GenDesc d = sc->D[g & 1];
+  Tally t;
+  for (ull i0 = (ull)d.qlo + (ull)blockIdx.x * NT; i0 < d.qhi; i0 += (ull)gridDim.x * NT) {
+    const ull i = i0 + threadIdx.x;
+    const bool valid = i < d.qhi;
+    const uint32_t key = valid ? pu.Q[i] : 0u;
+    const uint32_t units = valid ? units_of<FWD>(P, key) : 0u;
+    const bool hv = valid && units > LIGHT_SEARCH;
+    const unsigned long long m = __ballot(hv);
+    if (m) {
+      const ull mine = hv ? (ull)units : 0ull;
+      const ull incl = wave_incl_scan(mine);
+      const ull tot = __shfl(incl, WAVE - 1, WAVE);
+      const int leader = __ffsll(m) - 1;
+      ull old = 0;
+      if ((int)__lane_id() == leader) old = atomicAdd(&sc->hpack, (tot << 32) | (ull)__popcll(m));
+      old = __shfl(old, leader, WAVE);
+      if (hv) {
+        const ull pos = (ull)d.hlo + (old & 0xffffffffull) + (ull)__popcll(m & __lanemask_lt());
+        const ull off = (old >> 32) + incl - mine;
+        if (pos < pu.cap && (old >> 32) + tot < (1ull << 32)) {
+          heavy[pos] = key;
+          hoff[pos] = (uint32_t)off;
+        } else {
+          atomicOr(&sc->overflow, 2u);
         }
-        const uint32_t local = (uint32_t)(u - s_off[a]);
-        if (FWD) fwd_unit(P, s_key[a], local, qout, cap, sc, gen);
-        else bwd_unit(P, s_key[a], local, qout, cap, sc);
       }
     }
-    __syncthreads();
+    if (valid && !hv) run_chain<FWD>(P, key, 0, pu, acc, t);
   }
-  if (FWD) {
-    gen = wave_sum(gen);
-    if (__lane_id() == 0 && gen) atomicAdd(&sc->generated, gen);
+  if (FWD) flush_tally(t, sc);
+}
+
+// Generation step 2: one thread per unit of this generation's heavy keys.
+template <bool FWD>
+__global__ __launch_bounds__(NT) void k_gen_units(Problem P, Pusher pu, Pusher acc,
+                                                  const uint32_t *__restrict__ heavy,
+                                                  const uint32_t *__restrict__ hoff, int g) {
+  Scalars *sc = pu.sc;
+  if (sc->overflow) return;  // the heavy list may be incomplete
+  const GenDesc d = sc->D[g & 1];
+  const ull hp = sc->hpack;
+  const ull U = hp >> 32;
+  const uint32_t n = (uint32_t)(hp & 0xffffffffull);
+  const uint32_t *hk = heavy + d.hlo;
+  const uint32_t *ho = hoff + d.hlo;
+  Tally t;
+  for (ull u = (ull)blockIdx.x * NT + threadIdx.x; u < U; u += (ull)gridDim.x * NT) {
+    uint32_t a = 0, b = n - 1;  // largest i with ho[i] <= u
+    while (a < b) {
+      const uint32_t mid = (a + b + 1) >> 1;
+      if (ho[mid] <= u) a = mid; else b = mid - 1;
+    }
+    const uint32_t key = hk[a];
+    const uint32_t local = (uint32_t)(u - ho[a]);
+    uint32_t cont = NO_KEY;
+    auto f = [&](uint32_t v) { visit<FWD>(P, v, cont, 0, pu, acc, t); };
+    if (FWD) fwd_unit(P, fwd_info(P, key), local, f);
+    else bwd_unit(P, bwd_info(P, key), local, f);
+    if (cont != NO_KEY) run_chain<FWD>(P, cont, 1, pu, acc, t);
   }
+  if (FWD) flush_tally(t, sc);
+}
+
+// Generation step 3: the keys appended during this generation form the next
+// frontier.
+__global__ void k_gen_advance(Scalars *sc, int g, uint32_t cap) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  const GenDesc d = sc->D[g & 1];
+  GenDesc nd;
+  nd.qlo = d.qhi;
+  nd.qhi = sc->tail < cap ? sc->tail : cap;
+  nd.hlo = d.hlo + (uint32_t)(sc->hpack & 0xffffffffull);
+  nd.pad = 0;
+  sc->D[(g + 1) & 1] = nd;
+  sc->hpack = 0;
+  if (d.qlo < d.qhi) sc->gens = (uint32_t)g + 1;
+}
+
+__global__ void k_gen_init(Scalars *sc, uint32_t cap) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  GenDesc d;
+  d.qlo = 0;
+  d.qhi = sc->tail < cap ? sc->tail : cap;
+  d.hlo = 0;
+  d.pad = 0;
+  sc->D[0] = d;
+  sc->D[1] = d;
+  sc->hpack = 0;
+  sc->gens = 0;
 }
 
 __global__ __launch_bounds__(NT) void k_collect(const uint8_t *__restrict__ flags, int V,
@@ -389,35 +537,22 @@ __global__ __launch_bounds__(NT) void k_collect(const uint8_t *__restrict__ flag
 __global__ __launch_bounds__(NT) void k_seed(Problem P, const int32_t *__restrict__ la,
                                              const uint32_t *__restrict__ na_p,
                                              const int32_t *__restrict__ lb,
-                                             const uint32_t *__restrict__ nb_p, uint32_t *q,
-                                             uint32_t cap, Scalars *sc) {
+                                             const uint32_t *__restrict__ nb_p, Pusher pu,
+                                             Pusher acc) {
   const ull na = *na_p, nb = *nb_p, n = na * nb;
+  Tally t;
   for (ull i0 = (ull)blockIdx.x * NT; i0 < n; i0 += (ull)gridDim.x * NT) {
     const ull i = i0 + threadIdx.x;
-    bool want = false;
+    bool fresh = false;
     uint32_t k = 0;
     if (i < n) {
       k = make_key((uint32_t)la[i / nb], (uint32_t)lb[i % nb], 0u, P.shiftB);
-      want = claim(P.vis, k);
+      fresh = claim(P.vis, k);
     }
-    wave_push(want, k, q, cap, sc);
+    note_accessible(P, fresh, k, acc, t.nacc);
+    wave_push(fresh, k, pu);
   }
-}
-
-__global__ __launch_bounds__(NT) void k_bwd_seed(Problem P, const uint32_t *__restrict__ fq,
-                                                 uint32_t n, uint32_t *bq, uint32_t cap,
-                                                 Scalars *sc) {
-  for (ull i0 = (ull)blockIdx.x * NT; i0 < n; i0 += (ull)gridDim.x * NT) {
-    const ull i = i0 + threadIdx.x;
-    bool want = false;
-    uint32_t k = 0;
-    if (i < n) {
-      k = fq[i];
-      uint32_t qa = key_qa(k, P.shiftB), qb = key_qb(k, P.shiftB);
-      if (P.A.accept[qa] && P.B.accept[qb]) want = claim(P.coacc, k);
-    }
-    wave_push(want, k, bq, cap, sc);
-  }
+  flush_tally(t, pu.sc);
 }
 
 // ---------------------------------------------------------------------------
@@ -452,19 +587,19 @@ __device__ __forceinline__ uint32_t out_units(const Fwd &s) { return s.eA + (uin
 
 // Sequential enumeration of a state's moves in canonical order: A-epsilon
 // arcs, B-epsilon arcs, then matching arcs by (label, a, b).  The join walks
-// the label groups of the side with fewer non-epsilon arcs and binary-searches
-// the other side's bucket; each group is emitted row-major (a outer, b inner).
+// the label groups of the side with fewer non-epsilon arcs and looks up the
+// other side's bucket; each group is emitted row-major (a outer, b inner).
 template <class Visit>
 __device__ __forceinline__ void enum_light(const Problem &P, const Fwd &s, Visit &&vis) {
   const uint32_t sh = P.shiftB;
   for (int32_t p = s.aS; p < s.aS + (int32_t)s.eA; ++p) {
     int32_t ea = P.aOut.perm[p];
-    vis(make_key((uint32_t)P.A.dst[ea], s.qb, 0u, sh), P.A.il[ea], 0, P.A.w[ea], ea, -1);
+    vis(make_key((uint32_t)P.aOut.nbr[p], s.qb, 0u, sh), P.A.il[ea], 0, P.A.w[ea], ea, -1);
   }
   const uint32_t f2 = s.ae > 0 ? 1u : 0u;
   for (int32_t p = s.bS; p < s.bS + s.be; ++p) {
     int32_t eb = P.bOut.perm[p];
-    vis(make_key(s.qa, (uint32_t)P.B.dst[eb], f2, sh), 0, P.B.ol[eb], P.B.w[eb], -1, eb);
+    vis(make_key(s.qa, (uint32_t)P.bOut.nbr[p], f2, sh), 0, P.B.ol[eb], P.B.w[eb], -1, eb);
   }
   if (!s.mU) return;
   if (s.nA <= s.nB) {
@@ -473,17 +608,18 @@ __device__ __forceinline__ void enum_light(const Problem &P, const Fwd &s, Visit
       const int32_t lab = P.aOut.lab[p];
       int32_t pend = p + 1;
       while (pend < s.aE && P.aOut.lab[pend] == lab) ++pend;
-      const int32_t lo = lower_bound_i32(P.bOut.lab, bl, s.bE, lab);
-      const int32_t hi = upper_bound_i32(P.bOut.lab, lo, s.bE, lab);
-      bl = hi;
+      int32_t lo, hi;
+      label_range(P.bOut, s.qb, bl, s.bE, lab, lo, hi);
+      if (lo < hi) bl = hi;
       for (int32_t pa = p; pa < pend && lo < hi; ++pa) {
         const int32_t ea = P.aOut.perm[pa];
-        const uint32_t da = (uint32_t)P.A.dst[ea];
+        const uint32_t da = (uint32_t)P.aOut.nbr[pa];
         const int32_t ia = P.A.il[ea];
         const float wa = P.A.w[ea];
         for (int32_t pb = lo; pb < hi; ++pb) {
           const int32_t eb = P.bOut.perm[pb];
-          vis(make_key(da, (uint32_t)P.B.dst[eb], 0u, sh), ia, P.B.ol[eb], wa + P.B.w[eb], ea, eb);
+          vis(make_key(da, (uint32_t)P.bOut.nbr[pb], 0u, sh), ia, P.B.ol[eb], wa + P.B.w[eb], ea,
+              eb);
         }
       }
       p = pend;
@@ -494,17 +630,18 @@ __device__ __forceinline__ void enum_light(const Problem &P, const Fwd &s, Visit
       const int32_t lab = P.bOut.lab[p];
       int32_t pend = p + 1;
       while (pend < s.bE && P.bOut.lab[pend] == lab) ++pend;
-      const int32_t lo = lower_bound_i32(P.aOut.lab, al, s.aE, lab);
-      const int32_t hi = upper_bound_i32(P.aOut.lab, lo, s.aE, lab);
-      al = hi;
+      int32_t lo, hi;
+      label_range(P.aOut, s.qa, al, s.aE, lab, lo, hi);
+      if (lo < hi) al = hi;
       for (int32_t pa = lo; pa < hi; ++pa) {
         const int32_t ea = P.aOut.perm[pa];
-        const uint32_t da = (uint32_t)P.A.dst[ea];
+        const uint32_t da = (uint32_t)P.aOut.nbr[pa];
         const int32_t ia = P.A.il[ea];
         const float wa = P.A.w[ea];
         for (int32_t pb = p; pb < pend; ++pb) {
           const int32_t eb = P.bOut.perm[pb];
-          vis(make_key(da, (uint32_t)P.B.dst[eb], 0u, sh), ia, P.B.ol[eb], wa + P.B.w[eb], ea, eb);
+          vis(make_key(da, (uint32_t)P.bOut.nbr[pb], 0u, sh), ia, P.B.ol[eb], wa + P.B.w[eb], ea,
+              eb);
         }
       }
       p = pend;
@@ -541,7 +678,7 @@ __device__ uint32_t heavy_state(const Problem &P, uint32_t id, uint32_t key, uin
     uint32_t d = 0;
     if (i < s.eA) {
       ea = P.aOut.perm[s.aS + (int32_t)i];
-      d = make_key((uint32_t)P.A.dst[ea], s.qb, 0u, sh);
+      d = make_key((uint32_t)P.aOut.nbr[s.aS + (int32_t)i], s.qb, 0u, sh);
       keep = test_bit(P.coacc, d);
     }
     uint32_t tot;
@@ -557,7 +694,7 @@ __device__ uint32_t heavy_state(const Problem &P, uint32_t id, uint32_t key, uin
     uint32_t d = 0;
     if (i < (uint32_t)s.be) {
       eb = P.bOut.perm[s.bS + (int32_t)i];
-      d = make_key(s.qa, (uint32_t)P.B.dst[eb], f2, sh);
+      d = make_key(s.qa, (uint32_t)P.bOut.nbr[s.bS + (int32_t)i], f2, sh);
       keep = test_bit(P.coacc, d);
     }
     uint32_t tot;
@@ -571,27 +708,24 @@ __device__ uint32_t heavy_state(const Problem &P, uint32_t id, uint32_t key, uin
     for (uint32_t c = 0; c < s.nA; c += NT) {
       const uint32_t i = c + t;
       int32_t lo = 0, hi = 0, ea = 0;
-      uint32_t kept = 0;
+      uint32_t kept = 0, da = 0;
       if (i < s.nA) {
         const int32_t pa = s.aS + s.ae + (int32_t)i;
-        const int32_t lab = P.aOut.lab[pa];
         ea = P.aOut.perm[pa];
-        lo = lower_bound_i32(P.bOut.lab, s.bS + s.be, s.bE, lab);
-        hi = upper_bound_i32(P.bOut.lab, lo, s.bE, lab);
-        const uint32_t da = (uint32_t)P.A.dst[ea];
+        da = (uint32_t)P.aOut.nbr[pa];
+        label_range(P.bOut, s.qb, s.bS + s.be, s.bE, P.aOut.lab[pa], lo, hi);
         for (int32_t pb = lo; pb < hi; ++pb)
-          kept += test_bit(P.coacc, make_key(da, (uint32_t)P.B.dst[P.bOut.perm[pb]], 0u, sh));
+          kept += test_bit(P.coacc, make_key(da, (uint32_t)P.bOut.nbr[pb], 0u, sh));
       }
       uint32_t tot;
       uint32_t ex = block_excl_scan<uint32_t>(kept, s_w, tot);
       if (FILL && kept) {
-        const uint32_t da = (uint32_t)P.A.dst[ea];
         const int32_t ia = P.A.il[ea];
         const float wa = P.A.w[ea];
         uint32_t pos = pos0 + run + ex;
         for (int32_t pb = lo; pb < hi; ++pb) {
           const int32_t eb = P.bOut.perm[pb];
-          const uint32_t d = make_key(da, (uint32_t)P.B.dst[eb], 0u, sh);
+          const uint32_t d = make_key(da, (uint32_t)P.bOut.nbr[pb], 0u, sh);
           if (test_bit(P.coacc, d)) put_arc(O, P, pos++, id, d, ia, P.B.ol[eb], wa + P.B.w[eb], ea, eb);
         }
       }
@@ -703,10 +837,11 @@ hipError_t launch_validate(const DevGraph &g, int side, uint32_t *err, uint32_t 
   return hipGetLastError();
 }
 
-hipError_t build_view(const DevGraph &g, int side, bool by_dst, int lab_bits, int32_t *perm,
-                      int32_t *lab, int32_t *neps, int32_t *off_out, unsigned long long *k0,
-                      int32_t *v0, unsigned long long *k1, int32_t *v1, void *sort_temp,
-                      uint32_t *eps_states, hipStream_t s) {
+hipError_t build_view(const DevGraph &g, int side, bool by_dst, int lab_bits, int32_t lab_max,
+                      int32_t *perm, int32_t *lab, int32_t *nbr, int32_t *neps, int32_t *lut,
+                      int32_t *off_out, unsigned long long *k0, int32_t *v0,
+                      unsigned long long *k1, int32_t *v1, void *sort_temp, uint32_t *eps_states,
+                      hipStream_t s) {
   const size_t E = (size_t)g.E;
   hipError_t e;
   if (E) {
@@ -714,7 +849,8 @@ hipError_t build_view(const DevGraph &g, int side, bool by_dst, int lab_bits, in
     if ((e = hipGetLastError()) != hipSuccess) return e;
     int bits = bitlen((unsigned long long)(g.V > 0 ? g.V - 1 : 0)) + lab_bits;
     if ((e = radix_sort(k0, v0, k1, v1, E, bits, sort_temp, s)) != hipSuccess) return e;
-    k_split<<<grid_for(E), NT, 0, s>>>(k0, v0, (long long)E, lab_bits, perm, lab);
+    k_split<<<grid_for(E), NT, 0, s>>>(g, by_dst ? 1 : 0, k0, v0, (long long)E, lab_bits, perm,
+                                       lab, nbr);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   const int32_t *off = g.off;
@@ -727,36 +863,46 @@ hipError_t build_view(const DevGraph &g, int side, bool by_dst, int lab_bits, in
   if (g.V) {
     k_neps<<<grid_for((size_t)g.V), NT, 0, s>>>(off, lab, g.V, neps, eps_states);
     if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (lut) {
+      const size_t n = (size_t)g.V * (size_t)(lab_max + 2);
+      k_build_lut<<<grid_for(n, 8192), NT, 0, s>>>(off, lab, g.V, lab_max + 2, lut);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
   }
   return hipSuccess;
 }
 
 hipError_t launch_seed_lists(const Problem &P, int32_t *la, uint32_t *na, int32_t *lb,
-                             uint32_t *nb, uint32_t *queue, uint32_t cap, Scalars *sc,
-                             hipStream_t s) {
+                             uint32_t *nb, uint32_t *queue, uint32_t *acc_list, uint32_t cap,
+                             Scalars *sc, hipStream_t s) {
   k_collect<<<grid_for((size_t)P.A.V, 1024), NT, 0, s>>>(P.A.start, P.A.V, la, na);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   k_collect<<<grid_for((size_t)P.B.V, 1024), NT, 0, s>>>(P.B.start, P.B.V, lb, nb);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  k_seed<<<64, NT, 0, s>>>(P, la, na, lb, nb, queue, cap, sc);
+  const Pusher pu{queue, cap, &sc->tail, sc}, acc{acc_list, cap, &sc->tail2, sc};
+  k_seed<<<64, NT, 0, s>>>(P, la, na, lb, nb, pu, acc);
   return hipGetLastError();
 }
 
-hipError_t launch_expand(const Problem &P, bool forward, const uint32_t *qin, uint32_t lo,
-                         uint32_t hi, uint32_t *qout, uint32_t cap, Scalars *sc,
-                         hipStream_t s) {
-  if (hi <= lo) return hipSuccess;
-  unsigned g = grid_for((size_t)(hi - lo), 8192);
-  if (forward) k_expand<true><<<g, NT, 0, s>>>(P, qin, lo, hi, qout, cap, sc);
-  else k_expand<false><<<g, NT, 0, s>>>(P, qin, lo, hi, qout, cap, sc);
+hipError_t launch_gen_init(Scalars *sc, uint32_t cap, hipStream_t s) {
+  k_gen_init<<<1, 64, 0, s>>>(sc, cap);
   return hipGetLastError();
 }
 
-hipError_t launch_bwd_seed(const Problem &P, const uint32_t *fq, uint32_t n, uint32_t *bq,
-                           uint32_t cap, Scalars *sc, hipStream_t s) {
-  if (!n) return hipSuccess;
-  k_bwd_seed<<<grid_for(n, 8192), NT, 0, s>>>(P, fq, n, bq, cap, sc);
+hipError_t launch_generation(const Problem &P, bool forward, uint32_t *Q, uint32_t *acc_list,
+                             uint32_t cap, uint32_t *heavy, uint32_t *hoff, int g, Scalars *sc,
+                             hipStream_t s) {
+  const Pusher pu{Q, cap, &sc->tail, sc}, acc{acc_list, cap, &sc->tail2, sc};
+  constexpr unsigned GRID = 1024;
+  if (forward) {
+    k_gen_expand<true><<<GRID, NT, 0, s>>>(P, pu, acc, heavy, hoff, g);
+    k_gen_units<true><<<GRID, NT, 0, s>>>(P, pu, acc, heavy, hoff, g);
+  } else {
+    k_gen_expand<false><<<GRID, NT, 0, s>>>(P, pu, acc, heavy, hoff, g);
+    k_gen_units<false><<<GRID, NT, 0, s>>>(P, pu, acc, heavy, hoff, g);
+  }
+  k_gen_advance<<<1, 64, 0, s>>>(sc, g, cap);
   return hipGetLastError();
 }
 

@@ -26,6 +26,8 @@ FST_ERR_STATE = 6
 
 FST_OPT_MAX_WORKSPACE = 1
 FST_OPT_TIMING = 2
+FST_OPT_LABEL_BUCKETS = 3
+FST_OPT_CHAIN_DEPTH = 4
 
 PHASES = ("preprocess", "forward", "backward", "count", "fill")
 
