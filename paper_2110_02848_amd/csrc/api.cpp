@@ -41,10 +41,8 @@ struct fst_ctx {
 
   DevBuf scal, lists;
   DevBuf k0, k1, v0, v1, sort_tmp, scan_tmp;
-  DevBuf aOutPerm, aOutLab, aOutNbr, aOutNeps, aOutLut, bOutPerm, bOutLab, bOutNbr, bOutNeps,
-      bOutLut;
-  DevBuf aInOff, aInPerm, aInLab, aInNbr, aInNeps, aInLut, bInOff, bInPerm, bInLab, bInNbr,
-      bInNeps, bInLut;
+  DevBuf aOutPerm, aOutArc, aOutRec, aOutLut, bOutPerm, bOutArc, bOutRec, bOutLut;
+  DevBuf aInOff, aInPerm, aInArc, aInRec, aInLut, bInOff, bInPerm, bInArc, bInRec, bInLut;
   DevBuf vis, coacc, wbase, fq, bq, heavy, hoff, cnt;
   Scalars *h_sc = nullptr;
   hipEvent_t ev[NEV] = {};
@@ -164,22 +162,17 @@ int finish_empty(fst_ctx *c, int64_t *V_C, int64_t *E_C) {
   return FST_OK;
 }
 
-// Frontier search from the keys already in q[0, tail): generations are queued
-// in batches without host round trips; the host only checks after each
-// batch whether the frontier has emptied (extra generations are no-ops).
-int search(fst_ctx *c, bool forward, uint32_t *q, uint32_t cap, int64_t *levels,
-           hipStream_t s) {
-  Scalars *d_sc = as<Scalars>(c->scal);
-  HIP_TRY(launch_gen_init(d_sc, cap, s));
+// Generations are queued in batches with no host round trip; after each batch
+// the host checks whether the next generation has any work (generations
+// queued after the search has ended do nothing).
+int search(fst_ctx *c, const SearchArgs &S, bool forward, int64_t *levels, hipStream_t s) {
   int g = 0, batch = 4;
   for (;;) {
-    for (int b = 0; b < batch; ++b, ++g)
-      HIP_TRY(launch_generation(c->P, forward, q, as<uint32_t>(c->bq), cap,
-                                as<uint32_t>(c->heavy), as<uint32_t>(c->hoff), g, d_sc, s));
+    for (int b = 0; b < batch; ++b, ++g) HIP_TRY(launch_generation(c->P, S, forward, g, s));
     FST_TRY(readback(c, s));
     if (c->h_sc->overflow) return FST_ERR_TOO_LARGE;
-    const GenDesc d = c->h_sc->D[g & 1];
-    if (d.qlo == d.qhi) break;
+    const GenSlot &nx = c->h_sc->G[g % 3];
+    if (nx.qcount == 0 && (uint32_t)nx.hpack == 0) break;
     if (batch < 64) batch *= 2;
   }
   *levels = c->h_sc->gens;
@@ -190,7 +183,7 @@ int search(fst_ctx *c, bool forward, uint32_t *q, uint32_t cap, int64_t *levels,
 constexpr size_t LUT_BUDGET = (size_t)256 << 20;
 
 size_t lut_bytes(int32_t V, uint32_t lab_max) {
-  return (size_t)V * ((size_t)lab_max + 2) * sizeof(int32_t);
+  return (size_t)V * ((size_t)lab_max + 1) * sizeof(int4);
 }
 
 int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, int64_t *V_C,
@@ -228,13 +221,13 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   const bool lutA = c->buckets && lut_bytes(VA, maxA) <= LUT_BUDGET;
   const bool lutB = c->buckets && lut_bytes(VB, maxB) <= LUT_BUDGET;
   struct ViewBufs {
-    DevBuf *perm, *lab, *nbr, *neps, *lut, *off;
+    DevBuf *perm, *arc, *rec, *lut, *off;
   };
-  const ViewBufs vb[4] = {
-      {&c->aOutPerm, &c->aOutLab, &c->aOutNbr, &c->aOutNeps, &c->aOutLut, nullptr},
-      {&c->bOutPerm, &c->bOutLab, &c->bOutNbr, &c->bOutNeps, &c->bOutLut, nullptr},
-      {&c->aInPerm, &c->aInLab, &c->aInNbr, &c->aInNeps, &c->aInLut, &c->aInOff},
-      {&c->bInPerm, &c->bInLab, &c->bInNbr, &c->bInNeps, &c->bInLut, &c->bInOff}};
+  // built in this order: A's in-view needs A's out-view records
+  const ViewBufs vb[4] = {{&c->aOutPerm, &c->aOutArc, &c->aOutRec, &c->aOutLut, nullptr},
+                          {&c->bOutPerm, &c->bOutArc, &c->bOutRec, &c->bOutLut, nullptr},
+                          {&c->aInPerm, &c->aInArc, &c->aInRec, &c->aInLut, &c->aInOff},
+                          {&c->bInPerm, &c->bInArc, &c->bInRec, &c->bInLut, &c->bInOff}};
   unsigned long long *k0 = as<unsigned long long>(c->k0), *k1 = as<unsigned long long>(c->k1);
   int32_t *v0 = as<int32_t>(c->v0), *v1 = as<int32_t>(c->v1);
   View views[4];
@@ -243,21 +236,19 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
     const DevGraph &g = isA ? dA : dB;
     const bool lut = isA ? lutA : lutB;
     const uint32_t lmax = isA ? maxA : maxB;
-    FST_TRY(ensure(c, *vb[i].perm, (size_t)g.E * 4));
-    FST_TRY(ensure(c, *vb[i].lab, (size_t)g.E * 4));
-    FST_TRY(ensure(c, *vb[i].nbr, (size_t)g.E * 4));
-    FST_TRY(ensure(c, *vb[i].neps, (size_t)g.V * 4));
+    FST_TRY(ensure(c, *vb[i].perm, (size_t)g.E * sizeof(int32_t)));
+    FST_TRY(ensure(c, *vb[i].arc, (size_t)g.E * sizeof(int2)));
+    FST_TRY(ensure(c, *vb[i].rec, (size_t)g.V * sizeof(int4)));
     if (lut) FST_TRY(ensure(c, *vb[i].lut, lut_bytes(g.V, lmax)));
-    if (in) FST_TRY(ensure(c, *vb[i].off, ((size_t)g.V + 1) * 4));
-    int32_t *off = in ? as<int32_t>(*vb[i].off) : nullptr;
-    int32_t *lutp = lut ? as<int32_t>(*vb[i].lut) : nullptr;
-    HIP_TRY(build_view(g, isA ? 0 : 1, in, isA ? labA : labB, (int32_t)lmax,
-                       as<int32_t>(*vb[i].perm), as<int32_t>(*vb[i].lab), as<int32_t>(*vb[i].nbr),
-                       as<int32_t>(*vb[i].neps), lutp, off, k0, v0, k1, v1, c->sort_tmp.p,
-                       i == 0 ? &d_sc->nEpsStatesA : nullptr, s));
-    views[i] = View{in ? off : g.off, as<int32_t>(*vb[i].perm), as<int32_t>(*vb[i].lab),
-                    as<int32_t>(*vb[i].nbr), as<int32_t>(*vb[i].neps), lutp,
-                    (int32_t)lmax + 2};
+    if (in) FST_TRY(ensure(c, *vb[i].off, ((size_t)g.V + 1) * sizeof(int32_t)));
+    int4 *lutp = lut ? as<int4>(*vb[i].lut) : nullptr;
+    const int4 *eps_rec = (i == 2) ? as<int4>(c->aOutRec) : nullptr;
+    HIP_TRY(build_view(g, isA ? 0 : 1, in, isA ? labA : labB, (int32_t)lmax, as<int4>(*vb[i].rec),
+                       as<int2>(*vb[i].arc), as<int32_t>(*vb[i].perm), lutp,
+                       in ? as<int32_t>(*vb[i].off) : nullptr, eps_rec, k0, v0, k1, v1,
+                       c->sort_tmp.p, i == 0 ? &d_sc->nEpsStatesA : nullptr, s));
+    views[i] = View{as<int4>(*vb[i].rec), as<int2>(*vb[i].arc), as<int32_t>(*vb[i].perm), lutp,
+                    (int32_t)lmax + 1};
   }
   FST_TRY(readback(c, s));
 
@@ -299,16 +290,24 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   uint32_t *cnts = reinterpret_cast<uint32_t *>(lb + VB);
   HIP_TRY(hipMemsetAsync(cnts, 0, 8, s));
   uint32_t *fq = as<uint32_t>(c->fq), *bq = as<uint32_t>(c->bq);
-  HIP_TRY(launch_seed_lists(P, la, cnts, lb, cnts + 1, fq, bq, cap, d_sc, s));
-  FST_TRY(search(c, true, fq, cap, &c->stats.fwd_levels, s));
+  SearchArgs S;
+  S.Q = fq;
+  S.heavy = as<uint32_t>(c->heavy);
+  S.hoff = as<uint32_t>(c->hoff);
+  S.acc = bq;
+  S.cap = cap;
+  S.sc = d_sc;
+  HIP_TRY(hipMemsetAsync(d_sc->G, 0, sizeof(d_sc->G), s));
+  HIP_TRY(launch_seed_forward(P, S, la, cnts, lb, cnts + 1, s));
+  FST_TRY(search(c, S, true, &c->stats.fwd_levels, s));
   c->stats.accessible = c->h_sc->naccessible;
   c->stats.generated = (int64_t)c->h_sc->generated;
 
-  // ---- backward search ----
+  // ---- backward search, seeded by the accepting keys listed in bq ----
   mark(c, 2, s);
-  // the accepting keys listed in bq by the forward search seed it
-  HIP_TRY(hipMemcpyAsync(&d_sc->tail, &d_sc->tail2, sizeof(uint32_t), hipMemcpyDeviceToDevice, s));
-  FST_TRY(search(c, false, bq, cap, &c->stats.bwd_levels, s));
+  HIP_TRY(hipMemsetAsync(d_sc->G, 0, sizeof(d_sc->G), s));
+  HIP_TRY(launch_seed_backward(P, S, bq, s));
+  FST_TRY(search(c, S, false, &c->stats.bwd_levels, s));
 
   // ---- numbering and arc counts ----
   mark(c, 3, s);
@@ -386,14 +385,13 @@ void fst_ctx_destroy(fst_ctx *c) {
   if (!c) return;
   DeviceGuard g(c->device);
   (void)hipDeviceSynchronize();
-  DevBuf *bufs[] = {&c->scal,    &c->lists,    &c->k0,       &c->k1,       &c->v0,
-                    &c->v1,      &c->sort_tmp, &c->scan_tmp, &c->aOutPerm, &c->aOutLab,
-                    &c->aOutNbr, &c->aOutNeps, &c->aOutLut,  &c->bOutPerm, &c->bOutLab,
-                    &c->bOutNbr, &c->bOutNeps, &c->bOutLut,  &c->aInOff,   &c->aInPerm,
-                    &c->aInLab,  &c->aInNbr,   &c->aInNeps,  &c->aInLut,   &c->bInOff,
-                    &c->bInPerm, &c->bInLab,   &c->bInNbr,   &c->bInNeps,  &c->bInLut,
-                    &c->vis,     &c->coacc,    &c->wbase,    &c->fq,       &c->bq,
-                    &c->heavy,   &c->hoff,     &c->cnt};
+  DevBuf *bufs[] = {&c->scal,     &c->lists,    &c->k0,      &c->k1,      &c->v0,
+                    &c->v1,       &c->sort_tmp, &c->scan_tmp, &c->aOutPerm, &c->aOutArc,
+                    &c->aOutRec,  &c->aOutLut,  &c->bOutPerm, &c->bOutArc, &c->bOutRec,
+                    &c->bOutLut,  &c->aInOff,   &c->aInPerm, &c->aInArc,  &c->aInRec,
+                    &c->aInLut,   &c->bInOff,   &c->bInPerm, &c->bInArc,  &c->bInRec,
+                    &c->bInLut,   &c->vis,      &c->coacc,   &c->wbase,   &c->fq,
+                    &c->bq,       &c->heavy,    &c->hoff,    &c->cnt};
   for (DevBuf *b : bufs) release(*b);
   for (int i = 0; i < NEV; ++i)
     if (c->ev[i]) (void)hipEventDestroy(c->ev[i]);

@@ -1,13 +1,16 @@
 // Kernels of the eager composition C = A o B (paper Section 3.3) for gfx950.
 //
 //  * validation of the input layout (Section 3.2);
-//  * label-sorted arc views, the per-state "label buckets" used to join A's
-//    output labels with B's input labels in O(deg) instead of O(deg^2);
-//  * frontier expansion: one workgroup takes 256 frontier keys, a workgroup
-//    prefix sum spreads their (very uneven) work units over its threads, and
-//    new keys are claimed in a bitmap and appended with one atomic per
-//    wavefront (ballot + popcount);
-//  * the same expansion run backwards over in-arcs for co-accessibility;
+//  * label-sorted arc views with packed per-state and per-arc records and
+//    per-state label buckets, so that joining A's output labels with B's
+//    input labels costs one bucket lookup per arc instead of a scan of the
+//    arc-pair cross product;
+//  * the search over composite keys in generations: a light key is expanded
+//    by one thread, which then follows the light keys it reaches first
+//    depth-first; heavy keys (many epsilon arcs, large label joins) are cut
+//    into work units spread over the whole grid; new keys are claimed in a
+//    bitmap and appended with one atomic per wavefront (ballot + popcount);
+//  * the same search run backwards over in-arcs for co-accessibility;
 //  * compaction: a popcount prefix over the trim bitmap numbers the states in
 //    key order; arcs are counted, scanned and written in canonical order.
 #include "internal.h"
@@ -27,6 +30,8 @@ unsigned grid_for(size_t n, unsigned cap = 4096) {
   return (unsigned)g;
 }
 
+int bitlen(unsigned long long x) { return x ? 64 - __builtin_clzll(x) : 0; }
+
 __device__ __forceinline__ uint32_t wave_or(uint32_t x) {
 #pragma unroll
   for (int o = WAVE / 2; o > 0; o >>= 1) x |= __shfl_xor(x, o, WAVE);
@@ -39,6 +44,15 @@ __device__ __forceinline__ uint32_t wave_max(uint32_t x) {
     x = y > x ? y : x;
   }
   return x;
+}
+
+// First index in [lo, hi) whose label (.x) is >= x.
+__device__ __forceinline__ int32_t lb_label(const int2 *a, int32_t lo, int32_t hi, int32_t x) {
+  while (lo < hi) {
+    int32_t mid = lo + ((hi - lo) >> 1);
+    if (a[mid].x < x) lo = mid + 1; else hi = mid;
+  }
+  return lo;
 }
 
 // ---------------------------------------------------------------------------
@@ -94,30 +108,20 @@ __global__ __launch_bounds__(NT) void k_make_keys(DevGraph g, int side, int by_d
   }
 }
 
+// Sorted (key, arc) pairs -> arc records {label, other end} and arc ids.
 __global__ __launch_bounds__(NT) void k_split(DevGraph g, int by_dst, const ull *__restrict__ k,
                                               const int32_t *__restrict__ v, long long n,
-                                              int lab_bits, int32_t *__restrict__ perm,
-                                              int32_t *__restrict__ lab,
-                                              int32_t *__restrict__ nbr) {
+                                              int lab_bits, const int4 *__restrict__ eps_rec,
+                                              int32_t *__restrict__ perm,
+                                              int2 *__restrict__ arec) {
   const ull mask = (lab_bits >= 64) ? ~0ull : ((1ull << lab_bits) - 1ull);
   for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n;
        i += (long long)gridDim.x * NT) {
     const int32_t e = v[i];
     perm[i] = e;
-    lab[i] = (int32_t)(k[i] & mask);
-    nbr[i] = by_dst ? g.src[e] : g.dst[e];
-  }
-}
-
-// Label buckets: lut[v * S + l] = first position of label >= l in group v.
-__global__ __launch_bounds__(NT) void k_build_lut(const int32_t *__restrict__ off,
-                                                  const int32_t *__restrict__ lab, int V, int S,
-                                                  int32_t *__restrict__ lut) {
-  const long long n = (long long)V * S;
-  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n;
-       i += (long long)gridDim.x * NT) {
-    const int32_t v = (int32_t)(i / S), l = (int32_t)(i % S);
-    lut[i] = lower_bound_i32(lab, off[v], off[v + 1], l);
+    int32_t nb = by_dst ? g.src[e] : g.dst[e];
+    if (eps_rec && eps_rec[nb].y > 0) nb |= (int32_t)0x80000000;
+    arec[i] = make_int2((int32_t)(k[i] & mask), nb);
   }
 }
 
@@ -137,15 +141,23 @@ __global__ __launch_bounds__(NT) void k_group_offsets(const ull *__restrict__ k,
   }
 }
 
-__global__ __launch_bounds__(NT) void k_neps(const int32_t *__restrict__ off,
-                                             const int32_t *__restrict__ lab, int V,
-                                             int32_t *__restrict__ neps,
-                                             uint32_t *eps_states) {
+// State records.  eps_mode: 0 = no epsOutA flag (views of B), 1 = A's
+// out-view (flag from its own epsilon count), 2 = A's in-view (flag from
+// A's out-view records in eps_rec).
+__global__ __launch_bounds__(NT) void k_state_rec(const int32_t *__restrict__ off,
+                                                  const int2 *__restrict__ arec, int V,
+                                                  const uint8_t *__restrict__ accept,
+                                                  int eps_mode, const int4 *__restrict__ eps_rec,
+                                                  int4 *__restrict__ srec,
+                                                  uint32_t *eps_states) {
   for (long long v = (long long)blockIdx.x * NT + threadIdx.x; v < V;
        v += (long long)gridDim.x * NT) {
-    int32_t s0 = off[v], s1 = off[v + 1];
-    int32_t n = lower_bound_i32(lab, s0, s1, 1) - s0;
-    neps[v] = n;
+    const int32_t s0 = off[v], s1 = off[v + 1];
+    const int32_t n = lb_label(arec, s0, s1, 1) - s0;
+    int32_t flags = accept[v] ? (int32_t)FLAG_ACCEPT : 0;
+    if ((eps_mode == 1 && n > 0) || (eps_mode == 2 && eps_rec[v].y > 0))
+      flags |= (int32_t)FLAG_EPS_OUT;
+    srec[v] = make_int4(s0, n, s1, flags);
     if (eps_states) {
       unsigned long long m = __ballot(n > 0);
       if (m && __lane_id() == (unsigned)(__ffsll(m) - 1))
@@ -154,30 +166,58 @@ __global__ __launch_bounds__(NT) void k_neps(const int32_t *__restrict__ off,
   }
 }
 
+// Label buckets: lut[v * S + l] = {first position of label l, first > l,
+// neighbour of the first arc (or -1), 0}.
+__global__ __launch_bounds__(NT) void k_build_lut(const int4 *__restrict__ srec,
+                                                  const int2 *__restrict__ arec, int V, int S,
+                                                  int4 *__restrict__ lut) {
+  const long long n = (long long)V * S;
+  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n;
+       i += (long long)gridDim.x * NT) {
+    const int32_t v = (int32_t)(i / S), l = (int32_t)(i % S);
+    const int4 r = srec[v];
+    const int32_t lo = lb_label(arec, r.x, r.z, l);
+    const int32_t hi = lb_label(arec, lo, r.z, l + 1);
+    lut[i] = make_int4(lo, hi, lo < hi ? arec[lo].y : -1, 0);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // search helpers
 // ---------------------------------------------------------------------------
 
-// Positions of label `lab` inside group q of a view, whose non-epsilon part
-// is [lo, hi): one bucket lookup when the view has buckets, else a binary
-// search.
+// Positions [r0, r1) of label `lab` inside group q of a view, whose
+// non-epsilon part is [lo, hi), and the neighbour of the first of them: one
+// bucket lookup when the view has buckets, else a binary search.
 __device__ __forceinline__ void label_range(const View &v, uint32_t q, int32_t lo, int32_t hi,
-                                            int32_t lab, int32_t &r0, int32_t &r1) {
+                                            int32_t lab, int32_t &r0, int32_t &r1,
+                                            int32_t &nb0) {
   if (v.lut) {
-    if ((uint32_t)lab < (uint32_t)(v.lstride - 1)) {
-      const int32_t *b = v.lut + (size_t)q * (uint32_t)v.lstride + lab;
-      r0 = b[0];
-      r1 = b[1];
+    if ((uint32_t)lab < (uint32_t)v.lstride) {
+      const int4 b = v.lut[(size_t)q * (uint32_t)v.lstride + (uint32_t)lab];
+      r0 = b.x;
+      r1 = b.y;
+      nb0 = b.z;
     } else {
       r0 = r1 = hi;
+      nb0 = -1;
     }
     return;
   }
-  r0 = lower_bound_i32(v.lab, lo, hi, lab);
-  r1 = upper_bound_i32(v.lab, r0, hi, lab);
+  r0 = lb_label(v.arec, lo, hi, lab);
+  r1 = lb_label(v.arec, r0, hi, lab + 1);
+  nb0 = r0 < r1 ? v.arec[r0].y : -1;
 }
 
-// Claim key k in bitmap bm; true for exactly one caller per key.
+__device__ __forceinline__ void label_range(const View &v, uint32_t q, int32_t lo, int32_t hi,
+                                            int32_t lab, int32_t &r0, int32_t &r1) {
+  int32_t nb0;
+  label_range(v, q, lo, hi, lab, r0, r1, nb0);
+}
+
+// Claim key k in bitmap bm; true for exactly one caller per key.  The plain
+// load first matters: keys such as a lexicon root are reached by thousands
+// of threads at once, and only the first few should reach the atomic.
 __device__ __forceinline__ bool claim(uint32_t *bm, uint32_t k) {
   const uint32_t bit = 1u << (k & 31u);
   uint32_t *w = bm + (k >> 5);
@@ -208,24 +248,13 @@ __device__ __forceinline__ void wave_push(bool want, uint32_t key, const Pusher 
   }
 }
 
-// A key the forward search reached for the first time: count it, and if it
-// accepts, mark it co-accessible and list it as a seed of the backward search.
-__device__ __forceinline__ void note_accessible(const Problem &P, bool fresh, uint32_t v,
-                                                const Pusher &acc, uint32_t &nacc) {
-  bool accepting = false;
-  if (fresh) {
-    ++nacc;
-    accepting = P.A.accept[key_qa(v, P.shiftB)] && P.B.accept[key_qb(v, P.shiftB)];
-    if (accepting) atomicOr(P.coacc + (v >> 5), 1u << (v & 31u));
-  }
-  wave_push(accepting, v, acc);
-}
-
-// Move structure of a key (forward direction; also used by compaction).
+// Move structure of a key in the forward direction (also used to write C).
 struct Fwd {
   uint32_t qa, qb, f;
   int32_t aS, ae, aE, bS, be, bE;
   uint32_t eA, nA, nB, mU;
+  uint32_t epsA;    // epsOutA(qa)
+  uint32_t accept;  // accept(qa) and accept(qb)
 };
 
 __device__ __forceinline__ Fwd fwd_info(const Problem &P, uint32_t key) {
@@ -233,12 +262,16 @@ __device__ __forceinline__ Fwd fwd_info(const Problem &P, uint32_t key) {
   s.f = key_f(key);
   s.qb = key_qb(key, P.shiftB);
   s.qa = key_qa(key, P.shiftB);
-  s.aS = P.aOut.off[s.qa];
-  s.aE = P.aOut.off[s.qa + 1];
-  s.ae = P.aOut.neps[s.qa];
-  s.bS = P.bOut.off[s.qb];
-  s.bE = P.bOut.off[s.qb + 1];
-  s.be = P.bOut.neps[s.qb];
+  const int4 ra = P.aOut.srec[s.qa];
+  const int4 rb = P.bOut.srec[s.qb];
+  s.aS = ra.x;
+  s.ae = ra.y;
+  s.aE = ra.z;
+  s.bS = rb.x;
+  s.be = rb.y;
+  s.bE = rb.z;
+  s.epsA = ra.y > 0 ? 1u : 0u;
+  s.accept = (uint32_t)(ra.w & rb.w) & FLAG_ACCEPT;
   s.eA = s.f ? 0u : (uint32_t)s.ae;
   s.nA = (uint32_t)(s.aE - s.aS - s.ae);
   s.nB = (uint32_t)(s.bE - s.bS - s.be);
@@ -256,22 +289,23 @@ template <class F>
 __device__ __forceinline__ void fwd_unit(const Problem &P, const Fwd &s, uint32_t u, F &&f) {
   const uint32_t sh = P.shiftB;
   if (u < s.eA) {
-    f(make_key((uint32_t)P.aOut.nbr[s.aS + (int32_t)u], s.qb, 0u, sh));
+    f(make_key((uint32_t)P.aOut.arec[s.aS + (int32_t)u].y, s.qb, 0u, sh));
   } else if (u < s.eA + (uint32_t)s.be) {
-    f(make_key(s.qa, (uint32_t)P.bOut.nbr[s.bS + (int32_t)(u - s.eA)], s.ae > 0 ? 1u : 0u, sh));
+    f(make_key(s.qa, (uint32_t)P.bOut.arec[s.bS + (int32_t)(u - s.eA)].y, s.epsA, sh));
   } else {
     const uint32_t j = u - s.eA - (uint32_t)s.be;
     int32_t lo, hi;
+    int32_t nb;
     if (s.nA <= s.nB) {
-      const int32_t pa = s.aS + s.ae + (int32_t)j;
-      const uint32_t da = (uint32_t)P.aOut.nbr[pa];
-      label_range(P.bOut, s.qb, s.bS + s.be, s.bE, P.aOut.lab[pa], lo, hi);
-      for (int32_t p = lo; p < hi; ++p) f(make_key(da, (uint32_t)P.bOut.nbr[p], 0u, sh));
+      const int2 ar = P.aOut.arec[s.aS + s.ae + (int32_t)j];
+      label_range(P.bOut, s.qb, s.bS + s.be, s.bE, ar.x, lo, hi, nb);
+      for (int32_t p = lo; p < hi; ++p)
+        f(make_key((uint32_t)ar.y, (uint32_t)(p == lo ? nb : P.bOut.arec[p].y), 0u, sh));
     } else {
-      const int32_t pb = s.bS + s.be + (int32_t)j;
-      const uint32_t db = (uint32_t)P.bOut.nbr[pb];
-      label_range(P.aOut, s.qa, s.aS + s.ae, s.aE, P.bOut.lab[pb], lo, hi);
-      for (int32_t p = lo; p < hi; ++p) f(make_key((uint32_t)P.aOut.nbr[p], db, 0u, sh));
+      const int2 br = P.bOut.arec[s.bS + s.be + (int32_t)j];
+      label_range(P.aOut, s.qa, s.aS + s.ae, s.aE, br.x, lo, hi, nb);
+      for (int32_t p = lo; p < hi; ++p)
+        f(make_key((uint32_t)(p == lo ? nb : P.aOut.arec[p].y), (uint32_t)br.y, 0u, sh));
     }
   }
 }
@@ -289,13 +323,15 @@ __device__ __forceinline__ Bwd bwd_info(const Problem &P, uint32_t key) {
   s.g = key_f(key);
   s.vb = key_qb(key, P.shiftB);
   s.va = key_qa(key, P.shiftB);
-  s.aS = P.aIn.off[s.va];
-  s.aE = P.aIn.off[s.va + 1];
-  s.ae = P.aIn.neps[s.va];
-  s.bS = P.bIn.off[s.vb];
-  s.bE = P.bIn.off[s.vb + 1];
-  s.be = P.bIn.neps[s.vb];
-  s.epsV = P.aOut.neps[s.va] > 0 ? 1u : 0u;
+  const int4 ra = P.aIn.srec[s.va];
+  const int4 rb = P.bIn.srec[s.vb];
+  s.aS = ra.x;
+  s.ae = ra.y;
+  s.aE = ra.z;
+  s.bS = rb.x;
+  s.be = rb.y;
+  s.bE = rb.z;
+  s.epsV = (ra.w & (int32_t)FLAG_EPS_OUT) ? 1u : 0u;
   s.eA = (s.g == 0) ? (uint32_t)s.ae : 0u;          // A-epsilon moves land on f = 0
   s.eB = (s.g == s.epsV) ? (uint32_t)s.be : 0u;     // B-epsilon moves land on f = epsOutA
   s.nA = (uint32_t)(s.aE - s.aS - s.ae);
@@ -311,61 +347,63 @@ template <class F>
 __device__ __forceinline__ void bwd_unit(const Problem &P, const Bwd &s, uint32_t u, F &&f) {
   const uint32_t sh = P.shiftB;
   if (u < s.eA) {
-    f(make_key((uint32_t)P.aIn.nbr[s.aS + (int32_t)u], s.vb, 0u, sh));
+    f(make_key((uint32_t)(P.aIn.arec[s.aS + (int32_t)u].y & NBR_MASK), s.vb, 0u, sh));
   } else if (u < s.eA + s.eB) {
-    const uint32_t ub = (uint32_t)P.bIn.nbr[s.bS + (int32_t)(u - s.eA)];
+    const uint32_t ub = (uint32_t)P.bIn.arec[s.bS + (int32_t)(u - s.eA)].y;
     f(make_key(s.va, ub, 0u, sh));
     if (s.epsV) f(make_key(s.va, ub, 1u, sh));
   } else {
     const uint32_t j = u - s.eA - s.eB;
     int32_t lo, hi;
+    int32_t nb;
     if (s.nA <= s.nB) {
-      const int32_t pa = s.aS + s.ae + (int32_t)j;
-      const uint32_t ua = (uint32_t)P.aIn.nbr[pa];
-      const bool fa = P.aOut.neps[ua] > 0;
-      label_range(P.bIn, s.vb, s.bS + s.be, s.bE, P.aIn.lab[pa], lo, hi);
+      const int2 ar = P.aIn.arec[s.aS + s.ae + (int32_t)j];
+      const uint32_t ua = (uint32_t)(ar.y & NBR_MASK);
+      const bool fa = ar.y < 0;
+      label_range(P.bIn, s.vb, s.bS + s.be, s.bE, ar.x, lo, hi, nb);
       for (int32_t p = lo; p < hi; ++p) {
-        const uint32_t ub = (uint32_t)P.bIn.nbr[p];
+        const uint32_t ub = (uint32_t)(p == lo ? nb : P.bIn.arec[p].y);
         f(make_key(ua, ub, 0u, sh));
         if (fa) f(make_key(ua, ub, 1u, sh));
       }
     } else {
-      const int32_t pb = s.bS + s.be + (int32_t)j;
-      const uint32_t ub = (uint32_t)P.bIn.nbr[pb];
-      label_range(P.aIn, s.va, s.aS + s.ae, s.aE, P.bIn.lab[pb], lo, hi);
+      const int2 br = P.bIn.arec[s.bS + s.be + (int32_t)j];
+      const uint32_t ub = (uint32_t)br.y;
+      label_range(P.aIn, s.va, s.aS + s.ae, s.aE, br.x, lo, hi, nb);
       for (int32_t p = lo; p < hi; ++p) {
-        const uint32_t ua = (uint32_t)P.aIn.nbr[p];
+        // the neighbour keeps A's epsilon-output flag in bit 31
+        const int32_t y = p == lo ? nb : P.aIn.arec[p].y;
+        const uint32_t ua = (uint32_t)(y & NBR_MASK);
         f(make_key(ua, ub, 0u, sh));
-        if (P.aOut.neps[ua] > 0) f(make_key(ua, ub, 1u, sh));
+        if (y < 0) f(make_key(ua, ub, 1u, sh));
       }
     }
   }
 }
 
+// Direction traits: move structure, unit count and unit expansion.
 template <bool FWD>
-__device__ __forceinline__ uint32_t units_of(const Problem &P, uint32_t key) {
-  if (FWD) return fwd_units(fwd_info(P, key));
-  return bwd_units(bwd_info(P, key));
-}
-
-// A key reached for the first time: forward = newly accessible; backward =
-// accessible and newly co-accessible.
-template <bool FWD>
-__device__ __forceinline__ bool first_visit(const Problem &P, uint32_t k) {
-  if (FWD) return claim(P.vis, k);
-  return test_bit(P.vis, k) && claim(P.coacc, k);
-}
-
-// A newly claimed key either becomes this thread's next key (depth-first
-// continuation, only for light keys) or is appended to the next frontier.
-template <bool FWD>
-__device__ __forceinline__ void offer(const Problem &P, bool fresh, uint32_t v, uint32_t &cont,
-                                      int depth, const Pusher &pu) {
-  bool take = false;
-  if (fresh && cont == NO_KEY && depth < P.chain_max) take = units_of<FWD>(P, v) <= LIGHT_SEARCH;
-  if (take) cont = v;
-  wave_push(fresh && !take, v, pu);
-}
+struct Dir;
+template <>
+struct Dir<true> {
+  typedef Fwd Info;
+  static __device__ __forceinline__ Fwd info(const Problem &P, uint32_t k) { return fwd_info(P, k); }
+  static __device__ __forceinline__ uint32_t units(const Fwd &s) { return fwd_units(s); }
+  template <class F>
+  static __device__ __forceinline__ void unit(const Problem &P, const Fwd &s, uint32_t u, F &&f) {
+    fwd_unit(P, s, u, f);
+  }
+};
+template <>
+struct Dir<false> {
+  typedef Bwd Info;
+  static __device__ __forceinline__ Bwd info(const Problem &P, uint32_t k) { return bwd_info(P, k); }
+  static __device__ __forceinline__ uint32_t units(const Bwd &s) { return bwd_units(s); }
+  template <class F>
+  static __device__ __forceinline__ void unit(const Problem &P, const Bwd &s, uint32_t u, F &&f) {
+    bwd_unit(P, s, u, f);
+  }
+};
 
 // Per-thread search counters, summed per wavefront at kernel end.
 struct Tally {
@@ -382,139 +420,137 @@ __device__ __forceinline__ void flush_tally(Tally &t, Scalars *sc) {
   }
 }
 
-// Visit one move target (forward) or predecessor (backward) v.
-template <bool FWD>
-__device__ __forceinline__ void visit(const Problem &P, uint32_t v, uint32_t &cont, int depth,
-                                      const Pusher &pu, const Pusher &acc, Tally &t) {
-  const bool fresh = first_visit<FWD>(P, v);
-  if (FWD) {
-    ++t.gen;
-    note_accessible(P, fresh, v, acc, t.nacc);
+// Where the next generation's work goes.
+struct NextGen {
+  GenSlot *slot;
+  uint32_t qbase, hbase;
+};
+
+// List a heavy key for the next generation: one packed atomic gives its
+// position and the offset of its first unit, consistently.
+__device__ __forceinline__ void list_heavy(const SearchArgs &S, const NextGen &nx, uint32_t v,
+                                           uint32_t units) {
+  const ull old = atomicAdd(&nx.slot->hpack, ((ull)units << 32) | 1ull);
+  const ull pos = (ull)nx.hbase + (old & 0xffffffffull);
+  if (pos < S.cap && (old >> 32) + units < (1ull << 32)) {
+    S.heavy[pos] = v;
+    S.hoff[pos] = (uint32_t)(old >> 32);
+  } else {
+    atomicOr(&S.sc->overflow, 2u);
   }
-  offer<FWD>(P, fresh, v, cont, depth, pu);
 }
 
-// Expand `key` and then, depth-first, the light keys it discovers, until a
-// key discovers nothing new or the depth budget is spent.
+// A key reached for the first time (`fresh`).  Forward: it is counted, and if
+// it accepts it is marked co-accessible and listed as a seed of the backward
+// search.  Then: heavy keys go to the next generation's heavy list; a light
+// key becomes this thread's next key (depth-first continuation) if it has none
+// yet and the depth budget allows, else it joins the next frontier.  The
+// continuation's move structure is kept in `ci`.
 template <bool FWD>
-__device__ void run_chain(const Problem &P, uint32_t key, int depth, const Pusher &pu,
-                          const Pusher &acc, Tally &t) {
-  while (key != NO_KEY) {
-    uint32_t cont = NO_KEY;
-    auto f = [&](uint32_t v) { visit<FWD>(P, v, cont, depth, pu, acc, t); };
-    if (FWD) {
-      const Fwd s = fwd_info(P, key);
-      const uint32_t n = fwd_units(s);
-      for (uint32_t u = 0; u < n; ++u) fwd_unit(P, s, u, f);
-    } else {
-      const Bwd s = bwd_info(P, key);
-      const uint32_t n = bwd_units(s);
-      for (uint32_t u = 0; u < n; ++u) bwd_unit(P, s, u, f);
+__device__ __forceinline__ void place(const Problem &P, const SearchArgs &S, const NextGen &nx,
+                                      bool fresh, uint32_t v, const typename Dir<FWD>::Info &vi,
+                                      uint32_t &cont, typename Dir<FWD>::Info &ci, int depth,
+                                      Tally &t) {
+  bool push = false, seed = false;
+  if (fresh) {
+    const uint32_t u = Dir<FWD>::units(vi);
+    if constexpr (FWD) {
+      ++t.nacc;
+      seed = vi.accept != 0;
+      if (seed) atomicOr(P.coacc + (v >> 5), 1u << (v & 31u));
     }
-    key = cont;
+    if (u > LIGHT_SEARCH) {
+      list_heavy(S, nx, v, u);
+    } else if (cont == NO_KEY && depth < P.chain_max) {
+      cont = v;
+      ci = vi;
+    } else {
+      push = true;
+    }
+  }
+  if (FWD) wave_push(seed, v, Pusher{S.acc, S.cap, &S.sc->tail2, S.sc});
+  wave_push(push, v, Pusher{S.Q + nx.qbase, S.cap - nx.qbase, &nx.slot->qcount, S.sc});
+}
+
+// Visit a move target (forward) or a predecessor (backward, where only
+// accessible keys are claimed).  The key's state records are loaded before
+// the claim is resolved, so both memory round trips overlap.
+template <bool FWD>
+__device__ __forceinline__ void visit(const Problem &P, const SearchArgs &S, const NextGen &nx,
+                                      uint32_t v, uint32_t &cont, typename Dir<FWD>::Info &ci,
+                                      int depth, Tally &t) {
+  const typename Dir<FWD>::Info vi = Dir<FWD>::info(P, v);
+  bool fresh;
+  if (FWD) {
+    fresh = claim(P.vis, v);
+    ++t.gen;
+  } else {
+    fresh = test_bit(P.vis, v) && claim(P.coacc, v);
+  }
+  place<FWD>(P, S, nx, fresh, v, vi, cont, ci, depth, t);
+}
+
+// Expand a light key, then, depth-first, the light keys it reaches first.
+template <bool FWD>
+__device__ void run_chain(const Problem &P, const SearchArgs &S, const NextGen &nx,
+                          typename Dir<FWD>::Info info, int depth, Tally &t) {
+  for (;;) {
+    uint32_t cont = NO_KEY;
+    typename Dir<FWD>::Info ci = info;
+    const uint32_t n = Dir<FWD>::units(info);
+    for (uint32_t u = 0; u < n; ++u)
+      Dir<FWD>::unit(P, info, u, [&](uint32_t v) { visit<FWD>(P, S, nx, v, cont, ci, depth, t); });
+    if (cont == NO_KEY) break;
+    info = ci;
     ++depth;
   }
 }
 
-// Generation step 1: every frontier key Q[qlo, qhi).  Light keys are expanded
-// by their thread (with continuation); heavy keys are listed with the prefix
-// of their unit counts (one packed 64-bit atomic per wavefront keeps list
-// positions and unit offsets consistent) for step 2.
+// Generation g (one kernel): one thread per unit of the generation's heavy
+// keys, then one thread per light frontier key.  New work goes to the slot of
+// generation g + 1.
 template <bool FWD>
-__global__ __launch_bounds__(NT) void k_gen_expand(Problem P, Pusher pu, Pusher acc,
-                                                   uint32_t *heavy, uint32_t *hoff, int g) {
-  Scalars *sc = pu.sc;
+__global__ __launch_bounds__(NT) void k_gen(Problem P, SearchArgs S, int g) {
+  Scalars *sc = S.sc;
   if (sc->overflow) return;
-  const GenDesc d = sc->D[g & 1];
+  const GenSlot cur = sc->G[g % 3];
+  const uint32_t hcount = (uint32_t)(cur.hpack & 0xffffffffull);
+  const ull U = cur.hpack >> 32;
+  NextGen nx;
+  nx.slot = &sc->G[(g + 1) % 3];
+  nx.qbase = cur.qbase + cur.qcount;
+  nx.hbase = cur.hbase + hcount;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    nx.slot->qbase = nx.qbase;  // read by generation g + 1 only
+    nx.slot->hbase = nx.hbase;
+    GenSlot *done = &sc->G[(g + 2) % 3];  // generation g - 1: free
+    done->qcount = 0;
+    done->hpack = 0;
+    if (U + cur.qcount) sc->gens = (uint32_t)g + 1;
+  }
+  const uint32_t *hk = S.heavy + cur.hbase;
+  const uint32_t *ho = S.hoff + cur.hbase;
+  const ull n = U + cur.qcount;
   Tally t;
-  for (ull i0 = (ull)d.qlo + (ull)blockIdx.x * NT; i0 < d.qhi; i0 += (ull)gridDim.x * NT) {
-    const ull i = i0 + threadIdx.x;
-    const bool valid = i < d.qhi;
-    const uint32_t key = valid ? pu.Q[i] : 0u;
-    const uint32_t units = valid ? units_of<FWD>(P, key) : 0u;
-    const bool hv = valid && units > LIGHT_SEARCH;
-    const unsigned long long m = __ballot(hv);
-    if (m) {
-      const ull mine = hv ? (ull)units : 0ull;
-      const ull incl = wave_incl_scan(mine);
-      const ull tot = __shfl(incl, WAVE - 1, WAVE);
-      const int leader = __ffsll(m) - 1;
-      ull old = 0;
-      if ((int)__lane_id() == leader) old = atomicAdd(&sc->hpack, (tot << 32) | (ull)__popcll(m));
-      old = __shfl(old, leader, WAVE);
-      if (hv) {
-        const ull pos = (ull)d.hlo + (old & 0xffffffffull) + (ull)__popcll(m & __lanemask_lt());
-        const ull off = (old >> 32) + incl - mine;
-        if (pos < pu.cap && (old >> 32) + tot < (1ull << 32)) {
-          heavy[pos] = key;
-          hoff[pos] = (uint32_t)off;
-        } else {
-          atomicOr(&sc->overflow, 2u);
-        }
+  for (ull i = (ull)blockIdx.x * NT + threadIdx.x; i < n; i += (ull)gridDim.x * NT) {
+    if (i < U) {
+      uint32_t a = 0, b = hcount - 1;  // largest a with ho[a] <= i
+      while (a < b) {
+        const uint32_t mid = (a + b + 1) >> 1;
+        if (ho[mid] <= i) a = mid; else b = mid - 1;
       }
+      const typename Dir<FWD>::Info ki = Dir<FWD>::info(P, hk[a]);
+      uint32_t cont = NO_KEY;
+      typename Dir<FWD>::Info ci = ki;
+      Dir<FWD>::unit(P, ki, (uint32_t)(i - ho[a]),
+                     [&](uint32_t v) { visit<FWD>(P, S, nx, v, cont, ci, 0, t); });
+      if (cont != NO_KEY) run_chain<FWD>(P, S, nx, ci, 1, t);
+    } else {
+      const uint32_t key = S.Q[cur.qbase + (uint32_t)(i - U)];
+      run_chain<FWD>(P, S, nx, Dir<FWD>::info(P, key), 0, t);
     }
-    if (valid && !hv) run_chain<FWD>(P, key, 0, pu, acc, t);
   }
   if (FWD) flush_tally(t, sc);
-}
-
-// Generation step 2: one thread per unit of this generation's heavy keys.
-template <bool FWD>
-__global__ __launch_bounds__(NT) void k_gen_units(Problem P, Pusher pu, Pusher acc,
-                                                  const uint32_t *__restrict__ heavy,
-                                                  const uint32_t *__restrict__ hoff, int g) {
-  Scalars *sc = pu.sc;
-  if (sc->overflow) return;  // the heavy list may be incomplete
-  const GenDesc d = sc->D[g & 1];
-  const ull hp = sc->hpack;
-  const ull U = hp >> 32;
-  const uint32_t n = (uint32_t)(hp & 0xffffffffull);
-  const uint32_t *hk = heavy + d.hlo;
-  const uint32_t *ho = hoff + d.hlo;
-  Tally t;
-  for (ull u = (ull)blockIdx.x * NT + threadIdx.x; u < U; u += (ull)gridDim.x * NT) {
-    uint32_t a = 0, b = n - 1;  // largest i with ho[i] <= u
-    while (a < b) {
-      const uint32_t mid = (a + b + 1) >> 1;
-      if (ho[mid] <= u) a = mid; else b = mid - 1;
-    }
-    const uint32_t key = hk[a];
-    const uint32_t local = (uint32_t)(u - ho[a]);
-    uint32_t cont = NO_KEY;
-    auto f = [&](uint32_t v) { visit<FWD>(P, v, cont, 0, pu, acc, t); };
-    if (FWD) fwd_unit(P, fwd_info(P, key), local, f);
-    else bwd_unit(P, bwd_info(P, key), local, f);
-    if (cont != NO_KEY) run_chain<FWD>(P, cont, 1, pu, acc, t);
-  }
-  if (FWD) flush_tally(t, sc);
-}
-
-// Generation step 3: the keys appended during this generation form the next
-// frontier.
-__global__ void k_gen_advance(Scalars *sc, int g, uint32_t cap) {
-  if (threadIdx.x != 0 || blockIdx.x != 0) return;
-  const GenDesc d = sc->D[g & 1];
-  GenDesc nd;
-  nd.qlo = d.qhi;
-  nd.qhi = sc->tail < cap ? sc->tail : cap;
-  nd.hlo = d.hlo + (uint32_t)(sc->hpack & 0xffffffffull);
-  nd.pad = 0;
-  sc->D[(g + 1) & 1] = nd;
-  sc->hpack = 0;
-  if (d.qlo < d.qhi) sc->gens = (uint32_t)g + 1;
-}
-
-__global__ void k_gen_init(Scalars *sc, uint32_t cap) {
-  if (threadIdx.x != 0 || blockIdx.x != 0) return;
-  GenDesc d;
-  d.qlo = 0;
-  d.qhi = sc->tail < cap ? sc->tail : cap;
-  d.hlo = 0;
-  d.pad = 0;
-  sc->D[0] = d;
-  sc->D[1] = d;
-  sc->hpack = 0;
-  sc->gens = 0;
 }
 
 __global__ __launch_bounds__(NT) void k_collect(const uint8_t *__restrict__ flags, int V,
@@ -533,26 +569,48 @@ __global__ __launch_bounds__(NT) void k_collect(const uint8_t *__restrict__ flag
   }
 }
 
-// Start keys (sa, sb, 0) for every pair of start states (Algorithm 1).
-__global__ __launch_bounds__(NT) void k_seed(Problem P, const int32_t *__restrict__ la,
-                                             const uint32_t *__restrict__ na_p,
-                                             const int32_t *__restrict__ lb,
-                                             const uint32_t *__restrict__ nb_p, Pusher pu,
-                                             Pusher acc) {
+// Start keys (sa, sb, 0) for every pair of start states (Algorithm 1) form
+// generation 0 of the forward search.
+__global__ __launch_bounds__(NT) void k_seed_forward(Problem P, SearchArgs S,
+                                                     const int32_t *__restrict__ la,
+                                                     const uint32_t *__restrict__ na_p,
+                                                     const int32_t *__restrict__ lb,
+                                                     const uint32_t *__restrict__ nb_p) {
   const ull na = *na_p, nb = *nb_p, n = na * nb;
+  const NextGen nx{&S.sc->G[0], 0u, 0u};
   Tally t;
   for (ull i0 = (ull)blockIdx.x * NT; i0 < n; i0 += (ull)gridDim.x * NT) {
     const ull i = i0 + threadIdx.x;
+    uint32_t cont = NO_KEY, k = 0;
     bool fresh = false;
-    uint32_t k = 0;
+    Fwd ci;
     if (i < n) {
       k = make_key((uint32_t)la[i / nb], (uint32_t)lb[i % nb], 0u, P.shiftB);
       fresh = claim(P.vis, k);
+      ci = fwd_info(P, k);
     }
-    note_accessible(P, fresh, k, acc, t.nacc);
-    wave_push(fresh, k, pu);
+    // depth = chain_max: every light start key joins the frontier
+    place<true>(P, S, nx, fresh, k, ci, cont, ci, P.chain_max, t);
   }
-  flush_tally(t, pu.sc);
+  flush_tally(t, S.sc);
+}
+
+// The accepting keys listed by the forward search (already co-accessible)
+// form generation 0 of the backward search.
+__global__ __launch_bounds__(NT) void k_seed_backward(Problem P, SearchArgs S,
+                                                      const uint32_t *__restrict__ list) {
+  const uint32_t n = S.sc->tail2;
+  const NextGen nx{&S.sc->G[0], 0u, 0u};
+  Tally t;
+  for (ull i0 = (ull)blockIdx.x * NT; i0 < n; i0 += (ull)gridDim.x * NT) {
+    const ull i = i0 + threadIdx.x;
+    uint32_t cont = NO_KEY;
+    const bool valid = i < n;
+    const uint32_t k = valid ? list[i] : 0u;
+    Bwd ci;
+    if (valid) ci = bwd_info(P, k);
+    place<false>(P, S, nx, valid, k, ci, cont, ci, P.chain_max, t);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -593,33 +651,32 @@ template <class Visit>
 __device__ __forceinline__ void enum_light(const Problem &P, const Fwd &s, Visit &&vis) {
   const uint32_t sh = P.shiftB;
   for (int32_t p = s.aS; p < s.aS + (int32_t)s.eA; ++p) {
-    int32_t ea = P.aOut.perm[p];
-    vis(make_key((uint32_t)P.aOut.nbr[p], s.qb, 0u, sh), P.A.il[ea], 0, P.A.w[ea], ea, -1);
+    const int32_t ea = P.aOut.perm[p];
+    vis(make_key((uint32_t)P.aOut.arec[p].y, s.qb, 0u, sh), P.A.il[ea], 0, P.A.w[ea], ea, -1);
   }
-  const uint32_t f2 = s.ae > 0 ? 1u : 0u;
   for (int32_t p = s.bS; p < s.bS + s.be; ++p) {
-    int32_t eb = P.bOut.perm[p];
-    vis(make_key(s.qa, (uint32_t)P.bOut.nbr[p], f2, sh), 0, P.B.ol[eb], P.B.w[eb], -1, eb);
+    const int32_t eb = P.bOut.perm[p];
+    vis(make_key(s.qa, (uint32_t)P.bOut.arec[p].y, s.epsA, sh), 0, P.B.ol[eb], P.B.w[eb], -1, eb);
   }
   if (!s.mU) return;
   if (s.nA <= s.nB) {
     int32_t p = s.aS + s.ae, bl = s.bS + s.be;
     while (p < s.aE) {
-      const int32_t lab = P.aOut.lab[p];
+      const int32_t lab = P.aOut.arec[p].x;
       int32_t pend = p + 1;
-      while (pend < s.aE && P.aOut.lab[pend] == lab) ++pend;
+      while (pend < s.aE && P.aOut.arec[pend].x == lab) ++pend;
       int32_t lo, hi;
       label_range(P.bOut, s.qb, bl, s.bE, lab, lo, hi);
       if (lo < hi) bl = hi;
       for (int32_t pa = p; pa < pend && lo < hi; ++pa) {
         const int32_t ea = P.aOut.perm[pa];
-        const uint32_t da = (uint32_t)P.aOut.nbr[pa];
+        const uint32_t da = (uint32_t)P.aOut.arec[pa].y;
         const int32_t ia = P.A.il[ea];
         const float wa = P.A.w[ea];
         for (int32_t pb = lo; pb < hi; ++pb) {
           const int32_t eb = P.bOut.perm[pb];
-          vis(make_key(da, (uint32_t)P.bOut.nbr[pb], 0u, sh), ia, P.B.ol[eb], wa + P.B.w[eb], ea,
-              eb);
+          vis(make_key(da, (uint32_t)P.bOut.arec[pb].y, 0u, sh), ia, P.B.ol[eb], wa + P.B.w[eb],
+              ea, eb);
         }
       }
       p = pend;
@@ -627,21 +684,21 @@ __device__ __forceinline__ void enum_light(const Problem &P, const Fwd &s, Visit
   } else {
     int32_t p = s.bS + s.be, al = s.aS + s.ae;
     while (p < s.bE) {
-      const int32_t lab = P.bOut.lab[p];
+      const int32_t lab = P.bOut.arec[p].x;
       int32_t pend = p + 1;
-      while (pend < s.bE && P.bOut.lab[pend] == lab) ++pend;
+      while (pend < s.bE && P.bOut.arec[pend].x == lab) ++pend;
       int32_t lo, hi;
       label_range(P.aOut, s.qa, al, s.aE, lab, lo, hi);
       if (lo < hi) al = hi;
       for (int32_t pa = lo; pa < hi; ++pa) {
         const int32_t ea = P.aOut.perm[pa];
-        const uint32_t da = (uint32_t)P.aOut.nbr[pa];
+        const uint32_t da = (uint32_t)P.aOut.arec[pa].y;
         const int32_t ia = P.A.il[ea];
         const float wa = P.A.w[ea];
         for (int32_t pb = p; pb < pend; ++pb) {
           const int32_t eb = P.bOut.perm[pb];
-          vis(make_key(da, (uint32_t)P.bOut.nbr[pb], 0u, sh), ia, P.B.ol[eb], wa + P.B.w[eb], ea,
-              eb);
+          vis(make_key(da, (uint32_t)P.bOut.arec[pb].y, 0u, sh), ia, P.B.ol[eb], wa + P.B.w[eb],
+              ea, eb);
         }
       }
       p = pend;
@@ -678,7 +735,7 @@ __device__ uint32_t heavy_state(const Problem &P, uint32_t id, uint32_t key, uin
     uint32_t d = 0;
     if (i < s.eA) {
       ea = P.aOut.perm[s.aS + (int32_t)i];
-      d = make_key((uint32_t)P.aOut.nbr[s.aS + (int32_t)i], s.qb, 0u, sh);
+      d = make_key((uint32_t)P.aOut.arec[s.aS + (int32_t)i].y, s.qb, 0u, sh);
       keep = test_bit(P.coacc, d);
     }
     uint32_t tot;
@@ -686,7 +743,6 @@ __device__ uint32_t heavy_state(const Problem &P, uint32_t id, uint32_t key, uin
     if (FILL && keep) put_arc(O, P, pos0 + run + ex, id, d, P.A.il[ea], 0, P.A.w[ea], ea, -1);
     run += tot;
   }
-  const uint32_t f2 = s.ae > 0 ? 1u : 0u;
   for (uint32_t c = 0; c < (uint32_t)s.be; c += NT) {
     const uint32_t i = c + t;
     bool keep = false;
@@ -694,7 +750,7 @@ __device__ uint32_t heavy_state(const Problem &P, uint32_t id, uint32_t key, uin
     uint32_t d = 0;
     if (i < (uint32_t)s.be) {
       eb = P.bOut.perm[s.bS + (int32_t)i];
-      d = make_key(s.qa, (uint32_t)P.bOut.nbr[s.bS + (int32_t)i], f2, sh);
+      d = make_key(s.qa, (uint32_t)P.bOut.arec[s.bS + (int32_t)i].y, s.epsA, sh);
       keep = test_bit(P.coacc, d);
     }
     uint32_t tot;
@@ -711,11 +767,12 @@ __device__ uint32_t heavy_state(const Problem &P, uint32_t id, uint32_t key, uin
       uint32_t kept = 0, da = 0;
       if (i < s.nA) {
         const int32_t pa = s.aS + s.ae + (int32_t)i;
+        const int2 ar = P.aOut.arec[pa];
         ea = P.aOut.perm[pa];
-        da = (uint32_t)P.aOut.nbr[pa];
-        label_range(P.bOut, s.qb, s.bS + s.be, s.bE, P.aOut.lab[pa], lo, hi);
+        da = (uint32_t)ar.y;
+        label_range(P.bOut, s.qb, s.bS + s.be, s.bE, ar.x, lo, hi);
         for (int32_t pb = lo; pb < hi; ++pb)
-          kept += test_bit(P.coacc, make_key(da, (uint32_t)P.bOut.nbr[pb], 0u, sh));
+          kept += test_bit(P.coacc, make_key(da, (uint32_t)P.bOut.arec[pb].y, 0u, sh));
       }
       uint32_t tot;
       uint32_t ex = block_excl_scan<uint32_t>(kept, s_w, tot);
@@ -725,8 +782,9 @@ __device__ uint32_t heavy_state(const Problem &P, uint32_t id, uint32_t key, uin
         uint32_t pos = pos0 + run + ex;
         for (int32_t pb = lo; pb < hi; ++pb) {
           const int32_t eb = P.bOut.perm[pb];
-          const uint32_t d = make_key(da, (uint32_t)P.bOut.nbr[pb], 0u, sh);
-          if (test_bit(P.coacc, d)) put_arc(O, P, pos++, id, d, ia, P.B.ol[eb], wa + P.B.w[eb], ea, eb);
+          const uint32_t d = make_key(da, (uint32_t)P.bOut.arec[pb].y, 0u, sh);
+          if (test_bit(P.coacc, d))
+            put_arc(O, P, pos++, id, d, ia, P.B.ol[eb], wa + P.B.w[eb], ea, eb);
         }
       }
       run += tot;
@@ -823,8 +881,6 @@ __global__ __launch_bounds__(NT) void k_state_flags(Problem P, const uint32_t *_
   }
 }
 
-int bitlen(unsigned long long x) { return x ? 64 - __builtin_clzll(x) : 0; }
-
 }  // namespace
 
 // ---------------------------------------------------------------------------
@@ -838,8 +894,8 @@ hipError_t launch_validate(const DevGraph &g, int side, uint32_t *err, uint32_t 
 }
 
 hipError_t build_view(const DevGraph &g, int side, bool by_dst, int lab_bits, int32_t lab_max,
-                      int32_t *perm, int32_t *lab, int32_t *nbr, int32_t *neps, int32_t *lut,
-                      int32_t *off_out, unsigned long long *k0, int32_t *v0,
+                      int4 *srec, int2 *arec, int32_t *perm, int4 *lut, int32_t *off_tmp,
+                      const int4 *eps_rec, unsigned long long *k0, int32_t *v0,
                       unsigned long long *k1, int32_t *v1, void *sort_temp, uint32_t *eps_states,
                       hipStream_t s) {
   const size_t E = (size_t)g.E;
@@ -849,60 +905,53 @@ hipError_t build_view(const DevGraph &g, int side, bool by_dst, int lab_bits, in
     if ((e = hipGetLastError()) != hipSuccess) return e;
     int bits = bitlen((unsigned long long)(g.V > 0 ? g.V - 1 : 0)) + lab_bits;
     if ((e = radix_sort(k0, v0, k1, v1, E, bits, sort_temp, s)) != hipSuccess) return e;
-    k_split<<<grid_for(E), NT, 0, s>>>(g, by_dst ? 1 : 0, k0, v0, (long long)E, lab_bits, perm,
-                                       lab, nbr);
+    k_split<<<grid_for(E), NT, 0, s>>>(g, by_dst ? 1 : 0, k0, v0, (long long)E, lab_bits,
+                                       eps_rec, perm, arec);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   const int32_t *off = g.off;
   if (by_dst) {
     k_group_offsets<<<grid_for((size_t)g.V + 1), NT, 0, s>>>(k0, (long long)E, g.V, lab_bits,
-                                                            off_out);
+                                                            off_tmp);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    off = off_out;
+    off = off_tmp;
   }
   if (g.V) {
-    k_neps<<<grid_for((size_t)g.V), NT, 0, s>>>(off, lab, g.V, neps, eps_states);
+    const int eps_mode = side == 1 ? 0 : (by_dst ? 2 : 1);
+    k_state_rec<<<grid_for((size_t)g.V), NT, 0, s>>>(off, arec, g.V, g.accept, eps_mode, eps_rec,
+                                                     srec, eps_states);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (lut) {
-      const size_t n = (size_t)g.V * (size_t)(lab_max + 2);
-      k_build_lut<<<grid_for(n, 8192), NT, 0, s>>>(off, lab, g.V, lab_max + 2, lut);
+      const size_t n = (size_t)g.V * (size_t)(lab_max + 1);
+      k_build_lut<<<grid_for(n, 8192), NT, 0, s>>>(srec, arec, g.V, lab_max + 1, lut);
       if ((e = hipGetLastError()) != hipSuccess) return e;
     }
   }
   return hipSuccess;
 }
 
-hipError_t launch_seed_lists(const Problem &P, int32_t *la, uint32_t *na, int32_t *lb,
-                             uint32_t *nb, uint32_t *queue, uint32_t *acc_list, uint32_t cap,
-                             Scalars *sc, hipStream_t s) {
+hipError_t launch_seed_forward(const Problem &P, const SearchArgs &S, int32_t *la, uint32_t *na,
+                               int32_t *lb, uint32_t *nb, hipStream_t s) {
   k_collect<<<grid_for((size_t)P.A.V, 1024), NT, 0, s>>>(P.A.start, P.A.V, la, na);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   k_collect<<<grid_for((size_t)P.B.V, 1024), NT, 0, s>>>(P.B.start, P.B.V, lb, nb);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  const Pusher pu{queue, cap, &sc->tail, sc}, acc{acc_list, cap, &sc->tail2, sc};
-  k_seed<<<64, NT, 0, s>>>(P, la, na, lb, nb, pu, acc);
+  k_seed_forward<<<64, NT, 0, s>>>(P, S, la, na, lb, nb);
   return hipGetLastError();
 }
 
-hipError_t launch_gen_init(Scalars *sc, uint32_t cap, hipStream_t s) {
-  k_gen_init<<<1, 64, 0, s>>>(sc, cap);
+hipError_t launch_seed_backward(const Problem &P, const SearchArgs &S, const uint32_t *acc_list,
+                                hipStream_t s) {
+  k_seed_backward<<<1024, NT, 0, s>>>(P, S, acc_list);
   return hipGetLastError();
 }
 
-hipError_t launch_generation(const Problem &P, bool forward, uint32_t *Q, uint32_t *acc_list,
-                             uint32_t cap, uint32_t *heavy, uint32_t *hoff, int g, Scalars *sc,
+hipError_t launch_generation(const Problem &P, const SearchArgs &S, bool forward, int g,
                              hipStream_t s) {
-  const Pusher pu{Q, cap, &sc->tail, sc}, acc{acc_list, cap, &sc->tail2, sc};
   constexpr unsigned GRID = 1024;
-  if (forward) {
-    k_gen_expand<true><<<GRID, NT, 0, s>>>(P, pu, acc, heavy, hoff, g);
-    k_gen_units<true><<<GRID, NT, 0, s>>>(P, pu, acc, heavy, hoff, g);
-  } else {
-    k_gen_expand<false><<<GRID, NT, 0, s>>>(P, pu, acc, heavy, hoff, g);
-    k_gen_units<false><<<GRID, NT, 0, s>>>(P, pu, acc, heavy, hoff, g);
-  }
-  k_gen_advance<<<1, 64, 0, s>>>(sc, g, cap);
+  if (forward) k_gen<true><<<GRID, NT, 0, s>>>(P, S, g);
+  else k_gen<false><<<GRID, NT, 0, s>>>(P, S, g);
   return hipGetLastError();
 }
 
