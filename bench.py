@@ -88,6 +88,13 @@ def main():
         comp.fill(C)
         return C
 
+    # one untimed composition that also counts the moves out of accessible
+    # keys (an extra pass), for the algorithmic-bytes model
+    comp.set_option(gpu.FST_OPT_COUNT_MOVES, 1)
+    step()
+    torch.cuda.synchronize()
+    st_moves = comp.stats()
+    comp.set_option(gpu.FST_OPT_COUNT_MOVES, 0)
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -106,6 +113,7 @@ def main():
     ms = ev0.elapsed_time(ev1) / args.steps
     ms_wall = 1e3 * wall / args.steps
     st = comp.stats()
+    st["generated"] = st_moves["generated"]
     E_C = st["num_arcs"]
     phases = {k: v / args.steps for k, v in phases.items()}
 

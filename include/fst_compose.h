@@ -106,7 +106,8 @@ typedef struct {
   int64_t key_space;     /* number of key slots of the visited bitmaps       */
   int64_t accessible;    /* keys reached from the start keys                 */
   int64_t coaccessible;  /* accessible keys that reach an accepting key = V_C */
-  int64_t generated;     /* moves generated by the forward search            */
+  int64_t generated;     /* moves out of accessible keys; -1 unless
+                            FST_OPT_COUNT_MOVES was set                      */
   int64_t fwd_levels;    /* frontier generations of the forward search       */
   int64_t bwd_levels;    /* frontier generations of the backward search      */
   int64_t heavy_states;  /* states of C handled one workgroup per state      */
@@ -131,12 +132,15 @@ FST_API void fst_ctx_destroy(fst_ctx *ctx);
  * bucket tables when they fit in 256 MiB; 0 = binary search only) and
  * FST_OPT_CHAIN_DEPTH (default 64: how many newly found keys one search
  * thread may expand depth-first before handing keys to the next frontier;
- * 0 = plain frontier-by-frontier search). */
+ * 0 = plain frontier-by-frontier search).  FST_OPT_COUNT_MOVES = 1 makes
+ * each run also count the moves out of all accessible keys (an extra pass,
+ * reported in fst_stats.generated). */
 enum fst_option {
   FST_OPT_MAX_WORKSPACE = 1,
   FST_OPT_TIMING = 2,
   FST_OPT_LABEL_BUCKETS = 3,
-  FST_OPT_CHAIN_DEPTH = 4
+  FST_OPT_CHAIN_DEPTH = 4,
+  FST_OPT_COUNT_MOVES = 5
 };
 FST_API int fst_ctx_set_option(fst_ctx *ctx, int option, int64_t value);
 

@@ -35,6 +35,7 @@ struct fst_ctx {
   size_t ws_total = 0;
   bool timing = false;
   bool buckets = true;
+  bool count_moves = false;
   int chain_depth = CHAIN_MAX;
   bool have_times = false;
   bool timed_run = false;
@@ -300,8 +301,8 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   HIP_TRY(hipMemsetAsync(d_sc->G, 0, sizeof(d_sc->G), s));
   HIP_TRY(launch_seed_forward(P, S, la, cnts, lb, cnts + 1, s));
   FST_TRY(search(c, S, true, &c->stats.fwd_levels, s));
-  c->stats.accessible = c->h_sc->naccessible;
-  c->stats.generated = (int64_t)c->h_sc->generated;
+  HIP_TRY(launch_popcount(P.vis, nwords, &d_sc->naccessible, s));
+  if (c->count_moves) HIP_TRY(launch_count_moves(P, nwords, &d_sc->generated, s));
 
   // ---- backward search, seeded by the accepting keys listed in bq ----
   mark(c, 2, s);
@@ -335,6 +336,8 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   c->nstates = nstates;
   c->narcs = (uint32_t)narcs;
   c->nheavy = c->h_sc->heavy;
+  c->stats.accessible = (int64_t)c->h_sc->naccessible;
+  c->stats.generated = c->count_moves ? (int64_t)c->h_sc->generated : -1;
   c->stats.coaccessible = nstates;
   c->stats.heavy_states = c->nheavy;
   c->stats.num_states = nstates;
@@ -412,6 +415,9 @@ int fst_ctx_set_option(fst_ctx *c, int option, int64_t value) {
       return FST_OK;
     case FST_OPT_LABEL_BUCKETS:
       c->buckets = value != 0;
+      return FST_OK;
+    case FST_OPT_COUNT_MOVES:
+      c->count_moves = value != 0;
       return FST_OK;
     case FST_OPT_CHAIN_DEPTH:
       if (value < 0 || value > (1 << 20)) return FST_ERR_INVALID_ARG;

@@ -86,9 +86,20 @@ __global__ __launch_bounds__(NT) void k_validate(DevGraph g, int side, uint32_t 
       if (lab > 0 && (uint32_t)lab > mx) mx = (uint32_t)lab;
     }
   }
+  // one atomic per workgroup: same-address atomics serialize
+  __shared__ uint32_t s_bits[NWAVES], s_mx[NWAVES];
   bits = wave_or(bits);
   mx = wave_max(mx);
   if (__lane_id() == 0) {
+    s_bits[threadIdx.x / WAVE] = bits;
+    s_mx[threadIdx.x / WAVE] = mx;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < NWAVES; ++w) {
+      bits |= s_bits[w];
+      mx = s_mx[w] > mx ? s_mx[w] : mx;
+    }
     if (bits) atomicOr(err, bits);
     if (mx) atomicMax(maxlab, mx);
   }
@@ -150,6 +161,8 @@ __global__ __launch_bounds__(NT) void k_state_rec(const int32_t *__restrict__ of
                                                   int eps_mode, const int4 *__restrict__ eps_rec,
                                                   int4 *__restrict__ srec,
                                                   uint32_t *eps_states) {
+  __shared__ uint32_t s_w[NWAVES];
+  uint32_t neps_states = 0;
   for (long long v = (long long)blockIdx.x * NT + threadIdx.x; v < V;
        v += (long long)gridDim.x * NT) {
     const int32_t s0 = off[v], s1 = off[v + 1];
@@ -158,11 +171,11 @@ __global__ __launch_bounds__(NT) void k_state_rec(const int32_t *__restrict__ of
     if ((eps_mode == 1 && n > 0) || (eps_mode == 2 && eps_rec[v].y > 0))
       flags |= (int32_t)FLAG_EPS_OUT;
     srec[v] = make_int4(s0, n, s1, flags);
-    if (eps_states) {
-      unsigned long long m = __ballot(n > 0);
-      if (m && __lane_id() == (unsigned)(__ffsll(m) - 1))
-        atomicAdd(eps_states, (uint32_t)__popcll(m));
-    }
+    neps_states += n > 0 ? 1u : 0u;
+  }
+  if (eps_states) {
+    const uint32_t tot = block_sum(neps_states, s_w);
+    if (threadIdx.x == 0 && tot) atomicAdd(eps_states, tot);
   }
 }
 
@@ -213,6 +226,12 @@ __device__ __forceinline__ void label_range(const View &v, uint32_t q, int32_t l
                                             int32_t lab, int32_t &r0, int32_t &r1) {
   int32_t nb0;
   label_range(v, q, lo, hi, lab, r0, r1, nb0);
+}
+
+// Claim a key that few threads are expected to reach at once.
+__device__ __forceinline__ bool claim_cold(uint32_t *bm, uint32_t k) {
+  const uint32_t bit = 1u << (k & 31u);
+  return (atomicOr(bm + (k >> 5), bit) & bit) == 0;
 }
 
 // Claim key k in bitmap bm; true for exactly one caller per key.  The plain
@@ -284,30 +303,58 @@ __device__ __forceinline__ Fwd fwd_info(const Problem &P, uint32_t key) {
 // bucket of its label).
 __device__ __forceinline__ uint32_t fwd_units(const Fwd &s) { return s.eA + (uint32_t)s.be + s.mU; }
 
-// Calls f(dst key) for the moves of unit `u` of key s.
-template <class F>
-__device__ __forceinline__ void fwd_unit(const Problem &P, const Fwd &s, uint32_t u, F &&f) {
-  const uint32_t sh = P.shiftB;
-  if (u < s.eA) {
-    f(make_key((uint32_t)P.aOut.arec[s.aS + (int32_t)u].y, s.qb, 0u, sh));
-  } else if (u < s.eA + (uint32_t)s.be) {
-    f(make_key(s.qa, (uint32_t)P.bOut.arec[s.bS + (int32_t)(u - s.eA)].y, s.epsA, sh));
-  } else {
+// The keys a work unit reaches: for p in [lo, hi), with nb_p the neighbour
+// field of arcs[p] (nb_lo given), the key (A state, B state, f) where the
+// side named by varyA takes nb_p and the other side is fixed.  In the
+// backward direction a key is also visited with f = 1 when `dual` holds or,
+// with dual_from_nb, when bit 31 of nb_p (epsOutA of an A-side neighbour)
+// is set.  One shape for all move kinds keeps a single visit site per kernel.
+struct UnitRange {
+  const int2 *arcs;
+  int32_t lo, hi, nb0;
+  uint32_t fa, fb, f;
+  bool varyA, dual, dual_from_nb;
+  bool hot;  // the keys may be reached by many threads at once
+};
+
+__device__ __forceinline__ UnitRange fwd_range(const Problem &P, const Fwd &s, uint32_t u) {
+  UnitRange r;
+  r.f = 0;
+  r.fa = r.fb = 0;
+  r.dual = r.dual_from_nb = false;
+  r.hot = true;
+  if (u < s.eA) {  // A-epsilon move
+    r.arcs = P.aOut.arec;
+    r.lo = s.aS + (int32_t)u;
+    r.varyA = true;
+    r.fb = s.qb;
+  } else if (u < s.eA + (uint32_t)s.be) {  // B-epsilon move
+    r.arcs = P.bOut.arec;
+    r.lo = s.bS + (int32_t)(u - s.eA);
+    r.varyA = false;
+    r.fa = s.qa;
+    r.f = s.epsA;
+  } else {  // matching moves of one arc of the smaller side
+    r.hot = false;
     const uint32_t j = u - s.eA - (uint32_t)s.be;
-    int32_t lo, hi;
-    int32_t nb;
     if (s.nA <= s.nB) {
       const int2 ar = P.aOut.arec[s.aS + s.ae + (int32_t)j];
-      label_range(P.bOut, s.qb, s.bS + s.be, s.bE, ar.x, lo, hi, nb);
-      for (int32_t p = lo; p < hi; ++p)
-        f(make_key((uint32_t)ar.y, (uint32_t)(p == lo ? nb : P.bOut.arec[p].y), 0u, sh));
+      label_range(P.bOut, s.qb, s.bS + s.be, s.bE, ar.x, r.lo, r.hi, r.nb0);
+      r.arcs = P.bOut.arec;
+      r.varyA = false;
+      r.fa = (uint32_t)ar.y;
     } else {
       const int2 br = P.bOut.arec[s.bS + s.be + (int32_t)j];
-      label_range(P.aOut, s.qa, s.aS + s.ae, s.aE, br.x, lo, hi, nb);
-      for (int32_t p = lo; p < hi; ++p)
-        f(make_key((uint32_t)(p == lo ? nb : P.aOut.arec[p].y), (uint32_t)br.y, 0u, sh));
+      label_range(P.aOut, s.qa, s.aS + s.ae, s.aE, br.x, r.lo, r.hi, r.nb0);
+      r.arcs = P.aOut.arec;
+      r.varyA = true;
+      r.fb = (uint32_t)br.y;
     }
+    return r;
   }
+  r.hi = r.lo + 1;
+  r.nb0 = r.arcs[r.lo].y;
+  return r;
 }
 
 // Backward structure of key v = (va, vb, g): the predecessors are the exact
@@ -342,42 +389,61 @@ __device__ __forceinline__ Bwd bwd_info(const Problem &P, uint32_t key) {
 
 __device__ __forceinline__ uint32_t bwd_units(const Bwd &s) { return s.eA + s.eB + s.mU; }
 
-// Calls f(predecessor key) for the predecessors of unit `u` of key s.
-template <class F>
-__device__ __forceinline__ void bwd_unit(const Problem &P, const Bwd &s, uint32_t u, F &&f) {
-  const uint32_t sh = P.shiftB;
-  if (u < s.eA) {
-    f(make_key((uint32_t)(P.aIn.arec[s.aS + (int32_t)u].y & NBR_MASK), s.vb, 0u, sh));
-  } else if (u < s.eA + s.eB) {
-    const uint32_t ub = (uint32_t)P.bIn.arec[s.bS + (int32_t)(u - s.eA)].y;
-    f(make_key(s.va, ub, 0u, sh));
-    if (s.epsV) f(make_key(s.va, ub, 1u, sh));
-  } else {
+__device__ __forceinline__ UnitRange bwd_range(const Problem &P, const Bwd &s, uint32_t u) {
+  UnitRange r;
+  r.f = 0;
+  r.fa = r.fb = 0;
+  r.dual = r.dual_from_nb = false;
+  r.hot = true;
+  if (u < s.eA) {  // predecessor by an A-epsilon move: (ua, vb, 0)
+    r.arcs = P.aIn.arec;
+    r.lo = s.aS + (int32_t)u;
+    r.varyA = true;
+    r.fb = s.vb;
+  } else if (u < s.eA + s.eB) {  // by a B-epsilon move: (va, ub, 0 and 1)
+    r.arcs = P.bIn.arec;
+    r.lo = s.bS + (int32_t)(u - s.eA);
+    r.varyA = false;
+    r.fa = s.va;
+    r.dual = s.epsV != 0;
+  } else {  // by matching moves: (ua, ub, 0 and, if epsOutA(ua), 1)
+    r.hot = false;
     const uint32_t j = u - s.eA - s.eB;
-    int32_t lo, hi;
-    int32_t nb;
     if (s.nA <= s.nB) {
       const int2 ar = P.aIn.arec[s.aS + s.ae + (int32_t)j];
-      const uint32_t ua = (uint32_t)(ar.y & NBR_MASK);
-      const bool fa = ar.y < 0;
-      label_range(P.bIn, s.vb, s.bS + s.be, s.bE, ar.x, lo, hi, nb);
-      for (int32_t p = lo; p < hi; ++p) {
-        const uint32_t ub = (uint32_t)(p == lo ? nb : P.bIn.arec[p].y);
-        f(make_key(ua, ub, 0u, sh));
-        if (fa) f(make_key(ua, ub, 1u, sh));
-      }
+      label_range(P.bIn, s.vb, s.bS + s.be, s.bE, ar.x, r.lo, r.hi, r.nb0);
+      r.arcs = P.bIn.arec;
+      r.varyA = false;
+      r.fa = (uint32_t)(ar.y & NBR_MASK);
+      r.dual = ar.y < 0;
     } else {
       const int2 br = P.bIn.arec[s.bS + s.be + (int32_t)j];
-      const uint32_t ub = (uint32_t)br.y;
-      label_range(P.aIn, s.va, s.aS + s.ae, s.aE, br.x, lo, hi, nb);
-      for (int32_t p = lo; p < hi; ++p) {
-        // the neighbour keeps A's epsilon-output flag in bit 31
-        const int32_t y = p == lo ? nb : P.aIn.arec[p].y;
-        const uint32_t ua = (uint32_t)(y & NBR_MASK);
-        f(make_key(ua, ub, 0u, sh));
-        if (y < 0) f(make_key(ua, ub, 1u, sh));
-      }
+      label_range(P.aIn, s.va, s.aS + s.ae, s.aE, br.x, r.lo, r.hi, r.nb0);
+      r.arcs = P.aIn.arec;
+      r.varyA = true;
+      r.fb = (uint32_t)br.y;
+      r.dual_from_nb = true;
     }
+    return r;
+  }
+  r.hi = r.lo + 1;
+  r.nb0 = r.arcs[r.lo].y;
+  return r;
+}
+
+// Calls f(key) for every key of unit `u` of a key with structure s.
+template <bool FWD, class Info, class F>
+__device__ __forceinline__ void for_unit(const Problem &P, const Info &s, uint32_t u, F &&f) {
+  UnitRange r;
+  if constexpr (FWD) r = fwd_range(P, s, u);
+  else r = bwd_range(P, s, u);
+  const uint32_t sh = P.shiftB;
+  for (int32_t p = r.lo; p < r.hi; ++p) {
+    const int32_t y = p == r.lo ? r.nb0 : r.arcs[p].y;
+    const uint32_t nb = (uint32_t)(y & NBR_MASK);
+    const uint32_t qa = r.varyA ? nb : r.fa, qb = r.varyA ? r.fb : nb;
+    const uint32_t nf = (r.dual || (r.dual_from_nb && y < 0)) ? 2u : 1u;
+    for (uint32_t ff = 0; ff < nf; ++ff) f(make_key(qa, qb, FWD ? r.f : ff, sh), r.hot);
   }
 }
 
@@ -391,7 +457,7 @@ struct Dir<true> {
   static __device__ __forceinline__ uint32_t units(const Fwd &s) { return fwd_units(s); }
   template <class F>
   static __device__ __forceinline__ void unit(const Problem &P, const Fwd &s, uint32_t u, F &&f) {
-    fwd_unit(P, s, u, f);
+    for_unit<true>(P, s, u, f);
   }
 };
 template <>
@@ -401,24 +467,9 @@ struct Dir<false> {
   static __device__ __forceinline__ uint32_t units(const Bwd &s) { return bwd_units(s); }
   template <class F>
   static __device__ __forceinline__ void unit(const Problem &P, const Bwd &s, uint32_t u, F &&f) {
-    bwd_unit(P, s, u, f);
+    for_unit<false>(P, s, u, f);
   }
 };
-
-// Per-thread search counters, summed per wavefront at kernel end.
-struct Tally {
-  ull gen = 0;        // moves generated (forward)
-  uint32_t nacc = 0;  // keys reached for the first time (forward)
-};
-
-__device__ __forceinline__ void flush_tally(Tally &t, Scalars *sc) {
-  const ull gen = wave_sum(t.gen);
-  const uint32_t nacc = wave_sum(t.nacc);
-  if (__lane_id() == 0) {
-    if (gen) atomicAdd(&sc->generated, gen);
-    if (nacc) atomicAdd(&sc->naccessible, nacc);
-  }
-}
 
 // Where the next generation's work goes.
 struct NextGen {
@@ -449,13 +500,11 @@ __device__ __forceinline__ void list_heavy(const SearchArgs &S, const NextGen &n
 template <bool FWD>
 __device__ __forceinline__ void place(const Problem &P, const SearchArgs &S, const NextGen &nx,
                                       bool fresh, uint32_t v, const typename Dir<FWD>::Info &vi,
-                                      uint32_t &cont, typename Dir<FWD>::Info &ci, int depth,
-                                      Tally &t) {
+                                      uint32_t &cont, typename Dir<FWD>::Info &ci, int depth) {
   bool push = false, seed = false;
   if (fresh) {
     const uint32_t u = Dir<FWD>::units(vi);
     if constexpr (FWD) {
-      ++t.nacc;
       seed = vi.accept != 0;
       if (seed) atomicOr(P.coacc + (v >> 5), 1u << (v & 31u));
     }
@@ -477,40 +526,27 @@ __device__ __forceinline__ void place(const Problem &P, const SearchArgs &S, con
 // the claim is resolved, so both memory round trips overlap.
 template <bool FWD>
 __device__ __forceinline__ void visit(const Problem &P, const SearchArgs &S, const NextGen &nx,
-                                      uint32_t v, uint32_t &cont, typename Dir<FWD>::Info &ci,
-                                      int depth, Tally &t) {
+                                      uint32_t v, bool hot, uint32_t &cont,
+                                      typename Dir<FWD>::Info &ci, int depth) {
   const typename Dir<FWD>::Info vi = Dir<FWD>::info(P, v);
   bool fresh;
   if (FWD) {
-    fresh = claim(P.vis, v);
-    ++t.gen;
+    fresh = hot ? claim(P.vis, v) : claim_cold(P.vis, v);
   } else {
-    fresh = test_bit(P.vis, v) && claim(P.coacc, v);
+    const uint32_t bit = 1u << (v & 31u), w = v >> 5;
+    const uint32_t wv = P.vis[w], wc = P.coacc[w];  // one round trip for both
+    fresh = (wv & bit) && !(wc & bit) && (atomicOr(P.coacc + w, bit) & bit) == 0;
   }
-  place<FWD>(P, S, nx, fresh, v, vi, cont, ci, depth, t);
-}
-
-// Expand a light key, then, depth-first, the light keys it reaches first.
-template <bool FWD>
-__device__ void run_chain(const Problem &P, const SearchArgs &S, const NextGen &nx,
-                          typename Dir<FWD>::Info info, int depth, Tally &t) {
-  for (;;) {
-    uint32_t cont = NO_KEY;
-    typename Dir<FWD>::Info ci = info;
-    const uint32_t n = Dir<FWD>::units(info);
-    for (uint32_t u = 0; u < n; ++u)
-      Dir<FWD>::unit(P, info, u, [&](uint32_t v) { visit<FWD>(P, S, nx, v, cont, ci, depth, t); });
-    if (cont == NO_KEY) break;
-    info = ci;
-    ++depth;
-  }
+  place<FWD>(P, S, nx, fresh, v, vi, cont, ci, depth);
 }
 
 // Generation g (one kernel): one thread per unit of the generation's heavy
-// keys, then one thread per light frontier key.  New work goes to the slot of
-// generation g + 1.
+// keys, then one thread per light frontier key.  A thread expands its units,
+// then, depth-first, the light keys it reached first (one loop, so the visit
+// code exists once).  New work goes to the slot of generation g + 1.
 template <bool FWD>
 __global__ __launch_bounds__(NT) void k_gen(Problem P, SearchArgs S, int g) {
+  typedef typename Dir<FWD>::Info Info;
   Scalars *sc = S.sc;
   if (sc->overflow) return;
   const GenSlot cur = sc->G[g % 3];
@@ -531,26 +567,35 @@ __global__ __launch_bounds__(NT) void k_gen(Problem P, SearchArgs S, int g) {
   const uint32_t *hk = S.heavy + cur.hbase;
   const uint32_t *ho = S.hoff + cur.hbase;
   const ull n = U + cur.qcount;
-  Tally t;
   for (ull i = (ull)blockIdx.x * NT + threadIdx.x; i < n; i += (ull)gridDim.x * NT) {
+    uint32_t key, u0 = 0, u1 = 0;
+    bool one_unit = false;
     if (i < U) {
       uint32_t a = 0, b = hcount - 1;  // largest a with ho[a] <= i
       while (a < b) {
         const uint32_t mid = (a + b + 1) >> 1;
         if (ho[mid] <= i) a = mid; else b = mid - 1;
       }
-      const typename Dir<FWD>::Info ki = Dir<FWD>::info(P, hk[a]);
-      uint32_t cont = NO_KEY;
-      typename Dir<FWD>::Info ci = ki;
-      Dir<FWD>::unit(P, ki, (uint32_t)(i - ho[a]),
-                     [&](uint32_t v) { visit<FWD>(P, S, nx, v, cont, ci, 0, t); });
-      if (cont != NO_KEY) run_chain<FWD>(P, S, nx, ci, 1, t);
+      key = hk[a];
+      u0 = (uint32_t)(i - ho[a]);
+      one_unit = true;
     } else {
-      const uint32_t key = S.Q[cur.qbase + (uint32_t)(i - U)];
-      run_chain<FWD>(P, S, nx, Dir<FWD>::info(P, key), 0, t);
+      key = S.Q[cur.qbase + (uint32_t)(i - U)];
+    }
+    Info info = Dir<FWD>::info(P, key);
+    u1 = one_unit ? u0 + 1 : Dir<FWD>::units(info);
+    for (int depth = 0;; ++depth) {
+      uint32_t cont = NO_KEY;
+      Info ci = info;
+      for (uint32_t u = u0; u < u1; ++u)
+        Dir<FWD>::unit(P, info, u,
+                       [&](uint32_t v, bool hot) { visit<FWD>(P, S, nx, v, hot, cont, ci, depth); });
+      if (cont == NO_KEY) break;
+      info = ci;
+      u0 = 0;
+      u1 = Dir<FWD>::units(ci);
     }
   }
-  if (FWD) flush_tally(t, sc);
 }
 
 __global__ __launch_bounds__(NT) void k_collect(const uint8_t *__restrict__ flags, int V,
@@ -578,7 +623,6 @@ __global__ __launch_bounds__(NT) void k_seed_forward(Problem P, SearchArgs S,
                                                      const uint32_t *__restrict__ nb_p) {
   const ull na = *na_p, nb = *nb_p, n = na * nb;
   const NextGen nx{&S.sc->G[0], 0u, 0u};
-  Tally t;
   for (ull i0 = (ull)blockIdx.x * NT; i0 < n; i0 += (ull)gridDim.x * NT) {
     const ull i = i0 + threadIdx.x;
     uint32_t cont = NO_KEY, k = 0;
@@ -590,9 +634,8 @@ __global__ __launch_bounds__(NT) void k_seed_forward(Problem P, SearchArgs S,
       ci = fwd_info(P, k);
     }
     // depth = chain_max: every light start key joins the frontier
-    place<true>(P, S, nx, fresh, k, ci, cont, ci, P.chain_max, t);
+    place<true>(P, S, nx, fresh, k, ci, cont, ci, P.chain_max);
   }
-  flush_tally(t, S.sc);
 }
 
 // The accepting keys listed by the forward search (already co-accessible)
@@ -601,7 +644,6 @@ __global__ __launch_bounds__(NT) void k_seed_backward(Problem P, SearchArgs S,
                                                       const uint32_t *__restrict__ list) {
   const uint32_t n = S.sc->tail2;
   const NextGen nx{&S.sc->G[0], 0u, 0u};
-  Tally t;
   for (ull i0 = (ull)blockIdx.x * NT; i0 < n; i0 += (ull)gridDim.x * NT) {
     const ull i = i0 + threadIdx.x;
     uint32_t cont = NO_KEY;
@@ -609,8 +651,42 @@ __global__ __launch_bounds__(NT) void k_seed_backward(Problem P, SearchArgs S,
     const uint32_t k = valid ? list[i] : 0u;
     Bwd ci;
     if (valid) ci = bwd_info(P, k);
-    place<false>(P, S, nx, valid, k, ci, cont, ci, P.chain_max, t);
+    place<false>(P, S, nx, valid, k, ci, cont, ci, P.chain_max);
   }
+}
+
+// Number of moves out of the accessible keys (a statistic, on request):
+// one per epsilon unit, the bucket size for each matching unit.
+__global__ __launch_bounds__(NT) void k_count_moves(Problem P, ull nwords,
+                                                    unsigned long long *__restrict__ out) {
+  __shared__ ull s_w[NWAVES];
+  ull c = 0;
+  for (ull w = (ull)blockIdx.x * NT + threadIdx.x; w < nwords; w += (ull)gridDim.x * NT) {
+    uint32_t m = P.vis[w];
+    while (m) {
+      const uint32_t key = (uint32_t)(w * 32u) + (uint32_t)(__ffs(m) - 1);
+      m &= m - 1u;
+      const Fwd s = fwd_info(P, key);
+      c += s.eA + (uint32_t)s.be;
+      for (uint32_t u = s.eA + (uint32_t)s.be; u < fwd_units(s); ++u) {
+        const UnitRange r = fwd_range(P, s, u);
+        c += (ull)(r.hi - r.lo);
+      }
+    }
+  }
+  const ull tot = block_sum(c, s_w);
+  if (threadIdx.x == 0 && tot) atomicAdd(out, tot);
+}
+
+// Number of set bits of a bitmap (one atomic per workgroup).
+__global__ __launch_bounds__(NT) void k_popcount(const uint32_t *__restrict__ bm, ull nwords,
+                                                 unsigned long long *__restrict__ out) {
+  __shared__ ull s_w[NWAVES];
+  ull c = 0;
+  for (ull w = (ull)blockIdx.x * NT + threadIdx.x; w < nwords; w += (ull)gridDim.x * NT)
+    c += (ull)__popc(bm[w]);
+  const ull tot = block_sum(c, s_w);
+  if (threadIdx.x == 0 && tot) atomicAdd(out, tot);
 }
 
 // ---------------------------------------------------------------------------
@@ -889,7 +965,7 @@ __global__ __launch_bounds__(NT) void k_state_flags(Problem P, const uint32_t *_
 hipError_t launch_validate(const DevGraph &g, int side, uint32_t *err, uint32_t *maxlab,
                            hipStream_t s) {
   size_t n = (size_t)(g.V + 1 > g.E ? g.V + 1 : g.E);
-  k_validate<<<grid_for(n, 1024), NT, 0, s>>>(g, side, err, maxlab);
+  k_validate<<<grid_for(n, 64), NT, 0, s>>>(g, side, err, maxlab);
   return hipGetLastError();
 }
 
@@ -918,8 +994,8 @@ hipError_t build_view(const DevGraph &g, int side, bool by_dst, int lab_bits, in
   }
   if (g.V) {
     const int eps_mode = side == 1 ? 0 : (by_dst ? 2 : 1);
-    k_state_rec<<<grid_for((size_t)g.V), NT, 0, s>>>(off, arec, g.V, g.accept, eps_mode, eps_rec,
-                                                     srec, eps_states);
+    k_state_rec<<<grid_for((size_t)g.V, 256), NT, 0, s>>>(off, arec, g.V, g.accept, eps_mode,
+                                                          eps_rec, srec, eps_states);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (lut) {
       const size_t n = (size_t)g.V * (size_t)(lab_max + 1);
@@ -952,6 +1028,20 @@ hipError_t launch_generation(const Problem &P, const SearchArgs &S, bool forward
   constexpr unsigned GRID = 1024;
   if (forward) k_gen<true><<<GRID, NT, 0, s>>>(P, S, g);
   else k_gen<false><<<GRID, NT, 0, s>>>(P, S, g);
+  return hipGetLastError();
+}
+
+hipError_t launch_count_moves(const Problem &P, size_t nwords, unsigned long long *out,
+                              hipStream_t s) {
+  if (!nwords) return hipSuccess;
+  k_count_moves<<<grid_for(nwords, 1024), NT, 0, s>>>(P, nwords, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_popcount(const uint32_t *bm, size_t nwords, unsigned long long *out,
+                           hipStream_t s) {
+  if (!nwords) return hipSuccess;
+  k_popcount<<<grid_for(nwords, 256), NT, 0, s>>>(bm, nwords, out);
   return hipGetLastError();
 }
 

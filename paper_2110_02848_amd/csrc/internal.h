@@ -95,11 +95,12 @@ struct Scalars {
   uint32_t maxLabA, maxLabB;    // max matched label (A olabel, B ilabel)
   uint32_t nEpsStatesA;         // states of A with an epsilon-output arc
   uint32_t tail2;               // accepting keys found by the forward search
-  uint32_t naccessible;         // keys reached by the forward search
+  uint32_t pad0;
   uint32_t heavy;               // heavy states of C
   uint32_t overflow;            // a capacity was exceeded
   uint32_t gens;                // search generations that had work
-  unsigned long long generated; // moves generated by the forward search
+  unsigned long long generated; // moves out of accessible keys (on request)
+  unsigned long long naccessible; // keys reached by the forward search
   unsigned long long total;     // scan totals
   GenSlot G[3];
 };
@@ -174,6 +175,19 @@ __device__ __forceinline__ T wave_sum(T x) {
   return x;
 }
 
+// Sum over the NT threads of a workgroup, valid in thread 0.  Every thread
+// must call it (it contains a barrier).
+template <typename T>
+__device__ __forceinline__ T block_sum(T x, T *s_w) {
+  x = wave_sum(x);
+  if (__lane_id() == 0) s_w[threadIdx.x / WAVE] = x;
+  __syncthreads();
+  T t = 0;
+  if (threadIdx.x == 0)
+    for (int w = 0; w < NWAVES; ++w) t += s_w[w];
+  return t;
+}
+
 // First index in [lo, hi) whose value is >= x (values sorted ascending).
 __device__ __forceinline__ int32_t lower_bound_i32(const int32_t *a, int32_t lo, int32_t hi,
                                                    int32_t x) {
@@ -242,6 +256,12 @@ hipError_t launch_seed_backward(const Problem &P, const SearchArgs &S, const uin
 // Generation g of the forward (or backward) search: one kernel.
 hipError_t launch_generation(const Problem &P, const SearchArgs &S, bool forward, int g,
                              hipStream_t s);
+// *out += number of moves out of the keys set in P.vis (a statistic).
+hipError_t launch_count_moves(const Problem &P, size_t nwords, unsigned long long *out,
+                              hipStream_t s);
+// *out += number of set bits of bm[0, nwords).
+hipError_t launch_popcount(const uint32_t *bm, size_t nwords, unsigned long long *out,
+                           hipStream_t s);
 hipError_t launch_popc_words(const uint32_t *bm, uint32_t *cnt, size_t nwords, hipStream_t s);
 hipError_t launch_key_of_id(const uint32_t *bm, const uint32_t *wbase, size_t nwords,
                             uint32_t *key_of, hipStream_t s);

@@ -28,6 +28,7 @@ FST_OPT_MAX_WORKSPACE = 1
 FST_OPT_TIMING = 2
 FST_OPT_LABEL_BUCKETS = 3
 FST_OPT_CHAIN_DEPTH = 4
+FST_OPT_COUNT_MOVES = 5
 
 PHASES = ("preprocess", "forward", "backward", "count", "fill")
 
