@@ -4,7 +4,7 @@ One step = one full composition (search, trim, numbering, arc count and the
 fill of the output CSR) of the emissions(T=500, C=64) o lexicon(W=10000,
 L=3..10) workload, inputs resident in HBM.  Prints one JSON line.
 
-    python bench.py [--steps K] [--warmup W] [--config 5] [--seed 0]
+    python bench.py [--steps K] [--warmup W] [--workload lexicon-T500-W10000] [--seed 0]
 """
 from __future__ import annotations
 
@@ -23,9 +23,9 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, GB/s
 
 
 def algorithmic_bytes(A, B, st, provenance=False):
-    """Bytes the method itself must move (inputs read once, one dedupe probe
-    per generated move, each accessible key written and read once in the
-    frontier, the output CSR written once)."""
+    """Bytes the method itself must move per composition (inputs read once,
+    one dedupe probe per examined move, each kept key written to and read
+    from a frontier once, the output CSR written once)."""
     EA, EB = len(A["src"]), len(B["src"])
     VA, VB = A["num_states"], B["num_states"]
     b_in = 16 * (EA + EB) + 4 * (VA + VB + 2) + 2 * (VA + VB)
@@ -37,10 +37,38 @@ def algorithmic_bytes(A, B, st, provenance=False):
     return dict(inputs=b_in, search=b_search, output=b_out, total=b_in + b_search + b_out)
 
 
-def fill_bytes(st):
-    """Algorithmic bytes of the fill kernel: the output CSR it writes."""
+def kernel_bytes(st):
+    """Algorithmic bytes per composition of each timed kernel group:
+    forward search: 4 B probe per move out of an accessible key + 16 B per
+    accessible key (frontier write and read); backward search: the same over
+    the predecessor moves and the co-accessible keys; count: 8 B per state of
+    C (its key in, its count out) + 4 B per kept arc (the probe of its
+    target); fill: the output CSR (20 B per arc, 6 B per state + 4 B)."""
     V, E = st["num_states"], st["num_arcs"]
-    return 20 * E + 4 * (V + 1) + 2 * V
+    return {
+        "search_forward": 4 * st["generated"] + 16 * st["accessible"],
+        "search_backward": 4 * st["generated_backward"] + 16 * st["coaccessible"],
+        "count": 8 * V + 4 * E,
+        "fill": 20 * E + 4 * (V + 1) + 2 * V,
+    }
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_emissions_lexicon_T500_W10000.txt")
+
+
+def measured_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` from the committed counter table, or
+    None if there is none for this workload or the kernels changed since."""
+    if workload != "lexicon-T500-W10000":
+        return None
+    from paper_2110_02848_amd import profiling
+    t = profiling.read_traffic(TRAFFIC_FILE)
+    if t is None:
+        return None
+    sha, table = t
+    if sha != profiling.kernel_source_hash() or kernel not in table:
+        return None
+    return table[kernel]
 
 
 def cpu_baseline(A, B, E_C):
@@ -62,25 +90,38 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=5)
+    ap.add_argument("--workload", default="lexicon-T500-W10000")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-mb", type=int, default=0,
+                    help="first copy a buffer of this many MiB device to device "
+                         "(calibrates HBM byte counters under rocprofv3 --pmc)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the composition is a single-GPU kernel "
-              "pipeline (see the sharding notes in DESIGN.md); run with --gpus 1",
+              "pipeline on one device; run with --gpus 1",
               file=sys.stderr)
         sys.exit(2)
 
     import torch
     from paper_2110_02848_amd import gpu, synth
 
-    A, B = synth.config(args.config, args.seed)
+    if args.workload not in synth.WORKLOADS:
+        ap.error(f"--workload must be one of {', '.join(synth.WORKLOADS)}")
+    A, B = synth.workload(args.workload, args.seed)
     dev = "cuda:0"
     dA, dB = gpu.to_device(A, dev), gpu.to_device(B, dev)
     comp = gpu.Composer(0)
     comp.set_option(gpu.FST_OPT_TIMING, 1)
     stream = torch.cuda.current_stream()
+
+    if args.copy_probe_mb > 0:
+        n = args.copy_probe_mb << 20
+        src = torch.ones(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     def step():
         nv, ne = comp.run(dA, dB)
@@ -88,8 +129,8 @@ def main():
         comp.fill(C)
         return C
 
-    # one untimed composition that also counts the moves out of accessible
-    # keys (an extra pass), for the algorithmic-bytes model
+    # one untimed composition that also counts the examined moves (extra
+    # passes) for the algorithmic-bytes model
     comp.set_option(gpu.FST_OPT_COUNT_MOVES, 1)
     step()
     torch.cuda.synchronize()
@@ -99,6 +140,7 @@ def main():
         step()
     torch.cuda.synchronize()
     phases = {k: 0.0 for k in gpu.PHASES}
+    kern = {k: [0.0, 0] for k in gpu.KERNELS}
     t0 = time.perf_counter()
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
@@ -107,6 +149,9 @@ def main():
         step()
         for k, v in comp.phase_times().items():
             phases[k] += v
+        for k, (ms_k, n_k) in comp.kernel_times().items():
+            kern[k][0] += ms_k
+            kern[k][1] += n_k
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -114,13 +159,29 @@ def main():
     ms_wall = 1e3 * wall / args.steps
     st = comp.stats()
     st["generated"] = st_moves["generated"]
+    st["generated_backward"] = st_moves["generated_backward"]
     E_C = st["num_arcs"]
     phases = {k: v / args.steps for k, v in phases.items()}
 
     alg = algorithmic_bytes(A, B, st)
-    fill_ms = phases["fill"]
-    fb = fill_bytes(st)
-    achieved = fb / (fill_ms * 1e-3) / 1e9 if fill_ms > 0 else 0.0
+    kb = kernel_bytes(st)
+    kernels = {}
+    for k, (ms_k, n_k) in kern.items():
+        if n_k == 0 or ms_k <= 0:
+            continue
+        per_launch = kb[k] * args.steps / n_k
+        avg_ms = ms_k / n_k
+        kernels[k] = {"launches_per_step": n_k / args.steps, "ms_per_step": ms_k / args.steps,
+                      "avg_launch_us": 1e3 * avg_ms, "alg_bytes_per_launch": per_launch,
+                      "achieved_GBs": per_launch / (avg_ms * 1e-3) / 1e9}
+    dom = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
+    d = kernels[dom]
+    roofline = {"bound": "hbm", "kernel": dom, "achieved": d["achieved_GBs"],
+                "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": d["achieved_GBs"] / HBM_PEAK_GBS,
+                "traffic": measured_traffic(args.workload, dom),
+                "avg_launch_us": d["avg_launch_us"],
+                "alg_bytes_per_launch": d["alg_bytes_per_launch"]}
     out = {
         "metric": "composed arcs/sec (emissions o lexicon)",
         "value": E_C / (ms_wall * 1e-3),
@@ -134,17 +195,17 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": synth.CONFIG_NAMES[args.config], "seed": args.seed,
+        "config": {"workload": synth.WORKLOAD_TITLES[args.workload], "name": args.workload,
+                   "seed": args.seed,
                    "V_A": A["num_states"], "E_A": len(A["src"]), "V_B": B["num_states"],
                    "E_B": len(B["src"]), "V_C": st["num_states"], "E_C": E_C},
         "ms_per_composition_device": ms,
         "phases_ms": {k: round(v, 4) for k, v in phases.items()},
+        "kernels": kernels,
         "search_stats": st,
         "algorithmic_bytes": alg,
         "hbm_roofline_fraction_whole": (alg["total"] / (HBM_PEAK_GBS * 1e9)) / (ms_wall * 1e-3),
-        "roofline": {"bound": "hbm", "kernel": "fill", "achieved": achieved,
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": None},
+        "roofline": roofline,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(A, B, E_C)

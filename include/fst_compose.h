@@ -23,7 +23,7 @@
  * so each pair of paths of A and B maps to exactly one path of C.)  Start
  * keys are (sa, sb, 0) over start states of A and B.  A key accepts iff both
  * of its states accept.  C keeps only keys reachable from a start key that
- * can reach an accepting key (Section 3.1: the algorithm yields trim graphs).
+ * can reach an accepting key (Section 3.1: the composed graph is trim).
  * Parallel arcs are kept; no weights are summed.
  *
  * Output is canonical and deterministic: states are numbered in ascending
@@ -113,6 +113,9 @@ typedef struct {
   int64_t heavy_states;  /* states of C handled one workgroup per state      */
   int64_t num_states;    /* V_C                                              */
   int64_t num_arcs;      /* E_C                                              */
+  int64_t generated_backward; /* predecessor moves of the co-accessible keys
+                            (each probed once by the backward search); -1
+                            unless FST_OPT_COUNT_MOVES was set               */
 } fst_stats;
 
 typedef struct fst_ctx fst_ctx;
@@ -133,8 +136,9 @@ FST_API void fst_ctx_destroy(fst_ctx *ctx);
  * FST_OPT_CHAIN_DEPTH (default 64: how many newly found keys one search
  * thread may expand depth-first before handing keys to the next frontier;
  * 0 = plain frontier-by-frontier search).  FST_OPT_COUNT_MOVES = 1 makes
- * each run also count the moves out of all accessible keys (an extra pass,
- * reported in fst_stats.generated). */
+ * each run also count the moves out of all accessible keys and the
+ * predecessor moves of all co-accessible keys (extra passes, reported in
+ * fst_stats.generated and fst_stats.generated_backward). */
 enum fst_option {
   FST_OPT_MAX_WORKSPACE = 1,
   FST_OPT_TIMING = 2,
@@ -166,6 +170,24 @@ FST_API int fst_compose_stats(const fst_ctx *ctx, fst_stats *out);
  * search, [3] numbering + arc count, [4] fill.  Writes min(n, 5) values;
  * returns FST_ERR_STATE if timing was off. */
 FST_API int fst_compose_phase_times(const fst_ctx *ctx, float *ms, int n);
+
+/* Kernels timed with FST_OPT_TIMING on: every launch of the forward search
+ * kernel; every launch of the backward search kernel; the arc-count kernels
+ * (states with few moves, then states with many: 2 launches, 1 if C is
+ * empty); the fill kernels (light states, heavy states if any, state flags). */
+enum fst_kernel {
+  FST_KERNEL_SEARCH_FORWARD = 0,
+  FST_KERNEL_SEARCH_BACKWARD = 1,
+  FST_KERNEL_COUNT = 2,
+  FST_KERNEL_FILL = 3
+};
+
+/* With FST_OPT_TIMING on: *ms = summed device time of the launches of
+ * `kernel` in the last run + fill, each bracketed by HIP events on the
+ * caller's stream, and *launches = how many there were.  Returns
+ * FST_ERR_STATE if timing was off or no run + fill was timed,
+ * FST_ERR_INVALID_ARG for an unknown kernel. */
+FST_API int fst_compose_kernel_time(const fst_ctx *ctx, int kernel, float *ms, int64_t *launches);
 
 /* Static string for a status code. */
 FST_API const char *fst_strerror(int code);

@@ -26,6 +26,7 @@ struct DevBuf {
 };
 
 constexpr int NEV = 7;
+constexpr int NKERNELS = 4;  // enum fst_kernel
 
 }  // namespace
 
@@ -47,6 +48,9 @@ struct fst_ctx {
   DevBuf vis, coacc, wbase, fq, bq, heavy, hoff, cnt;
   Scalars *h_sc = nullptr;
   hipEvent_t ev[NEV] = {};
+  hipEvent_t kev[2 * NKERNELS] = {};  // per timed kernel: before, after
+  float kms[NKERNELS] = {};
+  int64_t klaunches[NKERNELS] = {};
 
   bool ready = false;
   Problem P = {};
@@ -166,11 +170,35 @@ int finish_empty(fst_ctx *c, int64_t *V_C, int64_t *E_C) {
 // Generations are queued in batches with no host round trip; after each batch
 // the host checks whether the next generation has any work (generations
 // queued after the search has ended do nothing).
+KernelTimer timer(const fst_ctx *c, int kernel) {
+  KernelTimer t;
+  if (c->timing) {
+    t.ev0 = c->kev[2 * kernel];
+    t.ev1 = c->kev[2 * kernel + 1];
+  }
+  return t;
+}
+
+// Adds the time between a timer's events (both complete) to kernel's total.
+int add_time(fst_ctx *c, int kernel, int64_t launches) {
+  if (!c->timing) return FST_OK;
+  float t = 0.f;
+  HIP_TRY(hipEventElapsedTime(&t, c->kev[2 * kernel], c->kev[2 * kernel + 1]));
+  c->kms[kernel] += t;
+  c->klaunches[kernel] += launches;
+  return FST_OK;
+}
+
 int search(fst_ctx *c, const SearchArgs &S, bool forward, int64_t *levels, hipStream_t s) {
+  const int kernel = forward ? FST_KERNEL_SEARCH_FORWARD : FST_KERNEL_SEARCH_BACKWARD;
+  const KernelTimer t = timer(c, kernel);
   int g = 0, batch = 4;
   for (;;) {
+    t.begin(s);
     for (int b = 0; b < batch; ++b, ++g) HIP_TRY(launch_generation(c->P, S, forward, g, s));
+    t.end(s);
     FST_TRY(readback(c, s));
+    FST_TRY(add_time(c, kernel, batch));
     if (c->h_sc->overflow) return FST_ERR_TOO_LARGE;
     const GenSlot &nx = c->h_sc->G[g % 3];
     if (nx.qcount == 0 && (uint32_t)nx.hpack == 0) break;
@@ -196,6 +224,10 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
 
   FST_TRY(ensure(c, c->scal, sizeof(Scalars)));
   Scalars *d_sc = as<Scalars>(c->scal);
+  for (int k = 0; k < NKERNELS; ++k) {
+    c->kms[k] = 0.f;
+    c->klaunches[k] = 0;
+  }
   mark(c, 0, s);
   HIP_TRY(hipMemsetAsync(d_sc, 0, sizeof(Scalars), s));
   if (VA) HIP_TRY(launch_validate(dA, 0, &d_sc->errA, &d_sc->maxLabA, s));
@@ -302,13 +334,14 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   HIP_TRY(launch_seed_forward(P, S, la, cnts, lb, cnts + 1, s));
   FST_TRY(search(c, S, true, &c->stats.fwd_levels, s));
   HIP_TRY(launch_popcount(P.vis, nwords, &d_sc->naccessible, s));
-  if (c->count_moves) HIP_TRY(launch_count_moves(P, nwords, &d_sc->generated, s));
+  if (c->count_moves) HIP_TRY(launch_count_moves(P, nwords, true, &d_sc->generated, s));
 
   // ---- backward search, seeded by the accepting keys listed in bq ----
   mark(c, 2, s);
   HIP_TRY(hipMemsetAsync(d_sc->G, 0, sizeof(d_sc->G), s));
   HIP_TRY(launch_seed_backward(P, S, bq, s));
   FST_TRY(search(c, S, false, &c->stats.bwd_levels, s));
+  if (c->count_moves) HIP_TRY(launch_count_moves(P, nwords, false, &d_sc->generated_bwd, s));
 
   // ---- numbering and arc counts ----
   mark(c, 3, s);
@@ -325,19 +358,24 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   FST_TRY(ensure(c, c->cnt, ((size_t)nstates + 1) * 4));
   uint32_t *cnt = as<uint32_t>(c->cnt);
   HIP_TRY(hipMemsetAsync(&d_sc->heavy, 0, sizeof(uint32_t), s));
+  const KernelTimer tc = timer(c, FST_KERNEL_COUNT);
+  tc.begin(s);
   HIP_TRY(launch_count(P, key_of, nstates, cnt, heavy, d_sc, s));
   HIP_TRY(launch_count_heavy(P, key_of, heavy, &d_sc->heavy, cnt, s));
+  tc.end(s);
   HIP_TRY(scan_u32(cnt, cnt, nstates, false, &d_sc->total, c->scan_tmp.p, s));
   mark(c, 4, s);
   FST_TRY(readback(c, s));
   const unsigned long long narcs = c->h_sc->total;
   if (narcs > (unsigned long long)INT32_MAX) return FST_ERR_TOO_LARGE;
+  FST_TRY(add_time(c, FST_KERNEL_COUNT, nstates ? 2 : 1));
 
   c->nstates = nstates;
   c->narcs = (uint32_t)narcs;
   c->nheavy = c->h_sc->heavy;
   c->stats.accessible = (int64_t)c->h_sc->naccessible;
   c->stats.generated = c->count_moves ? (int64_t)c->h_sc->generated : -1;
+  c->stats.generated_backward = c->count_moves ? (int64_t)c->h_sc->generated_bwd : -1;
   c->stats.coaccessible = nstates;
   c->stats.heavy_states = c->nheavy;
   c->stats.num_states = nstates;
@@ -380,6 +418,12 @@ int fst_ctx_create(int device, fst_ctx **ctx) {
       return FST_ERR_HIP;
     }
   }
+  for (int i = 0; i < 2 * NKERNELS; ++i) {
+    if (hipEventCreate(&c->kev[i]) != hipSuccess) {
+      fst_ctx_destroy(c);
+      return FST_ERR_HIP;
+    }
+  }
   *ctx = c;
   return FST_OK;
 }
@@ -398,6 +442,8 @@ void fst_ctx_destroy(fst_ctx *c) {
   for (DevBuf *b : bufs) release(*b);
   for (int i = 0; i < NEV; ++i)
     if (c->ev[i]) (void)hipEventDestroy(c->ev[i]);
+  for (int i = 0; i < 2 * NKERNELS; ++i)
+    if (c->kev[i]) (void)hipEventDestroy(c->kev[i]);
   if (c->h_sc) (void)hipHostFree(c->h_sc);
   delete c;
 }
@@ -473,8 +519,14 @@ int fst_compose_fill(fst_ctx *c, const fst_graph_out *C, void *stream) {
   O.arc_a = C->arc_a;
   O.arc_b = C->arc_b;
   mark(c, 5, s);
+  const KernelTimer tf = c->timed_run ? timer(c, FST_KERNEL_FILL) : KernelTimer{};
+  tf.begin(s);
   hipError_t e = launch_fill(c->P, as<uint32_t>(c->fq), c->nstates, as<uint32_t>(c->cnt),
                              as<uint32_t>(c->bq), c->nheavy, c->narcs, O, s);
+  tf.end(s);
+  // light-state fill (if any states), heavy-state fill (if any), flags
+  c->klaunches[FST_KERNEL_FILL] = c->timed_run ? (c->nstates ? 2 : 1) + (c->nheavy ? 1 : 0) : 0;
+  c->kms[FST_KERNEL_FILL] = 0.f;
   mark(c, 6, s);
   if (e != hipSuccess) {
     (void)hipGetLastError();
@@ -503,6 +555,22 @@ int fst_compose_phase_times(const fst_ctx *c, float *ms, int n) {
       return FST_ERR_HIP;
     ms[i] = t;
   }
+  return FST_OK;
+}
+
+int fst_compose_kernel_time(const fst_ctx *c, int kernel, float *ms, int64_t *launches) {
+  if (!c || !ms || !launches || kernel < 0 || kernel >= NKERNELS) return FST_ERR_INVALID_ARG;
+  if (!c->have_times) return FST_ERR_STATE;
+  float t = c->kms[kernel];
+  if (kernel == FST_KERNEL_FILL) {
+    // the fill is asynchronous: its events are read here
+    DeviceGuard g(c->device);
+    if (hipEventSynchronize(c->kev[2 * kernel + 1]) != hipSuccess) return FST_ERR_HIP;
+    if (hipEventElapsedTime(&t, c->kev[2 * kernel], c->kev[2 * kernel + 1]) != hipSuccess)
+      return FST_ERR_HIP;
+  }
+  *ms = t;
+  *launches = c->klaunches[kernel];
   return FST_OK;
 }
 

@@ -655,24 +655,21 @@ __global__ __launch_bounds__(NT) void k_seed_backward(Problem P, SearchArgs S,
   }
 }
 
-// Number of moves out of the accessible keys (a statistic, on request):
-// one per epsilon unit, the bucket size for each matching unit.
+// Number of moves the search examines (a statistic, on request): forward,
+// the moves out of the accessible keys; backward, the predecessor moves of
+// the co-accessible keys.
+template <bool FWD>
 __global__ __launch_bounds__(NT) void k_count_moves(Problem P, ull nwords,
                                                     unsigned long long *__restrict__ out) {
   __shared__ ull s_w[NWAVES];
+  const uint32_t *bm = FWD ? P.vis : P.coacc;
   ull c = 0;
-  for (ull w = (ull)blockIdx.x * NT + threadIdx.x; w < nwords; w += (ull)gridDim.x * NT) {
-    uint32_t m = P.vis[w];
-    while (m) {
-      const uint32_t key = (uint32_t)(w * 32u) + (uint32_t)(__ffs(m) - 1);
-      m &= m - 1u;
-      const Fwd s = fwd_info(P, key);
-      c += s.eA + (uint32_t)s.be;
-      for (uint32_t u = s.eA + (uint32_t)s.be; u < fwd_units(s); ++u) {
-        const UnitRange r = fwd_range(P, s, u);
-        c += (ull)(r.hi - r.lo);
-      }
-    }
+  const ull nkeys = nwords * 32u;
+  for (ull k = (ull)blockIdx.x * NT + threadIdx.x; k < nkeys; k += (ull)gridDim.x * NT) {
+    if (!test_bit(bm, (uint32_t)k)) continue;
+    const typename Dir<FWD>::Info s = Dir<FWD>::info(P, (uint32_t)k);
+    const uint32_t nu = Dir<FWD>::units(s);
+    for (uint32_t u = 0; u < nu; ++u) Dir<FWD>::unit(P, s, u, [&](uint32_t, bool) { ++c; });
   }
   const ull tot = block_sum(c, s_w);
   if (threadIdx.x == 0 && tot) atomicAdd(out, tot);
@@ -1031,10 +1028,11 @@ hipError_t launch_generation(const Problem &P, const SearchArgs &S, bool forward
   return hipGetLastError();
 }
 
-hipError_t launch_count_moves(const Problem &P, size_t nwords, unsigned long long *out,
-                              hipStream_t s) {
+hipError_t launch_count_moves(const Problem &P, size_t nwords, bool forward,
+                              unsigned long long *out, hipStream_t s) {
   if (!nwords) return hipSuccess;
-  k_count_moves<<<grid_for(nwords, 1024), NT, 0, s>>>(P, nwords, out);
+  if (forward) k_count_moves<true><<<grid_for(nwords * 32, 8192), NT, 0, s>>>(P, nwords, out);
+  else k_count_moves<false><<<grid_for(nwords * 32, 8192), NT, 0, s>>>(P, nwords, out);
   return hipGetLastError();
 }
 

@@ -100,6 +100,7 @@ struct Scalars {
   uint32_t overflow;            // a capacity was exceeded
   uint32_t gens;                // search generations that had work
   unsigned long long generated; // moves out of accessible keys (on request)
+  unsigned long long generated_bwd; // predecessor moves of co-accessible keys (on request)
   unsigned long long naccessible; // keys reached by the forward search
   unsigned long long total;     // scan totals
   GenSlot G[3];
@@ -207,6 +208,18 @@ __device__ __forceinline__ int32_t upper_bound_i32(const int32_t *a, int32_t lo,
   return lo;
 }
 
+// Optional pair of HIP events that brackets one kernel launch on its stream
+// (both null: no timing).
+struct KernelTimer {
+  hipEvent_t ev0 = nullptr, ev1 = nullptr;
+  void begin(hipStream_t s) const {
+    if (ev0) (void)hipEventRecord(ev0, s);
+  }
+  void end(hipStream_t s) const {
+    if (ev1) (void)hipEventRecord(ev1, s);
+  }
+};
+
 // ---------------------------------------------------------------------------
 // Host-side launchers (primitives.hip)
 // ---------------------------------------------------------------------------
@@ -256,9 +269,11 @@ hipError_t launch_seed_backward(const Problem &P, const SearchArgs &S, const uin
 // Generation g of the forward (or backward) search: one kernel.
 hipError_t launch_generation(const Problem &P, const SearchArgs &S, bool forward, int g,
                              hipStream_t s);
-// *out += number of moves out of the keys set in P.vis (a statistic).
-hipError_t launch_count_moves(const Problem &P, size_t nwords, unsigned long long *out,
-                              hipStream_t s);
+// *out += number of moves the forward search examines out of the keys set in
+// P.vis, or (backward) the backward search examines into the keys set in
+// P.coacc (a statistic).
+hipError_t launch_count_moves(const Problem &P, size_t nwords, bool forward,
+                              unsigned long long *out, hipStream_t s);
 // *out += number of set bits of bm[0, nwords).
 hipError_t launch_popcount(const uint32_t *bm, size_t nwords, unsigned long long *out,
                            hipStream_t s);

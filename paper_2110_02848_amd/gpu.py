@@ -32,6 +32,9 @@ FST_OPT_COUNT_MOVES = 5
 
 PHASES = ("preprocess", "forward", "backward", "count", "fill")
 
+# kernels timed one by one (enum fst_kernel)
+KERNELS = ("search_forward", "search_backward", "count", "fill")
+
 
 class FstError(RuntimeError):
     def __init__(self, code, where):
@@ -60,7 +63,7 @@ class _GraphOut(ctypes.Structure):
 class _Stats(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int64) for n in (
         "key_space", "accessible", "coaccessible", "generated", "fwd_levels",
-        "bwd_levels", "heavy_states", "num_states", "num_arcs")]
+        "bwd_levels", "heavy_states", "num_states", "num_arcs", "generated_backward")]
 
 
 _lib = None
@@ -93,6 +96,10 @@ def load():
     lib.fst_compose_phase_times.argtypes = [ctypes.c_void_p, ctypes.POINTER(ctypes.c_float),
                                             ctypes.c_int]
     lib.fst_compose_phase_times.restype = ctypes.c_int
+    lib.fst_compose_kernel_time.argtypes = [ctypes.c_void_p, ctypes.c_int,
+                                            ctypes.POINTER(ctypes.c_float),
+                                            ctypes.POINTER(ctypes.c_int64)]
+    lib.fst_compose_kernel_time.restype = ctypes.c_int
     lib.fst_strerror.argtypes = [ctypes.c_int]
     lib.fst_strerror.restype = ctypes.c_char_p
     _lib = lib
@@ -221,6 +228,16 @@ class Composer:
         _check(self._lib.fst_compose_phase_times(self._h, buf, len(PHASES)),
                "fst_compose_phase_times")
         return dict(zip(PHASES, [float(x) for x in buf]))
+
+    def kernel_times(self):
+        """{kernel: (ms, launches)} of the last timed run + fill."""
+        out = {}
+        for i, name in enumerate(KERNELS):
+            ms, n = ctypes.c_float(), ctypes.c_int64()
+            _check(self._lib.fst_compose_kernel_time(self._h, i, ctypes.byref(ms), ctypes.byref(n)),
+                   "fst_compose_kernel_time")
+            out[name] = (float(ms.value), int(n.value))
+        return out
 
 
 def to_numpy(C):

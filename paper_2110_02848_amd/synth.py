@@ -23,9 +23,13 @@ Workloads (Section 4 of the paper; the paper's LibriSpeech lexicon is not
 available, so uniform random spellings stand in for it):
 
 * random FST pairs (Section 4.1 recipe, with epsilon labels and several
-  accepting states): ``random_pair_config(i, seed)`` for i in 1..3;
+  accepting states): ``random_pair(name, seed)`` for the names of
+  ``RANDOM_SPECS`` ("random-64", "random-1000", "random-5000");
 * emissions (A) and lexicon (B) graphs (Section 4.2 recipe):
-  ``emissions_lexicon_config(i, seed)`` for i in 4..5.
+  ``emissions_lexicon(name, seed)`` for the names of ``LEX_SPECS``
+  ("lexicon-T100-W1000", "lexicon-T500-W10000").
+
+``workload(name, seed)`` returns the pair ``(A, B)`` of any of them.
 """
 from __future__ import annotations
 
@@ -167,20 +171,25 @@ class RandomSpec:
 
 
 RANDOM_SPECS = {
-    1: RandomSpec(64, 4, 16, 0.10, 0.10),
-    2: RandomSpec(1000, 8, 32, 0.05, 0.10),
-    3: RandomSpec(5000, 4, 64, 0.05, 0.05),
+    "random-64": RandomSpec(64, 4, 16, 0.10, 0.10),
+    "random-1000": RandomSpec(1000, 8, 32, 0.05, 0.10),
+    "random-5000": RandomSpec(5000, 4, 64, 0.05, 0.05),
 }
 
+# Seed stream of each workload: inputs are drawn from
+# SeedSequence([stream, seed]).spawn(2), one generator for A and one for B.
+_STREAM = {"random-64": 1, "random-1000": 2, "random-5000": 3,
+           "lexicon-T100-W1000": 4, "lexicon-T500-W10000": 5}
 
-def _rngs(cfg, seed):
-    ss = np.random.SeedSequence([int(cfg), int(seed)])
+
+def _rngs(name, seed):
+    ss = np.random.SeedSequence([_STREAM[name], int(seed)])
     return [np.random.default_rng(s) for s in ss.spawn(2)]
 
 
-def random_pair_config(cfg, seed=0):
-    spec = RANDOM_SPECS[cfg]
-    ra, rb = _rngs(cfg, seed)
+def random_pair(name, seed=0):
+    spec = RANDOM_SPECS[name]
+    ra, rb = _rngs(name, seed)
     A = random_fst(ra, spec.V, spec.degree, spec.n_sym, spec.p_eps, spec.p_accept)
     B = random_fst(rb, spec.V, spec.degree, spec.n_sym, spec.p_eps, spec.p_accept)
     return A, B
@@ -273,34 +282,38 @@ class LexSpec:
 
 
 LEX_SPECS = {
-    4: LexSpec(100, 28, 1000, 3, 8),
-    5: LexSpec(500, 64, 10000, 3, 10),
+    "lexicon-T100-W1000": LexSpec(100, 28, 1000, 3, 8),
+    "lexicon-T500-W10000": LexSpec(500, 64, 10000, 3, 10),
 }
 
 
-def emissions_lexicon_config(cfg, seed=0, spec=None):
-    """A = emissions, B = lexicon (so A o B maps token strings to word strings)."""
-    spec = spec or LEX_SPECS[cfg]
-    ra, rb = _rngs(cfg, seed)
+def emissions_lexicon(name, seed=0, spec=None):
+    """A = emissions, B = lexicon (so A o B maps token strings to word
+    strings).  ``spec`` overrides the sizes (the seed stream stays that of
+    ``name``)."""
+    spec = spec or LEX_SPECS[name]
+    ra, rb = _rngs(name, seed)
     A, table = emissions(ra, spec.T, spec.C)
     B, spell = lexicon(rb, spec.W, spec.C, spec.len_lo, spec.len_hi)
     return A, B, dict(table=table, spellings=spell, spec=spec)
 
 
-def config(cfg, seed=0):
-    """Inputs ``(A, B)`` of workload ``cfg`` (1..5) for a given seed."""
-    if cfg in RANDOM_SPECS:
-        return random_pair_config(cfg, seed)
-    A, B, _ = emissions_lexicon_config(cfg, seed)
+def workload(name, seed=0):
+    """Inputs ``(A, B)`` of a named workload for a given seed."""
+    if name in RANDOM_SPECS:
+        return random_pair(name, seed)
+    A, B, _ = emissions_lexicon(name, seed)
     return A, B
 
 
-CONFIG_NAMES = {
-    1: "random pair V=64 d=4 K=16 p_eps=0.1 p_acc=0.1",
-    2: "random pair V=1000 d=8 K=32 p_eps=0.05 p_acc=0.1",
-    3: "random pair V=5000 d=4 K=64 p_eps=0.05 p_acc=0.05",
-    4: "emissions(T=100,C=28) o lexicon(W=1000,L=3..8)",
-    5: "emissions(T=500,C=64) o lexicon(W=10000,L=3..10)",
+WORKLOADS = tuple(RANDOM_SPECS) + tuple(LEX_SPECS)
+
+WORKLOAD_TITLES = {
+    "random-64": "random pair V=64 d=4 K=16 p_eps=0.1 p_acc=0.1",
+    "random-1000": "random pair V=1000 d=8 K=32 p_eps=0.05 p_acc=0.1",
+    "random-5000": "random pair V=5000 d=4 K=64 p_eps=0.05 p_acc=0.05",
+    "lexicon-T100-W1000": "emissions(T=100,C=28) o lexicon(W=1000,L=3..8)",
+    "lexicon-T500-W10000": "emissions(T=500,C=64) o lexicon(W=10000,L=3..10)",
 }
 
 

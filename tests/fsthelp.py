@@ -270,10 +270,9 @@ def dag_total_score(C):
             break
         idx = order[np.repeat(lo - np.concatenate([[0], np.cumsum(cnt)[:-1]]), cnt) + np.arange(tot)]
         np.logaddexp.at(alpha, dst[idx], alpha[src[idx]] + w[idx])
-        dec = np.bincount(dst[idx], minlength=V)
-        before = indeg.copy()
-        indeg -= dec
-        frontier = np.flatnonzero((indeg == 0) & (before > 0))
+        heads, dec = np.unique(dst[idx], return_counts=True)
+        indeg[heads] -= dec
+        frontier = heads[indeg[heads] == 0]
     if done != V:
         raise ValueError("graph is not acyclic")
     acc = alpha[C["accept"] == 1]

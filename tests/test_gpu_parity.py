@@ -40,38 +40,38 @@ def check_pair(comp, A, B, tag, order=oracle.ORDER_FORWARD):
 
 
 @pytest.mark.parametrize("seed", range(100))
-def test_random_small_cfg1(comp, seed):
-    A, B = synth.config(1, seed)
-    got, _ = check_pair(comp, A, B, f"cfg1 seed {seed}")
+def test_random_64(comp, seed):
+    A, B = synth.workload("random-64", seed)
+    got, _ = check_pair(comp, A, B, f"random-64 seed {seed}")
     if seed < 10:
         assert not fsthelp.check_invariants(A, B, got)
 
 
 @pytest.mark.parametrize("seed", range(6))
-def test_random_cfg2(comp, seed):
-    A, B = synth.config(2, seed)
-    check_pair(comp, A, B, f"cfg2 seed {seed}")
+def test_random_1000(comp, seed):
+    A, B = synth.workload("random-1000", seed)
+    check_pair(comp, A, B, f"random-1000 seed {seed}")
 
 
 @pytest.mark.parametrize("seed", range(10))
-def test_random_cfg3(comp, seed):
-    A, B = synth.config(3, seed)
-    check_pair(comp, A, B, f"cfg3 seed {seed}")
+def test_random_5000(comp, seed):
+    A, B = synth.workload("random-5000", seed)
+    check_pair(comp, A, B, f"random-5000 seed {seed}")
 
 
 @pytest.mark.parametrize("seed", range(3))
-def test_lexicon_cfg4(comp, seed):
-    A, B, meta = synth.emissions_lexicon_config(4, seed)
-    got, _ = check_pair(comp, A, B, f"cfg4 seed {seed}")
+def test_lexicon_T100_W1000(comp, seed):
+    A, B, meta = synth.emissions_lexicon("lexicon-T100-W1000", seed)
+    got, _ = check_pair(comp, A, B, f"lexicon-T100-W1000 seed {seed}")
     V, E = fsthelp.lexicon_closed_form(meta["spec"].T, meta["spellings"])
     assert (got["num_states"], got["num_arcs"]) == (V, E)
 
 
 @pytest.mark.timeout(900)
-def test_lexicon_cfg5_full(comp):
+def test_lexicon_T500_W10000_full(comp):
     """Full-size emissions(T=500, C=64) o lexicon(W=10000): every element."""
-    A, B, meta = synth.emissions_lexicon_config(5, 0)
-    got, _ = check_pair(comp, A, B, "cfg5 seed 0")
+    A, B, meta = synth.emissions_lexicon("lexicon-T500-W10000", 0)
+    got, _ = check_pair(comp, A, B, "lexicon-T500-W10000 seed 0")
     V, E = fsthelp.lexicon_closed_form(meta["spec"].T, meta["spellings"])
     assert (got["num_states"], got["num_arcs"]) == (V, E)
 
@@ -113,7 +113,7 @@ def test_heavy_states(comp):
 
 def test_lexicon_small_many_words(comp):
     spec = synth.LexSpec(T=40, C=8, W=3000, len_lo=1, len_hi=4)
-    A, B, meta = synth.emissions_lexicon_config(4, 11, spec=spec)
+    A, B, meta = synth.emissions_lexicon("lexicon-T100-W1000", 11, spec=spec)
     got, _ = check_pair(comp, A, B, "lexicon W=3000")
     assert comp.stats()["heavy_states"] > 0
     V, E = fsthelp.lexicon_closed_form(spec.T, meta["spellings"])
@@ -147,7 +147,7 @@ def test_rounding_cases(comp):
 
 def test_degenerate_inputs(comp):
     E0 = synth.empty_graph()
-    A, B = synth.config(1, 0)
+    A, B = synth.workload("random-64", 0)
     for X, Y, tag in ((E0, E0, "empty/empty"), (E0, A, "empty/A"), (A, E0, "A/empty")):
         got, _ = check_pair(comp, X, Y, tag)
         assert got["num_states"] == 0 and got["arc_offset"].tolist() == [0]
@@ -163,8 +163,8 @@ def test_degenerate_inputs(comp):
 
 
 def test_deterministic_and_context_reuse(comp):
-    A2, B2 = synth.config(2, 1)
-    A1, B1 = synth.config(1, 3)
+    A2, B2 = synth.workload("random-1000", 1)
+    A1, B1 = synth.workload("random-64", 3)
     r1 = gpu_compose(comp, A2, B2)
     gpu_compose(comp, A1, B1)
     r2 = gpu_compose(comp, A2, B2)
@@ -174,7 +174,7 @@ def test_deterministic_and_context_reuse(comp):
 def test_errors(comp):
     import torch
     from paper_2110_02848_amd import gpu
-    A, B = synth.config(1, 0)
+    A, B = synth.workload("random-64", 0)
     bad = {k: (v.copy() if hasattr(v, "copy") else v) for k, v in A.items()}
     bad["dst"][3] = A["num_states"]  # out of range
     with pytest.raises(gpu.FstError) as ei:

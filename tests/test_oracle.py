@@ -238,16 +238,17 @@ def test_pins_detect_planted_mistakes(mutation):
 
 @pytest.mark.parametrize("seed", range(12))
 def test_orders_agree_random_small(seed):
-    A, B = synth.config(1, seed)
+    A, B = synth.workload("random-64", seed)
     Cp = oracle.compose(A, B, oracle.ORDER_PAPER)
     Cf = oracle.compose(A, B, oracle.ORDER_FORWARD)
     assert not fsthelp.compare_results(Cp, Cf)
     assert not fsthelp.check_invariants(A, B, Cp)
 
 
-@pytest.mark.parametrize("cfg,seed", [(2, 1), (2, 2), (3, 0), (3, 7)])
-def test_orders_agree_random_large(cfg, seed):
-    A, B = synth.config(cfg, seed)
+@pytest.mark.parametrize("name,seed", [("random-1000", 1), ("random-1000", 2),
+                                       ("random-5000", 0), ("random-5000", 7)])
+def test_orders_agree_random_large(name, seed):
+    A, B = synth.workload(name, seed)
     Cp = oracle.compose(A, B, oracle.ORDER_PAPER)
     Cf = oracle.compose(A, B, oracle.ORDER_FORWARD)
     assert not fsthelp.compare_results(Cp, Cf)
@@ -274,15 +275,15 @@ def _lex_check(A, B, meta, C):
 
 def test_lexicon_closed_form_small():
     spec = synth.LexSpec(T=30, C=6, W=40, len_lo=2, len_hi=5)
-    A, B, meta = synth.emissions_lexicon_config(4, 3, spec=spec)
+    A, B, meta = synth.emissions_lexicon("lexicon-T100-W1000", 3, spec=spec)
     for order in (oracle.ORDER_PAPER, oracle.ORDER_FORWARD):
         C = oracle.compose(A, B, order)
         assert not fsthelp.check_invariants(A, B, C)
         _lex_check(A, B, meta, C)
 
 
-def test_lexicon_closed_form_cfg4():
-    A, B, meta = synth.emissions_lexicon_config(4, 0)
+def test_lexicon_closed_form_T100_W1000():
+    A, B, meta = synth.emissions_lexicon("lexicon-T100-W1000", 0)
     C = oracle.compose(A, B, oracle.ORDER_FORWARD)
     assert not fsthelp.check_invariants(A, B, C)
     _lex_check(A, B, meta, C)
@@ -291,8 +292,8 @@ def test_lexicon_closed_form_cfg4():
 
 
 @pytest.mark.slow
-def test_lexicon_closed_form_cfg5():
-    A, B, meta = synth.emissions_lexicon_config(5, 0)
+def test_lexicon_closed_form_T500_W10000():
+    A, B, meta = synth.emissions_lexicon("lexicon-T500-W10000", 0)
     C = oracle.compose(A, B, oracle.ORDER_FORWARD)
     _lex_check(A, B, meta, C)
 
@@ -303,7 +304,7 @@ def test_lexicon_closed_form_cfg5():
 
 def test_empty_inputs():
     E0 = synth.empty_graph()
-    A, _ = synth.config(1, 0)
+    A, _ = synth.workload("random-64", 0)
     for X, Y in ((E0, E0), (E0, A), (A, E0)):
         C = oracle.compose(X, Y)
         assert C["num_states"] == 0 and C["num_arcs"] == 0

@@ -5,21 +5,22 @@ import pytest
 from paper_2110_02848_amd import synth
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4])
-def test_deterministic_per_seed(cfg):
-    A1, B1 = synth.config(cfg, 5)
-    A2, B2 = synth.config(cfg, 5)
-    A3, B3 = synth.config(cfg, 6)
+@pytest.mark.parametrize("name", ["random-64", "random-1000", "random-5000",
+                                  "lexicon-T100-W1000"])
+def test_deterministic_per_seed(name):
+    A1, B1 = synth.workload(name, 5)
+    A2, B2 = synth.workload(name, 5)
+    A3, B3 = synth.workload(name, 6)
     assert synth.graph_sha256(A1) == synth.graph_sha256(A2)
     assert synth.graph_sha256(B1) == synth.graph_sha256(B2)
     assert synth.graph_sha256(A1) != synth.graph_sha256(A3)
     assert synth.graph_sha256(A1) != synth.graph_sha256(B1)
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3])
-def test_random_recipe(cfg):
-    spec = synth.RANDOM_SPECS[cfg]
-    A, B = synth.config(cfg, 0)
+@pytest.mark.parametrize("name", list(synth.RANDOM_SPECS))
+def test_random_recipe(name):
+    spec = synth.RANDOM_SPECS[name]
+    A, B = synth.workload(name, 0)
     for g in (A, B):
         assert g["num_states"] == spec.V
         assert np.all(np.diff(g["arc_offset"]) == spec.degree)
@@ -30,10 +31,10 @@ def test_random_recipe(cfg):
         assert g["weight"].dtype == np.float32
 
 
-@pytest.mark.parametrize("cfg", [4, 5])
-def test_lexicon_recipe(cfg):
-    spec = synth.LEX_SPECS[cfg]
-    A, B, meta = synth.emissions_lexicon_config(cfg, 0)
+@pytest.mark.parametrize("name", list(synth.LEX_SPECS))
+def test_lexicon_recipe(name):
+    spec = synth.LEX_SPECS[name]
+    A, B, meta = synth.emissions_lexicon(name, 0)
     T, C, W = spec.T, spec.C, spec.W
     assert A["num_states"] == T + 1 and len(A["src"]) == T * C
     assert np.array_equal(A["ilabel"], A["olabel"])
