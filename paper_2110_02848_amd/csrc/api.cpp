@@ -237,6 +237,8 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   c->stats = fst_stats{};
   if (VA == 0 || VB == 0) return finish_empty(c, V_C, E_C);
 
+  // state ids share their arc-record word with two flag bits
+  if (VA > NBR_MASK || VB > NBR_MASK) return FST_ERR_TOO_LARGE;
   const uint32_t shiftB = (uint32_t)bitlen((unsigned long long)(VB - 1));
   const unsigned long long nkeys = (unsigned long long)VA << (shiftB + 1);
   if (nkeys >= (1ull << 32)) return FST_ERR_TOO_LARGE;
@@ -263,25 +265,40 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
                           {&c->bInPerm, &c->bInArc, &c->bInRec, &c->bInLut, &c->bInOff}};
   unsigned long long *k0 = as<unsigned long long>(c->k0), *k1 = as<unsigned long long>(c->k1);
   int32_t *v0 = as<int32_t>(c->v0), *v1 = as<int32_t>(c->v1);
-  View views[4];
+  int4 *rec[4], *lutp[4];
+  int2 *arc[4];
+  int32_t *perm[4];
   for (int i = 0; i < 4; ++i) {
     const bool isA = (i % 2) == 0, in = i >= 2;
     const DevGraph &g = isA ? dA : dB;
     const bool lut = isA ? lutA : lutB;
-    const uint32_t lmax = isA ? maxA : maxB;
     FST_TRY(ensure(c, *vb[i].perm, (size_t)g.E * sizeof(int32_t)));
     FST_TRY(ensure(c, *vb[i].arc, (size_t)g.E * sizeof(int2)));
-    FST_TRY(ensure(c, *vb[i].rec, (size_t)g.V * sizeof(int4)));
-    if (lut) FST_TRY(ensure(c, *vb[i].lut, lut_bytes(g.V, lmax)));
+    FST_TRY(ensure(c, *vb[i].rec, (size_t)g.V * 2 * sizeof(int4)));
+    if (lut) FST_TRY(ensure(c, *vb[i].lut, lut_bytes(g.V, isA ? maxA : maxB)));
     if (in) FST_TRY(ensure(c, *vb[i].off, ((size_t)g.V + 1) * sizeof(int32_t)));
-    int4 *lutp = lut ? as<int4>(*vb[i].lut) : nullptr;
-    const int4 *eps_rec = (i == 2) ? as<int4>(c->aOutRec) : nullptr;
-    HIP_TRY(build_view(g, isA ? 0 : 1, in, isA ? labA : labB, (int32_t)lmax, as<int4>(*vb[i].rec),
-                       as<int2>(*vb[i].arc), as<int32_t>(*vb[i].perm), lutp,
-                       in ? as<int32_t>(*vb[i].off) : nullptr, eps_rec, k0, v0, k1, v1,
-                       c->sort_tmp.p, i == 0 ? &d_sc->nEpsStatesA : nullptr, s));
-    views[i] = View{as<int4>(*vb[i].rec), as<int2>(*vb[i].arc), as<int32_t>(*vb[i].perm), lutp,
-                    (int32_t)lmax + 1};
+    rec[i] = as<int4>(*vb[i].rec);
+    arc[i] = as<int2>(*vb[i].arc);
+    perm[i] = as<int32_t>(*vb[i].perm);
+    lutp[i] = lut ? as<int4>(*vb[i].lut) : nullptr;
+  }
+  for (int i = 0; i < 4; ++i) {
+    const bool isA = (i % 2) == 0, in = i >= 2;
+    HIP_TRY(sort_view(isA ? dA : dB, isA ? 0 : 1, in, isA ? labA : labB, rec[i], arc[i], perm[i],
+                      in ? as<int32_t>(*vb[i].off) : nullptr, i == 2 ? rec[0] : nullptr, k0, v0,
+                      k1, v1, c->sort_tmp.p, i == 0 ? &d_sc->nEpsStatesA : nullptr, s));
+  }
+  // a view's FLAG_UNIQ comes from the opposite view of the same graph
+  for (int i = 0; i < 4; ++i) {
+    const bool isA = (i % 2) == 0, in = i >= 2;
+    HIP_TRY(mark_unique(isA ? dA : dB, isA ? 0 : 1, !in, rec[i], rec[i ^ 2], arc[i ^ 2], s));
+  }
+  View views[4];
+  for (int i = 0; i < 4; ++i) {
+    const bool isA = (i % 2) == 0;
+    const uint32_t lmax = isA ? maxA : maxB;
+    HIP_TRY(finish_view(isA ? dA : dB, (int32_t)lmax, rec[i], arc[i], lutp[i], s));
+    views[i] = View{rec[i], arc[i], perm[i], lutp[i], (int32_t)lmax + 1};
   }
   FST_TRY(readback(c, s));
 
@@ -341,6 +358,9 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   HIP_TRY(hipMemsetAsync(d_sc->G, 0, sizeof(d_sc->G), s));
   HIP_TRY(launch_seed_backward(P, S, bq, s));
   FST_TRY(search(c, S, false, &c->stats.bwd_levels, s));
+  // the backward search may set co-accessible bits of keys it never expands
+  // (not accessible); the trim set is what remains after masking them
+  HIP_TRY(launch_and_words(P.coacc, P.vis, nwords, s));
   if (c->count_moves) HIP_TRY(launch_count_moves(P, nwords, false, &d_sc->generated_bwd, s));
 
   // ---- numbering and arc counts ----

@@ -46,6 +46,9 @@ __device__ __forceinline__ uint32_t wave_max(uint32_t x) {
   return x;
 }
 
+// The state id in an arc record's neighbour field.
+__device__ __forceinline__ uint32_t nbr_of(int32_t y) { return (uint32_t)(y & NBR_MASK); }
+
 // First index in [lo, hi) whose label (.x) is >= x.
 __device__ __forceinline__ int32_t lb_label(const int2 *a, int32_t lo, int32_t hi, int32_t x) {
   while (lo < hi) {
@@ -131,7 +134,7 @@ __global__ __launch_bounds__(NT) void k_split(DevGraph g, int by_dst, const ull 
     const int32_t e = v[i];
     perm[i] = e;
     int32_t nb = by_dst ? g.src[e] : g.dst[e];
-    if (eps_rec && eps_rec[nb].y > 0) nb |= (int32_t)0x80000000;
+    if (eps_rec && eps_rec[2 * (size_t)nb].y > 0) nb |= NBR_EPS;
     arec[i] = make_int2((int32_t)(k[i] & mask), nb);
   }
 }
@@ -158,6 +161,7 @@ __global__ __launch_bounds__(NT) void k_group_offsets(const ull *__restrict__ k,
 __global__ __launch_bounds__(NT) void k_state_rec(const int32_t *__restrict__ off,
                                                   const int2 *__restrict__ arec, int V,
                                                   const uint8_t *__restrict__ accept,
+                                                  const uint8_t *__restrict__ start,
                                                   int eps_mode, const int4 *__restrict__ eps_rec,
                                                   int4 *__restrict__ srec,
                                                   uint32_t *eps_states) {
@@ -168,14 +172,69 @@ __global__ __launch_bounds__(NT) void k_state_rec(const int32_t *__restrict__ of
     const int32_t s0 = off[v], s1 = off[v + 1];
     const int32_t n = lb_label(arec, s0, s1, 1) - s0;
     int32_t flags = accept[v] ? (int32_t)FLAG_ACCEPT : 0;
-    if ((eps_mode == 1 && n > 0) || (eps_mode == 2 && eps_rec[v].y > 0))
+    if ((eps_mode == 1 && n > 0) || (eps_mode == 2 && eps_rec[2 * v].y > 0))
       flags |= (int32_t)FLAG_EPS_OUT;
-    srec[v] = make_int4(s0, n, s1, flags);
+    if (start && start[v]) flags |= (int32_t)FLAG_START;
+    srec[2 * v] = make_int4(s0, n, s1, flags);
     neps_states += n > 0 ? 1u : 0u;
   }
   if (eps_states) {
     const uint32_t tot = block_sum(neps_states, s_w);
     if (threadIdx.x == 0 && tot) atomicAdd(eps_states, tot);
+  }
+}
+
+// Groups longer than this are never marked FLAG_UNIQ in A (their labels are
+// not checked one by one).
+constexpr int32_t UNIQ_SCAN_MAX = 256;
+
+// FLAG_UNIQ of the records `self` of a view, from the opposite view's groups.
+__global__ __launch_bounds__(NT) void k_mark_unique(int V, int side, int out_view,
+                                                    const uint8_t *__restrict__ excl,
+                                                    int4 *__restrict__ self,
+                                                    const int4 *__restrict__ other,
+                                                    const int2 *__restrict__ oarec) {
+  for (long long v = (long long)blockIdx.x * NT + threadIdx.x; v < V;
+       v += (long long)gridDim.x * NT) {
+    const int4 o = other[2 * v];
+    const int4 me = self[2 * v];
+    const int32_t n = o.z - o.x;
+    bool u = excl[v] == 0;
+    if (side == 1) {
+      u = u && n == 1;
+    } else {
+      // no epsilon output of v itself (out-view: its own epsilon count)
+      if (out_view && me.y != 0) u = false;
+      if (o.y != 0 || n > UNIQ_SCAN_MAX) u = false;
+      for (int32_t i = o.x; u && i < o.z; ++i) {
+        const int2 a = oarec[i];
+        if (a.y & NBR_EPS) u = false;                          // source has epsilon output
+        if (i > o.x && oarec[i - 1].x == a.x) u = false;      // repeated label
+      }
+    }
+    if (u) self[2 * v] = make_int4(me.x, me.y, me.z, me.w | (int32_t)FLAG_UNIQ);
+  }
+}
+
+// Mark every arc whose other end has FLAG_UNIQ in this view.
+__global__ __launch_bounds__(NT) void k_mark_arcs(int2 *__restrict__ arec,
+                                                  const int4 *__restrict__ srec, long long E) {
+  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < E;
+       i += (long long)gridDim.x * NT) {
+    const int2 a = arec[i];
+    if (srec[2 * (size_t)(a.y & NBR_MASK)].w & (int32_t)FLAG_UNIQ)
+      arec[i] = make_int2(a.x, a.y | NBR_UNIQ);
+  }
+}
+
+// Second state record: the first epsilon and first non-epsilon arcs.
+__global__ __launch_bounds__(NT) void k_state_inline(int4 *__restrict__ srec,
+                                                     const int2 *__restrict__ arec, int V) {
+  for (long long v = (long long)blockIdx.x * NT + threadIdx.x; v < V;
+       v += (long long)gridDim.x * NT) {
+    const int4 r = srec[2 * v];
+    const int2 first_ne = r.x + r.y < r.z ? arec[r.x + r.y] : make_int2(0, 0);
+    srec[2 * v + 1] = make_int4(r.y > 0 ? arec[r.x].y : 0, first_ne.x, first_ne.y, 0);
   }
 }
 
@@ -188,7 +247,7 @@ __global__ __launch_bounds__(NT) void k_build_lut(const int4 *__restrict__ srec,
   for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n;
        i += (long long)gridDim.x * NT) {
     const int32_t v = (int32_t)(i / S), l = (int32_t)(i % S);
-    const int4 r = srec[v];
+    const int4 r = srec[2 * (size_t)v];
     const int32_t lo = lb_label(arec, r.x, r.z, l);
     const int32_t hi = lb_label(arec, lo, r.z, l + 1);
     lut[i] = make_int4(lo, hi, lo < hi ? arec[lo].y : -1, 0);
@@ -226,6 +285,15 @@ __device__ __forceinline__ void label_range(const View &v, uint32_t q, int32_t l
                                             int32_t lab, int32_t &r0, int32_t &r1) {
   int32_t nb0;
   label_range(v, q, lo, hi, lab, r0, r1, nb0);
+}
+
+// An opaque copy of a register value.  Selecting between it and a loaded
+// value stays a register select: without it the compiler may turn the
+// select into a load through a selected pointer, parking the register value
+// in scratch memory.
+__device__ __forceinline__ int32_t opaque(int32_t x) {
+  asm("" : "+v"(x));
+  return x;
 }
 
 // Claim a key that few threads are expected to reach at once.
@@ -268,21 +336,38 @@ __device__ __forceinline__ void wave_push(bool want, uint32_t key, const Pusher 
 }
 
 // Move structure of a key in the forward direction (also used to write C).
+// e0A/e0B: other end of the first epsilon arc of qa / qb; l1, n1: label and
+// other end of the first non-epsilon arc (valid when the arc exists).
 struct Fwd {
   uint32_t qa, qb, f;
   int32_t aS, ae, aE, bS, be, bE;
   uint32_t eA, nA, nB, mU;
   uint32_t epsA;    // epsOutA(qa)
   uint32_t accept;  // accept(qa) and accept(qb)
+  uint32_t uqA, uqB;  // FLAG_UNIQ of qa, qb (out-views)
+  int32_t e0A, e0B, l1A, n1A, l1B, n1B;
 };
 
+// INL: also load the inline first arcs (the search uses them; the output
+// passes walk the arc records anyway).
+template <bool INL = true>
 __device__ __forceinline__ Fwd fwd_info(const Problem &P, uint32_t key) {
   Fwd s;
   s.f = key_f(key);
   s.qb = key_qb(key, P.shiftB);
   s.qa = key_qa(key, P.shiftB);
-  const int4 ra = P.aOut.srec[s.qa];
-  const int4 rb = P.bOut.srec[s.qb];
+  const int4 ra = P.aOut.srec[2 * (size_t)s.qa];
+  const int4 rb = P.bOut.srec[2 * (size_t)s.qb];
+  if (INL) {
+    const int4 xa = P.aOut.srec[2 * (size_t)s.qa + 1];
+    const int4 xb = P.bOut.srec[2 * (size_t)s.qb + 1];
+    s.e0A = xa.x;
+    s.l1A = xa.y;
+    s.n1A = xa.z;
+    s.e0B = xb.x;
+    s.l1B = xb.y;
+    s.n1B = xb.z;
+  }
   s.aS = ra.x;
   s.ae = ra.y;
   s.aE = ra.z;
@@ -291,6 +376,8 @@ __device__ __forceinline__ Fwd fwd_info(const Problem &P, uint32_t key) {
   s.bE = rb.z;
   s.epsA = ra.y > 0 ? 1u : 0u;
   s.accept = (uint32_t)(ra.w & rb.w) & FLAG_ACCEPT;
+  s.uqA = (uint32_t)ra.w & FLAG_UNIQ;
+  s.uqB = (uint32_t)rb.w & FLAG_UNIQ;
   s.eA = s.f ? 0u : (uint32_t)s.ae;
   s.nA = (uint32_t)(s.aE - s.aS - s.ae);
   s.nB = (uint32_t)(s.bE - s.bS - s.be);
@@ -304,56 +391,52 @@ __device__ __forceinline__ Fwd fwd_info(const Problem &P, uint32_t key) {
 __device__ __forceinline__ uint32_t fwd_units(const Fwd &s) { return s.eA + (uint32_t)s.be + s.mU; }
 
 // The keys a work unit reaches: for p in [lo, hi), with nb_p the neighbour
-// field of arcs[p] (nb_lo given), the key (A state, B state, f) where the
-// side named by varyA takes nb_p and the other side is fixed.  In the
-// backward direction a key is also visited with f = 1 when `dual` holds or,
-// with dual_from_nb, when bit 31 of nb_p (epsOutA of an A-side neighbour)
-// is set.  One shape for all move kinds keeps a single visit site per kernel.
+// field of arc record p (nb_lo given) of the side named by VARY_A (A's view
+// when set, else B's), the key whose state on that side is nb_p and whose
+// state on the other side is `fixed`.  Forward keys take filter bit F_ONE;
+// backward keys are also visited with f = 1 under DUAL or, with
+// DUAL_FROM_NB, when bit 31 of nb_p (epsOutA of an A-side neighbour) is set.
+// HOT marks keys many threads may reach at once.  A key is reached at most
+// once by the search (needs no claim) when FIXED_UNIQ is set and nb_p has
+// NBR_UNIQ: both of its states are marked FLAG_UNIQ.  No pointer is kept, so
+// a range lives in a few registers.
+enum : uint32_t { VARY_A = 1, DUAL = 2, DUAL_FROM_NB = 4, HOT = 8, F_ONE = 16, FIXED_UNIQ = 32 };
 struct UnitRange {
-  const int2 *arcs;
   int32_t lo, hi, nb0;
-  uint32_t fa, fb, f;
-  bool varyA, dual, dual_from_nb;
-  bool hot;  // the keys may be reached by many threads at once
+  uint32_t fixed, flags;
 };
 
 __device__ __forceinline__ UnitRange fwd_range(const Problem &P, const Fwd &s, uint32_t u) {
   UnitRange r;
-  r.f = 0;
-  r.fa = r.fb = 0;
-  r.dual = r.dual_from_nb = false;
-  r.hot = true;
   if (u < s.eA) {  // A-epsilon move
-    r.arcs = P.aOut.arec;
     r.lo = s.aS + (int32_t)u;
-    r.varyA = true;
-    r.fb = s.qb;
+    r.hi = r.lo + 1;
+    r.fixed = s.qb;
+    r.flags = VARY_A | HOT | (s.uqB ? FIXED_UNIQ : 0u);
+    r.nb0 = u == 0 ? opaque(s.e0A) : P.aOut.arec[r.lo].y;
   } else if (u < s.eA + (uint32_t)s.be) {  // B-epsilon move
-    r.arcs = P.bOut.arec;
-    r.lo = s.bS + (int32_t)(u - s.eA);
-    r.varyA = false;
-    r.fa = s.qa;
-    r.f = s.epsA;
+    const uint32_t j = u - s.eA;
+    r.lo = s.bS + (int32_t)j;
+    r.hi = r.lo + 1;
+    r.fixed = s.qa;
+    r.flags = HOT | (s.epsA ? F_ONE : 0u) | (s.uqA ? FIXED_UNIQ : 0u);
+    r.nb0 = j == 0 ? opaque(s.e0B) : P.bOut.arec[r.lo].y;
   } else {  // matching moves of one arc of the smaller side
-    r.hot = false;
     const uint32_t j = u - s.eA - (uint32_t)s.be;
     if (s.nA <= s.nB) {
-      const int2 ar = P.aOut.arec[s.aS + s.ae + (int32_t)j];
+      const int2 ar = j == 0 ? make_int2(opaque(s.l1A), opaque(s.n1A))
+                             : P.aOut.arec[s.aS + s.ae + (int32_t)j];
       label_range(P.bOut, s.qb, s.bS + s.be, s.bE, ar.x, r.lo, r.hi, r.nb0);
-      r.arcs = P.bOut.arec;
-      r.varyA = false;
-      r.fa = (uint32_t)ar.y;
+      r.fixed = nbr_of(ar.y);
+      r.flags = (ar.y & NBR_UNIQ) ? FIXED_UNIQ : 0u;
     } else {
-      const int2 br = P.bOut.arec[s.bS + s.be + (int32_t)j];
+      const int2 br = j == 0 ? make_int2(opaque(s.l1B), opaque(s.n1B))
+                             : P.bOut.arec[s.bS + s.be + (int32_t)j];
       label_range(P.aOut, s.qa, s.aS + s.ae, s.aE, br.x, r.lo, r.hi, r.nb0);
-      r.arcs = P.aOut.arec;
-      r.varyA = true;
-      r.fb = (uint32_t)br.y;
+      r.fixed = nbr_of(br.y);
+      r.flags = VARY_A | ((br.y & NBR_UNIQ) ? FIXED_UNIQ : 0u);
     }
-    return r;
   }
-  r.hi = r.lo + 1;
-  r.nb0 = r.arcs[r.lo].y;
   return r;
 }
 
@@ -363,6 +446,8 @@ struct Bwd {
   uint32_t va, vb, g, epsV;
   int32_t aS, ae, aE, bS, be, bE;
   uint32_t eA, eB, nA, nB, mU;
+  uint32_t uqA, uqB;  // FLAG_UNIQ of va, vb (in-views)
+  int32_t e0A, e0B, l1A, n1A, l1B, n1B;  // inline first arcs, as in Fwd
 };
 
 __device__ __forceinline__ Bwd bwd_info(const Problem &P, uint32_t key) {
@@ -370,8 +455,16 @@ __device__ __forceinline__ Bwd bwd_info(const Problem &P, uint32_t key) {
   s.g = key_f(key);
   s.vb = key_qb(key, P.shiftB);
   s.va = key_qa(key, P.shiftB);
-  const int4 ra = P.aIn.srec[s.va];
-  const int4 rb = P.bIn.srec[s.vb];
+  const int4 ra = P.aIn.srec[2 * (size_t)s.va];
+  const int4 rb = P.bIn.srec[2 * (size_t)s.vb];
+  const int4 xa = P.aIn.srec[2 * (size_t)s.va + 1];
+  const int4 xb = P.bIn.srec[2 * (size_t)s.vb + 1];
+  s.e0A = xa.x;
+  s.l1A = xa.y;
+  s.n1A = xa.z;
+  s.e0B = xb.x;
+  s.l1B = xb.y;
+  s.n1B = xb.z;
   s.aS = ra.x;
   s.ae = ra.y;
   s.aE = ra.z;
@@ -379,6 +472,8 @@ __device__ __forceinline__ Bwd bwd_info(const Problem &P, uint32_t key) {
   s.be = rb.y;
   s.bE = rb.z;
   s.epsV = (ra.w & (int32_t)FLAG_EPS_OUT) ? 1u : 0u;
+  s.uqA = (uint32_t)ra.w & FLAG_UNIQ;
+  s.uqB = (uint32_t)rb.w & FLAG_UNIQ;
   s.eA = (s.g == 0) ? (uint32_t)s.ae : 0u;          // A-epsilon moves land on f = 0
   s.eB = (s.g == s.epsV) ? (uint32_t)s.be : 0u;     // B-epsilon moves land on f = epsOutA
   s.nA = (uint32_t)(s.aE - s.aS - s.ae);
@@ -391,63 +486,59 @@ __device__ __forceinline__ uint32_t bwd_units(const Bwd &s) { return s.eA + s.eB
 
 __device__ __forceinline__ UnitRange bwd_range(const Problem &P, const Bwd &s, uint32_t u) {
   UnitRange r;
-  r.f = 0;
-  r.fa = r.fb = 0;
-  r.dual = r.dual_from_nb = false;
-  r.hot = true;
   if (u < s.eA) {  // predecessor by an A-epsilon move: (ua, vb, 0)
-    r.arcs = P.aIn.arec;
     r.lo = s.aS + (int32_t)u;
-    r.varyA = true;
-    r.fb = s.vb;
+    r.hi = r.lo + 1;
+    r.fixed = s.vb;
+    r.flags = VARY_A | HOT | (s.uqB ? FIXED_UNIQ : 0u);
+    r.nb0 = u == 0 ? opaque(s.e0A) : P.aIn.arec[r.lo].y;
   } else if (u < s.eA + s.eB) {  // by a B-epsilon move: (va, ub, 0 and 1)
-    r.arcs = P.bIn.arec;
-    r.lo = s.bS + (int32_t)(u - s.eA);
-    r.varyA = false;
-    r.fa = s.va;
-    r.dual = s.epsV != 0;
+    const uint32_t j = u - s.eA;
+    r.lo = s.bS + (int32_t)j;
+    r.hi = r.lo + 1;
+    r.fixed = s.va;
+    r.flags = HOT | (s.epsV ? DUAL : 0u) | (s.uqA ? FIXED_UNIQ : 0u);
+    r.nb0 = j == 0 ? opaque(s.e0B) : P.bIn.arec[r.lo].y;
   } else {  // by matching moves: (ua, ub, 0 and, if epsOutA(ua), 1)
-    r.hot = false;
     const uint32_t j = u - s.eA - s.eB;
     if (s.nA <= s.nB) {
-      const int2 ar = P.aIn.arec[s.aS + s.ae + (int32_t)j];
+      const int2 ar = j == 0 ? make_int2(opaque(s.l1A), opaque(s.n1A))
+                             : P.aIn.arec[s.aS + s.ae + (int32_t)j];
       label_range(P.bIn, s.vb, s.bS + s.be, s.bE, ar.x, r.lo, r.hi, r.nb0);
-      r.arcs = P.bIn.arec;
-      r.varyA = false;
-      r.fa = (uint32_t)(ar.y & NBR_MASK);
-      r.dual = ar.y < 0;
+      r.fixed = nbr_of(ar.y);
+      r.flags = ((ar.y & NBR_EPS) ? DUAL : 0u) | ((ar.y & NBR_UNIQ) ? FIXED_UNIQ : 0u);
     } else {
-      const int2 br = P.bIn.arec[s.bS + s.be + (int32_t)j];
+      const int2 br = j == 0 ? make_int2(opaque(s.l1B), opaque(s.n1B))
+                             : P.bIn.arec[s.bS + s.be + (int32_t)j];
       label_range(P.aIn, s.va, s.aS + s.ae, s.aE, br.x, r.lo, r.hi, r.nb0);
-      r.arcs = P.aIn.arec;
-      r.varyA = true;
-      r.fb = (uint32_t)br.y;
-      r.dual_from_nb = true;
+      r.fixed = nbr_of(br.y);
+      r.flags = VARY_A | DUAL_FROM_NB | ((br.y & NBR_UNIQ) ? FIXED_UNIQ : 0u);
     }
-    return r;
   }
-  r.hi = r.lo + 1;
-  r.nb0 = r.arcs[r.lo].y;
   return r;
 }
 
-// Calls f(key) for every key of unit `u` of a key with structure s.
-template <bool FWD, class Info, class F>
-__device__ __forceinline__ void for_unit(const Problem &P, const Info &s, uint32_t u, F &&f) {
-  UnitRange r;
-  if constexpr (FWD) r = fwd_range(P, s, u);
-  else r = bwd_range(P, s, u);
+// Calls f(key, hot, uniq) for every key of a unit range.
+template <bool FWD, class F>
+__device__ __forceinline__ void for_range(const Problem &P, const UnitRange &r, F &&f) {
   const uint32_t sh = P.shiftB;
+  const bool varyA = (r.flags & VARY_A) != 0, hot = (r.flags & HOT) != 0;
+  const int2 *arcs = FWD ? (varyA ? P.aOut.arec : P.bOut.arec) : (varyA ? P.aIn.arec : P.bIn.arec);
   for (int32_t p = r.lo; p < r.hi; ++p) {
-    const int32_t y = p == r.lo ? r.nb0 : r.arcs[p].y;
-    const uint32_t nb = (uint32_t)(y & NBR_MASK);
-    const uint32_t qa = r.varyA ? nb : r.fa, qb = r.varyA ? r.fb : nb;
-    const uint32_t nf = (r.dual || (r.dual_from_nb && y < 0)) ? 2u : 1u;
-    for (uint32_t ff = 0; ff < nf; ++ff) f(make_key(qa, qb, FWD ? r.f : ff, sh), r.hot);
+    const int32_t y = p == r.lo ? r.nb0 : arcs[p].y;
+    const uint32_t nb = nbr_of(y);
+    const uint32_t qa = varyA ? nb : r.fixed, qb = varyA ? r.fixed : nb;
+    const bool uniq = (r.flags & FIXED_UNIQ) && (y & NBR_UNIQ);
+    if (FWD) {
+      f(make_key(qa, qb, (r.flags & F_ONE) ? 1u : 0u, sh), hot, uniq);
+    } else {
+      const uint32_t nf = ((r.flags & DUAL) || ((r.flags & DUAL_FROM_NB) && (y & NBR_EPS))) ? 2u : 1u;
+      for (uint32_t ff = 0; ff < nf; ++ff) f(make_key(qa, qb, ff, sh), hot, uniq);
+    }
   }
 }
 
-// Direction traits: move structure, unit count and unit expansion.
+// Direction traits: move structure, unit count and unit ranges.
 template <bool FWD>
 struct Dir;
 template <>
@@ -455,9 +546,8 @@ struct Dir<true> {
   typedef Fwd Info;
   static __device__ __forceinline__ Fwd info(const Problem &P, uint32_t k) { return fwd_info(P, k); }
   static __device__ __forceinline__ uint32_t units(const Fwd &s) { return fwd_units(s); }
-  template <class F>
-  static __device__ __forceinline__ void unit(const Problem &P, const Fwd &s, uint32_t u, F &&f) {
-    for_unit<true>(P, s, u, f);
+  static __device__ __forceinline__ UnitRange range(const Problem &P, const Fwd &s, uint32_t u) {
+    return fwd_range(P, s, u);
   }
 };
 template <>
@@ -465,11 +555,17 @@ struct Dir<false> {
   typedef Bwd Info;
   static __device__ __forceinline__ Bwd info(const Problem &P, uint32_t k) { return bwd_info(P, k); }
   static __device__ __forceinline__ uint32_t units(const Bwd &s) { return bwd_units(s); }
-  template <class F>
-  static __device__ __forceinline__ void unit(const Problem &P, const Bwd &s, uint32_t u, F &&f) {
-    for_unit<false>(P, s, u, f);
+  static __device__ __forceinline__ UnitRange range(const Problem &P, const Bwd &s, uint32_t u) {
+    return bwd_range(P, s, u);
   }
 };
+
+// Calls f(key, hot, uniq) for every key of unit `u` of a key with structure s.
+template <bool FWD, class F>
+__device__ __forceinline__ void for_unit(const Problem &P, const typename Dir<FWD>::Info &s,
+                                         uint32_t u, F &&f) {
+  for_range<FWD>(P, Dir<FWD>::range(P, s, u), f);
+}
 
 // Where the next generation's work goes.
 struct NextGen {
@@ -491,16 +587,22 @@ __device__ __forceinline__ void list_heavy(const SearchArgs &S, const NextGen &n
   }
 }
 
-// A key reached for the first time (`fresh`).  Forward: it is counted, and if
-// it accepts it is marked co-accessible and listed as a seed of the backward
-// search.  Then: heavy keys go to the next generation's heavy list; a light
-// key becomes this thread's next key (depth-first continuation) if it has none
-// yet and the depth budget allows, else it joins the next frontier.  The
-// continuation's move structure is kept in `ci`.
+// The key a search thread expands next (depth-first continuation).
+template <bool FWD>
+struct Next {
+  uint32_t key;
+  typename Dir<FWD>::Info info;
+};
+
+// A key reached for the first time (`fresh`).  Forward: if it accepts it is
+// marked co-accessible and listed as a seed of the backward search.  Then:
+// heavy keys go to the next generation's heavy list; a light key becomes this
+// thread's next key (depth-first continuation) if it has none yet and the
+// depth budget allows, else it joins the next frontier.
 template <bool FWD>
 __device__ __forceinline__ void place(const Problem &P, const SearchArgs &S, const NextGen &nx,
                                       bool fresh, uint32_t v, const typename Dir<FWD>::Info &vi,
-                                      uint32_t &cont, typename Dir<FWD>::Info &ci, int depth) {
+                                      Next<FWD> &nk, int depth) {
   bool push = false, seed = false;
   if (fresh) {
     const uint32_t u = Dir<FWD>::units(vi);
@@ -510,9 +612,9 @@ __device__ __forceinline__ void place(const Problem &P, const SearchArgs &S, con
     }
     if (u > LIGHT_SEARCH) {
       list_heavy(S, nx, v, u);
-    } else if (cont == NO_KEY && depth < P.chain_max) {
-      cont = v;
-      ci = vi;
+    } else if (nk.key == NO_KEY && depth < P.chain_max) {
+      nk.key = v;
+      nk.info = vi;
     } else {
       push = true;
     }
@@ -521,23 +623,48 @@ __device__ __forceinline__ void place(const Problem &P, const SearchArgs &S, con
   wave_push(push, v, Pusher{S.Q + nx.qbase, S.cap - nx.qbase, &nx.slot->qcount, S.sc});
 }
 
+// Sets a bit without reading the word back (no return value is waited for).
+__device__ __forceinline__ void set_bit(uint32_t *bm, uint32_t k) {
+  __hip_atomic_fetch_or(bm + (k >> 5), 1u << (k & 31u), __ATOMIC_RELAXED,
+                        __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Visit a move target (forward) or a predecessor (backward, where only
-// accessible keys are claimed).  The key's state records are loaded before
-// the claim is resolved, so both memory round trips overlap.
+// accessible keys are claimed).  The key's state records are loaded first and
+// its claim is issued after them, so both round trips overlap.  A key that
+// only one move leads to (uniq) is reached exactly once and just has its bit
+// set.  Hot keys (epsilon targets, which many threads may reach at once)
+// test-load the bitmap before the atomic.  Backward cold claims set the
+// co-accessible bit without looking at the accessible bit first; bits set on
+// keys that are not accessible are removed after the search (such keys are
+// never expanded: fresh needs both bits).
 template <bool FWD>
 __device__ __forceinline__ void visit(const Problem &P, const SearchArgs &S, const NextGen &nx,
-                                      uint32_t v, bool hot, uint32_t &cont,
-                                      typename Dir<FWD>::Info &ci, int depth) {
+                                      uint32_t v, bool hot, bool uniq, Next<FWD> &nk, int depth) {
   const typename Dir<FWD>::Info vi = Dir<FWD>::info(P, v);
+  const uint32_t bit = 1u << (v & 31u), w = v >> 5;
   bool fresh;
-  if (FWD) {
-    fresh = hot ? claim(P.vis, v) : claim_cold(P.vis, v);
+  if (uniq) {
+    if (FWD) {
+      set_bit(P.vis, v);
+      fresh = true;
+    } else {
+      fresh = (P.vis[w] & bit) != 0;
+      if (fresh) set_bit(P.coacc, v);
+    }
+  } else if (hot) {
+    if (FWD) {
+      fresh = claim(P.vis, v);
+    } else {
+      const uint32_t wv = P.vis[w], wc = P.coacc[w];  // one round trip for both
+      fresh = (wv & bit) && !(wc & bit) && (atomicOr(P.coacc + w, bit) & bit) == 0;
+    }
   } else {
-    const uint32_t bit = 1u << (v & 31u), w = v >> 5;
-    const uint32_t wv = P.vis[w], wc = P.coacc[w];  // one round trip for both
-    fresh = (wv & bit) && !(wc & bit) && (atomicOr(P.coacc + w, bit) & bit) == 0;
+    const uint32_t wv = FWD ? bit : P.vis[w];
+    const uint32_t old = atomicOr((FWD ? P.vis : P.coacc) + w, bit);
+    fresh = (wv & bit) && !(old & bit);
   }
-  place<FWD>(P, S, nx, fresh, v, vi, cont, ci, depth);
+  place<FWD>(P, S, nx, fresh, v, vi, nk, depth);
 }
 
 // Generation g (one kernel): one thread per unit of the generation's heavy
@@ -585,15 +712,16 @@ __global__ __launch_bounds__(NT) void k_gen(Problem P, SearchArgs S, int g) {
     Info info = Dir<FWD>::info(P, key);
     u1 = one_unit ? u0 + 1 : Dir<FWD>::units(info);
     for (int depth = 0;; ++depth) {
-      uint32_t cont = NO_KEY;
-      Info ci = info;
+      Next<FWD> nk;
+      nk.key = NO_KEY;
       for (uint32_t u = u0; u < u1; ++u)
-        Dir<FWD>::unit(P, info, u,
-                       [&](uint32_t v, bool hot) { visit<FWD>(P, S, nx, v, hot, cont, ci, depth); });
-      if (cont == NO_KEY) break;
-      info = ci;
+        for_unit<FWD>(P, info, u, [&](uint32_t v, bool hot, bool uniq) {
+          visit<FWD>(P, S, nx, v, hot, uniq, nk, depth);
+        });
+      if (nk.key == NO_KEY) break;
+      info = nk.info;
       u0 = 0;
-      u1 = Dir<FWD>::units(ci);
+      u1 = Dir<FWD>::units(info);
     }
   }
 }
@@ -625,16 +753,18 @@ __global__ __launch_bounds__(NT) void k_seed_forward(Problem P, SearchArgs S,
   const NextGen nx{&S.sc->G[0], 0u, 0u};
   for (ull i0 = (ull)blockIdx.x * NT; i0 < n; i0 += (ull)gridDim.x * NT) {
     const ull i = i0 + threadIdx.x;
-    uint32_t cont = NO_KEY, k = 0;
+    uint32_t k = 0;
     bool fresh = false;
-    Fwd ci;
+    Fwd ki;
     if (i < n) {
       k = make_key((uint32_t)la[i / nb], (uint32_t)lb[i % nb], 0u, P.shiftB);
       fresh = claim(P.vis, k);
-      ci = fwd_info(P, k);
+      ki = fwd_info(P, k);
     }
+    Next<true> nk;
+    nk.key = NO_KEY;
     // depth = chain_max: every light start key joins the frontier
-    place<true>(P, S, nx, fresh, k, ci, cont, ci, P.chain_max);
+    place<true>(P, S, nx, fresh, k, ki, nk, P.chain_max);
   }
 }
 
@@ -646,12 +776,13 @@ __global__ __launch_bounds__(NT) void k_seed_backward(Problem P, SearchArgs S,
   const NextGen nx{&S.sc->G[0], 0u, 0u};
   for (ull i0 = (ull)blockIdx.x * NT; i0 < n; i0 += (ull)gridDim.x * NT) {
     const ull i = i0 + threadIdx.x;
-    uint32_t cont = NO_KEY;
     const bool valid = i < n;
     const uint32_t k = valid ? list[i] : 0u;
-    Bwd ci;
-    if (valid) ci = bwd_info(P, k);
-    place<false>(P, S, nx, valid, k, ci, cont, ci, P.chain_max);
+    Bwd ki;
+    if (valid) ki = bwd_info(P, k);
+    Next<false> nk;
+    nk.key = NO_KEY;
+    place<false>(P, S, nx, valid, k, ki, nk, P.chain_max);
   }
 }
 
@@ -669,7 +800,7 @@ __global__ __launch_bounds__(NT) void k_count_moves(Problem P, ull nwords,
     if (!test_bit(bm, (uint32_t)k)) continue;
     const typename Dir<FWD>::Info s = Dir<FWD>::info(P, (uint32_t)k);
     const uint32_t nu = Dir<FWD>::units(s);
-    for (uint32_t u = 0; u < nu; ++u) Dir<FWD>::unit(P, s, u, [&](uint32_t, bool) { ++c; });
+    for (uint32_t u = 0; u < nu; ++u) for_unit<FWD>(P, s, u, [&](uint32_t, bool, bool) { ++c; });
   }
   const ull tot = block_sum(c, s_w);
   if (threadIdx.x == 0 && tot) atomicAdd(out, tot);
@@ -684,6 +815,13 @@ __global__ __launch_bounds__(NT) void k_popcount(const uint32_t *__restrict__ bm
     c += (ull)__popc(bm[w]);
   const ull tot = block_sum(c, s_w);
   if (threadIdx.x == 0 && tot) atomicAdd(out, tot);
+}
+
+// a[w] &= b[w]: drops co-accessible bits of keys that are not accessible.
+__global__ __launch_bounds__(NT) void k_and_words(uint32_t *__restrict__ a,
+                                                  const uint32_t *__restrict__ b, ull nwords) {
+  for (ull w = (ull)blockIdx.x * NT + threadIdx.x; w < nwords; w += (ull)gridDim.x * NT)
+    a[w] &= b[w];
 }
 
 // ---------------------------------------------------------------------------
@@ -725,11 +863,11 @@ __device__ __forceinline__ void enum_light(const Problem &P, const Fwd &s, Visit
   const uint32_t sh = P.shiftB;
   for (int32_t p = s.aS; p < s.aS + (int32_t)s.eA; ++p) {
     const int32_t ea = P.aOut.perm[p];
-    vis(make_key((uint32_t)P.aOut.arec[p].y, s.qb, 0u, sh), P.A.il[ea], 0, P.A.w[ea], ea, -1);
+    vis(make_key(nbr_of(P.aOut.arec[p].y), s.qb, 0u, sh), P.A.il[ea], 0, P.A.w[ea], ea, -1);
   }
   for (int32_t p = s.bS; p < s.bS + s.be; ++p) {
     const int32_t eb = P.bOut.perm[p];
-    vis(make_key(s.qa, (uint32_t)P.bOut.arec[p].y, s.epsA, sh), 0, P.B.ol[eb], P.B.w[eb], -1, eb);
+    vis(make_key(s.qa, nbr_of(P.bOut.arec[p].y), s.epsA, sh), 0, P.B.ol[eb], P.B.w[eb], -1, eb);
   }
   if (!s.mU) return;
   if (s.nA <= s.nB) {
@@ -743,12 +881,12 @@ __device__ __forceinline__ void enum_light(const Problem &P, const Fwd &s, Visit
       if (lo < hi) bl = hi;
       for (int32_t pa = p; pa < pend && lo < hi; ++pa) {
         const int32_t ea = P.aOut.perm[pa];
-        const uint32_t da = (uint32_t)P.aOut.arec[pa].y;
+        const uint32_t da = nbr_of(P.aOut.arec[pa].y);
         const int32_t ia = P.A.il[ea];
         const float wa = P.A.w[ea];
         for (int32_t pb = lo; pb < hi; ++pb) {
           const int32_t eb = P.bOut.perm[pb];
-          vis(make_key(da, (uint32_t)P.bOut.arec[pb].y, 0u, sh), ia, P.B.ol[eb], wa + P.B.w[eb],
+          vis(make_key(da, nbr_of(P.bOut.arec[pb].y), 0u, sh), ia, P.B.ol[eb], wa + P.B.w[eb],
               ea, eb);
         }
       }
@@ -765,12 +903,12 @@ __device__ __forceinline__ void enum_light(const Problem &P, const Fwd &s, Visit
       if (lo < hi) al = hi;
       for (int32_t pa = lo; pa < hi; ++pa) {
         const int32_t ea = P.aOut.perm[pa];
-        const uint32_t da = (uint32_t)P.aOut.arec[pa].y;
+        const uint32_t da = nbr_of(P.aOut.arec[pa].y);
         const int32_t ia = P.A.il[ea];
         const float wa = P.A.w[ea];
         for (int32_t pb = p; pb < pend; ++pb) {
           const int32_t eb = P.bOut.perm[pb];
-          vis(make_key(da, (uint32_t)P.bOut.arec[pb].y, 0u, sh), ia, P.B.ol[eb], wa + P.B.w[eb],
+          vis(make_key(da, nbr_of(P.bOut.arec[pb].y), 0u, sh), ia, P.B.ol[eb], wa + P.B.w[eb],
               ea, eb);
         }
       }
@@ -797,7 +935,7 @@ __device__ __forceinline__ void put_arc(const OutGraph &O, const Problem &P, uin
 template <bool FILL>
 __device__ uint32_t heavy_state(const Problem &P, uint32_t id, uint32_t key, uint32_t pos0,
                                 const OutGraph &O, uint32_t *s_w) {
-  const Fwd s = fwd_info(P, key);
+  const Fwd s = fwd_info<false>(P, key);
   const uint32_t sh = P.shiftB;
   const unsigned t = threadIdx.x;
   uint32_t run = 0;
@@ -808,7 +946,7 @@ __device__ uint32_t heavy_state(const Problem &P, uint32_t id, uint32_t key, uin
     uint32_t d = 0;
     if (i < s.eA) {
       ea = P.aOut.perm[s.aS + (int32_t)i];
-      d = make_key((uint32_t)P.aOut.arec[s.aS + (int32_t)i].y, s.qb, 0u, sh);
+      d = make_key(nbr_of(P.aOut.arec[s.aS + (int32_t)i].y), s.qb, 0u, sh);
       keep = test_bit(P.coacc, d);
     }
     uint32_t tot;
@@ -823,7 +961,7 @@ __device__ uint32_t heavy_state(const Problem &P, uint32_t id, uint32_t key, uin
     uint32_t d = 0;
     if (i < (uint32_t)s.be) {
       eb = P.bOut.perm[s.bS + (int32_t)i];
-      d = make_key(s.qa, (uint32_t)P.bOut.arec[s.bS + (int32_t)i].y, s.epsA, sh);
+      d = make_key(s.qa, nbr_of(P.bOut.arec[s.bS + (int32_t)i].y), s.epsA, sh);
       keep = test_bit(P.coacc, d);
     }
     uint32_t tot;
@@ -842,10 +980,10 @@ __device__ uint32_t heavy_state(const Problem &P, uint32_t id, uint32_t key, uin
         const int32_t pa = s.aS + s.ae + (int32_t)i;
         const int2 ar = P.aOut.arec[pa];
         ea = P.aOut.perm[pa];
-        da = (uint32_t)ar.y;
+        da = nbr_of(ar.y);
         label_range(P.bOut, s.qb, s.bS + s.be, s.bE, ar.x, lo, hi);
         for (int32_t pb = lo; pb < hi; ++pb)
-          kept += test_bit(P.coacc, make_key(da, (uint32_t)P.bOut.arec[pb].y, 0u, sh));
+          kept += test_bit(P.coacc, make_key(da, nbr_of(P.bOut.arec[pb].y), 0u, sh));
       }
       uint32_t tot;
       uint32_t ex = block_excl_scan<uint32_t>(kept, s_w, tot);
@@ -855,7 +993,7 @@ __device__ uint32_t heavy_state(const Problem &P, uint32_t id, uint32_t key, uin
         uint32_t pos = pos0 + run + ex;
         for (int32_t pb = lo; pb < hi; ++pb) {
           const int32_t eb = P.bOut.perm[pb];
-          const uint32_t d = make_key(da, (uint32_t)P.bOut.arec[pb].y, 0u, sh);
+          const uint32_t d = make_key(da, nbr_of(P.bOut.arec[pb].y), 0u, sh);
           if (test_bit(P.coacc, d))
             put_arc(O, P, pos++, id, d, ia, P.B.ol[eb], wa + P.B.w[eb], ea, eb);
         }
@@ -873,7 +1011,7 @@ __global__ __launch_bounds__(NT) void k_count(Problem P, const uint32_t *__restr
     const ull id = i0 + threadIdx.x;
     bool hv = false;
     if (id < n) {
-      const Fwd s = fwd_info(P, key_of[id]);
+      const Fwd s = fwd_info<false>(P, key_of[id]);
       uint32_t c = 0;
       if (out_units(s) > LIGHT_UNITS) {
         hv = true;
@@ -913,7 +1051,7 @@ __global__ __launch_bounds__(NT) void k_fill_light(Problem P, const uint32_t *__
                                                    uint32_t n, const uint32_t *__restrict__ arc_off,
                                                    OutGraph O) {
   for (ull id = (ull)blockIdx.x * NT + threadIdx.x; id < n; id += (ull)gridDim.x * NT) {
-    const Fwd s = fwd_info(P, key_of[id]);
+    const Fwd s = fwd_info<false>(P, key_of[id]);
     if (out_units(s) > LIGHT_UNITS) continue;
     uint32_t pos = arc_off[id];
     const uint32_t sid = (uint32_t)id;
@@ -966,11 +1104,10 @@ hipError_t launch_validate(const DevGraph &g, int side, uint32_t *err, uint32_t 
   return hipGetLastError();
 }
 
-hipError_t build_view(const DevGraph &g, int side, bool by_dst, int lab_bits, int32_t lab_max,
-                      int4 *srec, int2 *arec, int32_t *perm, int4 *lut, int32_t *off_tmp,
-                      const int4 *eps_rec, unsigned long long *k0, int32_t *v0,
-                      unsigned long long *k1, int32_t *v1, void *sort_temp, uint32_t *eps_states,
-                      hipStream_t s) {
+hipError_t sort_view(const DevGraph &g, int side, bool by_dst, int lab_bits, int4 *srec,
+                     int2 *arec, int32_t *perm, int32_t *off_tmp, const int4 *eps_rec,
+                     unsigned long long *k0, int32_t *v0, unsigned long long *k1, int32_t *v1,
+                     void *sort_temp, uint32_t *eps_states, hipStream_t s) {
   const size_t E = (size_t)g.E;
   hipError_t e;
   if (E) {
@@ -991,14 +1128,38 @@ hipError_t build_view(const DevGraph &g, int side, bool by_dst, int lab_bits, in
   }
   if (g.V) {
     const int eps_mode = side == 1 ? 0 : (by_dst ? 2 : 1);
-    k_state_rec<<<grid_for((size_t)g.V, 256), NT, 0, s>>>(off, arec, g.V, g.accept, eps_mode,
+    k_state_rec<<<grid_for((size_t)g.V, 256), NT, 0, s>>>(off, arec, g.V, g.accept,
+                                                          by_dst ? nullptr : g.start, eps_mode,
                                                           eps_rec, srec, eps_states);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    if (lut) {
-      const size_t n = (size_t)g.V * (size_t)(lab_max + 1);
-      k_build_lut<<<grid_for(n, 8192), NT, 0, s>>>(srec, arec, g.V, lab_max + 1, lut);
-      if ((e = hipGetLastError()) != hipSuccess) return e;
-    }
+  }
+  return hipSuccess;
+}
+
+hipError_t mark_unique(const DevGraph &g, int side, bool out_view, int4 *self,
+                       const int4 *other, const int2 *other_arec, hipStream_t s) {
+  if (!g.V) return hipSuccess;
+  // out-views exclude start states, in-views accepting states
+  k_mark_unique<<<grid_for((size_t)g.V), NT, 0, s>>>(g.V, side, out_view ? 1 : 0,
+                                                     out_view ? g.start : g.accept, self, other,
+                                                     other_arec);
+  return hipGetLastError();
+}
+
+hipError_t finish_view(const DevGraph &g, int32_t lab_max, int4 *srec, int2 *arec, int4 *lut,
+                       hipStream_t s) {
+  hipError_t e;
+  if (g.E) {
+    k_mark_arcs<<<grid_for((size_t)g.E), NT, 0, s>>>(arec, srec, (long long)g.E);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  if (!g.V) return hipSuccess;
+  k_state_inline<<<grid_for((size_t)g.V, 256), NT, 0, s>>>(srec, arec, g.V);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (lut) {
+    const size_t n = (size_t)g.V * (size_t)(lab_max + 1);
+    k_build_lut<<<grid_for(n, 8192), NT, 0, s>>>(srec, arec, g.V, lab_max + 1, lut);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   return hipSuccess;
 }
@@ -1040,6 +1201,12 @@ hipError_t launch_popcount(const uint32_t *bm, size_t nwords, unsigned long long
                            hipStream_t s) {
   if (!nwords) return hipSuccess;
   k_popcount<<<grid_for(nwords, 256), NT, 0, s>>>(bm, nwords, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_and_words(uint32_t *a, const uint32_t *b, size_t nwords, hipStream_t s) {
+  if (!nwords) return hipSuccess;
+  k_and_words<<<grid_for(nwords, 8192), NT, 0, s>>>(a, b, nwords);
   return hipGetLastError();
 }
 

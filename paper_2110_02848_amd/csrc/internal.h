@@ -33,12 +33,27 @@ struct DevGraph {
 // Arcs grouped by a state (their source for out-views, their destination for
 // in-views) and sorted inside each group by the matched label, ties by arc id.
 // Label 0 (epsilon) sorts first, so a group starts with its epsilon arcs.
-//   srec[v] = {group begin, epsilon arcs, group end, flags}: bit 0 of flags is
-//             accept(v); in views of A, bit 1 is epsOutA(v) (v has an
-//             out-arc with output epsilon).
+//   srec[2v]   = {group begin, epsilon arcs, group end, flags}: FLAG_ACCEPT
+//                is accept(v); in views of A, FLAG_EPS_OUT is epsOutA(v) (v
+//                has an out-arc with output epsilon); in out-views
+//                FLAG_START is start(v); FLAG_UNIQ, see below.
+//   srec[2v+1] = {other end of the group's first epsilon arc, label and
+//                other end of its first non-epsilon arc, 0} (arec fields,
+//                0 where there is no such arc): the 32-byte record of a
+//                state with one arc of a kind resolves that arc without an
+//                arc-record load.
 //   arec[i] = {matched label, other end}: the destination in out-views, the
-//             source in in-views; in A's in-view bit 31 of the source field
-//             carries epsOutA(source).
+//             source in in-views (NBR_MASK bits); NBR_UNIQ is the other end's
+//             FLAG_UNIQ in this view; in A's in-view NBR_EPS carries
+//             epsOutA(source).
+//   FLAG_UNIQ in an out-view marks a state that guarantees any key holding
+//   it has at most one incoming move (in B: not a start state and exactly
+//   one in-arc; in A: not a start state, no epsilon output, and in-arcs with
+//   distinct non-epsilon output labels from states without epsilon output).
+//   In an in-view it marks at most one outgoing move (in B: not accepting,
+//   exactly one out-arc; in A: not accepting, out-arcs with distinct
+//   non-epsilon output labels).  A key whose two states are both marked is
+//   reached once by a search in that direction, so it needs no claim.
 //   perm[i] = original arc id.
 //   lut, when present, holds every group's label buckets:
 //             lut[v * lstride + l] = {begin, end, other end of the first arc,
@@ -52,8 +67,10 @@ struct View {
   int32_t lstride;  // largest label + 1
 };
 
-constexpr uint32_t FLAG_ACCEPT = 1u, FLAG_EPS_OUT = 2u;
-constexpr int32_t NBR_MASK = 0x7fffffff;
+constexpr uint32_t FLAG_ACCEPT = 1u, FLAG_EPS_OUT = 2u, FLAG_START = 4u, FLAG_UNIQ = 8u;
+constexpr int32_t NBR_MASK = 0x3fffffff;            // state ids < 2^30
+constexpr int32_t NBR_UNIQ = 0x40000000;
+constexpr int32_t NBR_EPS = (int32_t)0x80000000u;
 
 // Everything a search / compaction kernel needs, passed by value.
 struct Problem {
@@ -244,18 +261,27 @@ hipError_t radix_sort(unsigned long long *k0, int32_t *v0, unsigned long long *k
 // ---------------------------------------------------------------------------
 hipError_t launch_validate(const DevGraph &g, int side, uint32_t *err, uint32_t *maxlab,
                            hipStream_t s);
-// Build a label-sorted view (side 0: A by olabel, side 1: B by ilabel);
-// by_dst selects in-views, for which `off_tmp` (V+1 words) receives the group
-// offsets.  k0/v0/k1/v1 are E-sized sort buffers.  eps_rec is A's out-view
-// records when building A's in-view (to carry epsOutA), else null.  If
-// eps_states is set, it counts the states with an epsilon arc in the view.
-// If lut is set, the label buckets of every group are written there
+// Views are built in three steps.  sort_view: sort the arcs of a view (side
+// 0: A by olabel, side 1: B by ilabel; by_dst selects in-views, for which
+// `off_tmp` (V+1 words) receives the group offsets) into arec / perm and
+// write the first record of every state.  k0/v0/k1/v1 are E-sized sort
+// buffers.  eps_rec is A's out-view records when building A's in-view (to
+// carry epsOutA), else null.  If eps_states is set, it counts the states with
+// an epsilon arc in the view.  Then mark_unique (once all four views are
+// sorted) sets FLAG_UNIQ; then finish_view marks the arcs, writes the second
+// record of every state and, if lut is set, the label buckets of every group
 // (V * (lab_max + 1) entries).
-hipError_t build_view(const DevGraph &g, int side, bool by_dst, int lab_bits, int32_t lab_max,
-                      int4 *srec, int2 *arec, int32_t *perm, int4 *lut, int32_t *off_tmp,
-                      const int4 *eps_rec, unsigned long long *k0, int32_t *v0,
-                      unsigned long long *k1, int32_t *v1, void *sort_temp, uint32_t *eps_states,
-                      hipStream_t s);
+hipError_t sort_view(const DevGraph &g, int side, bool by_dst, int lab_bits, int4 *srec,
+                     int2 *arec, int32_t *perm, int32_t *off_tmp, const int4 *eps_rec,
+                     unsigned long long *k0, int32_t *v0, unsigned long long *k1, int32_t *v1,
+                     void *sort_temp, uint32_t *eps_states, hipStream_t s);
+// FLAG_UNIQ for the records `self` of a view of graph g, from the groups of
+// the opposite view of the same graph (`other`, `other_arec`): side 0 = A,
+// side 1 = B; out_view says whether `self` is an out-view.
+hipError_t mark_unique(const DevGraph &g, int side, bool out_view, int4 *self,
+                       const int4 *other, const int2 *other_arec, hipStream_t s);
+hipError_t finish_view(const DevGraph &g, int32_t lab_max, int4 *srec, int2 *arec, int4 *lut,
+                       hipStream_t s);
 // Collect the start states of A and B into la/lb (counts na/nb, zeroed by the
 // caller) and place every start key in generation 0 of the forward search.
 // Accepting keys reached by the forward search (start keys included) are
@@ -277,6 +303,8 @@ hipError_t launch_count_moves(const Problem &P, size_t nwords, bool forward,
 // *out += number of set bits of bm[0, nwords).
 hipError_t launch_popcount(const uint32_t *bm, size_t nwords, unsigned long long *out,
                            hipStream_t s);
+// a[w] &= b[w] for w < nwords.
+hipError_t launch_and_words(uint32_t *a, const uint32_t *b, size_t nwords, hipStream_t s);
 hipError_t launch_popc_words(const uint32_t *bm, uint32_t *cnt, size_t nwords, hipStream_t s);
 hipError_t launch_key_of_id(const uint32_t *bm, const uint32_t *wbase, size_t nwords,
                             uint32_t *key_of, hipStream_t s);

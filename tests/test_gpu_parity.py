@@ -104,6 +104,50 @@ def _hub_pair():
     return A, B
 
 
+def _sparse_chain_graph(rng, V, n_sym, p_eps, p_par):
+    """Mostly one arc in and one arc out per state (the shape for which
+    searches skip claims), with random extra arcs, parallel same-label arcs,
+    epsilon labels, cycles back to start states and accepting states with
+    out-arcs, so every condition that disables the shortcut occurs."""
+    arcs = []
+    lab = lambda: 0 if rng.random() < p_eps else int(rng.integers(1, n_sym + 1))
+    for s in range(V):
+        d = (s + 1) % V if rng.random() < 0.8 else int(rng.integers(0, V))
+        il, ol = lab(), lab()
+        arcs.append((s, d, il, ol, float(np.float32(rng.standard_normal()))))
+        if rng.random() < p_par:  # parallel arc with the same labels
+            arcs.append((s, d, il, ol, float(np.float32(rng.standard_normal()))))
+        if rng.random() < 0.2:
+            arcs.append((s, int(rng.integers(0, V)), lab(), lab(), 0.5))
+    starts = [0] + [int(x) for x in rng.integers(0, V, size=int(rng.integers(0, 3)))]
+    accepts = [int(x) for x in rng.integers(0, V, size=int(rng.integers(1, V // 3 + 2)))]
+    return synth.from_arcs(V, arcs, start=sorted(set(starts)), accept=sorted(set(accepts)))
+
+
+@pytest.mark.parametrize("seed", range(60))
+def test_unique_move_chains(comp, seed):
+    rng = np.random.default_rng([77, seed])
+    V = int(rng.integers(3, 40))
+    n_sym = 1 + (seed % 4 == 3)
+    A = _sparse_chain_graph(rng, V, n_sym, [0.0, 0.2, 0.5][seed % 3], 0.1)
+    B = _sparse_chain_graph(rng, int(rng.integers(3, 40)), n_sym, [0.3, 0.0, 0.1][seed % 3], 0.1)
+    got, _ = check_pair(comp, A, B, f"unique-move chains seed {seed}")
+    assert not fsthelp.check_invariants(A, B, got)
+
+
+def test_unique_move_corner_cases(comp):
+    # a start state that a move also reaches; an accepting state that also
+    # has an out-move; an A state whose in-arc comes from a state with an
+    # epsilon output (two filter states lead to its key)
+    A = synth.from_arcs(4, [(0, 1, 1, 1, 0.5), (1, 2, 2, 2, 0.25), (2, 0, 3, 3, 1.0),
+                            (2, 3, 1, 0, 2.0), (3, 1, 1, 1, 0.125)], start=[0], accept=[0, 3])
+    B = synth.from_arcs(3, [(0, 1, 1, 5, 0.5), (1, 2, 2, 6, 0.0), (2, 0, 3, 7, 1.5),
+                            (0, 0, 0, 8, 0.75)], start=[0], accept=[0, 2])
+    for X, Y, tag in ((A, B, "A o B"), (B, A, "B o A"), (A, A, "A o A"), (B, B, "B o B")):
+        got, _ = check_pair(comp, X, Y, f"corner {tag}")
+        assert not fsthelp.check_invariants(X, Y, got)
+
+
 def test_heavy_states(comp):
     A, B = _hub_pair()
     got, _ = check_pair(comp, A, B, "hub states")
