@@ -174,7 +174,8 @@ FST_API int fst_compose_phase_times(const fst_ctx *ctx, float *ms, int n);
 /* Kernels timed with FST_OPT_TIMING on: every launch of the forward search
  * kernel; every launch of the backward search kernel; the arc-count kernels
  * (states with few moves, then states with many: 2 launches, 1 if C is
- * empty); the fill kernels (light states, heavy states if any, state flags). */
+ * empty); the fill kernels (every state's offset and flags with the arcs of
+ * light states, then heavy states' arcs if any). */
 enum fst_kernel {
   FST_KERNEL_SEARCH_FORWARD = 0,
   FST_KERNEL_SEARCH_BACKWARD = 1,

@@ -44,8 +44,9 @@ struct fst_ctx {
   DevBuf scal, lists;
   DevBuf k0, k1, v0, v1, sort_tmp, scan_tmp;
   DevBuf aOutPerm, aOutArc, aOutRec, aOutLut, bOutPerm, bOutArc, bOutRec, bOutLut;
+  DevBuf aOutLab, aOutW, bOutLab, bOutW;
   DevBuf aInOff, aInPerm, aInArc, aInRec, aInLut, bInOff, bInPerm, bInArc, bInRec, bInLut;
-  DevBuf vis, coacc, wbase, fq, bq, heavy, hoff, cnt;
+  DevBuf vis, coacc, wbase, fq, bq, heavy, hoff, cnt, btot;
   Scalars *h_sc = nullptr;
   hipEvent_t ev[NEV] = {};
   hipEvent_t kev[2 * NKERNELS] = {};  // per timed kernel: before, after
@@ -55,6 +56,7 @@ struct fst_ctx {
   bool ready = false;
   Problem P = {};
   uint32_t nstates = 0, narcs = 0, nheavy = 0;
+  size_t out_per = NT;  // states per workgroup in the output passes
   fst_stats stats = {};
 };
 
@@ -256,18 +258,20 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   const bool lutA = c->buckets && lut_bytes(VA, maxA) <= LUT_BUDGET;
   const bool lutB = c->buckets && lut_bytes(VB, maxB) <= LUT_BUDGET;
   struct ViewBufs {
-    DevBuf *perm, *arc, *rec, *lut, *off;
+    DevBuf *perm, *arc, *rec, *lut, *off, *lab, *w;
   };
   // built in this order: A's in-view needs A's out-view records
-  const ViewBufs vb[4] = {{&c->aOutPerm, &c->aOutArc, &c->aOutRec, &c->aOutLut, nullptr},
-                          {&c->bOutPerm, &c->bOutArc, &c->bOutRec, &c->bOutLut, nullptr},
-                          {&c->aInPerm, &c->aInArc, &c->aInRec, &c->aInLut, &c->aInOff},
-                          {&c->bInPerm, &c->bInArc, &c->bInRec, &c->bInLut, &c->bInOff}};
+  const ViewBufs vb[4] = {
+      {&c->aOutPerm, &c->aOutArc, &c->aOutRec, &c->aOutLut, nullptr, &c->aOutLab, &c->aOutW},
+      {&c->bOutPerm, &c->bOutArc, &c->bOutRec, &c->bOutLut, nullptr, &c->bOutLab, &c->bOutW},
+      {&c->aInPerm, &c->aInArc, &c->aInRec, &c->aInLut, &c->aInOff, nullptr, nullptr},
+      {&c->bInPerm, &c->bInArc, &c->bInRec, &c->bInLut, &c->bInOff, nullptr, nullptr}};
   unsigned long long *k0 = as<unsigned long long>(c->k0), *k1 = as<unsigned long long>(c->k1);
   int32_t *v0 = as<int32_t>(c->v0), *v1 = as<int32_t>(c->v1);
   int4 *rec[4], *lutp[4];
   int2 *arc[4];
-  int32_t *perm[4];
+  int32_t *perm[4], *olab[4];
+  float *wv[4];
   for (int i = 0; i < 4; ++i) {
     const bool isA = (i % 2) == 0, in = i >= 2;
     const DevGraph &g = isA ? dA : dB;
@@ -277,6 +281,14 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
     FST_TRY(ensure(c, *vb[i].rec, (size_t)g.V * 2 * sizeof(int4)));
     if (lut) FST_TRY(ensure(c, *vb[i].lut, lut_bytes(g.V, isA ? maxA : maxB)));
     if (in) FST_TRY(ensure(c, *vb[i].off, ((size_t)g.V + 1) * sizeof(int32_t)));
+    olab[i] = nullptr;
+    wv[i] = nullptr;
+    if (!in) {
+      FST_TRY(ensure(c, *vb[i].lab, (size_t)g.E * sizeof(int32_t)));
+      FST_TRY(ensure(c, *vb[i].w, (size_t)g.E * sizeof(float)));
+      olab[i] = as<int32_t>(*vb[i].lab);
+      wv[i] = as<float>(*vb[i].w);
+    }
     rec[i] = as<int4>(*vb[i].rec);
     arc[i] = as<int2>(*vb[i].arc);
     perm[i] = as<int32_t>(*vb[i].perm);
@@ -285,8 +297,9 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   for (int i = 0; i < 4; ++i) {
     const bool isA = (i % 2) == 0, in = i >= 2;
     HIP_TRY(sort_view(isA ? dA : dB, isA ? 0 : 1, in, isA ? labA : labB, rec[i], arc[i], perm[i],
-                      in ? as<int32_t>(*vb[i].off) : nullptr, i == 2 ? rec[0] : nullptr, k0, v0,
-                      k1, v1, c->sort_tmp.p, i == 0 ? &d_sc->nEpsStatesA : nullptr, s));
+                      olab[i], wv[i], in ? as<int32_t>(*vb[i].off) : nullptr,
+                      i == 2 ? rec[0] : nullptr, k0, v0, k1, v1, c->sort_tmp.p,
+                      i == 0 ? &d_sc->nEpsStatesA : nullptr, s));
   }
   // a view's FLAG_UNIQ comes from the opposite view of the same graph
   for (int i = 0; i < 4; ++i) {
@@ -298,7 +311,7 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
     const bool isA = (i % 2) == 0;
     const uint32_t lmax = isA ? maxA : maxB;
     HIP_TRY(finish_view(isA ? dA : dB, (int32_t)lmax, rec[i], arc[i], lutp[i], s));
-    views[i] = View{rec[i], arc[i], perm[i], lutp[i], (int32_t)lmax + 1};
+    views[i] = View{rec[i], arc[i], perm[i], lutp[i], (int32_t)lmax + 1, olab[i], wv[i]};
   }
   FST_TRY(readback(c, s));
 
@@ -359,14 +372,14 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   HIP_TRY(launch_seed_backward(P, S, bq, s));
   FST_TRY(search(c, S, false, &c->stats.bwd_levels, s));
   // the backward search may set co-accessible bits of keys it never expands
-  // (not accessible); the trim set is what remains after masking them
-  HIP_TRY(launch_and_words(P.coacc, P.vis, nwords, s));
+  // (not accessible); the trim set is what remains after masking them, and
+  // the same pass counts the trim keys of every bitmap word
+  uint32_t *wbase = as<uint32_t>(c->wbase);
+  HIP_TRY(launch_trim_words(P.coacc, P.vis, wbase, nwords, s));
   if (c->count_moves) HIP_TRY(launch_count_moves(P, nwords, false, &d_sc->generated_bwd, s));
 
   // ---- numbering and arc counts ----
   mark(c, 3, s);
-  uint32_t *wbase = as<uint32_t>(c->wbase);
-  HIP_TRY(launch_popc_words(P.coacc, wbase, nwords, s));
   HIP_TRY(scan_u32(wbase, wbase, nwords, false, &d_sc->total, c->scan_tmp.p, s));
   FST_TRY(readback(c, s));
   const unsigned long long nst = c->h_sc->total;
@@ -376,14 +389,19 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   uint32_t *heavy = bq;    // so is the backward queue
   HIP_TRY(launch_key_of_id(P.coacc, wbase, nwords, key_of, s));
   FST_TRY(ensure(c, c->cnt, ((size_t)nstates + 1) * 4));
-  uint32_t *cnt = as<uint32_t>(c->cnt);
+  FST_TRY(ensure(c, c->btot, (OUT_BLOCKS + 1) * 4));
+  uint32_t *cnt = as<uint32_t>(c->cnt), *btot = as<uint32_t>(c->btot);
+  const size_t per = out_chunk(nstates);
   HIP_TRY(hipMemsetAsync(&d_sc->heavy, 0, sizeof(uint32_t), s));
+  HIP_TRY(hipMemsetAsync(&d_sc->total, 0, sizeof(unsigned long long), s));
   const KernelTimer tc = timer(c, FST_KERNEL_COUNT);
   tc.begin(s);
-  HIP_TRY(launch_count(P, key_of, nstates, cnt, heavy, d_sc, s));
-  HIP_TRY(launch_count_heavy(P, key_of, heavy, &d_sc->heavy, cnt, s));
+  HIP_TRY(launch_count(P, key_of, nstates, per, cnt, btot, heavy, d_sc, s));
+  HIP_TRY(launch_count_heavy(P, key_of, heavy, &d_sc->heavy, per, cnt, btot, s));
   tc.end(s);
-  HIP_TRY(scan_u32(cnt, cnt, nstates, false, &d_sc->total, c->scan_tmp.p, s));
+  // exclusive arc offset of every chunk; the total is E_C
+  if (nstates)
+    HIP_TRY(scan_u32(btot, btot, out_grid(nstates, per), false, &d_sc->total, c->scan_tmp.p, s));
   mark(c, 4, s);
   FST_TRY(readback(c, s));
   const unsigned long long narcs = c->h_sc->total;
@@ -391,6 +409,7 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   FST_TRY(add_time(c, FST_KERNEL_COUNT, nstates ? 2 : 1));
 
   c->nstates = nstates;
+  c->out_per = per;
   c->narcs = (uint32_t)narcs;
   c->nheavy = c->h_sc->heavy;
   c->stats.accessible = (int64_t)c->h_sc->naccessible;
@@ -458,7 +477,8 @@ void fst_ctx_destroy(fst_ctx *c) {
                     &c->bOutLut,  &c->aInOff,   &c->aInPerm, &c->aInArc,  &c->aInRec,
                     &c->aInLut,   &c->bInOff,   &c->bInPerm, &c->bInArc,  &c->bInRec,
                     &c->bInLut,   &c->vis,      &c->coacc,   &c->wbase,   &c->fq,
-                    &c->bq,       &c->heavy,    &c->hoff,    &c->cnt};
+                    &c->bq,       &c->heavy,    &c->hoff,    &c->cnt,     &c->aOutLab,
+                    &c->aOutW,    &c->bOutLab,  &c->bOutW,   &c->btot};
   for (DevBuf *b : bufs) release(*b);
   for (int i = 0; i < NEV; ++i)
     if (c->ev[i]) (void)hipEventDestroy(c->ev[i]);
@@ -541,11 +561,12 @@ int fst_compose_fill(fst_ctx *c, const fst_graph_out *C, void *stream) {
   mark(c, 5, s);
   const KernelTimer tf = c->timed_run ? timer(c, FST_KERNEL_FILL) : KernelTimer{};
   tf.begin(s);
-  hipError_t e = launch_fill(c->P, as<uint32_t>(c->fq), c->nstates, as<uint32_t>(c->cnt),
-                             as<uint32_t>(c->bq), c->nheavy, c->narcs, O, s);
+  hipError_t e = launch_fill(c->P, as<uint32_t>(c->fq), c->nstates, c->out_per,
+                             as<uint32_t>(c->cnt), as<uint32_t>(c->btot), as<uint32_t>(c->bq),
+                             c->nheavy, c->narcs, O, s);
   tf.end(s);
-  // light-state fill (if any states), heavy-state fill (if any), flags
-  c->klaunches[FST_KERNEL_FILL] = c->timed_run ? (c->nstates ? 2 : 1) + (c->nheavy ? 1 : 0) : 0;
+  // per-state fill (offsets, flags, light states' arcs), heavy-state fill (if any)
+  c->klaunches[FST_KERNEL_FILL] = c->timed_run ? 1 + (c->nheavy ? 1 : 0) : 0;
   c->kms[FST_KERNEL_FILL] = 0.f;
   mark(c, 6, s);
   if (e != hipSuccess) {

@@ -126,13 +126,18 @@ __global__ __launch_bounds__(NT) void k_make_keys(DevGraph g, int side, int by_d
 __global__ __launch_bounds__(NT) void k_split(DevGraph g, int by_dst, const ull *__restrict__ k,
                                               const int32_t *__restrict__ v, long long n,
                                               int lab_bits, const int4 *__restrict__ eps_rec,
-                                              int32_t *__restrict__ perm,
+                                              int side, int32_t *__restrict__ perm,
+                                              int32_t *__restrict__ olab, float *__restrict__ wv,
                                               int2 *__restrict__ arec) {
   const ull mask = (lab_bits >= 64) ? ~0ull : ((1ull << lab_bits) - 1ull);
   for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n;
        i += (long long)gridDim.x * NT) {
     const int32_t e = v[i];
     perm[i] = e;
+    if (olab) {
+      olab[i] = side == 0 ? g.il[e] : g.ol[e];
+      wv[i] = g.w[e];
+    }
     int32_t nb = by_dst ? g.src[e] : g.dst[e];
     if (eps_rec && eps_rec[2 * (size_t)nb].y > 0) nb |= NBR_EPS;
     arec[i] = make_int2((int32_t)(k[i] & mask), nb);
@@ -345,6 +350,7 @@ struct Fwd {
   uint32_t epsA;    // epsOutA(qa)
   uint32_t accept;  // accept(qa) and accept(qb)
   uint32_t uqA, uqB;  // FLAG_UNIQ of qa, qb (out-views)
+  uint32_t start;     // a start key: f = 0, start(qa) and start(qb)
   int32_t e0A, e0B, l1A, n1A, l1B, n1B;
 };
 
@@ -378,6 +384,7 @@ __device__ __forceinline__ Fwd fwd_info(const Problem &P, uint32_t key) {
   s.accept = (uint32_t)(ra.w & rb.w) & FLAG_ACCEPT;
   s.uqA = (uint32_t)ra.w & FLAG_UNIQ;
   s.uqB = (uint32_t)rb.w & FLAG_UNIQ;
+  s.start = (s.f == 0 && (ra.w & rb.w & (int32_t)FLAG_START)) ? 1u : 0u;
   s.eA = s.f ? 0u : (uint32_t)s.ae;
   s.nA = (uint32_t)(s.aE - s.aS - s.ae);
   s.nB = (uint32_t)(s.bE - s.bS - s.be);
@@ -817,33 +824,36 @@ __global__ __launch_bounds__(NT) void k_popcount(const uint32_t *__restrict__ bm
   if (threadIdx.x == 0 && tot) atomicAdd(out, tot);
 }
 
-// a[w] &= b[w]: drops co-accessible bits of keys that are not accessible.
-__global__ __launch_bounds__(NT) void k_and_words(uint32_t *__restrict__ a,
-                                                  const uint32_t *__restrict__ b, ull nwords) {
-  for (ull w = (ull)blockIdx.x * NT + threadIdx.x; w < nwords; w += (ull)gridDim.x * NT)
-    a[w] &= b[w];
-}
-
 // ---------------------------------------------------------------------------
 // compaction
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(NT) void k_popc_words(const uint32_t *__restrict__ bm,
+
+// coacc[w] &= vis[w] (drops co-accessible bits of keys that are not
+// accessible), cnt[w] = popcount of the result.
+__global__ __launch_bounds__(NT) void k_trim_words(uint32_t *__restrict__ coacc,
+                                                   const uint32_t *__restrict__ vis,
                                                    uint32_t *__restrict__ cnt, ull nwords) {
-  for (ull w = (ull)blockIdx.x * NT + threadIdx.x; w < nwords; w += (ull)gridDim.x * NT)
-    cnt[w] = (uint32_t)__popc(bm[w]);
+  for (ull w = (ull)blockIdx.x * NT + threadIdx.x; w < nwords; w += (ull)gridDim.x * NT) {
+    const uint32_t m = coacc[w] & vis[w];
+    coacc[w] = m;
+    cnt[w] = (uint32_t)__popc(m);
+  }
 }
 
+// key_of[id] = the id-th trim key, one thread per key slot and one
+// contiguous chunk of `per` slots per workgroup, so the writes of a workgroup
+// are contiguous.
 __global__ __launch_bounds__(NT) void k_key_of_id(const uint32_t *__restrict__ bm,
                                                   const uint32_t *__restrict__ wbase,
-                                                  ull nwords, uint32_t *__restrict__ key_of) {
-  for (ull w = (ull)blockIdx.x * NT + threadIdx.x; w < nwords; w += (ull)gridDim.x * NT) {
-    uint32_t m = bm[w];
-    uint32_t id = wbase[w];
-    while (m) {
-      uint32_t b = (uint32_t)(__ffs(m) - 1);
-      key_of[id++] = (uint32_t)(w * 32u + b);
-      m &= m - 1u;
-    }
+                                                  ull nwords, ull per,
+                                                  uint32_t *__restrict__ key_of) {
+  const ull nkeys = nwords * 32u;
+  const ull begin = (ull)blockIdx.x * per;
+  const ull end = begin + per < nkeys ? begin + per : nkeys;
+  for (ull k = begin + threadIdx.x; k < end; k += NT) {
+    const uint32_t w = (uint32_t)(k >> 5), b = (uint32_t)(k & 31u);
+    const uint32_t m = bm[w];
+    if ((m >> b) & 1u) key_of[wbase[w] + (uint32_t)__popc(m & ((1u << b) - 1u))] = (uint32_t)k;
   }
 }
 
@@ -858,17 +868,16 @@ __device__ __forceinline__ uint32_t out_units(const Fwd &s) { return s.eA + (uin
 // arcs, B-epsilon arcs, then matching arcs by (label, a, b).  The join walks
 // the label groups of the side with fewer non-epsilon arcs and looks up the
 // other side's bucket; each group is emitted row-major (a outer, b inner).
+// vis(target key, ilabel, olabel, weight, position in A's out-view or -1,
+// position in B's out-view or -1).
 template <class Visit>
 __device__ __forceinline__ void enum_light(const Problem &P, const Fwd &s, Visit &&vis) {
   const uint32_t sh = P.shiftB;
-  for (int32_t p = s.aS; p < s.aS + (int32_t)s.eA; ++p) {
-    const int32_t ea = P.aOut.perm[p];
-    vis(make_key(nbr_of(P.aOut.arec[p].y), s.qb, 0u, sh), P.A.il[ea], 0, P.A.w[ea], ea, -1);
-  }
-  for (int32_t p = s.bS; p < s.bS + s.be; ++p) {
-    const int32_t eb = P.bOut.perm[p];
-    vis(make_key(s.qa, nbr_of(P.bOut.arec[p].y), s.epsA, sh), 0, P.B.ol[eb], P.B.w[eb], -1, eb);
-  }
+  for (int32_t p = s.aS; p < s.aS + (int32_t)s.eA; ++p)
+    vis(make_key(nbr_of(P.aOut.arec[p].y), s.qb, 0u, sh), P.aOut.olab[p], 0, P.aOut.w[p], p, -1);
+  for (int32_t p = s.bS; p < s.bS + s.be; ++p)
+    vis(make_key(s.qa, nbr_of(P.bOut.arec[p].y), s.epsA, sh), 0, P.bOut.olab[p], P.bOut.w[p], -1,
+        p);
   if (!s.mU) return;
   if (s.nA <= s.nB) {
     int32_t p = s.aS + s.ae, bl = s.bS + s.be;
@@ -880,15 +889,12 @@ __device__ __forceinline__ void enum_light(const Problem &P, const Fwd &s, Visit
       label_range(P.bOut, s.qb, bl, s.bE, lab, lo, hi);
       if (lo < hi) bl = hi;
       for (int32_t pa = p; pa < pend && lo < hi; ++pa) {
-        const int32_t ea = P.aOut.perm[pa];
         const uint32_t da = nbr_of(P.aOut.arec[pa].y);
-        const int32_t ia = P.A.il[ea];
-        const float wa = P.A.w[ea];
-        for (int32_t pb = lo; pb < hi; ++pb) {
-          const int32_t eb = P.bOut.perm[pb];
-          vis(make_key(da, nbr_of(P.bOut.arec[pb].y), 0u, sh), ia, P.B.ol[eb], wa + P.B.w[eb],
-              ea, eb);
-        }
+        const int32_t ia = P.aOut.olab[pa];
+        const float wa = P.aOut.w[pa];
+        for (int32_t pb = lo; pb < hi; ++pb)
+          vis(make_key(da, nbr_of(P.bOut.arec[pb].y), 0u, sh), ia, P.bOut.olab[pb],
+              wa + P.bOut.w[pb], pa, pb);
       }
       p = pend;
     }
@@ -902,31 +908,30 @@ __device__ __forceinline__ void enum_light(const Problem &P, const Fwd &s, Visit
       label_range(P.aOut, s.qa, al, s.aE, lab, lo, hi);
       if (lo < hi) al = hi;
       for (int32_t pa = lo; pa < hi; ++pa) {
-        const int32_t ea = P.aOut.perm[pa];
         const uint32_t da = nbr_of(P.aOut.arec[pa].y);
-        const int32_t ia = P.A.il[ea];
-        const float wa = P.A.w[ea];
-        for (int32_t pb = p; pb < pend; ++pb) {
-          const int32_t eb = P.bOut.perm[pb];
-          vis(make_key(da, nbr_of(P.bOut.arec[pb].y), 0u, sh), ia, P.B.ol[eb], wa + P.B.w[eb],
-              ea, eb);
-        }
+        const int32_t ia = P.aOut.olab[pa];
+        const float wa = P.aOut.w[pa];
+        for (int32_t pb = p; pb < pend; ++pb)
+          vis(make_key(da, nbr_of(P.bOut.arec[pb].y), 0u, sh), ia, P.bOut.olab[pb],
+              wa + P.bOut.w[pb], pa, pb);
       }
       p = pend;
     }
   }
 }
 
+// Write one arc of C; pa / pb are positions in the out-views (-1: none),
+// turned into arc ids only when provenance is requested.
 __device__ __forceinline__ void put_arc(const OutGraph &O, const Problem &P, uint32_t pos,
                                         uint32_t id, uint32_t dk, int32_t il, int32_t ol,
-                                        float w, int32_t ea, int32_t eb) {
+                                        float w, int32_t pa, int32_t pb) {
   O.src[pos] = (int32_t)id;
   O.dst[pos] = (int32_t)new_id(P, dk);
   O.il[pos] = il;
   O.ol[pos] = ol;
   O.w[pos] = w;
-  if (O.arc_a) O.arc_a[pos] = ea;
-  if (O.arc_b) O.arc_b[pos] = eb;
+  if (O.arc_a) O.arc_a[pos] = pa >= 0 ? P.aOut.perm[pa] : -1;
+  if (O.arc_b) O.arc_b[pos] = pb >= 0 ? P.bOut.perm[pb] : -1;
 }
 
 // Workgroup-cooperative canonical enumeration of one heavy state.  Every
@@ -942,31 +947,33 @@ __device__ uint32_t heavy_state(const Problem &P, uint32_t id, uint32_t key, uin
   for (uint32_t c = 0; c < s.eA; c += NT) {
     const uint32_t i = c + t;
     bool keep = false;
-    int32_t ea = 0;
+    int32_t pa = 0;
     uint32_t d = 0;
     if (i < s.eA) {
-      ea = P.aOut.perm[s.aS + (int32_t)i];
-      d = make_key(nbr_of(P.aOut.arec[s.aS + (int32_t)i].y), s.qb, 0u, sh);
+      pa = s.aS + (int32_t)i;
+      d = make_key(nbr_of(P.aOut.arec[pa].y), s.qb, 0u, sh);
       keep = test_bit(P.coacc, d);
     }
     uint32_t tot;
     uint32_t ex = block_excl_scan<uint32_t>(keep ? 1u : 0u, s_w, tot);
-    if (FILL && keep) put_arc(O, P, pos0 + run + ex, id, d, P.A.il[ea], 0, P.A.w[ea], ea, -1);
+    if (FILL && keep)
+      put_arc(O, P, pos0 + run + ex, id, d, P.aOut.olab[pa], 0, P.aOut.w[pa], pa, -1);
     run += tot;
   }
   for (uint32_t c = 0; c < (uint32_t)s.be; c += NT) {
     const uint32_t i = c + t;
     bool keep = false;
-    int32_t eb = 0;
+    int32_t pb = 0;
     uint32_t d = 0;
     if (i < (uint32_t)s.be) {
-      eb = P.bOut.perm[s.bS + (int32_t)i];
-      d = make_key(s.qa, nbr_of(P.bOut.arec[s.bS + (int32_t)i].y), s.epsA, sh);
+      pb = s.bS + (int32_t)i;
+      d = make_key(s.qa, nbr_of(P.bOut.arec[pb].y), s.epsA, sh);
       keep = test_bit(P.coacc, d);
     }
     uint32_t tot;
     uint32_t ex = block_excl_scan<uint32_t>(keep ? 1u : 0u, s_w, tot);
-    if (FILL && keep) put_arc(O, P, pos0 + run + ex, id, d, 0, P.B.ol[eb], P.B.w[eb], -1, eb);
+    if (FILL && keep)
+      put_arc(O, P, pos0 + run + ex, id, d, 0, P.bOut.olab[pb], P.bOut.w[pb], -1, pb);
     run += tot;
   }
   if (s.mU) {
@@ -974,12 +981,11 @@ __device__ uint32_t heavy_state(const Problem &P, uint32_t id, uint32_t key, uin
     // B's bucket of its label, gives (label, a, b) order.
     for (uint32_t c = 0; c < s.nA; c += NT) {
       const uint32_t i = c + t;
-      int32_t lo = 0, hi = 0, ea = 0;
+      int32_t lo = 0, hi = 0, pa = 0;
       uint32_t kept = 0, da = 0;
       if (i < s.nA) {
-        const int32_t pa = s.aS + s.ae + (int32_t)i;
+        pa = s.aS + s.ae + (int32_t)i;
         const int2 ar = P.aOut.arec[pa];
-        ea = P.aOut.perm[pa];
         da = nbr_of(ar.y);
         label_range(P.bOut, s.qb, s.bS + s.be, s.bE, ar.x, lo, hi);
         for (int32_t pb = lo; pb < hi; ++pb)
@@ -988,14 +994,13 @@ __device__ uint32_t heavy_state(const Problem &P, uint32_t id, uint32_t key, uin
       uint32_t tot;
       uint32_t ex = block_excl_scan<uint32_t>(kept, s_w, tot);
       if (FILL && kept) {
-        const int32_t ia = P.A.il[ea];
-        const float wa = P.A.w[ea];
+        const int32_t ia = P.aOut.olab[pa];
+        const float wa = P.aOut.w[pa];
         uint32_t pos = pos0 + run + ex;
         for (int32_t pb = lo; pb < hi; ++pb) {
-          const int32_t eb = P.bOut.perm[pb];
           const uint32_t d = make_key(da, nbr_of(P.bOut.arec[pb].y), 0u, sh);
           if (test_bit(P.coacc, d))
-            put_arc(O, P, pos++, id, d, ia, P.B.ol[eb], wa + P.B.w[eb], ea, eb);
+            put_arc(O, P, pos++, id, d, ia, P.bOut.olab[pb], wa + P.bOut.w[pb], pa, pb);
         }
       }
       run += tot;
@@ -1005,12 +1010,17 @@ __device__ uint32_t heavy_state(const Problem &P, uint32_t id, uint32_t key, uin
 }
 
 __global__ __launch_bounds__(NT) void k_count(Problem P, const uint32_t *__restrict__ key_of,
-                                              uint32_t n, uint32_t *__restrict__ cnt,
+                                              uint32_t n, ull per, uint32_t *__restrict__ cnt,
+                                              uint32_t *__restrict__ btot,
                                               uint32_t *__restrict__ heavy, Scalars *sc) {
-  for (ull i0 = (ull)blockIdx.x * NT; i0 < n; i0 += (ull)gridDim.x * NT) {
-    const ull id = i0 + threadIdx.x;
+  __shared__ uint32_t s_w[NWAVES];
+  const ull begin = (ull)blockIdx.x * per;
+  const ull end = begin + per < n ? begin + per : n;
+  uint32_t sum = 0;
+  for (ull base = begin; base < end; base += NT) {
+    const ull id = base + threadIdx.x;
     bool hv = false;
-    if (id < n) {
+    if (id < end) {
       const Fwd s = fwd_info<false>(P, key_of[id]);
       uint32_t c = 0;
       if (out_units(s) > LIGHT_UNITS) {
@@ -1021,74 +1031,85 @@ __global__ __launch_bounds__(NT) void k_count(Problem P, const uint32_t *__restr
         });
       }
       cnt[id] = c;
+      sum += c;
     }
     unsigned long long m = __ballot(hv);
     if (m) {
       const int leader = __ffsll(m) - 1;
-      uint32_t base = 0;
-      if ((int)__lane_id() == leader) base = atomicAdd(&sc->heavy, (uint32_t)__popcll(m));
-      base = __shfl(base, leader, WAVE);
-      if (hv) heavy[base + __popcll(m & __lanemask_lt())] = (uint32_t)id;
+      uint32_t hb = 0;
+      if ((int)__lane_id() == leader) hb = atomicAdd(&sc->heavy, (uint32_t)__popcll(m));
+      hb = __shfl(hb, leader, WAVE);
+      if (hv) heavy[hb + __popcll(m & __lanemask_lt())] = (uint32_t)id;
     }
   }
+  const uint32_t tot = block_sum(sum, s_w);
+  if (threadIdx.x == 0) btot[blockIdx.x] = tot;
 }
 
 __global__ __launch_bounds__(NT) void k_count_heavy(Problem P, const uint32_t *__restrict__ key_of,
                                                     const uint32_t *__restrict__ heavy,
-                                                    const uint32_t *__restrict__ nheavy_p,
-                                                    uint32_t *__restrict__ cnt) {
+                                                    const uint32_t *__restrict__ nheavy_p, ull per,
+                                                    uint32_t *__restrict__ cnt,
+                                                    uint32_t *__restrict__ btot) {
   __shared__ uint32_t s_w[NWAVES];
   const uint32_t nheavy = *nheavy_p;
   OutGraph none = {};
   for (uint32_t h = blockIdx.x; h < nheavy; h += gridDim.x) {
     const uint32_t id = heavy[h];
     uint32_t c = heavy_state<false>(P, id, key_of[id], 0, none, s_w);
-    if (threadIdx.x == 0) cnt[id] = c;
+    if (threadIdx.x == 0) {
+      cnt[id] = c;
+      atomicAdd(btot + id / per, c);
+    }
   }
 }
 
+// One thread per state of C, one contiguous chunk per workgroup: the state's
+// arc offset (chunk base + block scan of the counts), flags and key, and the
+// arcs of a light state (heavy states' arcs are written by k_fill_heavy).
 __global__ __launch_bounds__(NT) void k_fill_light(Problem P, const uint32_t *__restrict__ key_of,
-                                                   uint32_t n, const uint32_t *__restrict__ arc_off,
-                                                   OutGraph O) {
-  for (ull id = (ull)blockIdx.x * NT + threadIdx.x; id < n; id += (ull)gridDim.x * NT) {
+                                                   uint32_t n, ull per,
+                                                   const uint32_t *__restrict__ cnt,
+                                                   const uint32_t *__restrict__ btot,
+                                                   uint32_t narcs, OutGraph O) {
+  __shared__ uint32_t s_w[NWAVES];
+  const ull begin = (ull)blockIdx.x * per;
+  const ull end = begin + per < n ? begin + per : n;
+  uint32_t run = begin < end ? btot[blockIdx.x] : 0u;
+  for (ull base = begin; base < end; base += NT) {
+    const ull id = base + threadIdx.x;
+    const bool valid = id < end;
+    const uint32_t c = valid ? cnt[id] : 0u;
+    uint32_t tot;
+    const uint32_t ex = block_excl_scan<uint32_t>(c, s_w, tot);
+    uint32_t pos = run + ex;
+    run += tot;
+    if (!valid) continue;
     const Fwd s = fwd_info<false>(P, key_of[id]);
+    O.arc_offset[id] = (int32_t)pos;
+    O.accept[id] = s.accept ? 1 : 0;
+    O.start[id] = s.start ? 1 : 0;
+    if (O.key_a) O.key_a[id] = (int32_t)s.qa;
+    if (O.key_b) O.key_b[id] = (int32_t)s.qb;
+    if (O.key_f) O.key_f[id] = (uint8_t)s.f;
     if (out_units(s) > LIGHT_UNITS) continue;
-    uint32_t pos = arc_off[id];
     const uint32_t sid = (uint32_t)id;
-    enum_light(P, s, [&](uint32_t d, int32_t il, int32_t ol, float w, int32_t ea, int32_t eb) {
-      if (test_bit(P.coacc, d)) put_arc(O, P, pos++, sid, d, il, ol, w, ea, eb);
+    enum_light(P, s, [&](uint32_t d, int32_t il, int32_t ol, float w, int32_t pa, int32_t pb) {
+      if (test_bit(P.coacc, d)) put_arc(O, P, pos++, sid, d, il, ol, w, pa, pb);
     });
   }
+  if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) O.arc_offset[n] = (int32_t)narcs;
 }
 
+// Arcs of the heavy states, one workgroup per state, from the offsets
+// k_fill_light wrote.
 __global__ __launch_bounds__(NT) void k_fill_heavy(Problem P, const uint32_t *__restrict__ key_of,
                                                    const uint32_t *__restrict__ heavy,
-                                                   uint32_t nheavy,
-                                                   const uint32_t *__restrict__ arc_off,
-                                                   OutGraph O) {
+                                                   uint32_t nheavy, OutGraph O) {
   __shared__ uint32_t s_w[NWAVES];
   for (uint32_t h = blockIdx.x; h < nheavy; h += gridDim.x) {
     const uint32_t id = heavy[h];
-    heavy_state<true>(P, id, key_of[id], arc_off[id], O, s_w);
-  }
-}
-
-__global__ __launch_bounds__(NT) void k_state_flags(Problem P, const uint32_t *__restrict__ key_of,
-                                                    uint32_t n, const uint32_t *__restrict__ arc_off,
-                                                    uint32_t narcs, OutGraph O) {
-  for (ull id = (ull)blockIdx.x * NT + threadIdx.x; id <= n; id += (ull)gridDim.x * NT) {
-    if (id == n) {
-      O.arc_offset[n] = (int32_t)narcs;
-      continue;
-    }
-    const uint32_t k = key_of[id];
-    const uint32_t qa = key_qa(k, P.shiftB), qb = key_qb(k, P.shiftB), f = key_f(k);
-    O.arc_offset[id] = (int32_t)arc_off[id];
-    O.accept[id] = (P.A.accept[qa] && P.B.accept[qb]) ? 1 : 0;
-    O.start[id] = (f == 0 && P.A.start[qa] && P.B.start[qb]) ? 1 : 0;
-    if (O.key_a) O.key_a[id] = (int32_t)qa;
-    if (O.key_b) O.key_b[id] = (int32_t)qb;
-    if (O.key_f) O.key_f[id] = (uint8_t)f;
+    heavy_state<true>(P, id, key_of[id], (uint32_t)O.arc_offset[id], O, s_w);
   }
 }
 
@@ -1105,9 +1126,10 @@ hipError_t launch_validate(const DevGraph &g, int side, uint32_t *err, uint32_t 
 }
 
 hipError_t sort_view(const DevGraph &g, int side, bool by_dst, int lab_bits, int4 *srec,
-                     int2 *arec, int32_t *perm, int32_t *off_tmp, const int4 *eps_rec,
-                     unsigned long long *k0, int32_t *v0, unsigned long long *k1, int32_t *v1,
-                     void *sort_temp, uint32_t *eps_states, hipStream_t s) {
+                     int2 *arec, int32_t *perm, int32_t *olab, float *w, int32_t *off_tmp,
+                     const int4 *eps_rec, unsigned long long *k0, int32_t *v0,
+                     unsigned long long *k1, int32_t *v1, void *sort_temp, uint32_t *eps_states,
+                     hipStream_t s) {
   const size_t E = (size_t)g.E;
   hipError_t e;
   if (E) {
@@ -1116,7 +1138,7 @@ hipError_t sort_view(const DevGraph &g, int side, bool by_dst, int lab_bits, int
     int bits = bitlen((unsigned long long)(g.V > 0 ? g.V - 1 : 0)) + lab_bits;
     if ((e = radix_sort(k0, v0, k1, v1, E, bits, sort_temp, s)) != hipSuccess) return e;
     k_split<<<grid_for(E), NT, 0, s>>>(g, by_dst ? 1 : 0, k0, v0, (long long)E, lab_bits,
-                                       eps_rec, perm, arec);
+                                       eps_rec, side, perm, olab, w, arec);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   const int32_t *off = g.off;
@@ -1204,54 +1226,49 @@ hipError_t launch_popcount(const uint32_t *bm, size_t nwords, unsigned long long
   return hipGetLastError();
 }
 
-hipError_t launch_and_words(uint32_t *a, const uint32_t *b, size_t nwords, hipStream_t s) {
+hipError_t launch_trim_words(uint32_t *coacc, const uint32_t *vis, uint32_t *cnt, size_t nwords,
+                             hipStream_t s) {
   if (!nwords) return hipSuccess;
-  k_and_words<<<grid_for(nwords, 8192), NT, 0, s>>>(a, b, nwords);
-  return hipGetLastError();
-}
-
-hipError_t launch_popc_words(const uint32_t *bm, uint32_t *cnt, size_t nwords, hipStream_t s) {
-  if (!nwords) return hipSuccess;
-  k_popc_words<<<grid_for(nwords, 8192), NT, 0, s>>>(bm, cnt, nwords);
+  k_trim_words<<<grid_for(nwords, 8192), NT, 0, s>>>(coacc, vis, cnt, nwords);
   return hipGetLastError();
 }
 
 hipError_t launch_key_of_id(const uint32_t *bm, const uint32_t *wbase, size_t nwords,
                             uint32_t *key_of, hipStream_t s) {
   if (!nwords) return hipSuccess;
-  k_key_of_id<<<grid_for(nwords, 8192), NT, 0, s>>>(bm, wbase, nwords, key_of);
+  const size_t per = out_chunk(nwords * 32);
+  k_key_of_id<<<out_grid(nwords * 32, per), NT, 0, s>>>(bm, wbase, nwords, per, key_of);
   return hipGetLastError();
 }
 
-hipError_t launch_count(const Problem &P, const uint32_t *key_of, uint32_t nstates,
-                        uint32_t *cnt, uint32_t *heavy, Scalars *sc, hipStream_t s) {
+hipError_t launch_count(const Problem &P, const uint32_t *key_of, uint32_t nstates, size_t per,
+                        uint32_t *cnt, uint32_t *btot, uint32_t *heavy, Scalars *sc,
+                        hipStream_t s) {
   if (!nstates) return hipSuccess;
-  k_count<<<grid_for(nstates, 8192), NT, 0, s>>>(P, key_of, nstates, cnt, heavy, sc);
+  k_count<<<out_grid(nstates, per), NT, 0, s>>>(P, key_of, nstates, per, cnt, btot, heavy, sc);
   return hipGetLastError();
 }
 
 hipError_t launch_count_heavy(const Problem &P, const uint32_t *key_of, const uint32_t *heavy,
-                              const uint32_t *nheavy_dev, uint32_t *cnt, hipStream_t s) {
-  k_count_heavy<<<1024, NT, 0, s>>>(P, key_of, heavy, nheavy_dev, cnt);
+                              const uint32_t *nheavy_dev, size_t per, uint32_t *cnt,
+                              uint32_t *btot, hipStream_t s) {
+  k_count_heavy<<<1024, NT, 0, s>>>(P, key_of, heavy, nheavy_dev, per, cnt, btot);
   return hipGetLastError();
 }
 
-hipError_t launch_fill(const Problem &P, const uint32_t *key_of, uint32_t nstates,
-                       const uint32_t *arc_off, const uint32_t *heavy, uint32_t nheavy,
-                       uint32_t narcs, const OutGraph &O, hipStream_t s) {
+hipError_t launch_fill(const Problem &P, const uint32_t *key_of, uint32_t nstates, size_t per,
+                       const uint32_t *cnt, const uint32_t *btot, const uint32_t *heavy,
+                       uint32_t nheavy, uint32_t narcs, const OutGraph &O, hipStream_t s) {
   hipError_t e;
-  if (nstates) {
-    k_fill_light<<<grid_for(nstates, 8192), NT, 0, s>>>(P, key_of, nstates, arc_off, O);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-  }
+  k_fill_light<<<out_grid(nstates, per), NT, 0, s>>>(P, key_of, nstates, per, cnt, btot, narcs,
+                                                     O);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
   if (nheavy) {
     unsigned g = nheavy < 4096 ? nheavy : 4096;
-    k_fill_heavy<<<g, NT, 0, s>>>(P, key_of, heavy, nheavy, arc_off, O);
+    k_fill_heavy<<<g, NT, 0, s>>>(P, key_of, heavy, nheavy, O);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  k_state_flags<<<grid_for((size_t)nstates + 1, 8192), NT, 0, s>>>(P, key_of, nstates, arc_off,
-                                                                   narcs, O);
-  return hipGetLastError();
+  return hipSuccess;
 }
 
 }  // namespace fstc

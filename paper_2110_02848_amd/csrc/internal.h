@@ -18,6 +18,20 @@ constexpr uint32_t LIGHT_SEARCH = 64;  // search: a key with more units is split
 constexpr int CHAIN_MAX = 64;          // search: default depth-first budget per thread
 constexpr uint32_t NO_KEY = 0xFFFFFFFFu;
 
+// The output passes give every workgroup one contiguous chunk of states
+// (a multiple of NT), so the arcs a workgroup writes are contiguous and
+// stay in one L2; at most OUT_BLOCKS chunks.
+constexpr size_t OUT_BLOCKS = 8192;
+inline size_t out_chunk(size_t n) {
+  size_t per = (n + OUT_BLOCKS - 1) / OUT_BLOCKS;
+  per = (per + NT - 1) / NT * NT;
+  return per ? per : (size_t)NT;
+}
+inline unsigned out_grid(size_t n, size_t per) {
+  const size_t g = (n + per - 1) / per;
+  return (unsigned)(g ? g : 1);
+}
+
 // ---------------------------------------------------------------------------
 // Graph views
 // ---------------------------------------------------------------------------
@@ -55,6 +69,9 @@ struct DevGraph {
 //   non-epsilon output labels).  A key whose two states are both marked is
 //   reached once by a search in that direction, so it needs no claim.
 //   perm[i] = original arc id.
+//   olab[i], w[i] (out-views only) = the arc's label on the output side of
+//             the composition (A: input label, B: output label) and its
+//             weight, gathered into sorted order for writing C.
 //   lut, when present, holds every group's label buckets:
 //             lut[v * lstride + l] = {begin, end, other end of the first arc,
 //             0} for label l in group v, so a one-arc bucket resolves its
@@ -65,6 +82,8 @@ struct View {
   const int32_t *perm;
   const int4 *lut;
   int32_t lstride;  // largest label + 1
+  const int32_t *olab;
+  const float *w;
 };
 
 constexpr uint32_t FLAG_ACCEPT = 1u, FLAG_EPS_OUT = 2u, FLAG_START = 4u, FLAG_UNIQ = 8u;
@@ -272,9 +291,10 @@ hipError_t launch_validate(const DevGraph &g, int side, uint32_t *err, uint32_t 
 // record of every state and, if lut is set, the label buckets of every group
 // (V * (lab_max + 1) entries).
 hipError_t sort_view(const DevGraph &g, int side, bool by_dst, int lab_bits, int4 *srec,
-                     int2 *arec, int32_t *perm, int32_t *off_tmp, const int4 *eps_rec,
-                     unsigned long long *k0, int32_t *v0, unsigned long long *k1, int32_t *v1,
-                     void *sort_temp, uint32_t *eps_states, hipStream_t s);
+                     int2 *arec, int32_t *perm, int32_t *olab, float *w, int32_t *off_tmp,
+                     const int4 *eps_rec, unsigned long long *k0, int32_t *v0,
+                     unsigned long long *k1, int32_t *v1, void *sort_temp, uint32_t *eps_states,
+                     hipStream_t s);
 // FLAG_UNIQ for the records `self` of a view of graph g, from the groups of
 // the opposite view of the same graph (`other`, `other_arec`): side 0 = A,
 // side 1 = B; out_view says whether `self` is an out-view.
@@ -303,17 +323,24 @@ hipError_t launch_count_moves(const Problem &P, size_t nwords, bool forward,
 // *out += number of set bits of bm[0, nwords).
 hipError_t launch_popcount(const uint32_t *bm, size_t nwords, unsigned long long *out,
                            hipStream_t s);
-// a[w] &= b[w] for w < nwords.
-hipError_t launch_and_words(uint32_t *a, const uint32_t *b, size_t nwords, hipStream_t s);
-hipError_t launch_popc_words(const uint32_t *bm, uint32_t *cnt, size_t nwords, hipStream_t s);
+// coacc[w] &= vis[w] and cnt[w] = popcount(coacc[w]) for w < nwords.
+hipError_t launch_trim_words(uint32_t *coacc, const uint32_t *vis, uint32_t *cnt, size_t nwords,
+                             hipStream_t s);
 hipError_t launch_key_of_id(const uint32_t *bm, const uint32_t *wbase, size_t nwords,
                             uint32_t *key_of, hipStream_t s);
-hipError_t launch_count(const Problem &P, const uint32_t *key_of, uint32_t nstates,
-                        uint32_t *cnt, uint32_t *heavy, Scalars *sc, hipStream_t s);
+// Kept-arc count of every state of C (chunks of `per` states per workgroup):
+// cnt[id] for light states, heavy state ids listed in `heavy` (count in
+// Scalars::heavy), btot[chunk] = the chunk's light total.
+hipError_t launch_count(const Problem &P, const uint32_t *key_of, uint32_t nstates, size_t per,
+                        uint32_t *cnt, uint32_t *btot, uint32_t *heavy, Scalars *sc,
+                        hipStream_t s);
+// Counts of the heavy states (cnt[id], added to their chunk's btot).
 hipError_t launch_count_heavy(const Problem &P, const uint32_t *key_of, const uint32_t *heavy,
-                              const uint32_t *nheavy_dev, uint32_t *cnt, hipStream_t s);
-hipError_t launch_fill(const Problem &P, const uint32_t *key_of, uint32_t nstates,
-                       const uint32_t *arc_off, const uint32_t *heavy, uint32_t nheavy,
-                       uint32_t narcs, const OutGraph &O, hipStream_t s);
+                              const uint32_t *nheavy_dev, size_t per, uint32_t *cnt,
+                              uint32_t *btot, hipStream_t s);
+// Write C: btot holds the exclusive arc offset of every chunk.
+hipError_t launch_fill(const Problem &P, const uint32_t *key_of, uint32_t nstates, size_t per,
+                       const uint32_t *cnt, const uint32_t *btot, const uint32_t *heavy,
+                       uint32_t nheavy, uint32_t narcs, const OutGraph &O, hipStream_t s);
 
 }  // namespace fstc

@@ -36,7 +36,7 @@ FAMILIES = {
     "search_forward": ("k_gen<true>",),
     "search_backward": ("k_gen<false>",),
     "count": ("k_count(", "k_count_heavy("),
-    "fill": ("k_fill_light(", "k_fill_heavy(", "k_state_flags("),
+    "fill": ("k_fill_light(", "k_fill_heavy("),
 }
 
 
