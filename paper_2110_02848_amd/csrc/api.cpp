@@ -169,9 +169,6 @@ int finish_empty(fst_ctx *c, int64_t *V_C, int64_t *E_C) {
   return FST_OK;
 }
 
-// Generations are queued in batches with no host round trip; after each batch
-// the host checks whether the next generation has any work (generations
-// queued after the search has ended do nothing).
 KernelTimer timer(const fst_ctx *c, int kernel) {
   KernelTimer t;
   if (c->timing) {
@@ -191,6 +188,9 @@ int add_time(fst_ctx *c, int kernel, int64_t launches) {
   return FST_OK;
 }
 
+// Generations are queued in batches (4, 16, 32, 64, 64, ...) with no host
+// round trip; after each batch the host checks whether the next generation
+// has any work (generations queued after the search has ended do nothing).
 int search(fst_ctx *c, const SearchArgs &S, bool forward, int64_t *levels, hipStream_t s) {
   const int kernel = forward ? FST_KERNEL_SEARCH_FORWARD : FST_KERNEL_SEARCH_BACKWARD;
   const KernelTimer t = timer(c, kernel);
@@ -204,7 +204,7 @@ int search(fst_ctx *c, const SearchArgs &S, bool forward, int64_t *levels, hipSt
     if (c->h_sc->overflow) return FST_ERR_TOO_LARGE;
     const GenSlot &nx = c->h_sc->G[g % 3];
     if (nx.qcount == 0 && (uint32_t)nx.hpack == 0) break;
-    if (batch < 64) batch *= 2;
+    batch = batch == 4 ? 16 : (batch < 64 ? 2 * batch : 64);
   }
   *levels = c->h_sc->gens;
   return FST_OK;
@@ -389,7 +389,7 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   uint32_t *heavy = bq;    // so is the backward queue
   HIP_TRY(launch_key_of_id(P.coacc, wbase, nwords, key_of, s));
   FST_TRY(ensure(c, c->cnt, ((size_t)nstates + 1) * 4));
-  FST_TRY(ensure(c, c->btot, (OUT_BLOCKS + 1) * 4));
+  FST_TRY(ensure(c, c->btot, (OUT_CHUNKS + 1) * 4));
   uint32_t *cnt = as<uint32_t>(c->cnt), *btot = as<uint32_t>(c->btot);
   const size_t per = out_chunk(nstates);
   HIP_TRY(hipMemsetAsync(&d_sc->heavy, 0, sizeof(uint32_t), s));
@@ -401,7 +401,8 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   tc.end(s);
   // exclusive arc offset of every chunk; the total is E_C
   if (nstates)
-    HIP_TRY(scan_u32(btot, btot, out_grid(nstates, per), false, &d_sc->total, c->scan_tmp.p, s));
+    HIP_TRY(scan_u32(btot, btot, out_chunks(nstates, per), false, &d_sc->total, c->scan_tmp.p,
+                     s));
   mark(c, 4, s);
   FST_TRY(readback(c, s));
   const unsigned long long narcs = c->h_sc->total;

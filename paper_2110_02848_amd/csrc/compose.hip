@@ -340,56 +340,96 @@ __device__ __forceinline__ void wave_push(bool want, uint32_t key, const Pusher 
   }
 }
 
+// A state's two records in one view (see View).
+struct Rec {
+  int4 r0, r1;
+};
+
+// An opaque copy of a record pair held in registers (see opaque(int32_t)).
+__device__ __forceinline__ Rec opaque(const Rec &r) {
+  Rec o;
+  o.r0 = make_int4(opaque(r.r0.x), opaque(r.r0.y), opaque(r.r0.z), opaque(r.r0.w));
+  o.r1 = make_int4(opaque(r.r1.x), opaque(r.r1.y), opaque(r.r1.z), opaque(r.r1.w));
+  return o;
+}
+
+__device__ __forceinline__ Rec load_rec(const View &v, uint32_t q) {
+  Rec r;
+  r.r0 = v.srec[2 * (size_t)q];
+  r.r1 = v.srec[2 * (size_t)q + 1];
+  return r;
+}
+
 // Move structure of a key in the forward direction (also used to write C).
-// e0A/e0B: other end of the first epsilon arc of qa / qb; l1, n1: label and
-// other end of the first non-epsilon arc (valid when the arc exists).
+// flA/flB: record flags of qa / qb; e0A/e0B: other end of the first epsilon
+// arc of qa / qb; l1, n1: label and other end of the first non-epsilon arc
+// (valid when the arc exists).
 struct Fwd {
   uint32_t qa, qb, f;
   int32_t aS, ae, aE, bS, be, bE;
+  int32_t flA, flB;
   uint32_t eA, nA, nB, mU;
-  uint32_t epsA;    // epsOutA(qa)
-  uint32_t accept;  // accept(qa) and accept(qb)
+  uint32_t epsA;      // epsOutA(qa)
+  uint32_t accept;    // accept(qa) and accept(qb)
   uint32_t uqA, uqB;  // FLAG_UNIQ of qa, qb (out-views)
   uint32_t start;     // a start key: f = 0, start(qa) and start(qb)
   int32_t e0A, e0B, l1A, n1A, l1B, n1B;
 };
 
-// INL: also load the inline first arcs (the search uses them; the output
-// passes walk the arc records anyway).
-template <bool INL = true>
-__device__ __forceinline__ Fwd fwd_info(const Problem &P, uint32_t key) {
+__device__ __forceinline__ Fwd make_fwd(uint32_t key, uint32_t shiftB, const Rec &A, const Rec &B) {
   Fwd s;
   s.f = key_f(key);
-  s.qb = key_qb(key, P.shiftB);
-  s.qa = key_qa(key, P.shiftB);
-  const int4 ra = P.aOut.srec[2 * (size_t)s.qa];
-  const int4 rb = P.bOut.srec[2 * (size_t)s.qb];
-  if (INL) {
-    const int4 xa = P.aOut.srec[2 * (size_t)s.qa + 1];
-    const int4 xb = P.bOut.srec[2 * (size_t)s.qb + 1];
-    s.e0A = xa.x;
-    s.l1A = xa.y;
-    s.n1A = xa.z;
-    s.e0B = xb.x;
-    s.l1B = xb.y;
-    s.n1B = xb.z;
-  }
-  s.aS = ra.x;
-  s.ae = ra.y;
-  s.aE = ra.z;
-  s.bS = rb.x;
-  s.be = rb.y;
-  s.bE = rb.z;
-  s.epsA = ra.y > 0 ? 1u : 0u;
-  s.accept = (uint32_t)(ra.w & rb.w) & FLAG_ACCEPT;
-  s.uqA = (uint32_t)ra.w & FLAG_UNIQ;
-  s.uqB = (uint32_t)rb.w & FLAG_UNIQ;
-  s.start = (s.f == 0 && (ra.w & rb.w & (int32_t)FLAG_START)) ? 1u : 0u;
+  s.qb = key_qb(key, shiftB);
+  s.qa = key_qa(key, shiftB);
+  s.aS = A.r0.x;
+  s.ae = A.r0.y;
+  s.aE = A.r0.z;
+  s.flA = A.r0.w;
+  s.bS = B.r0.x;
+  s.be = B.r0.y;
+  s.bE = B.r0.z;
+  s.flB = B.r0.w;
+  s.e0A = A.r1.x;
+  s.l1A = A.r1.y;
+  s.n1A = A.r1.z;
+  s.e0B = B.r1.x;
+  s.l1B = B.r1.y;
+  s.n1B = B.r1.z;
+  s.epsA = s.ae > 0 ? 1u : 0u;
+  s.accept = (uint32_t)(s.flA & s.flB) & FLAG_ACCEPT;
+  s.uqA = (uint32_t)s.flA & FLAG_UNIQ;
+  s.uqB = (uint32_t)s.flB & FLAG_UNIQ;
+  s.start = (s.f == 0 && (s.flA & s.flB & (int32_t)FLAG_START)) ? 1u : 0u;
   s.eA = s.f ? 0u : (uint32_t)s.ae;
   s.nA = (uint32_t)(s.aE - s.aS - s.ae);
   s.nB = (uint32_t)(s.bE - s.bS - s.be);
   s.mU = (s.nA && s.nB) ? (s.nA < s.nB ? s.nA : s.nB) : 0u;
   return s;
+}
+
+// The records a move structure was made from.
+__device__ __forceinline__ Rec rec_a(const Fwd &s) {
+  return Rec{make_int4(s.aS, s.ae, s.aE, s.flA), make_int4(s.e0A, s.l1A, s.n1A, 0)};
+}
+__device__ __forceinline__ Rec rec_b(const Fwd &s) {
+  return Rec{make_int4(s.bS, s.be, s.bE, s.flB), make_int4(s.e0B, s.l1B, s.n1B, 0)};
+}
+
+// INL: also load the second records (the inline first arcs); the general
+// enumeration of the output passes walks the arc records instead.
+template <bool INL = true>
+__device__ __forceinline__ Fwd fwd_info(const Problem &P, uint32_t key) {
+  const uint32_t qa = key_qa(key, P.shiftB), qb = key_qb(key, P.shiftB);
+  Rec A, B;
+  if (INL) {
+    A = load_rec(P.aOut, qa);
+    B = load_rec(P.bOut, qb);
+  } else {
+    A.r0 = P.aOut.srec[2 * (size_t)qa];
+    B.r0 = P.bOut.srec[2 * (size_t)qb];
+    A.r1 = B.r1 = make_int4(0, 0, 0, 0);
+  }
+  return make_fwd(key, P.shiftB, A, B);
 }
 
 // Work units of a key: its A-epsilon arcs, its B-epsilon arcs, and the
@@ -400,17 +440,19 @@ __device__ __forceinline__ uint32_t fwd_units(const Fwd &s) { return s.eA + (uin
 // The keys a work unit reaches: for p in [lo, hi), with nb_p the neighbour
 // field of arc record p (nb_lo given) of the side named by VARY_A (A's view
 // when set, else B's), the key whose state on that side is nb_p and whose
-// state on the other side is `fixed`.  Forward keys take filter bit F_ONE;
-// backward keys are also visited with f = 1 under DUAL or, with
-// DUAL_FROM_NB, when bit 31 of nb_p (epsOutA of an A-side neighbour) is set.
-// HOT marks keys many threads may reach at once.  A key is reached at most
-// once by the search (needs no claim) when FIXED_UNIQ is set and nb_p has
-// NBR_UNIQ: both of its states are marked FLAG_UNIQ.  No pointer is kept, so
-// a range lives in a few registers.
+// state on the other side is `fixed`, with records `fix` (loaded before the
+// bucket lookup resolves, or the current key's own records for epsilon
+// moves, so visiting a key loads only the varying side's records).  Forward
+// keys take filter bit F_ONE; backward keys are also visited with f = 1 under
+// DUAL or, with DUAL_FROM_NB, when NBR_EPS of nb_p (epsOutA of an A-side
+// neighbour) is set.  HOT marks keys many threads may reach at once.  A key
+// is reached at most once by the search (needs no claim) when FIXED_UNIQ is
+// set and nb_p has NBR_UNIQ: both of its states are marked FLAG_UNIQ.
 enum : uint32_t { VARY_A = 1, DUAL = 2, DUAL_FROM_NB = 4, HOT = 8, F_ONE = 16, FIXED_UNIQ = 32 };
 struct UnitRange {
   int32_t lo, hi, nb0;
   uint32_t fixed, flags;
+  Rec fix;
 };
 
 __device__ __forceinline__ UnitRange fwd_range(const Problem &P, const Fwd &s, uint32_t u) {
@@ -419,6 +461,7 @@ __device__ __forceinline__ UnitRange fwd_range(const Problem &P, const Fwd &s, u
     r.lo = s.aS + (int32_t)u;
     r.hi = r.lo + 1;
     r.fixed = s.qb;
+    r.fix = rec_b(s);
     r.flags = VARY_A | HOT | (s.uqB ? FIXED_UNIQ : 0u);
     r.nb0 = u == 0 ? opaque(s.e0A) : P.aOut.arec[r.lo].y;
   } else if (u < s.eA + (uint32_t)s.be) {  // B-epsilon move
@@ -426,6 +469,7 @@ __device__ __forceinline__ UnitRange fwd_range(const Problem &P, const Fwd &s, u
     r.lo = s.bS + (int32_t)j;
     r.hi = r.lo + 1;
     r.fixed = s.qa;
+    r.fix = rec_a(s);
     r.flags = HOT | (s.epsA ? F_ONE : 0u) | (s.uqA ? FIXED_UNIQ : 0u);
     r.nb0 = j == 0 ? opaque(s.e0B) : P.bOut.arec[r.lo].y;
   } else {  // matching moves of one arc of the smaller side
@@ -433,14 +477,16 @@ __device__ __forceinline__ UnitRange fwd_range(const Problem &P, const Fwd &s, u
     if (s.nA <= s.nB) {
       const int2 ar = j == 0 ? make_int2(opaque(s.l1A), opaque(s.n1A))
                              : P.aOut.arec[s.aS + s.ae + (int32_t)j];
-      label_range(P.bOut, s.qb, s.bS + s.be, s.bE, ar.x, r.lo, r.hi, r.nb0);
       r.fixed = nbr_of(ar.y);
+      r.fix = load_rec(P.aOut, r.fixed);
+      label_range(P.bOut, s.qb, s.bS + s.be, s.bE, ar.x, r.lo, r.hi, r.nb0);
       r.flags = (ar.y & NBR_UNIQ) ? FIXED_UNIQ : 0u;
     } else {
       const int2 br = j == 0 ? make_int2(opaque(s.l1B), opaque(s.n1B))
                              : P.bOut.arec[s.bS + s.be + (int32_t)j];
-      label_range(P.aOut, s.qa, s.aS + s.ae, s.aE, br.x, r.lo, r.hi, r.nb0);
       r.fixed = nbr_of(br.y);
+      r.fix = load_rec(P.bOut, r.fixed);
+      label_range(P.aOut, s.qa, s.aS + s.ae, s.aE, br.x, r.lo, r.hi, r.nb0);
       r.flags = VARY_A | ((br.y & NBR_UNIQ) ? FIXED_UNIQ : 0u);
     }
   }
@@ -452,41 +498,52 @@ __device__ __forceinline__ UnitRange fwd_range(const Problem &P, const Fwd &s, u
 struct Bwd {
   uint32_t va, vb, g, epsV;
   int32_t aS, ae, aE, bS, be, bE;
+  int32_t flA, flB;
   uint32_t eA, eB, nA, nB, mU;
   uint32_t uqA, uqB;  // FLAG_UNIQ of va, vb (in-views)
   int32_t e0A, e0B, l1A, n1A, l1B, n1B;  // inline first arcs, as in Fwd
 };
 
-__device__ __forceinline__ Bwd bwd_info(const Problem &P, uint32_t key) {
+__device__ __forceinline__ Bwd make_bwd(uint32_t key, uint32_t shiftB, const Rec &A, const Rec &B) {
   Bwd s;
   s.g = key_f(key);
-  s.vb = key_qb(key, P.shiftB);
-  s.va = key_qa(key, P.shiftB);
-  const int4 ra = P.aIn.srec[2 * (size_t)s.va];
-  const int4 rb = P.bIn.srec[2 * (size_t)s.vb];
-  const int4 xa = P.aIn.srec[2 * (size_t)s.va + 1];
-  const int4 xb = P.bIn.srec[2 * (size_t)s.vb + 1];
-  s.e0A = xa.x;
-  s.l1A = xa.y;
-  s.n1A = xa.z;
-  s.e0B = xb.x;
-  s.l1B = xb.y;
-  s.n1B = xb.z;
-  s.aS = ra.x;
-  s.ae = ra.y;
-  s.aE = ra.z;
-  s.bS = rb.x;
-  s.be = rb.y;
-  s.bE = rb.z;
-  s.epsV = (ra.w & (int32_t)FLAG_EPS_OUT) ? 1u : 0u;
-  s.uqA = (uint32_t)ra.w & FLAG_UNIQ;
-  s.uqB = (uint32_t)rb.w & FLAG_UNIQ;
-  s.eA = (s.g == 0) ? (uint32_t)s.ae : 0u;          // A-epsilon moves land on f = 0
-  s.eB = (s.g == s.epsV) ? (uint32_t)s.be : 0u;     // B-epsilon moves land on f = epsOutA
+  s.vb = key_qb(key, shiftB);
+  s.va = key_qa(key, shiftB);
+  s.aS = A.r0.x;
+  s.ae = A.r0.y;
+  s.aE = A.r0.z;
+  s.flA = A.r0.w;
+  s.bS = B.r0.x;
+  s.be = B.r0.y;
+  s.bE = B.r0.z;
+  s.flB = B.r0.w;
+  s.e0A = A.r1.x;
+  s.l1A = A.r1.y;
+  s.n1A = A.r1.z;
+  s.e0B = B.r1.x;
+  s.l1B = B.r1.y;
+  s.n1B = B.r1.z;
+  s.epsV = (s.flA & (int32_t)FLAG_EPS_OUT) ? 1u : 0u;
+  s.uqA = (uint32_t)s.flA & FLAG_UNIQ;
+  s.uqB = (uint32_t)s.flB & FLAG_UNIQ;
+  s.eA = (s.g == 0) ? (uint32_t)s.ae : 0u;       // A-epsilon moves land on f = 0
+  s.eB = (s.g == s.epsV) ? (uint32_t)s.be : 0u;  // B-epsilon moves land on f = epsOutA
   s.nA = (uint32_t)(s.aE - s.aS - s.ae);
   s.nB = (uint32_t)(s.bE - s.bS - s.be);
   s.mU = (s.g == 0 && s.nA && s.nB) ? (s.nA < s.nB ? s.nA : s.nB) : 0u;
   return s;
+}
+
+__device__ __forceinline__ Rec rec_a(const Bwd &s) {
+  return Rec{make_int4(s.aS, s.ae, s.aE, s.flA), make_int4(s.e0A, s.l1A, s.n1A, 0)};
+}
+__device__ __forceinline__ Rec rec_b(const Bwd &s) {
+  return Rec{make_int4(s.bS, s.be, s.bE, s.flB), make_int4(s.e0B, s.l1B, s.n1B, 0)};
+}
+
+__device__ __forceinline__ Bwd bwd_info(const Problem &P, uint32_t key) {
+  return make_bwd(key, P.shiftB, load_rec(P.aIn, key_qa(key, P.shiftB)),
+                  load_rec(P.bIn, key_qb(key, P.shiftB)));
 }
 
 __device__ __forceinline__ uint32_t bwd_units(const Bwd &s) { return s.eA + s.eB + s.mU; }
@@ -497,6 +554,7 @@ __device__ __forceinline__ UnitRange bwd_range(const Problem &P, const Bwd &s, u
     r.lo = s.aS + (int32_t)u;
     r.hi = r.lo + 1;
     r.fixed = s.vb;
+    r.fix = rec_b(s);
     r.flags = VARY_A | HOT | (s.uqB ? FIXED_UNIQ : 0u);
     r.nb0 = u == 0 ? opaque(s.e0A) : P.aIn.arec[r.lo].y;
   } else if (u < s.eA + s.eB) {  // by a B-epsilon move: (va, ub, 0 and 1)
@@ -504,6 +562,7 @@ __device__ __forceinline__ UnitRange bwd_range(const Problem &P, const Bwd &s, u
     r.lo = s.bS + (int32_t)j;
     r.hi = r.lo + 1;
     r.fixed = s.va;
+    r.fix = rec_a(s);
     r.flags = HOT | (s.epsV ? DUAL : 0u) | (s.uqA ? FIXED_UNIQ : 0u);
     r.nb0 = j == 0 ? opaque(s.e0B) : P.bIn.arec[r.lo].y;
   } else {  // by matching moves: (ua, ub, 0 and, if epsOutA(ua), 1)
@@ -511,21 +570,30 @@ __device__ __forceinline__ UnitRange bwd_range(const Problem &P, const Bwd &s, u
     if (s.nA <= s.nB) {
       const int2 ar = j == 0 ? make_int2(opaque(s.l1A), opaque(s.n1A))
                              : P.aIn.arec[s.aS + s.ae + (int32_t)j];
-      label_range(P.bIn, s.vb, s.bS + s.be, s.bE, ar.x, r.lo, r.hi, r.nb0);
       r.fixed = nbr_of(ar.y);
+      r.fix = load_rec(P.aIn, r.fixed);
+      label_range(P.bIn, s.vb, s.bS + s.be, s.bE, ar.x, r.lo, r.hi, r.nb0);
       r.flags = ((ar.y & NBR_EPS) ? DUAL : 0u) | ((ar.y & NBR_UNIQ) ? FIXED_UNIQ : 0u);
     } else {
       const int2 br = j == 0 ? make_int2(opaque(s.l1B), opaque(s.n1B))
                              : P.bIn.arec[s.bS + s.be + (int32_t)j];
-      label_range(P.aIn, s.va, s.aS + s.ae, s.aE, br.x, r.lo, r.hi, r.nb0);
       r.fixed = nbr_of(br.y);
+      r.fix = load_rec(P.bIn, r.fixed);
+      label_range(P.aIn, s.va, s.aS + s.ae, s.aE, br.x, r.lo, r.hi, r.nb0);
       r.flags = VARY_A | DUAL_FROM_NB | ((br.y & NBR_UNIQ) ? FIXED_UNIQ : 0u);
     }
   }
   return r;
 }
 
-// Calls f(key, hot, uniq) for every key of a unit range.
+// A key reached by a unit: its key, whether it may be hot or is reached
+// only once, and the records of its fixed side.
+struct Target {
+  uint32_t key;
+  bool hot, uniq, fixA;
+};
+
+// Calls f(target, fix) for every key of a unit range.
 template <bool FWD, class F>
 __device__ __forceinline__ void for_range(const Problem &P, const UnitRange &r, F &&f) {
   const uint32_t sh = P.shiftB;
@@ -535,12 +603,19 @@ __device__ __forceinline__ void for_range(const Problem &P, const UnitRange &r, 
     const int32_t y = p == r.lo ? r.nb0 : arcs[p].y;
     const uint32_t nb = nbr_of(y);
     const uint32_t qa = varyA ? nb : r.fixed, qb = varyA ? r.fixed : nb;
-    const bool uniq = (r.flags & FIXED_UNIQ) && (y & NBR_UNIQ);
+    Target t;
+    t.hot = hot;
+    t.uniq = (r.flags & FIXED_UNIQ) && (y & NBR_UNIQ);
+    t.fixA = !varyA;
     if (FWD) {
-      f(make_key(qa, qb, (r.flags & F_ONE) ? 1u : 0u, sh), hot, uniq);
+      t.key = make_key(qa, qb, (r.flags & F_ONE) ? 1u : 0u, sh);
+      f(t, r.fix);
     } else {
       const uint32_t nf = ((r.flags & DUAL) || ((r.flags & DUAL_FROM_NB) && (y & NBR_EPS))) ? 2u : 1u;
-      for (uint32_t ff = 0; ff < nf; ++ff) f(make_key(qa, qb, ff, sh), hot, uniq);
+      for (uint32_t ff = 0; ff < nf; ++ff) {
+        t.key = make_key(qa, qb, ff, sh);
+        f(t, r.fix);
+      }
     }
   }
 }
@@ -552,6 +627,11 @@ template <>
 struct Dir<true> {
   typedef Fwd Info;
   static __device__ __forceinline__ Fwd info(const Problem &P, uint32_t k) { return fwd_info(P, k); }
+  static __device__ __forceinline__ Fwd make(uint32_t k, uint32_t sh, const Rec &A, const Rec &B) {
+    return make_fwd(k, sh, A, B);
+  }
+  static __device__ __forceinline__ const View &viewA(const Problem &P) { return P.aOut; }
+  static __device__ __forceinline__ const View &viewB(const Problem &P) { return P.bOut; }
   static __device__ __forceinline__ uint32_t units(const Fwd &s) { return fwd_units(s); }
   static __device__ __forceinline__ UnitRange range(const Problem &P, const Fwd &s, uint32_t u) {
     return fwd_range(P, s, u);
@@ -561,13 +641,18 @@ template <>
 struct Dir<false> {
   typedef Bwd Info;
   static __device__ __forceinline__ Bwd info(const Problem &P, uint32_t k) { return bwd_info(P, k); }
+  static __device__ __forceinline__ Bwd make(uint32_t k, uint32_t sh, const Rec &A, const Rec &B) {
+    return make_bwd(k, sh, A, B);
+  }
+  static __device__ __forceinline__ const View &viewA(const Problem &P) { return P.aIn; }
+  static __device__ __forceinline__ const View &viewB(const Problem &P) { return P.bIn; }
   static __device__ __forceinline__ uint32_t units(const Bwd &s) { return bwd_units(s); }
   static __device__ __forceinline__ UnitRange range(const Problem &P, const Bwd &s, uint32_t u) {
     return bwd_range(P, s, u);
   }
 };
 
-// Calls f(key, hot, uniq) for every key of unit `u` of a key with structure s.
+// Calls f(target, fix) for every key of unit `u` of a key with structure s.
 template <bool FWD, class F>
 __device__ __forceinline__ void for_unit(const Problem &P, const typename Dir<FWD>::Info &s,
                                          uint32_t u, F &&f) {
@@ -647,11 +732,17 @@ __device__ __forceinline__ void set_bit(uint32_t *bm, uint32_t k) {
 // never expanded: fresh needs both bits).
 template <bool FWD>
 __device__ __forceinline__ void visit(const Problem &P, const SearchArgs &S, const NextGen &nx,
-                                      uint32_t v, bool hot, bool uniq, Next<FWD> &nk, int depth) {
-  const typename Dir<FWD>::Info vi = Dir<FWD>::info(P, v);
+                                      const Target &t, const Rec &fix, Next<FWD> &nk, int depth) {
+  const uint32_t v = t.key;
+  // one load for every lane: the records of the side that is not fixed
+  const Rec L = load_rec(t.fixA ? Dir<FWD>::viewB(P) : Dir<FWD>::viewA(P),
+                         t.fixA ? key_qb(v, P.shiftB) : key_qa(v, P.shiftB));
+  const Rec F = opaque(fix);
+  const typename Dir<FWD>::Info vi =
+      Dir<FWD>::make(v, P.shiftB, t.fixA ? F : L, t.fixA ? L : F);
   const uint32_t bit = 1u << (v & 31u), w = v >> 5;
   bool fresh;
-  if (uniq) {
+  if (t.uniq) {
     if (FWD) {
       set_bit(P.vis, v);
       fresh = true;
@@ -659,7 +750,7 @@ __device__ __forceinline__ void visit(const Problem &P, const SearchArgs &S, con
       fresh = (P.vis[w] & bit) != 0;
       if (fresh) set_bit(P.coacc, v);
     }
-  } else if (hot) {
+  } else if (t.hot) {
     if (FWD) {
       fresh = claim(P.vis, v);
     } else {
@@ -722,8 +813,8 @@ __global__ __launch_bounds__(NT) void k_gen(Problem P, SearchArgs S, int g) {
       Next<FWD> nk;
       nk.key = NO_KEY;
       for (uint32_t u = u0; u < u1; ++u)
-        for_unit<FWD>(P, info, u, [&](uint32_t v, bool hot, bool uniq) {
-          visit<FWD>(P, S, nx, v, hot, uniq, nk, depth);
+        for_unit<FWD>(P, info, u, [&](const Target &t, const Rec &fix) {
+          visit<FWD>(P, S, nx, t, fix, nk, depth);
         });
       if (nk.key == NO_KEY) break;
       info = nk.info;
@@ -807,7 +898,8 @@ __global__ __launch_bounds__(NT) void k_count_moves(Problem P, ull nwords,
     if (!test_bit(bm, (uint32_t)k)) continue;
     const typename Dir<FWD>::Info s = Dir<FWD>::info(P, (uint32_t)k);
     const uint32_t nu = Dir<FWD>::units(s);
-    for (uint32_t u = 0; u < nu; ++u) for_unit<FWD>(P, s, u, [&](uint32_t, bool, bool) { ++c; });
+    for (uint32_t u = 0; u < nu; ++u)
+      for_unit<FWD>(P, s, u, [&](const Target &, const Rec &) { ++c; });
   }
   const ull tot = block_sum(c, s_w);
   if (threadIdx.x == 0 && tot) atomicAdd(out, tot);
@@ -840,17 +932,24 @@ __global__ __launch_bounds__(NT) void k_trim_words(uint32_t *__restrict__ coacc,
   }
 }
 
+// The chunk of `per` items of this wavefront: [begin, end).
+__device__ __forceinline__ void wave_chunk(ull n, ull per, ull &chunk, ull &begin, ull &end) {
+  chunk = (ull)blockIdx.x * NWAVES + threadIdx.x / WAVE;
+  begin = chunk * per;
+  end = begin + per < n ? begin + per : n;
+  if (begin > end) begin = end;
+}
+
 // key_of[id] = the id-th trim key, one thread per key slot and one
-// contiguous chunk of `per` slots per workgroup, so the writes of a workgroup
-// are contiguous.
+// contiguous chunk of `per` slots per wavefront, so a wavefront's writes are
+// contiguous.
 __global__ __launch_bounds__(NT) void k_key_of_id(const uint32_t *__restrict__ bm,
                                                   const uint32_t *__restrict__ wbase,
                                                   ull nwords, ull per,
                                                   uint32_t *__restrict__ key_of) {
-  const ull nkeys = nwords * 32u;
-  const ull begin = (ull)blockIdx.x * per;
-  const ull end = begin + per < nkeys ? begin + per : nkeys;
-  for (ull k = begin + threadIdx.x; k < end; k += NT) {
+  ull chunk, begin, end;
+  wave_chunk(nwords * 32u, per, chunk, begin, end);
+  for (ull k = begin + __lane_id(); k < end; k += WAVE) {
     const uint32_t w = (uint32_t)(k >> 5), b = (uint32_t)(k & 31u);
     const uint32_t m = bm[w];
     if ((m >> b) & 1u) key_of[wbase[w] + (uint32_t)__popc(m & ((1u << b) - 1u))] = (uint32_t)k;
@@ -864,6 +963,76 @@ __device__ __forceinline__ uint32_t new_id(const Problem &P, uint32_t k) {
 
 __device__ __forceinline__ uint32_t out_units(const Fwd &s) { return s.eA + (uint32_t)s.be + s.mU; }
 
+// The move of a state that has a single candidate: one epsilon arc and no
+// matching unit, or no epsilon arc and one non-epsilon arc on the smaller
+// side whose label bucket on the other side holds at most one arc.  Lanes of
+// both kinds run the same straight-line loads, so a wavefront mixing them
+// pays for one chain of dependent loads, not two.  `fast` is false when the
+// state needs the general enumeration.
+struct Move {
+  bool fast, has;
+  uint32_t d;
+  int32_t il, ol;
+  float w;
+  int32_t pa, pb;
+};
+
+__device__ __forceinline__ Move single_move(const Problem &P, const Fwd &s) {
+  Move m;
+  m.fast = false;
+  m.has = false;
+  const uint32_t neps = s.eA + (uint32_t)s.be;
+  const bool eps1 = neps == 1 && s.mU == 0;
+  const bool m1 = neps == 0 && s.mU == 1;
+  if (!eps1 && !m1) return m;
+  int32_t pa = -1, pb = -1;
+  uint32_t da, db, f = 0;
+  if (eps1) {
+    if (s.eA) {
+      pa = s.aS;
+      da = nbr_of(s.e0A);
+      db = s.qb;
+    } else {
+      pb = s.bS;
+      da = s.qa;
+      db = nbr_of(s.e0B);
+      f = s.epsA;
+    }
+  } else {
+    int32_t lo, hi, nb0;
+    if (s.nA <= s.nB) {
+      pa = s.aS + s.ae;
+      da = nbr_of(s.n1A);
+      label_range(P.bOut, s.qb, s.bS + s.be, s.bE, s.l1A, lo, hi, nb0);
+      pb = lo;
+      db = nbr_of(nb0);
+    } else {
+      pb = s.bS + s.be;
+      db = nbr_of(s.n1B);
+      label_range(P.aOut, s.qa, s.aS + s.ae, s.aE, s.l1B, lo, hi, nb0);
+      pa = lo;
+      da = nbr_of(nb0);
+    }
+    if (hi - lo > 1) return m;  // several pairs: general enumeration
+    m.fast = true;
+    if (hi == lo) return m;  // no move
+  }
+  m.fast = true;
+  m.has = true;
+  m.d = make_key(da, db, f, P.shiftB);
+  m.pa = pa;
+  m.pb = pb;
+  const int32_t ia = pa >= 0 ? P.aOut.olab[pa] : 0;
+  const float wa = pa >= 0 ? P.aOut.w[pa] : 0.f;
+  const int32_t ob = pb >= 0 ? P.bOut.olab[pb] : 0;
+  const float wb = pb >= 0 ? P.bOut.w[pb] : 0.f;
+  m.il = ia;
+  m.ol = ob;
+  // epsilon arcs copy their weight (no + 0.0f, which would turn -0.0 into +0.0)
+  m.w = (pa >= 0 && pb >= 0) ? wa + wb : (pa >= 0 ? wa : wb);
+  return m;
+}
+
 // Sequential enumeration of a state's moves in canonical order: A-epsilon
 // arcs, B-epsilon arcs, then matching arcs by (label, a, b).  The join walks
 // the label groups of the side with fewer non-epsilon arcs and looks up the
@@ -872,6 +1041,11 @@ __device__ __forceinline__ uint32_t out_units(const Fwd &s) { return s.eA + (uin
 // position in B's out-view or -1).
 template <class Visit>
 __device__ __forceinline__ void enum_light(const Problem &P, const Fwd &s, Visit &&vis) {
+  const Move m = single_move(P, s);
+  if (m.fast) {
+    if (m.has) vis(m.d, m.il, m.ol, m.w, m.pa, m.pb);
+    return;
+  }
   const uint32_t sh = P.shiftB;
   for (int32_t p = s.aS; p < s.aS + (int32_t)s.eA; ++p)
     vis(make_key(nbr_of(P.aOut.arec[p].y), s.qb, 0u, sh), P.aOut.olab[p], 0, P.aOut.w[p], p, -1);
@@ -899,21 +1073,23 @@ __device__ __forceinline__ void enum_light(const Problem &P, const Fwd &s, Visit
       p = pend;
     }
   } else {
-    int32_t p = s.bS + s.be, al = s.aS + s.ae;
+    // the first non-epsilon arc of qb comes from its record (no arc load)
+    const int32_t p1 = s.bS + s.be;
+    int32_t p = p1, al = s.aS + s.ae;
     while (p < s.bE) {
-      const int32_t lab = P.bOut.arec[p].x;
+      const int32_t lab = p == p1 ? opaque(s.l1B) : P.bOut.arec[p].x;
       int32_t pend = p + 1;
       while (pend < s.bE && P.bOut.arec[pend].x == lab) ++pend;
-      int32_t lo, hi;
-      label_range(P.aOut, s.qa, al, s.aE, lab, lo, hi);
+      int32_t lo, hi, nb0;
+      label_range(P.aOut, s.qa, al, s.aE, lab, lo, hi, nb0);
       if (lo < hi) al = hi;
       for (int32_t pa = lo; pa < hi; ++pa) {
-        const uint32_t da = nbr_of(P.aOut.arec[pa].y);
+        const uint32_t da = nbr_of(pa == lo ? nb0 : P.aOut.arec[pa].y);
         const int32_t ia = P.aOut.olab[pa];
         const float wa = P.aOut.w[pa];
         for (int32_t pb = p; pb < pend; ++pb)
-          vis(make_key(da, nbr_of(P.bOut.arec[pb].y), 0u, sh), ia, P.bOut.olab[pb],
-              wa + P.bOut.w[pb], pa, pb);
+          vis(make_key(da, nbr_of(pb == p1 ? opaque(s.n1B) : P.bOut.arec[pb].y), 0u, sh), ia,
+              P.bOut.olab[pb], wa + P.bOut.w[pb], pa, pb);
       }
       p = pend;
     }
@@ -1012,16 +1188,16 @@ __device__ uint32_t heavy_state(const Problem &P, uint32_t id, uint32_t key, uin
 __global__ __launch_bounds__(NT) void k_count(Problem P, const uint32_t *__restrict__ key_of,
                                               uint32_t n, ull per, uint32_t *__restrict__ cnt,
                                               uint32_t *__restrict__ btot,
-                                              uint32_t *__restrict__ heavy, Scalars *sc) {
-  __shared__ uint32_t s_w[NWAVES];
-  const ull begin = (ull)blockIdx.x * per;
-  const ull end = begin + per < n ? begin + per : n;
+                                              uint32_t *__restrict__ heavy, Scalars *sc,
+                                              uint32_t nchunks) {
+  ull chunk, begin, end;
+  wave_chunk(n, per, chunk, begin, end);
   uint32_t sum = 0;
-  for (ull base = begin; base < end; base += NT) {
-    const ull id = base + threadIdx.x;
+  for (ull base = begin; base < end; base += WAVE) {
+    const ull id = base + __lane_id();
     bool hv = false;
     if (id < end) {
-      const Fwd s = fwd_info<false>(P, key_of[id]);
+      const Fwd s = fwd_info(P, key_of[id]);
       uint32_t c = 0;
       if (out_units(s) > LIGHT_UNITS) {
         hv = true;
@@ -1042,8 +1218,8 @@ __global__ __launch_bounds__(NT) void k_count(Problem P, const uint32_t *__restr
       if (hv) heavy[hb + __popcll(m & __lanemask_lt())] = (uint32_t)id;
     }
   }
-  const uint32_t tot = block_sum(sum, s_w);
-  if (threadIdx.x == 0) btot[blockIdx.x] = tot;
+  sum = wave_sum(sum);
+  if (__lane_id() == 0 && chunk < nchunks) btot[chunk] = sum;
 }
 
 __global__ __launch_bounds__(NT) void k_count_heavy(Problem P, const uint32_t *__restrict__ key_of,
@@ -1064,28 +1240,26 @@ __global__ __launch_bounds__(NT) void k_count_heavy(Problem P, const uint32_t *_
   }
 }
 
-// One thread per state of C, one contiguous chunk per workgroup: the state's
-// arc offset (chunk base + block scan of the counts), flags and key, and the
-// arcs of a light state (heavy states' arcs are written by k_fill_heavy).
+// One thread per state of C, one contiguous chunk per wavefront: the state's
+// arc offset (chunk base + wavefront scan of the counts), flags and key, and
+// the arcs of a light state (heavy states' arcs are written by k_fill_heavy).
 __global__ __launch_bounds__(NT) void k_fill_light(Problem P, const uint32_t *__restrict__ key_of,
                                                    uint32_t n, ull per,
                                                    const uint32_t *__restrict__ cnt,
                                                    const uint32_t *__restrict__ btot,
                                                    uint32_t narcs, OutGraph O) {
-  __shared__ uint32_t s_w[NWAVES];
-  const ull begin = (ull)blockIdx.x * per;
-  const ull end = begin + per < n ? begin + per : n;
-  uint32_t run = begin < end ? btot[blockIdx.x] : 0u;
-  for (ull base = begin; base < end; base += NT) {
-    const ull id = base + threadIdx.x;
+  ull chunk, begin, end;
+  wave_chunk(n, per, chunk, begin, end);
+  uint32_t run = begin < end ? btot[chunk] : 0u;
+  for (ull base = begin; base < end; base += WAVE) {
+    const ull id = base + __lane_id();
     const bool valid = id < end;
     const uint32_t c = valid ? cnt[id] : 0u;
-    uint32_t tot;
-    const uint32_t ex = block_excl_scan<uint32_t>(c, s_w, tot);
-    uint32_t pos = run + ex;
-    run += tot;
+    const uint32_t incl = wave_incl_scan(c);
+    uint32_t pos = run + incl - c;
+    run += __shfl(incl, WAVE - 1, WAVE);
     if (!valid) continue;
-    const Fwd s = fwd_info<false>(P, key_of[id]);
+    const Fwd s = fwd_info(P, key_of[id]);
     O.arc_offset[id] = (int32_t)pos;
     O.accept[id] = s.accept ? 1 : 0;
     O.start[id] = s.start ? 1 : 0;
@@ -1245,7 +1419,8 @@ hipError_t launch_count(const Problem &P, const uint32_t *key_of, uint32_t nstat
                         uint32_t *cnt, uint32_t *btot, uint32_t *heavy, Scalars *sc,
                         hipStream_t s) {
   if (!nstates) return hipSuccess;
-  k_count<<<out_grid(nstates, per), NT, 0, s>>>(P, key_of, nstates, per, cnt, btot, heavy, sc);
+  k_count<<<out_grid(nstates, per), NT, 0, s>>>(P, key_of, nstates, per, cnt, btot, heavy, sc,
+                                                out_chunks(nstates, per));
   return hipGetLastError();
 }
 

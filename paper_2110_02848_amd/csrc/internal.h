@@ -18,18 +18,22 @@ constexpr uint32_t LIGHT_SEARCH = 64;  // search: a key with more units is split
 constexpr int CHAIN_MAX = 64;          // search: default depth-first budget per thread
 constexpr uint32_t NO_KEY = 0xFFFFFFFFu;
 
-// The output passes give every workgroup one contiguous chunk of states
-// (a multiple of NT), so the arcs a workgroup writes are contiguous and
-// stay in one L2; at most OUT_BLOCKS chunks.
-constexpr size_t OUT_BLOCKS = 8192;
+// The output passes give every wavefront one contiguous chunk of states (a
+// multiple of WAVE; at most OUT_CHUNKS chunks), so the arcs a wavefront
+// writes are contiguous and its offsets need only wavefront scans.  Every
+// workgroup covers NWAVES consecutive chunks.
+constexpr size_t OUT_CHUNKS = 32768;
 inline size_t out_chunk(size_t n) {
-  size_t per = (n + OUT_BLOCKS - 1) / OUT_BLOCKS;
-  per = (per + NT - 1) / NT * NT;
-  return per ? per : (size_t)NT;
+  size_t per = (n + OUT_CHUNKS - 1) / OUT_CHUNKS;
+  per = (per + WAVE - 1) / WAVE * WAVE;
+  return per ? per : (size_t)WAVE;
 }
-inline unsigned out_grid(size_t n, size_t per) {
+inline unsigned out_chunks(size_t n, size_t per) {
   const size_t g = (n + per - 1) / per;
   return (unsigned)(g ? g : 1);
+}
+inline unsigned out_grid(size_t n, size_t per) {
+  return (out_chunks(n, per) + NWAVES - 1) / NWAVES;
 }
 
 // ---------------------------------------------------------------------------
@@ -328,9 +332,9 @@ hipError_t launch_trim_words(uint32_t *coacc, const uint32_t *vis, uint32_t *cnt
                              hipStream_t s);
 hipError_t launch_key_of_id(const uint32_t *bm, const uint32_t *wbase, size_t nwords,
                             uint32_t *key_of, hipStream_t s);
-// Kept-arc count of every state of C (chunks of `per` states per workgroup):
-// cnt[id] for light states, heavy state ids listed in `heavy` (count in
-// Scalars::heavy), btot[chunk] = the chunk's light total.
+// Kept-arc count of every state of C (chunks of `per` states per
+// wavefront): cnt[id] for light states, heavy state ids listed in `heavy`
+// (count in Scalars::heavy), btot[chunk] = the chunk's light total.
 hipError_t launch_count(const Problem &P, const uint32_t *key_of, uint32_t nstates, size_t per,
                         uint32_t *cnt, uint32_t *btot, uint32_t *heavy, Scalars *sc,
                         hipStream_t s);
