@@ -235,7 +235,9 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   if (VA) HIP_TRY(launch_validate(dA, 0, &d_sc->errA, &d_sc->maxLabA, s));
   if (VB) HIP_TRY(launch_validate(dB, 1, &d_sc->errB, &d_sc->maxLabB, s));
   FST_TRY(readback(c, s));
-  if (c->h_sc->errA || c->h_sc->errB) return FST_ERR_INVALID_GRAPH;
+  const uint32_t info_bits = 1u << 16;  // validation's "not in label order" note
+  if ((c->h_sc->errA & ~info_bits) || (c->h_sc->errB & ~info_bits)) return FST_ERR_INVALID_GRAPH;
+  const bool presortedA = !(c->h_sc->errA & info_bits), presortedB = !(c->h_sc->errB & info_bits);
   c->stats = fst_stats{};
   if (VA == 0 || VB == 0) return finish_empty(c, V_C, E_C);
 
@@ -296,23 +298,26 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   }
   for (int i = 0; i < 4; ++i) {
     const bool isA = (i % 2) == 0, in = i >= 2;
-    HIP_TRY(sort_view(isA ? dA : dB, isA ? 0 : 1, in, isA ? labA : labB, rec[i], arc[i], perm[i],
-                      olab[i], wv[i], in ? as<int32_t>(*vb[i].off) : nullptr,
-                      i == 2 ? rec[0] : nullptr, k0, v0, k1, v1, c->sort_tmp.p,
-                      i == 0 ? &d_sc->nEpsStatesA : nullptr, s));
+    HIP_TRY(sort_view(isA ? dA : dB, isA ? 0 : 1, in, isA ? presortedA : presortedB,
+                      isA ? labA : labB, rec[i], arc[i], perm[i], olab[i], wv[i],
+                      in ? as<int32_t>(*vb[i].off) : nullptr, i == 2 ? rec[0] : nullptr, k0, v0,
+                      k1, v1, c->sort_tmp.p, i == 0 ? &d_sc->nEpsStatesA : nullptr, s));
   }
-  // a view's FLAG_UNIQ comes from the opposite view of the same graph
-  for (int i = 0; i < 4; ++i) {
-    const bool isA = (i % 2) == 0, in = i >= 2;
-    HIP_TRY(mark_unique(isA ? dA : dB, isA ? 0 : 1, !in, rec[i], rec[i ^ 2], arc[i ^ 2], s));
-  }
+  // a view's FLAG_UNIQ comes from the opposite view (i ^ 2) of the same graph
+  ViewJobs J = {};
   View views[4];
   for (int i = 0; i < 4; ++i) {
-    const bool isA = (i % 2) == 0;
+    const bool isA = (i % 2) == 0, in = i >= 2;
+    const DevGraph &g = isA ? dA : dB;
     const uint32_t lmax = isA ? maxA : maxB;
-    HIP_TRY(finish_view(isA ? dA : dB, (int32_t)lmax, rec[i], arc[i], lutp[i], s));
+    J.j[i] = ViewJob{rec[i], arc[i], lutp[i], rec[i ^ 2], arc[i ^ 2], in ? g.accept : g.start,
+                     isA ? 0 : 1, in ? 0 : 1, (int32_t)lmax + 1};
+    J.vbegin[i + 1] = J.vbegin[i] + g.V;
+    J.ebegin[i + 1] = J.ebegin[i] + g.E;
+    J.lbegin[i + 1] = J.lbegin[i] + (lutp[i] ? (long long)g.V * ((long long)lmax + 1) : 0);
     views[i] = View{rec[i], arc[i], perm[i], lutp[i], (int32_t)lmax + 1, olab[i], wv[i]};
   }
+  HIP_TRY(finish_views(J, s));
   FST_TRY(readback(c, s));
 
   // ---- search state ----

@@ -22,6 +22,9 @@ namespace {
 typedef unsigned long long ull;
 
 enum : uint32_t { ERR_OFFSETS = 1, ERR_SRC = 2, ERR_DST = 4, ERR_LABEL = 8, ERR_FLAG = 16 };
+// Validation also notes whether some state's arcs are not ordered by the
+// matched label (then the out-view is sorted; otherwise it is the input).
+constexpr uint32_t INFO_UNSORTED = 1u << 16;
 
 unsigned grid_for(size_t n, unsigned cap = 4096) {
   size_t g = (n + NT - 1) / NT;
@@ -84,6 +87,8 @@ __global__ __launch_bounds__(NT) void k_validate(DevGraph g, int side, uint32_t 
         bits |= ERR_SRC;
       } else if (!(g.off[s] <= i && i < g.off[s + 1])) {
         bits |= ERR_SRC;
+      } else if (i > g.off[s] && (side == 0 ? g.ol[i - 1] : g.il[i - 1]) > (side == 0 ? ol : il)) {
+        bits |= INFO_UNSORTED;  // not an error: the out-view needs a sort
       }
       int32_t lab = side == 0 ? ol : il;
       if (lab > 0 && (uint32_t)lab > mx) mx = (uint32_t)lab;
@@ -132,7 +137,8 @@ __global__ __launch_bounds__(NT) void k_split(DevGraph g, int by_dst, const ull 
   const ull mask = (lab_bits >= 64) ? ~0ull : ((1ull << lab_bits) - 1ull);
   for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n;
        i += (long long)gridDim.x * NT) {
-    const int32_t e = v[i];
+    // without sorted pairs (k null) the arcs are already in view order
+    const int32_t e = k ? v[i] : (int32_t)i;
     perm[i] = e;
     if (olab) {
       olab[i] = side == 0 ? g.il[e] : g.ol[e];
@@ -140,7 +146,7 @@ __global__ __launch_bounds__(NT) void k_split(DevGraph g, int by_dst, const ull 
     }
     int32_t nb = by_dst ? g.src[e] : g.dst[e];
     if (eps_rec && eps_rec[2 * (size_t)nb].y > 0) nb |= NBR_EPS;
-    arec[i] = make_int2((int32_t)(k[i] & mask), nb);
+    arec[i] = make_int2(k ? (int32_t)(k[i] & mask) : (side == 0 ? g.ol[e] : g.il[e]), nb);
   }
 }
 
@@ -193,69 +199,83 @@ __global__ __launch_bounds__(NT) void k_state_rec(const int32_t *__restrict__ of
 // not checked one by one).
 constexpr int32_t UNIQ_SCAN_MAX = 256;
 
-// FLAG_UNIQ of the records `self` of a view, from the opposite view's groups.
-__global__ __launch_bounds__(NT) void k_mark_unique(int V, int side, int out_view,
-                                                    const uint8_t *__restrict__ excl,
-                                                    int4 *__restrict__ self,
-                                                    const int4 *__restrict__ other,
-                                                    const int2 *__restrict__ oarec) {
-  for (long long v = (long long)blockIdx.x * NT + threadIdx.x; v < V;
-       v += (long long)gridDim.x * NT) {
-    const int4 o = other[2 * v];
-    const int4 me = self[2 * v];
+// The four views are finished together: each kernel runs over the
+// concatenated states (or arcs, or bucket entries) of all views; a thread
+// finds its view with a few comparisons against the prefix sums.
+__device__ __forceinline__ int job_of(const ViewJobs &J, const long long *begin, long long i) {
+  int j = 0;
+#pragma unroll
+  for (int t = 1; t < 4; ++t)
+    if (i >= begin[t]) j = t;
+  return j;
+}
+
+// FLAG_UNIQ of a view's records, from the opposite view's groups.
+__global__ __launch_bounds__(NT) void k_mark_unique(ViewJobs J) {
+  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < J.vbegin[4];
+       i += (long long)gridDim.x * NT) {
+    const int j = job_of(J, J.vbegin, i);
+    const ViewJob &b = J.j[j];
+    const long long v = i - J.vbegin[j];
+    const int4 o = b.other[2 * v];
+    const int4 me = b.srec[2 * v];
     const int32_t n = o.z - o.x;
-    bool u = excl[v] == 0;
-    if (side == 1) {
+    bool u = b.excl[v] == 0;
+    if (b.side == 1) {
       u = u && n == 1;
     } else {
       // no epsilon output of v itself (out-view: its own epsilon count)
-      if (out_view && me.y != 0) u = false;
+      if (b.out_view && me.y != 0) u = false;
       if (o.y != 0 || n > UNIQ_SCAN_MAX) u = false;
-      for (int32_t i = o.x; u && i < o.z; ++i) {
-        const int2 a = oarec[i];
-        if (a.y & NBR_EPS) u = false;                          // source has epsilon output
-        if (i > o.x && oarec[i - 1].x == a.x) u = false;      // repeated label
+      for (int32_t k = o.x; u && k < o.z; ++k) {
+        const int2 a = b.other_arec[k];
+        if (a.y & NBR_EPS) u = false;                              // source has epsilon output
+        if (k > o.x && b.other_arec[k - 1].x == a.x) u = false;    // repeated label
       }
     }
-    if (u) self[2 * v] = make_int4(me.x, me.y, me.z, me.w | (int32_t)FLAG_UNIQ);
+    if (u) b.srec[2 * v] = make_int4(me.x, me.y, me.z, me.w | (int32_t)FLAG_UNIQ);
   }
 }
 
-// Mark every arc whose other end has FLAG_UNIQ in this view.
-__global__ __launch_bounds__(NT) void k_mark_arcs(int2 *__restrict__ arec,
-                                                  const int4 *__restrict__ srec, long long E) {
-  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < E;
+// Mark every arc whose other end has FLAG_UNIQ in its view.
+__global__ __launch_bounds__(NT) void k_mark_arcs(ViewJobs J) {
+  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < J.ebegin[4];
        i += (long long)gridDim.x * NT) {
-    const int2 a = arec[i];
-    if (srec[2 * (size_t)(a.y & NBR_MASK)].w & (int32_t)FLAG_UNIQ)
-      arec[i] = make_int2(a.x, a.y | NBR_UNIQ);
+    const int j = job_of(J, J.ebegin, i);
+    const ViewJob &b = J.j[j];
+    const long long e = i - J.ebegin[j];
+    const int2 a = b.arec[e];
+    if (b.srec[2 * (size_t)(a.y & NBR_MASK)].w & (int32_t)FLAG_UNIQ)
+      b.arec[e] = make_int2(a.x, a.y | NBR_UNIQ);
   }
 }
 
 // Second state record: the first epsilon and first non-epsilon arcs.
-__global__ __launch_bounds__(NT) void k_state_inline(int4 *__restrict__ srec,
-                                                     const int2 *__restrict__ arec, int V) {
-  for (long long v = (long long)blockIdx.x * NT + threadIdx.x; v < V;
-       v += (long long)gridDim.x * NT) {
-    const int4 r = srec[2 * v];
-    const int2 first_ne = r.x + r.y < r.z ? arec[r.x + r.y] : make_int2(0, 0);
-    srec[2 * v + 1] = make_int4(r.y > 0 ? arec[r.x].y : 0, first_ne.x, first_ne.y, 0);
+__global__ __launch_bounds__(NT) void k_state_inline(ViewJobs J) {
+  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < J.vbegin[4];
+       i += (long long)gridDim.x * NT) {
+    const int j = job_of(J, J.vbegin, i);
+    const ViewJob &b = J.j[j];
+    const long long v = i - J.vbegin[j];
+    const int4 r = b.srec[2 * v];
+    const int2 first_ne = r.x + r.y < r.z ? b.arec[r.x + r.y] : make_int2(0, 0);
+    b.srec[2 * v + 1] = make_int4(r.y > 0 ? b.arec[r.x].y : 0, first_ne.x, first_ne.y, 0);
   }
 }
 
 // Label buckets: lut[v * S + l] = {first position of label l, first > l,
-// neighbour of the first arc (or -1), 0}.
-__global__ __launch_bounds__(NT) void k_build_lut(const int4 *__restrict__ srec,
-                                                  const int2 *__restrict__ arec, int V, int S,
-                                                  int4 *__restrict__ lut) {
-  const long long n = (long long)V * S;
-  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n;
+// neighbour of the first arc (or -1), 0}, for the views that have them.
+__global__ __launch_bounds__(NT) void k_build_lut(ViewJobs J) {
+  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < J.lbegin[4];
        i += (long long)gridDim.x * NT) {
-    const int32_t v = (int32_t)(i / S), l = (int32_t)(i % S);
-    const int4 r = srec[2 * (size_t)v];
-    const int32_t lo = lb_label(arec, r.x, r.z, l);
-    const int32_t hi = lb_label(arec, lo, r.z, l + 1);
-    lut[i] = make_int4(lo, hi, lo < hi ? arec[lo].y : -1, 0);
+    const int j = job_of(J, J.lbegin, i);
+    const ViewJob &b = J.j[j];
+    const long long x = i - J.lbegin[j];
+    const int32_t v = (int32_t)(x / b.lstride), l = (int32_t)(x % b.lstride);
+    const int4 r = b.srec[2 * (size_t)v];
+    const int32_t lo = lb_label(b.arec, r.x, r.z, l);
+    const int32_t hi = lb_label(b.arec, lo, r.z, l + 1);
+    b.lut[x] = make_int4(lo, hi, lo < hi ? b.arec[lo].y : -1, 0);
   }
 }
 
@@ -1299,20 +1319,23 @@ hipError_t launch_validate(const DevGraph &g, int side, uint32_t *err, uint32_t 
   return hipGetLastError();
 }
 
-hipError_t sort_view(const DevGraph &g, int side, bool by_dst, int lab_bits, int4 *srec,
-                     int2 *arec, int32_t *perm, int32_t *olab, float *w, int32_t *off_tmp,
-                     const int4 *eps_rec, unsigned long long *k0, int32_t *v0,
+hipError_t sort_view(const DevGraph &g, int side, bool by_dst, bool presorted, int lab_bits,
+                     int4 *srec, int2 *arec, int32_t *perm, int32_t *olab, float *w,
+                     int32_t *off_tmp, const int4 *eps_rec, unsigned long long *k0, int32_t *v0,
                      unsigned long long *k1, int32_t *v1, void *sort_temp, uint32_t *eps_states,
                      hipStream_t s) {
   const size_t E = (size_t)g.E;
   hipError_t e;
   if (E) {
-    k_make_keys<<<grid_for(E), NT, 0, s>>>(g, side, by_dst ? 1 : 0, lab_bits, k0, v0);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    int bits = bitlen((unsigned long long)(g.V > 0 ? g.V - 1 : 0)) + lab_bits;
-    if ((e = radix_sort(k0, v0, k1, v1, E, bits, sort_temp, s)) != hipSuccess) return e;
-    k_split<<<grid_for(E), NT, 0, s>>>(g, by_dst ? 1 : 0, k0, v0, (long long)E, lab_bits,
-                                       eps_rec, side, perm, olab, w, arec);
+    const bool sort = by_dst || !presorted;
+    if (sort) {
+      k_make_keys<<<grid_for(E), NT, 0, s>>>(g, side, by_dst ? 1 : 0, lab_bits, k0, v0);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+      int bits = bitlen((unsigned long long)(g.V > 0 ? g.V - 1 : 0)) + lab_bits;
+      if ((e = radix_sort(k0, v0, k1, v1, E, bits, sort_temp, s)) != hipSuccess) return e;
+    }
+    k_split<<<grid_for(E), NT, 0, s>>>(g, by_dst ? 1 : 0, sort ? k0 : nullptr, sort ? v0 : nullptr,
+                                       (long long)E, lab_bits, eps_rec, side, perm, olab, w, arec);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   const int32_t *off = g.off;
@@ -1332,29 +1355,22 @@ hipError_t sort_view(const DevGraph &g, int side, bool by_dst, int lab_bits, int
   return hipSuccess;
 }
 
-hipError_t mark_unique(const DevGraph &g, int side, bool out_view, int4 *self,
-                       const int4 *other, const int2 *other_arec, hipStream_t s) {
-  if (!g.V) return hipSuccess;
-  // out-views exclude start states, in-views accepting states
-  k_mark_unique<<<grid_for((size_t)g.V), NT, 0, s>>>(g.V, side, out_view ? 1 : 0,
-                                                     out_view ? g.start : g.accept, self, other,
-                                                     other_arec);
-  return hipGetLastError();
-}
-
-hipError_t finish_view(const DevGraph &g, int32_t lab_max, int4 *srec, int2 *arec, int4 *lut,
-                       hipStream_t s) {
+hipError_t finish_views(ViewJobs J, hipStream_t s) {
   hipError_t e;
-  if (g.E) {
-    k_mark_arcs<<<grid_for((size_t)g.E), NT, 0, s>>>(arec, srec, (long long)g.E);
+  if (J.vbegin[4]) {
+    k_mark_unique<<<grid_for((size_t)J.vbegin[4]), NT, 0, s>>>(J);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  if (!g.V) return hipSuccess;
-  k_state_inline<<<grid_for((size_t)g.V, 256), NT, 0, s>>>(srec, arec, g.V);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  if (lut) {
-    const size_t n = (size_t)g.V * (size_t)(lab_max + 1);
-    k_build_lut<<<grid_for(n, 8192), NT, 0, s>>>(srec, arec, g.V, lab_max + 1, lut);
+  if (J.ebegin[4]) {
+    k_mark_arcs<<<grid_for((size_t)J.ebegin[4]), NT, 0, s>>>(J);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  if (J.vbegin[4]) {
+    k_state_inline<<<grid_for((size_t)J.vbegin[4]), NT, 0, s>>>(J);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  if (J.lbegin[4]) {
+    k_build_lut<<<grid_for((size_t)J.lbegin[4], 8192), NT, 0, s>>>(J);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   return hipSuccess;
@@ -1388,8 +1404,9 @@ hipError_t launch_generation(const Problem &P, const SearchArgs &S, bool forward
 hipError_t launch_count_moves(const Problem &P, size_t nwords, bool forward,
                               unsigned long long *out, hipStream_t s) {
   if (!nwords) return hipSuccess;
-  if (forward) k_count_moves<true><<<grid_for(nwords * 32, 8192), NT, 0, s>>>(P, nwords, out);
-  else k_count_moves<false><<<grid_for(nwords * 32, 8192), NT, 0, s>>>(P, nwords, out);
+  const unsigned g = grid_for(nwords * 32, 1u << 17);
+  if (forward) k_count_moves<true><<<g, NT, 0, s>>>(P, nwords, out);
+  else k_count_moves<false><<<g, NT, 0, s>>>(P, nwords, out);
   return hipGetLastError();
 }
 

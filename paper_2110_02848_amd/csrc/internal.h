@@ -284,28 +284,43 @@ hipError_t radix_sort(unsigned long long *k0, int32_t *v0, unsigned long long *k
 // ---------------------------------------------------------------------------
 hipError_t launch_validate(const DevGraph &g, int side, uint32_t *err, uint32_t *maxlab,
                            hipStream_t s);
-// Views are built in three steps.  sort_view: sort the arcs of a view (side
+// Views are built in two steps.  sort_view: sort the arcs of a view (side
 // 0: A by olabel, side 1: B by ilabel; by_dst selects in-views, for which
-// `off_tmp` (V+1 words) receives the group offsets) into arec / perm and
-// write the first record of every state.  k0/v0/k1/v1 are E-sized sort
-// buffers.  eps_rec is A's out-view records when building A's in-view (to
-// carry epsOutA), else null.  If eps_states is set, it counts the states with
-// an epsilon arc in the view.  Then mark_unique (once all four views are
-// sorted) sets FLAG_UNIQ; then finish_view marks the arcs, writes the second
-// record of every state and, if lut is set, the label buckets of every group
-// (V * (lab_max + 1) entries).
-hipError_t sort_view(const DevGraph &g, int side, bool by_dst, int lab_bits, int4 *srec,
-                     int2 *arec, int32_t *perm, int32_t *olab, float *w, int32_t *off_tmp,
-                     const int4 *eps_rec, unsigned long long *k0, int32_t *v0,
+// `off_tmp` (V+1 words) receives the group offsets; an out-view of an input
+// whose groups are already in label order (presorted) is not sorted) into
+// arec / perm, gather olab / w for out-views, and write the first record of
+// every state.  k0/v0/k1/v1 are E-sized sort buffers.  eps_rec is A's
+// out-view records when building A's in-view (to carry epsOutA), else null.
+// If eps_states is set, it counts the states with an epsilon arc in the
+// view.  Then finish_views (once all four views are sorted) sets FLAG_UNIQ
+// (from the opposite view of the same graph), marks the arcs, writes the
+// second record of every state and the label buckets.
+hipError_t sort_view(const DevGraph &g, int side, bool by_dst, bool presorted, int lab_bits,
+                     int4 *srec, int2 *arec, int32_t *perm, int32_t *olab, float *w,
+                     int32_t *off_tmp, const int4 *eps_rec, unsigned long long *k0, int32_t *v0,
                      unsigned long long *k1, int32_t *v1, void *sort_temp, uint32_t *eps_states,
                      hipStream_t s);
-// FLAG_UNIQ for the records `self` of a view of graph g, from the groups of
-// the opposite view of the same graph (`other`, `other_arec`): side 0 = A,
-// side 1 = B; out_view says whether `self` is an out-view.
-hipError_t mark_unique(const DevGraph &g, int side, bool out_view, int4 *self,
-                       const int4 *other, const int2 *other_arec, hipStream_t s);
-hipError_t finish_view(const DevGraph &g, int32_t lab_max, int4 *srec, int2 *arec, int4 *lut,
-                       hipStream_t s);
+
+// One view for finish_views: its records and arcs, the opposite view's
+// (`other`), the states excluded from FLAG_UNIQ (start states for out-views,
+// accepting states for in-views), the graph side (0 = A, 1 = B) and, when
+// lut is set, its bucket table with lstride labels per state.
+struct ViewJob {
+  int4 *srec;
+  int2 *arec;
+  int4 *lut;
+  const int4 *other;
+  const int2 *other_arec;
+  const uint8_t *excl;
+  int32_t side, out_view, lstride;
+};
+// Four views with the prefix sums of their state, arc and bucket counts
+// (entry 4 is the total).
+struct ViewJobs {
+  ViewJob j[4];
+  long long vbegin[5], ebegin[5], lbegin[5];
+};
+hipError_t finish_views(ViewJobs J, hipStream_t s);
 // Collect the start states of A and B into la/lb (counts na/nb, zeroed by the
 // caller) and place every start key in generation 0 of the forward search.
 // Accepting keys reached by the forward search (start keys included) are
