@@ -301,7 +301,7 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
     HIP_TRY(sort_view(isA ? dA : dB, isA ? 0 : 1, in, isA ? presortedA : presortedB,
                       isA ? labA : labB, rec[i], arc[i], perm[i], olab[i], wv[i],
                       in ? as<int32_t>(*vb[i].off) : nullptr, i == 2 ? rec[0] : nullptr, k0, v0,
-                      k1, v1, c->sort_tmp.p, i == 0 ? &d_sc->nEpsStatesA : nullptr, s));
+                      k1, v1, c->sort_tmp.p, nullptr, s));
   }
   // a view's FLAG_UNIQ comes from the opposite view (i ^ 2) of the same graph
   ViewJobs J = {};
@@ -318,12 +318,12 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
     views[i] = View{rec[i], arc[i], perm[i], lutp[i], (int32_t)lmax + 1, olab[i], wv[i]};
   }
   HIP_TRY(finish_views(J, s));
-  FST_TRY(readback(c, s));
 
   // ---- search state ----
-  const unsigned long long capll =
-      (unsigned long long)VB * ((unsigned long long)VA + c->h_sc->nEpsStatesA);
-  const uint32_t cap = (uint32_t)capll;  // <= nkeys < 2^32
+  // every list holds at most one entry per key: 2 V_A V_B bounds the keys
+  // (f = 1 only where epsOutA), without waiting for a count of those states
+  const unsigned long long capll = 2ull * (unsigned long long)VA * (unsigned long long)VB;
+  const uint32_t cap = (uint32_t)(capll < nkeys ? capll : nkeys);  // <= nkeys < 2^32
   const size_t nwords = (size_t)((nkeys + 31) / 32);
   FST_TRY(ensure(c, c->vis, nwords * 4));
   FST_TRY(ensure(c, c->coacc, nwords * 4));

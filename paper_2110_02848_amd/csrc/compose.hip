@@ -1328,23 +1328,29 @@ hipError_t sort_view(const DevGraph &g, int side, bool by_dst, bool presorted, i
   hipError_t e;
   if (E) {
     const bool sort = by_dst || !presorted;
+    bool second = false;
     if (sort) {
       k_make_keys<<<grid_for(E), NT, 0, s>>>(g, side, by_dst ? 1 : 0, lab_bits, k0, v0);
       if ((e = hipGetLastError()) != hipSuccess) return e;
       int bits = bitlen((unsigned long long)(g.V > 0 ? g.V - 1 : 0)) + lab_bits;
-      if ((e = radix_sort(k0, v0, k1, v1, E, bits, sort_temp, s)) != hipSuccess) return e;
+      if ((e = radix_sort(k0, v0, k1, v1, E, bits, sort_temp, s, &second)) != hipSuccess)
+        return e;
     }
-    k_split<<<grid_for(E), NT, 0, s>>>(g, by_dst ? 1 : 0, sort ? k0 : nullptr, sort ? v0 : nullptr,
-                                       (long long)E, lab_bits, eps_rec, side, perm, olab, w, arec);
+    const ull *ks = sort ? (second ? k1 : k0) : nullptr;
+    const int32_t *vs = sort ? (second ? v1 : v0) : nullptr;
+    k_split<<<grid_for(E), NT, 0, s>>>(g, by_dst ? 1 : 0, ks, vs, (long long)E, lab_bits, eps_rec,
+                                       side, perm, olab, w, arec);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (by_dst) {
+      k_group_offsets<<<grid_for((size_t)g.V + 1), NT, 0, s>>>(ks, (long long)E, g.V, lab_bits,
+                                                              off_tmp);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+  } else if (by_dst) {
+    k_group_offsets<<<grid_for((size_t)g.V + 1), NT, 0, s>>>(nullptr, 0, g.V, lab_bits, off_tmp);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  const int32_t *off = g.off;
-  if (by_dst) {
-    k_group_offsets<<<grid_for((size_t)g.V + 1), NT, 0, s>>>(k0, (long long)E, g.V, lab_bits,
-                                                            off_tmp);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    off = off_tmp;
-  }
+  const int32_t *off = by_dst ? off_tmp : g.off;
   if (g.V) {
     const int eps_mode = side == 1 ? 0 : (by_dst ? 2 : 1);
     k_state_rec<<<grid_for((size_t)g.V, 256), NT, 0, s>>>(off, arec, g.V, g.accept,

@@ -274,10 +274,11 @@ hipError_t scan_u32(const uint32_t *in, uint32_t *out, size_t n, bool out_last,
 
 // Bytes of temporary storage for radix_sort over n elements.
 size_t sort_temp_bytes(size_t n);
-// Stable LSD radix sort of (key, value) pairs on the low `bits` key bits.
-// The sorted result is left in (k0, v0); (k1, v1) are scratch of equal size.
+// Stable LSD radix sort of (key, value) pairs on the low `bits` key bits,
+// ping-ponging between (k0, v0) and (k1, v1); *in_second says whether the
+// sorted result ended in (k1, v1).
 hipError_t radix_sort(unsigned long long *k0, int32_t *v0, unsigned long long *k1, int32_t *v1,
-                      size_t n, int bits, void *temp, hipStream_t s);
+                      size_t n, int bits, void *temp, hipStream_t s, bool *in_second);
 
 // ---------------------------------------------------------------------------
 // Host-side launchers (compose.hip)

@@ -169,7 +169,8 @@ size_t sort_temp_bytes(size_t n) {
 }
 
 hipError_t radix_sort(unsigned long long *k0, int32_t *v0, unsigned long long *k1, int32_t *v1,
-                      size_t n, int bits, void *temp, hipStream_t s) {
+                      size_t n, int bits, void *temp, hipStream_t s, bool *in_second) {
+  *in_second = false;
   if (n == 0 || bits <= 0) return hipSuccess;
   const uint32_t nb = (uint32_t)((n + SORT_TILE - 1) / SORT_TILE);
   const size_t nh = (size_t)256 * nb;
@@ -193,12 +194,7 @@ hipError_t radix_sort(unsigned long long *k0, int32_t *v0, unsigned long long *k
     ull *tk = ka; ka = kb; kb = tk;
     int32_t *tv = va; va = vb; vb = tv;
   }
-  if (ka != k0) {
-    hipError_t e = hipMemcpyAsync(k0, ka, n * sizeof(ull), hipMemcpyDeviceToDevice, s);
-    if (e != hipSuccess) return e;
-    e = hipMemcpyAsync(v0, va, n * sizeof(int32_t), hipMemcpyDeviceToDevice, s);
-    if (e != hipSuccess) return e;
-  }
+  *in_second = ka != k0;
   return hipSuccess;
 }
 
