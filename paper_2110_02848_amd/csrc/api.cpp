@@ -44,7 +44,7 @@ struct fst_ctx {
   DevBuf scal, lists;
   DevBuf k0, k1, v0, v1, sort_tmp, scan_tmp;
   DevBuf aOutPerm, aOutArc, aOutRec, aOutLut, bOutPerm, bOutArc, bOutRec, bOutLut;
-  DevBuf aOutLab, aOutW, bOutLab, bOutW;
+  DevBuf aOutLab, aOutW, bOutLab, bOutW, bOutChain, bInChain;
   DevBuf aInOff, aInPerm, aInArc, aInRec, aInLut, bInOff, bInPerm, bInArc, bInRec, bInLut;
   DevBuf vis, coacc, wbase, fq, bq, heavy, hoff, cnt, btot;
   Scalars *h_sc = nullptr;
@@ -210,8 +210,10 @@ int search(fst_ctx *c, const SearchArgs &S, bool forward, int64_t *levels, hipSt
   return FST_OK;
 }
 
-// Label buckets are kept when the table is at most this large.
+// Label buckets are kept when the table is at most this large; so are the
+// chain records of each view of B.
 constexpr size_t LUT_BUDGET = (size_t)256 << 20;
+constexpr size_t CHAIN_BUDGET = (size_t)256 << 20;
 
 size_t lut_bytes(int32_t V, uint32_t lab_max) {
   return (size_t)V * ((size_t)lab_max + 1) * sizeof(int4);
@@ -310,12 +312,18 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
     const bool isA = (i % 2) == 0, in = i >= 2;
     const DevGraph &g = isA ? dA : dB;
     const uint32_t lmax = isA ? maxA : maxB;
+    // chain records for B's views, when they fit the budget
+    int4 *chain = nullptr;
+    if (!isA && (size_t)g.V * 4 * sizeof(int4) <= CHAIN_BUDGET) {
+      FST_TRY(ensure(c, in ? c->bInChain : c->bOutChain, (size_t)g.V * 4 * sizeof(int4)));
+      chain = as<int4>(in ? c->bInChain : c->bOutChain);
+    }
     J.j[i] = ViewJob{rec[i], arc[i], lutp[i], rec[i ^ 2], arc[i ^ 2], in ? g.accept : g.start,
-                     isA ? 0 : 1, in ? 0 : 1, (int32_t)lmax + 1};
+                     isA ? 0 : 1, in ? 0 : 1, (int32_t)lmax + 1, chain};
     J.vbegin[i + 1] = J.vbegin[i] + g.V;
     J.ebegin[i + 1] = J.ebegin[i] + g.E;
     J.lbegin[i + 1] = J.lbegin[i] + (lutp[i] ? (long long)g.V * ((long long)lmax + 1) : 0);
-    views[i] = View{rec[i], arc[i], perm[i], lutp[i], (int32_t)lmax + 1, olab[i], wv[i]};
+    views[i] = View{rec[i], arc[i], perm[i], lutp[i], (int32_t)lmax + 1, olab[i], wv[i], chain};
   }
   HIP_TRY(finish_views(J, s));
 
@@ -484,7 +492,8 @@ void fst_ctx_destroy(fst_ctx *c) {
                     &c->aInLut,   &c->bInOff,   &c->bInPerm, &c->bInArc,  &c->bInRec,
                     &c->bInLut,   &c->vis,      &c->coacc,   &c->wbase,   &c->fq,
                     &c->bq,       &c->heavy,    &c->hoff,    &c->cnt,     &c->aOutLab,
-                    &c->aOutW,    &c->bOutLab,  &c->bOutW,   &c->btot};
+                    &c->aOutW,    &c->bOutLab,  &c->bOutW,   &c->btot,    &c->bOutChain,
+                    &c->bInChain};
   for (DevBuf *b : bufs) release(*b);
   for (int i = 0; i < NEV; ++i)
     if (c->ev[i]) (void)hipEventDestroy(c->ev[i]);

@@ -224,8 +224,9 @@ __global__ __launch_bounds__(NT) void k_mark_unique(ViewJobs J) {
     if (b.side == 1) {
       u = u && n == 1;
     } else {
-      // no epsilon output of v itself (out-view: its own epsilon count)
-      if (b.out_view && me.y != 0) u = false;
+      // no epsilon arc of v itself in this view (out-view: no epsilon
+      // output; in-view: no epsilon in-arc)
+      if (me.y != 0) u = false;
       if (o.y != 0 || n > UNIQ_SCAN_MAX) u = false;
       for (int32_t k = o.x; u && k < o.z; ++k) {
         const int2 a = b.other_arec[k];
@@ -260,6 +261,39 @@ __global__ __launch_bounds__(NT) void k_state_inline(ViewJobs J) {
     const int4 r = b.srec[2 * v];
     const int2 first_ne = r.x + r.y < r.z ? b.arec[r.x + r.y] : make_int2(0, 0);
     b.srec[2 * v + 1] = make_int4(r.y > 0 ? b.arec[r.x].y : 0, first_ne.x, first_ne.y, 0);
+  }
+}
+
+// Chain records of the views that have them (see View).
+__global__ __launch_bounds__(NT) void k_chains(ViewJobs J) {
+  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < J.vbegin[4];
+       i += (long long)gridDim.x * NT) {
+    const int j = job_of(J, J.vbegin, i);
+    const ViewJob &b = J.j[j];
+    if (!b.chain) continue;
+    const long long v = i - J.vbegin[j];
+    int32_t w[4 * 4] = {};
+    int n = 0;
+    uint32_t cur = (uint32_t)v;
+#pragma unroll
+    for (int k = 0; k < CHAIN_STEPS; ++k) {
+      if (n == k) {
+        const int4 r = b.srec[2 * (size_t)cur];
+        const int2 a = r.z - r.x == 1 ? b.arec[r.x] : make_int2(0, 0);
+        const bool step = r.z - r.x == 1 && a.x != 0 && (a.y & NBR_UNIQ) &&
+                          !(b.out_view && (r.w & (int32_t)FLAG_ACCEPT));
+        if (step) {
+          w[1 + 2 * k] = a.x;
+          w[2 + 2 * k] = a.y;
+          cur = (uint32_t)(a.y & NBR_MASK);
+          n = k + 1;
+        }
+      }
+    }
+    w[0] = n;
+    int4 *c = b.chain + 4 * v;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) c[q] = make_int4(w[4 * q], w[4 * q + 1], w[4 * q + 2], w[4 * q + 3]);
   }
 }
 
@@ -785,6 +819,81 @@ __device__ __forceinline__ void visit(const Problem &P, const SearchArgs &S, con
   place<FWD>(P, S, nx, fresh, v, vi, nk, depth);
 }
 
+// Chain jumps.  A key whose only move follows the single arc of its B state
+// takes up to CHAIN_STEPS hops from the B state's chain record (one load) and
+// one bucket lookup in A per hop; every reached key has both states marked
+// FLAG_UNIQ (so it needs no claim) and exactly one move, so it is expanded
+// on the spot.  Forward, the reached keys get their accessible bits;
+// backward, the accessible bits of all reached keys are loaded at once and
+// the jump stops before the first key that is not accessible.  The last key
+// reached goes to place(); depth advances by the keys expanded.  Returns
+// false (nothing done) when the key does not have that shape.
+__device__ __forceinline__ uint32_t state_a(const Fwd &s) { return s.qa; }
+__device__ __forceinline__ uint32_t state_b(const Fwd &s) { return s.qb; }
+__device__ __forceinline__ uint32_t state_a(const Bwd &s) { return s.va; }
+__device__ __forceinline__ uint32_t state_b(const Bwd &s) { return s.vb; }
+__device__ __forceinline__ bool chain_shape(const Fwd &s) {
+  return s.eA == 0 && s.be == 0 && s.nB == 1 && s.nA >= 1;
+}
+__device__ __forceinline__ bool chain_shape(const Bwd &s) {
+  return s.g == 0 && s.eA == 0 && s.eB == 0 && s.nB == 1 && s.nA >= 1;
+}
+
+template <bool FWD>
+__device__ __forceinline__ bool chain_jump(const Problem &P, const SearchArgs &S, const NextGen &nx,
+                                           const typename Dir<FWD>::Info &info, Next<FWD> &nk,
+                                           int &depth) {
+  const int4 *chain = FWD ? P.bOut.chain : P.bIn.chain;
+  const int4 *lut = FWD ? P.aOut.lut : P.aIn.lut;
+  const uint32_t stride = (uint32_t)(FWD ? P.aOut.lstride : P.aIn.lstride);
+  if (!chain || !lut || !chain_shape(info) || depth >= P.chain_max) return false;
+  const int4 *cr = chain + 4 * (size_t)state_b(info);
+  const int4 c0 = cr[0], c1 = cr[1], c2 = cr[2], c3 = cr[3];
+  const int32_t lab[CHAIN_STEPS] = {c0.y, c0.w, c1.y, c1.w, c2.y, c2.w, c3.y};
+  const int32_t nbs[CHAIN_STEPS] = {c0.z, c1.x, c1.z, c2.x, c2.z, c3.x, c3.z};
+  int n = c0.x;
+  if (n > P.chain_max - depth) n = P.chain_max - depth;
+  uint32_t qa = state_a(info);
+  uint32_t keys[CHAIN_STEPS];
+  int done = 0;
+#pragma unroll
+  for (int i = 0; i < CHAIN_STEPS; ++i) {
+    keys[i] = 0;
+    if (i < n && done == i && (uint32_t)lab[i] < stride) {
+      const int4 b = lut[(size_t)qa * stride + (uint32_t)lab[i]];
+      if (b.y - b.x == 1 && (b.z & NBR_UNIQ) && !(b.z & NBR_EPS)) {
+        qa = nbr_of(b.z);
+        keys[i] = make_key(qa, nbr_of(nbs[i]), 0u, P.shiftB);
+        if (FWD) set_bit(P.vis, keys[i]);
+        done = i + 1;
+      }
+    }
+  }
+  if (done == 0) return false;
+  int m = done;  // keys reached and kept
+  if (!FWD) {
+    bool acc[CHAIN_STEPS];
+#pragma unroll
+    for (int i = 0; i < CHAIN_STEPS; ++i) acc[i] = i < done && test_bit(P.vis, keys[i]);
+    m = 0;
+#pragma unroll
+    for (int i = 0; i < CHAIN_STEPS; ++i)
+      if (m == i && acc[i]) {
+        set_bit(P.coacc, keys[i]);
+        m = i + 1;
+      }
+  }
+  depth += m > 0 ? m - 1 : 0;
+  if (m > 0) {
+    uint32_t last = keys[0];
+#pragma unroll
+    for (int i = 1; i < CHAIN_STEPS; ++i)
+      if (i < m) last = keys[i];
+    place<FWD>(P, S, nx, true, last, Dir<FWD>::info(P, last), nk, depth);
+  }
+  return true;
+}
+
 // Generation g (one kernel): one thread per unit of the generation's heavy
 // keys, then one thread per light frontier key.  A thread expands its units,
 // then, depth-first, the light keys it reached first (one loop, so the visit
@@ -832,10 +941,12 @@ __global__ __launch_bounds__(NT) void k_gen(Problem P, SearchArgs S, int g) {
     for (int depth = 0;; ++depth) {
       Next<FWD> nk;
       nk.key = NO_KEY;
-      for (uint32_t u = u0; u < u1; ++u)
-        for_unit<FWD>(P, info, u, [&](const Target &t, const Rec &fix) {
-          visit<FWD>(P, S, nx, t, fix, nk, depth);
-        });
+      if (one_unit || !chain_jump<FWD>(P, S, nx, info, nk, depth))
+        for (uint32_t u = u0; u < u1; ++u)
+          for_unit<FWD>(P, info, u, [&](const Target &t, const Rec &fix) {
+            visit<FWD>(P, S, nx, t, fix, nk, depth);
+          });
+      one_unit = false;
       if (nk.key == NO_KEY) break;
       info = nk.info;
       u0 = 0;
@@ -1374,6 +1485,10 @@ hipError_t finish_views(ViewJobs J, hipStream_t s) {
   if (J.vbegin[4]) {
     k_state_inline<<<grid_for((size_t)J.vbegin[4]), NT, 0, s>>>(J);
     if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (J.j[0].chain || J.j[1].chain || J.j[2].chain || J.j[3].chain) {
+      k_chains<<<grid_for((size_t)J.vbegin[4]), NT, 0, s>>>(J);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
   }
   if (J.lbegin[4]) {
     k_build_lut<<<grid_for((size_t)J.lbegin[4], 8192), NT, 0, s>>>(J);

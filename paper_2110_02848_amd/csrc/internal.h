@@ -69,9 +69,16 @@ struct DevGraph {
 //   one in-arc; in A: not a start state, no epsilon output, and in-arcs with
 //   distinct non-epsilon output labels from states without epsilon output).
 //   In an in-view it marks at most one outgoing move (in B: not accepting,
-//   exactly one out-arc; in A: not accepting, out-arcs with distinct
-//   non-epsilon output labels).  A key whose two states are both marked is
-//   reached once by a search in that direction, so it needs no claim.
+//   exactly one out-arc; in A: not accepting, no epsilon in-arc, out-arcs
+//   with distinct non-epsilon output labels).  A key whose two states are
+//   both marked is reached once by a search in that direction, so it needs
+//   no claim.
+//   chain (views of B, optional): per state, up to CHAIN_STEPS steps of its
+//   single-arc path in the view: {n, l0, s0, l1, s1, ..., l6, s6, 0} as 4
+//   int4, where step i follows the only arc (label l_i, non-epsilon) of the
+//   state reached after i steps to s_i (an arc-record neighbour field with
+//   NBR_UNIQ), and a step is recorded only while the state it leaves has
+//   exactly one arc in the view (in out-views: and is not accepting).
 //   perm[i] = original arc id.
 //   olab[i], w[i] (out-views only) = the arc's label on the output side of
 //             the composition (A: input label, B: output label) and its
@@ -88,7 +95,10 @@ struct View {
   int32_t lstride;  // largest label + 1
   const int32_t *olab;
   const float *w;
+  const int4 *chain;
 };
+
+constexpr int CHAIN_STEPS = 7;
 
 constexpr uint32_t FLAG_ACCEPT = 1u, FLAG_EPS_OUT = 2u, FLAG_START = 4u, FLAG_UNIQ = 8u;
 constexpr int32_t NBR_MASK = 0x3fffffff;            // state ids < 2^30
@@ -314,6 +324,7 @@ struct ViewJob {
   const int2 *other_arec;
   const uint8_t *excl;
   int32_t side, out_view, lstride;
+  int4 *chain;  // chain records to write, or null
 };
 // Four views with the prefix sums of their state, arc and bucket counts
 // (entry 4 is the total).

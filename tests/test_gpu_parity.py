@@ -148,6 +148,49 @@ def test_unique_move_corner_cases(comp):
         assert not fsthelp.check_invariants(X, Y, got)
 
 
+def _sparse_emissions(rng, T, C, p_tok, p_dup, p_acc):
+    """Linear acceptor where each frame has a random subset of tokens, some
+    tokens twice (buckets of two arcs), and some extra accepting frames."""
+    arcs = []
+    for t in range(T):
+        toks = [c for c in range(1, C + 1) if rng.random() < p_tok] or [1]
+        for c in toks:
+            w = float(np.float32(rng.standard_normal()))
+            arcs.append((t, t + 1, c, c, w))
+            if rng.random() < p_dup:
+                arcs.append((t, t + 1, c, c, w + 1.0))
+    acc = [T] + [t for t in range(T) if rng.random() < p_acc]
+    return synth.from_arcs(T + 1, arcs, start=[0], accept=sorted(set(acc)))
+
+
+def _long_word_lexicon(rng, W, C, lo, hi, p_acc):
+    """Lexicon whose words can be longer than a chain record (so chains are
+    followed over several records), with some accepting word states."""
+    arcs, V, acc = [], 1, [0]
+    for w in range(1, W + 1):
+        L = int(rng.integers(lo, hi + 1))
+        first = V
+        arcs.append((0, first, 0, w, 0.0))
+        for j in range(L):
+            arcs.append((first + j, first + j + 1, int(rng.integers(1, C + 1)), 0, 0.0))
+            if rng.random() < p_acc:
+                acc.append(first + j + 1)
+        arcs.append((first + L, 0, 0, 0, 0.0))
+        V = first + L + 1
+    return synth.from_arcs(V, arcs, start=[0], accept=sorted(set(acc)))
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_chain_jump_conditions(comp, seed):
+    rng = np.random.default_rng([91, seed])
+    C = int(rng.integers(2, 5))
+    A = _sparse_emissions(rng, int(rng.integers(10, 40)), C, [1.0, 0.7][seed % 2],
+                          [0.0, 0.15][(seed // 2) % 2], [0.0, 0.1][(seed // 4) % 2])
+    B = _long_word_lexicon(rng, int(rng.integers(5, 40)), C, 2, 16, [0.0, 0.05][(seed // 8) % 2])
+    got, _ = check_pair(comp, A, B, f"chain-jump conditions seed {seed}")
+    assert not fsthelp.check_invariants(A, B, got)
+
+
 def test_heavy_states(comp):
     A, B = _hub_pair()
     got, _ = check_pair(comp, A, B, "hub states")
