@@ -93,6 +93,10 @@ def main():
     ap.add_argument("--workload", default="lexicon-T500-W10000")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--order", choices=("forward-first", "coaccessible-first"),
+                    default="forward-first",
+                    help="order of the two searches (Algorithm 1 computes the co-accessible "
+                         "set first); the result is the same")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="first copy a buffer of this many MiB device to device "
                          "(calibrates HBM byte counters under rocprofv3 --pmc)")
@@ -113,6 +117,8 @@ def main():
     dA, dB = gpu.to_device(A, dev), gpu.to_device(B, dev)
     comp = gpu.Composer(0)
     comp.set_option(gpu.FST_OPT_TIMING, 1)
+    comp.set_option(gpu.FST_OPT_ORDER, gpu.FST_ORDER_FORWARD_FIRST if args.order == "forward-first"
+                    else gpu.FST_ORDER_COACCESSIBLE_FIRST)
     stream = torch.cuda.current_stream()
 
     if args.copy_probe_mb > 0:
@@ -196,7 +202,7 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": synth.WORKLOAD_TITLES[args.workload], "name": args.workload,
-                   "seed": args.seed,
+                   "seed": args.seed, "order": args.order,
                    "V_A": A["num_states"], "E_A": len(A["src"]), "V_B": B["num_states"],
                    "E_B": len(B["src"]), "V_C": st["num_states"], "E_C": E_C},
         "ms_per_composition_device": ms,

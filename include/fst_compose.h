@@ -138,14 +138,23 @@ FST_API void fst_ctx_destroy(fst_ctx *ctx);
  * 0 = plain frontier-by-frontier search).  FST_OPT_COUNT_MOVES = 1 makes
  * each run also count the moves out of all accessible keys and the
  * predecessor moves of all co-accessible keys (extra passes, reported in
- * fst_stats.generated and fst_stats.generated_backward). */
+ * fst_stats.generated and fst_stats.generated_backward).
+ * FST_OPT_ORDER picks the order of the two searches (the result is the same):
+ * FST_ORDER_FORWARD_FIRST (default) searches forward from the start keys,
+ * then backward from the accepting keys it reached, inside the accessible
+ * set; FST_ORDER_COACCESSIBLE_FIRST is Algorithm 1's order: the co-accessible
+ * set over all key pairs first (backward from every accepting pair), then the
+ * forward search inside it (fst_stats.accessible then counts only keys that
+ * are also co-accessible). */
 enum fst_option {
   FST_OPT_MAX_WORKSPACE = 1,
   FST_OPT_TIMING = 2,
   FST_OPT_LABEL_BUCKETS = 3,
   FST_OPT_CHAIN_DEPTH = 4,
-  FST_OPT_COUNT_MOVES = 5
+  FST_OPT_COUNT_MOVES = 5,
+  FST_OPT_ORDER = 6
 };
+enum fst_order { FST_ORDER_FORWARD_FIRST = 0, FST_ORDER_COACCESSIBLE_FIRST = 1 };
 FST_API int fst_ctx_set_option(fst_ctx *ctx, int option, int64_t value);
 
 /* Phase 1 (Algorithm 1 up to the size of C): validate A and B, search the

@@ -25,7 +25,7 @@ struct DevBuf {
   size_t cap = 0;
 };
 
-constexpr int NEV = 7;
+constexpr int NEV = 10;  // a begin and an end event per phase (enum in fst_compose_phase_times)
 constexpr int NKERNELS = 4;  // enum fst_kernel
 
 }  // namespace
@@ -37,6 +37,7 @@ struct fst_ctx {
   bool timing = false;
   bool buckets = true;
   bool count_moves = false;
+  int order = FST_ORDER_FORWARD_FIRST;
   int chain_depth = CHAIN_MAX;
   bool have_times = false;
   bool timed_run = false;
@@ -154,8 +155,12 @@ DevGraph dev_graph(const fst_graph *g) {
   return d;
 }
 
-void mark(fst_ctx *c, int i, hipStream_t s) {
-  if (c->timing) (void)hipEventRecord(c->ev[i], s);
+enum { PH_PRE = 0, PH_FWD = 1, PH_BWD = 2, PH_COUNT = 3, PH_FILL = 4 };
+void phase_begin(fst_ctx *c, int ph, hipStream_t s) {
+  if (c->timing) (void)hipEventRecord(c->ev[2 * ph], s);
+}
+void phase_end(fst_ctx *c, int ph, hipStream_t s) {
+  if (c->timing) (void)hipEventRecord(c->ev[2 * ph + 1], s);
 }
 
 int finish_empty(fst_ctx *c, int64_t *V_C, int64_t *E_C) {
@@ -232,7 +237,7 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
     c->kms[k] = 0.f;
     c->klaunches[k] = 0;
   }
-  mark(c, 0, s);
+  phase_begin(c, PH_PRE, s);
   HIP_TRY(hipMemsetAsync(d_sc, 0, sizeof(Scalars), s));
   if (VA) HIP_TRY(launch_validate(dA, 0, &d_sc->errA, &d_sc->maxLabA, s));
   if (VB) HIP_TRY(launch_validate(dB, 1, &d_sc->errB, &d_sc->maxLabB, s));
@@ -360,11 +365,9 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   P.coacc = as<uint32_t>(c->coacc);
   P.wbase = as<uint32_t>(c->wbase);
 
-  // ---- forward search ----
-  mark(c, 1, s);
+  // ---- the two searches ----
   int32_t *la = as<int32_t>(c->lists), *lb = la + VA;
   uint32_t *cnts = reinterpret_cast<uint32_t *>(lb + VB);
-  HIP_TRY(hipMemsetAsync(cnts, 0, 8, s));
   uint32_t *fq = as<uint32_t>(c->fq), *bq = as<uint32_t>(c->bq);
   SearchArgs S;
   S.Q = fq;
@@ -373,26 +376,55 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   S.acc = bq;
   S.cap = cap;
   S.sc = d_sc;
-  HIP_TRY(hipMemsetAsync(d_sc->G, 0, sizeof(d_sc->G), s));
-  HIP_TRY(launch_seed_forward(P, S, la, cnts, lb, cnts + 1, s));
-  FST_TRY(search(c, S, true, &c->stats.fwd_levels, s));
-  HIP_TRY(launch_popcount(P.vis, nwords, &d_sc->naccessible, s));
-  if (c->count_moves) HIP_TRY(launch_count_moves(P, nwords, true, &d_sc->generated, s));
-
-  // ---- backward search, seeded by the accepting keys listed in bq ----
-  mark(c, 2, s);
-  HIP_TRY(hipMemsetAsync(d_sc->G, 0, sizeof(d_sc->G), s));
-  HIP_TRY(launch_seed_backward(P, S, bq, s));
-  FST_TRY(search(c, S, false, &c->stats.bwd_levels, s));
-  // the backward search may set co-accessible bits of keys it never expands
-  // (not accessible); the trim set is what remains after masking them, and
-  // the same pass counts the trim keys of every bitmap word
   uint32_t *wbase = as<uint32_t>(c->wbase);
-  HIP_TRY(launch_trim_words(P.coacc, P.vis, wbase, nwords, s));
+  phase_end(c, PH_PRE, s);
+  if (c->order == FST_ORDER_COACCESSIBLE_FIRST) {
+    // Algorithm 1's order: the co-accessible set over all key pairs first,
+    // from every accepting pair, then the forward search inside it
+    P.restrict_fwd = 1;
+    P.restrict_bwd = 0;
+    phase_begin(c, PH_BWD, s);
+    HIP_TRY(hipMemsetAsync(cnts, 0, 8, s));
+    HIP_TRY(hipMemsetAsync(d_sc->G, 0, sizeof(d_sc->G), s));
+    HIP_TRY(launch_seed_backward_all(P, S, la, cnts, lb, cnts + 1, s));
+    FST_TRY(search(c, S, false, &c->stats.bwd_levels, s));
+    phase_end(c, PH_BWD, s);
+    phase_begin(c, PH_FWD, s);
+    HIP_TRY(hipMemsetAsync(cnts, 0, 8, s));
+    HIP_TRY(hipMemsetAsync(d_sc->G, 0, sizeof(d_sc->G), s));
+    HIP_TRY(launch_seed_forward(P, S, la, cnts, lb, cnts + 1, s));
+    FST_TRY(search(c, S, true, &c->stats.fwd_levels, s));
+    HIP_TRY(launch_popcount(P.vis, nwords, &d_sc->naccessible, s));
+    if (c->count_moves) HIP_TRY(launch_count_moves(P, nwords, true, &d_sc->generated, s));
+    HIP_TRY(launch_trim_words(P.coacc, P.vis, wbase, nwords, s));
+    phase_end(c, PH_FWD, s);
+  } else {
+    P.restrict_fwd = 0;
+    P.restrict_bwd = 1;
+    phase_begin(c, PH_FWD, s);
+    HIP_TRY(hipMemsetAsync(cnts, 0, 8, s));
+    HIP_TRY(hipMemsetAsync(d_sc->G, 0, sizeof(d_sc->G), s));
+    HIP_TRY(launch_seed_forward(P, S, la, cnts, lb, cnts + 1, s));
+    FST_TRY(search(c, S, true, &c->stats.fwd_levels, s));
+    HIP_TRY(launch_popcount(P.vis, nwords, &d_sc->naccessible, s));
+    if (c->count_moves) HIP_TRY(launch_count_moves(P, nwords, true, &d_sc->generated, s));
+    phase_end(c, PH_FWD, s);
+
+    // backward search, seeded by the accepting keys listed in bq
+    phase_begin(c, PH_BWD, s);
+    HIP_TRY(hipMemsetAsync(d_sc->G, 0, sizeof(d_sc->G), s));
+    HIP_TRY(launch_seed_backward(P, S, bq, s));
+    FST_TRY(search(c, S, false, &c->stats.bwd_levels, s));
+    // the backward search may set co-accessible bits of keys it never
+    // expands (not accessible); the trim set is what remains after masking
+    // them, and the same pass counts the trim keys of every bitmap word
+    HIP_TRY(launch_trim_words(P.coacc, P.vis, wbase, nwords, s));
+    phase_end(c, PH_BWD, s);
+  }
   if (c->count_moves) HIP_TRY(launch_count_moves(P, nwords, false, &d_sc->generated_bwd, s));
 
   // ---- numbering and arc counts ----
-  mark(c, 3, s);
+  phase_begin(c, PH_COUNT, s);
   HIP_TRY(scan_u32(wbase, wbase, nwords, false, &d_sc->total, c->scan_tmp.p, s));
   FST_TRY(readback(c, s));
   const unsigned long long nst = c->h_sc->total;
@@ -416,7 +448,7 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   if (nstates)
     HIP_TRY(scan_u32(btot, btot, out_chunks(nstates, per), false, &d_sc->total, c->scan_tmp.p,
                      s));
-  mark(c, 4, s);
+  phase_end(c, PH_COUNT, s);
   FST_TRY(readback(c, s));
   const unsigned long long narcs = c->h_sc->total;
   if (narcs > (unsigned long long)INT32_MAX) return FST_ERR_TOO_LARGE;
@@ -520,6 +552,11 @@ int fst_ctx_set_option(fst_ctx *c, int option, int64_t value) {
     case FST_OPT_COUNT_MOVES:
       c->count_moves = value != 0;
       return FST_OK;
+    case FST_OPT_ORDER:
+      if (value != FST_ORDER_FORWARD_FIRST && value != FST_ORDER_COACCESSIBLE_FIRST)
+        return FST_ERR_INVALID_ARG;
+      c->order = (int)value;
+      return FST_OK;
     case FST_OPT_CHAIN_DEPTH:
       if (value < 0 || value > (1 << 20)) return FST_ERR_INVALID_ARG;
       c->chain_depth = (int)value;
@@ -573,7 +610,7 @@ int fst_compose_fill(fst_ctx *c, const fst_graph_out *C, void *stream) {
   O.key_f = C->key_f;
   O.arc_a = C->arc_a;
   O.arc_b = C->arc_b;
-  mark(c, 5, s);
+  phase_begin(c, PH_FILL, s);
   const KernelTimer tf = c->timed_run ? timer(c, FST_KERNEL_FILL) : KernelTimer{};
   tf.begin(s);
   hipError_t e = launch_fill(c->P, as<uint32_t>(c->fq), c->nstates, c->out_per,
@@ -583,7 +620,7 @@ int fst_compose_fill(fst_ctx *c, const fst_graph_out *C, void *stream) {
   // per-state fill (offsets, flags, light states' arcs), heavy-state fill (if any)
   c->klaunches[FST_KERNEL_FILL] = c->timed_run ? 1 + (c->nheavy ? 1 : 0) : 0;
   c->kms[FST_KERNEL_FILL] = 0.f;
-  mark(c, 6, s);
+  phase_end(c, PH_FILL, s);
   if (e != hipSuccess) {
     (void)hipGetLastError();
     return FST_ERR_HIP;
@@ -603,11 +640,10 @@ int fst_compose_phase_times(const fst_ctx *c, float *ms, int n) {
   if (!c || !ms || n < 0) return FST_ERR_INVALID_ARG;
   if (!c->have_times) return FST_ERR_STATE;
   DeviceGuard g(c->device);
-  if (hipEventSynchronize(c->ev[6]) != hipSuccess) return FST_ERR_HIP;
-  const int pairs[5][2] = {{0, 1}, {1, 2}, {2, 3}, {3, 4}, {5, 6}};
+  if (hipEventSynchronize(c->ev[2 * PH_FILL + 1]) != hipSuccess) return FST_ERR_HIP;
   for (int i = 0; i < n && i < 5; ++i) {
     float t = 0.f;
-    if (hipEventElapsedTime(&t, c->ev[pairs[i][0]], c->ev[pairs[i][1]]) != hipSuccess)
+    if (hipEventElapsedTime(&t, c->ev[2 * i], c->ev[2 * i + 1]) != hipSuccess)
       return FST_ERR_HIP;
     ms[i] = t;
   }

@@ -796,25 +796,20 @@ __device__ __forceinline__ void visit(const Problem &P, const SearchArgs &S, con
       Dir<FWD>::make(v, P.shiftB, t.fixA ? F : L, t.fixA ? L : F);
   const uint32_t bit = 1u << (v & 31u), w = v >> 5;
   bool fresh;
+  // a restricted search expands only keys the other search has reached
+  const uint32_t *other = FWD ? P.coacc : P.vis;
+  uint32_t *mine = FWD ? P.vis : P.coacc;
+  const bool restricted = FWD ? P.restrict_fwd != 0 : P.restrict_bwd != 0;
   if (t.uniq) {
-    if (FWD) {
-      set_bit(P.vis, v);
-      fresh = true;
-    } else {
-      fresh = (P.vis[w] & bit) != 0;
-      if (fresh) set_bit(P.coacc, v);
-    }
-  } else if (t.hot) {
-    if (FWD) {
-      fresh = claim(P.vis, v);
-    } else {
-      const uint32_t wv = P.vis[w], wc = P.coacc[w];  // one round trip for both
-      fresh = (wv & bit) && !(wc & bit) && (atomicOr(P.coacc + w, bit) & bit) == 0;
-    }
+    fresh = !restricted || (other[w] & bit) != 0;
+    if (fresh) set_bit(mine, v);
+  } else if (t.hot || (FWD && restricted)) {
+    const uint32_t wo = restricted ? other[w] : bit, wm = mine[w];  // one round trip
+    fresh = (wo & bit) && !(wm & bit) && (atomicOr(mine + w, bit) & bit) == 0;
   } else {
-    const uint32_t wv = FWD ? bit : P.vis[w];
-    const uint32_t old = atomicOr((FWD ? P.vis : P.coacc) + w, bit);
-    fresh = (wv & bit) && !(old & bit);
+    const uint32_t wo = restricted ? other[w] : bit;
+    const uint32_t old = atomicOr(mine + w, bit);
+    fresh = (wo & bit) && !(old & bit);
   }
   place<FWD>(P, S, nx, fresh, v, vi, nk, depth);
 }
@@ -864,25 +859,26 @@ __device__ __forceinline__ bool chain_jump(const Problem &P, const SearchArgs &S
       if (b.y - b.x == 1 && (b.z & NBR_UNIQ) && !(b.z & NBR_EPS)) {
         qa = nbr_of(b.z);
         keys[i] = make_key(qa, nbr_of(nbs[i]), 0u, P.shiftB);
-        if (FWD) set_bit(P.vis, keys[i]);
         done = i + 1;
       }
     }
   }
   if (done == 0) return false;
-  int m = done;  // keys reached and kept
-  if (!FWD) {
-    bool acc[CHAIN_STEPS];
+  // a restricted search keeps the reached keys up to the first one the other
+  // search has not reached (their bits are loaded together)
+  const uint32_t *other = FWD ? P.coacc : P.vis;
+  uint32_t *mine = FWD ? P.vis : P.coacc;
+  const bool restricted = FWD ? P.restrict_fwd != 0 : P.restrict_bwd != 0;
+  bool ok[CHAIN_STEPS];
 #pragma unroll
-    for (int i = 0; i < CHAIN_STEPS; ++i) acc[i] = i < done && test_bit(P.vis, keys[i]);
-    m = 0;
+  for (int i = 0; i < CHAIN_STEPS; ++i) ok[i] = i < done && (!restricted || test_bit(other, keys[i]));
+  int m = 0;  // keys reached and kept
 #pragma unroll
-    for (int i = 0; i < CHAIN_STEPS; ++i)
-      if (m == i && acc[i]) {
-        set_bit(P.coacc, keys[i]);
-        m = i + 1;
-      }
-  }
+  for (int i = 0; i < CHAIN_STEPS; ++i)
+    if (m == i && ok[i]) {
+      set_bit(mine, keys[i]);
+      m = i + 1;
+    }
   depth += m > 0 ? m - 1 : 0;
   if (m > 0) {
     uint32_t last = keys[0];
@@ -987,13 +983,41 @@ __global__ __launch_bounds__(NT) void k_seed_forward(Problem P, SearchArgs S,
     Fwd ki;
     if (i < n) {
       k = make_key((uint32_t)la[i / nb], (uint32_t)lb[i % nb], 0u, P.shiftB);
-      fresh = claim(P.vis, k);
+      fresh = (!P.restrict_fwd || test_bit(P.coacc, k)) && claim(P.vis, k);
       ki = fwd_info(P, k);
     }
     Next<true> nk;
     nk.key = NO_KEY;
     // depth = chain_max: every light start key joins the frontier
     place<true>(P, S, nx, fresh, k, ki, nk, P.chain_max);
+  }
+}
+
+// Every accepting key (f = 0, and f = 1 where its A state has an epsilon
+// output) forms generation 0 of a backward search over all key pairs.
+__global__ __launch_bounds__(NT) void k_seed_backward_all(Problem P, SearchArgs S,
+                                                          const int32_t *__restrict__ la,
+                                                          const uint32_t *__restrict__ na_p,
+                                                          const int32_t *__restrict__ lb,
+                                                          const uint32_t *__restrict__ nb_p) {
+  const ull na = *na_p, nb = *nb_p, n = 2 * na * nb;
+  const NextGen nx{&S.sc->G[0], 0u, 0u};
+  for (ull i0 = (ull)blockIdx.x * NT; i0 < n; i0 += (ull)gridDim.x * NT) {
+    const ull i = i0 + threadIdx.x;
+    uint32_t k = 0;
+    bool fresh = false;
+    Bwd ki;
+    if (i < n) {
+      const ull pair = i >> 1;
+      const uint32_t qa = (uint32_t)la[pair / nb], f = (uint32_t)(i & 1);
+      const bool eps = (P.aOut.srec[2 * (size_t)qa].w & (int32_t)FLAG_EPS_OUT) != 0;
+      k = make_key(qa, (uint32_t)lb[pair % nb], f, P.shiftB);
+      fresh = (f == 0 || eps) && claim(P.coacc, k);
+      ki = bwd_info(P, k);
+    }
+    Next<false> nk;
+    nk.key = NO_KEY;
+    place<false>(P, S, nx, fresh, k, ki, nk, P.chain_max);
   }
 }
 
@@ -1505,6 +1529,17 @@ hipError_t launch_seed_forward(const Problem &P, const SearchArgs &S, int32_t *l
   k_collect<<<grid_for((size_t)P.B.V, 1024), NT, 0, s>>>(P.B.start, P.B.V, lb, nb);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   k_seed_forward<<<64, NT, 0, s>>>(P, S, la, na, lb, nb);
+  return hipGetLastError();
+}
+
+hipError_t launch_seed_backward_all(const Problem &P, const SearchArgs &S, int32_t *la,
+                                    uint32_t *na, int32_t *lb, uint32_t *nb, hipStream_t s) {
+  k_collect<<<grid_for((size_t)P.A.V, 1024), NT, 0, s>>>(P.A.accept, P.A.V, la, na);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  k_collect<<<grid_for((size_t)P.B.V, 1024), NT, 0, s>>>(P.B.accept, P.B.V, lb, nb);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  k_seed_backward_all<<<1024, NT, 0, s>>>(P, S, la, na, lb, nb);
   return hipGetLastError();
 }
 

@@ -114,6 +114,8 @@ struct Problem {
   View bIn;    // B by (dst, ilabel)
   uint32_t shiftB;        // bits of the B state inside a key
   int chain_max;          // keys one search thread may follow depth-first
+  int restrict_fwd;       // forward search expands only keys already in coacc
+  int restrict_bwd;       // backward search expands only keys already in vis
   uint32_t *vis;          // accessible-key bitmap
   uint32_t *coacc;        // trim-key bitmap (accessible and co-accessible)
   const uint32_t *wbase;  // exclusive popcount prefix of coacc words
@@ -339,6 +341,11 @@ hipError_t finish_views(ViewJobs J, hipStream_t s);
 // marked co-accessible and listed in S.acc (count in Scalars::tail2).
 hipError_t launch_seed_forward(const Problem &P, const SearchArgs &S, int32_t *la, uint32_t *na,
                                int32_t *lb, uint32_t *nb, hipStream_t s);
+// Collect the accepting states of A and B into la/lb (counts na/nb, zeroed
+// by the caller) and place every accepting key (f = 0, and f = 1 where
+// epsOutA) in generation 0 of a backward search over all key pairs.
+hipError_t launch_seed_backward_all(const Problem &P, const SearchArgs &S, int32_t *la,
+                                    uint32_t *na, int32_t *lb, uint32_t *nb, hipStream_t s);
 // Place the accepting keys listed by the forward search (acc_list) in
 // generation 0 of the backward search.
 hipError_t launch_seed_backward(const Problem &P, const SearchArgs &S, const uint32_t *acc_list,

@@ -29,6 +29,10 @@ FST_OPT_TIMING = 2
 FST_OPT_LABEL_BUCKETS = 3
 FST_OPT_CHAIN_DEPTH = 4
 FST_OPT_COUNT_MOVES = 5
+FST_OPT_ORDER = 6
+
+FST_ORDER_FORWARD_FIRST = 0
+FST_ORDER_COACCESSIBLE_FIRST = 1
 
 PHASES = ("preprocess", "forward", "backward", "count", "fill")
 

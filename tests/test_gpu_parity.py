@@ -191,6 +191,45 @@ def test_chain_jump_conditions(comp, seed):
     assert not fsthelp.check_invariants(A, B, got)
 
 
+@pytest.fixture(scope="module")
+def comp_paper_order():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2110_02848_amd import gpu
+    c = gpu.Composer(0)
+    c.set_option(gpu.FST_OPT_ORDER, gpu.FST_ORDER_COACCESSIBLE_FIRST)
+    yield c
+    c.close()
+
+
+def _paper_order_cases():
+    cases = [("random-64", s) for s in range(30)] + [("random-1000", s) for s in (1, 2)]
+    cases += [("random-5000", s) for s in (0, 3)] + [("lexicon-T100-W1000", 0)]
+    return cases
+
+
+@pytest.mark.parametrize("name,seed", _paper_order_cases())
+def test_coaccessible_first_order(comp_paper_order, name, seed):
+    A, B = synth.workload(name, seed)
+    got, _ = check_pair(comp_paper_order, A, B, f"co-accessible first {name} seed {seed}")
+    if seed < 3:
+        assert not fsthelp.check_invariants(A, B, got)
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_coaccessible_first_order_small(comp_paper_order, seed):
+    rng = np.random.default_rng([123, seed])
+    if seed % 2:
+        V = int(rng.integers(3, 40))
+        A = _sparse_chain_graph(rng, V, 1 + (seed % 4 == 3), 0.2, 0.1)
+        B = _sparse_chain_graph(rng, int(rng.integers(3, 40)), 1 + (seed % 4 == 3), 0.1, 0.1)
+    else:
+        A = synth.tiny_random(rng, int(rng.integers(1, 6)), 3, 3, 0.4)
+        B = synth.tiny_random(rng, int(rng.integers(1, 6)), 3, 3, 0.4)
+    got, _ = check_pair(comp_paper_order, A, B, f"co-accessible first small seed {seed}")
+    assert not fsthelp.check_invariants(A, B, got)
+
+
 def test_heavy_states(comp):
     A, B = _hub_pair()
     got, _ = check_pair(comp, A, B, "hub states")
