@@ -16,6 +16,11 @@ Algorithm 1 (Section 3.1) with the epsilon-sequencing filter described in
   its matching arcs grouped by middle label, each group in (a, b) order.
 
 Parity with the GPU path is checked on this canonical form.
+
+``score(G)``, ``posterior(G, ...)`` and ``scatter(...)`` (``score.c``) give
+the log-semiring forward and backward scores of an acyclic graph, the arc
+posteriors that are the total score's gradient, and the scatter of per-arc
+gradients of a composed graph to its operands through provenance.
 """
 from __future__ import annotations
 
@@ -26,7 +31,8 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_SRC = os.path.join(_HERE, "oracle.c")
+_SRCS = [os.path.join(_HERE, n) for n in ("oracle.c", "score.c")]
+_DEPS = _SRCS + [os.path.join(_HERE, "og.h")]
 _LIB = os.path.join(_HERE, "liboracle.so")
 
 ORDER_PAPER = 0
@@ -40,17 +46,30 @@ MUT_ACCEPT_A = 4
 MUT_NO_TRIM = 5
 MUT_EPS_MATCH = 6
 
-_ERRORS = {1: "invalid argument", 2: "out of memory", 3: "key space too large"}
+# deliberate mistakes of the score oracle (tests of the pins only)
+SMUT_NONE = 0
+SMUT_MAX = 1
+SMUT_DROP_WEIGHT = 2
+SMUT_ALL_ACCEPT = 3
+SMUT_NO_START = 4
+
+_ERRORS = {1: "invalid argument", 2: "out of memory", 3: "key space too large",
+           4: "graph has a cycle"}
+
+
+class CycleError(ValueError):
+    """The graph has a cycle, so its path sums are not defined here."""
 
 
 def build(force=True):
     """Compile the oracle with gcc (IEEE binary32 adds: no fast-math)."""
-    if not force and os.path.exists(_LIB) and os.path.getmtime(_LIB) >= os.path.getmtime(_SRC):
+    if not force and os.path.exists(_LIB) and all(
+            os.path.getmtime(_LIB) >= os.path.getmtime(f) for f in _DEPS):
         return _LIB
     tmp = _LIB + ".tmp%d" % os.getpid()
     cmd = ["gcc", "-O2", "-std=gnu11", "-fPIC", "-shared", "-fno-fast-math",
            "-ffp-contract=off", "-Wall", "-Wextra", "-Wno-unused-parameter",
-           "-o", tmp, _SRC]
+           "-o", tmp, *_SRCS, "-lm"]
     subprocess.run(cmd, check=True)
     os.replace(tmp, _LIB)
     return _LIB
@@ -94,6 +113,17 @@ def _load():
         lib.oracle_in_csr.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
                                       ctypes.c_void_p, ctypes.c_void_p]
         lib.oracle_in_csr.restype = ctypes.c_int
+        lib.oracle_score.argtypes = [ctypes.POINTER(_Graph), ctypes.c_int, ctypes.c_void_p,
+                                     ctypes.c_void_p, ctypes.POINTER(ctypes.c_double),
+                                     ctypes.POINTER(ctypes.c_double),
+                                     ctypes.POINTER(ctypes.c_int32)]
+        lib.oracle_score.restype = ctypes.c_int
+        lib.oracle_posterior.argtypes = [ctypes.POINTER(_Graph), ctypes.c_void_p,
+                                         ctypes.c_void_p, ctypes.c_double, ctypes.c_void_p]
+        lib.oracle_posterior.restype = ctypes.c_int
+        lib.oracle_scatter.argtypes = [ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                                       ctypes.c_int32, ctypes.c_void_p]
+        lib.oracle_scatter.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -205,3 +235,67 @@ def compose(A, B, order=ORDER_PAPER, mutation=MUT_NONE):
 
 RESULT_KEYS = ("arc_offset", "src", "dst", "ilabel", "olabel", "weight", "arc_a", "arc_b",
                "start", "accept", "key_a", "key_b", "key_f")
+
+
+def _graph_of(G, keep):
+    """A graph dict without labels (a score needs none) gets zero labels."""
+    g = dict(G)
+    E = len(g["src"])
+    for k in ("ilabel", "olabel"):
+        if k not in g:
+            g[k] = np.zeros(E, np.int32)
+    return _as_struct(g, keep)
+
+
+def score(G, mutation=SMUT_NONE):
+    """Forward and backward log-semiring scores of an acyclic graph.
+
+    Returns dict(alpha[V], beta[V], total, total_bwd, longest): ``total`` is
+    the log-add of alpha over accepting states, ``total_bwd`` that of beta
+    over start states (equal up to rounding), ``longest`` the number of
+    states on the longest path.  Raises CycleError for a cyclic graph."""
+    lib = _load()
+    keep = []
+    g = _graph_of(G, keep)
+    V = int(G["num_states"])
+    alpha = np.zeros(V, np.float64)
+    beta = np.zeros(V, np.float64)
+    tf, tb = ctypes.c_double(), ctypes.c_double()
+    longest = ctypes.c_int32()
+    rc = lib.oracle_score(ctypes.byref(g), mutation, alpha.ctypes.data, beta.ctypes.data,
+                          ctypes.byref(tf), ctypes.byref(tb), ctypes.byref(longest))
+    if rc == 4:
+        raise CycleError("oracle_score: graph has a cycle")
+    if rc:
+        raise ValueError("oracle_score: " + _ERRORS.get(rc, str(rc)))
+    return dict(alpha=alpha, beta=beta, total=tf.value, total_bwd=tb.value,
+                longest=int(longest.value))
+
+
+def posterior(G, alpha, beta, total):
+    """Arc posteriors exp(alpha[src] + w + beta[dst] - total) (float64)."""
+    lib = _load()
+    keep = []
+    g = _graph_of(G, keep)
+    alpha = np.ascontiguousarray(alpha, np.float64)
+    beta = np.ascontiguousarray(beta, np.float64)
+    out = np.zeros(len(G["src"]), np.float64)
+    rc = lib.oracle_posterior(ctypes.byref(g), alpha.ctypes.data, beta.ctypes.data,
+                              float(total), out.ctypes.data)
+    if rc:
+        raise ValueError("oracle_posterior: " + _ERRORS.get(rc, str(rc)))
+    return out
+
+
+def scatter(grad, idx, m):
+    """out[i] = sum of grad[e] over e with idx[e] = i (idx -1 is skipped),
+    summed in index order in float64."""
+    lib = _load()
+    grad = np.ascontiguousarray(grad, np.float64)
+    idx = np.ascontiguousarray(idx, np.int32)
+    out = np.zeros(int(m), np.float64)
+    rc = lib.oracle_scatter(len(grad), grad.ctypes.data, idx.ctypes.data, int(m),
+                            out.ctypes.data)
+    if rc:
+        raise ValueError("oracle_scatter: " + _ERRORS.get(rc, str(rc)))
+    return out
