@@ -62,7 +62,8 @@ enum fst_status {
   FST_ERR_TOO_LARGE = 3,     /* key space > 2^32 keys, or |C| > INT32_MAX    */
   FST_ERR_NOMEM = 4,         /* device allocation failed or over the cap     */
   FST_ERR_HIP = 5,           /* a HIP runtime call failed                    */
-  FST_ERR_STATE = 6          /* fill without a successful run               */
+  FST_ERR_STATE = 6,         /* fill without a successful run               */
+  FST_ERR_CYCLIC = 7         /* fst_score on a graph with a cycle            */
 };
 
 /* Read-only transducer view (device memory, caller-owned).
@@ -189,15 +190,62 @@ enum fst_kernel {
   FST_KERNEL_SEARCH_FORWARD = 0,
   FST_KERNEL_SEARCH_BACKWARD = 1,
   FST_KERNEL_COUNT = 2,
-  FST_KERNEL_FILL = 3
+  FST_KERNEL_FILL = 3,
+  FST_KERNEL_SCORE_FORWARD = 4,  /* fst_score: generations of alpha          */
+  FST_KERNEL_SCORE_BACKWARD = 5  /* fst_score: generations of beta           */
 };
 
 /* With FST_OPT_TIMING on: *ms = summed device time of the launches of
- * `kernel` in the last run + fill, each bracketed by HIP events on the
- * caller's stream, and *launches = how many there were.  Returns
- * FST_ERR_STATE if timing was off or no run + fill was timed,
- * FST_ERR_INVALID_ARG for an unknown kernel. */
+ * `kernel` in the last run + fill (kernels 0-3) or the last fst_score
+ * (kernels 4-5), each bracketed by HIP events on the caller's stream, and
+ * *launches = how many there were.  Returns FST_ERR_STATE if timing was off
+ * or no such call was timed, FST_ERR_INVALID_ARG for an unknown kernel. */
 FST_API int fst_compose_kernel_time(const fst_ctx *ctx, int kernel, float *ms, int64_t *launches);
+
+/* ---- Scores of C and their gradient ------------------------------------
+ * The log-semiring weight of C's paths (Eq. (1)) is what a training user
+ * differentiates through (the introduction motivates eager composition by
+ * automatic differentiation).  For an acyclic graph G (any fst_graph, e.g.
+ * a composed C):
+ *   alpha[v] = log-sum over paths from a start state to v of exp(weight),
+ *              0 for a start state's empty path;
+ *   beta[v]  = log-sum over paths from v to an accepting state;
+ *   total    = log-sum over all paths from a start state to an accepting
+ *              state (-inf if there is none); the weight of a path is the
+ *              sum of its arc weights, and sums are float64.
+ * Every log-sum is exact up to its final rounding and independent of the
+ * order of its terms, so results are bitwise reproducible. */
+
+/* Forward and backward scores of G (device arrays of V doubles; either may
+ * be NULL to skip that direction) and the total (one device double, the
+ * log-sum of alpha over accepting states when alpha is computed, else of
+ * beta over start states).  G is validated as in fst_compose_run.  Queued on
+ * `stream`; blocks on small readbacks as the recursion advances.  Returns
+ * FST_ERR_CYCLIC (outputs undefined) if G has a cycle.  Weights must be
+ * finite (an infinite or NaN weight gives unspecified values, never a
+ * fault).  G must stay valid until the work has completed. */
+FST_API int fst_score(fst_ctx *ctx, const fst_graph *G, double *alpha, double *beta,
+                      double *total, void *stream);
+
+/* Arc posteriors times `scale`: grad[e] = scale * exp(alpha[src e] + w(e) +
+ * beta[dst e] - *total), the derivative of scale * total by w(e) (0 for every
+ * arc when *total is -inf).  alpha, beta, total come from fst_score on the
+ * same G; grad has E floats (device).  G is validated.  Asynchronous after
+ * the validation readback. */
+FST_API int fst_score_posterior(fst_ctx *ctx, const fst_graph *G, const double *alpha,
+                                const double *beta, const double *total, float scale,
+                                float *grad, void *stream);
+
+/* Gradient scatter through provenance: out[i] = sum of grad[e] over the
+ * e < n with idx[e] = i (idx[e] = -1 is skipped), for i < m.  With idx =
+ * C's arc_a (arc_b) and grad = the gradient of a loss by C's arc weights,
+ * out is its gradient by the weights of A's (B's) arcs, since an arc of C
+ * weighs w(a) + w(b).  Sums are exact to 2^-64 of the largest |grad| per
+ * term, rounded once to float, so they do not depend on the order of
+ * accumulation.  grad, idx: n entries; out: m floats (device).  Blocks until
+ * done; returns FST_ERR_INVALID_ARG if an index lies outside [-1, m). */
+FST_API int fst_grad_scatter(fst_ctx *ctx, int64_t n, const float *grad, const int32_t *idx,
+                             int32_t m, float *out, void *stream);
 
 /* Static string for a status code. */
 FST_API const char *fst_strerror(int code);

@@ -9,6 +9,10 @@
 //   4. number the trim keys in key order and count each state's kept arcs
 //      (the paper's first pass), scan the counts into arc offsets;
 // fst_compose_fill then writes the arcs (the paper's second pass).
+//
+// fst_score, fst_score_posterior and fst_grad_scatter compute the
+// log-semiring scores of an acyclic graph (such as C), their gradient, and
+// its scatter to the operands through provenance (score.hip).
 #include <stdlib.h>
 #include <string.h>
 
@@ -26,7 +30,8 @@ struct DevBuf {
 };
 
 constexpr int NEV = 10;  // a begin and an end event per phase (enum in fst_compose_phase_times)
-constexpr int NKERNELS = 4;  // enum fst_kernel
+constexpr int NKERNELS = 6;  // enum fst_kernel
+constexpr int NCOMPOSE_KERNELS = 4;  // kernels 0-3 time a composition, 4-5 a score
 
 }  // namespace
 
@@ -48,7 +53,12 @@ struct fst_ctx {
   DevBuf aOutLab, aOutW, bOutLab, bOutW, bOutChain, bInChain;
   DevBuf aInOff, aInPerm, aInArc, aInRec, aInLut, bInOff, bInPerm, bInArc, bInRec, bInLut;
   DevBuf vis, coacc, wbase, fq, bq, heavy, hoff, cnt, btot;
+  // score workspace
+  DevBuf s_sc, s_owner, s_extra, s_inref, s_mbeg, s_mlen, s_mcur, s_marc, s_pend, s_q, s_h,
+      s_hoff, s_val, s_acc, s_rec, s_term, s_mpos;
   Scalars *h_sc = nullptr;
+  ScoreScalars *h_ssc = nullptr;
+  bool have_score_times = false;
   hipEvent_t ev[NEV] = {};
   hipEvent_t kev[2 * NKERNELS] = {};  // per timed kernel: before, after
   float kms[NKERNELS] = {};
@@ -213,6 +223,154 @@ int search(fst_ctx *c, const SearchArgs &S, bool forward, int64_t *levels, hipSt
   }
   *levels = c->h_sc->gens;
   return FST_OK;
+}
+
+// ---------------------------------------------------------------------------
+// scores
+// ---------------------------------------------------------------------------
+
+int score_readback(fst_ctx *c, hipStream_t s) {
+  HIP_TRY(hipMemcpyAsync(c->h_ssc, c->s_sc.p, sizeof(ScoreScalars), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  return FST_OK;
+}
+
+// Validates G (one readback): FST_ERR_INVALID_GRAPH on a violation.
+int score_validate(fst_ctx *c, const DevGraph &d, hipStream_t s) {
+  ScoreScalars *dsc = as<ScoreScalars>(c->s_sc);
+  HIP_TRY(hipMemsetAsync(dsc, 0, sizeof(ScoreScalars), s));
+  if (d.V > 0) HIP_TRY(launch_validate(d, 0, &dsc->err, &dsc->maxlab, s));
+  FST_TRY(score_readback(c, s));
+  const uint32_t info_bits = 1u << 16;  // "not in label order": not an error here
+  return (c->h_ssc->err & ~info_bits) ? FST_ERR_INVALID_GRAPH : FST_OK;
+}
+
+// One direction of the recursion, generation after generation (batches as in
+// search()); FST_ERR_CYCLIC if some state never became ready.
+int score_direction(fst_ctx *c, const ScoreArgs &S, bool forward, hipStream_t s) {
+  ScoreScalars *dsc = S.sc;
+  HIP_TRY(hipMemsetAsync(dsc->G, 0, sizeof(dsc->G), s));
+  HIP_TRY(hipMemsetAsync(&dsc->finished, 0, sizeof(dsc->finished), s));
+  HIP_TRY(launch_score_seed(S, forward, s));
+  const int kernel = forward ? FST_KERNEL_SCORE_FORWARD : FST_KERNEL_SCORE_BACKWARD;
+  const KernelTimer t = timer(c, kernel);
+  int g = 0, batch = 4;
+  for (;;) {
+    t.begin(s);
+    for (int b = 0; b < batch; ++b, ++g) HIP_TRY(launch_score_generation(S, forward, g, s));
+    t.end(s);
+    FST_TRY(score_readback(c, s));
+    FST_TRY(add_time(c, kernel, batch));
+    if (c->h_ssc->overflow) return FST_ERR_TOO_LARGE;  // cannot happen: each state listed once
+    const GenSlot &nx = c->h_ssc->G[g % 3];
+    if (nx.qcount == 0 && (uint32_t)nx.hpack == 0) break;
+    batch = batch == 4 ? 16 : (batch < 64 ? 2 * batch : 64);
+  }
+  if (c->h_ssc->finished != (unsigned long long)S.G.V) return FST_ERR_CYCLIC;
+  return FST_OK;
+}
+
+int score_total(fst_ctx *c, const double *val, const uint8_t *flag, int32_t V, double *total,
+                hipStream_t s) {
+  ScoreScalars *dsc = as<ScoreScalars>(c->s_sc);
+  HIP_TRY(hipMemsetAsync(&dsc->zmax, 0, 3 * sizeof(unsigned long long), s));
+  HIP_TRY(launch_score_total(val, flag, V, dsc, total, s));
+  return FST_OK;
+}
+
+int score_impl(fst_ctx *c, const fst_graph *G, double *alpha, double *beta, double *total,
+               hipStream_t s) {
+  FST_TRY(check_graph_args(G));
+  const DevGraph d = dev_graph(G);
+  FST_TRY(ensure(c, c->s_sc, sizeof(ScoreScalars)));
+  for (int k = NCOMPOSE_KERNELS; k < NKERNELS; ++k) {
+    c->kms[k] = 0.f;
+    c->klaunches[k] = 0;
+  }
+  FST_TRY(score_validate(c, d, s));
+  const int32_t V = d.V;
+  const size_t E = (size_t)d.E;
+  ScoreScalars *dsc = as<ScoreScalars>(c->s_sc);
+  const bool fwd = alpha != nullptr || beta == nullptr;
+  if (V == 0) {
+    // no path at all: total = log 0
+    HIP_TRY(hipMemsetAsync(&dsc->zmax, 0, 3 * sizeof(unsigned long long), s));
+    HIP_TRY(launch_score_total(nullptr, nullptr, 0, dsc, total, s));
+    return FST_OK;
+  }
+  FST_TRY(ensure(c, c->s_owner, (size_t)V * 4));
+  FST_TRY(ensure(c, c->s_extra, (size_t)V * 4));
+  FST_TRY(ensure(c, c->s_inref, (size_t)V * 4));
+  FST_TRY(ensure(c, c->s_mbeg, (size_t)V * 4));
+  FST_TRY(ensure(c, c->s_mlen, (size_t)V * 4));
+  FST_TRY(ensure(c, c->s_mcur, (size_t)V * 4));
+  FST_TRY(ensure(c, c->s_marc, E * 4));
+  FST_TRY(ensure(c, c->s_pend, (size_t)V * 4));
+  FST_TRY(ensure(c, c->s_q, (size_t)V * 4));
+  FST_TRY(ensure(c, c->s_h, (size_t)V * 4));
+  FST_TRY(ensure(c, c->s_hoff, (size_t)V * 4));
+  if (fwd && !alpha) FST_TRY(ensure(c, c->s_val, (size_t)V * 8));
+  FST_TRY(ensure(c, c->s_rec, (size_t)V * sizeof(int4)));
+  FST_TRY(ensure(c, c->s_term, 2 * E * sizeof(double)));
+  FST_TRY(ensure(c, c->s_mpos, E * 4));
+
+  ScoreGraph SG = {};
+  SG.V = V;
+  SG.E = (long long)E;
+  SG.off = d.off;
+  SG.src = d.src;
+  SG.dst = d.dst;
+  SG.w = d.w;
+  SG.start = d.start;
+  SG.accept = d.accept;
+  SG.inref = as<int32_t>(c->s_inref);
+  SG.mbeg = as<int32_t>(c->s_mbeg);
+  SG.mlen = as<int32_t>(c->s_mlen);
+  SG.marc = as<int32_t>(c->s_marc);
+  HIP_TRY(hipMemsetAsync(c->s_owner.p, 0xff, (size_t)V * 4, s));
+  HIP_TRY(hipMemsetAsync(c->s_extra.p, 0, (size_t)V * 4, s));
+  HIP_TRY(launch_score_structure(SG, as<int32_t>(c->s_owner), as<int32_t>(c->s_extra),
+                                 as<int32_t>(c->s_inref), as<int32_t>(c->s_mbeg),
+                                 as<int32_t>(c->s_mlen), as<int32_t>(c->s_mcur),
+                                 as<int32_t>(c->s_marc), as<int32_t>(c->s_mpos), dsc, s));
+
+  ScoreArgs S = {};
+  S.G = SG;
+  S.rec = as<int4>(c->s_rec);
+  S.term = as<double>(c->s_term);
+  S.mpos = as<int32_t>(c->s_mpos);
+  S.pend = as<int32_t>(c->s_pend);
+  S.Q = as<int32_t>(c->s_q);
+  S.H = as<int32_t>(c->s_h);
+  S.hoff = as<uint32_t>(c->s_hoff);
+  S.cap = (uint32_t)V;
+  S.chain = c->chain_depth;
+  S.sc = dsc;
+  if (fwd) {
+    S.val = alpha ? alpha : as<double>(c->s_val);
+    FST_TRY(score_direction(c, S, true, s));
+    FST_TRY(score_total(c, S.val, d.accept, V, total, s));
+  }
+  if (beta) {
+    S.val = beta;
+    FST_TRY(score_direction(c, S, false, s));
+    if (!fwd) FST_TRY(score_total(c, beta, d.start, V, total, s));
+  }
+  c->have_score_times = c->timing;
+  return FST_OK;
+}
+
+ScoreGraph plain_score_graph(const DevGraph &d) {
+  ScoreGraph SG = {};
+  SG.V = d.V;
+  SG.E = d.E;
+  SG.off = d.off;
+  SG.src = d.src;
+  SG.dst = d.dst;
+  SG.w = d.w;
+  SG.start = d.start;
+  SG.accept = d.accept;
+  return SG;
 }
 
 // Label buckets are kept when the table is at most this large; so are the
@@ -497,6 +655,12 @@ int fst_ctx_create(int device, fst_ctx **ctx) {
     return FST_ERR_NOMEM;
   }
   memset(c->h_sc, 0, sizeof(Scalars));
+  if (hipHostMalloc(reinterpret_cast<void **>(&c->h_ssc), sizeof(ScoreScalars), 0) !=
+      hipSuccess) {
+    fst_ctx_destroy(c);
+    return FST_ERR_NOMEM;
+  }
+  memset(c->h_ssc, 0, sizeof(ScoreScalars));
   for (int i = 0; i < NEV; ++i) {
     if (hipEventCreate(&c->ev[i]) != hipSuccess) {
       fst_ctx_destroy(c);
@@ -525,13 +689,17 @@ void fst_ctx_destroy(fst_ctx *c) {
                     &c->bInLut,   &c->vis,      &c->coacc,   &c->wbase,   &c->fq,
                     &c->bq,       &c->heavy,    &c->hoff,    &c->cnt,     &c->aOutLab,
                     &c->aOutW,    &c->bOutLab,  &c->bOutW,   &c->btot,    &c->bOutChain,
-                    &c->bInChain};
+                    &c->bInChain, &c->s_sc,     &c->s_owner, &c->s_extra, &c->s_inref,
+                    &c->s_mbeg,   &c->s_mlen,   &c->s_mcur,  &c->s_marc,  &c->s_pend,
+                    &c->s_q,      &c->s_h,      &c->s_hoff,  &c->s_val,   &c->s_acc,
+                    &c->s_rec,    &c->s_term,   &c->s_mpos};
   for (DevBuf *b : bufs) release(*b);
   for (int i = 0; i < NEV; ++i)
     if (c->ev[i]) (void)hipEventDestroy(c->ev[i]);
   for (int i = 0; i < 2 * NKERNELS; ++i)
     if (c->kev[i]) (void)hipEventDestroy(c->kev[i]);
   if (c->h_sc) (void)hipHostFree(c->h_sc);
+  if (c->h_ssc) (void)hipHostFree(c->h_ssc);
   delete c;
 }
 
@@ -652,7 +820,7 @@ int fst_compose_phase_times(const fst_ctx *c, float *ms, int n) {
 
 int fst_compose_kernel_time(const fst_ctx *c, int kernel, float *ms, int64_t *launches) {
   if (!c || !ms || !launches || kernel < 0 || kernel >= NKERNELS) return FST_ERR_INVALID_ARG;
-  if (!c->have_times) return FST_ERR_STATE;
+  if (!(kernel < NCOMPOSE_KERNELS ? c->have_times : c->have_score_times)) return FST_ERR_STATE;
   float t = c->kms[kernel];
   if (kernel == FST_KERNEL_FILL) {
     // the fill is asynchronous: its events are read here
@@ -666,6 +834,56 @@ int fst_compose_kernel_time(const fst_ctx *c, int kernel, float *ms, int64_t *la
   return FST_OK;
 }
 
+int fst_score(fst_ctx *c, const fst_graph *G, double *alpha, double *beta, double *total,
+              void *stream) {
+  if (!c || !G || !total) return FST_ERR_INVALID_ARG;
+  DeviceGuard g(c->device);
+  if (!g.ok) return FST_ERR_HIP;
+  c->have_score_times = false;
+  int rc = score_impl(c, G, alpha, beta, total, reinterpret_cast<hipStream_t>(stream));
+  if (rc != FST_OK) (void)hipGetLastError();
+  return rc;
+}
+
+int fst_score_posterior(fst_ctx *c, const fst_graph *G, const double *alpha, const double *beta,
+                        const double *total, float scale, float *grad, void *stream) {
+  if (!c || !G || !total) return FST_ERR_INVALID_ARG;
+  FST_TRY(check_graph_args(G));
+  if (G->num_arcs > 0 && (!alpha || !beta || !grad)) return FST_ERR_INVALID_ARG;
+  DeviceGuard g(c->device);
+  if (!g.ok) return FST_ERR_HIP;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const DevGraph d = dev_graph(G);
+  FST_TRY(ensure(c, c->s_sc, sizeof(ScoreScalars)));
+  FST_TRY(score_validate(c, d, s));
+  if (launch_posterior(plain_score_graph(d), alpha, beta, total, scale, grad, s) != hipSuccess) {
+    (void)hipGetLastError();
+    return FST_ERR_HIP;
+  }
+  return FST_OK;
+}
+
+int fst_grad_scatter(fst_ctx *c, int64_t n, const float *grad, const int32_t *idx, int32_t m,
+                     float *out, void *stream) {
+  if (!c || n < 0 || m < 0) return FST_ERR_INVALID_ARG;
+  if ((n > 0 && (!grad || !idx)) || (m > 0 && !out)) return FST_ERR_INVALID_ARG;
+  DeviceGuard g(c->device);
+  if (!g.ok) return FST_ERR_HIP;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  FST_TRY(ensure(c, c->s_sc, sizeof(ScoreScalars)));
+  FST_TRY(ensure(c, c->s_acc, (size_t)m * 4 * sizeof(unsigned long long)));
+  ScoreScalars *dsc = as<ScoreScalars>(c->s_sc);
+  HIP_TRY(hipMemsetAsync(dsc, 0, sizeof(ScoreScalars), s));
+  if (m > 0) HIP_TRY(hipMemsetAsync(c->s_acc.p, 0, (size_t)m * 4 * sizeof(unsigned long long), s));
+  if (launch_scatter(grad, idx, (long long)n, m, as<unsigned long long>(c->s_acc), &dsc->absmax,
+                     &dsc->bad, out, s) != hipSuccess) {
+    (void)hipGetLastError();
+    return FST_ERR_HIP;
+  }
+  FST_TRY(score_readback(c, s));
+  return c->h_ssc->bad ? FST_ERR_INVALID_ARG : FST_OK;
+}
+
 const char *fst_strerror(int code) {
   switch (code) {
     case FST_OK: return "ok";
@@ -675,6 +893,7 @@ const char *fst_strerror(int code) {
     case FST_ERR_NOMEM: return "out of device memory or over the workspace cap";
     case FST_ERR_HIP: return "HIP runtime error";
     case FST_ERR_STATE: return "no successful fst_compose_run to fill from";
+    case FST_ERR_CYCLIC: return "graph has a cycle (scores need an acyclic graph)";
     default: return "unknown error";
   }
 }

@@ -1450,7 +1450,7 @@ __global__ __launch_bounds__(NT) void k_fill_heavy(Problem P, const uint32_t *__
 hipError_t launch_validate(const DevGraph &g, int side, uint32_t *err, uint32_t *maxlab,
                            hipStream_t s) {
   size_t n = (size_t)(g.V + 1 > g.E ? g.V + 1 : g.E);
-  k_validate<<<grid_for(n, 64), NT, 0, s>>>(g, side, err, maxlab);
+  k_validate<<<grid_for(n, 2048), NT, 0, s>>>(g, side, err, maxlab);
   return hipGetLastError();
 }
 

@@ -169,6 +169,54 @@ struct SearchArgs {
 };
 
 // ---------------------------------------------------------------------------
+// Scores of an acyclic graph (score.hip)
+// ---------------------------------------------------------------------------
+
+// The caller's graph plus its in-arc structure: inref[v] >= 0 is v's only
+// in-arc, -1 means none, and -2 - m names merge m (a state with two or more
+// in-arcs), whose in-arcs are marc[mbeg[m] .. mbeg[m] + mlen[m]) in any order.
+struct ScoreGraph {
+  int32_t V;
+  long long E;
+  const int32_t *off, *src, *dst;
+  const float *w;
+  const uint8_t *start, *accept;
+  const int32_t *inref;
+  const int32_t *mbeg, *mlen, *marc;
+};
+
+// Device scalars of a score computation, read back by the host.
+struct ScoreScalars {
+  uint32_t err, maxlab;      // validation
+  uint32_t overflow, gens;   // a list overflowed; generations that had work
+  uint32_t nmerge, bad;      // merges; a provenance index out of range
+  unsigned long long finished;  // states given a value
+  unsigned long long mtotal;    // in-arcs of all merges
+  unsigned long long zmax, zlo, zhi;  // total: order key of the maximum, 128-bit sum
+  uint32_t absmax, pad;         // scatter: bits of the largest |gradient|
+  GenSlot G[3];
+};
+
+// One direction of the score recursion (forward: alpha from in-arcs;
+// backward: beta from out-arcs): records, term slots, values, pending counters (per merge
+// forward, per state backward), the generation lists (light states in Q,
+// heavy states in H with their workgroup offsets in hoff; cap entries each),
+// and the depth budget of a thread's walk.
+struct ScoreArgs {
+  ScoreGraph G;
+  int4 *rec;     // per-state record of this direction
+  double *term;  // term slots (value + weight) for pulls: 2 E entries
+  const int32_t *mpos;  // position of an in-arc of a merge in marc
+  double *val;
+  int32_t *pend;
+  int32_t *Q, *H;
+  uint32_t *hoff;
+  uint32_t cap;
+  int chain;
+  ScoreScalars *sc;
+};
+
+// ---------------------------------------------------------------------------
 // Keys: ((qa << shiftB | qb) << 1) | f, in canonical (qa, qb, f) order.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ uint32_t make_key(uint32_t qa, uint32_t qb, uint32_t f,
@@ -380,5 +428,31 @@ hipError_t launch_count_heavy(const Problem &P, const uint32_t *key_of, const ui
 hipError_t launch_fill(const Problem &P, const uint32_t *key_of, uint32_t nstates, size_t per,
                        const uint32_t *cnt, const uint32_t *btot, const uint32_t *heavy,
                        uint32_t nheavy, uint32_t narcs, const OutGraph &O, hipStream_t s);
+
+// Score launchers (score.hip).
+// In-arc structure of G: owner (V words, all -1) and extra (V words, all 0)
+// are scratch; inref (V), mbeg/mlen/mcur (V each), marc (E) and mpos (E;
+// set for the in-arcs of merges) receive it; sc->nmerge and sc->mtotal
+// must be 0.
+hipError_t launch_score_structure(const ScoreGraph &G, int32_t *owner, int32_t *extra,
+                                  int32_t *inref, int32_t *mbeg, int32_t *mlen, int32_t *mcur,
+                                  int32_t *marc, int32_t *mpos, ScoreScalars *sc,
+                                  hipStream_t s);
+// Pending counters and generation 0 of one direction (sc->G zeroed).
+hipError_t launch_score_seed(const ScoreArgs &S, bool forward, hipStream_t s);
+// Generation g of one direction: one kernel.
+hipError_t launch_score_generation(const ScoreArgs &S, bool forward, int g, hipStream_t s);
+// *total = log-add of val[v] over the states with flag[v] (sc->zmax, zlo,
+// zhi zeroed).
+hipError_t launch_score_total(const double *val, const uint8_t *flag, int32_t V,
+                              ScoreScalars *sc, double *total, hipStream_t s);
+// grad[e] = scale * exp(alpha[src e] + w(e) + beta[dst e] - *total).
+hipError_t launch_posterior(const ScoreGraph &G, const double *alpha, const double *beta,
+                            const double *total, float scale, float *grad, hipStream_t s);
+// out[i] = sum of g[e] over e < n with idx[e] = i; acc (4 m words), *mx and
+// *bad zeroed by the caller; *bad becomes nonzero if an index is out of range.
+hipError_t launch_scatter(const float *g, const int32_t *idx, long long n, int32_t m,
+                          unsigned long long *acc, uint32_t *mx, uint32_t *bad, float *out,
+                          hipStream_t s);
 
 }  // namespace fstc

@@ -1,0 +1,843 @@
+// Log-semiring scores of an acyclic graph, their gradient (the arc
+// posteriors), and the scatter of per-arc gradients of a composed graph back
+// to the arcs of its operands through provenance, for gfx950.
+//
+// Scores.  alpha[v] is the log-sum over the paths from a start state to v of
+// exp(path weight), beta[v] the log-sum over the paths from v to an accepting
+// state, and the total the log-sum over accepting paths: the forward and
+// backward shortest distances of the log semiring in which Eq. (1) reads the
+// composed weight.  A state's value is final once the values it pulls from
+// are (its in-arcs' sources for alpha, its out-arcs' targets for beta), so
+// states are finished in topological generations, one kernel each, and a
+// kernel boundary separates every value from its reads by other threads:
+//   * In-degrees are classified without atomics: every arc stores its id in
+//     owner[dst] (one store wins), then every arc that does not find its own
+//     id there counts itself as an extra in-arc of dst.  A state with no extra
+//     in-arc has at most one in-arc (owner, or none).  Only the states with
+//     several in-arcs ("merges") get an in-arc list, built with atomics; in a
+//     composed speech graph almost every state has exactly one in-arc.
+//   * A thread that finishes a state walks on, in the same kernel, to a
+//     successor whose only dependency that state was: the successor's value
+//     follows from the thread's registers.  Other ready successors go to the
+//     next generation's lists; a successor with several dependencies counts
+//     an atomic pending counter down, and the thread that takes it to zero
+//     lists it.  Every dependency a listed state still has to pull is left
+//     as a term (value + arc weight) in a slot indexed by the arc, so a pull
+//     reads slots (contiguous ones backward) instead of chasing sources.
+//   * A 16-byte record per state packs what a walk needs: its flags and, for
+//     a state with one arc to notify, that arc's other end, weight and id; a
+//     walk along a chain takes one dependent load per state.
+//   * A state with more than SCORE_LIGHT arcs to pull from or to notify is
+//     heavy: the next generation gives every NT of its notified arcs a
+//     workgroup, which pulls the value cooperatively; then each thread walks
+//     on from one successor.
+// Log-add is exact up to its final rounding and does not depend on the order
+// of its terms: the maximum m first, then every exp(x - m), which lies in
+// (0, 1], truncated to a multiple of 2^-64 and added as a 128-bit integer.
+// In-arc lists may therefore be in any order, and every thread, workgroup
+// and run returns the same bits.
+//
+// Provenance scatter.  out[i] = sum of g[e] over the arcs e with idx[e] = i.
+// Each g[e] is turned into a 64-bit fixed-point magnitude relative to the
+// largest |g| and added into a positive or negative pair of 64-bit words as
+// two 32-bit digits (lazy carries), so the sums are exact integers and the
+// result does not depend on the order of the atomics.
+#include <math.h>
+
+#include "internal.h"
+
+namespace fstc {
+namespace {
+
+typedef unsigned long long ull;
+
+constexpr int32_t SCORE_LIGHT = 64;  // arcs a single thread pulls or notifies
+constexpr unsigned SCORE_GRID = 1024;
+
+// ---------------------------------------------------------------------------
+// exact log-add
+// ---------------------------------------------------------------------------
+
+// Adds exp-term y in [0, 1] as y * 2^64 truncated: (hi, lo) is a 128-bit sum.
+__device__ __forceinline__ void acc_add(ull &lo, ull &hi, double y) {
+  if (!(y > 0.0)) return;  // zero (or a term made of non-finite weights)
+  if (y >= 1.0) {
+    hi += 1ull;
+    return;
+  }
+  const ull t = (ull)(y * 18446744073709551616.0);  // < 2^64
+  lo += t;
+  hi += lo < t ? 1ull : 0ull;
+}
+
+__device__ __forceinline__ double acc_finish(double m, ull lo, ull hi) {
+  if (m == -INFINITY || m == INFINITY) return m;
+  const double s = (double)hi + (double)lo * 0x1p-64;  // >= 1: the maximum adds 1
+  return m + log(s);
+}
+
+__device__ __forceinline__ void add128(ull &lo, ull &hi, ull olo, ull ohi) {
+  const ull n = lo + olo;
+  hi += ohi + (n < lo ? 1ull : 0ull);
+  lo = n;
+}
+
+__device__ __forceinline__ double wave_fmax(double x) {
+#pragma unroll
+  for (int o = WAVE / 2; o > 0; o >>= 1) x = fmax(x, __shfl_xor(x, o));
+  return x;
+}
+
+__device__ __forceinline__ void wave_sum128(ull &lo, ull &hi) {
+#pragma unroll
+  for (int o = WAVE / 2; o > 0; o >>= 1) {
+    const ull olo = __shfl_xor(lo, o), ohi = __shfl_xor(hi, o);
+    add128(lo, hi, olo, ohi);
+  }
+}
+
+// Workgroup reductions (every thread gets the result; all must call).
+__device__ __forceinline__ double block_fmax(double x) {
+  __shared__ double s_m[NWAVES];
+  x = wave_fmax(x);
+  __syncthreads();
+  if (__lane_id() == 0) s_m[threadIdx.x / WAVE] = x;
+  __syncthreads();
+  double r = s_m[0];
+#pragma unroll
+  for (int w = 1; w < NWAVES; ++w) r = fmax(r, s_m[w]);
+  return r;
+}
+
+__device__ __forceinline__ void block_sum128(ull &lo, ull &hi) {
+  __shared__ ull s_lo[NWAVES], s_hi[NWAVES];
+  wave_sum128(lo, hi);
+  __syncthreads();
+  if (__lane_id() == 0) {
+    s_lo[threadIdx.x / WAVE] = lo;
+    s_hi[threadIdx.x / WAVE] = hi;
+  }
+  __syncthreads();
+  lo = s_lo[0];
+  hi = s_hi[0];
+#pragma unroll
+  for (int w = 1; w < NWAVES; ++w) add128(lo, hi, s_lo[w], s_hi[w]);
+}
+
+// ---------------------------------------------------------------------------
+// arc lists of a state
+// ---------------------------------------------------------------------------
+
+// Arcs beg .. beg + n - 1, or (ind) marc[beg .. beg + n - 1].
+struct AList {
+  int32_t beg, n;
+  bool ind;
+};
+
+__device__ __forceinline__ AList in_list(const ScoreGraph &G, int32_t v) {
+  const int32_t r = G.inref[v];
+  if (r >= 0) return AList{r, 1, false};
+  if (r == -1) return AList{0, 0, false};
+  const int32_t m = -2 - r;
+  return AList{G.mbeg[m], G.mlen[m], true};
+}
+
+__device__ __forceinline__ AList out_list(const ScoreGraph &G, int32_t v) {
+  const int32_t b = G.off[v];
+  return AList{b, G.off[v + 1] - b, false};
+}
+
+__device__ __forceinline__ int32_t arc_at(const ScoreGraph &G, const AList &l, int32_t j) {
+  return l.ind ? G.marc[l.beg + j] : l.beg + j;
+}
+
+// Forward: pull over in-arcs (value at the source), notify over out-arcs.
+// Backward: pull over out-arcs (value at the target), notify over in-arcs.
+template <bool FWD>
+__device__ __forceinline__ AList pull_list(const ScoreGraph &G, int32_t v) {
+  return FWD ? in_list(G, v) : out_list(G, v);
+}
+template <bool FWD>
+__device__ __forceinline__ AList notify_list(const ScoreGraph &G, int32_t v) {
+  return FWD ? out_list(G, v) : in_list(G, v);
+}
+// Per-state record of one direction (built by k_score_rec):
+//   x: with one notified arc, the state it reaches; else the first entry of
+//      the notify list (an arc id, or a marc position when REC_IND)
+//   y: flags << 28 | number of notified arcs (saturated at 2^28 - 1)
+//   z: with one notified arc, its weight (binary32 bits)
+//   w: with one notified arc, its id; else -1
+// so a walk takes one dependent load per state.
+constexpr uint32_t REC_INIT = 1u << 28;    // start (forward) / accepting (backward)
+constexpr uint32_t REC_SINGLE = 1u << 29;  // exactly one arc to pull from
+constexpr uint32_t REC_HEAVY = 1u << 30;   // more than SCORE_LIGHT arcs to pull or notify
+constexpr uint32_t REC_IND = 1u << 31;     // notify list is marc[x ...]
+constexpr uint32_t REC_COUNT = (1u << 28) - 1u;
+
+__device__ __forceinline__ uint32_t rec_flags(const int4 &r) { return (uint32_t)r.y; }
+__device__ __forceinline__ int32_t rec_count(const int4 &r) {
+  return (int32_t)((uint32_t)r.y & REC_COUNT);
+}
+
+// Value of a state from the term slots of its pull list, by one thread.
+// Terms were stored by the states it depends on: term[e] = value + w(e).
+// Slots of a pull list: the terms of a merge's in-arcs (forward) sit at
+// E + their position in marc, every other term at its arc id, so the slots
+// of a pull list are contiguous except for one forward in-arc.
+__device__ __forceinline__ const double *pull_slots(const ScoreArgs &S, const AList &l) {
+  return S.term + (l.ind ? S.G.E : 0) + l.beg;
+}
+
+template <bool FWD>
+__device__ double thread_pull(const ScoreArgs &S, const AList &l, bool init) {
+  const double *t = pull_slots(S, l);
+  if (l.n == 1 && !init) return t[0];
+  double m = init ? 0.0 : -INFINITY;
+#pragma unroll 4
+  for (int32_t j = 0; j < l.n; ++j) m = fmax(m, t[j]);
+  if (m == -INFINITY || m == INFINITY) return m;
+  ull lo = 0, hi = 0;
+  if (init) acc_add(lo, hi, exp(0.0 - m));
+#pragma unroll 4
+  for (int32_t j = 0; j < l.n; ++j) acc_add(lo, hi, exp(t[j] - m));
+  return acc_finish(m, lo, hi);
+}
+
+// The same value, formed by a whole workgroup (identical bits).
+template <bool FWD>
+__device__ double block_pull(const ScoreArgs &S, const AList &l, bool init) {
+  const double *t = pull_slots(S, l);
+  double m = (threadIdx.x == 0 && init) ? 0.0 : -INFINITY;
+#pragma unroll 4
+  for (int32_t j = threadIdx.x; j < l.n; j += NT) m = fmax(m, t[j]);
+  m = block_fmax(m);
+  if (m == -INFINITY || m == INFINITY) return m;
+  ull lo = 0, hi = 0;
+  if (threadIdx.x == 0 && init) acc_add(lo, hi, exp(0.0 - m));
+#pragma unroll 4
+  for (int32_t j = threadIdx.x; j < l.n; j += NT) acc_add(lo, hi, exp(t[j] - m));
+  block_sum128(lo, hi);
+  return acc_finish(m, lo, hi);
+}
+
+// Value of a state whose one dependency contributes x (and its own empty
+// path when init): the same arithmetic as thread_pull over that one term.
+__device__ __forceinline__ double one_term(double x, bool init) {
+  if (!init) return x;
+  const double m = fmax(0.0, x);
+  if (m == INFINITY) return m;
+  ull lo = 0, hi = 0;
+  acc_add(lo, hi, exp(0.0 - m));
+  acc_add(lo, hi, exp(x - m));
+  return acc_finish(m, lo, hi);
+}
+
+// ---------------------------------------------------------------------------
+// generation lists
+// ---------------------------------------------------------------------------
+
+struct ScoreNext {
+  GenSlot *slot;
+  uint32_t qbase, hbase;
+};
+
+// Appends ready state y (record ry) to the next generation: light states to
+// the light list (one atomic per wavefront), heavy ones with a workgroup per
+// NT notified arcs.
+template <bool FWD>
+__device__ void list_ready(const ScoreArgs &S, const ScoreNext &nx, bool want, int32_t y,
+                           const int4 &ry) {
+  const bool heavy = want && (rec_flags(ry) & REC_HEAVY);
+  const bool light = want && !heavy;
+  const ull m = __ballot(light);
+  if (m) {
+    const int leader = __ffsll((long long)m) - 1;
+    uint32_t base = 0;
+    if ((int)__lane_id() == leader) base = atomicAdd(&nx.slot->qcount, (uint32_t)__popcll(m));
+    base = __shfl(base, leader);
+    if (light) {
+      const uint32_t pos = nx.qbase + base + (uint32_t)__popcll(m & __lanemask_lt());
+      if (pos < S.cap) S.Q[pos] = y;
+      else S.sc->overflow = 1u;
+    }
+  }
+  if (heavy) {
+    const int32_t nd = notify_list<FWD>(S.G, y).n;
+    const uint32_t blocks = nd > 0 ? (uint32_t)((nd + NT - 1) / NT) : 1u;
+    const ull old = atomicAdd(&nx.slot->hpack, ((ull)blocks << 32) | 1ull);
+    const uint32_t pos = nx.hbase + (uint32_t)(old & 0xffffffffull);
+    if (pos < S.cap) {
+      S.H[pos] = y;
+      S.hoff[pos] = (uint32_t)(old >> 32);
+    } else {
+      S.sc->overflow = 1u;
+    }
+  }
+}
+
+// The finished state's value x reaches y over arc e of weight w.  If y
+// depends on nothing else it is ready: the caller walks on to it (the first
+// such light y, within the depth budget) or it is listed with its term.
+// Otherwise the term goes to its slot and y's pending counter counts down;
+// the thread that takes it to zero lists y.
+template <bool FWD>
+__device__ __forceinline__ void settle(const ScoreArgs &S, const ScoreNext &nx, int32_t y,
+                                       float w, int32_t e, double x, int depth, int32_t &next,
+                                       double &next_val, int4 &next_rec) {
+  const int4 ry = S.rec[y];
+  const uint32_t fy = rec_flags(ry);
+  const double t = x + (double)w;
+  bool ready, walk = false;
+  if (fy & REC_SINGLE) {
+    ready = true;
+    walk = next < 0 && depth + 1 < S.chain && !(fy & REC_HEAVY);
+    if (!walk) S.term[e] = t;
+  } else {
+    // a forward merge's term goes to its in-list position (contiguous pull)
+    S.term[FWD ? S.G.E + S.mpos[e] : (long long)e] = t;
+    const int32_t p = FWD ? -2 - S.G.inref[y] : y;
+    // lanes of the wavefront counting down the first lane's counter do it
+    // with one atomic; the one that reaches zero lists y
+    const ull act = __ballot(true);
+    const int leader = __ffsll((long long)act) - 1;
+    const bool grouped = p == __shfl(p, leader);
+    const int k = (int)__popcll(__ballot(grouped));
+    if (grouped) {
+      int32_t old = 0;
+      if ((int)__lane_id() == leader) old = atomicSub(S.pend + p, k);
+      ready = (int)__lane_id() == leader && old == k;
+    } else {
+      ready = atomicSub(S.pend + p, 1) == 1;
+    }
+  }
+  if (walk) {
+    next = y;
+    next_val = one_term(t, (fy & REC_INIT) != 0);
+    next_rec = ry;
+  }
+  list_ready<FWD>(S, nx, ready && !walk, y, ry);
+}
+
+// Notified arc j of a state's notify list: arc id, other end, weight.
+template <bool FWD>
+__device__ __forceinline__ void notified(const ScoreGraph &G, const int4 &rv, int32_t j,
+                                         int32_t &e, int32_t &y, float &w) {
+  e = (rec_flags(rv) & REC_IND) ? G.marc[rv.x + j] : rv.x + j;
+  y = FWD ? G.dst[e] : G.src[e];
+  w = G.w[e];
+}
+
+// Finishes state v (record rv) with value x, then walks on depth-first.
+template <bool FWD>
+__device__ void walk_from(const ScoreArgs &S, const ScoreNext &nx, int32_t v, int4 rv, double x,
+                          int depth, uint32_t &fin) {
+  for (;;) {
+    S.val[v] = x;
+    ++fin;
+    const int32_t nd = rec_count(rv);
+    int32_t next = -1;
+    double next_val = 0.0;
+    int4 next_rec = rv;
+    if (nd == 1) {
+      settle<FWD>(S, nx, rv.x, __int_as_float(rv.z), rv.w, x, depth, next, next_val, next_rec);
+    } else {
+      for (int32_t j = 0; j < nd; ++j) {
+        int32_t e, y;
+        float w;
+        notified<FWD>(S.G, rv, j, e, y, w);
+        settle<FWD>(S, nx, y, w, e, x, depth, next, next_val, next_rec);
+      }
+    }
+    if (next < 0) return;
+    v = next;
+    x = next_val;
+    rv = next_rec;
+    ++depth;
+  }
+}
+
+// Generation g: workgroups of heavy states, then one thread per light state.
+template <bool FWD>
+__global__ __launch_bounds__(NT) void k_score_gen(ScoreArgs S, int g) {
+  ScoreScalars *sc = S.sc;
+  if (sc->overflow) return;
+  const GenSlot cur = sc->G[g % 3];
+  const uint32_t hcount = (uint32_t)(cur.hpack & 0xffffffffull);
+  const ull HB = cur.hpack >> 32;
+  ScoreNext nx;
+  nx.slot = &sc->G[(g + 1) % 3];
+  nx.qbase = cur.qbase + cur.qcount;
+  nx.hbase = cur.hbase + hcount;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    nx.slot->qbase = nx.qbase;  // read by generation g + 1 only
+    nx.slot->hbase = nx.hbase;
+    GenSlot *done = &sc->G[(g + 2) % 3];  // generation g - 1: free
+    done->qcount = 0;
+    done->hpack = 0;
+    if (HB + cur.qcount) sc->gens = (uint32_t)g + 1;
+  }
+  uint32_t fin = 0;
+  const uint32_t *ho = S.hoff + cur.hbase;
+  for (ull ub = blockIdx.x; ub < HB; ub += gridDim.x) {
+    uint32_t a = 0, b = hcount - 1;  // largest a with ho[a] <= ub
+    while (a < b) {
+      const uint32_t mid = (a + b + 1) >> 1;
+      if (ho[mid] <= ub) a = mid; else b = mid - 1;
+    }
+    const int32_t v = S.H[cur.hbase + a];
+    const uint32_t part = (uint32_t)(ub - ho[a]);
+    const int4 rv = S.rec[v];
+    const double x = block_pull<FWD>(S, pull_list<FWD>(S.G, v), (rec_flags(rv) & REC_INIT) != 0);
+    if (part == 0 && threadIdx.x == 0) {
+      S.val[v] = x;
+      ++fin;
+    }
+    const AList nl = notify_list<FWD>(S.G, v);
+    const long long j = (long long)part * NT + threadIdx.x;
+    int32_t next = -1;
+    double next_val = 0.0;
+    int4 next_rec = rv;
+    if (j < nl.n) {
+      const int32_t e = arc_at(S.G, nl, (int32_t)j);
+      const int32_t y = FWD ? S.G.dst[e] : S.G.src[e];
+      settle<FWD>(S, nx, y, S.G.w[e], e, x, 0, next, next_val, next_rec);
+    }
+    if (next >= 0) walk_from<FWD>(S, nx, next, next_rec, next_val, 1, fin);
+  }
+  const ull n = cur.qcount;
+  for (ull i = (ull)blockIdx.x * NT + threadIdx.x; i < n; i += (ull)gridDim.x * NT) {
+    const int32_t v = S.Q[cur.qbase + (uint32_t)i];
+    const int4 rv = S.rec[v];
+    const double x = thread_pull<FWD>(S, pull_list<FWD>(S.G, v), (rec_flags(rv) & REC_INIT) != 0);
+    walk_from<FWD>(S, nx, v, rv, x, 0, fin);
+  }
+  // one atomic per wavefront
+#pragma unroll
+  for (int o = WAVE / 2; o > 0; o >>= 1) fin += __shfl_xor(fin, o);
+  if (__lane_id() == 0 && fin) atomicAdd(&sc->finished, (ull)fin);
+}
+
+// Records of one direction (see REC_*).
+template <bool FWD>
+__global__ __launch_bounds__(NT) void k_score_rec(ScoreArgs S) {
+  const ScoreGraph &G = S.G;
+  for (long long v = (long long)blockIdx.x * NT + threadIdx.x; v < G.V;
+       v += (long long)gridDim.x * NT) {
+    const AList pl = pull_list<FWD>(G, (int32_t)v), nl = notify_list<FWD>(G, (int32_t)v);
+    uint32_t f = (FWD ? G.start[v] : G.accept[v]) ? REC_INIT : 0u;
+    if (pl.n == 1) f |= REC_SINGLE;
+    if (pl.n > SCORE_LIGHT || nl.n > SCORE_LIGHT) f |= REC_HEAVY;
+    if (nl.ind) f |= REC_IND;
+    int4 r;
+    r.y = (int32_t)(f | (uint32_t)(nl.n < (int32_t)REC_COUNT ? nl.n : (int32_t)REC_COUNT));
+    if (nl.n == 1) {
+      const int32_t e = arc_at(G, nl, 0);
+      r.x = FWD ? G.dst[e] : G.src[e];
+      r.z = __float_as_int(G.w[e]);
+      r.w = e;
+    } else {
+      r.x = nl.beg;
+      r.z = 0;
+      r.w = -1;
+    }
+    S.rec[v] = r;
+  }
+}
+
+// Generation 0: the states that depend on nothing (forward: no in-arc;
+// backward: no out-arc).  Loops run in whole wavefronts (list_ready uses
+// wavefront ballots).
+template <bool FWD>
+__global__ __launch_bounds__(NT) void k_score_seed(ScoreArgs S) {
+  ScoreNext nx;
+  nx.slot = &S.sc->G[0];
+  nx.qbase = 0;
+  nx.hbase = 0;
+  const long long V = S.G.V;
+  const long long stride = (long long)gridDim.x * NT;
+  for (long long base = (long long)blockIdx.x * NT; base < V; base += stride) {
+    const long long v = base + threadIdx.x;
+    bool want = false;
+    int4 rv = make_int4(0, 0, 0, 0);
+    if (v < V) {
+      want = pull_list<FWD>(S.G, (int32_t)v).n == 0;
+      if (want) rv = S.rec[v];
+    }
+    list_ready<FWD>(S, nx, want, (int32_t)v, rv);
+  }
+}
+
+// Pending counters: forward, per merge (its in-arc count); backward, per
+// state (its out-arc count; only states with two or more are counted down).
+template <bool FWD>
+__global__ __launch_bounds__(NT) void k_score_pending(ScoreArgs S) {
+  const long long n = FWD ? (long long)S.sc->nmerge : (long long)S.G.V;
+  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n;
+       i += (long long)gridDim.x * NT)
+    S.pend[i] = FWD ? S.G.mlen[i] : S.G.off[i + 1] - S.G.off[i];
+}
+
+// ---------------------------------------------------------------------------
+// in-arc structure
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(NT) void k_owner(ScoreGraph G, int32_t *owner) {
+  for (long long e = (long long)blockIdx.x * NT + threadIdx.x; e < G.E;
+       e += (long long)gridDim.x * NT)
+    __hip_atomic_store(owner + G.dst[e], (int32_t)e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Lanes of a wavefront that add to the same counter as the first needy lane
+// add together (the targets of a merge's in-arcs are often adjacent).
+__device__ __forceinline__ uint32_t wave_group(bool need, int32_t key, bool &grouped,
+                                               int &leader) {
+  const ull m = __ballot(need);
+  grouped = false;
+  leader = 0;
+  if (!m) return 0;
+  leader = __ffsll((long long)m) - 1;
+  const int32_t lk = __shfl(key, leader);
+  grouped = need && key == lk;
+  const ull g = __ballot(grouped);
+  return (uint32_t)__popcll(g);
+}
+
+__global__ __launch_bounds__(NT) void k_extra(ScoreGraph G, const int32_t *owner,
+                                              int32_t *extra) {
+  const long long stride = (long long)gridDim.x * NT;
+  for (long long base = (long long)blockIdx.x * NT; base < G.E; base += stride) {
+    const long long e = base + threadIdx.x;
+    int32_t x = -1;
+    bool need = false;
+    if (e < G.E) {
+      x = G.dst[e];
+      need = __hip_atomic_load(owner + x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != (int32_t)e;
+    }
+    bool grouped;
+    int leader;
+    const uint32_t cnt = wave_group(need, x, grouped, leader);
+    if (grouped) {
+      if ((int)__lane_id() == leader) atomicAdd(extra + x, (int32_t)cnt);
+    } else if (need) {
+      atomicAdd(extra + x, 1);
+    }
+  }
+}
+
+// Numbers the merges (any order), gives each an in-arc list range, and sets
+// inref for every state.
+__global__ __launch_bounds__(NT) void k_merge_index(ScoreGraph G, const int32_t *owner,
+                                                    const int32_t *extra, int32_t *inref,
+                                                    int32_t *mbeg, int32_t *mlen, int32_t *mcur,
+                                                    ScoreScalars *sc) {
+  const long long stride = (long long)gridDim.x * NT;
+  for (long long base = (long long)blockIdx.x * NT; base < G.V; base += stride) {
+    const long long v = base + threadIdx.x;
+    int32_t len = 0;
+    if (v < G.V) {
+      const int32_t ex = extra[v];
+      len = ex > 0 ? ex + 1 : 0;
+      if (!len) inref[v] = owner[v];
+    }
+    const bool want = len > 0;
+    const ull m = __ballot(want);
+    if (!m) continue;
+    // inclusive prefix of the lengths over the wavefront
+    int32_t pre = len;
+#pragma unroll
+    for (int o = 1; o < WAVE; o <<= 1) {
+      const int32_t t = __shfl_up(pre, o);
+      if ((int)__lane_id() >= o) pre += t;
+    }
+    const int32_t total = __shfl(pre, WAVE - 1);
+    uint32_t mb = 0, lb = 0;
+    if (__lane_id() == 0) {
+      mb = atomicAdd(&sc->nmerge, (uint32_t)__popcll(m));
+      lb = (uint32_t)atomicAdd(&sc->mtotal, (ull)total);
+    }
+    mb = __shfl(mb, 0);
+    lb = __shfl(lb, 0);
+    if (want) {
+      const int32_t mi = (int32_t)(mb + (uint32_t)__popcll(m & __lanemask_lt()));
+      const int32_t beg = (int32_t)lb + pre - len;
+      inref[v] = -2 - mi;
+      mbeg[mi] = beg;
+      mlen[mi] = len;
+      mcur[mi] = beg;
+    }
+  }
+}
+
+__global__ __launch_bounds__(NT) void k_merge_place(ScoreGraph G, const int32_t *inref,
+                                                    int32_t *mcur, int32_t *marc,
+                                                    int32_t *mpos) {
+  const long long stride = (long long)gridDim.x * NT;
+  for (long long base = (long long)blockIdx.x * NT; base < G.E; base += stride) {
+    const long long e = base + threadIdx.x;
+    int32_t mi = -1;
+    if (e < G.E) {
+      const int32_t r = inref[G.dst[e]];
+      if (r <= -2) mi = -2 - r;
+    }
+    const bool need = mi >= 0;
+    bool grouped;
+    int leader;
+    const uint32_t cnt = wave_group(need, mi, grouped, leader);
+    int32_t pos = 0;
+    if (grouped) {
+      int32_t b = 0;
+      if ((int)__lane_id() == leader) b = atomicAdd(mcur + mi, (int32_t)cnt);
+      // leader is grouped, so it is active in this branch
+      b = __shfl(b, leader);
+      const ull gm = __ballot(true);  // the grouped lanes (active here)
+      pos = b + (int32_t)__popcll(gm & __lanemask_lt());
+    } else if (need) {
+      pos = atomicAdd(mcur + mi, 1);
+    }
+    if (need) {
+      marc[pos] = (int32_t)e;
+      mpos[e] = pos;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// total: log-add of val over the flagged states (same exact log-add)
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ ull order_key(double d) {
+  const ull b = (ull)__double_as_longlong(d);
+  return (b >> 63) ? ~b : (b | (1ull << 63));
+}
+__device__ __forceinline__ double from_order_key(ull k) {
+  const ull b = (k >> 63) ? (k & ~(1ull << 63)) : ~k;
+  return __longlong_as_double((long long)b);
+}
+
+__global__ __launch_bounds__(NT) void k_total_max(const double *val, const uint8_t *flag,
+                                                  int32_t V, ScoreScalars *sc) {
+  double m = -INFINITY;
+  for (long long v = (long long)blockIdx.x * NT + threadIdx.x; v < V;
+       v += (long long)gridDim.x * NT)
+    if (flag[v]) m = fmax(m, val[v]);
+  m = block_fmax(m);
+  if (threadIdx.x == 0 && m != -INFINITY) atomicMax(&sc->zmax, order_key(m));
+}
+
+__global__ __launch_bounds__(NT) void k_total_sum(const double *val, const uint8_t *flag,
+                                                  int32_t V, ScoreScalars *sc) {
+  if (sc->zmax == 0) return;  // nothing flagged is finite
+  const double M = from_order_key(sc->zmax);
+  if (M == INFINITY) return;
+  ull lo = 0, hi = 0;
+  for (long long v = (long long)blockIdx.x * NT + threadIdx.x; v < V;
+       v += (long long)gridDim.x * NT)
+    if (flag[v]) acc_add(lo, hi, exp(val[v] - M));
+  block_sum128(lo, hi);
+  if (threadIdx.x == 0 && (lo | hi)) {
+    const ull old = atomicAdd(&sc->zlo, lo);
+    const ull carry = old + lo < old ? 1ull : 0ull;
+    atomicAdd(&sc->zhi, hi + carry);
+  }
+}
+
+__global__ void k_total_final(ScoreScalars *sc, double *total) {
+  if (sc->zmax == 0) {
+    *total = -INFINITY;
+    return;
+  }
+  *total = acc_finish(from_order_key(sc->zmax), sc->zlo, sc->zhi);
+}
+
+// ---------------------------------------------------------------------------
+// posteriors and the provenance scatter
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(NT) void k_posterior(ScoreGraph G, const double *alpha,
+                                                  const double *beta, const double *total,
+                                                  float scale, float *grad) {
+  const double Z = *total;
+  for (long long e = (long long)blockIdx.x * NT + threadIdx.x; e < G.E;
+       e += (long long)gridDim.x * NT) {
+    double p = 0.0;
+    if (Z != -INFINITY) p = exp(alpha[G.src[e]] + (double)G.w[e] + beta[G.dst[e]] - Z);
+    grad[e] = (float)((double)scale * p);
+  }
+}
+
+__global__ __launch_bounds__(NT) void k_absmax(const float *g, long long n, uint32_t *mx) {
+  uint32_t m = 0;
+  for (long long e = (long long)blockIdx.x * NT + threadIdx.x; e < n;
+       e += (long long)gridDim.x * NT)
+    m = max(m, __float_as_uint(g[e]) & 0x7fffffffu);  // |g| orders as its bits
+#pragma unroll
+  for (int o = WAVE / 2; o > 0; o >>= 1) m = max(m, (uint32_t)__shfl_xor(m, o));
+  if (__lane_id() == 0 && m) atomicMax(mx, m);
+}
+
+// Scale exponent: every |g| < 2^ex, so |g| * 2^(64 - ex) < 2^64.
+__device__ __forceinline__ int scale_exp(uint32_t mbits) {
+  int ex = 0;
+  (void)frexpf(__uint_as_float(mbits), &ex);
+  return ex;
+}
+
+// acc[4 i + 0, 1]: digits of the positive terms of target i, [2, 3] of the
+// negative ones (low 32 bits, high 32 bits of each 64-bit magnitude).
+__global__ __launch_bounds__(NT) void k_scatter(const float *g, const int32_t *idx, long long n,
+                                                int32_t m, const uint32_t *mx, ull *acc,
+                                                uint32_t *bad) {
+  const uint32_t mbits = *mx;
+  if (mbits == 0 || mbits >= 0x7f800000u) return;  // all zero, or not finite
+  const int ex = scale_exp(mbits);
+  const long long stride = (long long)gridDim.x * NT;
+  for (long long base = (long long)blockIdx.x * NT; base < n; base += stride) {
+    const long long e = base + threadIdx.x;
+    int32_t key = -1;
+    ull d0 = 0, d1 = 0;
+    if (e < n) {
+      const int32_t i = idx[e];
+      if (i < -1 || i >= m) {
+        atomicOr(bad, 1u);
+      } else if (i >= 0) {
+        const float x = g[e];
+        const ull T = (ull)ldexp(fabs((double)x), 64 - ex);
+        if (T) {
+          key = 2 * i + (x < 0.f ? 1 : 0);
+          d0 = T & 0xffffffffull;
+          d1 = T >> 32;
+        }
+      }
+    }
+    const bool need = key >= 0;
+    bool grouped;
+    int leader;
+    (void)wave_group(need, key, grouped, leader);
+    // digit sums of the grouped lanes (zeros elsewhere), over the wavefront
+    ull s0 = grouped ? d0 : 0ull, s1 = grouped ? d1 : 0ull;
+#pragma unroll
+    for (int o = WAVE / 2; o > 0; o >>= 1) {
+      s0 += __shfl_xor(s0, o);
+      s1 += __shfl_xor(s1, o);
+    }
+    if (grouped && (int)__lane_id() == leader) {
+      ull *a = acc + 2 * (size_t)key;
+      if (s0) atomicAdd(a, s0);
+      if (s1) atomicAdd(a + 1, s1);
+    } else if (need && !grouped) {
+      ull *a = acc + 2 * (size_t)key;
+      if (d0) atomicAdd(a, d0);
+      if (d1) atomicAdd(a + 1, d1);
+    }
+  }
+}
+
+// 128-bit (hi, lo) of d1 * 2^32 + d0.
+__device__ __forceinline__ void digits128(ull d0, ull d1, ull &lo, ull &hi) {
+  lo = d0 + (d1 << 32);
+  hi = (d1 >> 32) + (lo < d0 ? 1ull : 0ull);
+}
+
+__global__ __launch_bounds__(NT) void k_scatter_final(const ull *acc, int32_t m,
+                                                      const uint32_t *mx, float *out) {
+  const uint32_t mbits = *mx;
+  const int ex = (mbits == 0 || mbits >= 0x7f800000u) ? 0 : scale_exp(mbits);
+  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < m;
+       i += (long long)gridDim.x * NT) {
+    if (mbits == 0) {
+      out[i] = 0.f;
+      continue;
+    }
+    if (mbits >= 0x7f800000u) {
+      out[i] = __uint_as_float(0x7fc00000u);  // NaN in, NaN out
+      continue;
+    }
+    ull plo, phi, nlo, nhi;
+    digits128(acc[4 * i], acc[4 * i + 1], plo, phi);
+    digits128(acc[4 * i + 2], acc[4 * i + 3], nlo, nhi);
+    // difference of the two 128-bit magnitudes, then one conversion
+    bool neg = nhi > phi || (nhi == phi && nlo > plo);
+    ull dlo, dhi;
+    if (!neg) {
+      dlo = plo - nlo;
+      dhi = phi - nhi - (plo < nlo ? 1ull : 0ull);
+    } else {
+      dlo = nlo - plo;
+      dhi = nhi - phi - (nlo < plo ? 1ull : 0ull);
+    }
+    double d = (double)dhi * 0x1p64 + (double)dlo;
+    d = ldexp(d, ex - 64);
+    out[i] = (float)(neg ? -d : d);
+  }
+}
+
+int grid_for(long long n) {
+  long long b = (n + NT - 1) / NT;
+  if (b < 1) b = 1;
+  if (b > 4096) b = 4096;
+  return (int)b;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// host-side launchers
+// ---------------------------------------------------------------------------
+
+hipError_t launch_score_structure(const ScoreGraph &G, int32_t *owner, int32_t *extra,
+                                  int32_t *inref, int32_t *mbeg, int32_t *mlen, int32_t *mcur,
+                                  int32_t *marc, int32_t *mpos, ScoreScalars *sc,
+                                  hipStream_t s) {
+  if (G.E > 0) {
+    k_owner<<<grid_for(G.E), NT, 0, s>>>(G, owner);
+    k_extra<<<grid_for(G.E), NT, 0, s>>>(G, owner, extra);
+  }
+  k_merge_index<<<grid_for(G.V), NT, 0, s>>>(G, owner, extra, inref, mbeg, mlen, mcur, sc);
+  if (G.E > 0) k_merge_place<<<grid_for(G.E), NT, 0, s>>>(G, inref, mcur, marc, mpos);
+  return hipGetLastError();
+}
+
+hipError_t launch_score_seed(const ScoreArgs &S, bool forward, hipStream_t s) {
+  if (forward) {
+    k_score_rec<true><<<grid_for(S.G.V), NT, 0, s>>>(S);
+    k_score_pending<true><<<grid_for(S.G.V), NT, 0, s>>>(S);
+    k_score_seed<true><<<grid_for(S.G.V), NT, 0, s>>>(S);
+  } else {
+    k_score_rec<false><<<grid_for(S.G.V), NT, 0, s>>>(S);
+    k_score_pending<false><<<grid_for(S.G.V), NT, 0, s>>>(S);
+    k_score_seed<false><<<grid_for(S.G.V), NT, 0, s>>>(S);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_score_generation(const ScoreArgs &S, bool forward, int g, hipStream_t s) {
+  if (forward) k_score_gen<true><<<SCORE_GRID, NT, 0, s>>>(S, g);
+  else k_score_gen<false><<<SCORE_GRID, NT, 0, s>>>(S, g);
+  return hipGetLastError();
+}
+
+hipError_t launch_score_total(const double *val, const uint8_t *flag, int32_t V,
+                              ScoreScalars *sc, double *total, hipStream_t s) {
+  k_total_max<<<grid_for(V), NT, 0, s>>>(val, flag, V, sc);
+  k_total_sum<<<grid_for(V), NT, 0, s>>>(val, flag, V, sc);
+  k_total_final<<<1, 1, 0, s>>>(sc, total);
+  return hipGetLastError();
+}
+
+hipError_t launch_posterior(const ScoreGraph &G, const double *alpha, const double *beta,
+                            const double *total, float scale, float *grad, hipStream_t s) {
+  if (G.E > 0) k_posterior<<<grid_for(G.E), NT, 0, s>>>(G, alpha, beta, total, scale, grad);
+  return hipGetLastError();
+}
+
+hipError_t launch_scatter(const float *g, const int32_t *idx, long long n, int32_t m, ull *acc,
+                          uint32_t *mx, uint32_t *bad, float *out, hipStream_t s) {
+  if (n > 0) {
+    k_absmax<<<grid_for(n), NT, 0, s>>>(g, n, mx);
+    k_scatter<<<grid_for(n), NT, 0, s>>>(g, idx, n, m, mx, acc, bad);
+  }
+  if (m > 0) k_scatter_final<<<grid_for(m), NT, 0, s>>>(acc, m, mx, out);
+  return hipGetLastError();
+}
+
+}  // namespace fstc

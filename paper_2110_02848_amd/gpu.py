@@ -23,6 +23,7 @@ FST_ERR_TOO_LARGE = 3
 FST_ERR_NOMEM = 4
 FST_ERR_HIP = 5
 FST_ERR_STATE = 6
+FST_ERR_CYCLIC = 7
 
 FST_OPT_MAX_WORKSPACE = 1
 FST_OPT_TIMING = 2
@@ -36,8 +37,9 @@ FST_ORDER_COACCESSIBLE_FIRST = 1
 
 PHASES = ("preprocess", "forward", "backward", "count", "fill")
 
-# kernels timed one by one (enum fst_kernel)
+# kernels timed one by one (enum fst_kernel): a composition's, then a score's
 KERNELS = ("search_forward", "search_backward", "count", "fill")
+SCORE_KERNELS = ("score_forward", "score_backward")
 
 
 class FstError(RuntimeError):
@@ -104,6 +106,17 @@ def load():
                                             ctypes.POINTER(ctypes.c_float),
                                             ctypes.POINTER(ctypes.c_int64)]
     lib.fst_compose_kernel_time.restype = ctypes.c_int
+    lib.fst_score.argtypes = [ctypes.c_void_p, ctypes.POINTER(_Graph), ctypes.c_void_p,
+                              ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    lib.fst_score.restype = ctypes.c_int
+    lib.fst_score_posterior.argtypes = [ctypes.c_void_p, ctypes.POINTER(_Graph),
+                                        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                        ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p]
+    lib.fst_score_posterior.restype = ctypes.c_int
+    lib.fst_grad_scatter.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                     ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
+                                     ctypes.c_void_p]
+    lib.fst_grad_scatter.restype = ctypes.c_int
     lib.fst_strerror.argtypes = [ctypes.c_int]
     lib.fst_strerror.restype = ctypes.c_char_p
     _lib = lib
@@ -239,6 +252,65 @@ class Composer:
         for i, name in enumerate(KERNELS):
             ms, n = ctypes.c_float(), ctypes.c_int64()
             _check(self._lib.fst_compose_kernel_time(self._h, i, ctypes.byref(ms), ctypes.byref(n)),
+                   "fst_compose_kernel_time")
+            out[name] = (float(ms.value), int(n.value))
+        return out
+
+
+    # ---- scores of an acyclic graph and their gradient ----
+
+    def score(self, G, alpha=True, beta=True, stream=None):
+        """Forward / backward log-semiring scores of an acyclic graph of
+        device tensors: dict(alpha, beta: float64 [V] tensors or None, total:
+        float64 [1] tensor).  Raises FstError(FST_ERR_CYCLIC) on a cycle."""
+        import torch
+        dev = f"cuda:{self.device}"
+        V = int(G["num_states"])
+        a = torch.empty(V, dtype=torch.float64, device=dev) if alpha else None
+        b = torch.empty(V, dtype=torch.float64, device=dev) if beta else None
+        total = torch.empty(1, dtype=torch.float64, device=dev)
+        g = _graph_struct(G)
+        rc = self._lib.fst_score(self._h, ctypes.byref(g), _ptr(a), _ptr(b),
+                                 ctypes.c_void_p(total.data_ptr()), _stream_handle(stream))
+        _check(rc, "fst_score")
+        return dict(alpha=a, beta=b, total=total)
+
+    def posterior(self, G, alpha, beta, total, scale=1.0, stream=None):
+        """scale * d total / d w for every arc (float32 [E] tensor)."""
+        import torch
+        grad = torch.empty(int(G["src"].numel()), dtype=torch.float32,
+                           device=f"cuda:{self.device}")
+        g = _graph_struct(G)
+        rc = self._lib.fst_score_posterior(self._h, ctypes.byref(g), _ptr(alpha), _ptr(beta),
+                                           ctypes.c_void_p(total.data_ptr()), float(scale),
+                                           _ptr(grad), _stream_handle(stream))
+        _check(rc, "fst_score_posterior")
+        return grad
+
+    def grad_scatter(self, grad, idx, m, stream=None):
+        """out[i] = sum of grad[e] over idx[e] = i (float32 [m] tensor)."""
+        import torch
+        out = torch.empty(int(m), dtype=torch.float32, device=f"cuda:{self.device}")
+        rc = self._lib.fst_grad_scatter(self._h, int(grad.numel()), _ptr(grad), _ptr(idx),
+                                        int(m), _ptr(out), _stream_handle(stream))
+        _check(rc, "fst_grad_scatter")
+        return out
+
+    def operand_grads(self, C, A_arcs, B_arcs, scale=1.0, stream=None):
+        """Gradient of scale * total(C) by the arc weights of A and B (C
+        filled with provenance): (grad_A [A_arcs], grad_B [B_arcs])."""
+        sc = self.score(C, stream=stream)
+        post = self.posterior(C, sc["alpha"], sc["beta"], sc["total"], scale, stream)
+        return (self.grad_scatter(post, C["arc_a"], A_arcs, stream),
+                self.grad_scatter(post, C["arc_b"], B_arcs, stream))
+
+    def score_kernel_times(self):
+        """{kernel: (ms, launches)} of the last timed fst_score."""
+        out = {}
+        for i, name in enumerate(SCORE_KERNELS):
+            ms, n = ctypes.c_float(), ctypes.c_int64()
+            _check(self._lib.fst_compose_kernel_time(self._h, len(KERNELS) + i, ctypes.byref(ms),
+                                                     ctypes.byref(n)),
                    "fst_compose_kernel_time")
             out[name] = (float(ms.value), int(n.value))
         return out

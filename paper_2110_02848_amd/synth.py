@@ -337,6 +337,64 @@ def tiny_random(rng, V, max_degree, n_sym, p_eps, p_accept=0.4, n_start=1):
     return from_arcs(V, arcs, start=starts, accept=acc)
 
 
+def random_dag(seed, V, mean_out=2.0, window=16, hubs=0, hub_degree=0, p_global=0.1,
+               n_start=2, p_accept=0.05, p_parallel=0.05):
+    """Seeded random acyclic graph (inputs of the score tests and benchmark).
+
+    States get a random topological rank; each state has Poisson(mean_out)
+    out-arcs, each to a later rank, within ``window`` ranks ahead (long
+    paths) or, with probability p_global, anywhere later.  ``hubs`` states
+    (ranks in the middle) also get ``hub_degree`` in-arcs from earlier ranks
+    and as many out-arcs to later ranks.  An arc is duplicated with
+    probability p_parallel.  Weights are binary32 N(0, 1) samples; labels
+    are 1.  Starts are drawn from the first tenth of the ranks; accepting
+    states at rate p_accept, plus the last rank."""
+    rng = np.random.default_rng(np.random.SeedSequence([7, int(seed)]))
+    V = int(V)
+    rank = rng.permutation(V)          # rank[v]: topological position of v
+    by_rank = np.argsort(rank)         # by_rank[r]: the state at position r
+    src_r, dst_r = [], []
+    deg = rng.poisson(mean_out, size=V)
+    for r in range(V - 1):
+        k = int(deg[r])
+        if k == 0:
+            continue
+        far = rng.random(k) < p_global
+        near = r + 1 + rng.integers(0, max(1, min(window, V - 1 - r)), size=k)
+        wide = r + 1 + rng.integers(0, V - 1 - r, size=k)
+        src_r.append(np.full(k, r))
+        dst_r.append(np.where(far, wide, near))
+    for _ in range(int(hubs)):
+        if V < 3:
+            break
+        h = int(rng.integers(V // 4, max(V // 4 + 1, 3 * V // 4)))
+        if h == 0 or h >= V - 1:
+            continue
+        src_r.append(rng.integers(0, h, size=hub_degree))
+        dst_r.append(np.full(hub_degree, h))
+        src_r.append(np.full(hub_degree, h))
+        dst_r.append(rng.integers(h + 1, V, size=hub_degree))
+    sr = np.concatenate(src_r) if src_r else np.zeros(0, np.int64)
+    dr = np.concatenate(dst_r) if dst_r else np.zeros(0, np.int64)
+    dup = rng.random(len(sr)) < p_parallel
+    sr = np.concatenate([sr, sr[dup]])
+    dr = np.concatenate([dr, dr[dup]])
+    src = by_rank[sr].astype(np.int32)
+    dst = by_rank[dr].astype(np.int32)
+    order = np.argsort(src, kind="stable")
+    src, dst = src[order], dst[order]
+    E = len(src)
+    w = rng.standard_normal(E).astype(np.float32)
+    lab = np.ones(E, np.int32)
+    st = np.zeros(V, np.uint8)
+    if V:
+        st[by_rank[rng.integers(0, max(1, V // 10), size=n_start)]] = 1
+    ac = (rng.random(V) < p_accept).astype(np.uint8)
+    if V:
+        ac[by_rank[V - 1]] = 1
+    return _finish(V, src, dst, lab, lab.copy(), w, st, ac)
+
+
 def identity_fst(n_sym):
     """One state, start and accepting, with a loop s:s of weight 0 per symbol."""
     return from_arcs(1, [(0, 0, s, s, 0.0) for s in range(1, n_sym + 1)], start=[0], accept=[0])

@@ -77,3 +77,17 @@ def test_check_graph_rejects(bad):
         g["src"][0] = 1
     with pytest.raises(ValueError):
         synth.check_graph(g)
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_random_dag_is_acyclic_and_seeded(seed):
+    import oracle
+    kw = dict(V=3000, mean_out=2.0, window=8, hubs=2, hub_degree=400)
+    G = synth.random_dag(seed, **kw)
+    synth.check_graph(G)
+    assert synth.graph_sha256(G) == synth.graph_sha256(synth.random_dag(seed, **kw))
+    r = oracle.score(G)  # raises on a cycle
+    assert r["longest"] > 1
+    assert G["start"].sum() >= 1 and G["accept"].sum() >= 1
+    indeg = np.bincount(G["dst"], minlength=G["num_states"])
+    assert indeg.max() >= 400  # the hubs
