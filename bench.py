@@ -5,6 +5,11 @@ fill of the output CSR) of the emissions(T=500, C=64) o lexicon(W=10000,
 L=3..10) workload, inputs resident in HBM.  Prints one JSON line.
 
     python bench.py [--steps K] [--warmup W] [--workload lexicon-T500-W10000] [--seed 0]
+
+``--task score`` measures what a training step runs on the composed graph
+instead: one step = forward and backward log-semiring scores of C, the arc
+posteriors, and their scatter to the arcs of A and B through provenance (C
+is composed once, untimed).
 """
 from __future__ import annotations
 
@@ -54,21 +59,120 @@ def kernel_bytes(st):
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_emissions_lexicon_T500_W10000.txt")
+SCORE_TRAFFIC_FILE = os.path.join(ROOT, "profiles",
+                                  "traffic_score_emissions_lexicon_T500_W10000.txt")
 
 
-def measured_traffic(workload, kernel):
+def measured_traffic(workload, kernel, path=TRAFFIC_FILE):
     """HBM bytes per launch of `kernel` from the committed counter table, or
     None if there is none for this workload or the kernels changed since."""
     if workload != "lexicon-T500-W10000":
         return None
     from paper_2110_02848_amd import profiling
-    t = profiling.read_traffic(TRAFFIC_FILE)
+    t = profiling.read_traffic(path)
     if t is None:
         return None
     sha, table = t
     if sha != profiling.kernel_source_hash() or kernel not in table:
         return None
     return table[kernel]
+
+
+def score_kernel_bytes(V, E):
+    """Algorithmic bytes of one direction of the score recursion: every
+    state's value written once (8 B); every arc's term formed from the value
+    at its other end, its weight and that end's id (8 + 4 + 4 B)."""
+    return 8 * V + 16 * E
+
+
+def cpu_score_baseline(A, B):
+    import oracle
+    oracle.build(force=False)
+    C = oracle.compose(A, B)
+    t0 = time.perf_counter()
+    r = oracle.score(C)
+    post = oracle.posterior(C, r["alpha"], r["beta"], r["total"])
+    oracle.scatter(post, C["arc_a"], len(A["src"]))
+    oracle.scatter(post, C["arc_b"], len(B["src"]))
+    t = time.perf_counter() - t0
+    return {"value": C["num_arcs"] / t, "unit": "arcs/s", "cores": 1, "kind": "oracle",
+            "sample": "one full step (forward and backward scores, posteriors, both "
+                      "scatters) of the benchmark workload by the C oracle on its own "
+                      "composed graph, single thread",
+            "seconds": round(t, 3)}
+
+
+def run_score(args, A, B, comp, dA, dB):
+    import torch
+    from paper_2110_02848_amd import gpu, synth
+    C = comp.compose(dA, dB, provenance=True, keys=False)
+    torch.cuda.synchronize()
+    V, E = int(C["num_states"]), int(C["num_arcs"])
+    EA, EB = len(A["src"]), len(B["src"])
+
+    def step():
+        sc = comp.score(C)
+        post = comp.posterior(C, sc["alpha"], sc["beta"], sc["total"])
+        ga = comp.grad_scatter(post, C["arc_a"], EA)
+        gb = comp.grad_scatter(post, C["arc_b"], EB)
+        return sc, ga, gb
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    kern = {k: [0.0, 0] for k in gpu.SCORE_KERNELS}
+    stream = torch.cuda.current_stream()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        sc, ga, gb = step()
+        for k, (ms_k, n_k) in comp.score_kernel_times().items():
+            kern[k][0] += ms_k
+            kern[k][1] += n_k
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms_wall = 1e3 * (time.perf_counter() - t0) / args.steps
+    ms_dev = ev0.elapsed_time(ev1) / args.steps
+    kernels = {}
+    for k, (ms_k, n_k) in kern.items():
+        per_launch = score_kernel_bytes(V, E) * args.steps / n_k
+        avg_ms = ms_k / n_k
+        kernels[k] = {"launches_per_step": n_k / args.steps, "ms_per_step": ms_k / args.steps,
+                      "avg_launch_us": 1e3 * avg_ms, "alg_bytes_per_launch": per_launch,
+                      "achieved_GBs": per_launch / (avg_ms * 1e-3) / 1e9}
+    dom = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
+    d = kernels[dom]
+    out = {
+        "metric": "scored arcs/sec (scores and operand gradients of emissions o lexicon)",
+        "value": E / (ms_wall * 1e-3),
+        "unit": "arcs/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_wall,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {"workload": synth.WORKLOAD_TITLES[args.workload], "name": args.workload,
+                   "seed": args.seed, "task": "score", "V_C": V, "E_C": E, "E_A": EA,
+                   "E_B": EB},
+        "ms_per_step_device": ms_dev,
+        "total": float(sc["total"].item()),
+        "kernels": kernels,
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": d["achieved_GBs"],
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": d["achieved_GBs"] / HBM_PEAK_GBS,
+                     "traffic": measured_traffic(args.workload, dom, SCORE_TRAFFIC_FILE),
+                     "avg_launch_us": d["avg_launch_us"],
+                     "alg_bytes_per_launch": d["alg_bytes_per_launch"]},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_score_baseline(A, B)
+    return out
 
 
 def cpu_baseline(A, B, E_C):
@@ -97,6 +201,9 @@ def main():
                     default="forward-first",
                     help="order of the two searches (Algorithm 1 computes the co-accessible "
                          "set first); the result is the same")
+    ap.add_argument("--task", choices=("compose", "score"), default="compose",
+                    help="compose: the composition itself; score: scores and operand "
+                         "gradients of the composed graph")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="first copy a buffer of this many MiB device to device "
                          "(calibrates HBM byte counters under rocprofv3 --pmc)")
@@ -128,6 +235,12 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+
+    if args.task == "score":
+        out = run_score(args, A, B, comp, dA, dB)
+        comp.close()
+        print(json.dumps(out), flush=True)
+        return
 
     def step():
         nv, ne = comp.run(dA, dB)

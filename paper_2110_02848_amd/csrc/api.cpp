@@ -55,7 +55,7 @@ struct fst_ctx {
   DevBuf vis, coacc, wbase, fq, bq, heavy, hoff, cnt, btot;
   // score workspace
   DevBuf s_sc, s_owner, s_extra, s_inref, s_mbeg, s_mlen, s_mcur, s_marc, s_pend, s_q, s_h,
-      s_hoff, s_val, s_acc, s_rec, s_term, s_mpos;
+      s_hoff, s_val, s_acc, s_rec, s_term, s_mpos, s_mkey;
   Scalars *h_sc = nullptr;
   ScoreScalars *h_ssc = nullptr;
   bool have_score_times = false;
@@ -313,6 +313,7 @@ int score_impl(fst_ctx *c, const fst_graph *G, double *alpha, double *beta, doub
   FST_TRY(ensure(c, c->s_rec, (size_t)V * sizeof(int4)));
   FST_TRY(ensure(c, c->s_term, 2 * E * sizeof(double)));
   FST_TRY(ensure(c, c->s_mpos, E * 4));
+  FST_TRY(ensure(c, c->s_mkey, (size_t)V * 8));
 
   ScoreGraph SG = {};
   SG.V = V;
@@ -339,6 +340,7 @@ int score_impl(fst_ctx *c, const fst_graph *G, double *alpha, double *beta, doub
   S.rec = as<int4>(c->s_rec);
   S.term = as<double>(c->s_term);
   S.mpos = as<int32_t>(c->s_mpos);
+  S.mkey = as<unsigned long long>(c->s_mkey);
   S.pend = as<int32_t>(c->s_pend);
   S.Q = as<int32_t>(c->s_q);
   S.H = as<int32_t>(c->s_h);
@@ -692,7 +694,7 @@ void fst_ctx_destroy(fst_ctx *c) {
                     &c->bInChain, &c->s_sc,     &c->s_owner, &c->s_extra, &c->s_inref,
                     &c->s_mbeg,   &c->s_mlen,   &c->s_mcur,  &c->s_marc,  &c->s_pend,
                     &c->s_q,      &c->s_h,      &c->s_hoff,  &c->s_val,   &c->s_acc,
-                    &c->s_rec,    &c->s_term,   &c->s_mpos};
+                    &c->s_rec,    &c->s_term,   &c->s_mpos,  &c->s_mkey};
   for (DevBuf *b : bufs) release(*b);
   for (int i = 0; i < NEV; ++i)
     if (c->ev[i]) (void)hipEventDestroy(c->ev[i]);

@@ -198,8 +198,8 @@ struct ScoreScalars {
 };
 
 // One direction of the score recursion (forward: alpha from in-arcs;
-// backward: beta from out-arcs): records, term slots, values, pending counters (per merge
-// forward, per state backward), the generation lists (light states in Q,
+// backward: beta from out-arcs): records, term slots, values, pending counters and
+// largest terms (per state), the generation lists (light states in Q,
 // heavy states in H with their workgroup offsets in hoff; cap entries each),
 // and the depth budget of a thread's walk.
 struct ScoreArgs {
@@ -207,6 +207,7 @@ struct ScoreArgs {
   int4 *rec;     // per-state record of this direction
   double *term;  // term slots (value + weight) for pulls: 2 E entries
   const int32_t *mpos;  // position of an in-arc of a merge in marc
+  unsigned long long *mkey;  // per state: order key of its largest term so far
   double *val;
   int32_t *pend;
   int32_t *Q, *H;

@@ -124,6 +124,17 @@ __device__ __forceinline__ void block_sum128(ull &lo, ull &hi) {
   for (int w = 1; w < NWAVES; ++w) add128(lo, hi, s_lo[w], s_hi[w]);
 }
 
+// Order-preserving integer key of a double (a larger double has a larger key;
+// key 0 is below every double).
+__device__ __forceinline__ ull order_key(double d) {
+  const ull b = (ull)__double_as_longlong(d);
+  return (b >> 63) ? ~b : (b | (1ull << 63));
+}
+__device__ __forceinline__ double from_order_key(ull k) {
+  const ull b = (k >> 63) ? (k & ~(1ull << 63)) : ~k;
+  return __longlong_as_double((long long)b);
+}
+
 // ---------------------------------------------------------------------------
 // arc lists of a state
 // ---------------------------------------------------------------------------
@@ -166,7 +177,8 @@ __device__ __forceinline__ AList notify_list(const ScoreGraph &G, int32_t v) {
 //      the notify list (an arc id, or a marc position when REC_IND)
 //   y: flags << 28 | number of notified arcs (saturated at 2^28 - 1)
 //   z: with one notified arc, its weight (binary32 bits)
-//   w: with one notified arc, its id; else -1
+//   w: with one notified arc, the slot its term goes to when the state it
+//      reaches is not walked to (see pull_slots); else -1
 // so a walk takes one dependent load per state.
 constexpr uint32_t REC_INIT = 1u << 28;    // start (forward) / accepting (backward)
 constexpr uint32_t REC_SINGLE = 1u << 29;  // exactly one arc to pull from
@@ -188,13 +200,24 @@ __device__ __forceinline__ const double *pull_slots(const ScoreArgs &S, const AL
   return S.term + (l.ind ? S.G.E : 0) + l.beg;
 }
 
+// The largest term of a state with two or more, kept by its notifiers.
+__device__ __forceinline__ double pull_max(const ScoreArgs &S, int32_t v, bool init) {
+  const ull k = S.mkey[v];
+  const double m = k ? from_order_key(k) : -INFINITY;
+  return init ? fmax(m, 0.0) : m;
+}
+
 template <bool FWD>
-__device__ double thread_pull(const ScoreArgs &S, const AList &l, bool init) {
+__device__ double thread_pull(const ScoreArgs &S, int32_t v, const AList &l, bool init) {
   const double *t = pull_slots(S, l);
   if (l.n == 1 && !init) return t[0];
-  double m = init ? 0.0 : -INFINITY;
-#pragma unroll 4
-  for (int32_t j = 0; j < l.n; ++j) m = fmax(m, t[j]);
+  double m;
+  if (l.n >= 2) {
+    m = pull_max(S, v, init);
+  } else {
+    m = init ? 0.0 : -INFINITY;
+    if (l.n == 1) m = fmax(m, t[0]);
+  }
   if (m == -INFINITY || m == INFINITY) return m;
   ull lo = 0, hi = 0;
   if (init) acc_add(lo, hi, exp(0.0 - m));
@@ -205,16 +228,19 @@ __device__ double thread_pull(const ScoreArgs &S, const AList &l, bool init) {
 
 // The same value, formed by a whole workgroup (identical bits).
 template <bool FWD>
-__device__ double block_pull(const ScoreArgs &S, const AList &l, bool init) {
+__device__ double block_pull(const ScoreArgs &S, int32_t v, const AList &l, bool init) {
   const double *t = pull_slots(S, l);
-  double m = (threadIdx.x == 0 && init) ? 0.0 : -INFINITY;
-#pragma unroll 4
-  for (int32_t j = threadIdx.x; j < l.n; j += NT) m = fmax(m, t[j]);
-  m = block_fmax(m);
+  double m;
+  if (l.n >= 2) {
+    m = pull_max(S, v, init);
+  } else {
+    m = init ? 0.0 : -INFINITY;
+    if (l.n == 1) m = fmax(m, t[0]);
+  }
   if (m == -INFINITY || m == INFINITY) return m;
   ull lo = 0, hi = 0;
   if (threadIdx.x == 0 && init) acc_add(lo, hi, exp(0.0 - m));
-#pragma unroll 4
+#pragma unroll 8
   for (int32_t j = threadIdx.x; j < l.n; j += NT) acc_add(lo, hi, exp(t[j] - m));
   block_sum128(lo, hi);
   return acc_finish(m, lo, hi);
@@ -280,10 +306,11 @@ __device__ void list_ready(const ScoreArgs &S, const ScoreNext &nx, bool want, i
 // such light y, within the depth budget) or it is listed with its term.
 // Otherwise the term goes to its slot and y's pending counter counts down;
 // the thread that takes it to zero lists y.
+// slot >= 0 is the precomputed slot of arc e's term; -1 derives it from e.
 template <bool FWD>
 __device__ __forceinline__ void settle(const ScoreArgs &S, const ScoreNext &nx, int32_t y,
-                                       float w, int32_t e, double x, int depth, int32_t &next,
-                                       double &next_val, int4 &next_rec) {
+                                       float w, int32_t e, long long slot, double x, int depth,
+                                       int32_t &next, double &next_val, int4 &next_rec) {
   const int4 ry = S.rec[y];
   const uint32_t fy = rec_flags(ry);
   const double t = x + (double)w;
@@ -294,20 +321,31 @@ __device__ __forceinline__ void settle(const ScoreArgs &S, const ScoreNext &nx, 
     if (!walk) S.term[e] = t;
   } else {
     // a forward merge's term goes to its in-list position (contiguous pull)
-    S.term[FWD ? S.G.E + S.mpos[e] : (long long)e] = t;
-    const int32_t p = FWD ? -2 - S.G.inref[y] : y;
-    // lanes of the wavefront counting down the first lane's counter do it
-    // with one atomic; the one that reaches zero lists y
+    if (slot < 0) slot = FWD ? S.G.E + S.mpos[e] : (long long)e;
+    S.term[slot] = t;
+    // lanes of the wavefront reaching the first lane's state count its
+    // pending counter down with one atomic (the one that reaches zero lists
+    // it) and raise its largest term with one atomic
     const ull act = __ballot(true);
     const int leader = __ffsll((long long)act) - 1;
-    const bool grouped = p == __shfl(p, leader);
-    const int k = (int)__popcll(__ballot(grouped));
+    const bool grouped = y == __shfl(y, leader);
+    const ull gm = __ballot(grouped);
+    const ull key = order_key(t);
     if (grouped) {
+      ull kmax = key;
+      for (ull b = gm; b; b &= b - 1) {
+        const ull o = __shfl(key, __ffsll((long long)b) - 1);
+        kmax = o > kmax ? o : kmax;
+      }
       int32_t old = 0;
-      if ((int)__lane_id() == leader) old = atomicSub(S.pend + p, k);
-      ready = (int)__lane_id() == leader && old == k;
+      if ((int)__lane_id() == leader) {
+        atomicMax(S.mkey + y, kmax);
+        old = atomicSub(S.pend + y, (int32_t)__popcll(gm));
+      }
+      ready = (int)__lane_id() == leader && old == (int32_t)__popcll(gm);
     } else {
-      ready = atomicSub(S.pend + p, 1) == 1;
+      atomicMax(S.mkey + y, key);
+      ready = atomicSub(S.pend + y, 1) == 1;
     }
   }
   if (walk) {
@@ -339,13 +377,18 @@ __device__ void walk_from(const ScoreArgs &S, const ScoreNext &nx, int32_t v, in
     double next_val = 0.0;
     int4 next_rec = rv;
     if (nd == 1) {
-      settle<FWD>(S, nx, rv.x, __int_as_float(rv.z), rv.w, x, depth, next, next_val, next_rec);
+      // the slot is the arc id unless it leads to a forward merge, where the
+      // arc id is not needed (a merge's terms go to their precomputed slots)
+      const long long slot = (long long)(uint32_t)rv.w;
+      const int32_t e = slot < S.G.E ? (int32_t)slot : -1;
+      settle<FWD>(S, nx, rv.x, __int_as_float(rv.z), e, slot, x, depth, next, next_val,
+                  next_rec);
     } else {
       for (int32_t j = 0; j < nd; ++j) {
         int32_t e, y;
         float w;
         notified<FWD>(S.G, rv, j, e, y, w);
-        settle<FWD>(S, nx, y, w, e, x, depth, next, next_val, next_rec);
+        settle<FWD>(S, nx, y, w, e, -1, x, depth, next, next_val, next_rec);
       }
     }
     if (next < 0) return;
@@ -387,7 +430,8 @@ __global__ __launch_bounds__(NT) void k_score_gen(ScoreArgs S, int g) {
     const int32_t v = S.H[cur.hbase + a];
     const uint32_t part = (uint32_t)(ub - ho[a]);
     const int4 rv = S.rec[v];
-    const double x = block_pull<FWD>(S, pull_list<FWD>(S.G, v), (rec_flags(rv) & REC_INIT) != 0);
+    const double x =
+        block_pull<FWD>(S, v, pull_list<FWD>(S.G, v), (rec_flags(rv) & REC_INIT) != 0);
     if (part == 0 && threadIdx.x == 0) {
       S.val[v] = x;
       ++fin;
@@ -400,7 +444,7 @@ __global__ __launch_bounds__(NT) void k_score_gen(ScoreArgs S, int g) {
     if (j < nl.n) {
       const int32_t e = arc_at(S.G, nl, (int32_t)j);
       const int32_t y = FWD ? S.G.dst[e] : S.G.src[e];
-      settle<FWD>(S, nx, y, S.G.w[e], e, x, 0, next, next_val, next_rec);
+      settle<FWD>(S, nx, y, S.G.w[e], e, -1, x, 0, next, next_val, next_rec);
     }
     if (next >= 0) walk_from<FWD>(S, nx, next, next_rec, next_val, 1, fin);
   }
@@ -408,7 +452,8 @@ __global__ __launch_bounds__(NT) void k_score_gen(ScoreArgs S, int g) {
   for (ull i = (ull)blockIdx.x * NT + threadIdx.x; i < n; i += (ull)gridDim.x * NT) {
     const int32_t v = S.Q[cur.qbase + (uint32_t)i];
     const int4 rv = S.rec[v];
-    const double x = thread_pull<FWD>(S, pull_list<FWD>(S.G, v), (rec_flags(rv) & REC_INIT) != 0);
+    const double x =
+        thread_pull<FWD>(S, v, pull_list<FWD>(S.G, v), (rec_flags(rv) & REC_INIT) != 0);
     walk_from<FWD>(S, nx, v, rv, x, 0, fin);
   }
   // one atomic per wavefront
@@ -434,7 +479,10 @@ __global__ __launch_bounds__(NT) void k_score_rec(ScoreArgs S) {
       const int32_t e = arc_at(G, nl, 0);
       r.x = FWD ? G.dst[e] : G.src[e];
       r.z = __float_as_int(G.w[e]);
-      r.w = e;
+      // slot of the term (see pull_slots); < 2^32 since E < 2^31
+      const bool to_merge = FWD && G.inref[r.x] <= -2;
+      r.w = (int32_t)(uint32_t)(to_merge ? (unsigned long long)G.E + (uint32_t)S.mpos[e]
+                                         : (unsigned long long)e);
     } else {
       r.x = nl.beg;
       r.z = 0;
@@ -467,14 +515,15 @@ __global__ __launch_bounds__(NT) void k_score_seed(ScoreArgs S) {
   }
 }
 
-// Pending counters: forward, per merge (its in-arc count); backward, per
-// state (its out-arc count; only states with two or more are counted down).
+// Pending counter of every state: the number of arcs it pulls from (only
+// states with two or more are counted down); and no largest term yet.
 template <bool FWD>
 __global__ __launch_bounds__(NT) void k_score_pending(ScoreArgs S) {
-  const long long n = FWD ? (long long)S.sc->nmerge : (long long)S.G.V;
-  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n;
-       i += (long long)gridDim.x * NT)
-    S.pend[i] = FWD ? S.G.mlen[i] : S.G.off[i + 1] - S.G.off[i];
+  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < S.G.V;
+       i += (long long)gridDim.x * NT) {
+    S.pend[i] = pull_list<FWD>(S.G, (int32_t)i).n;
+    S.mkey[i] = 0ull;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -605,14 +654,6 @@ __global__ __launch_bounds__(NT) void k_merge_place(ScoreGraph G, const int32_t 
 // total: log-add of val over the flagged states (same exact log-add)
 // ---------------------------------------------------------------------------
 
-__device__ __forceinline__ ull order_key(double d) {
-  const ull b = (ull)__double_as_longlong(d);
-  return (b >> 63) ? ~b : (b | (1ull << 63));
-}
-__device__ __forceinline__ double from_order_key(ull k) {
-  const ull b = (k >> 63) ? (k & ~(1ull << 63)) : ~k;
-  return __longlong_as_double((long long)b);
-}
 
 __global__ __launch_bounds__(NT) void k_total_max(const double *val, const uint8_t *flag,
                                                   int32_t V, ScoreScalars *sc) {
@@ -684,50 +725,125 @@ __device__ __forceinline__ int scale_exp(uint32_t mbits) {
 
 // acc[4 i + 0, 1]: digits of the positive terms of target i, [2, 3] of the
 // negative ones (low 32 bits, high 32 bits of each 64-bit magnitude).
+//
+// Each workgroup takes chunks of SC_CHUNK terms.  When a chunk's targets
+// span at most SC_BINS indices (provenance of consecutive arcs of C often
+// does: they come from a few states of A), the chunk is added up in LDS with
+// LDS atomics and only its nonzero words go to global atomics; otherwise
+// every term goes to global atomics, lanes of a wavefront that share the
+// first lane's target adding together.  Integer sums: the order is free.
+constexpr int SC_CHUNK = NT * 32;
+constexpr int SC_BINS = 2048;
+
+__device__ __forceinline__ bool scatter_digits(const float *g, const int32_t *idx, long long e,
+                                               int32_t m, int ex, int32_t &key, ull &d0,
+                                               ull &d1, uint32_t *bad) {
+  key = -1;
+  d0 = d1 = 0;
+  const int32_t i = idx[e];
+  if (i < -1 || i >= m) {
+    atomicOr(bad, 1u);
+    return false;
+  }
+  if (i < 0) return false;
+  const float x = g[e];
+  const ull T = (ull)ldexp(fabs((double)x), 64 - ex);
+  if (!T) return false;
+  key = 2 * i + (x < 0.f ? 1 : 0);
+  d0 = T & 0xffffffffull;
+  d1 = T >> 32;
+  return true;
+}
+
 __global__ __launch_bounds__(NT) void k_scatter(const float *g, const int32_t *idx, long long n,
                                                 int32_t m, const uint32_t *mx, ull *acc,
                                                 uint32_t *bad) {
+  __shared__ ull s_acc[4 * SC_BINS];
+  __shared__ int32_t s_lo[NWAVES], s_hi[NWAVES];
   const uint32_t mbits = *mx;
   if (mbits == 0 || mbits >= 0x7f800000u) return;  // all zero, or not finite
   const int ex = scale_exp(mbits);
-  const long long stride = (long long)gridDim.x * NT;
-  for (long long base = (long long)blockIdx.x * NT; base < n; base += stride) {
-    const long long e = base + threadIdx.x;
-    int32_t key = -1;
-    ull d0 = 0, d1 = 0;
-    if (e < n) {
+  for (long long base = (long long)blockIdx.x * SC_CHUNK; base < n;
+       base += (long long)gridDim.x * SC_CHUNK) {
+    const long long end = base + SC_CHUNK < n ? base + SC_CHUNK : n;
+    // index range of the chunk
+    int32_t lo = 0x7fffffff, hi = -1;
+    for (long long e = base + threadIdx.x; e < end; e += NT) {
       const int32_t i = idx[e];
-      if (i < -1 || i >= m) {
-        atomicOr(bad, 1u);
-      } else if (i >= 0) {
-        const float x = g[e];
-        const ull T = (ull)ldexp(fabs((double)x), 64 - ex);
-        if (T) {
-          key = 2 * i + (x < 0.f ? 1 : 0);
-          d0 = T & 0xffffffffull;
-          d1 = T >> 32;
-        }
+      if (i >= 0 && i < m) {
+        lo = min(lo, i);
+        hi = max(hi, i);
       }
     }
-    const bool need = key >= 0;
-    bool grouped;
-    int leader;
-    (void)wave_group(need, key, grouped, leader);
-    // digit sums of the grouped lanes (zeros elsewhere), over the wavefront
-    ull s0 = grouped ? d0 : 0ull, s1 = grouped ? d1 : 0ull;
 #pragma unroll
     for (int o = WAVE / 2; o > 0; o >>= 1) {
-      s0 += __shfl_xor(s0, o);
-      s1 += __shfl_xor(s1, o);
+      lo = min(lo, __shfl_xor(lo, o));
+      hi = max(hi, __shfl_xor(hi, o));
     }
-    if (grouped && (int)__lane_id() == leader) {
-      ull *a = acc + 2 * (size_t)key;
-      if (s0) atomicAdd(a, s0);
-      if (s1) atomicAdd(a + 1, s1);
-    } else if (need && !grouped) {
-      ull *a = acc + 2 * (size_t)key;
-      if (d0) atomicAdd(a, d0);
-      if (d1) atomicAdd(a + 1, d1);
+    __syncthreads();  // s_acc / s_lo of the previous chunk are no longer read
+    if (__lane_id() == 0) {
+      s_lo[threadIdx.x / WAVE] = lo;
+      s_hi[threadIdx.x / WAVE] = hi;
+    }
+    __syncthreads();
+    lo = s_lo[0];
+    hi = s_hi[0];
+#pragma unroll
+    for (int w = 1; w < NWAVES; ++w) {
+      lo = min(lo, s_lo[w]);
+      hi = max(hi, s_hi[w]);
+    }
+    if (hi < 0) {
+      // nothing to add; still report bad indices
+      for (long long e = base + threadIdx.x; e < end; e += NT) {
+        const int32_t i = idx[e];
+        if (i < -1 || i >= m) atomicOr(bad, 1u);
+      }
+      continue;
+    }
+    if (hi - lo < SC_BINS) {
+      const int words = 4 * (hi - lo + 1);
+      for (int b = threadIdx.x; b < words; b += NT) s_acc[b] = 0ull;
+      __syncthreads();
+      for (long long e = base + threadIdx.x; e < end; e += NT) {
+        int32_t key;
+        ull d0, d1;
+        if (scatter_digits(g, idx, e, m, ex, key, d0, d1, bad)) {
+          ull *a = s_acc + 2 * (key - 2 * lo);
+          if (d0) atomicAdd(a, d0);
+          if (d1) atomicAdd(a + 1, d1);
+        }
+      }
+      __syncthreads();
+      ull *ga = acc + 4 * (size_t)lo;
+      for (int b = threadIdx.x; b < words; b += NT)
+        if (s_acc[b]) atomicAdd(ga + b, s_acc[b]);
+    } else {
+      // whole wavefronts per iteration (the grouping reads every lane)
+      for (long long off = 0; off < end - base; off += NT) {
+        const long long e = base + off + threadIdx.x;
+        int32_t key = -1;
+        ull d0 = 0, d1 = 0;
+        const bool need = e < end && scatter_digits(g, idx, e, m, ex, key, d0, d1, bad);
+        bool grouped;
+        int leader;
+        (void)wave_group(need, key, grouped, leader);
+        ull s0 = grouped ? d0 : 0ull, s1 = grouped ? d1 : 0ull;
+#pragma unroll
+        for (int o = WAVE / 2; o > 0; o >>= 1) {
+          s0 += __shfl_xor(s0, o);
+          s1 += __shfl_xor(s1, o);
+        }
+        if (grouped && (int)__lane_id() == leader) {
+          ull *a = acc + 2 * (size_t)key;
+          if (s0) atomicAdd(a, s0);
+          if (s1) atomicAdd(a + 1, s1);
+        } else if (need && !grouped) {
+          ull *a = acc + 2 * (size_t)key;
+          if (d0) atomicAdd(a, d0);
+          if (d1) atomicAdd(a + 1, d1);
+        }
+      }
     }
   }
 }
@@ -834,7 +950,9 @@ hipError_t launch_scatter(const float *g, const int32_t *idx, long long n, int32
                           uint32_t *mx, uint32_t *bad, float *out, hipStream_t s) {
   if (n > 0) {
     k_absmax<<<grid_for(n), NT, 0, s>>>(g, n, mx);
-    k_scatter<<<grid_for(n), NT, 0, s>>>(g, idx, n, m, mx, acc, bad);
+    long long chunks = (n + SC_CHUNK - 1) / SC_CHUNK;
+    k_scatter<<<(unsigned)(chunks < 2048 ? chunks : 2048), NT, 0, s>>>(g, idx, n, m, mx, acc,
+                                                                      bad);
   }
   if (m > 0) k_scatter_final<<<grid_for(m), NT, 0, s>>>(acc, m, mx, out);
   return hipGetLastError();
