@@ -79,10 +79,13 @@ def measured_traffic(workload, kernel, path=TRAFFIC_FILE):
 
 
 def score_kernel_bytes(V, E):
-    """Algorithmic bytes of one direction of the score recursion: every
-    state's value written once (8 B); every arc's term formed from the value
-    at its other end, its weight and that end's id (8 + 4 + 4 B)."""
-    return 8 * V + 16 * E
+    """Algorithmic bytes per score call of each timed kernel group.
+    Generations (both directions): every state's value written once (8 B)
+    and every arc's term formed from the value at its other end, its weight
+    and that end's id (8 + 4 + 4 B), per direction.  In-arc structure: the
+    destination of every arc read twice and an owner word stored (12 B), and
+    an in-arc reference per state (4 B)."""
+    return {"score_gen": 2 * (8 * V + 16 * E), "score_prep": 12 * E + 4 * V}
 
 
 def cpu_score_baseline(A, B):
@@ -136,8 +139,9 @@ def run_score(args, A, B, comp, dA, dB):
     ms_wall = 1e3 * (time.perf_counter() - t0) / args.steps
     ms_dev = ev0.elapsed_time(ev1) / args.steps
     kernels = {}
+    kb = score_kernel_bytes(V, E)
     for k, (ms_k, n_k) in kern.items():
-        per_launch = score_kernel_bytes(V, E) * args.steps / n_k
+        per_launch = kb[k] * args.steps / n_k
         avg_ms = ms_k / n_k
         kernels[k] = {"launches_per_step": n_k / args.steps, "ms_per_step": ms_k / args.steps,
                       "avg_launch_us": 1e3 * avg_ms, "alg_bytes_per_launch": per_launch,

@@ -191,8 +191,9 @@ enum fst_kernel {
   FST_KERNEL_SEARCH_BACKWARD = 1,
   FST_KERNEL_COUNT = 2,
   FST_KERNEL_FILL = 3,
-  FST_KERNEL_SCORE_FORWARD = 4,  /* fst_score: generations of alpha          */
-  FST_KERNEL_SCORE_BACKWARD = 5  /* fst_score: generations of beta           */
+  FST_KERNEL_SCORE_GEN = 4,   /* fst_score: generation kernels (one launch
+                                 advances every direction asked for)       */
+  FST_KERNEL_SCORE_PREP = 5   /* fst_score: in-arc structure of the graph   */
 };
 
 /* With FST_OPT_TIMING on: *ms = summed device time of the launches of

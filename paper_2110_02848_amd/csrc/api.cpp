@@ -16,6 +16,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <initializer_list>
 #include <new>
 
 #include "internal.h"
@@ -32,6 +33,12 @@ struct DevBuf {
 constexpr int NEV = 10;  // a begin and an end event per phase (enum in fst_compose_phase_times)
 constexpr int NKERNELS = 6;  // enum fst_kernel
 constexpr int NCOMPOSE_KERNELS = 4;  // kernels 0-3 time a composition, 4-5 a score
+
+// Per-direction working arrays of the score recursion.
+struct ScoreBufs {
+  DevBuf sc, rec, term, mkey, pend, q, h, hoff;
+  ScoreScalars *host = nullptr;  // pinned mirror of sc
+};
 
 }  // namespace
 
@@ -54,10 +61,11 @@ struct fst_ctx {
   DevBuf aInOff, aInPerm, aInArc, aInRec, aInLut, bInOff, bInPerm, bInArc, bInRec, bInLut;
   DevBuf vis, coacc, wbase, fq, bq, heavy, hoff, cnt, btot;
   // score workspace
-  DevBuf s_sc, s_owner, s_extra, s_inref, s_mbeg, s_mlen, s_mcur, s_marc, s_pend, s_q, s_h,
-      s_hoff, s_val, s_acc, s_rec, s_term, s_mpos, s_mkey;
+  DevBuf s_sc, s_owner, s_extra, s_inref, s_mbeg, s_mlen, s_mcur, s_marc, s_val, s_acc,
+      s_mpos;
   Scalars *h_sc = nullptr;
   ScoreScalars *h_ssc = nullptr;
+  ScoreBufs score_f, score_b;  // forward / backward recursion
   bool have_score_times = false;
   hipEvent_t ev[NEV] = {};
   hipEvent_t kev[2 * NKERNELS] = {};  // per timed kernel: before, after
@@ -245,28 +253,74 @@ int score_validate(fst_ctx *c, const DevGraph &d, hipStream_t s) {
   return (c->h_ssc->err & ~info_bits) ? FST_ERR_INVALID_GRAPH : FST_OK;
 }
 
-// One direction of the recursion, generation after generation (batches as in
+int score_bufs(fst_ctx *c, ScoreBufs &b, int32_t V, size_t E) {
+  FST_TRY(ensure(c, b.sc, sizeof(ScoreScalars)));
+  FST_TRY(ensure(c, b.rec, (size_t)V * sizeof(int4)));
+  FST_TRY(ensure(c, b.term, 2 * E * sizeof(double)));
+  FST_TRY(ensure(c, b.mkey, (size_t)V * 8));
+  FST_TRY(ensure(c, b.pend, (size_t)V * 4));
+  FST_TRY(ensure(c, b.q, (size_t)V * 4));
+  FST_TRY(ensure(c, b.h, (size_t)V * 4));
+  FST_TRY(ensure(c, b.hoff, (size_t)V * 4));
+  return FST_OK;
+}
+
+ScoreArgs score_args(fst_ctx *c, ScoreBufs &b, const ScoreGraph &SG, double *val) {
+  ScoreArgs S = {};
+  S.G = SG;
+  S.rec = as<int4>(b.rec);
+  S.term = as<double>(b.term);
+  S.mpos = as<int32_t>(c->s_mpos);
+  S.mkey = as<unsigned long long>(b.mkey);
+  S.val = val;
+  S.pend = as<int32_t>(b.pend);
+  S.Q = as<int32_t>(b.q);
+  S.H = as<int32_t>(b.h);
+  S.hoff = as<uint32_t>(b.hoff);
+  S.cap = (uint32_t)SG.V;
+  S.chain = c->chain_depth;
+  S.sc = as<ScoreScalars>(b.sc);
+  return S;
+}
+
+// The recursions asked for (F forward, B backward, either may be null),
+// generation after generation, both in the same kernels (batches as in
 // search()); FST_ERR_CYCLIC if some state never became ready.
-int score_direction(fst_ctx *c, const ScoreArgs &S, bool forward, hipStream_t s) {
-  ScoreScalars *dsc = S.sc;
-  HIP_TRY(hipMemsetAsync(dsc->G, 0, sizeof(dsc->G), s));
-  HIP_TRY(hipMemsetAsync(&dsc->finished, 0, sizeof(dsc->finished), s));
-  HIP_TRY(launch_score_seed(S, forward, s));
-  const int kernel = forward ? FST_KERNEL_SCORE_FORWARD : FST_KERNEL_SCORE_BACKWARD;
-  const KernelTimer t = timer(c, kernel);
+int score_generations(fst_ctx *c, const ScoreArgs *F, const ScoreArgs *B, ScoreBufs *bf,
+                      ScoreBufs *bb, hipStream_t s) {
+  const ScoreArgs *dirs[2] = {F, B};
+  ScoreBufs *bufs[2] = {bf, bb};
+  for (int i = 0; i < 2; ++i) {
+    if (!dirs[i]) continue;
+    HIP_TRY(hipMemsetAsync(dirs[i]->sc, 0, sizeof(ScoreScalars), s));
+    HIP_TRY(launch_score_seed(*dirs[i], i == 0, s));
+  }
+  const KernelTimer t = timer(c, FST_KERNEL_SCORE_GEN);
   int g = 0, batch = 4;
   for (;;) {
     t.begin(s);
-    for (int b = 0; b < batch; ++b, ++g) HIP_TRY(launch_score_generation(S, forward, g, s));
+    for (int b = 0; b < batch; ++b, ++g) HIP_TRY(launch_score_generation(F, B, g, s));
     t.end(s);
-    FST_TRY(score_readback(c, s));
-    FST_TRY(add_time(c, kernel, batch));
-    if (c->h_ssc->overflow) return FST_ERR_TOO_LARGE;  // cannot happen: each state listed once
-    const GenSlot &nx = c->h_ssc->G[g % 3];
-    if (nx.qcount == 0 && (uint32_t)nx.hpack == 0) break;
+    for (int i = 0; i < 2; ++i)
+      if (dirs[i])
+        HIP_TRY(hipMemcpyAsync(bufs[i]->host, dirs[i]->sc, sizeof(ScoreScalars),
+                               hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    FST_TRY(add_time(c, FST_KERNEL_SCORE_GEN, batch));
+    bool more = false;
+    for (int i = 0; i < 2; ++i) {
+      if (!dirs[i]) continue;
+      // cannot happen: each state is listed at most once
+      if (bufs[i]->host->overflow) return FST_ERR_TOO_LARGE;
+      const GenSlot &nx = bufs[i]->host->G[g % 3];
+      more = more || nx.qcount != 0 || (uint32_t)nx.hpack != 0;
+    }
+    if (!more) break;
     batch = batch == 4 ? 16 : (batch < 64 ? 2 * batch : 64);
   }
-  if (c->h_ssc->finished != (unsigned long long)S.G.V) return FST_ERR_CYCLIC;
+  for (int i = 0; i < 2; ++i)
+    if (dirs[i] && bufs[i]->host->finished != (unsigned long long)dirs[i]->G.V)
+      return FST_ERR_CYCLIC;
   return FST_OK;
 }
 
@@ -298,6 +352,8 @@ int score_impl(fst_ctx *c, const fst_graph *G, double *alpha, double *beta, doub
     HIP_TRY(launch_score_total(nullptr, nullptr, 0, dsc, total, s));
     return FST_OK;
   }
+  const KernelTimer tp = timer(c, FST_KERNEL_SCORE_PREP);
+  tp.begin(s);
   FST_TRY(ensure(c, c->s_owner, (size_t)V * 4));
   FST_TRY(ensure(c, c->s_extra, (size_t)V * 4));
   FST_TRY(ensure(c, c->s_inref, (size_t)V * 4));
@@ -305,15 +361,10 @@ int score_impl(fst_ctx *c, const fst_graph *G, double *alpha, double *beta, doub
   FST_TRY(ensure(c, c->s_mlen, (size_t)V * 4));
   FST_TRY(ensure(c, c->s_mcur, (size_t)V * 4));
   FST_TRY(ensure(c, c->s_marc, E * 4));
-  FST_TRY(ensure(c, c->s_pend, (size_t)V * 4));
-  FST_TRY(ensure(c, c->s_q, (size_t)V * 4));
-  FST_TRY(ensure(c, c->s_h, (size_t)V * 4));
-  FST_TRY(ensure(c, c->s_hoff, (size_t)V * 4));
-  if (fwd && !alpha) FST_TRY(ensure(c, c->s_val, (size_t)V * 8));
-  FST_TRY(ensure(c, c->s_rec, (size_t)V * sizeof(int4)));
-  FST_TRY(ensure(c, c->s_term, 2 * E * sizeof(double)));
   FST_TRY(ensure(c, c->s_mpos, E * 4));
-  FST_TRY(ensure(c, c->s_mkey, (size_t)V * 8));
+  if (fwd && !alpha) FST_TRY(ensure(c, c->s_val, (size_t)V * 8));
+  if (fwd) FST_TRY(score_bufs(c, c->score_f, V, E));
+  if (beta) FST_TRY(score_bufs(c, c->score_b, V, E));
 
   ScoreGraph SG = {};
   SG.V = V;
@@ -334,30 +385,15 @@ int score_impl(fst_ctx *c, const fst_graph *G, double *alpha, double *beta, doub
                                  as<int32_t>(c->s_inref), as<int32_t>(c->s_mbeg),
                                  as<int32_t>(c->s_mlen), as<int32_t>(c->s_mcur),
                                  as<int32_t>(c->s_marc), as<int32_t>(c->s_mpos), dsc, s));
-
-  ScoreArgs S = {};
-  S.G = SG;
-  S.rec = as<int4>(c->s_rec);
-  S.term = as<double>(c->s_term);
-  S.mpos = as<int32_t>(c->s_mpos);
-  S.mkey = as<unsigned long long>(c->s_mkey);
-  S.pend = as<int32_t>(c->s_pend);
-  S.Q = as<int32_t>(c->s_q);
-  S.H = as<int32_t>(c->s_h);
-  S.hoff = as<uint32_t>(c->s_hoff);
-  S.cap = (uint32_t)V;
-  S.chain = c->chain_depth;
-  S.sc = dsc;
-  if (fwd) {
-    S.val = alpha ? alpha : as<double>(c->s_val);
-    FST_TRY(score_direction(c, S, true, s));
-    FST_TRY(score_total(c, S.val, d.accept, V, total, s));
-  }
-  if (beta) {
-    S.val = beta;
-    FST_TRY(score_direction(c, S, false, s));
-    if (!fwd) FST_TRY(score_total(c, beta, d.start, V, total, s));
-  }
+  tp.end(s);
+  ScoreArgs SF = {}, SB = {};
+  if (fwd) SF = score_args(c, c->score_f, SG, alpha ? alpha : as<double>(c->s_val));
+  if (beta) SB = score_args(c, c->score_b, SG, beta);
+  FST_TRY(score_generations(c, fwd ? &SF : nullptr, beta ? &SB : nullptr, &c->score_f,
+                            &c->score_b, s));
+  FST_TRY(add_time(c, FST_KERNEL_SCORE_PREP, 1));
+  if (fwd) FST_TRY(score_total(c, SF.val, d.accept, V, total, s));
+  else FST_TRY(score_total(c, beta, d.start, V, total, s));
   c->have_score_times = c->timing;
   return FST_OK;
 }
@@ -663,6 +699,14 @@ int fst_ctx_create(int device, fst_ctx **ctx) {
     return FST_ERR_NOMEM;
   }
   memset(c->h_ssc, 0, sizeof(ScoreScalars));
+  for (ScoreBufs *b : {&c->score_f, &c->score_b}) {
+    if (hipHostMalloc(reinterpret_cast<void **>(&b->host), sizeof(ScoreScalars), 0) !=
+        hipSuccess) {
+      fst_ctx_destroy(c);
+      return FST_ERR_NOMEM;
+    }
+    memset(b->host, 0, sizeof(ScoreScalars));
+  }
   for (int i = 0; i < NEV; ++i) {
     if (hipEventCreate(&c->ev[i]) != hipSuccess) {
       fst_ctx_destroy(c);
@@ -692,10 +736,15 @@ void fst_ctx_destroy(fst_ctx *c) {
                     &c->bq,       &c->heavy,    &c->hoff,    &c->cnt,     &c->aOutLab,
                     &c->aOutW,    &c->bOutLab,  &c->bOutW,   &c->btot,    &c->bOutChain,
                     &c->bInChain, &c->s_sc,     &c->s_owner, &c->s_extra, &c->s_inref,
-                    &c->s_mbeg,   &c->s_mlen,   &c->s_mcur,  &c->s_marc,  &c->s_pend,
-                    &c->s_q,      &c->s_h,      &c->s_hoff,  &c->s_val,   &c->s_acc,
-                    &c->s_rec,    &c->s_term,   &c->s_mpos,  &c->s_mkey};
+                    &c->s_mbeg,   &c->s_mlen,   &c->s_mcur,  &c->s_marc,  &c->s_val,
+                    &c->s_acc,    &c->s_mpos};
   for (DevBuf *b : bufs) release(*b);
+  for (ScoreBufs *sb : {&c->score_f, &c->score_b}) {
+    for (DevBuf *b : {&sb->sc, &sb->rec, &sb->term, &sb->mkey, &sb->pend, &sb->q, &sb->h,
+                      &sb->hoff})
+      release(*b);
+    if (sb->host) (void)hipHostFree(sb->host);
+  }
   for (int i = 0; i < NEV; ++i)
     if (c->ev[i]) (void)hipEventDestroy(c->ev[i]);
   for (int i = 0; i < 2 * NKERNELS; ++i)

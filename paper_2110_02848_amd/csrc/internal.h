@@ -441,8 +441,9 @@ hipError_t launch_score_structure(const ScoreGraph &G, int32_t *owner, int32_t *
                                   hipStream_t s);
 // Pending counters and generation 0 of one direction (sc->G zeroed).
 hipError_t launch_score_seed(const ScoreArgs &S, bool forward, hipStream_t s);
-// Generation g of one direction: one kernel.
-hipError_t launch_score_generation(const ScoreArgs &S, bool forward, int g, hipStream_t s);
+// Generation g of the forward (F) and / or backward (B) recursion: one kernel.
+hipError_t launch_score_generation(const ScoreArgs *F, const ScoreArgs *B, int g,
+                                   hipStream_t s);
 // *total = log-add of val[v] over the states with flag[v] (sc->zmax, zlo,
 // zhi zeroed).
 hipError_t launch_score_total(const double *val, const uint8_t *flag, int32_t V,

@@ -323,29 +323,27 @@ __device__ __forceinline__ void settle(const ScoreArgs &S, const ScoreNext &nx, 
     // a forward merge's term goes to its in-list position (contiguous pull)
     if (slot < 0) slot = FWD ? S.G.E + S.mpos[e] : (long long)e;
     S.term[slot] = t;
-    // lanes of the wavefront reaching the first lane's state count its
-    // pending counter down with one atomic (the one that reaches zero lists
-    // it) and raise its largest term with one atomic
-    const ull act = __ballot(true);
-    const int leader = __ffsll((long long)act) - 1;
-    const bool grouped = y == __shfl(y, leader);
-    const ull gm = __ballot(grouped);
+    // the lanes of the wavefront here that reach the same state count its
+    // pending counter down with one atomic (the lane that takes it to zero
+    // lists it) and raise its largest term with one atomic; one round per
+    // distinct state
     const ull key = order_key(t);
-    if (grouped) {
-      ull kmax = key;
+    ull rem = __ballot(true);
+    ready = false;
+    while (rem) {
+      const int leader = __ffsll((long long)rem) - 1;
+      const ull gm = __ballot(y == __shfl(y, leader));
+      ull kmax = 0;
       for (ull b = gm; b; b &= b - 1) {
         const ull o = __shfl(key, __ffsll((long long)b) - 1);
         kmax = o > kmax ? o : kmax;
       }
-      int32_t old = 0;
       if ((int)__lane_id() == leader) {
         atomicMax(S.mkey + y, kmax);
-        old = atomicSub(S.pend + y, (int32_t)__popcll(gm));
+        const int32_t k = (int32_t)__popcll(gm);
+        ready = atomicSub(S.pend + y, k) == k;
       }
-      ready = (int)__lane_id() == leader && old == (int32_t)__popcll(gm);
-    } else {
-      atomicMax(S.mkey + y, key);
-      ready = atomicSub(S.pend + y, 1) == 1;
+      rem &= ~gm;
     }
   }
   if (walk) {
@@ -399,9 +397,10 @@ __device__ void walk_from(const ScoreArgs &S, const ScoreNext &nx, int32_t v, in
   }
 }
 
-// Generation g: workgroups of heavy states, then one thread per light state.
+// Generation g of one direction on workgroups bid = 0 .. nb - 1: workgroups
+// of heavy states, then one thread per light state.
 template <bool FWD>
-__global__ __launch_bounds__(NT) void k_score_gen(ScoreArgs S, int g) {
+__device__ void gen_body(const ScoreArgs &S, int g, unsigned bid, unsigned nb) {
   ScoreScalars *sc = S.sc;
   if (sc->overflow) return;
   const GenSlot cur = sc->G[g % 3];
@@ -411,7 +410,7 @@ __global__ __launch_bounds__(NT) void k_score_gen(ScoreArgs S, int g) {
   nx.slot = &sc->G[(g + 1) % 3];
   nx.qbase = cur.qbase + cur.qcount;
   nx.hbase = cur.hbase + hcount;
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
+  if (bid == 0 && threadIdx.x == 0) {
     nx.slot->qbase = nx.qbase;  // read by generation g + 1 only
     nx.slot->hbase = nx.hbase;
     GenSlot *done = &sc->G[(g + 2) % 3];  // generation g - 1: free
@@ -421,7 +420,7 @@ __global__ __launch_bounds__(NT) void k_score_gen(ScoreArgs S, int g) {
   }
   uint32_t fin = 0;
   const uint32_t *ho = S.hoff + cur.hbase;
-  for (ull ub = blockIdx.x; ub < HB; ub += gridDim.x) {
+  for (ull ub = bid; ub < HB; ub += nb) {
     uint32_t a = 0, b = hcount - 1;  // largest a with ho[a] <= ub
     while (a < b) {
       const uint32_t mid = (a + b + 1) >> 1;
@@ -449,7 +448,7 @@ __global__ __launch_bounds__(NT) void k_score_gen(ScoreArgs S, int g) {
     if (next >= 0) walk_from<FWD>(S, nx, next, next_rec, next_val, 1, fin);
   }
   const ull n = cur.qcount;
-  for (ull i = (ull)blockIdx.x * NT + threadIdx.x; i < n; i += (ull)gridDim.x * NT) {
+  for (ull i = (ull)bid * NT + threadIdx.x; i < n; i += (ull)nb * NT) {
     const int32_t v = S.Q[cur.qbase + (uint32_t)i];
     const int4 rv = S.rec[v];
     const double x =
@@ -460,6 +459,19 @@ __global__ __launch_bounds__(NT) void k_score_gen(ScoreArgs S, int g) {
 #pragma unroll
   for (int o = WAVE / 2; o > 0; o >>= 1) fin += __shfl_xor(fin, o);
   if (__lane_id() == 0 && fin) atomicAdd(&sc->finished, (ull)fin);
+}
+
+template <bool FWD>
+__global__ __launch_bounds__(NT) void k_score_gen(ScoreArgs S, int g) {
+  gen_body<FWD>(S, g, blockIdx.x, gridDim.x);
+}
+
+// Both directions at once (they are independent): the first half of the
+// workgroups advances the forward recursion, the second half the backward.
+__global__ __launch_bounds__(NT) void k_score_gen2(ScoreArgs F, ScoreArgs B, int g) {
+  const unsigned half = gridDim.x / 2;
+  if (blockIdx.x < half) gen_body<true>(F, g, blockIdx.x, half);
+  else gen_body<false>(B, g, blockIdx.x - half, half);
 }
 
 // Records of one direction (see REC_*).
@@ -628,22 +640,20 @@ __global__ __launch_bounds__(NT) void k_merge_place(ScoreGraph G, const int32_t 
       const int32_t r = inref[G.dst[e]];
       if (r <= -2) mi = -2 - r;
     }
-    const bool need = mi >= 0;
-    bool grouped;
-    int leader;
-    const uint32_t cnt = wave_group(need, mi, grouped, leader);
-    int32_t pos = 0;
-    if (grouped) {
+    // the lanes that place into the same merge take consecutive positions
+    // from one atomic; one round per distinct merge in the wavefront
+    ull rem = __ballot(mi >= 0);
+    int32_t pos = -1;
+    while (rem) {
+      const int leader = __ffsll((long long)rem) - 1;
+      const ull gm = __ballot(mi >= 0 && mi == __shfl(mi, leader));
       int32_t b = 0;
-      if ((int)__lane_id() == leader) b = atomicAdd(mcur + mi, (int32_t)cnt);
-      // leader is grouped, so it is active in this branch
+      if ((int)__lane_id() == leader) b = atomicAdd(mcur + mi, (int32_t)__popcll(gm));
       b = __shfl(b, leader);
-      const ull gm = __ballot(true);  // the grouped lanes (active here)
-      pos = b + (int32_t)__popcll(gm & __lanemask_lt());
-    } else if (need) {
-      pos = atomicAdd(mcur + mi, 1);
+      if ((gm >> __lane_id()) & 1ull) pos = b + (int32_t)__popcll(gm & __lanemask_lt());
+      rem &= ~gm;
     }
-    if (need) {
+    if (pos >= 0) {
       marc[pos] = (int32_t)e;
       mpos[e] = pos;
     }
@@ -707,10 +717,20 @@ __global__ __launch_bounds__(NT) void k_posterior(ScoreGraph G, const double *al
 }
 
 __global__ __launch_bounds__(NT) void k_absmax(const float *g, long long n, uint32_t *mx) {
-  uint32_t m = 0;
-  for (long long e = (long long)blockIdx.x * NT + threadIdx.x; e < n;
+  uint32_t m = 0;  // |g| orders as its bits
+  const long long n4 = ((uintptr_t)g & 15) ? 0 : n / 4;
+  const float4 *g4 = reinterpret_cast<const float4 *>(g);
+  for (long long e = (long long)blockIdx.x * NT + threadIdx.x; e < n4;
+       e += (long long)gridDim.x * NT) {
+    const float4 q = g4[e];
+    m = max(m, __float_as_uint(q.x) & 0x7fffffffu);
+    m = max(m, __float_as_uint(q.y) & 0x7fffffffu);
+    m = max(m, __float_as_uint(q.z) & 0x7fffffffu);
+    m = max(m, __float_as_uint(q.w) & 0x7fffffffu);
+  }
+  for (long long e = 4 * n4 + (long long)blockIdx.x * NT + threadIdx.x; e < n;
        e += (long long)gridDim.x * NT)
-    m = max(m, __float_as_uint(g[e]) & 0x7fffffffu);  // |g| orders as its bits
+    m = max(m, __float_as_uint(g[e]) & 0x7fffffffu);
 #pragma unroll
   for (int o = WAVE / 2; o > 0; o >>= 1) m = max(m, (uint32_t)__shfl_xor(m, o));
   if (__lane_id() == 0 && m) atomicMax(mx, m);
@@ -926,9 +946,11 @@ hipError_t launch_score_seed(const ScoreArgs &S, bool forward, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_score_generation(const ScoreArgs &S, bool forward, int g, hipStream_t s) {
-  if (forward) k_score_gen<true><<<SCORE_GRID, NT, 0, s>>>(S, g);
-  else k_score_gen<false><<<SCORE_GRID, NT, 0, s>>>(S, g);
+hipError_t launch_score_generation(const ScoreArgs *F, const ScoreArgs *B, int g,
+                                   hipStream_t s) {
+  if (F && B) k_score_gen2<<<2 * SCORE_GRID, NT, 0, s>>>(*F, *B, g);
+  else if (F) k_score_gen<true><<<SCORE_GRID, NT, 0, s>>>(*F, g);
+  else if (B) k_score_gen<false><<<SCORE_GRID, NT, 0, s>>>(*B, g);
   return hipGetLastError();
 }
 
@@ -949,7 +971,7 @@ hipError_t launch_posterior(const ScoreGraph &G, const double *alpha, const doub
 hipError_t launch_scatter(const float *g, const int32_t *idx, long long n, int32_t m, ull *acc,
                           uint32_t *mx, uint32_t *bad, float *out, hipStream_t s) {
   if (n > 0) {
-    k_absmax<<<grid_for(n), NT, 0, s>>>(g, n, mx);
+    k_absmax<<<grid_for(n / 4 + 1), NT, 0, s>>>(g, n, mx);
     long long chunks = (n + SC_CHUNK - 1) / SC_CHUNK;
     k_scatter<<<(unsigned)(chunks < 2048 ? chunks : 2048), NT, 0, s>>>(g, idx, n, m, mx, acc,
                                                                       bad);

@@ -39,7 +39,7 @@ PHASES = ("preprocess", "forward", "backward", "count", "fill")
 
 # kernels timed one by one (enum fst_kernel): a composition's, then a score's
 KERNELS = ("search_forward", "search_backward", "count", "fill")
-SCORE_KERNELS = ("score_forward", "score_backward")
+SCORE_KERNELS = ("score_gen", "score_prep")
 
 
 class FstError(RuntimeError):

@@ -38,8 +38,7 @@ FAMILIES = {
     "count": ("k_count(", "k_count_heavy("),
     "fill": ("k_fill_light(", "k_fill_heavy("),
     # scores of the composed graph (bench.py --task score)
-    "score_forward": ("k_score_gen<true>",),
-    "score_backward": ("k_score_gen<false>",),
+    "score_gen": ("k_score_gen<true>", "k_score_gen<false>", "k_score_gen2("),
     "score_structure": ("k_owner(", "k_extra(", "k_merge_index(", "k_merge_place(",
                         "k_score_rec<", "k_score_pending<", "k_score_seed<"),
     "posterior": ("k_posterior(",),
