@@ -10,6 +10,9 @@ L=3..10) workload, inputs resident in HBM.  Prints one JSON line.
 instead: one step = forward and backward log-semiring scores of C, the arc
 posteriors, and their scatter to the arcs of A and B through provenance (C
 is composed once, untimed).
+
+``--task batch --batch N`` composes N utterances (emissions of T=500 frames,
+different seeds) with the one lexicon in a single pass per step.
 """
 from __future__ import annotations
 
@@ -179,6 +182,64 @@ def run_score(args, A, B, comp, dA, dB):
     return out
 
 
+def run_batch(args, comp):
+    import torch
+    from paper_2110_02848_amd import gpu, synth
+    As, B, _ = synth.lexicon_batch(args.workload, args.batch, args.seed)
+    dAs = [gpu.to_device(A) for A in As]
+    dB = gpu.to_device(B)
+
+    def step():
+        nv, ne, st, ar = comp.run_batch(dAs, dB)
+        C = comp.alloc_output(nv, ne, provenance=False, keys=False)
+        comp.fill(C)
+        return C, st, ar
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    kern = {k: [0.0, 0] for k in gpu.KERNELS}
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        C, st, ar = step()
+        for k, (ms_k, n_k) in comp.kernel_times().items():
+            kern[k][0] += ms_k
+            kern[k][1] += n_k
+    torch.cuda.synchronize()
+    ms_wall = 1e3 * (time.perf_counter() - t0) / args.steps
+    V, E = int(C["num_states"]), int(C["num_arcs"])
+    st_moves = comp.stats()
+    kernels = {k: {"launches_per_step": n / args.steps, "ms_per_step": ms / args.steps,
+                   "avg_launch_us": 1e3 * ms / n if n else 0.0}
+               for k, (ms, n) in kern.items()}
+    out = {
+        "metric": "composed arcs/sec (batch of emissions o one lexicon)",
+        "value": E / (ms_wall * 1e-3),
+        "unit": "arcs/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_wall,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{args.batch} x " + synth.WORKLOAD_TITLES[args.workload],
+                   "name": args.workload, "seed": args.seed, "task": "batch",
+                   "batch": args.batch, "V_C": V, "E_C": E,
+                   "item_states": [int(x) for x in np.diff(st)],
+                   "item_arcs": [int(x) for x in np.diff(ar)]},
+        "kernels": kernels,
+        "search_stats": {k: st_moves[k] for k in ("key_space", "fwd_levels", "bwd_levels")},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(As[0], B, int(ar[1] - ar[0]))
+        out["cpu_baseline"]["sample"] = ("one item of the batch composed by the sequential C "
+                                         "oracle (forward-then-trim order), single thread")
+    return out
+
+
 def cpu_baseline(A, B, E_C):
     import oracle
     oracle.build(force=False)
@@ -205,9 +266,11 @@ def main():
                     default="forward-first",
                     help="order of the two searches (Algorithm 1 computes the co-accessible "
                          "set first); the result is the same")
-    ap.add_argument("--task", choices=("compose", "score"), default="compose",
+    ap.add_argument("--task", choices=("compose", "score", "batch"), default="compose",
                     help="compose: the composition itself; score: scores and operand "
-                         "gradients of the composed graph")
+                         "gradients of the composed graph; batch: --batch utterances "
+                         "composed with one lexicon per step")
+    ap.add_argument("--batch", type=int, default=8)
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="first copy a buffer of this many MiB device to device "
                          "(calibrates HBM byte counters under rocprofv3 --pmc)")
@@ -240,8 +303,9 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    if args.task == "score":
-        out = run_score(args, A, B, comp, dA, dB)
+    if args.task in ("score", "batch"):
+        out = run_score(args, A, B, comp, dA, dB) if args.task == "score" else \
+            run_batch(args, comp)
         comp.close()
         print(json.dumps(out), flush=True)
         return

@@ -248,6 +248,35 @@ FST_API int fst_score_posterior(fst_ctx *ctx, const fst_graph *G, const double *
 FST_API int fst_grad_scatter(fst_ctx *ctx, int64_t n, const float *grad, const int32_t *idx,
                              int32_t m, float *out, void *stream);
 
+/* ---- Batches and chains ------------------------------------------------
+ * Batch (the realistic workload of Section 4.2: the emission graphs of many
+ * utterances composed with one lexicon): C_i = A_i o B for i < n in one
+ * pass.  The A_i (host array of n device graphs) are composed as their
+ * disjoint union; keys of different items never meet, and in the canonical
+ * order (qa first) item i's states and arcs are the contiguous ranges
+ * [item_states[i], item_states[i+1]) and [item_arcs[i], item_arcs[i+1]) of
+ * the one C that fst_compose_fill then writes.  Ids in that C are those of
+ * the union: subtract item_states[i] from src, dst (and item_arcs[i] from
+ * arc_offset) for item-local values; key_a and arc_a index the union of the
+ * A_i (subtract the states / arcs of the items before i).  item_states and
+ * item_arcs are host arrays of n + 1 entries, filled on success (the last
+ * entries are V_C and E_C).  Limits as for one A, applied to the union.
+ * Chains (N-way composition): C has the input layout, so A o B o D is two
+ * calls (compose, then compose C with D). */
+FST_API int fst_compose_batch_run(fst_ctx *ctx, const fst_graph *A, int32_t n,
+                                  const fst_graph *B, void *stream, int64_t *num_states,
+                                  int64_t *num_arcs, int64_t *item_states,
+                                  int64_t *item_arcs);
+
+/* Per-item totals of a batch: totals[i] = log-sum of exp(val[v]) over the
+ * v in [bounds[i], bounds[i+1]) with flag[v] != 0, for i < n (exact as in
+ * fst_score; -inf for an empty set).  With val = alpha of the batch's C,
+ * flag = its accept array and bounds = item_states, totals are the items'
+ * forward scores.  val, flag, totals: device; bounds: host, n + 1
+ * non-decreasing entries within the arrays.  Blocks until done. */
+FST_API int fst_segment_logsum(fst_ctx *ctx, const double *val, const uint8_t *flag, int32_t n,
+                               const int64_t *bounds, double *totals, void *stream);
+
 /* Static string for a status code. */
 FST_API const char *fst_strerror(int code);
 

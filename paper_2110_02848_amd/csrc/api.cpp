@@ -18,6 +18,7 @@
 
 #include <initializer_list>
 #include <new>
+#include <vector>
 
 #include "internal.h"
 
@@ -63,6 +64,8 @@ struct fst_ctx {
   // score workspace
   DevBuf s_sc, s_owner, s_extra, s_inref, s_mbeg, s_mlen, s_mcur, s_marc, s_val, s_acc,
       s_mpos;
+  // batches: the union of the A graphs, item tables, segment sums
+  DevBuf u_off, u_src, u_dst, u_il, u_ol, u_w, u_start, u_accept, u_items, seg;
   Scalars *h_sc = nullptr;
   ScoreScalars *h_ssc = nullptr;
   ScoreBufs score_f, score_b;  // forward / backward recursion
@@ -75,6 +78,7 @@ struct fst_ctx {
   bool ready = false;
   Problem P = {};
   uint32_t nstates = 0, narcs = 0, nheavy = 0;
+  unsigned long long nkeys = 0;
   size_t out_per = NT;  // states per workgroup in the output passes
   fst_stats stats = {};
 };
@@ -450,6 +454,7 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   const unsigned long long nkeys = (unsigned long long)VA << (shiftB + 1);
   if (nkeys >= (1ull << 32)) return FST_ERR_TOO_LARGE;
   c->stats.key_space = (int64_t)nkeys;
+  c->nkeys = nkeys;
   const int labA = bitlen(c->h_sc->maxLabA), labB = bitlen(c->h_sc->maxLabB);
 
   // ---- label-sorted views ----
@@ -668,6 +673,101 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   return FST_OK;
 }
 
+// Batch: validate every item, lay the items out as one disjoint union (state
+// and arc offsets shifted), compose the union with B, then find each item's
+// state and arc range in C.
+int batch_impl(fst_ctx *c, const fst_graph *A, int32_t n, const fst_graph *B, hipStream_t s,
+               int64_t *V_C, int64_t *E_C, int64_t *item_states, int64_t *item_arcs) {
+  long long VA = 0, EA = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    FST_TRY(check_graph_args(&A[i]));
+    VA += A[i].num_states;
+    EA += A[i].num_arcs;
+  }
+  if (VA > NBR_MASK || EA > INT32_MAX) return FST_ERR_TOO_LARGE;
+  // each item on its own first: an arc of one item must not name a state
+  // of another once the union shifts its ids
+  FST_TRY(ensure(c, c->scal, sizeof(Scalars)));
+  Scalars *d_sc = as<Scalars>(c->scal);
+  HIP_TRY(hipMemsetAsync(d_sc, 0, sizeof(Scalars), s));
+  for (int32_t i = 0; i < n; ++i)
+    if (A[i].num_states > 0)
+      HIP_TRY(launch_validate(dev_graph(&A[i]), 0, &d_sc->errA, &d_sc->maxLabA, s));
+  FST_TRY(readback(c, s));
+  if (c->h_sc->errA & ~(1u << 16)) return FST_ERR_INVALID_GRAPH;
+
+  FST_TRY(ensure(c, c->u_off, ((size_t)VA + 1) * 4));
+  FST_TRY(ensure(c, c->u_src, (size_t)EA * 4));
+  FST_TRY(ensure(c, c->u_dst, (size_t)EA * 4));
+  FST_TRY(ensure(c, c->u_il, (size_t)EA * 4));
+  FST_TRY(ensure(c, c->u_ol, (size_t)EA * 4));
+  FST_TRY(ensure(c, c->u_w, (size_t)EA * 4));
+  FST_TRY(ensure(c, c->u_start, (size_t)VA));
+  FST_TRY(ensure(c, c->u_accept, (size_t)VA));
+  FST_TRY(ensure(c, c->u_items, ((size_t)n + 1) * 3 * sizeof(long long)));
+  int32_t *off = as<int32_t>(c->u_off);
+  HIP_TRY(hipMemsetAsync(off, 0, 4, s));  // the offsets of an empty union
+  long long vb = 0, eb = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    const DevGraph a = dev_graph(&A[i]);
+    if (a.V > 0) {
+      HIP_TRY(launch_union_copy(a, vb, eb, off, as<int32_t>(c->u_src), as<int32_t>(c->u_dst), s));
+      HIP_TRY(hipMemcpyAsync(as<uint8_t>(c->u_start) + vb, a.start, (size_t)a.V,
+                             hipMemcpyDeviceToDevice, s));
+      HIP_TRY(hipMemcpyAsync(as<uint8_t>(c->u_accept) + vb, a.accept, (size_t)a.V,
+                             hipMemcpyDeviceToDevice, s));
+    }
+    if (a.E > 0) {
+      HIP_TRY(hipMemcpyAsync(as<int32_t>(c->u_il) + eb, a.il, (size_t)a.E * 4,
+                             hipMemcpyDeviceToDevice, s));
+      HIP_TRY(hipMemcpyAsync(as<int32_t>(c->u_ol) + eb, a.ol, (size_t)a.E * 4,
+                             hipMemcpyDeviceToDevice, s));
+      HIP_TRY(hipMemcpyAsync(as<float>(c->u_w) + eb, a.w, (size_t)a.E * 4,
+                             hipMemcpyDeviceToDevice, s));
+    }
+    vb += a.V;
+    eb += a.E;
+  }
+  fst_graph U = {};
+  U.num_states = (int32_t)VA;
+  U.num_arcs = (int32_t)EA;
+  U.arc_offset = off;
+  U.src = as<int32_t>(c->u_src);
+  U.dst = as<int32_t>(c->u_dst);
+  U.ilabel = as<int32_t>(c->u_il);
+  U.olabel = as<int32_t>(c->u_ol);
+  U.weight = as<float>(c->u_w);
+  U.start = as<uint8_t>(c->u_start);
+  U.accept = as<uint8_t>(c->u_accept);
+  FST_TRY(run_impl(c, &U, B, s, V_C, E_C));
+
+  // item ranges: qa_base[0..n] (first state of A of each item, then VA)
+  std::vector<long long> h(3 * ((size_t)n + 1), 0);
+  long long acc = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    h[i] = acc;
+    acc += A[i].num_states;
+  }
+  h[n] = acc;
+  if (c->nstates == 0) {
+    for (int32_t i = 0; i <= n; ++i) item_states[i] = item_arcs[i] = 0;
+    return FST_OK;
+  }
+  long long *dq = as<long long>(c->u_items), *dout = dq + (n + 1);
+  HIP_TRY(hipMemcpyAsync(dq, h.data(), ((size_t)n + 1) * sizeof(long long),
+                         hipMemcpyHostToDevice, s));
+  HIP_TRY(launch_item_ranges(c->P, c->nkeys, n, dq, as<uint32_t>(c->cnt), as<uint32_t>(c->btot),
+                             c->out_per, c->nstates, c->narcs, dout, s));
+  HIP_TRY(hipMemcpyAsync(h.data() + (n + 1), dout, 2 * ((size_t)n + 1) * sizeof(long long),
+                         hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  for (int32_t i = 0; i <= n; ++i) {
+    item_states[i] = h[(n + 1) + i];
+    item_arcs[i] = h[2 * (n + 1) + i];
+  }
+  return FST_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -737,7 +837,9 @@ void fst_ctx_destroy(fst_ctx *c) {
                     &c->aOutW,    &c->bOutLab,  &c->bOutW,   &c->btot,    &c->bOutChain,
                     &c->bInChain, &c->s_sc,     &c->s_owner, &c->s_extra, &c->s_inref,
                     &c->s_mbeg,   &c->s_mlen,   &c->s_mcur,  &c->s_marc,  &c->s_val,
-                    &c->s_acc,    &c->s_mpos};
+                    &c->s_acc,    &c->s_mpos,   &c->u_off,   &c->u_src,   &c->u_dst,
+                    &c->u_il,     &c->u_ol,     &c->u_w,     &c->u_start, &c->u_accept,
+                    &c->u_items,  &c->seg};
   for (DevBuf *b : bufs) release(*b);
   for (ScoreBufs *sb : {&c->score_f, &c->score_b}) {
     for (DevBuf *b : {&sb->sc, &sb->rec, &sb->term, &sb->mkey, &sb->pend, &sb->q, &sb->h,
@@ -800,6 +902,36 @@ int fst_compose_run(fst_ctx *c, const fst_graph *A, const fst_graph *B, void *st
     c->ready = false;
     *num_states = 0;
     *num_arcs = 0;
+    (void)hipGetLastError();
+  }
+  return rc;
+}
+
+int fst_compose_batch_run(fst_ctx *c, const fst_graph *A, int32_t n, const fst_graph *B,
+                          void *stream, int64_t *num_states, int64_t *num_arcs,
+                          int64_t *item_states, int64_t *item_arcs) {
+  if (!c || n < 0 || (n > 0 && !A) || !B || !num_states || !num_arcs || !item_states ||
+      !item_arcs)
+    return FST_ERR_INVALID_ARG;
+  DeviceGuard g(c->device);
+  if (!g.ok) return FST_ERR_HIP;
+  c->ready = false;
+  c->have_times = false;
+  c->timed_run = false;
+  *num_states = 0;
+  *num_arcs = 0;
+  int rc = FST_OK;
+  try {
+    rc = batch_impl(c, A, n, B, reinterpret_cast<hipStream_t>(stream), num_states, num_arcs,
+                    item_states, item_arcs);
+  } catch (const std::bad_alloc &) {
+    rc = FST_ERR_NOMEM;
+  }
+  if (rc != FST_OK) {
+    c->ready = false;
+    *num_states = 0;
+    *num_arcs = 0;
+    for (int32_t i = 0; i <= n; ++i) item_states[i] = item_arcs[i] = 0;
     (void)hipGetLastError();
   }
   return rc;
@@ -933,6 +1065,37 @@ int fst_grad_scatter(fst_ctx *c, int64_t n, const float *grad, const int32_t *id
   }
   FST_TRY(score_readback(c, s));
   return c->h_ssc->bad ? FST_ERR_INVALID_ARG : FST_OK;
+}
+
+int fst_segment_logsum(fst_ctx *c, const double *val, const uint8_t *flag, int32_t n,
+                       const int64_t *bounds, double *totals, void *stream) {
+  if (!c || n < 0 || !bounds) return FST_ERR_INVALID_ARG;
+  if (n > 0 && !totals) return FST_ERR_INVALID_ARG;
+  long long max_len = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    if (bounds[i] < 0 || bounds[i + 1] < bounds[i]) return FST_ERR_INVALID_ARG;
+    if (bounds[i + 1] - bounds[i] > max_len) max_len = bounds[i + 1] - bounds[i];
+  }
+  if (max_len > 0 && (!val || !flag)) return FST_ERR_INVALID_ARG;
+  if (n == 0) return FST_OK;
+  DeviceGuard g(c->device);
+  if (!g.ok) return FST_ERR_HIP;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  FST_TRY(ensure(c, c->seg, ((size_t)n + 1) * sizeof(long long) +
+                                3 * (size_t)n * sizeof(unsigned long long)));
+  long long *db = as<long long>(c->seg);
+  unsigned long long *z = reinterpret_cast<unsigned long long *>(db + n + 1);
+  HIP_TRY(hipMemcpyAsync(db, bounds, ((size_t)n + 1) * sizeof(long long), hipMemcpyHostToDevice,
+                         s));
+  HIP_TRY(hipMemsetAsync(z, 0, 3 * (size_t)n * sizeof(unsigned long long), s));
+  if (launch_segment_logsum(val, flag, n, db, max_len, z, totals, s) != hipSuccess) {
+    (void)hipGetLastError();
+    return FST_ERR_HIP;
+  }
+  // the host bounds were read by the copy above; nothing else is pending on
+  // host memory
+  HIP_TRY(hipStreamSynchronize(s));
+  return FST_OK;
 }
 
 const char *fst_strerror(int code) {

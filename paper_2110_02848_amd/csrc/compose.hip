@@ -1442,6 +1442,51 @@ __global__ __launch_bounds__(NT) void k_fill_heavy(Problem P, const uint32_t *__
   }
 }
 
+// ---------------------------------------------------------------------------
+// batches: the disjoint union of several A, and each item's range in C
+// ---------------------------------------------------------------------------
+
+// Item graph a at state offset vbase and arc offset ebase of the union:
+// offsets, sources and destinations shifted (labels, weights and flags are
+// copied as they are).
+__global__ __launch_bounds__(NT) void k_union_copy(DevGraph a, long long vbase, long long ebase,
+                                                   int32_t *__restrict__ off,
+                                                   int32_t *__restrict__ src,
+                                                   int32_t *__restrict__ dst) {
+  const long long n = (long long)a.V + 1 > (long long)a.E ? (long long)a.V + 1 : (long long)a.E;
+  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n;
+       i += (long long)gridDim.x * NT) {
+    if (i <= a.V) off[vbase + i] = (int32_t)(a.off[i] + ebase);
+    if (i < a.E) {
+      src[ebase + i] = (int32_t)(a.src[i] + vbase);
+      dst[ebase + i] = (int32_t)(a.dst[i] + vbase);
+    }
+  }
+}
+
+// out[i] = first state of item i in C (the number of trim keys below the
+// item's first key), out[n + 1 + i] = its first arc (the chunk's arc offset
+// plus the counts of the chunk's earlier states), for i <= n.
+__global__ __launch_bounds__(NT) void k_item_ranges(Problem P, ull nkeys, int32_t n,
+                                                    const long long *__restrict__ qa_base,
+                                                    const uint32_t *__restrict__ cnt,
+                                                    const uint32_t *__restrict__ btot, ull per,
+                                                    uint32_t nstates, uint32_t narcs,
+                                                    long long *__restrict__ out) {
+  for (int i = blockIdx.x * NT + threadIdx.x; i <= n; i += gridDim.x * NT) {
+    const ull K = (ull)qa_base[i] << (P.shiftB + 1);
+    const uint32_t st = K >= nkeys ? nstates : new_id(P, (uint32_t)K);
+    uint32_t a = narcs;
+    if (st < nstates) {
+      const ull c = st / per;
+      a = btot[c];
+      for (ull j = c * per; j < st; ++j) a += cnt[j];
+    }
+    out[i] = st;
+    out[n + 1 + i] = a;
+  }
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
@@ -1617,6 +1662,22 @@ hipError_t launch_fill(const Problem &P, const uint32_t *key_of, uint32_t nstate
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   return hipSuccess;
+}
+
+hipError_t launch_union_copy(const DevGraph &a, long long vbase, long long ebase, int32_t *off,
+                             int32_t *src, int32_t *dst, hipStream_t s) {
+  const size_t n = (size_t)(a.V + 1 > a.E ? a.V + 1 : a.E);
+  k_union_copy<<<grid_for(n), NT, 0, s>>>(a, vbase, ebase, off, src, dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_item_ranges(const Problem &P, unsigned long long nkeys, int32_t n,
+                              const long long *qa_base, const uint32_t *cnt,
+                              const uint32_t *btot, size_t per, uint32_t nstates,
+                              uint32_t narcs, long long *out, hipStream_t s) {
+  k_item_ranges<<<grid_for((size_t)n + 1), NT, 0, s>>>(P, nkeys, n, qa_base, cnt, btot, per,
+                                                      nstates, narcs, out);
+  return hipGetLastError();
 }
 
 }  // namespace fstc

@@ -430,6 +430,17 @@ hipError_t launch_fill(const Problem &P, const uint32_t *key_of, uint32_t nstate
                        const uint32_t *cnt, const uint32_t *btot, const uint32_t *heavy,
                        uint32_t nheavy, uint32_t narcs, const OutGraph &O, hipStream_t s);
 
+// Batches (compose.hip): copy item graph a into the union arrays at state
+// offset vbase and arc offset ebase (off, src, dst shifted); and, after a
+// run on the union, the first state and first arc of every item (out[i],
+// out[n + 1 + i] for i <= n; qa_base[i] = the item's first state of A).
+hipError_t launch_union_copy(const DevGraph &a, long long vbase, long long ebase, int32_t *off,
+                             int32_t *src, int32_t *dst, hipStream_t s);
+hipError_t launch_item_ranges(const Problem &P, unsigned long long nkeys, int32_t n,
+                              const long long *qa_base, const uint32_t *cnt,
+                              const uint32_t *btot, size_t per, uint32_t nstates,
+                              uint32_t narcs, long long *out, hipStream_t s);
+
 // Score launchers (score.hip).
 // In-arc structure of G: owner (V words, all -1) and extra (V words, all 0)
 // are scratch; inref (V), mbeg/mlen/mcur (V each), marc (E) and mpos (E;
@@ -448,6 +459,12 @@ hipError_t launch_score_generation(const ScoreArgs *F, const ScoreArgs *B, int g
 // zhi zeroed).
 hipError_t launch_score_total(const double *val, const uint8_t *flag, int32_t V,
                               ScoreScalars *sc, double *total, hipStream_t s);
+// totals[i] = log-add of val[v] over the flagged v in [bounds[i],
+// bounds[i + 1]) for i < n (bounds: n + 1 device words; max_len the longest
+// segment; z: 3 n words, zeroed by the caller).
+hipError_t launch_segment_logsum(const double *val, const uint8_t *flag, int32_t n,
+                                 const long long *bounds, long long max_len,
+                                 unsigned long long *z, double *totals, hipStream_t s);
 // grad[e] = scale * exp(alpha[src e] + w(e) + beta[dst e] - *total).
 hipError_t launch_posterior(const ScoreGraph &G, const double *alpha, const double *beta,
                             const double *total, float scale, float *grad, hipStream_t s);

@@ -700,6 +700,46 @@ __global__ void k_total_final(ScoreScalars *sc, double *total) {
   *total = acc_finish(from_order_key(sc->zmax), sc->zlo, sc->zhi);
 }
 
+// Segments (blockIdx.y = segment i, states [bounds[i], bounds[i + 1])):
+// the same exact log-add per segment; z holds 3 words per segment (order
+// key of the maximum, 128-bit sum).
+__global__ __launch_bounds__(NT) void k_seg_max(const double *val, const uint8_t *flag,
+                                                const long long *bounds, ull *z) {
+  const int i = blockIdx.y;
+  const long long lo = bounds[i], hi = bounds[i + 1];
+  double m = -INFINITY;
+  for (long long v = lo + (long long)blockIdx.x * NT + threadIdx.x; v < hi;
+       v += (long long)gridDim.x * NT)
+    if (flag[v]) m = fmax(m, val[v]);
+  m = block_fmax(m);
+  if (threadIdx.x == 0 && m != -INFINITY) atomicMax(z + 3 * i, order_key(m));
+}
+
+__global__ __launch_bounds__(NT) void k_seg_sum(const double *val, const uint8_t *flag,
+                                                const long long *bounds, ull *z) {
+  const int i = blockIdx.y;
+  if (z[3 * i] == 0) return;  // nothing flagged is finite
+  const double M = from_order_key(z[3 * i]);
+  if (M == INFINITY) return;
+  const long long lo = bounds[i], hi = bounds[i + 1];
+  ull slo = 0, shi = 0;
+  for (long long v = lo + (long long)blockIdx.x * NT + threadIdx.x; v < hi;
+       v += (long long)gridDim.x * NT)
+    if (flag[v]) acc_add(slo, shi, exp(val[v] - M));
+  block_sum128(slo, shi);
+  if (threadIdx.x == 0 && (slo | shi)) {
+    const ull old = atomicAdd(z + 3 * i + 1, slo);
+    const ull carry = old + slo < old ? 1ull : 0ull;
+    atomicAdd(z + 3 * i + 2, shi + carry);
+  }
+}
+
+__global__ __launch_bounds__(NT) void k_seg_final(int32_t n, const ull *z, double *totals) {
+  for (int i = blockIdx.x * NT + threadIdx.x; i < n; i += gridDim.x * NT)
+    totals[i] = z[3 * i] == 0 ? -INFINITY : acc_finish(from_order_key(z[3 * i]), z[3 * i + 1],
+                                                       z[3 * i + 2]);
+}
+
 // ---------------------------------------------------------------------------
 // posteriors and the provenance scatter
 // ---------------------------------------------------------------------------
@@ -959,6 +999,21 @@ hipError_t launch_score_total(const double *val, const uint8_t *flag, int32_t V,
   k_total_max<<<grid_for(V), NT, 0, s>>>(val, flag, V, sc);
   k_total_sum<<<grid_for(V), NT, 0, s>>>(val, flag, V, sc);
   k_total_final<<<1, 1, 0, s>>>(sc, total);
+  return hipGetLastError();
+}
+
+hipError_t launch_segment_logsum(const double *val, const uint8_t *flag, int32_t n,
+                                 const long long *bounds, long long max_len, ull *z,
+                                 double *totals, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (max_len > 0) {
+    long long bx = (max_len + NT - 1) / NT;
+    if (bx > 1024) bx = 1024;
+    const dim3 grid((unsigned)bx, (unsigned)n);
+    k_seg_max<<<grid, NT, 0, s>>>(val, flag, bounds, z);
+    k_seg_sum<<<grid, NT, 0, s>>>(val, flag, bounds, z);
+  }
+  k_seg_final<<<grid_for(n), NT, 0, s>>>(n, z, totals);
   return hipGetLastError();
 }
 

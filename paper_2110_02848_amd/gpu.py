@@ -117,6 +117,16 @@ def load():
                                      ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
                                      ctypes.c_void_p]
     lib.fst_grad_scatter.restype = ctypes.c_int
+    lib.fst_compose_batch_run.argtypes = [ctypes.c_void_p, ctypes.POINTER(_Graph), ctypes.c_int32,
+                                          ctypes.POINTER(_Graph), ctypes.c_void_p,
+                                          ctypes.POINTER(ctypes.c_int64),
+                                          ctypes.POINTER(ctypes.c_int64), ctypes.c_void_p,
+                                          ctypes.c_void_p]
+    lib.fst_compose_batch_run.restype = ctypes.c_int
+    lib.fst_segment_logsum.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                       ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                       ctypes.c_void_p]
+    lib.fst_segment_logsum.restype = ctypes.c_int
     lib.fst_strerror.argtypes = [ctypes.c_int]
     lib.fst_strerror.restype = ctypes.c_char_p
     _lib = lib
@@ -234,6 +244,44 @@ class Composer:
         nv, ne = self.run(A, B, stream)
         C = self.alloc_output(nv, ne, provenance, keys)
         return self.fill(C, stream)
+
+    def run_batch(self, As, B, stream=None):
+        """Phase 1 of C_i = A_i o B for every A_i of the list, in one pass.
+        Returns (V_C, E_C, item_states, item_arcs): the sizes of the one C
+        (the union of the C_i) and the numpy int64 [n + 1] ranges of each
+        item's states and arcs in it."""
+        n = len(As)
+        arr = (_Graph * max(n, 1))()
+        for i, A in enumerate(As):
+            arr[i] = _graph_struct(A)
+        gb = _graph_struct(B)
+        nv, ne = ctypes.c_int64(), ctypes.c_int64()
+        st = np.zeros(n + 1, np.int64)
+        ar = np.zeros(n + 1, np.int64)
+        rc = self._lib.fst_compose_batch_run(self._h, arr, n, ctypes.byref(gb),
+                                             _stream_handle(stream), ctypes.byref(nv),
+                                             ctypes.byref(ne), st.ctypes.data, ar.ctypes.data)
+        _check(rc, "fst_compose_batch_run")
+        return int(nv.value), int(ne.value), st, ar
+
+    def compose_batch(self, As, B, provenance=True, keys=True, stream=None):
+        """C = union of A_i o B as one dict of device tensors (ids of the
+        union), with the per-item ranges: (C, item_states, item_arcs)."""
+        nv, ne, st, ar = self.run_batch(As, B, stream)
+        C = self.alloc_output(nv, ne, provenance, keys)
+        return self.fill(C, stream), st, ar
+
+    def segment_logsum(self, val, flag, bounds, stream=None):
+        """totals[i] = log-sum of exp(val[v]) over flagged v in
+        [bounds[i], bounds[i + 1]) (float64 [n] tensor)."""
+        import torch
+        b = np.ascontiguousarray(bounds, dtype=np.int64)
+        n = len(b) - 1
+        out = torch.empty(max(n, 0), dtype=torch.float64, device=f"cuda:{self.device}")
+        rc = self._lib.fst_segment_logsum(self._h, _ptr(val), _ptr(flag), n, b.ctypes.data,
+                                          _ptr(out), _stream_handle(stream))
+        _check(rc, "fst_segment_logsum")
+        return out
 
     def stats(self):
         st = _Stats()

@@ -298,6 +298,24 @@ def emissions_lexicon(name, seed=0, spec=None):
     return A, B, dict(table=table, spellings=spell, spec=spec)
 
 
+def lexicon_batch(name, n, seed=0, spec=None, frames=None):
+    """A batch of emission graphs with one lexicon: item i is the emissions
+    of ``emissions_lexicon(name, seed + i)`` (T frames, or ``frames[i]``),
+    and B is the lexicon of ``emissions_lexicon(name, seed)``.  Returns
+    (list of A_i, B, meta with the per-item tables and the spellings)."""
+    spec = spec or LEX_SPECS[name]
+    As, tables = [], []
+    for i in range(int(n)):
+        ra, _ = _rngs(name, seed + i)
+        T = spec.T if frames is None else int(frames[i])
+        A, table = emissions(ra, T, spec.C)
+        As.append(A)
+        tables.append(table)
+    _, rb = _rngs(name, seed)
+    B, spell = lexicon(rb, spec.W, spec.C, spec.len_lo, spec.len_hi)
+    return As, B, dict(tables=tables, spellings=spell, spec=spec)
+
+
 def workload(name, seed=0):
     """Inputs ``(A, B)`` of a named workload for a given seed."""
     if name in RANDOM_SPECS:
