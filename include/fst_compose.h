@@ -141,12 +141,19 @@ FST_API void fst_ctx_destroy(fst_ctx *ctx);
  * predecessor moves of all co-accessible keys (extra passes, reported in
  * fst_stats.generated and fst_stats.generated_backward).
  * FST_OPT_ORDER picks the order of the two searches (the result is the same):
- * FST_ORDER_FORWARD_FIRST (default) searches forward from the start keys,
+ * FST_ORDER_FORWARD_FIRST searches forward from the start keys,
  * then backward from the accepting keys it reached, inside the accessible
  * set; FST_ORDER_COACCESSIBLE_FIRST is Algorithm 1's order: the co-accessible
  * set over all key pairs first (backward from every accepting pair), then the
  * forward search inside it (fst_stats.accessible then counts only keys that
- * are also co-accessible). */
+ * are also co-accessible); FST_ORDER_CONCURRENT (default) runs the forward
+ * search's first generations alone, then, unless it has ended (then it goes
+ * on as forward-first), a backward search from every accepting pair beside
+ * the rest of it in the same kernels, restricted to accessible keys once
+ * the forward search has ended and held back while its frontier is far
+ * wider than the forward one (kernel FST_KERNEL_SEARCH_FORWARD then times
+ * the launches that advance either search, and FST_KERNEL_SEARCH_BACKWARD
+ * has none). */
 enum fst_option {
   FST_OPT_MAX_WORKSPACE = 1,
   FST_OPT_TIMING = 2,
@@ -155,7 +162,11 @@ enum fst_option {
   FST_OPT_COUNT_MOVES = 5,
   FST_OPT_ORDER = 6
 };
-enum fst_order { FST_ORDER_FORWARD_FIRST = 0, FST_ORDER_COACCESSIBLE_FIRST = 1 };
+enum fst_order {
+  FST_ORDER_FORWARD_FIRST = 0,
+  FST_ORDER_COACCESSIBLE_FIRST = 1,
+  FST_ORDER_CONCURRENT = 2
+};
 FST_API int fst_ctx_set_option(fst_ctx *ctx, int option, int64_t value);
 
 /* Phase 1 (Algorithm 1 up to the size of C): validate A and B, search the

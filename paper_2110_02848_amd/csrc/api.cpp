@@ -50,7 +50,7 @@ struct fst_ctx {
   bool timing = false;
   bool buckets = true;
   bool count_moves = false;
-  int order = FST_ORDER_FORWARD_FIRST;
+  int order = FST_ORDER_CONCURRENT;
   int chain_depth = CHAIN_MAX;
   bool have_times = false;
   bool timed_run = false;
@@ -60,7 +60,7 @@ struct fst_ctx {
   DevBuf aOutPerm, aOutArc, aOutRec, aOutLut, bOutPerm, bOutArc, bOutRec, bOutLut;
   DevBuf aOutLab, aOutW, bOutLab, bOutW, bOutChain, bInChain;
   DevBuf aInOff, aInPerm, aInArc, aInRec, aInLut, bInOff, bInPerm, bInArc, bInRec, bInLut;
-  DevBuf vis, coacc, wbase, fq, bq, heavy, hoff, cnt, btot;
+  DevBuf vis, coacc, wbase, fq, bq, heavy, hoff, heavy2, hoff2, cnt, btot;
   // score workspace
   DevBuf s_sc, s_owner, s_extra, s_inref, s_mbeg, s_mlen, s_mcur, s_marc, s_val, s_acc,
       s_mpos;
@@ -415,6 +415,44 @@ ScoreGraph plain_score_graph(const DevGraph &d) {
   return SG;
 }
 
+// The forward search (generations from g0 on) and an unrestricted backward
+// search (from every accepting key pair, seeded by the caller) side by side,
+// both advanced by the same kernels; once the forward search has ended, the
+// remaining backward generations expand only accessible keys and run alone.
+// The trim set is the keys both reached.
+int search_concurrent(fst_ctx *c, Problem P, const SearchArgs &SF, const SearchArgs &SB, int g0,
+                      hipStream_t s) {
+  const KernelTimer t = timer(c, FST_KERNEL_SEARCH_FORWARD);
+  int gf = g0, gb = 0, batch = 16;  // each search numbers its own generations
+  bool fdone = false, bdone = false, pause = false;
+  for (;;) {
+    t.begin(s);
+    for (int b = 0; b < batch; ++b) {
+      if (!fdone && !bdone && !pause) HIP_TRY(launch_generation2(P, SF, SB, gf++, gb++, s));
+      else if (!fdone) HIP_TRY(launch_generation(P, SF, true, gf++, s));
+      else HIP_TRY(launch_generation(P, SB, false, gb++, s));
+    }
+    t.end(s);
+    FST_TRY(readback(c, s));
+    FST_TRY(add_time(c, FST_KERNEL_SEARCH_FORWARD, batch));
+    if (c->h_sc->overflow) return FST_ERR_TOO_LARGE;
+    const GenSlot &nf = c->h_sc->G[gf % 3], &nb = c->h_sc->G2[gb % 3];
+    fdone = fdone || (nf.qcount == 0 && (uint32_t)nf.hpack == 0);
+    bdone = bdone || (nb.qcount == 0 && (uint32_t)nb.hpack == 0);
+    if (fdone) P.restrict_bwd = 1;  // the accessible set is complete
+    // an unrestricted backward frontier far wider than the forward one is
+    // mostly keys that are not accessible: the backward search waits (its
+    // frontier stays in its slot) until the forward search has ended
+    const unsigned long long wf = nf.qcount + (nf.hpack >> 32), wb = nb.qcount + (nb.hpack >> 32);
+    pause = pause || (!fdone && wb > 4 * wf + 65536);
+    if (fdone && bdone) break;
+    batch = batch < 64 ? 2 * batch : 64;
+  }
+  c->stats.fwd_levels = c->h_sc->gens;
+  c->stats.bwd_levels = c->h_sc->gens2;
+  return FST_OK;
+}
+
 // Label buckets are kept when the table is at most this large; so are the
 // chain records of each view of B.
 constexpr size_t LUT_BUDGET = (size_t)256 << 20;
@@ -546,6 +584,10 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   FST_TRY(ensure(c, c->bq, (size_t)cap * 4));
   FST_TRY(ensure(c, c->heavy, (size_t)cap * 4));
   FST_TRY(ensure(c, c->hoff, (size_t)cap * 4));
+  if (c->order == FST_ORDER_CONCURRENT) {
+    FST_TRY(ensure(c, c->heavy2, (size_t)cap * 4));
+    FST_TRY(ensure(c, c->hoff2, (size_t)cap * 4));
+  }
   FST_TRY(ensure(c, c->lists, ((size_t)VA + VB + 2) * 4));
   size_t scan_n = nwords > (size_t)cap + 1 ? nwords : (size_t)cap + 1;
   FST_TRY(ensure(c, c->scan_tmp, scan_temp_bytes(scan_n)));
@@ -562,6 +604,7 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   P.bIn = views[3];
   P.shiftB = shiftB;
   P.chain_max = c->chain_depth;
+  P.mark_accept = 1;
   P.vis = as<uint32_t>(c->vis);
   P.coacc = as<uint32_t>(c->coacc);
   P.wbase = as<uint32_t>(c->wbase);
@@ -577,9 +620,64 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   S.acc = bq;
   S.cap = cap;
   S.sc = d_sc;
+  S.G = d_sc->G;
+  S.gens = &d_sc->gens;
   uint32_t *wbase = as<uint32_t>(c->wbase);
   phase_end(c, PH_PRE, s);
-  if (c->order == FST_ORDER_COACCESSIBLE_FIRST) {
+  if (c->order == FST_ORDER_CONCURRENT) {
+    // The forward search's first generations run alone (listing accepting
+    // keys as in the forward-first order).  If it has ended by then, the
+    // backward search follows as in that order; otherwise a backward search
+    // from every accepting pair runs beside the rest of it.
+    constexpr int FIRST = 4;
+    P.restrict_fwd = 0;
+    P.restrict_bwd = 0;
+    phase_begin(c, PH_FWD, s);
+    HIP_TRY(hipMemsetAsync(cnts, 0, 8, s));
+    HIP_TRY(hipMemsetAsync(d_sc->G, 0, sizeof(d_sc->G), s));
+    HIP_TRY(hipMemsetAsync(d_sc->G2, 0, sizeof(d_sc->G2), s));
+    HIP_TRY(launch_seed_forward(P, S, la, cnts, lb, cnts + 1, s));
+    const KernelTimer tf = timer(c, FST_KERNEL_SEARCH_FORWARD);
+    tf.begin(s);
+    for (int g = 0; g < FIRST; ++g) HIP_TRY(launch_generation(P, S, true, g, s));
+    tf.end(s);
+    FST_TRY(readback(c, s));
+    FST_TRY(add_time(c, FST_KERNEL_SEARCH_FORWARD, FIRST));
+    if (c->h_sc->overflow) return FST_ERR_TOO_LARGE;
+    const GenSlot &nf = c->h_sc->G[FIRST % 3];
+    if (nf.qcount == 0 && (uint32_t)nf.hpack == 0) {
+      c->stats.fwd_levels = c->h_sc->gens;
+      HIP_TRY(launch_popcount(P.vis, nwords, &d_sc->naccessible, s));
+      if (c->count_moves) HIP_TRY(launch_count_moves(P, nwords, true, &d_sc->generated, s));
+      phase_end(c, PH_FWD, s);
+      phase_begin(c, PH_BWD, s);
+      P.restrict_bwd = 1;
+      HIP_TRY(hipMemsetAsync(d_sc->G, 0, sizeof(d_sc->G), s));
+      HIP_TRY(launch_seed_backward(P, S, bq, s));
+      FST_TRY(search(c, S, false, &c->stats.bwd_levels, s));
+      HIP_TRY(launch_trim_words(P.coacc, P.vis, wbase, nwords, s));
+      phase_end(c, PH_BWD, s);
+    } else {
+      P.mark_accept = 0;  // the backward seeds below are every accepting pair
+      SearchArgs SB = S;
+      SB.Q = bq;  // the forward search's list of accepting keys is not needed
+      SB.heavy = as<uint32_t>(c->heavy2);
+      SB.hoff = as<uint32_t>(c->hoff2);
+      SB.acc = nullptr;
+      SB.G = d_sc->G2;
+      SB.gens = &d_sc->gens2;
+      HIP_TRY(hipMemsetAsync(cnts, 0, 8, s));
+      HIP_TRY(launch_seed_backward_all(P, SB, la, cnts, lb, cnts + 1, s));
+      FST_TRY(search_concurrent(c, P, S, SB, FIRST, s));
+      HIP_TRY(launch_popcount(P.vis, nwords, &d_sc->naccessible, s));
+      if (c->count_moves) HIP_TRY(launch_count_moves(P, nwords, true, &d_sc->generated, s));
+      phase_end(c, PH_FWD, s);
+      // the backward phase is the final intersection only
+      phase_begin(c, PH_BWD, s);
+      HIP_TRY(launch_trim_words(P.coacc, P.vis, wbase, nwords, s));
+      phase_end(c, PH_BWD, s);
+    }
+  } else if (c->order == FST_ORDER_COACCESSIBLE_FIRST) {
     // Algorithm 1's order: the co-accessible set over all key pairs first,
     // from every accepting pair, then the forward search inside it
     P.restrict_fwd = 1;
@@ -832,7 +930,8 @@ void fst_ctx_destroy(fst_ctx *c) {
                     &c->aOutRec,  &c->aOutLut,  &c->bOutPerm, &c->bOutArc, &c->bOutRec,
                     &c->bOutLut,  &c->aInOff,   &c->aInPerm, &c->aInArc,  &c->aInRec,
                     &c->aInLut,   &c->bInOff,   &c->bInPerm, &c->bInArc,  &c->bInRec,
-                    &c->bInLut,   &c->vis,      &c->coacc,   &c->wbase,   &c->fq,
+                    &c->bInLut,   &c->vis,      &c->coacc,   &c->wbase,   &c->heavy2,
+                    &c->hoff2,    &c->fq,
                     &c->bq,       &c->heavy,    &c->hoff,    &c->cnt,     &c->aOutLab,
                     &c->aOutW,    &c->bOutLab,  &c->bOutW,   &c->btot,    &c->bOutChain,
                     &c->bInChain, &c->s_sc,     &c->s_owner, &c->s_extra, &c->s_inref,
@@ -874,7 +973,8 @@ int fst_ctx_set_option(fst_ctx *c, int option, int64_t value) {
       c->count_moves = value != 0;
       return FST_OK;
     case FST_OPT_ORDER:
-      if (value != FST_ORDER_FORWARD_FIRST && value != FST_ORDER_COACCESSIBLE_FIRST)
+      if (value != FST_ORDER_FORWARD_FIRST && value != FST_ORDER_COACCESSIBLE_FIRST &&
+          value != FST_ORDER_CONCURRENT)
         return FST_ERR_INVALID_ARG;
       c->order = (int)value;
       return FST_OK;

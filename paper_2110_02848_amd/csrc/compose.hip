@@ -753,7 +753,7 @@ __device__ __forceinline__ void place(const Problem &P, const SearchArgs &S, con
   if (fresh) {
     const uint32_t u = Dir<FWD>::units(vi);
     if constexpr (FWD) {
-      seed = vi.accept != 0;
+      seed = P.mark_accept && vi.accept != 0;
       if (seed) atomicOr(P.coacc + (v >> 5), 1u << (v & 31u));
     }
     if (u > LIGHT_SEARCH) {
@@ -895,29 +895,30 @@ __device__ __forceinline__ bool chain_jump(const Problem &P, const SearchArgs &S
 // then, depth-first, the light keys it reached first (one loop, so the visit
 // code exists once).  New work goes to the slot of generation g + 1.
 template <bool FWD>
-__global__ __launch_bounds__(NT) void k_gen(Problem P, SearchArgs S, int g) {
+__device__ __forceinline__ void gen_body(const Problem &P, const SearchArgs &S, int g,
+                                         unsigned bid, unsigned nb) {
   typedef typename Dir<FWD>::Info Info;
   Scalars *sc = S.sc;
   if (sc->overflow) return;
-  const GenSlot cur = sc->G[g % 3];
+  const GenSlot cur = S.G[g % 3];
   const uint32_t hcount = (uint32_t)(cur.hpack & 0xffffffffull);
   const ull U = cur.hpack >> 32;
   NextGen nx;
-  nx.slot = &sc->G[(g + 1) % 3];
+  nx.slot = &S.G[(g + 1) % 3];
   nx.qbase = cur.qbase + cur.qcount;
   nx.hbase = cur.hbase + hcount;
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
+  if (bid == 0 && threadIdx.x == 0) {
     nx.slot->qbase = nx.qbase;  // read by generation g + 1 only
     nx.slot->hbase = nx.hbase;
-    GenSlot *done = &sc->G[(g + 2) % 3];  // generation g - 1: free
+    GenSlot *done = &S.G[(g + 2) % 3];  // generation g - 1: free
     done->qcount = 0;
     done->hpack = 0;
-    if (U + cur.qcount) sc->gens = (uint32_t)g + 1;
+    if (U + cur.qcount) *S.gens = (uint32_t)g + 1;
   }
   const uint32_t *hk = S.heavy + cur.hbase;
   const uint32_t *ho = S.hoff + cur.hbase;
   const ull n = U + cur.qcount;
-  for (ull i = (ull)blockIdx.x * NT + threadIdx.x; i < n; i += (ull)gridDim.x * NT) {
+  for (ull i = (ull)bid * NT + threadIdx.x; i < n; i += (ull)nb * NT) {
     uint32_t key, u0 = 0, u1 = 0;
     bool one_unit = false;
     if (i < U) {
@@ -951,6 +952,20 @@ __global__ __launch_bounds__(NT) void k_gen(Problem P, SearchArgs S, int g) {
   }
 }
 
+template <bool FWD>
+__global__ __launch_bounds__(NT) void k_gen(Problem P, SearchArgs S, int g) {
+  gen_body<FWD>(P, S, g, blockIdx.x, gridDim.x);
+}
+
+// A forward and a backward search side by side: the first half of the
+// workgroups advances the forward search, the second half the backward.
+__global__ __launch_bounds__(NT) void k_gen2(Problem P, SearchArgs SF, SearchArgs SB, int gf,
+                                             int gb) {
+  const unsigned half = gridDim.x / 2;
+  if (blockIdx.x < half) gen_body<true>(P, SF, gf, blockIdx.x, half);
+  else gen_body<false>(P, SB, gb, blockIdx.x - half, half);
+}
+
 __global__ __launch_bounds__(NT) void k_collect(const uint8_t *__restrict__ flags, int V,
                                                 int32_t *__restrict__ list,
                                                 uint32_t *__restrict__ count) {
@@ -975,7 +990,7 @@ __global__ __launch_bounds__(NT) void k_seed_forward(Problem P, SearchArgs S,
                                                      const int32_t *__restrict__ lb,
                                                      const uint32_t *__restrict__ nb_p) {
   const ull na = *na_p, nb = *nb_p, n = na * nb;
-  const NextGen nx{&S.sc->G[0], 0u, 0u};
+  const NextGen nx{&S.G[0], 0u, 0u};
   for (ull i0 = (ull)blockIdx.x * NT; i0 < n; i0 += (ull)gridDim.x * NT) {
     const ull i = i0 + threadIdx.x;
     uint32_t k = 0;
@@ -1001,7 +1016,7 @@ __global__ __launch_bounds__(NT) void k_seed_backward_all(Problem P, SearchArgs 
                                                           const int32_t *__restrict__ lb,
                                                           const uint32_t *__restrict__ nb_p) {
   const ull na = *na_p, nb = *nb_p, n = 2 * na * nb;
-  const NextGen nx{&S.sc->G[0], 0u, 0u};
+  const NextGen nx{&S.G[0], 0u, 0u};
   for (ull i0 = (ull)blockIdx.x * NT; i0 < n; i0 += (ull)gridDim.x * NT) {
     const ull i = i0 + threadIdx.x;
     uint32_t k = 0;
@@ -1012,7 +1027,10 @@ __global__ __launch_bounds__(NT) void k_seed_backward_all(Problem P, SearchArgs 
       const uint32_t qa = (uint32_t)la[pair / nb], f = (uint32_t)(i & 1);
       const bool eps = (P.aOut.srec[2 * (size_t)qa].w & (int32_t)FLAG_EPS_OUT) != 0;
       k = make_key(qa, (uint32_t)lb[pair % nb], f, P.shiftB);
-      fresh = (f == 0 || eps) && claim(P.coacc, k);
+      // every pair is enumerated once, so it is placed once; a forward
+      // search running first may already have marked it co-accessible
+      fresh = f == 0 || eps;
+      if (fresh) set_bit(P.coacc, k);
       ki = bwd_info(P, k);
     }
     Next<false> nk;
@@ -1026,7 +1044,7 @@ __global__ __launch_bounds__(NT) void k_seed_backward_all(Problem P, SearchArgs 
 __global__ __launch_bounds__(NT) void k_seed_backward(Problem P, SearchArgs S,
                                                       const uint32_t *__restrict__ list) {
   const uint32_t n = S.sc->tail2;
-  const NextGen nx{&S.sc->G[0], 0u, 0u};
+  const NextGen nx{&S.G[0], 0u, 0u};
   for (ull i0 = (ull)blockIdx.x * NT; i0 < n; i0 += (ull)gridDim.x * NT) {
     const ull i = i0 + threadIdx.x;
     const bool valid = i < n;
@@ -1599,6 +1617,13 @@ hipError_t launch_generation(const Problem &P, const SearchArgs &S, bool forward
   constexpr unsigned GRID = 1024;
   if (forward) k_gen<true><<<GRID, NT, 0, s>>>(P, S, g);
   else k_gen<false><<<GRID, NT, 0, s>>>(P, S, g);
+  return hipGetLastError();
+}
+
+hipError_t launch_generation2(const Problem &P, const SearchArgs &SF, const SearchArgs &SB, int gf,
+                              int gb, hipStream_t s) {
+  constexpr unsigned GRID = 1024;
+  k_gen2<<<2 * GRID, NT, 0, s>>>(P, SF, SB, gf, gb);
   return hipGetLastError();
 }
 

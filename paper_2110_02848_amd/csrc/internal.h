@@ -116,6 +116,8 @@ struct Problem {
   int chain_max;          // keys one search thread may follow depth-first
   int restrict_fwd;       // forward search expands only keys already in coacc
   int restrict_bwd;       // backward search expands only keys already in vis
+  int mark_accept;        // forward search marks accepting keys co-accessible
+                          // and lists them as backward seeds
   uint32_t *vis;          // accessible-key bitmap
   uint32_t *coacc;        // trim-key bitmap (accessible and co-accessible)
   const uint32_t *wbase;  // exclusive popcount prefix of coacc words
@@ -155,7 +157,9 @@ struct Scalars {
   unsigned long long generated_bwd; // predecessor moves of co-accessible keys (on request)
   unsigned long long naccessible; // keys reached by the forward search
   unsigned long long total;     // scan totals
-  GenSlot G[3];
+  GenSlot G[3];                 // generation slots of a search
+  GenSlot G2[3];                // of the backward search running beside it
+  uint32_t gens2, pad1;         // its generations that had work
 };
 
 // Arrays of one search (each holds up to `cap` keys).
@@ -166,6 +170,8 @@ struct SearchArgs {
   uint32_t *acc;    // forward search: accepting keys, the backward seeds
   uint32_t cap;
   Scalars *sc;
+  GenSlot *G;       // this search's three generation slots
+  uint32_t *gens;   // this search's count of generations that had work
 };
 
 // ---------------------------------------------------------------------------
@@ -402,6 +408,11 @@ hipError_t launch_seed_backward(const Problem &P, const SearchArgs &S, const uin
 // Generation g of the forward (or backward) search: one kernel.
 hipError_t launch_generation(const Problem &P, const SearchArgs &S, bool forward, int g,
                              hipStream_t s);
+// Generation gf of a forward search (SF) and generation gb of a backward
+// search (SB) running side by side in one kernel (half of the workgroups
+// each).
+hipError_t launch_generation2(const Problem &P, const SearchArgs &SF, const SearchArgs &SB, int gf,
+                              int gb, hipStream_t s);
 // *out += number of moves the forward search examines out of the keys set in
 // P.vis, or (backward) the backward search examines into the keys set in
 // P.coacc (a statistic).

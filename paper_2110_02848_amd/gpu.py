@@ -34,6 +34,7 @@ FST_OPT_ORDER = 6
 
 FST_ORDER_FORWARD_FIRST = 0
 FST_ORDER_COACCESSIBLE_FIRST = 1
+FST_ORDER_CONCURRENT = 2
 
 PHASES = ("preprocess", "forward", "backward", "count", "fill")
 

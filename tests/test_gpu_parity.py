@@ -230,6 +230,77 @@ def test_coaccessible_first_order_small(comp_paper_order, seed):
     assert not fsthelp.check_invariants(A, B, got)
 
 
+@pytest.fixture(scope="module")
+def comp_concurrent():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2110_02848_amd import gpu
+    c = gpu.Composer(0)
+    c.set_option(gpu.FST_OPT_ORDER, gpu.FST_ORDER_CONCURRENT)
+    yield c
+    c.close()
+
+
+@pytest.fixture(scope="module")
+def comp_forward_first():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2110_02848_amd import gpu
+    c = gpu.Composer(0)
+    c.set_option(gpu.FST_OPT_ORDER, gpu.FST_ORDER_FORWARD_FIRST)
+    yield c
+    c.close()
+
+
+@pytest.mark.parametrize("name,seed", _paper_order_cases() + [("lexicon-T100-W1000", 2)])
+def test_forward_first_order(comp_forward_first, name, seed):
+    A, B = synth.workload(name, seed)
+    got, _ = check_pair(comp_forward_first, A, B, f"forward first {name} seed {seed}")
+    if seed < 3:
+        assert not fsthelp.check_invariants(A, B, got)
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_forward_first_order_small(comp_forward_first, seed):
+    rng = np.random.default_rng([987, seed])
+    A = synth.tiny_random(rng, int(rng.integers(1, 6)), 3, 3, 0.4)
+    B = synth.tiny_random(rng, int(rng.integers(1, 6)), 3, 3, 0.4)
+    got, _ = check_pair(comp_forward_first, A, B, f"forward first small seed {seed}")
+    assert not fsthelp.check_invariants(A, B, got)
+
+
+@pytest.mark.parametrize("name,seed", _paper_order_cases() + [("lexicon-T100-W1000", 2)])
+def test_concurrent_order(comp_concurrent, name, seed):
+    A, B = synth.workload(name, seed)
+    got, _ = check_pair(comp_concurrent, A, B, f"concurrent {name} seed {seed}")
+    if seed < 3:
+        assert not fsthelp.check_invariants(A, B, got)
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_concurrent_order_small(comp_concurrent, seed):
+    rng = np.random.default_rng([321, seed])
+    if seed % 2:
+        A = _sparse_chain_graph(rng, int(rng.integers(3, 40)), 1 + (seed % 4 == 3), 0.2, 0.1)
+        B = _sparse_chain_graph(rng, int(rng.integers(3, 40)), 1 + (seed % 4 == 3), 0.1, 0.1)
+    else:
+        A = synth.tiny_random(rng, int(rng.integers(1, 6)), 3, 3, 0.4)
+        B = synth.tiny_random(rng, int(rng.integers(1, 6)), 3, 3, 0.4)
+    got, _ = check_pair(comp_concurrent, A, B, f"concurrent small seed {seed}")
+    assert not fsthelp.check_invariants(A, B, got)
+
+
+def test_concurrent_order_hubs_and_full_lexicon(comp_concurrent):
+    A, B = _hub_pair()
+    check_pair(comp_concurrent, A, B, "concurrent hub states")
+    A, B, meta = synth.emissions_lexicon("lexicon-T500-W10000", 0)
+    C = gpu_compose(comp_concurrent, A, B)
+    V, E = fsthelp.lexicon_closed_form(meta["spec"].T, meta["spellings"])
+    assert (C["num_states"], C["num_arcs"]) == (V, E)
+    st = comp_concurrent.stats()
+    assert st["fwd_levels"] > 0 and st["bwd_levels"] > 0
+
+
 def test_heavy_states(comp):
     A, B = _hub_pair()
     got, _ = check_pair(comp, A, B, "hub states")
