@@ -959,7 +959,9 @@ __global__ __launch_bounds__(NT) void k_gen(Problem P, SearchArgs S, int g) {
 
 // A forward and a backward search side by side: the first half of the
 // workgroups advances the forward search, the second half the backward.
-__global__ __launch_bounds__(NT) void k_gen2(Problem P, SearchArgs SF, SearchArgs SB, int gf,
+// Held to 128 VGPRs (four wavefronts per SIMD; one more register would
+// leave three, and the kernel is bound by the latency of its loads).
+__global__ __launch_bounds__(NT, 4) void k_gen2(Problem P, SearchArgs SF, SearchArgs SB, int gf,
                                              int gb) {
   const unsigned half = gridDim.x / 2;
   if (blockIdx.x < half) gen_body<true>(P, SF, gf, blockIdx.x, half);
