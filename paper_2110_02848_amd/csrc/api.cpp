@@ -446,7 +446,8 @@ int search_concurrent(fst_ctx *c, Problem P, const SearchArgs &SF, const SearchA
     const unsigned long long wf = nf.qcount + (nf.hpack >> 32), wb = nb.qcount + (nb.hpack >> 32);
     pause = pause || (!fdone && wb > 4 * wf + 65536);
     if (fdone && bdone) break;
-    batch = batch < 64 ? 2 * batch : 64;
+    // (no growth: a read-back every 16 generations costs less than the
+    // empty launches a larger batch leaves after the searches end)
   }
   c->stats.fwd_levels = c->h_sc->gens;
   c->stats.bwd_levels = c->h_sc->gens2;
