@@ -629,34 +629,71 @@ __global__ __launch_bounds__(NT) void k_merge_index(ScoreGraph G, const int32_t 
   }
 }
 
+// In-arc lists of the merges, in any order.  Each workgroup takes chunks of
+// MP_ITEMS * NT arcs and counts, in an LDS hash table, how many of them go
+// into each merge; one global atomic per (chunk, merge) then reserves their
+// positions (the in-arcs of a merge in a composed speech graph come from
+// runs of neighbouring arcs, so a chunk meets few merges).  Arcs whose merge
+// finds no table slot take their position with their own atomic.
+constexpr int MP_ITEMS = 16;
+constexpr int MP_TABLE = 512;
+
+__device__ __forceinline__ int mp_slot(int32_t *keys, int32_t m, bool insert) {
+  int h = (int)(((uint32_t)m * 2654435761u) >> 23) & (MP_TABLE - 1);
+  for (int probe = 0; probe < 32; ++probe) {
+    const int32_t k = insert ? atomicCAS(keys + h, -1, m) : keys[h];
+    if (k == m || (insert && k == -1)) return h;
+    if (!insert && k == -1) return -1;
+    h = (h + 1) & (MP_TABLE - 1);
+  }
+  return -1;
+}
+
 __global__ __launch_bounds__(NT) void k_merge_place(ScoreGraph G, const int32_t *inref,
                                                     int32_t *mcur, int32_t *marc,
                                                     int32_t *mpos) {
-  const long long stride = (long long)gridDim.x * NT;
-  for (long long base = (long long)blockIdx.x * NT; base < G.E; base += stride) {
-    const long long e = base + threadIdx.x;
-    int32_t mi = -1;
-    if (e < G.E) {
-      const int32_t r = inref[G.dst[e]];
-      if (r <= -2) mi = -2 - r;
+  __shared__ int32_t s_key[MP_TABLE], s_cnt[MP_TABLE], s_base[MP_TABLE];
+  const long long chunk = (long long)MP_ITEMS * NT;
+  for (long long base = (long long)blockIdx.x * chunk; base < G.E;
+       base += (long long)gridDim.x * chunk) {
+    for (int i = threadIdx.x; i < MP_TABLE; i += NT) {
+      s_key[i] = -1;
+      s_cnt[i] = 0;
     }
-    // the lanes that place into the same merge take consecutive positions
-    // from one atomic; one round per distinct merge in the wavefront
-    ull rem = __ballot(mi >= 0);
-    int32_t pos = -1;
-    while (rem) {
-      const int leader = __ffsll((long long)rem) - 1;
-      const ull gm = __ballot(mi >= 0 && mi == __shfl(mi, leader));
-      int32_t b = 0;
-      if ((int)__lane_id() == leader) b = atomicAdd(mcur + mi, (int32_t)__popcll(gm));
-      b = __shfl(b, leader);
-      if ((gm >> __lane_id()) & 1ull) pos = b + (int32_t)__popcll(gm & __lanemask_lt());
-      rem &= ~gm;
+    __syncthreads();
+    int32_t mi[MP_ITEMS];
+    int slot[MP_ITEMS];
+#pragma unroll
+    for (int j = 0; j < MP_ITEMS; ++j) {
+      const long long e = base + (long long)j * NT + threadIdx.x;
+      mi[j] = -1;
+      slot[j] = -1;
+      if (e < G.E) {
+        const int32_t r = inref[G.dst[e]];
+        if (r <= -2) mi[j] = -2 - r;
+      }
+      if (mi[j] >= 0) {
+        slot[j] = mp_slot(s_key, mi[j], true);
+        if (slot[j] >= 0) atomicAdd(s_cnt + slot[j], 1);
+      }
     }
-    if (pos >= 0) {
+    __syncthreads();
+    for (int i = threadIdx.x; i < MP_TABLE; i += NT)
+      if (s_key[i] >= 0) {
+        s_base[i] = atomicAdd(mcur + s_key[i], s_cnt[i]);
+        s_cnt[i] = 0;  // now the cursor inside the reservation
+      }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < MP_ITEMS; ++j) {
+      if (mi[j] < 0) continue;
+      const long long e = base + (long long)j * NT + threadIdx.x;
+      const int32_t pos = slot[j] >= 0 ? s_base[slot[j]] + atomicAdd(s_cnt + slot[j], 1)
+                                       : atomicAdd(mcur + mi[j], 1);
       marc[pos] = (int32_t)e;
       mpos[e] = pos;
     }
+    __syncthreads();
   }
 }
 
@@ -773,7 +810,14 @@ __global__ __launch_bounds__(NT) void k_absmax(const float *g, long long n, uint
     m = max(m, __float_as_uint(g[e]) & 0x7fffffffu);
 #pragma unroll
   for (int o = WAVE / 2; o > 0; o >>= 1) m = max(m, (uint32_t)__shfl_xor(m, o));
-  if (__lane_id() == 0 && m) atomicMax(mx, m);
+  // one atomic per workgroup (same-address atomics serialize)
+  __shared__ uint32_t s_m[NWAVES];
+  if (__lane_id() == 0) s_m[threadIdx.x / WAVE] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < NWAVES; ++w) m = max(m, s_m[w]);
+    if (m) atomicMax(mx, m);
+  }
 }
 
 // Scale exponent: every |g| < 2^ex, so |g| * 2^(64 - ex) < 2^64.
@@ -969,7 +1013,11 @@ hipError_t launch_score_structure(const ScoreGraph &G, int32_t *owner, int32_t *
     k_extra<<<grid_for(G.E), NT, 0, s>>>(G, owner, extra);
   }
   k_merge_index<<<grid_for(G.V), NT, 0, s>>>(G, owner, extra, inref, mbeg, mlen, mcur, sc);
-  if (G.E > 0) k_merge_place<<<grid_for(G.E), NT, 0, s>>>(G, inref, mcur, marc, mpos);
+  if (G.E > 0) {
+    const long long chunks = (G.E + (long long)MP_ITEMS * NT - 1) / ((long long)MP_ITEMS * NT);
+    k_merge_place<<<(unsigned)(chunks < 4096 ? chunks : 4096), NT, 0, s>>>(G, inref, mcur, marc,
+                                                                          mpos);
+  }
   return hipGetLastError();
 }
 
