@@ -31,10 +31,12 @@ from collections import defaultdict
 _HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(_HERE, "csrc")
 
-# kernel families, as timed by the library (enum fst_kernel)
+# kernel families, as timed by the library (enum fst_kernel) in the default
+# (concurrent) search order, where one timer covers every search launch:
+# both searches side by side (k_gen2), the forward search alone (its first
+# generations) and either search alone once the other has ended
 FAMILIES = {
-    "search_forward": ("k_gen<true>",),
-    "search_backward": ("k_gen<false>",),
+    "search_forward": ("k_gen<true>", "k_gen<false>", "k_gen2("),
     "count": ("k_count(", "k_count_heavy("),
     "fill": ("k_fill_light(", "k_fill_heavy("),
     # scores of the composed graph (bench.py --task score)
