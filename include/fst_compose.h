@@ -104,7 +104,7 @@ typedef struct {
 
 /* Statistics of the last successful run. */
 typedef struct {
-  int64_t key_space;     /* number of key slots of the visited bitmaps       */
+  int64_t key_space;     /* key slots: V_A x 2^(b+1), b = max(4, bits(V_B-1)) */
   int64_t accessible;    /* keys reached from the start keys                 */
   int64_t coaccessible;  /* accessible keys that reach an accepting key = V_C */
   int64_t generated;     /* moves out of accessible keys; -1 unless

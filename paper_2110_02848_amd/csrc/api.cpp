@@ -60,7 +60,7 @@ struct fst_ctx {
   DevBuf aOutPerm, aOutArc, aOutRec, aOutLut, bOutPerm, bOutArc, bOutRec, bOutLut;
   DevBuf aOutLab, aOutW, bOutLab, bOutW, bOutChain, bInChain;
   DevBuf aInOff, aInPerm, aInArc, aInRec, aInLut, bInOff, bInPerm, bInArc, bInRec, bInLut;
-  DevBuf vis, coacc, wbase, fq, bq, heavy, hoff, heavy2, hoff2, cnt, btot;
+  DevBuf vis, coacc, trim, wbase, fq, bq, heavy, hoff, heavy2, hoff2, cnt, btot;
   // score workspace
   DevBuf s_sc, s_owner, s_extra, s_inref, s_mbeg, s_mlen, s_mcur, s_marc, s_val, s_acc,
       s_mpos;
@@ -489,9 +489,14 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
 
   // state ids share their arc-record word with two flag bits
   if (VA > NBR_MASK || VB > NBR_MASK) return FST_ERR_TOO_LARGE;
-  const uint32_t shiftB = (uint32_t)bitlen((unsigned long long)(VB - 1));
+  // at least 4 bits, so that a key-order bitmap word holds keys of one A state
+  const int bitsB = bitlen((unsigned long long)(VB - 1));
+  const uint32_t shiftB = (uint32_t)(bitsB > 4 ? bitsB : 4);
   const unsigned long long nkeys = (unsigned long long)VA << (shiftB + 1);
-  if (nkeys >= (1ull << 32)) return FST_ERR_TOO_LARGE;
+  // the search bitmaps' diagonal layout: rows of A states rounded up to 64
+  const unsigned long long rowA = ((unsigned long long)VA + 63) / 64 * 64;
+  const unsigned long long nsbits = rowA << (shiftB + 1);
+  if (nkeys >= (1ull << 32) || nsbits >= (1ull << 32)) return FST_ERR_TOO_LARGE;
   c->stats.key_space = (int64_t)nkeys;
   c->nkeys = nkeys;
   const int labA = bitlen(c->h_sc->maxLabA), labB = bitlen(c->h_sc->maxLabB);
@@ -577,9 +582,11 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   // (f = 1 only where epsOutA), without waiting for a count of those states
   const unsigned long long capll = 2ull * (unsigned long long)VA * (unsigned long long)VB;
   const uint32_t cap = (uint32_t)(capll < nkeys ? capll : nkeys);  // <= nkeys < 2^32
-  const size_t nwords = (size_t)((nkeys + 31) / 32);
-  FST_TRY(ensure(c, c->vis, nwords * 4));
-  FST_TRY(ensure(c, c->coacc, nwords * 4));
+  const size_t nwords = (size_t)((nkeys + 31) / 32);  // key-order bitmaps
+  const size_t snwords = (size_t)(nsbits / 32);          // search bitmaps
+  FST_TRY(ensure(c, c->vis, snwords * 4));
+  FST_TRY(ensure(c, c->coacc, snwords * 4));
+  FST_TRY(ensure(c, c->trim, nwords * 4));
   FST_TRY(ensure(c, c->wbase, nwords * 4));
   FST_TRY(ensure(c, c->fq, (size_t)cap * 4));
   FST_TRY(ensure(c, c->bq, (size_t)cap * 4));
@@ -592,8 +599,8 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   FST_TRY(ensure(c, c->lists, ((size_t)VA + VB + 2) * 4));
   size_t scan_n = nwords > (size_t)cap + 1 ? nwords : (size_t)cap + 1;
   FST_TRY(ensure(c, c->scan_tmp, scan_temp_bytes(scan_n)));
-  HIP_TRY(hipMemsetAsync(c->vis.p, 0, nwords * 4, s));
-  HIP_TRY(hipMemsetAsync(c->coacc.p, 0, nwords * 4, s));
+  HIP_TRY(hipMemsetAsync(c->vis.p, 0, snwords * 4, s));
+  HIP_TRY(hipMemsetAsync(c->coacc.p, 0, snwords * 4, s));
 
   Problem &P = c->P;
   P = Problem{};
@@ -604,10 +611,13 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   P.aIn = views[2];
   P.bIn = views[3];
   P.shiftB = shiftB;
+  P.maskB = (1u << shiftB) - 1u;
+  P.rowA = (uint32_t)rowA;
   P.chain_max = c->chain_depth;
   P.mark_accept = 1;
   P.vis = as<uint32_t>(c->vis);
   P.coacc = as<uint32_t>(c->coacc);
+  P.trim = as<uint32_t>(c->trim);
   P.wbase = as<uint32_t>(c->wbase);
 
   // ---- the two searches ----
@@ -648,15 +658,15 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
     const GenSlot &nf = c->h_sc->G[FIRST % 3];
     if (nf.qcount == 0 && (uint32_t)nf.hpack == 0) {
       c->stats.fwd_levels = c->h_sc->gens;
-      HIP_TRY(launch_popcount(P.vis, nwords, &d_sc->naccessible, s));
-      if (c->count_moves) HIP_TRY(launch_count_moves(P, nwords, true, &d_sc->generated, s));
+      HIP_TRY(launch_popcount(P.vis, snwords, &d_sc->naccessible, s));
+      if (c->count_moves) HIP_TRY(launch_count_moves(P, snwords, true, &d_sc->generated, s));
       phase_end(c, PH_FWD, s);
       phase_begin(c, PH_BWD, s);
       P.restrict_bwd = 1;
       HIP_TRY(hipMemsetAsync(d_sc->G, 0, sizeof(d_sc->G), s));
       HIP_TRY(launch_seed_backward(P, S, bq, s));
       FST_TRY(search(c, S, false, &c->stats.bwd_levels, s));
-      HIP_TRY(launch_trim_words(P.coacc, P.vis, wbase, nwords, s));
+      HIP_TRY(launch_trim(P, (uint32_t)VA, as<uint32_t>(c->trim), wbase, s));
       phase_end(c, PH_BWD, s);
     } else {
       P.mark_accept = 0;  // the backward seeds below are every accepting pair
@@ -670,12 +680,12 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
       HIP_TRY(hipMemsetAsync(cnts, 0, 8, s));
       HIP_TRY(launch_seed_backward_all(P, SB, la, cnts, lb, cnts + 1, s));
       FST_TRY(search_concurrent(c, P, S, SB, FIRST, s));
-      HIP_TRY(launch_popcount(P.vis, nwords, &d_sc->naccessible, s));
-      if (c->count_moves) HIP_TRY(launch_count_moves(P, nwords, true, &d_sc->generated, s));
+      HIP_TRY(launch_popcount(P.vis, snwords, &d_sc->naccessible, s));
+      if (c->count_moves) HIP_TRY(launch_count_moves(P, snwords, true, &d_sc->generated, s));
       phase_end(c, PH_FWD, s);
       // the backward phase is the final intersection only
       phase_begin(c, PH_BWD, s);
-      HIP_TRY(launch_trim_words(P.coacc, P.vis, wbase, nwords, s));
+      HIP_TRY(launch_trim(P, (uint32_t)VA, as<uint32_t>(c->trim), wbase, s));
       phase_end(c, PH_BWD, s);
     }
   } else if (c->order == FST_ORDER_COACCESSIBLE_FIRST) {
@@ -694,9 +704,9 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
     HIP_TRY(hipMemsetAsync(d_sc->G, 0, sizeof(d_sc->G), s));
     HIP_TRY(launch_seed_forward(P, S, la, cnts, lb, cnts + 1, s));
     FST_TRY(search(c, S, true, &c->stats.fwd_levels, s));
-    HIP_TRY(launch_popcount(P.vis, nwords, &d_sc->naccessible, s));
-    if (c->count_moves) HIP_TRY(launch_count_moves(P, nwords, true, &d_sc->generated, s));
-    HIP_TRY(launch_trim_words(P.coacc, P.vis, wbase, nwords, s));
+    HIP_TRY(launch_popcount(P.vis, snwords, &d_sc->naccessible, s));
+    if (c->count_moves) HIP_TRY(launch_count_moves(P, snwords, true, &d_sc->generated, s));
+    HIP_TRY(launch_trim(P, (uint32_t)VA, as<uint32_t>(c->trim), wbase, s));
     phase_end(c, PH_FWD, s);
   } else {
     P.restrict_fwd = 0;
@@ -706,8 +716,8 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
     HIP_TRY(hipMemsetAsync(d_sc->G, 0, sizeof(d_sc->G), s));
     HIP_TRY(launch_seed_forward(P, S, la, cnts, lb, cnts + 1, s));
     FST_TRY(search(c, S, true, &c->stats.fwd_levels, s));
-    HIP_TRY(launch_popcount(P.vis, nwords, &d_sc->naccessible, s));
-    if (c->count_moves) HIP_TRY(launch_count_moves(P, nwords, true, &d_sc->generated, s));
+    HIP_TRY(launch_popcount(P.vis, snwords, &d_sc->naccessible, s));
+    if (c->count_moves) HIP_TRY(launch_count_moves(P, snwords, true, &d_sc->generated, s));
     phase_end(c, PH_FWD, s);
 
     // backward search, seeded by the accepting keys listed in bq
@@ -718,7 +728,7 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
     // the backward search may set co-accessible bits of keys it never
     // expands (not accessible); the trim set is what remains after masking
     // them, and the same pass counts the trim keys of every bitmap word
-    HIP_TRY(launch_trim_words(P.coacc, P.vis, wbase, nwords, s));
+    HIP_TRY(launch_trim(P, (uint32_t)VA, as<uint32_t>(c->trim), wbase, s));
     phase_end(c, PH_BWD, s);
   }
   if (c->count_moves) HIP_TRY(launch_count_moves(P, nwords, false, &d_sc->generated_bwd, s));
@@ -732,7 +742,7 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   const uint32_t nstates = (uint32_t)nst;
   uint32_t *key_of = fq;   // the forward queue is free now (nstates <= cap)
   uint32_t *heavy = bq;    // so is the backward queue
-  HIP_TRY(launch_key_of_id(P.coacc, wbase, nwords, key_of, s));
+  HIP_TRY(launch_key_of_id(P.trim, wbase, nwords, key_of, s));
   FST_TRY(ensure(c, c->cnt, ((size_t)nstates + 1) * 4));
   FST_TRY(ensure(c, c->btot, (OUT_CHUNKS + 1) * 4));
   uint32_t *cnt = as<uint32_t>(c->cnt), *btot = as<uint32_t>(c->btot);
@@ -931,7 +941,7 @@ void fst_ctx_destroy(fst_ctx *c) {
                     &c->aOutRec,  &c->aOutLut,  &c->bOutPerm, &c->bOutArc, &c->bOutRec,
                     &c->bOutLut,  &c->aInOff,   &c->aInPerm, &c->aInArc,  &c->aInRec,
                     &c->aInLut,   &c->bInOff,   &c->bInPerm, &c->bInArc,  &c->bInRec,
-                    &c->bInLut,   &c->vis,      &c->coacc,   &c->wbase,   &c->heavy2,
+                    &c->bInLut,   &c->vis,      &c->coacc,   &c->trim,    &c->wbase,   &c->heavy2,
                     &c->hoff2,    &c->fq,
                     &c->bq,       &c->heavy,    &c->hoff,    &c->cnt,     &c->aOutLab,
                     &c->aOutW,    &c->bOutLab,  &c->bOutW,   &c->btot,    &c->bOutChain,

@@ -740,6 +740,15 @@ struct Next {
   typename Dir<FWD>::Info info;
 };
 
+// Sets bits `m` of word w without reading the word back (no return value is
+// waited for).
+__device__ __forceinline__ void set_bits(uint32_t *bm, uint32_t w, uint32_t m) {
+  __hip_atomic_fetch_or(bm + w, m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void set_bit(uint32_t *bm, uint32_t b) {
+  set_bits(bm, b >> 5, 1u << (b & 31u));
+}
+
 // A key reached for the first time (`fresh`).  Forward: if it accepts it is
 // marked co-accessible and listed as a seed of the backward search.  Then:
 // heavy keys go to the next generation's heavy list; a light key becomes this
@@ -754,7 +763,7 @@ __device__ __forceinline__ void place(const Problem &P, const SearchArgs &S, con
     const uint32_t u = Dir<FWD>::units(vi);
     if constexpr (FWD) {
       seed = P.mark_accept && vi.accept != 0;
-      if (seed) atomicOr(P.coacc + (v >> 5), 1u << (v & 31u));
+      if (seed) set_bit(P.coacc, search_bit(P, v));
     }
     if (u > LIGHT_SEARCH) {
       list_heavy(S, nx, v, u);
@@ -767,12 +776,6 @@ __device__ __forceinline__ void place(const Problem &P, const SearchArgs &S, con
   }
   if (FWD) wave_push(seed, v, Pusher{S.acc, S.cap, &S.sc->tail2, S.sc});
   wave_push(push, v, Pusher{S.Q + nx.qbase, S.cap - nx.qbase, &nx.slot->qcount, S.sc});
-}
-
-// Sets a bit without reading the word back (no return value is waited for).
-__device__ __forceinline__ void set_bit(uint32_t *bm, uint32_t k) {
-  __hip_atomic_fetch_or(bm + (k >> 5), 1u << (k & 31u), __ATOMIC_RELAXED,
-                        __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Visit a move target (forward) or a predecessor (backward, where only
@@ -794,7 +797,8 @@ __device__ __forceinline__ void visit(const Problem &P, const SearchArgs &S, con
   const Rec F = opaque(fix);
   const typename Dir<FWD>::Info vi =
       Dir<FWD>::make(v, P.shiftB, t.fixA ? F : L, t.fixA ? L : F);
-  const uint32_t bit = 1u << (v & 31u), w = v >> 5;
+  const uint32_t sb = search_bit(P, v);
+  const uint32_t bit = 1u << (sb & 31u), w = sb >> 5;
   bool fresh;
   // a restricted search expands only keys the other search has reached
   const uint32_t *other = FWD ? P.coacc : P.vis;
@@ -802,7 +806,7 @@ __device__ __forceinline__ void visit(const Problem &P, const SearchArgs &S, con
   const bool restricted = FWD ? P.restrict_fwd != 0 : P.restrict_bwd != 0;
   if (t.uniq) {
     fresh = !restricted || (other[w] & bit) != 0;
-    if (fresh) set_bit(mine, v);
+    if (fresh) set_bit(mine, sb);
   } else if (t.hot || (FWD && restricted)) {
     const uint32_t wo = restricted ? other[w] : bit, wm = mine[w];  // one round trip
     fresh = (wo & bit) && !(wm & bit) && (atomicOr(mine + w, bit) & bit) == 0;
@@ -849,16 +853,18 @@ __device__ __forceinline__ bool chain_jump(const Problem &P, const SearchArgs &S
   int n = c0.x;
   if (n > P.chain_max - depth) n = P.chain_max - depth;
   uint32_t qa = state_a(info);
-  uint32_t keys[CHAIN_STEPS];
+  uint32_t keys[CHAIN_STEPS], sbs[CHAIN_STEPS];
   int done = 0;
 #pragma unroll
   for (int i = 0; i < CHAIN_STEPS; ++i) {
     keys[i] = 0;
+    sbs[i] = 0;
     if (i < n && done == i && (uint32_t)lab[i] < stride) {
       const int4 b = lut[(size_t)qa * stride + (uint32_t)lab[i]];
       if (b.y - b.x == 1 && (b.z & NBR_UNIQ) && !(b.z & NBR_EPS)) {
         qa = nbr_of(b.z);
         keys[i] = make_key(qa, nbr_of(nbs[i]), 0u, P.shiftB);
+        sbs[i] = search_bit(P, keys[i]);
         done = i + 1;
       }
     }
@@ -871,14 +877,25 @@ __device__ __forceinline__ bool chain_jump(const Problem &P, const SearchArgs &S
   const bool restricted = FWD ? P.restrict_fwd != 0 : P.restrict_bwd != 0;
   bool ok[CHAIN_STEPS];
 #pragma unroll
-  for (int i = 0; i < CHAIN_STEPS; ++i) ok[i] = i < done && (!restricted || test_bit(other, keys[i]));
+  for (int i = 0; i < CHAIN_STEPS; ++i) ok[i] = i < done && (!restricted || test_bit(other, sbs[i]));
   int m = 0;  // keys reached and kept
 #pragma unroll
   for (int i = 0; i < CHAIN_STEPS; ++i)
-    if (m == i && ok[i]) {
-      set_bit(mine, keys[i]);
-      m = i + 1;
+    if (m == i && ok[i]) m = i + 1;
+  // their bits, one atomic per run of keys in the same bitmap word (a chain
+  // whose A and B states both advance by one stays on one diagonal)
+  uint32_t cw = 0, cm = 0;
+#pragma unroll
+  for (int i = 0; i < CHAIN_STEPS; ++i)
+    if (i < m) {
+      if (cm && (sbs[i] >> 5) != cw) {
+        set_bits(mine, cw, cm);
+        cm = 0;
+      }
+      cw = sbs[i] >> 5;
+      cm |= 1u << (sbs[i] & 31u);
     }
+  if (cm) set_bits(mine, cw, cm);
   depth += m > 0 ? m - 1 : 0;
   if (m > 0) {
     uint32_t last = keys[0];
@@ -1000,7 +1017,8 @@ __global__ __launch_bounds__(NT) void k_seed_forward(Problem P, SearchArgs S,
     Fwd ki;
     if (i < n) {
       k = make_key((uint32_t)la[i / nb], (uint32_t)lb[i % nb], 0u, P.shiftB);
-      fresh = (!P.restrict_fwd || test_bit(P.coacc, k)) && claim(P.vis, k);
+      const uint32_t sb = search_bit(P, k);
+      fresh = (!P.restrict_fwd || test_bit(P.coacc, sb)) && claim(P.vis, sb);
       ki = fwd_info(P, k);
     }
     Next<true> nk;
@@ -1032,7 +1050,7 @@ __global__ __launch_bounds__(NT) void k_seed_backward_all(Problem P, SearchArgs 
       // every pair is enumerated once, so it is placed once; a forward
       // search running first may already have marked it co-accessible
       fresh = f == 0 || eps;
-      if (fresh) set_bit(P.coacc, k);
+      if (fresh) set_bit(P.coacc, search_bit(P, k));
       ki = bwd_info(P, k);
     }
     Next<false> nk;
@@ -1060,18 +1078,23 @@ __global__ __launch_bounds__(NT) void k_seed_backward(Problem P, SearchArgs S,
 }
 
 // Number of moves the search examines (a statistic, on request): forward,
-// the moves out of the accessible keys; backward, the predecessor moves of
-// the co-accessible keys.
+// the moves out of the accessible keys (search layout); backward, the
+// predecessor moves of the trim keys (key order).
 template <bool FWD>
 __global__ __launch_bounds__(NT) void k_count_moves(Problem P, ull nwords,
                                                     unsigned long long *__restrict__ out) {
   __shared__ ull s_w[NWAVES];
-  const uint32_t *bm = FWD ? P.vis : P.coacc;
+  const uint32_t *bm = FWD ? P.vis : P.trim;
   ull c = 0;
-  const ull nkeys = nwords * 32u;
-  for (ull k = (ull)blockIdx.x * NT + threadIdx.x; k < nkeys; k += (ull)gridDim.x * NT) {
+  const ull nbits = nwords * 32u;
+  for (ull k = (ull)blockIdx.x * NT + threadIdx.x; k < nbits; k += (ull)gridDim.x * NT) {
     if (!test_bit(bm, (uint32_t)k)) continue;
-    const typename Dir<FWD>::Info s = Dir<FWD>::info(P, (uint32_t)k);
+    uint32_t key = (uint32_t)k;
+    if (FWD) {
+      const uint32_t x = (uint32_t)(k >> 1), d = x / P.rowA, qa = x - d * P.rowA;
+      key = make_key(qa, (d + qa) & P.maskB, (uint32_t)(k & 1u), P.shiftB);
+    }
+    const typename Dir<FWD>::Info s = Dir<FWD>::info(P, key);
     const uint32_t nu = Dir<FWD>::units(s);
     for (uint32_t u = 0; u < nu; ++u)
       for_unit<FWD>(P, s, u, [&](const Target &, const Rec &) { ++c; });
@@ -1095,15 +1118,67 @@ __global__ __launch_bounds__(NT) void k_popcount(const uint32_t *__restrict__ bm
 // compaction
 // ---------------------------------------------------------------------------
 
-// coacc[w] &= vis[w] (drops co-accessible bits of keys that are not
-// accessible), cnt[w] = popcount of the result.
-__global__ __launch_bounds__(NT) void k_trim_words(uint32_t *__restrict__ coacc,
-                                                   const uint32_t *__restrict__ vis,
-                                                   uint32_t *__restrict__ cnt, ull nwords) {
-  for (ull w = (ull)blockIdx.x * NT + threadIdx.x; w < nwords; w += (ull)gridDim.x * NT) {
-    const uint32_t m = coacc[w] & vis[w];
-    coacc[w] = m;
-    cnt[w] = (uint32_t)__popc(m);
+// The trim bitmap in key order: vis AND coacc (which drops co-accessible
+// bits of keys that are not accessible), moved from the diagonal search
+// layout to rows of one A state (a trim word: 16 B states x 2 f), and
+// cnt[w] = popcount(trim[w]).  One tile = TRIM_ROWS A states x TRIM_QB B
+// states: the TRIM_QB + TRIM_ROWS - 1 diagonals it meets, TRIM_ROWS / 16
+// words of each (the tile's A states), go to LDS; each thread then builds
+// four trim words of one A state, 16 diagonals per word.  The workgroups of
+// one XCD take consecutive tiles, which share search-bitmap lines.
+constexpr uint32_t TRIM_ROWS = 64, TRIM_QB = 256, TRIM_D = TRIM_QB + TRIM_ROWS - 1;
+
+__global__ __launch_bounds__(NT) void k_trim(Problem P, uint32_t VA, uint32_t ntA, ull ntiles,
+                                             uint32_t *__restrict__ trim,
+                                             uint32_t *__restrict__ cnt) {
+  static_assert(NT == 4 * TRIM_ROWS, "four threads per A state of a tile");
+  __shared__ uint32_t L[TRIM_D][TRIM_ROWS / 16];
+  const uint32_t WR = (P.maskB >> 4) + 1;  // trim words per A state
+  const uint32_t rw = P.rowA >> 4;         // search words per diagonal
+  const ull first = (ull)(blockIdx.x & 7u) * (gridDim.x >> 3) + (blockIdx.x >> 3);
+  const uint32_t r = threadIdx.x >> 2, q = threadIdx.x & 3u;
+  for (ull t = first; t < ntiles; t += gridDim.x) {
+    const uint32_t a0 = (uint32_t)(t % ntA) * TRIM_ROWS, b0 = (uint32_t)(t / ntA) * TRIM_QB;
+    __syncthreads();  // the previous tile's LDS readers are done
+    for (uint32_t i = threadIdx.x; i < TRIM_D; i += NT) {
+      const uint32_t d = (b0 - a0 - (TRIM_ROWS - 1) + i) & P.maskB;
+      const size_t o = (size_t)d * rw + (a0 >> 4);
+      const uint4 v = *reinterpret_cast<const uint4 *>(P.vis + o);
+      const uint4 c = *reinterpret_cast<const uint4 *>(P.coacc + o);
+      L[i][0] = v.x & c.x;
+      L[i][1] = v.y & c.y;
+      L[i][2] = v.z & c.z;
+      L[i][3] = v.w & c.w;
+    }
+    __syncthreads();
+    // trim word j of this A state holds B states b0 + 16 j + [0, 16): key
+    // (a0 + r, b0 + 16 j + u) lies on diagonal entry 16 j + u - r + 63
+    uint32_t out[4];
+#pragma unroll
+    for (uint32_t jj = 0; jj < 4; ++jj) {
+      const uint32_t j = 4 * q + jj;
+      uint32_t wv = 0;
+#pragma unroll
+      for (uint32_t u = 0; u < 16; ++u)
+        wv |= ((L[16 * j + u + (TRIM_ROWS - 1) - r][r >> 4] >> ((r & 15u) * 2)) & 3u) << (2 * u);
+      out[jj] = wv;
+    }
+    const uint32_t qa = a0 + r;
+    if (qa < VA) {
+      const size_t o = (size_t)qa * WR + (b0 >> 4) + 4 * q;
+      if (WR >= 16) {
+        *reinterpret_cast<uint4 *>(trim + o) = make_uint4(out[0], out[1], out[2], out[3]);
+        *reinterpret_cast<uint4 *>(cnt + o) = make_uint4(__popc(out[0]), __popc(out[1]),
+                                                         __popc(out[2]), __popc(out[3]));
+      } else {
+#pragma unroll
+        for (uint32_t jj = 0; jj < 4; ++jj)
+          if (4 * q + jj < WR) {
+            trim[o + jj] = out[jj];
+            cnt[o + jj] = (uint32_t)__popc(out[jj]);
+          }
+      }
+    }
   }
 }
 
@@ -1133,7 +1208,7 @@ __global__ __launch_bounds__(NT) void k_key_of_id(const uint32_t *__restrict__ b
 
 __device__ __forceinline__ uint32_t new_id(const Problem &P, uint32_t k) {
   const uint32_t w = k >> 5;
-  return P.wbase[w] + (uint32_t)__popc(P.coacc[w] & ((1u << (k & 31u)) - 1u));
+  return P.wbase[w] + (uint32_t)__popc(P.trim[w] & ((1u << (k & 31u)) - 1u));
 }
 
 __device__ __forceinline__ uint32_t out_units(const Fwd &s) { return s.eA + (uint32_t)s.be + s.mU; }
@@ -1303,7 +1378,7 @@ __device__ uint32_t heavy_state(const Problem &P, uint32_t id, uint32_t key, uin
     if (i < s.eA) {
       pa = s.aS + (int32_t)i;
       d = make_key(nbr_of(P.aOut.arec[pa].y), s.qb, 0u, sh);
-      keep = test_bit(P.coacc, d);
+      keep = test_bit(P.trim, d);
     }
     uint32_t tot;
     uint32_t ex = block_excl_scan<uint32_t>(keep ? 1u : 0u, s_w, tot);
@@ -1319,7 +1394,7 @@ __device__ uint32_t heavy_state(const Problem &P, uint32_t id, uint32_t key, uin
     if (i < (uint32_t)s.be) {
       pb = s.bS + (int32_t)i;
       d = make_key(s.qa, nbr_of(P.bOut.arec[pb].y), s.epsA, sh);
-      keep = test_bit(P.coacc, d);
+      keep = test_bit(P.trim, d);
     }
     uint32_t tot;
     uint32_t ex = block_excl_scan<uint32_t>(keep ? 1u : 0u, s_w, tot);
@@ -1340,7 +1415,7 @@ __device__ uint32_t heavy_state(const Problem &P, uint32_t id, uint32_t key, uin
         da = nbr_of(ar.y);
         label_range(P.bOut, s.qb, s.bS + s.be, s.bE, ar.x, lo, hi);
         for (int32_t pb = lo; pb < hi; ++pb)
-          kept += test_bit(P.coacc, make_key(da, nbr_of(P.bOut.arec[pb].y), 0u, sh));
+          kept += test_bit(P.trim, make_key(da, nbr_of(P.bOut.arec[pb].y), 0u, sh));
       }
       uint32_t tot;
       uint32_t ex = block_excl_scan<uint32_t>(kept, s_w, tot);
@@ -1350,7 +1425,7 @@ __device__ uint32_t heavy_state(const Problem &P, uint32_t id, uint32_t key, uin
         uint32_t pos = pos0 + run + ex;
         for (int32_t pb = lo; pb < hi; ++pb) {
           const uint32_t d = make_key(da, nbr_of(P.bOut.arec[pb].y), 0u, sh);
-          if (test_bit(P.coacc, d))
+          if (test_bit(P.trim, d))
             put_arc(O, P, pos++, id, d, ia, P.bOut.olab[pb], wa + P.bOut.w[pb], pa, pb);
         }
       }
@@ -1378,7 +1453,7 @@ __global__ __launch_bounds__(NT) void k_count(Problem P, const uint32_t *__restr
         hv = true;
       } else {
         enum_light(P, s, [&](uint32_t d, int32_t, int32_t, float, int32_t, int32_t) {
-          c += test_bit(P.coacc, d) ? 1u : 0u;
+          c += test_bit(P.trim, d) ? 1u : 0u;
         });
       }
       cnt[id] = c;
@@ -1444,7 +1519,7 @@ __global__ __launch_bounds__(NT) void k_fill_light(Problem P, const uint32_t *__
     if (out_units(s) > LIGHT_UNITS) continue;
     const uint32_t sid = (uint32_t)id;
     enum_light(P, s, [&](uint32_t d, int32_t il, int32_t ol, float w, int32_t pa, int32_t pb) {
-      if (test_bit(P.coacc, d)) put_arc(O, P, pos++, sid, d, il, ol, w, pa, pb);
+      if (test_bit(P.trim, d)) put_arc(O, P, pos++, sid, d, il, ol, w, pa, pb);
     });
   }
   if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) O.arc_offset[n] = (int32_t)narcs;
@@ -1645,10 +1720,16 @@ hipError_t launch_popcount(const uint32_t *bm, size_t nwords, unsigned long long
   return hipGetLastError();
 }
 
-hipError_t launch_trim_words(uint32_t *coacc, const uint32_t *vis, uint32_t *cnt, size_t nwords,
-                             hipStream_t s) {
-  if (!nwords) return hipSuccess;
-  k_trim_words<<<grid_for(nwords, 8192), NT, 0, s>>>(coacc, vis, cnt, nwords);
+hipError_t launch_trim(const Problem &P, uint32_t VA, uint32_t *trim, uint32_t *cnt,
+                       hipStream_t s) {
+  if (!VA) return hipSuccess;
+  const uint32_t ntA = (VA + TRIM_ROWS - 1) / TRIM_ROWS;
+  const ull WR = ((ull)P.maskB + 1) >> 4, ntB = (WR + 15) / 16;
+  const ull ntiles = (ull)ntA * ntB;
+  // a multiple of 8 workgroups (one share per XCD), at most 8 x 2048
+  const ull per = (ntiles + 7) / 8;
+  const unsigned grid = (unsigned)(8 * (per < 2048 ? per : 2048));
+  k_trim<<<grid, NT, 0, s>>>(P, VA, ntA, ntiles, trim, cnt);
   return hipGetLastError();
 }
 

@@ -118,9 +118,16 @@ struct Problem {
   int restrict_bwd;       // backward search expands only keys already in vis
   int mark_accept;        // forward search marks accepting keys co-accessible
                           // and lists them as backward seeds
-  uint32_t *vis;          // accessible-key bitmap
-  uint32_t *coacc;        // trim-key bitmap (accessible and co-accessible)
-  const uint32_t *wbase;  // exclusive popcount prefix of coacc words
+  // The two search bitmaps use the diagonal layout of search_bit(): a key
+  // (qa, qb, f) sits at bit 2 (d rowA + qa) + f with d = (qb - qa) mod
+  // 2^shiftB, so the keys of a chain that advances both states by one share
+  // a bitmap word.  The trim bitmap is in key order (bit = key).
+  uint32_t maskB;         // 2^shiftB - 1
+  uint32_t rowA;          // A states per diagonal, rounded up to 16
+  uint32_t *vis;          // accessible keys (search layout)
+  uint32_t *coacc;        // co-accessible keys (search layout)
+  const uint32_t *trim;   // accessible and co-accessible keys (key order)
+  const uint32_t *wbase;  // exclusive popcount prefix of trim words
 };
 
 // Output arrays of C.
@@ -239,6 +246,11 @@ __device__ __forceinline__ uint32_t key_qa(uint32_t k, uint32_t shiftB) {
 }
 __device__ __forceinline__ bool test_bit(const uint32_t *bm, uint32_t k) {
   return (bm[k >> 5] >> (k & 31u)) & 1u;
+}
+// Bit of key k in the search bitmaps (diagonal layout, see Problem).
+__device__ __forceinline__ uint32_t search_bit(const Problem &P, uint32_t k) {
+  const uint32_t qa = key_qa(k, P.shiftB), qb = key_qb(k, P.shiftB);
+  return (((qb - qa) & P.maskB) * P.rowA + qa) << 1 | (k & 1u);
 }
 
 // ---------------------------------------------------------------------------
@@ -414,16 +426,20 @@ hipError_t launch_generation(const Problem &P, const SearchArgs &S, bool forward
 hipError_t launch_generation2(const Problem &P, const SearchArgs &SF, const SearchArgs &SB, int gf,
                               int gb, hipStream_t s);
 // *out += number of moves the forward search examines out of the keys set in
-// P.vis, or (backward) the backward search examines into the keys set in
-// P.coacc (a statistic).
+// P.vis (search layout, nwords words), or (backward) the backward search
+// examines into the keys set in P.trim (key order, nwords words): a
+// statistic.
 hipError_t launch_count_moves(const Problem &P, size_t nwords, bool forward,
                               unsigned long long *out, hipStream_t s);
 // *out += number of set bits of bm[0, nwords).
 hipError_t launch_popcount(const uint32_t *bm, size_t nwords, unsigned long long *out,
                            hipStream_t s);
-// coacc[w] &= vis[w] and cnt[w] = popcount(coacc[w]) for w < nwords.
-hipError_t launch_trim_words(uint32_t *coacc, const uint32_t *vis, uint32_t *cnt, size_t nwords,
-                             hipStream_t s);
+// The trim bitmap in key order from the two search bitmaps (search layout):
+// trim = vis AND coacc, transposed from diagonals to rows of A states, and
+// cnt[w] = popcount(trim[w]) for each of its VA << (shiftB + 1) / 32 words.
+// Needs shiftB >= 4 (a trim word then holds keys of one A state).
+hipError_t launch_trim(const Problem &P, uint32_t VA, uint32_t *trim, uint32_t *cnt,
+                       hipStream_t s);
 hipError_t launch_key_of_id(const uint32_t *bm, const uint32_t *wbase, size_t nwords,
                             uint32_t *key_of, hipStream_t s);
 // Kept-arc count of every state of C (chunks of `per` states per
