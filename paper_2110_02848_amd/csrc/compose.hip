@@ -852,24 +852,52 @@ __device__ __forceinline__ bool chain_jump(const Problem &P, const SearchArgs &S
   const int32_t nbs[CHAIN_STEPS] = {c0.z, c1.x, c1.z, c2.x, c2.z, c3.x, c3.z};
   int n = c0.x;
   if (n > P.chain_max - depth) n = P.chain_max - depth;
-  uint32_t qa = state_a(info);
+  // The A side of hop i is the bucket of label lab[i] at the A state hop
+  // i - 1 reached.  Hop 0 is looked up first; the buckets of the later hops
+  // are then loaded together at A states guessed to continue with the step
+  // hop 0 took (chains of consecutively numbered states take one round trip
+  // instead of seven).  A hop whose guessed A state differs from the one
+  // the previous hop reached ends the jump there; the key it reached is
+  // expanded next, which continues the chain.
+  const uint32_t VA = (uint32_t)P.A.V;
   uint32_t keys[CHAIN_STEPS], sbs[CHAIN_STEPS];
   int done = 0;
-#pragma unroll
-  for (int i = 0; i < CHAIN_STEPS; ++i) {
-    keys[i] = 0;
-    sbs[i] = 0;
-    if (i < n && done == i && (uint32_t)lab[i] < stride) {
-      const int4 b = lut[(size_t)qa * stride + (uint32_t)lab[i]];
-      if (b.y - b.x == 1 && (b.z & NBR_UNIQ) && !(b.z & NBR_EPS)) {
-        qa = nbr_of(b.z);
-        keys[i] = make_key(qa, nbr_of(nbs[i]), 0u, P.shiftB);
-        sbs[i] = search_bit(P, keys[i]);
-        done = i + 1;
-      }
+  const uint32_t qa0 = state_a(info);
+  uint32_t qa = qa0;
+  if (n > 0 && (uint32_t)lab[0] < stride) {
+    const int4 b = lut[(size_t)qa0 * stride + (uint32_t)lab[0]];
+    if (b.y - b.x == 1 && (b.z & NBR_UNIQ) && !(b.z & NBR_EPS)) {
+      qa = nbr_of(b.z);
+      done = 1;
     }
   }
   if (done == 0) return false;
+  keys[0] = make_key(qa, nbr_of(nbs[0]), 0u, P.shiftB);
+  sbs[0] = search_bit(P, keys[0]);
+  const uint32_t step = qa - qa0;  // modulo 2^32
+  int4 bk[CHAIN_STEPS];
+#pragma unroll
+  for (int i = 1; i < CHAIN_STEPS; ++i) {
+    const uint32_t g = qa + (uint32_t)(i - 1) * step;  // guessed A state before hop i
+    bk[i] = make_int4(0, 0, 0, 0);
+    if (i < n && g < VA && (uint32_t)lab[i] < stride)
+      bk[i] = lut[(size_t)g * stride + (uint32_t)lab[i]];
+  }
+  uint32_t cur_a = qa;  // the A state the last verified hop reached
+#pragma unroll
+  for (int i = 1; i < CHAIN_STEPS; ++i) {
+    keys[i] = 0;
+    sbs[i] = 0;
+    const uint32_t g = qa + (uint32_t)(i - 1) * step;
+    const int4 b = bk[i];
+    if (i < n && done == i && g == cur_a && b.y - b.x == 1 && (b.z & NBR_UNIQ) &&
+        !(b.z & NBR_EPS)) {
+      cur_a = nbr_of(b.z);
+      keys[i] = make_key(cur_a, nbr_of(nbs[i]), 0u, P.shiftB);
+      sbs[i] = search_bit(P, keys[i]);
+      done = i + 1;
+    }
+  }
   // a restricted search keeps the reached keys up to the first one the other
   // search has not reached (their bits are loaded together)
   const uint32_t *other = FWD ? P.coacc : P.vis;
