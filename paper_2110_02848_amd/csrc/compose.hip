@@ -1218,19 +1218,29 @@ __device__ __forceinline__ void wave_chunk(ull n, ull per, ull &chunk, ull &begi
   if (begin > end) begin = end;
 }
 
-// key_of[id] = the id-th trim key, one thread per key slot and one
-// contiguous chunk of `per` slots per wavefront, so a wavefront's writes are
-// contiguous.
+// key_of[id] = the id-th trim key.  One workgroup per NT bitmap words (one
+// word per thread): a workgroup scan of the words' popcounts places each
+// word's keys in an LDS list, which the workgroup then writes out
+// contiguously from the prefix of its first word.
 __global__ __launch_bounds__(NT) void k_key_of_id(const uint32_t *__restrict__ bm,
                                                   const uint32_t *__restrict__ wbase,
-                                                  ull nwords, ull per,
-                                                  uint32_t *__restrict__ key_of) {
-  ull chunk, begin, end;
-  wave_chunk(nwords * 32u, per, chunk, begin, end);
-  for (ull k = begin + __lane_id(); k < end; k += WAVE) {
-    const uint32_t w = (uint32_t)(k >> 5), b = (uint32_t)(k & 31u);
-    const uint32_t m = bm[w];
-    if ((m >> b) & 1u) key_of[wbase[w] + (uint32_t)__popc(m & ((1u << b) - 1u))] = (uint32_t)k;
+                                                  ull nwords, uint32_t *__restrict__ key_of) {
+  __shared__ uint32_t s_keys[NT * 32];
+  __shared__ uint32_t s_w[NWAVES];
+  for (ull w0 = (ull)blockIdx.x * NT; w0 < nwords; w0 += (ull)gridDim.x * NT) {
+    const ull w = w0 + threadIdx.x;
+    uint32_t m = w < nwords ? bm[w] : 0u;
+    const uint32_t base = wbase[w0];
+    uint32_t total;
+    uint32_t o = block_excl_scan<uint32_t>((uint32_t)__popc(m), s_w, total);
+    while (m) {
+      const uint32_t b = (uint32_t)__ffs(m) - 1u;
+      s_keys[o++] = (uint32_t)(w * 32u) + b;
+      m &= m - 1u;
+    }
+    __syncthreads();
+    for (uint32_t i = threadIdx.x; i < total; i += NT) key_of[base + i] = s_keys[i];
+    __syncthreads();  // the list is read before the next chunk overwrites it
   }
 }
 
@@ -1374,18 +1384,26 @@ __device__ __forceinline__ void enum_light(const Problem &P, const Fwd &s, Visit
   }
 }
 
-// Write one arc of C; pa / pb are positions in the out-views (-1: none),
-// turned into arc ids only when provenance is requested.
-__device__ __forceinline__ void put_arc(const OutGraph &O, const Problem &P, uint32_t pos,
+// Write one arc of C if its target dk is a trim key; pa / pb are positions
+// in the out-views (-1: none), turned into arc ids only when provenance is
+// requested.  Every load (the target's trim word and prefix, the arc ids)
+// is issued before the test and the stores, so they share one round trip.
+__device__ __forceinline__ bool put_arc(const OutGraph &O, const Problem &P, uint32_t pos,
                                         uint32_t id, uint32_t dk, int32_t il, int32_t ol,
                                         float w, int32_t pa, int32_t pb) {
+  const uint32_t tw = P.trim[dk >> 5], base = P.wbase[dk >> 5];
+  const int32_t ida = O.arc_a && pa >= 0 ? P.aOut.perm[pa] : -1;
+  const int32_t idb = O.arc_b && pb >= 0 ? P.bOut.perm[pb] : -1;
+  const uint32_t below = tw & ((1u << (dk & 31u)) - 1u);
+  if (!((tw >> (dk & 31u)) & 1u)) return false;
   O.src[pos] = (int32_t)id;
-  O.dst[pos] = (int32_t)new_id(P, dk);
+  O.dst[pos] = (int32_t)(base + (uint32_t)__popc(below));
   O.il[pos] = il;
   O.ol[pos] = ol;
   O.w[pos] = w;
-  if (O.arc_a) O.arc_a[pos] = pa >= 0 ? P.aOut.perm[pa] : -1;
-  if (O.arc_b) O.arc_b[pos] = pb >= 0 ? P.bOut.perm[pb] : -1;
+  if (O.arc_a) O.arc_a[pos] = ida;
+  if (O.arc_b) O.arc_b[pos] = idb;
+  return true;
 }
 
 // Workgroup-cooperative canonical enumeration of one heavy state.  Every
@@ -1547,7 +1565,7 @@ __global__ __launch_bounds__(NT) void k_fill_light(Problem P, const uint32_t *__
     if (out_units(s) > LIGHT_UNITS) continue;
     const uint32_t sid = (uint32_t)id;
     enum_light(P, s, [&](uint32_t d, int32_t il, int32_t ol, float w, int32_t pa, int32_t pb) {
-      if (test_bit(P.trim, d)) put_arc(O, P, pos++, sid, d, il, ol, w, pa, pb);
+      if (put_arc(O, P, pos, sid, d, il, ol, w, pa, pb)) ++pos;
     });
   }
   if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) O.arc_offset[n] = (int32_t)narcs;
@@ -1764,8 +1782,7 @@ hipError_t launch_trim(const Problem &P, uint32_t VA, uint32_t *trim, uint32_t *
 hipError_t launch_key_of_id(const uint32_t *bm, const uint32_t *wbase, size_t nwords,
                             uint32_t *key_of, hipStream_t s) {
   if (!nwords) return hipSuccess;
-  const size_t per = out_chunk(nwords * 32);
-  k_key_of_id<<<out_grid(nwords * 32, per), NT, 0, s>>>(bm, wbase, nwords, per, key_of);
+  k_key_of_id<<<grid_for(nwords, 16384), NT, 0, s>>>(bm, wbase, nwords, key_of);
   return hipGetLastError();
 }
 
