@@ -133,7 +133,8 @@ FST_API void fst_ctx_destroy(fst_ctx *ctx);
  * exceeding it gives FST_ERR_NOMEM); FST_OPT_TIMING = 1 records per-phase
  * HIP events (read with fst_compose_phase_times).  Tuning knobs that never
  * change the result: FST_OPT_LABEL_BUCKETS (1 = default: per-state label
- * bucket tables when they fit in 256 MiB; 0 = binary search only) and
+ * bucket tables for a graph whose table fits in 256 MiB and in 64 times its
+ * arc records (8 bytes per arc); 0 = binary search only) and
  * FST_OPT_CHAIN_DEPTH (default 64: how many newly found keys one search
  * thread may expand depth-first before handing keys to the next frontier;
  * 0 = plain frontier-by-frontier search).  FST_OPT_COUNT_MOVES = 1 makes

@@ -454,13 +454,22 @@ int search_concurrent(fst_ctx *c, Problem P, const SearchArgs &SF, const SearchA
   return FST_OK;
 }
 
-// Label buckets are kept when the table is at most this large; so are the
-// chain records of each view of B.
+// Label buckets are kept when the table is at most this large, and at most
+// LUT_PER_ARC times the size of the graph's arc records (a graph with few
+// arcs per state finds a label in its short groups about as fast, and its
+// table would cost more to build than it saves); chain records of each view
+// of B are kept up to CHAIN_BUDGET.
 constexpr size_t LUT_BUDGET = (size_t)256 << 20;
+constexpr size_t LUT_PER_ARC = 64;
 constexpr size_t CHAIN_BUDGET = (size_t)256 << 20;
 
 size_t lut_bytes(int32_t V, uint32_t lab_max) {
   return (size_t)V * ((size_t)lab_max + 1) * sizeof(int4);
+}
+
+bool want_lut(const fst_ctx *c, int32_t V, int32_t E, uint32_t lab_max) {
+  const size_t b = lut_bytes(V, lab_max);
+  return c->buckets && b <= LUT_BUDGET && b <= LUT_PER_ARC * (size_t)E * sizeof(int2);
 }
 
 int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, int64_t *V_C,
@@ -509,8 +518,8 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   FST_TRY(ensure(c, c->v1, Emax * 4));
   FST_TRY(ensure(c, c->sort_tmp, sort_temp_bytes(Emax)));
   const uint32_t maxA = c->h_sc->maxLabA, maxB = c->h_sc->maxLabB;
-  const bool lutA = c->buckets && lut_bytes(VA, maxA) <= LUT_BUDGET;
-  const bool lutB = c->buckets && lut_bytes(VB, maxB) <= LUT_BUDGET;
+  const bool lutA = want_lut(c, (int32_t)VA, (int32_t)EA, maxA);
+  const bool lutB = want_lut(c, (int32_t)VB, (int32_t)EB, maxB);
   struct ViewBufs {
     DevBuf *perm, *arc, *rec, *lut, *off, *lab, *w;
   };
