@@ -720,12 +720,16 @@ struct NextGen {
 };
 
 // List a heavy key for the next generation: one packed atomic gives its
-// position and the offset of its first unit, consistently.
+// position and the offset of its first unit, consistently.  Its units take
+// a multiple of 8 slots of the generation's unit range (the slots past its
+// last unit are skipped), so unit u of every heavy key lands on slots
+// congruent to u mod 8: see gen_body.
 __device__ __forceinline__ void list_heavy(const SearchArgs &S, const NextGen &nx, uint32_t v,
                                            uint32_t units) {
-  const ull old = atomicAdd(&nx.slot->hpack, ((ull)units << 32) | 1ull);
+  const ull slots = ((ull)units + 7) & ~7ull;
+  const ull old = atomicAdd(&nx.slot->hpack, (slots << 32) | 1ull);
   const ull pos = (ull)nx.hbase + (old & 0xffffffffull);
-  if (pos < S.cap && (old >> 32) + units < (1ull << 32)) {
+  if (pos < S.cap && (old >> 32) + slots < (1ull << 32)) {
     S.heavy[pos] = v;
     S.hoff[pos] = (uint32_t)(old >> 32);
   } else {
@@ -935,10 +939,16 @@ __device__ __forceinline__ bool chain_jump(const Problem &P, const SearchArgs &S
   return true;
 }
 
-// Generation g (one kernel): one thread per unit of the generation's heavy
-// keys, then one thread per light frontier key.  A thread expands its units,
-// then, depth-first, the light keys it reached first (one loop, so the visit
-// code exists once).  New work goes to the slot of generation g + 1.
+// Generation g (one kernel): one thread per unit slot of the generation's
+// heavy keys, then one thread per light frontier key.  A thread expands its
+// units, then, depth-first, the light keys it reached first (one loop, so
+// the visit code exists once).  New work goes to the slot of generation
+// g + 1.  Workgroups are dispatched to the eight XCDs in turn (workgroup b
+// to XCD b mod 8), and the workgroups of XCD x take the items congruent to
+// x mod 8: unit u of a heavy key is expanded on XCD u mod 8, so the keys
+// reached from units with the same residue (in a lexicon, the words whose
+// entry arcs have it) and the records and bitmap lines they touch stay in
+// one XCD's L2.  nb is a multiple of 8.
 template <bool FWD>
 __device__ __forceinline__ void gen_body(const Problem &P, const SearchArgs &S, int g,
                                          unsigned bid, unsigned nb) {
@@ -963,7 +973,10 @@ __device__ __forceinline__ void gen_body(const Problem &P, const SearchArgs &S, 
   const uint32_t *hk = S.heavy + cur.hbase;
   const uint32_t *ho = S.hoff + cur.hbase;
   const ull n = U + cur.qcount;
-  for (ull i = (ull)bid * NT + threadIdx.x; i < n; i += (ull)nb * NT) {
+  const unsigned xcd = bid & 7u, nl = nb >> 3;
+  for (ull j = (ull)(bid >> 3) * NT + threadIdx.x; (bid >> 3) < nl; j += (ull)nl * NT) {
+    const ull i = 8 * j + xcd;
+    if (i >= n) break;
     uint32_t key, u0 = 0, u1 = 0;
     bool one_unit = false;
     if (i < U) {
@@ -979,6 +992,7 @@ __device__ __forceinline__ void gen_body(const Problem &P, const SearchArgs &S, 
       key = S.Q[cur.qbase + (uint32_t)(i - U)];
     }
     Info info = Dir<FWD>::info(P, key);
+    if (one_unit && u0 >= Dir<FWD>::units(info)) continue;  // a slot past the key's units
     u1 = one_unit ? u0 + 1 : Dir<FWD>::units(info);
     for (int depth = 0;; ++depth) {
       Next<FWD> nk;
