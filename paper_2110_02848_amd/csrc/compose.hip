@@ -1561,15 +1561,26 @@ __global__ __launch_bounds__(NT) void k_fill_light(Problem P, const uint32_t *__
   ull chunk, begin, end;
   wave_chunk(n, per, chunk, begin, end);
   uint32_t run = begin < end ? btot[chunk] : 0u;
+  // each iteration loads the next one's count and key (one round trip
+  // fewer on the chain of dependent loads)
+  uint32_t c_next = 0, k_next = 0;
+  if (begin + __lane_id() < end) {
+    c_next = cnt[begin + __lane_id()];
+    k_next = key_of[begin + __lane_id()];
+  }
   for (ull base = begin; base < end; base += WAVE) {
     const ull id = base + __lane_id();
     const bool valid = id < end;
-    const uint32_t c = valid ? cnt[id] : 0u;
+    const uint32_t c = c_next, key = k_next;
+    if (id + WAVE < end) {
+      c_next = cnt[id + WAVE];
+      k_next = key_of[id + WAVE];
+    }
     const uint32_t incl = wave_incl_scan(c);
     uint32_t pos = run + incl - c;
     run += __shfl(incl, WAVE - 1, WAVE);
     if (!valid) continue;
-    const Fwd s = fwd_info(P, key_of[id]);
+    const Fwd s = fwd_info(P, key);
     O.arc_offset[id] = (int32_t)pos;
     O.accept[id] = s.accept ? 1 : 0;
     O.start[id] = s.start ? 1 : 0;
