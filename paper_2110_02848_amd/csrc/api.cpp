@@ -573,8 +573,8 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
     const uint32_t lmax = isA ? maxA : maxB;
     // chain records for B's views, when they fit the budget
     int4 *chain = nullptr;
-    if (!isA && (size_t)g.V * 4 * sizeof(int4) <= CHAIN_BUDGET) {
-      FST_TRY(ensure(c, in ? c->bInChain : c->bOutChain, (size_t)g.V * 4 * sizeof(int4)));
+    if (!isA && (size_t)g.V * CHAIN_INT4 * sizeof(int4) <= CHAIN_BUDGET) {
+      FST_TRY(ensure(c, in ? c->bInChain : c->bOutChain, (size_t)g.V * CHAIN_INT4 * sizeof(int4)));
       chain = as<int4>(in ? c->bInChain : c->bOutChain);
     }
     J.j[i] = ViewJob{rec[i], arc[i], lutp[i], rec[i ^ 2], arc[i ^ 2], in ? g.accept : g.start,

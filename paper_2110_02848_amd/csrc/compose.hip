@@ -272,7 +272,7 @@ __global__ __launch_bounds__(NT) void k_chains(ViewJobs J) {
     const ViewJob &b = J.j[j];
     if (!b.chain) continue;
     const long long v = i - J.vbegin[j];
-    int32_t w[4 * 4] = {};
+    int32_t w[4 * CHAIN_INT4] = {};
     int n = 0;
     uint32_t cur = (uint32_t)v;
 #pragma unroll
@@ -291,9 +291,10 @@ __global__ __launch_bounds__(NT) void k_chains(ViewJobs J) {
       }
     }
     w[0] = n;
-    int4 *c = b.chain + 4 * v;
+    int4 *c = b.chain + CHAIN_INT4 * v;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) c[q] = make_int4(w[4 * q], w[4 * q + 1], w[4 * q + 2], w[4 * q + 3]);
+    for (int q = 0; q < CHAIN_INT4; ++q)
+      c[q] = make_int4(w[4 * q], w[4 * q + 1], w[4 * q + 2], w[4 * q + 3]);
   }
 }
 
@@ -850,58 +851,63 @@ __device__ __forceinline__ bool chain_jump(const Problem &P, const SearchArgs &S
   const int4 *lut = FWD ? P.aOut.lut : P.aIn.lut;
   const uint32_t stride = (uint32_t)(FWD ? P.aOut.lstride : P.aIn.lstride);
   if (!chain || !lut || !chain_shape(info) || depth >= P.chain_max) return false;
-  const int4 *cr = chain + 4 * (size_t)state_b(info);
-  const int4 c0 = cr[0], c1 = cr[1], c2 = cr[2], c3 = cr[3];
-  const int32_t lab[CHAIN_STEPS] = {c0.y, c0.w, c1.y, c1.w, c2.y, c2.w, c3.y};
-  const int32_t nbs[CHAIN_STEPS] = {c0.z, c1.x, c1.z, c2.x, c2.z, c3.x, c3.z};
-  int n = c0.x;
+  const int4 *cr = chain + CHAIN_INT4 * (size_t)state_b(info);
+  int32_t cw[4 * CHAIN_INT4];
+#pragma unroll
+  for (int q = 0; q < CHAIN_INT4; ++q) {
+    const int4 c = cr[q];
+    cw[4 * q] = c.x;
+    cw[4 * q + 1] = c.y;
+    cw[4 * q + 2] = c.z;
+    cw[4 * q + 3] = c.w;
+  }
+  int n = cw[0];
   if (n > P.chain_max - depth) n = P.chain_max - depth;
-  // The A side of hop i is the bucket of label lab[i] at the A state hop
-  // i - 1 reached.  Hop 0 is looked up first; the buckets of the later hops
-  // are then loaded together at A states guessed to continue with the step
-  // hop 0 took (chains of consecutively numbered states take one round trip
-  // instead of seven).  A hop whose guessed A state differs from the one
-  // the previous hop reached ends the jump there; the key it reached is
+  // The A side of hop i is the bucket of label l_i at the A state hop i - 1
+  // reached.  Hop 0 is looked up first; the buckets of the later hops are
+  // then loaded together at A states guessed to continue with the step hop
+  // 0 took (chains of consecutively numbered states take two round trips
+  // instead of one per hop).  A hop whose guessed A state differs from the
+  // one the previous hop reached ends the jump there; the key it reached is
   // expanded next, which continues the chain.
   const uint32_t VA = (uint32_t)P.A.V;
-  uint32_t keys[CHAIN_STEPS], sbs[CHAIN_STEPS];
+  uint32_t qa[CHAIN_STEPS];  // A state reached by hop i, for i < done
   int done = 0;
-  const uint32_t qa0 = state_a(info);
-  uint32_t qa = qa0;
-  if (n > 0 && (uint32_t)lab[0] < stride) {
-    const int4 b = lut[(size_t)qa0 * stride + (uint32_t)lab[0]];
-    if (b.y - b.x == 1 && (b.z & NBR_UNIQ) && !(b.z & NBR_EPS)) {
-      qa = nbr_of(b.z);
-      done = 1;
+  {
+    const uint32_t q0 = state_a(info);
+    if (n > 0 && (uint32_t)cw[1] < stride) {
+      const int4 b = lut[(size_t)q0 * stride + (uint32_t)cw[1]];
+      if (b.y - b.x == 1 && (b.z & NBR_UNIQ) && !(b.z & NBR_EPS)) {
+        qa[0] = nbr_of(b.z);
+        done = 1;
+      }
+    }
+    if (done == 0) return false;
+    const uint32_t step = qa[0] - q0;  // modulo 2^32
+    uint32_t nbv[CHAIN_STEPS];  // A state hop i reaches from its guessed state, or NO_KEY
+#pragma unroll
+    for (int i = 1; i < CHAIN_STEPS; ++i) {
+      const uint32_t g = qa[0] + (uint32_t)(i - 1) * step;
+      const uint32_t lab = (uint32_t)cw[1 + 2 * i];
+      nbv[i] = NO_KEY;
+      if (i < n && g < VA && lab < stride) {
+        const int4 b = lut[(size_t)g * stride + lab];
+        if (b.y - b.x == 1 && (b.z & NBR_UNIQ) && !(b.z & NBR_EPS)) nbv[i] = nbr_of(b.z);
+      }
+    }
+#pragma unroll
+    for (int i = 1; i < CHAIN_STEPS; ++i) {
+      const uint32_t g = qa[0] + (uint32_t)(i - 1) * step;
+      if (i < n && done == i && g == qa[i - 1] && nbv[i] != NO_KEY) {
+        qa[i] = nbv[i];
+        done = i + 1;
+      }
     }
   }
-  if (done == 0) return false;
-  keys[0] = make_key(qa, nbr_of(nbs[0]), 0u, P.shiftB);
-  sbs[0] = search_bit(P, keys[0]);
-  const uint32_t step = qa - qa0;  // modulo 2^32
-  int4 bk[CHAIN_STEPS];
+  uint32_t sbs[CHAIN_STEPS];
 #pragma unroll
-  for (int i = 1; i < CHAIN_STEPS; ++i) {
-    const uint32_t g = qa + (uint32_t)(i - 1) * step;  // guessed A state before hop i
-    bk[i] = make_int4(0, 0, 0, 0);
-    if (i < n && g < VA && (uint32_t)lab[i] < stride)
-      bk[i] = lut[(size_t)g * stride + (uint32_t)lab[i]];
-  }
-  uint32_t cur_a = qa;  // the A state the last verified hop reached
-#pragma unroll
-  for (int i = 1; i < CHAIN_STEPS; ++i) {
-    keys[i] = 0;
-    sbs[i] = 0;
-    const uint32_t g = qa + (uint32_t)(i - 1) * step;
-    const int4 b = bk[i];
-    if (i < n && done == i && g == cur_a && b.y - b.x == 1 && (b.z & NBR_UNIQ) &&
-        !(b.z & NBR_EPS)) {
-      cur_a = nbr_of(b.z);
-      keys[i] = make_key(cur_a, nbr_of(nbs[i]), 0u, P.shiftB);
-      sbs[i] = search_bit(P, keys[i]);
-      done = i + 1;
-    }
-  }
+  for (int i = 0; i < CHAIN_STEPS; ++i)
+    sbs[i] = i < done ? search_bit(P, make_key(qa[i], nbr_of(cw[2 + 2 * i]), 0u, P.shiftB)) : 0u;
   // a restricted search keeps the reached keys up to the first one the other
   // search has not reached (their bits are loaded together)
   const uint32_t *other = FWD ? P.coacc : P.vis;
@@ -916,24 +922,28 @@ __device__ __forceinline__ bool chain_jump(const Problem &P, const SearchArgs &S
     if (m == i && ok[i]) m = i + 1;
   // their bits, one atomic per run of keys in the same bitmap word (a chain
   // whose A and B states both advance by one stays on one diagonal)
-  uint32_t cw = 0, cm = 0;
+  uint32_t mw = 0, mm = 0;
 #pragma unroll
   for (int i = 0; i < CHAIN_STEPS; ++i)
     if (i < m) {
-      if (cm && (sbs[i] >> 5) != cw) {
-        set_bits(mine, cw, cm);
-        cm = 0;
+      if (mm && (sbs[i] >> 5) != mw) {
+        set_bits(mine, mw, mm);
+        mm = 0;
       }
-      cw = sbs[i] >> 5;
-      cm |= 1u << (sbs[i] & 31u);
+      mw = sbs[i] >> 5;
+      mm |= 1u << (sbs[i] & 31u);
     }
-  if (cm) set_bits(mine, cw, cm);
+  if (mm) set_bits(mine, mw, mm);
   depth += m > 0 ? m - 1 : 0;
   if (m > 0) {
-    uint32_t last = keys[0];
+    uint32_t la = qa[0], lb = (uint32_t)cw[2];
 #pragma unroll
     for (int i = 1; i < CHAIN_STEPS; ++i)
-      if (i < m) last = keys[i];
+      if (i < m) {
+        la = qa[i];
+        lb = (uint32_t)cw[2 + 2 * i];
+      }
+    const uint32_t last = make_key(la, nbr_of(lb), 0u, P.shiftB);
     place<FWD>(P, S, nx, true, last, Dir<FWD>::info(P, last), nk, depth);
   }
   return true;
@@ -954,10 +964,17 @@ __device__ __forceinline__ void gen_body(const Problem &P, const SearchArgs &S, 
                                          unsigned bid, unsigned nb) {
   typedef typename Dir<FWD>::Info Info;
   Scalars *sc = S.sc;
-  if (sc->overflow) return;
   const GenSlot cur = S.G[g % 3];
   const uint32_t hcount = (uint32_t)(cur.hpack & 0xffffffffull);
   const ull U = cur.hpack >> 32;
+  // a heavy list of at most NT keys is searched in LDS
+  __shared__ uint32_t s_ho[NT], s_hk[NT];
+  if (threadIdx.x < hcount) {
+    s_ho[threadIdx.x] = S.hoff[cur.hbase + threadIdx.x];
+    s_hk[threadIdx.x] = S.heavy[cur.hbase + threadIdx.x];
+  }
+  __syncthreads();
+  if (sc->overflow) return;
   NextGen nx;
   nx.slot = &S.G[(g + 1) % 3];
   nx.qbase = cur.qbase + cur.qcount;
@@ -981,12 +998,21 @@ __device__ __forceinline__ void gen_body(const Problem &P, const SearchArgs &S, 
     bool one_unit = false;
     if (i < U) {
       uint32_t a = 0, b = hcount - 1;  // largest a with ho[a] <= i
-      while (a < b) {
-        const uint32_t mid = (a + b + 1) >> 1;
-        if (ho[mid] <= i) a = mid; else b = mid - 1;
+      if (hcount <= NT) {
+        while (a < b) {
+          const uint32_t mid = (a + b + 1) >> 1;
+          if (s_ho[mid] <= i) a = mid; else b = mid - 1;
+        }
+        key = s_hk[a];
+        u0 = (uint32_t)(i - s_ho[a]);
+      } else {
+        while (a < b) {
+          const uint32_t mid = (a + b + 1) >> 1;
+          if (ho[mid] <= i) a = mid; else b = mid - 1;
+        }
+        key = hk[a];
+        u0 = (uint32_t)(i - ho[a]);
       }
-      key = hk[a];
-      u0 = (uint32_t)(i - ho[a]);
       one_unit = true;
     } else {
       key = S.Q[cur.qbase + (uint32_t)(i - U)];

@@ -74,8 +74,8 @@ struct DevGraph {
 //   both marked is reached once by a search in that direction, so it needs
 //   no claim.
 //   chain (views of B, optional): per state, up to CHAIN_STEPS steps of its
-//   single-arc path in the view: {n, l0, s0, l1, s1, ..., l6, s6, 0} as 4
-//   int4, where step i follows the only arc (label l_i, non-epsilon) of the
+//   single-arc path in the view: {n, l0, s0, l1, s1, ..., l10, s10} as
+//   CHAIN_INT4 int4, where step i follows the only arc (label l_i, non-epsilon) of the
 //   state reached after i steps to s_i (an arc-record neighbour field with
 //   NBR_UNIQ), and a step is recorded only while the state it leaves has
 //   exactly one arc in the view (in out-views: and is not accepting).
@@ -98,7 +98,8 @@ struct View {
   const int4 *chain;
 };
 
-constexpr int CHAIN_STEPS = 7;
+constexpr int CHAIN_STEPS = 11;
+constexpr int CHAIN_INT4 = (1 + 2 * CHAIN_STEPS + 3) / 4;  // int4 per chain record
 
 constexpr uint32_t FLAG_ACCEPT = 1u, FLAG_EPS_OUT = 2u, FLAG_START = 4u, FLAG_UNIQ = 8u;
 constexpr int32_t NBR_MASK = 0x3fffffff;            // state ids < 2^30
