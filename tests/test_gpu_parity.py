@@ -191,6 +191,39 @@ def test_chain_jump_conditions(comp, seed):
     assert not fsthelp.check_invariants(A, B, got)
 
 
+def _renumber(g, perm):
+    """The same graph with state s renamed perm[s] (arcs keep their order
+    within a state)."""
+    perm = np.asarray(perm, dtype=np.int64)
+    arcs = [(int(perm[s]), int(perm[d]), int(i), int(o), float(w))
+            for s, d, i, o, w in zip(g["src"], g["dst"], g["ilabel"], g["olabel"], g["weight"])]
+    return synth.from_arcs(g["num_states"], arcs,
+                           start=[int(perm[v]) for v in np.flatnonzero(g["start"])],
+                           accept=[int(perm[v]) for v in np.flatnonzero(g["accept"])])
+
+
+@pytest.mark.parametrize("mode", ["A shuffled", "A reversed", "B shuffled", "both shuffled"])
+@pytest.mark.parametrize("seed", range(2))
+def test_renumbered_states(comp, mode, seed):
+    """Emissions and lexicon with their states renumbered: chains whose A
+    states are not consecutive (a chain jump's guessed A states miss and
+    the jump looks them up again, or ends early) and word states scattered
+    over the search bitmaps' diagonals.  Same result as the oracle's on the
+    same renumbered inputs."""
+    spec = synth.LexSpec(T=60, C=8, W=300, len_lo=2, len_hi=14)
+    A, B, _ = synth.emissions_lexicon("lexicon-T100-W1000", seed, spec=spec)
+    rng = np.random.default_rng([17, seed])
+    if mode in ("A shuffled", "both shuffled"):
+        A = _renumber(A, rng.permutation(A["num_states"]))
+    if mode == "A reversed":
+        A = _renumber(A, np.arange(A["num_states"])[::-1])
+    if mode in ("B shuffled", "both shuffled"):
+        B = _renumber(B, rng.permutation(B["num_states"]))
+    got, _ = check_pair(comp, A, B, f"renumbered states ({mode}) seed {seed}")
+    assert got["num_arcs"] > 0
+    assert not fsthelp.check_invariants(A, B, got)
+
+
 @pytest.fixture(scope="module")
 def comp_paper_order():
     import torch
