@@ -227,6 +227,7 @@ __device__ double thread_pull(const ScoreArgs &S, int32_t v, const AList &l, boo
 }
 
 // The same value, formed by a whole workgroup (identical bits).
+constexpr int PULL_BATCH = 20;
 template <bool FWD>
 __device__ double block_pull(const ScoreArgs &S, int32_t v, const AList &l, bool init) {
   const double *t = pull_slots(S, l);
@@ -240,8 +241,19 @@ __device__ double block_pull(const ScoreArgs &S, int32_t v, const AList &l, bool
   if (m == -INFINITY || m == INFINITY) return m;
   ull lo = 0, hi = 0;
   if (threadIdx.x == 0 && init) acc_add(lo, hi, exp(0.0 - m));
-#pragma unroll 8
-  for (int32_t j = threadIdx.x; j < l.n; j += NT) acc_add(lo, hi, exp(t[j] - m));
+  // PULL_BATCH terms per thread are loaded before any is used (one round
+  // trip per batch; the sum is exact, so the grouping changes no bit)
+  for (int32_t j0 = 0; j0 < l.n; j0 += PULL_BATCH * NT) {
+    double x[PULL_BATCH];
+#pragma unroll
+    for (int k = 0; k < PULL_BATCH; ++k) {
+      const int32_t j = j0 + k * NT + (int32_t)threadIdx.x;
+      x[k] = j < l.n ? t[j] : 0.0;
+    }
+#pragma unroll
+    for (int k = 0; k < PULL_BATCH; ++k)
+      if (j0 + k * NT + (int32_t)threadIdx.x < l.n) acc_add(lo, hi, exp(x[k] - m));
+  }
   block_sum128(lo, hi);
   return acc_finish(m, lo, hi);
 }
