@@ -62,6 +62,7 @@ struct fst_ctx {
   DevBuf aInOff, aInPerm, aInArc, aInRec, aInLut, bInOff, bInPerm, bInArc, bInRec, bInLut;
   DevBuf vis, coacc, trim, wbase, fq, bq, heavy, hoff, heavy2, hoff2, cnt, btot;
   // score workspace
+  DevBuf s_pg, s_pidx, s_bcnt, s_bscan, s_btotal;  // grouped scatter
   DevBuf s_sc, s_owner, s_extra, s_inref, s_mbeg, s_mlen, s_mcur, s_marc, s_val, s_acc,
       s_mpos;
   // batches: the union of the A graphs, item tables, segment sums
@@ -956,7 +957,8 @@ void fst_ctx_destroy(fst_ctx *c) {
                     &c->aOutW,    &c->bOutLab,  &c->bOutW,   &c->btot,    &c->bOutChain,
                     &c->bInChain, &c->s_sc,     &c->s_owner, &c->s_extra, &c->s_inref,
                     &c->s_mbeg,   &c->s_mlen,   &c->s_mcur,  &c->s_marc,  &c->s_val,
-                    &c->s_acc,    &c->s_mpos,   &c->u_off,   &c->u_src,   &c->u_dst,
+                    &c->s_acc,    &c->s_pg,     &c->s_pidx,  &c->s_bcnt,  &c->s_bscan,
+                    &c->s_btotal, &c->s_mpos,   &c->u_off,   &c->u_src,   &c->u_dst,
                     &c->u_il,     &c->u_ol,     &c->u_w,     &c->u_start, &c->u_accept,
                     &c->u_items,  &c->seg};
   for (DevBuf *b : bufs) release(*b);
@@ -1178,8 +1180,23 @@ int fst_grad_scatter(fst_ctx *c, int64_t n, const float *grad, const int32_t *id
   ScoreScalars *dsc = as<ScoreScalars>(c->s_sc);
   HIP_TRY(hipMemsetAsync(dsc, 0, sizeof(ScoreScalars), s));
   if (m > 0) HIP_TRY(hipMemsetAsync(c->s_acc.p, 0, (size_t)m * 4 * sizeof(unsigned long long), s));
+  // grouping the terms by target range needs 8 bytes per term of workspace;
+  // without it (workspace cap) every term goes to the plain scatter
+  ScatterTemp tmp{}, *tp = nullptr;
+  if (scatter_grouped((long long)n, m)) {
+    const size_t words = scatter_count_words((long long)n, m);
+    if (ensure(c, c->s_pg, (size_t)n * sizeof(float)) == FST_OK &&
+        ensure(c, c->s_pidx, (size_t)n * sizeof(int32_t)) == FST_OK &&
+        ensure(c, c->s_bcnt, words * sizeof(uint32_t)) == FST_OK &&
+        ensure(c, c->s_bscan, scan_temp_bytes(words)) == FST_OK &&
+        ensure(c, c->s_btotal, sizeof(unsigned long long)) == FST_OK) {
+      tmp = ScatterTemp{as<float>(c->s_pg), as<int32_t>(c->s_pidx), as<uint32_t>(c->s_bcnt),
+                        c->s_bscan.p, as<unsigned long long>(c->s_btotal)};
+      tp = &tmp;
+    }
+  }
   if (launch_scatter(grad, idx, (long long)n, m, as<unsigned long long>(c->s_acc), &dsc->absmax,
-                     &dsc->bad, out, s) != hipSuccess) {
+                     &dsc->bad, out, tp, s) != hipSuccess) {
     (void)hipGetLastError();
     return FST_ERR_HIP;
   }

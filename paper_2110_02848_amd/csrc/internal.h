@@ -496,10 +496,25 @@ hipError_t launch_segment_logsum(const double *val, const uint8_t *flag, int32_t
 // grad[e] = scale * exp(alpha[src e] + w(e) + beta[dst e] - *total).
 hipError_t launch_posterior(const ScoreGraph &G, const double *alpha, const double *beta,
                             const double *total, float scale, float *grad, hipStream_t s);
+// Workspace of the grouped scatter: the terms grouped by target range (pg,
+// pidx: n each), the per-workgroup bucket counts (scatter_count_words), scan
+// storage for them and the number of grouped terms.
+struct ScatterTemp {
+  float *pg;
+  int32_t *pidx;
+  uint32_t *cnt;
+  void *scan;
+  unsigned long long *total;
+};
+// Whether launch_scatter groups the terms first (when given a ScatterTemp).
+bool scatter_grouped(long long n, int32_t m);
+size_t scatter_count_words(long long n, int32_t m);
 // out[i] = sum of g[e] over e < n with idx[e] = i; acc (4 m words), *mx and
 // *bad zeroed by the caller; *bad becomes nonzero if an index is out of range.
+// With tmp (may be null) the terms are grouped by target range first when
+// scatter_grouped(n, m).
 hipError_t launch_scatter(const float *g, const int32_t *idx, long long n, int32_t m,
                           unsigned long long *acc, uint32_t *mx, uint32_t *bad, float *out,
-                          hipStream_t s);
+                          const ScatterTemp *tmp, hipStream_t s);
 
 }  // namespace fstc

@@ -850,6 +850,7 @@ __device__ __forceinline__ int scale_exp(uint32_t mbits) {
 // first lane's target adding together.  Integer sums: the order is free.
 constexpr int SC_CHUNK = NT * 32;
 constexpr int SC_BINS = 2048;
+constexpr long long SC_BLOCKS = 2048;  // workgroups of the grouping passes
 
 __device__ __forceinline__ bool scatter_digits(const float *g, const int32_t *idx, long long e,
                                                int32_t m, int ex, int32_t &key, ull &d0,
@@ -871,11 +872,13 @@ __device__ __forceinline__ bool scatter_digits(const float *g, const int32_t *id
   return true;
 }
 
+// n_dev, when given, holds the number of terms instead of n.
 __global__ __launch_bounds__(NT) void k_scatter(const float *g, const int32_t *idx, long long n,
                                                 int32_t m, const uint32_t *mx, ull *acc,
-                                                uint32_t *bad) {
+                                                uint32_t *bad, const ull *n_dev) {
   __shared__ ull s_acc[4 * SC_BINS];
   __shared__ int32_t s_lo[NWAVES], s_hi[NWAVES];
+  if (n_dev) n = (long long)*n_dev;
   const uint32_t mbits = *mx;
   if (mbits == 0 || mbits >= 0x7f800000u) return;  // all zero, or not finite
   const int ex = scale_exp(mbits);
@@ -960,6 +963,75 @@ __global__ __launch_bounds__(NT) void k_scatter(const float *g, const int32_t *i
           if (d1) atomicAdd(a + 1, d1);
         }
       }
+    }
+  }
+}
+
+// Terms whose targets are spread wider than SC_BINS within a chunk are first
+// grouped by target range (bucket = target / SC_BINS): a counting pass and a
+// placing pass, each workgroup over one contiguous share of the terms, with
+// the wavefront's lanes of one bucket taking their places with one LDS
+// atomic.  k_scatter then adds every chunk of the grouped terms in LDS.
+constexpr int SC_BUCKETS = 1024;  // at most this many buckets (m <= 2^21)
+
+// The lanes of a wavefront with want set and the same bucket b: one of them
+// adds their count to h[b] (LDS); each gets the old value plus its rank.
+__device__ __forceinline__ uint32_t wave_bucket_add(uint32_t *h, bool want, int32_t b) {
+  uint32_t pos = 0;
+  ull rem = __ballot(want);
+  while (rem) {
+    const int leader = __ffsll((long long)rem) - 1;
+    const int32_t lb = __shfl(b, leader);
+    const ull same = __ballot(want && b == lb);
+    uint32_t base = 0;
+    if ((int)__lane_id() == leader) base = atomicAdd(h + lb, (uint32_t)__popcll(same));
+    base = __shfl(base, leader);
+    if (want && b == lb) pos = base + (uint32_t)__popcll(same & __lanemask_lt());
+    rem &= ~same;
+  }
+  return pos;
+}
+
+// cnt[b * gridDim.x + block] = terms of the block's share with a target in
+// bucket b (valid targets only).
+__global__ __launch_bounds__(NT) void k_bucket_count(const int32_t *idx, long long n, int32_t m,
+                                                     int32_t nbk, long long per,
+                                                     uint32_t *__restrict__ cnt) {
+  __shared__ uint32_t h[SC_BUCKETS];
+  for (int b = threadIdx.x; b < nbk; b += NT) h[b] = 0;
+  __syncthreads();
+  const long long e0 = (long long)blockIdx.x * per, e1 = e0 + per < n ? e0 + per : n;
+  for (long long base = e0; base < e1; base += NT) {
+    const long long e = base + threadIdx.x;
+    const int32_t i = e < e1 ? idx[e] : -1;
+    const bool want = i >= 0 && i < m;
+    (void)wave_bucket_add(h, want, want ? i / SC_BINS : 0);
+  }
+  __syncthreads();
+  for (int b = threadIdx.x; b < nbk; b += NT) cnt[(size_t)b * gridDim.x + blockIdx.x] = h[b];
+}
+
+// Places every valid term of the block's share at off[bucket * gridDim.x +
+// block] + its rank: pidx / pg grouped by bucket.  Out-of-range targets set
+// *bad.
+__global__ __launch_bounds__(NT) void k_bucket_place(const float *g, const int32_t *idx,
+                                                     long long n, int32_t m, int32_t nbk,
+                                                     long long per, const uint32_t *off,
+                                                     float *__restrict__ pg,
+                                                     int32_t *__restrict__ pidx, uint32_t *bad) {
+  __shared__ uint32_t h[SC_BUCKETS];
+  for (int b = threadIdx.x; b < nbk; b += NT) h[b] = off[(size_t)b * gridDim.x + blockIdx.x];
+  __syncthreads();
+  const long long e0 = (long long)blockIdx.x * per, e1 = e0 + per < n ? e0 + per : n;
+  for (long long base = e0; base < e1; base += NT) {
+    const long long e = base + threadIdx.x;
+    const int32_t i = e < e1 ? idx[e] : -1;
+    if (e < e1 && (i < -1 || i >= m)) atomicOr(bad, 1u);
+    const bool want = i >= 0 && i < m;
+    const uint32_t p = wave_bucket_add(h, want, want ? i / SC_BINS : 0);
+    if (want) {
+      pidx[p] = i;
+      pg[p] = g[e];
     }
   }
 }
@@ -1084,15 +1156,43 @@ hipError_t launch_posterior(const ScoreGraph &G, const double *alpha, const doub
 }
 
 hipError_t launch_scatter(const float *g, const int32_t *idx, long long n, int32_t m, ull *acc,
-                          uint32_t *mx, uint32_t *bad, float *out, hipStream_t s) {
+                          uint32_t *mx, uint32_t *bad, float *out, const ScatterTemp *tmp,
+                          hipStream_t s) {
   if (n > 0) {
     k_absmax<<<grid_for(n / 4 + 1), NT, 0, s>>>(g, n, mx);
-    long long chunks = (n + SC_CHUNK - 1) / SC_CHUNK;
-    k_scatter<<<(unsigned)(chunks < 2048 ? chunks : 2048), NT, 0, s>>>(g, idx, n, m, mx, acc,
-                                                                      bad);
+    const int32_t nbk = (int32_t)((m + SC_BINS - 1) / SC_BINS);
+    if (tmp && scatter_grouped(n, m)) {
+      const long long nblk = (n + 8 * NT - 1) / (8 * NT) < SC_BLOCKS ? (n + 8 * NT - 1) / (8 * NT)
+                                                                     : SC_BLOCKS;
+      const long long per = (n + nblk - 1) / nblk;
+      k_bucket_count<<<(unsigned)nblk, NT, 0, s>>>(idx, n, m, nbk, per, tmp->cnt);
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      e = scan_u32(tmp->cnt, tmp->cnt, (size_t)nbk * nblk, false, tmp->total, tmp->scan, s);
+      if (e != hipSuccess) return e;
+      k_bucket_place<<<(unsigned)nblk, NT, 0, s>>>(g, idx, n, m, nbk, per, tmp->cnt, tmp->pg,
+                                                   tmp->pidx, bad);
+      const long long chunks = (n + SC_CHUNK - 1) / SC_CHUNK;
+      k_scatter<<<(unsigned)(chunks < 2048 ? chunks : 2048), NT, 0, s>>>(
+          tmp->pg, tmp->pidx, n, m, mx, acc, bad, tmp->total);
+    } else {
+      const long long chunks = (n + SC_CHUNK - 1) / SC_CHUNK;
+      k_scatter<<<(unsigned)(chunks < 2048 ? chunks : 2048), NT, 0, s>>>(g, idx, n, m, mx, acc,
+                                                                        bad, nullptr);
+    }
   }
   if (m > 0) k_scatter_final<<<grid_for(m), NT, 0, s>>>(acc, m, mx, out);
   return hipGetLastError();
+}
+
+bool scatter_grouped(long long n, int32_t m) {
+  return m > SC_BINS && (long long)m <= (long long)SC_BUCKETS * SC_BINS && n >= 4 * SC_CHUNK;
+}
+
+size_t scatter_count_words(long long n, int32_t m) {
+  const long long nblk = (n + 8 * NT - 1) / (8 * NT) < SC_BLOCKS ? (n + 8 * NT - 1) / (8 * NT)
+                                                                 : SC_BLOCKS;
+  return (size_t)((m + SC_BINS - 1) / SC_BINS) * (size_t)nblk;
 }
 
 }  // namespace fstc

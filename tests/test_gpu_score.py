@@ -299,6 +299,39 @@ def test_scatter_random(comp, seed):
     check_scatter(comp, g, idx, m, f"random seed {seed}")
 
 
+@pytest.mark.parametrize("m,pattern", [(5000, "random"), (100000, "random"),
+                                       (100000, "runs"), (1 << 21, "random"),
+                                       ((1 << 21) + 1, "random")])
+def test_scatter_wide_targets(comp, m, pattern):
+    """Targets spread wider than one chunk's LDS table: the terms are grouped
+    by target range first (up to 2^21 targets), else added with global
+    atomics; both give the oracle's sums."""
+    rng = np.random.default_rng(m + len(pattern))
+    n = 300000
+    if pattern == "random":
+        idx = rng.integers(-1, m, size=n).astype(np.int32)
+    else:
+        # ascending runs over the whole range, like the provenance of the
+        # arcs of one frame after another
+        idx = (np.arange(n) * 7 % m).astype(np.int32)
+        idx[rng.random(n) < 0.05] = -1
+    g = rng.standard_normal(n).astype(np.float32)
+    check_scatter(comp, g, idx, m, f"wide targets m={m} {pattern}")
+
+
+def test_scatter_wide_targets_bad_index(comp):
+    import torch
+    from paper_2110_02848_amd import gpu
+    n, m = 100000, 10000
+    idx = np.random.default_rng(5).integers(0, m, size=n).astype(np.int32)
+    idx[77777] = m
+    with pytest.raises(gpu.FstError) as e:
+        comp.grad_scatter(torch.ones(n, device="cuda"), torch.from_numpy(idx).cuda(), m)
+    assert e.value.code == gpu.FST_ERR_INVALID_ARG
+    # the context still works
+    check_scatter(comp, np.ones(n, np.float32), np.minimum(idx, m - 1), m, "after a bad index")
+
+
 def test_scatter_edge_cases(comp):
     from paper_2110_02848_amd import gpu
     check_scatter(comp, np.zeros(0, np.float32), np.zeros(0, np.int32), 5, "empty input")
