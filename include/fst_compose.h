@@ -232,7 +232,8 @@ FST_API int fst_compose_kernel_time(const fst_ctx *ctx, int kernel, float *ms, i
 /* Forward and backward scores of G (device arrays of V doubles; either may
  * be NULL to skip that direction) and the total (one device double, the
  * log-sum of alpha over accepting states when alpha is computed, else of
- * beta over start states).  G is validated as in fst_compose_run.  Queued on
+ * beta over start states).  G's structure is validated as in
+ * fst_compose_run (labels are not read: scores do not depend on them).  Queued on
  * `stream`; blocks on small readbacks as the recursion advances.  Returns
  * FST_ERR_CYCLIC (outputs undefined) if G has a cycle.  Weights must be
  * finite (an infinite or NaN weight gives unspecified values, never a

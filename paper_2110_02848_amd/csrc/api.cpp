@@ -252,10 +252,10 @@ int score_readback(fst_ctx *c, hipStream_t s) {
 int score_validate(fst_ctx *c, const DevGraph &d, hipStream_t s) {
   ScoreScalars *dsc = as<ScoreScalars>(c->s_sc);
   HIP_TRY(hipMemsetAsync(dsc, 0, sizeof(ScoreScalars), s));
-  if (d.V > 0) HIP_TRY(launch_validate(d, 0, &dsc->err, &dsc->maxlab, s));
+  // scores read no label: the structure alone is checked
+  if (d.V > 0) HIP_TRY(launch_validate(d, 2, &dsc->err, &dsc->maxlab, s));
   FST_TRY(score_readback(c, s));
-  const uint32_t info_bits = 1u << 16;  // "not in label order": not an error here
-  return (c->h_ssc->err & ~info_bits) ? FST_ERR_INVALID_GRAPH : FST_OK;
+  return c->h_ssc->err ? FST_ERR_INVALID_GRAPH : FST_OK;
 }
 
 int score_bufs(fst_ctx *c, ScoreBufs &b, int32_t V, size_t E) {

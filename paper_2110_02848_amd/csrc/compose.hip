@@ -80,18 +80,19 @@ __global__ __launch_bounds__(NT) void k_validate(DevGraph g, int side, uint32_t 
       }
     }
     if (i < E) {
-      int32_t s = g.src[i], d = g.dst[i], il = g.il[i], ol = g.ol[i];
+      const int32_t s = g.src[i], d = g.dst[i];
       if (d < 0 || d >= V) bits |= ERR_DST;
-      if (il < 0 || ol < 0) bits |= ERR_LABEL;
-      if (s < 0 || s >= V) {
-        bits |= ERR_SRC;
-      } else if (!(g.off[s] <= i && i < g.off[s + 1])) {
-        bits |= ERR_SRC;
-      } else if (i > g.off[s] && (side == 0 ? g.ol[i - 1] : g.il[i - 1]) > (side == 0 ? ol : il)) {
-        bits |= INFO_UNSORTED;  // not an error: the out-view needs a sort
+      const bool src_ok = s >= 0 && s < V && g.off[s] <= i && i < g.off[s + 1];
+      if (!src_ok) bits |= ERR_SRC;
+      if (side != 2) {
+        const int32_t il = g.il[i], ol = g.ol[i];
+        if (il < 0 || ol < 0) bits |= ERR_LABEL;
+        if (src_ok && i > g.off[s] &&
+            (side == 0 ? g.ol[i - 1] : g.il[i - 1]) > (side == 0 ? ol : il))
+          bits |= INFO_UNSORTED;  // not an error: the out-view needs a sort
+        const int32_t lab = side == 0 ? ol : il;
+        if (lab > 0 && (uint32_t)lab > mx) mx = (uint32_t)lab;
       }
-      int32_t lab = side == 0 ? ol : il;
-      if (lab > 0 && (uint32_t)lab > mx) mx = (uint32_t)lab;
     }
   }
   // one atomic per workgroup: same-address atomics serialize

@@ -363,6 +363,10 @@ hipError_t radix_sort(unsigned long long *k0, int32_t *v0, unsigned long long *k
 // ---------------------------------------------------------------------------
 // Host-side launchers (compose.hip)
 // ---------------------------------------------------------------------------
+// Validation of g's structure (offsets, sources, targets, flags) and, for
+// side 0 (A: matched label = olabel) or 1 (B: ilabel), its labels, the
+// largest matched label and whether the arcs are in label order; side 2
+// checks the structure only.
 hipError_t launch_validate(const DevGraph &g, int side, uint32_t *err, uint32_t *maxlab,
                            hipStream_t s);
 // Views are built in two steps.  sort_view: sort the arcs of a view (side
