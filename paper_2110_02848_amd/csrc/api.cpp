@@ -421,12 +421,18 @@ ScoreGraph plain_score_graph(const DevGraph &d) {
 // both advanced by the same kernels; once the forward search has ended, the
 // remaining backward generations expand only accessible keys and run alone.
 // The trim set is the keys both reached.
+// Accepting pairs up to which the concurrent order starts both searches at
+// once.
+constexpr unsigned long long FEW_ACCEPTING_PAIRS = 1024;
+
 int search_concurrent(fst_ctx *c, Problem P, const SearchArgs &SF, const SearchArgs &SB, int g0,
                       hipStream_t s) {
   const KernelTimer t = timer(c, FST_KERNEL_SEARCH_FORWARD);
-  int gf = g0, gb = 0, batch = 16;  // each search numbers its own generations
+  int gf = g0, gb = 0;  // each search numbers its own generations
   bool fdone = false, bdone = false, pause = false;
   for (;;) {
+    // the one search left after the other ends is usually near its end too
+    const int batch = fdone || bdone ? 8 : 16;
     t.begin(s);
     for (int b = 0; b < batch; ++b) {
       if (!fdone && !bdone && !pause) HIP_TRY(launch_generation2(P, SF, SB, gf++, gb++, s));
@@ -488,8 +494,8 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   }
   phase_begin(c, PH_PRE, s);
   HIP_TRY(hipMemsetAsync(d_sc, 0, sizeof(Scalars), s));
-  if (VA) HIP_TRY(launch_validate(dA, 0, &d_sc->errA, &d_sc->maxLabA, s));
-  if (VB) HIP_TRY(launch_validate(dB, 1, &d_sc->errB, &d_sc->maxLabB, s));
+  if (VA) HIP_TRY(launch_validate(dA, 0, &d_sc->errA, &d_sc->maxLabA, s, &d_sc->naccA));
+  if (VB) HIP_TRY(launch_validate(dB, 1, &d_sc->errB, &d_sc->maxLabB, s, &d_sc->naccB));
   FST_TRY(readback(c, s));
   const uint32_t info_bits = 1u << 16;  // validation's "not in label order" note
   if ((c->h_sc->errA & ~info_bits) || (c->h_sc->errB & ~info_bits)) return FST_ERR_INVALID_GRAPH;
@@ -650,7 +656,10 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
     // keys as in the forward-first order).  If it has ended by then, the
     // backward search follows as in that order; otherwise a backward search
     // from every accepting pair runs beside the rest of it.
-    constexpr int FIRST = 4;
+    // With few accepting pairs the backward search starts at once (its
+    // seeds cannot outnumber much of the forward work).
+    const int FIRST =
+        (unsigned long long)c->h_sc->naccA * c->h_sc->naccB <= FEW_ACCEPTING_PAIRS ? 0 : 4;
     P.restrict_fwd = 0;
     P.restrict_bwd = 0;
     phase_begin(c, PH_FWD, s);

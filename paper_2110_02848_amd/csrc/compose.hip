@@ -65,8 +65,8 @@ __device__ __forceinline__ int32_t lb_label(const int2 *a, int32_t lo, int32_t h
 // validation
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(NT) void k_validate(DevGraph g, int side, uint32_t *err,
-                                                 uint32_t *maxlab) {
-  uint32_t bits = 0, mx = 0;
+                                                 uint32_t *maxlab, uint32_t *nacc) {
+  uint32_t bits = 0, mx = 0, na = 0;
   const long long V = g.V, E = g.E;
   const long long n = (V + 1 > E) ? V + 1 : E;
   for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n;
@@ -77,6 +77,7 @@ __global__ __launch_bounds__(NT) void k_validate(DevGraph g, int side, uint32_t 
       if (i < V) {
         if (g.off[i + 1] < g.off[i]) bits |= ERR_OFFSETS;
         if (g.start[i] > 1 || g.accept[i] > 1) bits |= ERR_FLAG;
+        na += g.accept[i] == 1 ? 1u : 0u;
       }
     }
     if (i < E) {
@@ -96,21 +97,25 @@ __global__ __launch_bounds__(NT) void k_validate(DevGraph g, int side, uint32_t 
     }
   }
   // one atomic per workgroup: same-address atomics serialize
-  __shared__ uint32_t s_bits[NWAVES], s_mx[NWAVES];
+  __shared__ uint32_t s_bits[NWAVES], s_mx[NWAVES], s_na[NWAVES];
   bits = wave_or(bits);
   mx = wave_max(mx);
+  na = wave_sum(na);
   if (__lane_id() == 0) {
     s_bits[threadIdx.x / WAVE] = bits;
     s_mx[threadIdx.x / WAVE] = mx;
+    s_na[threadIdx.x / WAVE] = na;
   }
   __syncthreads();
   if (threadIdx.x == 0) {
     for (int w = 1; w < NWAVES; ++w) {
       bits |= s_bits[w];
       mx = s_mx[w] > mx ? s_mx[w] : mx;
+      na += s_na[w];
     }
     if (bits) atomicOr(err, bits);
     if (mx) atomicMax(maxlab, mx);
+    if (na && nacc) atomicAdd(nacc, na);
   }
 }
 
@@ -1693,9 +1698,9 @@ __global__ __launch_bounds__(NT) void k_item_ranges(Problem P, ull nkeys, int32_
 // launchers
 // ---------------------------------------------------------------------------
 hipError_t launch_validate(const DevGraph &g, int side, uint32_t *err, uint32_t *maxlab,
-                           hipStream_t s) {
+                           hipStream_t s, uint32_t *nacc) {
   size_t n = (size_t)(g.V + 1 > g.E ? g.V + 1 : g.E);
-  k_validate<<<grid_for(n, 2048), NT, 0, s>>>(g, side, err, maxlab);
+  k_validate<<<grid_for(n, 2048), NT, 0, s>>>(g, side, err, maxlab, nacc);
   return hipGetLastError();
 }
 

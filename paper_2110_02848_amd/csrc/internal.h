@@ -157,10 +157,12 @@ struct Scalars {
   uint32_t maxLabA, maxLabB;    // max matched label (A olabel, B ilabel)
   uint32_t nEpsStatesA;         // states of A with an epsilon-output arc
   uint32_t tail2;               // accepting keys found by the forward search
+  uint32_t naccA, naccB;        // accepting states of A and B
   uint32_t pad0;
   uint32_t heavy;               // heavy states of C
   uint32_t overflow;            // a capacity was exceeded
   uint32_t gens;                // search generations that had work
+  uint32_t pad2;
   unsigned long long generated; // moves out of accessible keys (on request)
   unsigned long long generated_bwd; // predecessor moves of co-accessible keys (on request)
   unsigned long long naccessible; // keys reached by the forward search
@@ -366,9 +368,9 @@ hipError_t radix_sort(unsigned long long *k0, int32_t *v0, unsigned long long *k
 // Validation of g's structure (offsets, sources, targets, flags) and, for
 // side 0 (A: matched label = olabel) or 1 (B: ilabel), its labels, the
 // largest matched label and whether the arcs are in label order; side 2
-// checks the structure only.
+// checks the structure only.  *nacc (if given) += number of accepting states.
 hipError_t launch_validate(const DevGraph &g, int side, uint32_t *err, uint32_t *maxlab,
-                           hipStream_t s);
+                           hipStream_t s, uint32_t *nacc = nullptr);
 // Views are built in two steps.  sort_view: sort the arcs of a view (side
 // 0: A by olabel, side 1: B by ilabel; by_dst selects in-views, for which
 // `off_tmp` (V+1 words) receives the group offsets; an out-view of an input
