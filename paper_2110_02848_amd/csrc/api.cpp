@@ -1099,8 +1099,8 @@ int fst_compose_fill(fst_ctx *c, const fst_graph_out *C, void *stream) {
                              as<uint32_t>(c->cnt), as<uint32_t>(c->btot), as<uint32_t>(c->bq),
                              c->nheavy, c->narcs, O, s);
   tf.end(s);
-  // per-state fill (offsets, flags, light states' arcs), heavy-state fill (if any)
-  c->klaunches[FST_KERNEL_FILL] = c->timed_run ? 1 + (c->nheavy ? 1 : 0) : 0;
+  // one launch: offsets, flags and arcs of every state
+  c->klaunches[FST_KERNEL_FILL] = c->timed_run ? 1 : 0;
   c->kms[FST_KERNEL_FILL] = 0.f;
   phase_end(c, PH_FILL, s);
   if (e != hipSuccess) {

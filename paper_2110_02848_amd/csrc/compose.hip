@@ -1257,8 +1257,9 @@ __global__ __launch_bounds__(NT) void k_trim(Problem P, uint32_t VA, uint32_t nt
 }
 
 // The chunk of `per` items of this wavefront: [begin, end).
-__device__ __forceinline__ void wave_chunk(ull n, ull per, ull &chunk, ull &begin, ull &end) {
-  chunk = (ull)blockIdx.x * NWAVES + threadIdx.x / WAVE;
+__device__ __forceinline__ void wave_chunk(ull n, ull per, ull &chunk, ull &begin, ull &end,
+                                           unsigned block = blockIdx.x) {
+  chunk = (ull)block * NWAVES + threadIdx.x / WAVE;
   begin = chunk * per;
   end = begin + per < n ? begin + per : n;
   if (begin > end) begin = end;
@@ -1591,14 +1592,14 @@ __global__ __launch_bounds__(NT) void k_count_heavy(Problem P, const uint32_t *_
 
 // One thread per state of C, one contiguous chunk per wavefront: the state's
 // arc offset (chunk base + wavefront scan of the counts), flags and key, and
-// the arcs of a light state (heavy states' arcs are written by k_fill_heavy).
-__global__ __launch_bounds__(NT) void k_fill_light(Problem P, const uint32_t *__restrict__ key_of,
-                                                   uint32_t n, ull per,
-                                                   const uint32_t *__restrict__ cnt,
-                                                   const uint32_t *__restrict__ btot,
-                                                   uint32_t narcs, OutGraph O) {
+// the arcs of a light state (heavy states are written by the workgroups of
+// k_fill set aside for them).
+__device__ __forceinline__ void fill_light(const Problem &P, const uint32_t *__restrict__ key_of,
+                                           uint32_t n, ull per, const uint32_t *__restrict__ cnt,
+                                           const uint32_t *__restrict__ btot,
+                                           const OutGraph &O, unsigned block) {
   ull chunk, begin, end;
-  wave_chunk(n, per, chunk, begin, end);
+  wave_chunk(n, per, chunk, begin, end, block);
   uint32_t run = begin < end ? btot[chunk] : 0u;
   // each iteration loads the next one's count and key (one round trip
   // fewer on the chain of dependent loads)
@@ -1632,19 +1633,37 @@ __global__ __launch_bounds__(NT) void k_fill_light(Problem P, const uint32_t *__
       if (put_arc(O, P, pos, sid, d, il, ol, w, pa, pb)) ++pos;
     });
   }
-  if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) O.arc_offset[n] = (int32_t)narcs;
 }
 
-// Arcs of the heavy states, one workgroup per state, from the offsets
-// k_fill_light wrote.
-__global__ __launch_bounds__(NT) void k_fill_heavy(Problem P, const uint32_t *__restrict__ key_of,
-                                                   const uint32_t *__restrict__ heavy,
-                                                   uint32_t nheavy, OutGraph O) {
-  __shared__ uint32_t s_w[NWAVES];
-  for (uint32_t h = blockIdx.x; h < nheavy; h += gridDim.x) {
-    const uint32_t id = heavy[h];
-    heavy_state<true>(P, id, key_of[id], (uint32_t)O.arc_offset[id], O, s_w);
+// The fill in one launch: workgroups [0, hb) write the heavy states (one
+// workgroup per state, the heavy list strided over them), the others the
+// light chunks, so the heavy states' workgroup loops run under the light
+// work.  A heavy state's first arc position is its chunk's offset plus the
+// counts of the chunk's earlier states, summed by its workgroup.
+__global__ __launch_bounds__(NT) void k_fill(Problem P, const uint32_t *__restrict__ key_of,
+                                             uint32_t n, ull per, const uint32_t *__restrict__ cnt,
+                                             const uint32_t *__restrict__ btot, uint32_t narcs,
+                                             const uint32_t *__restrict__ heavy, uint32_t nheavy,
+                                             unsigned hb, OutGraph O) {
+  if (blockIdx.x < hb) {
+    __shared__ uint32_t s_w[NWAVES];
+    __shared__ uint32_t s_pos;
+    for (uint32_t h = blockIdx.x; h < nheavy; h += hb) {
+      const uint32_t id = heavy[h];
+      const ull chunk = id / per;
+      uint32_t part = 0;
+      for (ull j = chunk * per + threadIdx.x; j < id; j += NT) part += cnt[j];
+      const uint32_t before = block_sum(part, s_w);  // valid in thread 0
+      if (threadIdx.x == 0) s_pos = btot[chunk] + before;
+      __syncthreads();
+      heavy_state<true>(P, id, key_of[id], s_pos, O, s_w);
+      __syncthreads();  // s_pos and s_w are reused by the next heavy state
+    }
+    return;
   }
+  const unsigned block = blockIdx.x - hb;
+  fill_light(P, key_of, n, per, cnt, btot, O, block);
+  if (block == gridDim.x - hb - 1 && threadIdx.x == 0) O.arc_offset[n] = (int32_t)narcs;
 }
 
 // ---------------------------------------------------------------------------
@@ -1869,16 +1888,10 @@ hipError_t launch_count_heavy(const Problem &P, const uint32_t *key_of, const ui
 hipError_t launch_fill(const Problem &P, const uint32_t *key_of, uint32_t nstates, size_t per,
                        const uint32_t *cnt, const uint32_t *btot, const uint32_t *heavy,
                        uint32_t nheavy, uint32_t narcs, const OutGraph &O, hipStream_t s) {
-  hipError_t e;
-  k_fill_light<<<out_grid(nstates, per), NT, 0, s>>>(P, key_of, nstates, per, cnt, btot, narcs,
-                                                     O);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  if (nheavy) {
-    unsigned g = nheavy < 4096 ? nheavy : 4096;
-    k_fill_heavy<<<g, NT, 0, s>>>(P, key_of, heavy, nheavy, O);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-  }
-  return hipSuccess;
+  const unsigned hb = nheavy < 4096 ? nheavy : 4096;
+  k_fill<<<hb + out_grid(nstates, per), NT, 0, s>>>(P, key_of, nstates, per, cnt, btot, narcs,
+                                                    heavy, nheavy, hb, O);
+  return hipGetLastError();
 }
 
 hipError_t launch_union_copy(const DevGraph &a, long long vbase, long long ebase, int32_t *off,

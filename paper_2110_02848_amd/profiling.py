@@ -38,7 +38,7 @@ CSRC = os.path.join(_HERE, "csrc")
 FAMILIES = {
     "search_forward": ("k_gen<true>", "k_gen<false>", "k_gen2("),
     "count": ("k_count(", "k_count_heavy("),
-    "fill": ("k_fill_light(", "k_fill_heavy("),
+    "fill": ("k_fill(", "k_fill_light(", "k_fill_heavy("),
     # scores of the composed graph (bench.py --task score)
     "score_gen": ("k_score_gen<true>", "k_score_gen<false>", "k_score_gen2("),
     "score_structure": ("k_owner(", "k_extra(", "k_merge_index(", "k_merge_place(",
