@@ -9,8 +9,10 @@ namespace {
 
 constexpr int SCAN_ITEMS = 8;
 constexpr size_t SCAN_TILE = (size_t)NT * SCAN_ITEMS;
-constexpr int SORT_ITEMS = 16;
-constexpr size_t SORT_TILE = (size_t)NT * SORT_ITEMS;
+// Elements per thread of a sort tile: small inputs (the views of most
+// operands) take short tiles for more workgroups, large ones long tiles for a
+// smaller digit histogram.
+inline int sort_items(size_t n) { return n <= ((size_t)1 << 20) ? 4 : 16; }
 
 typedef unsigned long long ull;
 
@@ -91,13 +93,13 @@ hipError_t scan_rec(const TI *in, TO *out, size_t n, bool out_last, ull *total, 
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(NT) void k_radix_hist(const ull *__restrict__ k, size_t n,
                                                    int shift, uint32_t *__restrict__ hist,
-                                                   uint32_t nb) {
+                                                   uint32_t nb, int items) {
   __shared__ uint32_t s_h[256];
   s_h[threadIdx.x] = 0;
   __syncthreads();
-  const size_t base = (size_t)blockIdx.x * SORT_TILE;
+  const size_t base = (size_t)blockIdx.x * NT * items;
 #pragma unroll 4
-  for (int r = 0; r < SORT_ITEMS; ++r) {
+  for (int r = 0; r < items; ++r) {
     size_t i = base + (size_t)r * NT + threadIdx.x;
     if (i < n) atomicAdd(&s_h[(uint32_t)(k[i] >> shift) & 255u], 1u);
   }
@@ -114,13 +116,13 @@ __global__ __launch_bounds__(NT) void k_radix_scatter(const ull *__restrict__ ki
                                                       int32_t *__restrict__ vout, size_t n,
                                                       int shift,
                                                       const uint32_t *__restrict__ gofs,
-                                                      uint32_t nb) {
+                                                      uint32_t nb, int items) {
   __shared__ uint32_t s_run[256];
   __shared__ uint32_t s_wc[NWAVES][256];
   const unsigned tid = threadIdx.x, wid = tid / WAVE;
   s_run[tid] = gofs[(size_t)tid * nb + blockIdx.x];
-  const size_t base = (size_t)blockIdx.x * SORT_TILE;
-  for (int r = 0; r < SORT_ITEMS; ++r) {
+  const size_t base = (size_t)blockIdx.x * NT * items;
+  for (int r = 0; r < items; ++r) {
 #pragma unroll
     for (int w = 0; w < NWAVES; ++w) s_wc[w][tid] = 0;
     __syncthreads();
@@ -162,8 +164,13 @@ hipError_t scan_u32(const uint32_t *in, uint32_t *out, size_t n, bool out_last,
                                       reinterpret_cast<char *>(temp), s);
 }
 
+// Enough for every radix_sort of at most n elements (the tile depends on the
+// element count).
 size_t sort_temp_bytes(size_t n) {
-  size_t nb = (n + SORT_TILE - 1) / SORT_TILE;
+  const size_t small = n < ((size_t)1 << 20) ? n : ((size_t)1 << 20);
+  const size_t ts = (size_t)NT * sort_items(small), tl = (size_t)NT * sort_items(n + 1);
+  const size_t nbs = (small + ts - 1) / ts, nbl = (n + tl - 1) / tl;
+  const size_t nb = nbs > nbl ? nbs : nbl;
   size_t nh = 256 * (nb ? nb : 1);
   return align_up(nh * sizeof(uint32_t)) + align_up(sizeof(ull)) + scan_temp_bytes(nh);
 }
@@ -172,7 +179,9 @@ hipError_t radix_sort(unsigned long long *k0, int32_t *v0, unsigned long long *k
                       size_t n, int bits, void *temp, hipStream_t s, bool *in_second) {
   *in_second = false;
   if (n == 0 || bits <= 0) return hipSuccess;
-  const uint32_t nb = (uint32_t)((n + SORT_TILE - 1) / SORT_TILE);
+  const int items = sort_items(n);
+  const size_t tile = (size_t)NT * items;
+  const uint32_t nb = (uint32_t)((n + tile - 1) / tile);
   const size_t nh = (size_t)256 * nb;
   char *t = reinterpret_cast<char *>(temp);
   uint32_t *hist = reinterpret_cast<uint32_t *>(t);
@@ -183,12 +192,12 @@ hipError_t radix_sort(unsigned long long *k0, int32_t *v0, unsigned long long *k
   int passes = (bits + 7) / 8;
   for (int p = 0; p < passes; ++p) {
     int shift = 8 * p;
-    k_radix_hist<<<nb, NT, 0, s>>>(ka, n, shift, hist, nb);
+    k_radix_hist<<<nb, NT, 0, s>>>(ka, n, shift, hist, nb, items);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     e = scan_u32(hist, hist, nh, false, tot, stemp, s);
     if (e != hipSuccess) return e;
-    k_radix_scatter<<<nb, NT, 0, s>>>(ka, va, kb, vb, n, shift, hist, nb);
+    k_radix_scatter<<<nb, NT, 0, s>>>(ka, va, kb, vb, n, shift, hist, nb, items);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     ull *tk = ka; ka = kb; kb = tk;
