@@ -663,9 +663,8 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
     P.restrict_fwd = 0;
     P.restrict_bwd = 0;
     phase_begin(c, PH_FWD, s);
+    // the generation slots are still zero from the run's first memset
     HIP_TRY(hipMemsetAsync(cnts, 0, 8, s));
-    HIP_TRY(hipMemsetAsync(d_sc->G, 0, sizeof(d_sc->G), s));
-    HIP_TRY(hipMemsetAsync(d_sc->G2, 0, sizeof(d_sc->G2), s));
     HIP_TRY(launch_seed_forward(P, S, la, cnts, lb, cnts + 1, s));
     const KernelTimer tf = timer(c, FST_KERNEL_SEARCH_FORWARD);
     tf.begin(s);
