@@ -13,6 +13,7 @@ constexpr size_t SCAN_TILE = (size_t)NT * SCAN_ITEMS;
 // operands) take short tiles for more workgroups, large ones long tiles for a
 // smaller digit histogram.
 inline int sort_items(size_t n) { return n <= ((size_t)1 << 20) ? 4 : 16; }
+constexpr uint32_t SORT_LOCAL = 256;  // tiles up to which a pass needs no scan
 
 typedef unsigned long long ull;
 
@@ -109,18 +110,37 @@ __global__ __launch_bounds__(NT) void k_radix_hist(const ull *__restrict__ k, si
 
 // Stable scatter: inside the tile, elements are ranked in index order.  Each
 // round ranks 256 elements: inside a wavefront by matching the 8 digit bits
-// with ballots, across the four wavefronts through LDS counts.
+// with ballots, across the four wavefronts through LDS counts.  With
+// local_offsets the histogram is the raw per-tile counts (digit-major, at
+// most SORT_LOCAL tiles) and every workgroup forms its own starting offsets
+// (thread d: digit d's counts over all tiles and over the tiles before its
+// own, then a workgroup scan over the digits), which saves the device-wide
+// scan of small sorts.
 __global__ __launch_bounds__(NT) void k_radix_scatter(const ull *__restrict__ kin,
                                                       const int32_t *__restrict__ vin,
                                                       ull *__restrict__ kout,
                                                       int32_t *__restrict__ vout, size_t n,
                                                       int shift,
                                                       const uint32_t *__restrict__ gofs,
-                                                      uint32_t nb, int items) {
+                                                      uint32_t nb, int items, int local_offsets) {
   __shared__ uint32_t s_run[256];
   __shared__ uint32_t s_wc[NWAVES][256];
   const unsigned tid = threadIdx.x, wid = tid / WAVE;
-  s_run[tid] = gofs[(size_t)tid * nb + blockIdx.x];
+  if (local_offsets) {
+    uint32_t total = 0, before = 0;
+    const uint32_t *h = gofs + (size_t)tid * nb;
+#pragma unroll 16
+    for (uint32_t t = 0; t < nb; ++t) {
+      const uint32_t c = h[t];
+      total += c;
+      before += t < blockIdx.x ? c : 0u;
+    }
+    __shared__ uint32_t s_sum[NWAVES];
+    uint32_t all;
+    s_run[tid] = block_excl_scan<uint32_t>(total, s_sum, all) + before;
+  } else {
+    s_run[tid] = gofs[(size_t)tid * nb + blockIdx.x];
+  }
   const size_t base = (size_t)blockIdx.x * NT * items;
   for (int r = 0; r < items; ++r) {
 #pragma unroll
@@ -195,9 +215,12 @@ hipError_t radix_sort(unsigned long long *k0, int32_t *v0, unsigned long long *k
     k_radix_hist<<<nb, NT, 0, s>>>(ka, n, shift, hist, nb, items);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    e = scan_u32(hist, hist, nh, false, tot, stemp, s);
-    if (e != hipSuccess) return e;
-    k_radix_scatter<<<nb, NT, 0, s>>>(ka, va, kb, vb, n, shift, hist, nb, items);
+    const int local = nb <= SORT_LOCAL ? 1 : 0;
+    if (!local) {
+      e = scan_u32(hist, hist, nh, false, tot, stemp, s);
+      if (e != hipSuccess) return e;
+    }
+    k_radix_scatter<<<nb, NT, 0, s>>>(ka, va, kb, vb, n, shift, hist, nb, items, local);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     ull *tk = ka; ka = kb; kb = tk;
