@@ -1690,24 +1690,28 @@ __global__ __launch_bounds__(NT) void k_union_copy(DevGraph a, long long vbase, 
 
 // out[i] = first state of item i in C (the number of trim keys below the
 // item's first key), out[n + 1 + i] = its first arc (the chunk's arc offset
-// plus the counts of the chunk's earlier states), for i <= n.
+// plus the counts of the chunk's earlier states, summed by the workgroup of
+// the item), for i <= n.
 __global__ __launch_bounds__(NT) void k_item_ranges(Problem P, ull nkeys, int32_t n,
                                                     const long long *__restrict__ qa_base,
                                                     const uint32_t *__restrict__ cnt,
                                                     const uint32_t *__restrict__ btot, ull per,
                                                     uint32_t nstates, uint32_t narcs,
                                                     long long *__restrict__ out) {
-  for (int i = blockIdx.x * NT + threadIdx.x; i <= n; i += gridDim.x * NT) {
+  __shared__ ull s_w[NWAVES];
+  for (int i = blockIdx.x; i <= n; i += gridDim.x) {
     const ull K = (ull)qa_base[i] << (P.shiftB + 1);
     const uint32_t st = K >= nkeys ? nstates : new_id(P, (uint32_t)K);
-    uint32_t a = narcs;
-    if (st < nstates) {
-      const ull c = st / per;
-      a = btot[c];
-      for (ull j = c * per; j < st; ++j) a += cnt[j];
+    ull part = 0;
+    const ull c = st / per;
+    if (st < nstates)
+      for (ull j = c * per + threadIdx.x; j < st; j += NT) part += cnt[j];
+    const ull before = block_sum(part, s_w);  // valid in thread 0
+    if (threadIdx.x == 0) {
+      out[i] = st;
+      out[n + 1 + i] = st < nstates ? (long long)(btot[c] + before) : (long long)narcs;
     }
-    out[i] = st;
-    out[n + 1 + i] = a;
+    __syncthreads();  // s_w is reused by the next item
   }
 }
 
@@ -1905,8 +1909,8 @@ hipError_t launch_item_ranges(const Problem &P, unsigned long long nkeys, int32_
                               const long long *qa_base, const uint32_t *cnt,
                               const uint32_t *btot, size_t per, uint32_t nstates,
                               uint32_t narcs, long long *out, hipStream_t s) {
-  k_item_ranges<<<grid_for((size_t)n + 1), NT, 0, s>>>(P, nkeys, n, qa_base, cnt, btot, per,
-                                                      nstates, narcs, out);
+  const unsigned g = (unsigned)(n + 1 < 4096 ? n + 1 : 4096);
+  k_item_ranges<<<g, NT, 0, s>>>(P, nkeys, n, qa_base, cnt, btot, per, nstates, narcs, out);
   return hipGetLastError();
 }
 
