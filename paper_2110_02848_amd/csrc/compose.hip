@@ -234,10 +234,19 @@ __global__ __launch_bounds__(NT) void k_mark_unique(ViewJobs J) {
       // output; in-view: no epsilon in-arc)
       if (me.y != 0) u = false;
       if (o.y != 0 || n > UNIQ_SCAN_MAX) u = false;
-      for (int32_t k = o.x; u && k < o.z; ++k) {
-        const int2 a = b.other_arec[k];
-        if (a.y & NBR_EPS) u = false;                              // source has epsilon output
-        if (k > o.x && b.other_arec[k - 1].x == a.x) u = false;    // repeated label
+      // eight arcs per round, loaded together
+      int32_t last = -1;  // label of the arc before the round (none: -1, labels are >= 0)
+      for (int32_t k0 = o.x; u && k0 < o.z; k0 += 8) {
+        int2 a[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) a[q] = k0 + q < o.z ? b.other_arec[k0 + q] : make_int2(-1, 0);
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+          if (k0 + q < o.z) {
+            if (a[q].y & NBR_EPS) u = false;                       // source has epsilon output
+            if ((q ? a[q - 1].x : last) == a[q].x) u = false;      // repeated label
+          }
+        last = a[7].x;
       }
     }
     if (u) b.srec[2 * v] = make_int4(me.x, me.y, me.z, me.w | (int32_t)FLAG_UNIQ);
