@@ -157,6 +157,8 @@ __global__ __launch_bounds__(NT) void k_split(DevGraph g, int by_dst, const ull 
 }
 
 // off[v] = first sorted position whose group is >= v (v = 0..V).
+// off[v] = first position whose key's group is >= v, for v <= V: by binary
+// search (one thread per group; for graphs with few arcs per state) ...
 __global__ __launch_bounds__(NT) void k_group_offsets(const ull *__restrict__ k, long long n,
                                                       int V, int lab_bits,
                                                       int32_t *__restrict__ off) {
@@ -169,6 +171,21 @@ __global__ __launch_bounds__(NT) void k_group_offsets(const ull *__restrict__ k,
       if (k[mid] < x) lo = mid + 1; else hi = mid;
     }
     off[v] = (int32_t)lo;
+  }
+}
+
+// ... or from adjacent keys (one thread per position; runs of empty groups
+// are short when there are at least a few arcs per four states)
+__global__ __launch_bounds__(NT) void k_group_bounds(const ull *__restrict__ k, long long n,
+                                                     int V, int lab_bits,
+                                                     int32_t *__restrict__ off) {
+  // position i (0 <= i <= n) starts the groups after the group of key i - 1
+  // up to the group of key i (groups past the last key start at n)
+  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i <= n;
+       i += (long long)gridDim.x * NT) {
+    const long long g0 = i > 0 ? (long long)(k[i - 1] >> lab_bits) + 1 : 0;
+    const long long g1 = i < n ? (long long)(k[i] >> lab_bits) : (long long)V;
+    for (long long v = g0; v <= g1; ++v) off[v] = (int32_t)i;
   }
 }
 
@@ -1759,8 +1776,12 @@ hipError_t sort_view(const DevGraph &g, int side, bool by_dst, bool presorted, i
                                        side, perm, olab, w, arec);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (by_dst) {
-      k_group_offsets<<<grid_for((size_t)g.V + 1), NT, 0, s>>>(ks, (long long)E, g.V, lab_bits,
-                                                              off_tmp);
+      if (4 * E >= (size_t)g.V)
+        k_group_bounds<<<grid_for(E + 1, 2048), NT, 0, s>>>(ks, (long long)E, g.V, lab_bits,
+                                                           off_tmp);
+      else
+        k_group_offsets<<<grid_for((size_t)g.V + 1), NT, 0, s>>>(ks, (long long)E, g.V,
+                                                                lab_bits, off_tmp);
       if ((e = hipGetLastError()) != hipSuccess) return e;
     }
   } else if (by_dst) {
