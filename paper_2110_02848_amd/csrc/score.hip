@@ -554,10 +554,15 @@ __global__ __launch_bounds__(NT) void k_score_pending(ScoreArgs S) {
 // in-arc structure
 // ---------------------------------------------------------------------------
 
+// owner[v] = the id of one in-arc of v (whichever store lands last).  Plain
+// aligned 32-bit stores: concurrent ones to one address leave one of the
+// stored values, and the next kernel (after the kernel boundary's release
+// and acquire) reads that one value everywhere.  Device-scope atomic stores
+// and loads would write through and read past the L2 at every access.
 __global__ __launch_bounds__(NT) void k_owner(ScoreGraph G, int32_t *owner) {
   for (long long e = (long long)blockIdx.x * NT + threadIdx.x; e < G.E;
        e += (long long)gridDim.x * NT)
-    __hip_atomic_store(owner + G.dst[e], (int32_t)e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    owner[G.dst[e]] = (int32_t)e;
 }
 
 // Lanes of a wavefront that add to the same counter as the first needy lane
@@ -584,7 +589,7 @@ __global__ __launch_bounds__(NT) void k_extra(ScoreGraph G, const int32_t *owner
     bool need = false;
     if (e < G.E) {
       x = G.dst[e];
-      need = __hip_atomic_load(owner + x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != (int32_t)e;
+      need = owner[x] != (int32_t)e;  // written by k_owner, an earlier kernel
     }
     bool grouped;
     int leader;
