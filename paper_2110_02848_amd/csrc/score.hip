@@ -172,7 +172,7 @@ template <bool FWD>
 __device__ __forceinline__ AList notify_list(const ScoreGraph &G, int32_t v) {
   return FWD ? out_list(G, v) : in_list(G, v);
 }
-// Per-state record of one direction (built by k_score_rec):
+// Per-state record of one direction (built by k_score_init):
 //   x: with one notified arc, the state it reaches; else the first entry of
 //      the notify list (an arc id, or a marc position when REC_IND)
 //   y: flags << 28 | number of notified arcs (saturated at 2^28 - 1)
@@ -486,67 +486,49 @@ __global__ __launch_bounds__(NT) void k_score_gen2(ScoreArgs F, ScoreArgs B, int
   else gen_body<false>(B, g, blockIdx.x - half, half);
 }
 
-// Records of one direction (see REC_*).
+// Every state of one direction in one pass: its record (see REC_*), its
+// pending counter (the number of arcs it pulls from; only states with two or
+// more are counted down), no largest term yet, and, for a state that depends
+// on nothing (forward: no in-arc; backward: no out-arc), its place in
+// generation 0.  Loops run in whole wavefronts (list_ready uses ballots).
 template <bool FWD>
-__global__ __launch_bounds__(NT) void k_score_rec(ScoreArgs S) {
+__global__ __launch_bounds__(NT) void k_score_init(ScoreArgs S) {
   const ScoreGraph &G = S.G;
-  for (long long v = (long long)blockIdx.x * NT + threadIdx.x; v < G.V;
-       v += (long long)gridDim.x * NT) {
-    const AList pl = pull_list<FWD>(G, (int32_t)v), nl = notify_list<FWD>(G, (int32_t)v);
-    uint32_t f = (FWD ? G.start[v] : G.accept[v]) ? REC_INIT : 0u;
-    if (pl.n == 1) f |= REC_SINGLE;
-    if (pl.n > SCORE_LIGHT || nl.n > SCORE_LIGHT) f |= REC_HEAVY;
-    if (nl.ind) f |= REC_IND;
-    int4 r;
-    r.y = (int32_t)(f | (uint32_t)(nl.n < (int32_t)REC_COUNT ? nl.n : (int32_t)REC_COUNT));
-    if (nl.n == 1) {
-      const int32_t e = arc_at(G, nl, 0);
-      r.x = FWD ? G.dst[e] : G.src[e];
-      r.z = __float_as_int(G.w[e]);
-      // slot of the term (see pull_slots); < 2^32 since E < 2^31
-      const bool to_merge = FWD && G.inref[r.x] <= -2;
-      r.w = (int32_t)(uint32_t)(to_merge ? (unsigned long long)G.E + (uint32_t)S.mpos[e]
-                                         : (unsigned long long)e);
-    } else {
-      r.x = nl.beg;
-      r.z = 0;
-      r.w = -1;
-    }
-    S.rec[v] = r;
-  }
-}
-
-// Generation 0: the states that depend on nothing (forward: no in-arc;
-// backward: no out-arc).  Loops run in whole wavefronts (list_ready uses
-// wavefront ballots).
-template <bool FWD>
-__global__ __launch_bounds__(NT) void k_score_seed(ScoreArgs S) {
   ScoreNext nx;
   nx.slot = &S.sc->G[0];
   nx.qbase = 0;
   nx.hbase = 0;
-  const long long V = S.G.V;
-  const long long stride = (long long)gridDim.x * NT;
+  const long long V = G.V, stride = (long long)gridDim.x * NT;
   for (long long base = (long long)blockIdx.x * NT; base < V; base += stride) {
     const long long v = base + threadIdx.x;
     bool want = false;
-    int4 rv = make_int4(0, 0, 0, 0);
+    int4 r = make_int4(0, 0, 0, 0);
     if (v < V) {
-      want = pull_list<FWD>(S.G, (int32_t)v).n == 0;
-      if (want) rv = S.rec[v];
+      const AList pl = pull_list<FWD>(G, (int32_t)v), nl = notify_list<FWD>(G, (int32_t)v);
+      uint32_t f = (FWD ? G.start[v] : G.accept[v]) ? REC_INIT : 0u;
+      if (pl.n == 1) f |= REC_SINGLE;
+      if (pl.n > SCORE_LIGHT || nl.n > SCORE_LIGHT) f |= REC_HEAVY;
+      if (nl.ind) f |= REC_IND;
+      r.y = (int32_t)(f | (uint32_t)(nl.n < (int32_t)REC_COUNT ? nl.n : (int32_t)REC_COUNT));
+      if (nl.n == 1) {
+        const int32_t e = arc_at(G, nl, 0);
+        r.x = FWD ? G.dst[e] : G.src[e];
+        r.z = __float_as_int(G.w[e]);
+        // slot of the term (see pull_slots); < 2^32 since E < 2^31
+        const bool to_merge = FWD && G.inref[r.x] <= -2;
+        r.w = (int32_t)(uint32_t)(to_merge ? (unsigned long long)G.E + (uint32_t)S.mpos[e]
+                                           : (unsigned long long)e);
+      } else {
+        r.x = nl.beg;
+        r.z = 0;
+        r.w = -1;
+      }
+      S.rec[v] = r;
+      S.pend[v] = pl.n;
+      S.mkey[v] = 0ull;
+      want = pl.n == 0;
     }
-    list_ready<FWD>(S, nx, want, (int32_t)v, rv);
-  }
-}
-
-// Pending counter of every state: the number of arcs it pulls from (only
-// states with two or more are counted down); and no largest term yet.
-template <bool FWD>
-__global__ __launch_bounds__(NT) void k_score_pending(ScoreArgs S) {
-  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < S.G.V;
-       i += (long long)gridDim.x * NT) {
-    S.pend[i] = pull_list<FWD>(S.G, (int32_t)i).n;
-    S.mkey[i] = 0ull;
+    list_ready<FWD>(S, nx, want, (int32_t)v, r);
   }
 }
 
@@ -1111,15 +1093,8 @@ hipError_t launch_score_structure(const ScoreGraph &G, int32_t *owner, int32_t *
 }
 
 hipError_t launch_score_seed(const ScoreArgs &S, bool forward, hipStream_t s) {
-  if (forward) {
-    k_score_rec<true><<<grid_for(S.G.V), NT, 0, s>>>(S);
-    k_score_pending<true><<<grid_for(S.G.V), NT, 0, s>>>(S);
-    k_score_seed<true><<<grid_for(S.G.V), NT, 0, s>>>(S);
-  } else {
-    k_score_rec<false><<<grid_for(S.G.V), NT, 0, s>>>(S);
-    k_score_pending<false><<<grid_for(S.G.V), NT, 0, s>>>(S);
-    k_score_seed<false><<<grid_for(S.G.V), NT, 0, s>>>(S);
-  }
+  if (forward) k_score_init<true><<<grid_for(S.G.V), NT, 0, s>>>(S);
+  else k_score_init<false><<<grid_for(S.G.V), NT, 0, s>>>(S);
   return hipGetLastError();
 }
 
