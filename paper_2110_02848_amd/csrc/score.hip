@@ -226,33 +226,26 @@ __device__ double thread_pull(const ScoreArgs &S, int32_t v, const AList &l, boo
   return acc_finish(m, lo, hi);
 }
 
-// The same value, formed by a whole workgroup (identical bits).
+// The same value, formed by a whole workgroup (identical bits), from the n
+// term slots at t whose largest term (with the empty path's 0 when init) is
+// m.
 constexpr int PULL_BATCH = 20;
-template <bool FWD>
-__device__ double block_pull(const ScoreArgs &S, int32_t v, const AList &l, bool init) {
-  const double *t = pull_slots(S, l);
-  double m;
-  if (l.n >= 2) {
-    m = pull_max(S, v, init);
-  } else {
-    m = init ? 0.0 : -INFINITY;
-    if (l.n == 1) m = fmax(m, t[0]);
-  }
+__device__ __forceinline__ double block_logsum(const double *t, int32_t n, double m, bool init) {
   if (m == -INFINITY || m == INFINITY) return m;
   ull lo = 0, hi = 0;
   if (threadIdx.x == 0 && init) acc_add(lo, hi, exp(0.0 - m));
   // PULL_BATCH terms per thread are loaded before any is used (one round
   // trip per batch; the sum is exact, so the grouping changes no bit)
-  for (int32_t j0 = 0; j0 < l.n; j0 += PULL_BATCH * NT) {
+  for (int32_t j0 = 0; j0 < n; j0 += PULL_BATCH * NT) {
     double x[PULL_BATCH];
 #pragma unroll
     for (int k = 0; k < PULL_BATCH; ++k) {
       const int32_t j = j0 + k * NT + (int32_t)threadIdx.x;
-      x[k] = j < l.n ? t[j] : 0.0;
+      x[k] = j < n ? t[j] : 0.0;
     }
 #pragma unroll
     for (int k = 0; k < PULL_BATCH; ++k)
-      if (j0 + k * NT + (int32_t)threadIdx.x < l.n) acc_add(lo, hi, exp(x[k] - m));
+      if (j0 + k * NT + (int32_t)threadIdx.x < n) acc_add(lo, hi, exp(x[k] - m));
   }
   block_sum128(lo, hi);
   return acc_finish(m, lo, hi);
@@ -319,11 +312,12 @@ __device__ void list_ready(const ScoreArgs &S, const ScoreNext &nx, bool want, i
 // Otherwise the term goes to its slot and y's pending counter counts down;
 // the thread that takes it to zero lists y.
 // slot >= 0 is the precomputed slot of arc e's term; -1 derives it from e.
+// ry is y's record.
 template <bool FWD>
 __device__ __forceinline__ void settle(const ScoreArgs &S, const ScoreNext &nx, int32_t y,
-                                       float w, int32_t e, long long slot, double x, int depth,
-                                       int32_t &next, double &next_val, int4 &next_rec) {
-  const int4 ry = S.rec[y];
+                                       const int4 &ry, float w, int32_t e, long long slot,
+                                       double x, int depth, int32_t &next, double &next_val,
+                                       int4 &next_rec) {
   const uint32_t fy = rec_flags(ry);
   const double t = x + (double)w;
   bool ready, walk = false;
@@ -375,38 +369,132 @@ __device__ __forceinline__ void notified(const ScoreGraph &G, const int4 &rv, in
   w = G.w[e];
 }
 
+// A settle left for later: state y (record ry) gets the term x + w over arc
+// e (slot as in settle).  y < 0: none.
+struct Pending {
+  int32_t y, e;
+  int4 ry;
+  float w;
+  long long slot;
+  double x;
+};
+
 // Finishes state v (record rv) with value x, then walks on depth-first.
+// A walk along single arcs stops at the first state it may not walk to.
+// That last settle is left in *defer when given (the caller settles it
+// together with the workgroup's others), else it is done after the loop,
+// when every lane of the wavefront has stopped: walks have different
+// lengths, and the atomics of lanes that stop early would otherwise hold up
+// the lanes still walking.
 template <bool FWD>
-__device__ void walk_from(const ScoreArgs &S, const ScoreNext &nx, int32_t v, int4 rv, double x,
-                          int depth, uint32_t &fin) {
+__device__ __forceinline__ void walk_from(const ScoreArgs &S, const ScoreNext &nx, int32_t v, int4 rv, double x,
+                          int depth, uint32_t &fin, Pending *defer) {
+  Pending p;
+  p.y = -1;
   for (;;) {
     S.val[v] = x;
     ++fin;
     const int32_t nd = rec_count(rv);
+    if (nd == 1) {
+      const int32_t y = rv.x;
+      const int4 ry = S.rec[y];
+      const float w = __int_as_float(rv.z);
+      const uint32_t fy = rec_flags(ry);
+      if ((fy & REC_SINGLE) && !(fy & REC_HEAVY) && depth + 1 < S.chain) {
+        // v was y's only dependency: y's value follows here
+        x = one_term(x + (double)w, (fy & REC_INIT) != 0);
+        v = y;
+        rv = ry;
+        ++depth;
+        continue;
+      }
+      // the slot is the arc id unless it leads to a forward merge, where the
+      // arc id is not needed (a merge's terms go to their precomputed slots)
+      p.slot = (long long)(uint32_t)rv.w;
+      p.e = p.slot < S.G.E ? (int32_t)p.slot : -1;
+      p.y = y;
+      p.ry = ry;
+      p.w = w;
+      p.x = x;
+      break;
+    }
     int32_t next = -1;
     double next_val = 0.0;
     int4 next_rec = rv;
-    if (nd == 1) {
-      // the slot is the arc id unless it leads to a forward merge, where the
-      // arc id is not needed (a merge's terms go to their precomputed slots)
-      const long long slot = (long long)(uint32_t)rv.w;
-      const int32_t e = slot < S.G.E ? (int32_t)slot : -1;
-      settle<FWD>(S, nx, rv.x, __int_as_float(rv.z), e, slot, x, depth, next, next_val,
-                  next_rec);
-    } else {
-      for (int32_t j = 0; j < nd; ++j) {
-        int32_t e, y;
-        float w;
-        notified<FWD>(S.G, rv, j, e, y, w);
-        settle<FWD>(S, nx, y, w, e, -1, x, depth, next, next_val, next_rec);
-      }
+    for (int32_t j = 0; j < nd; ++j) {
+      int32_t e, y;
+      float w;
+      notified<FWD>(S.G, rv, j, e, y, w);
+      settle<FWD>(S, nx, y, S.rec[y], w, e, -1, x, depth, next, next_val, next_rec);
     }
-    if (next < 0) return;
+    if (next < 0) break;
     v = next;
     x = next_val;
     rv = next_rec;
     ++depth;
   }
+  if (defer) {
+    *defer = p;
+  } else if (p.y >= 0) {
+    int32_t none = 0;  // >= 0: no walk from here
+    double nv;
+    int4 nr;
+    settle<FWD>(S, nx, p.y, p.ry, p.w, p.e, p.slot, p.x, depth, none, nv, nr);
+  }
+}
+
+// The pending settles of a workgroup (every thread calls; p.y < 0: none).
+// Terms go to their slots; the arrivals at each merge are first gathered in
+// an LDS table keyed by the merge, so that one atomic per distinct merge
+// and workgroup counts its pending counter down and raises its largest
+// term.  Many walks of a generation end at the same few merges, where
+// atomics of single wavefronts would queue up behind each other.
+template <bool FWD>
+__device__ void settle_block(const ScoreArgs &S, const ScoreNext &nx, const Pending &p) {
+  __shared__ int32_t s_y[NT];
+  __shared__ uint32_t s_n[NT];
+  __shared__ ull s_k[NT];
+  __shared__ uint32_t s_f[NT];
+  const unsigned tid = threadIdx.x;
+  __syncthreads();  // the previous use of the table is over
+  s_y[tid] = -1;
+  s_n[tid] = 0;
+  s_k[tid] = 0;
+  __syncthreads();
+  const uint32_t fy = rec_flags(p.ry);
+  const bool single = p.y >= 0 && (fy & REC_SINGLE);
+  const bool merge = p.y >= 0 && !(fy & REC_SINGLE);
+  if (p.y >= 0) {
+    const double t = p.x + (double)p.w;
+    long long slot = p.slot;
+    if (single) slot = p.e;
+    else if (slot < 0) slot = FWD ? S.G.E + S.mpos[p.e] : (long long)p.e;
+    S.term[slot] = t;
+    if (merge) {
+      uint32_t h = ((uint32_t)p.y * 2654435761u) >> 24;  // NT = 256 buckets
+      for (;;) {
+        const int32_t old = atomicCAS(&s_y[h], -1, p.y);
+        if (old == -1 || old == p.y) break;
+        h = (h + 1) & (NT - 1);
+      }
+      atomicAdd(&s_n[h], 1u);
+      atomicMax(&s_k[h], order_key(t));
+      s_f[h] = fy;  // the same flags from every lane that reaches p.y
+    }
+  }
+  __syncthreads();
+  // a single-dependency state not walked to is ready
+  list_ready<FWD>(S, nx, single, p.y, p.ry);
+  const int32_t y = s_y[tid];
+  bool ready = false;
+  int4 ry = make_int4(0, 0, 0, 0);
+  if (y >= 0) {
+    const int32_t k = (int32_t)s_n[tid];
+    atomicMax(S.mkey + y, s_k[tid]);
+    ready = atomicSub(S.pend + y, k) == k;
+    ry.y = (int32_t)s_f[tid];
+  }
+  list_ready<FWD>(S, nx, ready, y, ry);
 }
 
 // Generation g of one direction on workgroups bid = 0 .. nb - 1: workgroups
@@ -414,8 +502,9 @@ __device__ void walk_from(const ScoreArgs &S, const ScoreNext &nx, int32_t v, in
 template <bool FWD>
 __device__ void gen_body(const ScoreArgs &S, int g, unsigned bid, unsigned nb) {
   ScoreScalars *sc = S.sc;
-  if (sc->overflow) return;
+  const uint32_t ovf = sc->overflow;
   const GenSlot cur = sc->G[g % 3];
+  if (ovf) return;
   const uint32_t hcount = (uint32_t)(cur.hpack & 0xffffffffull);
   const ull HB = cur.hpack >> 32;
   ScoreNext nx;
@@ -433,31 +522,76 @@ __device__ void gen_body(const ScoreArgs &S, int g, unsigned bid, unsigned nb) {
   uint32_t fin = 0;
   const uint32_t *ho = S.hoff + cur.hbase;
   for (ull ub = bid; ub < HB; ub += nb) {
-    uint32_t a = 0, b = hcount - 1;  // largest a with ho[a] <= ub
-    while (a < b) {
-      const uint32_t mid = (a + b + 1) >> 1;
-      if (ho[mid] <= ub) a = mid; else b = mid - 1;
+    // the heavy state of unit ub: entry a, the last one with ho[a] <= ub
+    int32_t v;
+    uint32_t hoa;
+    if (hcount <= (uint32_t)WAVE) {
+      const uint32_t l = __lane_id();
+      const bool in = l < hcount;
+      const uint32_t hl = in ? ho[l] : 0u;
+      const int32_t vl = in ? S.H[cur.hbase + l] : 0;
+      const int a = __popcll(__ballot(in && (ull)hl <= ub)) - 1;  // ho[0] = 0
+      v = __shfl(vl, a);
+      hoa = __shfl(hl, a);
+    } else {
+      uint32_t a = 0, b = hcount - 1;
+      while (a < b) {
+        const uint32_t mid = (a + b + 1) >> 1;
+        if (ho[mid] <= ub) a = mid; else b = mid - 1;
+      }
+      v = S.H[cur.hbase + a];
+      hoa = ho[a];
     }
-    const int32_t v = S.H[cur.hbase + a];
-    const uint32_t part = (uint32_t)(ub - ho[a]);
+    const uint32_t part = (uint32_t)(ub - hoa);
+    const long long j = (long long)part * NT + threadIdx.x;
+    // The loads of the pull and of this thread's notified arc are issued
+    // round by round together: neither needs the other's values, and only
+    // the settle at the end needs the pulled value.
+    const int32_t r_in = S.G.inref[v];
+    const int32_t o0 = S.G.off[v], o1 = S.G.off[v + 1];
+    const ull mk = S.mkey[v];
     const int4 rv = S.rec[v];
-    const double x =
-        block_pull<FWD>(S, v, pull_list<FWD>(S.G, v), (rec_flags(rv) & REC_INIT) != 0);
+    const AList out = AList{o0, o1 - o0, false};
+    int32_t e = -1, y = -1;
+    float w = 0.0f;
+    if (FWD && j < out.n) {
+      e = o0 + (int32_t)j;
+      y = S.G.dst[e];
+      w = S.G.w[e];
+    }
+    AList in = AList{r_in >= 0 ? r_in : 0, r_in >= 0 ? 1 : 0, false};
+    if (r_in <= -2) in = AList{S.G.mbeg[-2 - r_in], S.G.mlen[-2 - r_in], true};
+    if (!FWD && j < in.n) {
+      e = arc_at(S.G, in, (int32_t)j);
+      y = S.G.src[e];
+      w = S.G.w[e];
+    }
+    const AList nl = FWD ? out : in, pl = FWD ? in : out;
+    int4 ry = make_int4(0, 0, 0, 0);
+    if (j < nl.n) ry = S.rec[y];
+    const bool init = (rec_flags(rv) & REC_INIT) != 0;
+    const double *t = pull_slots(S, pl);
+    double m;
+    if (pl.n >= 2) {
+      m = mk ? from_order_key(mk) : -INFINITY;
+      if (init) m = fmax(m, 0.0);
+    } else {
+      m = init ? 0.0 : -INFINITY;
+      if (pl.n == 1) m = fmax(m, t[0]);
+    }
+    const double x = block_logsum(t, pl.n, m, init);
     if (part == 0 && threadIdx.x == 0) {
       S.val[v] = x;
       ++fin;
     }
-    const AList nl = notify_list<FWD>(S.G, v);
-    const long long j = (long long)part * NT + threadIdx.x;
     int32_t next = -1;
     double next_val = 0.0;
     int4 next_rec = rv;
-    if (j < nl.n) {
-      const int32_t e = arc_at(S.G, nl, (int32_t)j);
-      const int32_t y = FWD ? S.G.dst[e] : S.G.src[e];
-      settle<FWD>(S, nx, y, S.G.w[e], e, -1, x, 0, next, next_val, next_rec);
-    }
-    if (next >= 0) walk_from<FWD>(S, nx, next, next_rec, next_val, 1, fin);
+    if (j < nl.n) settle<FWD>(S, nx, y, ry, w, e, -1, x, 0, next, next_val, next_rec);
+    Pending pd;
+    pd.y = -1;
+    if (next >= 0) walk_from<FWD>(S, nx, next, next_rec, next_val, 1, fin, &pd);
+    settle_block<FWD>(S, nx, pd);
   }
   const ull n = cur.qcount;
   for (ull i = (ull)bid * NT + threadIdx.x; i < n; i += (ull)nb * NT) {
@@ -465,7 +599,7 @@ __device__ void gen_body(const ScoreArgs &S, int g, unsigned bid, unsigned nb) {
     const int4 rv = S.rec[v];
     const double x =
         thread_pull<FWD>(S, v, pull_list<FWD>(S.G, v), (rec_flags(rv) & REC_INIT) != 0);
-    walk_from<FWD>(S, nx, v, rv, x, 0, fin);
+    walk_from<FWD>(S, nx, v, rv, x, 0, fin, nullptr);
   }
   // one atomic per wavefront
 #pragma unroll
