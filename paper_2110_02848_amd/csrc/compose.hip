@@ -64,35 +64,77 @@ __device__ __forceinline__ int32_t lb_label(const int2 *a, int32_t lo, int32_t h
 // ---------------------------------------------------------------------------
 // validation
 // ---------------------------------------------------------------------------
+// VAL_ITEMS items per thread and round: the loads of all of them are issued
+// before any check (the source check's offsets depend on the source).
+constexpr int VAL_ITEMS = 8;
+
 __global__ __launch_bounds__(NT) void k_validate(DevGraph g, int side, uint32_t *err,
                                                  uint32_t *maxlab, uint32_t *nacc) {
   uint32_t bits = 0, mx = 0, na = 0;
   const long long V = g.V, E = g.E;
   const long long n = (V + 1 > E) ? V + 1 : E;
-  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n;
-       i += (long long)gridDim.x * NT) {
-    if (i <= V) {
-      if (i == 0 && g.off[0] != 0) bits |= ERR_OFFSETS;
-      if (i == V && g.off[V] != E) bits |= ERR_OFFSETS;
+  const long long tile = (long long)NT * VAL_ITEMS;
+  for (long long base = (long long)blockIdx.x * tile; base < n;
+       base += (long long)gridDim.x * tile) {
+    // states: offsets and flags
+    int32_t oa[VAL_ITEMS], ob[VAL_ITEMS];
+    uint8_t st[VAL_ITEMS], ac[VAL_ITEMS];
+#pragma unroll
+    for (int r = 0; r < VAL_ITEMS; ++r) {
+      const long long i = base + (long long)r * NT + threadIdx.x;
+      oa[r] = ob[r] = 0;
+      st[r] = ac[r] = 0;
+      if (i <= V) oa[r] = g.off[i];
       if (i < V) {
-        if (g.off[i + 1] < g.off[i]) bits |= ERR_OFFSETS;
-        if (g.start[i] > 1 || g.accept[i] > 1) bits |= ERR_FLAG;
-        na += g.accept[i] == 1 ? 1u : 0u;
+        ob[r] = g.off[i + 1];
+        st[r] = g.start[i];
+        ac[r] = g.accept[i];
       }
     }
-    if (i < E) {
-      const int32_t s = g.src[i], d = g.dst[i];
-      if (d < 0 || d >= V) bits |= ERR_DST;
-      const bool src_ok = s >= 0 && s < V && g.off[s] <= i && i < g.off[s + 1];
-      if (!src_ok) bits |= ERR_SRC;
-      if (side != 2) {
-        const int32_t il = g.il[i], ol = g.ol[i];
-        if (il < 0 || ol < 0) bits |= ERR_LABEL;
-        if (src_ok && i > g.off[s] &&
-            (side == 0 ? g.ol[i - 1] : g.il[i - 1]) > (side == 0 ? ol : il))
-          bits |= INFO_UNSORTED;  // not an error: the out-view needs a sort
-        const int32_t lab = side == 0 ? ol : il;
-        if (lab > 0 && (uint32_t)lab > mx) mx = (uint32_t)lab;
+    // arcs: source and target, then the source's offsets
+    int32_t sr[VAL_ITEMS], ds[VAL_ITEMS], s0[VAL_ITEMS], s1[VAL_ITEMS];
+#pragma unroll
+    for (int r = 0; r < VAL_ITEMS; ++r) {
+      const long long i = base + (long long)r * NT + threadIdx.x;
+      sr[r] = -1;
+      ds[r] = 0;
+      if (i < E) {
+        sr[r] = g.src[i];
+        ds[r] = g.dst[i];
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < VAL_ITEMS; ++r) {
+      s0[r] = s1[r] = 0;
+      if (sr[r] >= 0 && sr[r] < V) {
+        s0[r] = g.off[sr[r]];
+        s1[r] = g.off[sr[r] + 1];
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < VAL_ITEMS; ++r) {
+      const long long i = base + (long long)r * NT + threadIdx.x;
+      if (i == 0 && oa[r] != 0) bits |= ERR_OFFSETS;
+      if (i == V && oa[r] != E) bits |= ERR_OFFSETS;
+      if (i < V) {
+        if (ob[r] < oa[r]) bits |= ERR_OFFSETS;
+        if (st[r] > 1 || ac[r] > 1) bits |= ERR_FLAG;
+        na += ac[r] == 1 ? 1u : 0u;
+      }
+      if (i < E) {
+        const int32_t sv = sr[r], d = ds[r];
+        if (d < 0 || d >= V) bits |= ERR_DST;
+        const bool src_ok = sv >= 0 && sv < V && s0[r] <= i && i < s1[r];
+        if (!src_ok) bits |= ERR_SRC;
+        if (side != 2) {
+          const int32_t il = g.il[i], ol = g.ol[i];
+          if (il < 0 || ol < 0) bits |= ERR_LABEL;
+          if (src_ok && i > s0[r] &&
+              (side == 0 ? g.ol[i - 1] : g.il[i - 1]) > (side == 0 ? ol : il))
+            bits |= INFO_UNSORTED;  // not an error: the out-view needs a sort
+          const int32_t lab = side == 0 ? ol : il;
+          if (lab > 0 && (uint32_t)lab > mx) mx = (uint32_t)lab;
+        }
       }
     }
   }
