@@ -1425,15 +1425,19 @@ __device__ __forceinline__ Move single_move(const Problem &P, const Fwd &s) {
   m.d = make_key(da, db, f, P.shiftB);
   m.pa = pa;
   m.pb = pb;
-  const int32_t ia = pa >= 0 ? P.aOut.olab[pa] : 0;
-  const float wa = pa >= 0 ? P.aOut.w[pa] : 0.f;
-  const int32_t ob = pb >= 0 ? P.bOut.olab[pb] : 0;
-  const float wb = pb >= 0 ? P.bOut.w[pb] : 0.f;
+  return m;
+}
+
+// The labels and weight of a single move.
+__device__ __forceinline__ void move_labels(const Problem &P, Move &m) {
+  const int32_t ia = m.pa >= 0 ? P.aOut.olab[m.pa] : 0;
+  const float wa = m.pa >= 0 ? P.aOut.w[m.pa] : 0.f;
+  const int32_t ob = m.pb >= 0 ? P.bOut.olab[m.pb] : 0;
+  const float wb = m.pb >= 0 ? P.bOut.w[m.pb] : 0.f;
   m.il = ia;
   m.ol = ob;
   // epsilon arcs copy their weight (no + 0.0f, which would turn -0.0 into +0.0)
-  m.w = (pa >= 0 && pb >= 0) ? wa + wb : (pa >= 0 ? wa : wb);
-  return m;
+  m.w = (m.pa >= 0 && m.pb >= 0) ? wa + wb : (m.pa >= 0 ? wa : wb);
 }
 
 // Sequential enumeration of a state's moves in canonical order: A-epsilon
@@ -1443,12 +1447,7 @@ __device__ __forceinline__ Move single_move(const Problem &P, const Fwd &s) {
 // vis(target key, ilabel, olabel, weight, position in A's out-view or -1,
 // position in B's out-view or -1).
 template <class Visit>
-__device__ __forceinline__ void enum_light(const Problem &P, const Fwd &s, Visit &&vis) {
-  const Move m = single_move(P, s);
-  if (m.fast) {
-    if (m.has) vis(m.d, m.il, m.ol, m.w, m.pa, m.pb);
-    return;
-  }
+__device__ __forceinline__ void enum_general(const Problem &P, const Fwd &s, Visit &&vis) {
   const uint32_t sh = P.shiftB;
   for (int32_t p = s.aS; p < s.aS + (int32_t)s.eA; ++p)
     vis(make_key(nbr_of(P.aOut.arec[p].y), s.qb, 0u, sh), P.aOut.olab[p], 0, P.aOut.w[p], p, -1);
@@ -1499,6 +1498,19 @@ __device__ __forceinline__ void enum_light(const Problem &P, const Fwd &s, Visit
   }
 }
 
+template <class Visit>
+__device__ __forceinline__ void enum_light(const Problem &P, const Fwd &s, Visit &&vis) {
+  Move m = single_move(P, s);
+  if (m.fast) {
+    if (m.has) {
+      move_labels(P, m);
+      vis(m.d, m.il, m.ol, m.w, m.pa, m.pb);
+    }
+    return;
+  }
+  enum_general(P, s, vis);
+}
+
 // Output of C is written once and not read back here: streaming stores
 // (no allocation in the caches; 7 % faster fill).
 template <class T>
@@ -1526,6 +1538,26 @@ __device__ __forceinline__ bool put_arc(const OutGraph &O, const Problem &P, uin
   if (O.arc_a) out_store(O.arc_a + pos, ida);
   if (O.arc_b) out_store(O.arc_b + pos, idb);
   return true;
+}
+
+// put_arc for a single move: the target's trim word and prefix, the arc ids
+// and the move's labels and weights are all loaded in one round trip.
+__device__ __forceinline__ void put_move(const OutGraph &O, const Problem &P, uint32_t pos,
+                                         uint32_t id, Move m) {
+  const uint32_t dk = m.d;
+  const uint32_t tw = P.trim[dk >> 5], base = P.wbase[dk >> 5];
+  const int32_t ida = O.arc_a && m.pa >= 0 ? P.aOut.perm[m.pa] : -1;
+  const int32_t idb = O.arc_b && m.pb >= 0 ? P.bOut.perm[m.pb] : -1;
+  move_labels(P, m);
+  const uint32_t below = tw & ((1u << (dk & 31u)) - 1u);
+  if (!((tw >> (dk & 31u)) & 1u)) return;
+  out_store(O.src + pos, (int32_t)id);
+  out_store(O.dst + pos, (int32_t)(base + (uint32_t)__popc(below)));
+  out_store(O.il + pos, m.il);
+  out_store(O.ol + pos, m.ol);
+  out_store(O.w + pos, m.w);
+  if (O.arc_a) out_store(O.arc_a + pos, ida);
+  if (O.arc_b) out_store(O.arc_b + pos, idb);
 }
 
 // Workgroup-cooperative canonical enumeration of one heavy state.  Every
@@ -1611,11 +1643,16 @@ __global__ __launch_bounds__(NT) void k_count(Problem P, const uint32_t *__restr
   ull chunk, begin, end;
   wave_chunk(n, per, chunk, begin, end);
   uint32_t sum = 0;
+  // each iteration loads the next one's key (one round trip fewer on the
+  // chain of dependent loads)
+  uint32_t k_next = begin + __lane_id() < end ? key_of[begin + __lane_id()] : 0u;
   for (ull base = begin; base < end; base += WAVE) {
     const ull id = base + __lane_id();
+    const uint32_t key = k_next;
+    if (id + WAVE < end) k_next = key_of[id + WAVE];
     bool hv = false;
     if (id < end) {
-      const Fwd s = fwd_info(P, key_of[id]);
+      const Fwd s = fwd_info(P, key);
       uint32_t c = 0;
       if (out_units(s) > LIGHT_UNITS) {
         hv = true;
@@ -1697,9 +1734,14 @@ __device__ __forceinline__ void fill_light(const Problem &P, const uint32_t *__r
     if (O.key_f) out_store(O.key_f + id, (uint8_t)s.f);
     if (out_units(s) > LIGHT_UNITS) continue;
     const uint32_t sid = (uint32_t)id;
-    enum_light(P, s, [&](uint32_t d, int32_t il, int32_t ol, float w, int32_t pa, int32_t pb) {
-      if (put_arc(O, P, pos, sid, d, il, ol, w, pa, pb)) ++pos;
-    });
+    const Move m = single_move(P, s);
+    if (m.fast) {
+      if (m.has) put_move(O, P, pos, sid, m);
+    } else {
+      enum_general(P, s, [&](uint32_t d, int32_t il, int32_t ol, float w, int32_t pa, int32_t pb) {
+        if (put_arc(O, P, pos, sid, d, il, ol, w, pa, pb)) ++pos;
+      });
+    }
   }
 }
 

@@ -22,7 +22,7 @@ constexpr uint32_t NO_KEY = 0xFFFFFFFFu;
 // multiple of WAVE; at most OUT_CHUNKS chunks), so the arcs a wavefront
 // writes are contiguous and its offsets need only wavefront scans.  Every
 // workgroup covers NWAVES consecutive chunks.
-constexpr size_t OUT_CHUNKS = 32768;
+constexpr size_t OUT_CHUNKS = 262144;
 inline size_t out_chunk(size_t n) {
   size_t per = (n + OUT_CHUNKS - 1) / OUT_CHUNKS;
   per = (per + WAVE - 1) / WAVE * WAVE;
