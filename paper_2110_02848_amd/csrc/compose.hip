@@ -1038,6 +1038,7 @@ __device__ __forceinline__ void gen_body(const Problem &P, const SearchArgs &S, 
                                          unsigned bid, unsigned nb) {
   typedef typename Dir<FWD>::Info Info;
   Scalars *sc = S.sc;
+  const uint32_t ovf = sc->overflow;  // loaded with the slot (one round trip)
   const GenSlot cur = S.G[g % 3];
   const uint32_t hcount = (uint32_t)(cur.hpack & 0xffffffffull);
   const ull U = cur.hpack >> 32;
@@ -1048,7 +1049,7 @@ __device__ __forceinline__ void gen_body(const Problem &P, const SearchArgs &S, 
     s_hk[threadIdx.x] = S.heavy[cur.hbase + threadIdx.x];
   }
   __syncthreads();
-  if (sc->overflow) return;
+  if (ovf) return;
   NextGen nx;
   nx.slot = &S.G[(g + 1) % 3];
   nx.qbase = cur.qbase + cur.qcount;
