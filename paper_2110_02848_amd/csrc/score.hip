@@ -675,10 +675,25 @@ __global__ __launch_bounds__(NT) void k_score_init(ScoreArgs S) {
 // stored values, and the next kernel (after the kernel boundary's release
 // and acquire) reads that one value everywhere.  Device-scope atomic stores
 // and loads would write through and read past the L2 at every access.
+// Structure passes take ST_ITEMS items per thread and round, their loads
+// issued before any store or atomic (which would otherwise make every load
+// wait for the previous item's store).
+constexpr int ST_ITEMS = 8;
+
 __global__ __launch_bounds__(NT) void k_owner(ScoreGraph G, int32_t *owner) {
-  for (long long e = (long long)blockIdx.x * NT + threadIdx.x; e < G.E;
-       e += (long long)gridDim.x * NT)
-    owner[G.dst[e]] = (int32_t)e;
+  const long long stride = (long long)gridDim.x * NT * ST_ITEMS;
+  for (long long e0 = (long long)blockIdx.x * NT * ST_ITEMS + threadIdx.x; e0 < G.E;
+       e0 += stride) {
+    int32_t d[ST_ITEMS];
+#pragma unroll
+    for (int k = 0; k < ST_ITEMS; ++k) {
+      const long long e = e0 + (long long)k * NT;
+      d[k] = e < G.E ? G.dst[e] : -1;
+    }
+#pragma unroll
+    for (int k = 0; k < ST_ITEMS; ++k)
+      if (d[k] >= 0) owner[d[k]] = (int32_t)(e0 + (long long)k * NT);
+  }
 }
 
 // Lanes of a wavefront that add to the same counter as the first needy lane
@@ -698,22 +713,29 @@ __device__ __forceinline__ uint32_t wave_group(bool need, int32_t key, bool &gro
 
 __global__ __launch_bounds__(NT) void k_extra(ScoreGraph G, const int32_t *owner,
                                               int32_t *extra) {
-  const long long stride = (long long)gridDim.x * NT;
-  for (long long base = (long long)blockIdx.x * NT; base < G.E; base += stride) {
-    const long long e = base + threadIdx.x;
-    int32_t x = -1;
-    bool need = false;
-    if (e < G.E) {
-      x = G.dst[e];
-      need = owner[x] != (int32_t)e;  // written by k_owner, an earlier kernel
+  const long long stride = (long long)gridDim.x * NT * ST_ITEMS;
+  for (long long base = (long long)blockIdx.x * NT * ST_ITEMS; base < G.E; base += stride) {
+    int32_t xs[ST_ITEMS], ow[ST_ITEMS];
+#pragma unroll
+    for (int k = 0; k < ST_ITEMS; ++k) {
+      const long long e = base + (long long)k * NT + threadIdx.x;
+      xs[k] = e < G.E ? G.dst[e] : -1;
     }
-    bool grouped;
-    int leader;
-    const uint32_t cnt = wave_group(need, x, grouped, leader);
-    if (grouped) {
-      if ((int)__lane_id() == leader) atomicAdd(extra + x, (int32_t)cnt);
-    } else if (need) {
-      atomicAdd(extra + x, 1);
+#pragma unroll
+    for (int k = 0; k < ST_ITEMS; ++k) ow[k] = xs[k] >= 0 ? owner[xs[k]] : 0;
+#pragma unroll
+    for (int k = 0; k < ST_ITEMS; ++k) {
+      const long long e = base + (long long)k * NT + threadIdx.x;
+      const int32_t x = xs[k];
+      const bool need = x >= 0 && ow[k] != (int32_t)e;  // owner: k_owner, an earlier kernel
+      bool grouped;
+      int leader;
+      const uint32_t cnt = wave_group(need, x, grouped, leader);
+      if (grouped) {
+        if ((int)__lane_id() == leader) atomicAdd(extra + x, (int32_t)cnt);
+      } else if (need) {
+        atomicAdd(extra + x, 1);
+      }
     }
   }
 }
@@ -796,15 +818,20 @@ __global__ __launch_bounds__(NT) void k_merge_place(ScoreGraph G, const int32_t 
     __syncthreads();
     int32_t mi[MP_ITEMS];
     int slot[MP_ITEMS];
+    // the loads of all items first (targets, then their inref)
 #pragma unroll
     for (int j = 0; j < MP_ITEMS; ++j) {
       const long long e = base + (long long)j * NT + threadIdx.x;
-      mi[j] = -1;
+      mi[j] = e < G.E ? G.dst[e] : -1;
+    }
+#pragma unroll
+    for (int j = 0; j < MP_ITEMS; ++j) {
+      const int32_t r = mi[j] >= 0 ? inref[mi[j]] : -1;
+      mi[j] = r <= -2 ? -2 - r : -1;
+    }
+#pragma unroll
+    for (int j = 0; j < MP_ITEMS; ++j) {
       slot[j] = -1;
-      if (e < G.E) {
-        const int32_t r = inref[G.dst[e]];
-        if (r <= -2) mi[j] = -2 - r;
-      }
       if (mi[j] >= 0) {
         slot[j] = mp_slot(s_key, mi[j], true);
         if (slot[j] >= 0) atomicAdd(s_cnt + slot[j], 1);
@@ -930,6 +957,7 @@ __global__ __launch_bounds__(NT) void k_absmax(const float *g, long long n, uint
   uint32_t m = 0;  // |g| orders as its bits
   const long long n4 = ((uintptr_t)g & 15) ? 0 : n / 4;
   const float4 *g4 = reinterpret_cast<const float4 *>(g);
+#pragma unroll 4
   for (long long e = (long long)blockIdx.x * NT + threadIdx.x; e < n4;
        e += (long long)gridDim.x * NT) {
     const float4 q = g4[e];
@@ -972,25 +1000,32 @@ __device__ __forceinline__ int scale_exp(uint32_t mbits) {
 constexpr int SC_CHUNK = NT * 32;
 constexpr int SC_BINS = 2048;
 constexpr long long SC_BLOCKS = 2048;  // workgroups of the grouping passes
+constexpr int SC_ITEMS = 8;  // terms per thread whose loads are issued together
 
-__device__ __forceinline__ bool scatter_digits(const float *g, const int32_t *idx, long long e,
-                                               int32_t m, int ex, int32_t &key, ull &d0,
-                                               ull &d1, uint32_t *bad) {
+// Fixed-point digits of one term (target i, gradient x); i = -1: no term
+// (also the lanes of a batch past the end of the terms).
+__device__ __forceinline__ bool term_digits(int32_t i, float x, int32_t m, int ex, int32_t &key,
+                                            ull &d0, ull &d1, uint32_t *bad) {
   key = -1;
   d0 = d1 = 0;
-  const int32_t i = idx[e];
   if (i < -1 || i >= m) {
     atomicOr(bad, 1u);
     return false;
   }
   if (i < 0) return false;
-  const float x = g[e];
   const ull T = (ull)ldexp(fabs((double)x), 64 - ex);
   if (!T) return false;
   key = 2 * i + (x < 0.f ? 1 : 0);
   d0 = T & 0xffffffffull;
   d1 = T >> 32;
   return true;
+}
+
+__device__ __forceinline__ bool scatter_digits(const float *g, const int32_t *idx, long long e,
+                                               int32_t m, int ex, int32_t &key, ull &d0,
+                                               ull &d1, uint32_t *bad) {
+  const int32_t i = idx[e];
+  return term_digits(i, (i >= 0 && i < m) ? g[e] : 0.f, m, ex, key, d0, d1, bad);
 }
 
 // n_dev, when given, holds the number of terms instead of n.
@@ -1008,12 +1043,19 @@ __global__ __launch_bounds__(NT) void k_scatter(const float *g, const int32_t *i
     const long long end = base + SC_CHUNK < n ? base + SC_CHUNK : n;
     // index range of the chunk
     int32_t lo = 0x7fffffff, hi = -1;
-    for (long long e = base + threadIdx.x; e < end; e += NT) {
-      const int32_t i = idx[e];
-      if (i >= 0 && i < m) {
-        lo = min(lo, i);
-        hi = max(hi, i);
+    for (long long e0 = base + threadIdx.x; e0 < end; e0 += (long long)NT * SC_ITEMS) {
+      int32_t iv[SC_ITEMS];
+#pragma unroll
+      for (int k = 0; k < SC_ITEMS; ++k) {
+        const long long e = e0 + (long long)k * NT;
+        iv[k] = e < end ? idx[e] : -1;
       }
+#pragma unroll
+      for (int k = 0; k < SC_ITEMS; ++k)
+        if (iv[k] >= 0 && iv[k] < m) {
+          lo = min(lo, iv[k]);
+          hi = max(hi, iv[k]);
+        }
     }
 #pragma unroll
     for (int o = WAVE / 2; o > 0; o >>= 1) {
@@ -1045,13 +1087,24 @@ __global__ __launch_bounds__(NT) void k_scatter(const float *g, const int32_t *i
       const int words = 4 * (hi - lo + 1);
       for (int b = threadIdx.x; b < words; b += NT) s_acc[b] = 0ull;
       __syncthreads();
-      for (long long e = base + threadIdx.x; e < end; e += NT) {
-        int32_t key;
-        ull d0, d1;
-        if (scatter_digits(g, idx, e, m, ex, key, d0, d1, bad)) {
-          ull *a = s_acc + 2 * (key - 2 * lo);
-          if (d0) atomicAdd(a, d0);
-          if (d1) atomicAdd(a + 1, d1);
+      for (long long e0 = base + threadIdx.x; e0 < end; e0 += (long long)NT * SC_ITEMS) {
+        int32_t iv[SC_ITEMS];
+        float gv[SC_ITEMS];
+#pragma unroll
+        for (int k = 0; k < SC_ITEMS; ++k) {
+          const long long e = e0 + (long long)k * NT;
+          iv[k] = e < end ? idx[e] : -1;
+          gv[k] = e < end ? g[e] : 0.f;
+        }
+#pragma unroll
+        for (int k = 0; k < SC_ITEMS; ++k) {
+          int32_t key;
+          ull d0, d1;
+          if (term_digits(iv[k], gv[k], m, ex, key, d0, d1, bad)) {
+            ull *a = s_acc + 2 * (key - 2 * lo);
+            if (d0) atomicAdd(a, d0);
+            if (d1) atomicAdd(a + 1, d1);
+          }
         }
       }
       __syncthreads();
@@ -1122,11 +1175,18 @@ __global__ __launch_bounds__(NT) void k_bucket_count(const int32_t *idx, long lo
   for (int b = threadIdx.x; b < nbk; b += NT) h[b] = 0;
   __syncthreads();
   const long long e0 = (long long)blockIdx.x * per, e1 = e0 + per < n ? e0 + per : n;
-  for (long long base = e0; base < e1; base += NT) {
-    const long long e = base + threadIdx.x;
-    const int32_t i = e < e1 ? idx[e] : -1;
-    const bool want = i >= 0 && i < m;
-    (void)wave_bucket_add(h, want, want ? i / SC_BINS : 0);
+  for (long long base = e0; base < e1; base += (long long)NT * SC_ITEMS) {
+    int32_t iv[SC_ITEMS];
+#pragma unroll
+    for (int k = 0; k < SC_ITEMS; ++k) {
+      const long long e = base + (long long)k * NT + threadIdx.x;
+      iv[k] = e < e1 ? idx[e] : -1;
+    }
+#pragma unroll
+    for (int k = 0; k < SC_ITEMS; ++k) {
+      const bool want = iv[k] >= 0 && iv[k] < m;
+      (void)wave_bucket_add(h, want, want ? iv[k] / SC_BINS : 0);
+    }
   }
   __syncthreads();
   for (int b = threadIdx.x; b < nbk; b += NT) cnt[(size_t)b * gridDim.x + blockIdx.x] = h[b];
@@ -1144,15 +1204,25 @@ __global__ __launch_bounds__(NT) void k_bucket_place(const float *g, const int32
   for (int b = threadIdx.x; b < nbk; b += NT) h[b] = off[(size_t)b * gridDim.x + blockIdx.x];
   __syncthreads();
   const long long e0 = (long long)blockIdx.x * per, e1 = e0 + per < n ? e0 + per : n;
-  for (long long base = e0; base < e1; base += NT) {
-    const long long e = base + threadIdx.x;
-    const int32_t i = e < e1 ? idx[e] : -1;
-    if (e < e1 && (i < -1 || i >= m)) atomicOr(bad, 1u);
-    const bool want = i >= 0 && i < m;
-    const uint32_t p = wave_bucket_add(h, want, want ? i / SC_BINS : 0);
-    if (want) {
-      pidx[p] = i;
-      pg[p] = g[e];
+  for (long long base = e0; base < e1; base += (long long)NT * SC_ITEMS) {
+    int32_t iv[SC_ITEMS];
+    float gv[SC_ITEMS];
+#pragma unroll
+    for (int k = 0; k < SC_ITEMS; ++k) {
+      const long long e = base + (long long)k * NT + threadIdx.x;
+      iv[k] = e < e1 ? idx[e] : -1;
+      gv[k] = e < e1 ? g[e] : 0.f;
+    }
+#pragma unroll
+    for (int k = 0; k < SC_ITEMS; ++k) {
+      const int32_t i = iv[k];
+      if (i < -1 || i >= m) atomicOr(bad, 1u);
+      const bool want = i >= 0 && i < m;
+      const uint32_t p = wave_bucket_add(h, want, want ? i / SC_BINS : 0);
+      if (want) {
+        pidx[p] = i;
+        pg[p] = gv[k];
+      }
     }
   }
 }
