@@ -53,6 +53,10 @@ typedef unsigned long long ull;
 
 constexpr int32_t SCORE_LIGHT = 64;  // arcs a single thread pulls or notifies
 constexpr unsigned SCORE_GRID = 1024;
+// Structure passes take ST_ITEMS items per thread and round, their loads
+// issued before any store or atomic (which would otherwise make every load
+// wait for the previous item's store).
+constexpr int ST_ITEMS = 8;
 
 // ---------------------------------------------------------------------------
 // exact log-add
@@ -621,10 +625,12 @@ __global__ __launch_bounds__(NT) void k_score_gen2(ScoreArgs F, ScoreArgs B, int
 }
 
 // Every state of one direction in one pass: its record (see REC_*), its
-// pending counter (the number of arcs it pulls from; only states with two or
-// more are counted down), no largest term yet, and, for a state that depends
-// on nothing (forward: no in-arc; backward: no out-arc), its place in
-// generation 0.  Loops run in whole wavefronts (list_ready uses ballots).
+// pending counter (the number of arcs it pulls from) and no largest term
+// yet, both only for states with two or more (no other state's are read),
+// and, for a state that depends on nothing (forward: no in-arc; backward:
+// no out-arc), its place in generation 0.  ST_ITEMS states per thread and
+// round, each round's loads issued level by level before the stores; the
+// rounds run in whole wavefronts (list_ready uses ballots).
 template <bool FWD>
 __global__ __launch_bounds__(NT) void k_score_init(ScoreArgs S) {
   const ScoreGraph &G = S.G;
@@ -632,37 +638,82 @@ __global__ __launch_bounds__(NT) void k_score_init(ScoreArgs S) {
   nx.slot = &S.sc->G[0];
   nx.qbase = 0;
   nx.hbase = 0;
-  const long long V = G.V, stride = (long long)gridDim.x * NT;
-  for (long long base = (long long)blockIdx.x * NT; base < V; base += stride) {
-    const long long v = base + threadIdx.x;
-    bool want = false;
-    int4 r = make_int4(0, 0, 0, 0);
-    if (v < V) {
-      const AList pl = pull_list<FWD>(G, (int32_t)v), nl = notify_list<FWD>(G, (int32_t)v);
-      uint32_t f = (FWD ? G.start[v] : G.accept[v]) ? REC_INIT : 0u;
-      if (pl.n == 1) f |= REC_SINGLE;
-      if (pl.n > SCORE_LIGHT || nl.n > SCORE_LIGHT) f |= REC_HEAVY;
-      if (nl.ind) f |= REC_IND;
-      r.y = (int32_t)(f | (uint32_t)(nl.n < (int32_t)REC_COUNT ? nl.n : (int32_t)REC_COUNT));
-      if (nl.n == 1) {
-        const int32_t e = arc_at(G, nl, 0);
-        r.x = FWD ? G.dst[e] : G.src[e];
-        r.z = __float_as_int(G.w[e]);
-        // slot of the term (see pull_slots); < 2^32 since E < 2^31
-        const bool to_merge = FWD && G.inref[r.x] <= -2;
-        r.w = (int32_t)(uint32_t)(to_merge ? (unsigned long long)G.E + (uint32_t)S.mpos[e]
-                                           : (unsigned long long)e);
-      } else {
-        r.x = nl.beg;
-        r.z = 0;
-        r.w = -1;
+  const long long V = G.V, stride = (long long)gridDim.x * NT * ST_ITEMS;
+  for (long long base = (long long)blockIdx.x * NT * ST_ITEMS; base < V; base += stride) {
+    int32_t o0[ST_ITEMS], o1[ST_ITEMS], ir[ST_ITEMS];
+    uint8_t fl[ST_ITEMS];
+#pragma unroll
+    for (int k = 0; k < ST_ITEMS; ++k) {
+      const long long v = base + (long long)k * NT + threadIdx.x;
+      o0[k] = o1[k] = 0;
+      ir[k] = -1;
+      fl[k] = 0;
+      if (v < V) {
+        o0[k] = G.off[v];
+        o1[k] = G.off[v + 1];
+        ir[k] = G.inref[v];
+        fl[k] = FWD ? G.start[v] : G.accept[v];
       }
-      S.rec[v] = r;
-      S.pend[v] = pl.n;
-      S.mkey[v] = 0ull;
-      want = pl.n == 0;
     }
-    list_ready<FWD>(S, nx, want, (int32_t)v, r);
+    AList pl[ST_ITEMS], nl[ST_ITEMS];
+#pragma unroll
+    for (int k = 0; k < ST_ITEMS; ++k) {
+      AList in = AList{ir[k] >= 0 ? ir[k] : 0, ir[k] >= 0 ? 1 : 0, false};
+      if (ir[k] <= -2) in = AList{G.mbeg[-2 - ir[k]], G.mlen[-2 - ir[k]], true};
+      const AList out = AList{o0[k], o1[k] - o0[k], false};
+      pl[k] = FWD ? in : out;
+      nl[k] = FWD ? out : in;
+    }
+    // the one notified arc (if so): its id, other end, weight and slot
+    int32_t e[ST_ITEMS], x[ST_ITEMS], wz[ST_ITEMS], mp[ST_ITEMS];
+#pragma unroll
+    for (int k = 0; k < ST_ITEMS; ++k) {
+      e[k] = -1;
+      if (nl[k].n == 1) e[k] = nl[k].ind ? G.marc[nl[k].beg] : nl[k].beg;
+    }
+#pragma unroll
+    for (int k = 0; k < ST_ITEMS; ++k) {
+      x[k] = wz[k] = mp[k] = 0;
+      if (e[k] >= 0) {
+        x[k] = FWD ? G.dst[e[k]] : G.src[e[k]];
+        wz[k] = __float_as_int(G.w[e[k]]);
+        if (FWD) mp[k] = S.mpos[e[k]];
+      }
+    }
+    bool to_merge[ST_ITEMS];
+#pragma unroll
+    for (int k = 0; k < ST_ITEMS; ++k) to_merge[k] = FWD && e[k] >= 0 && G.inref[x[k]] <= -2;
+#pragma unroll
+    for (int k = 0; k < ST_ITEMS; ++k) {
+      const long long v = base + (long long)k * NT + threadIdx.x;
+      bool want = false;
+      int4 r = make_int4(0, 0, 0, 0);
+      if (v < V) {
+        uint32_t f = fl[k] ? REC_INIT : 0u;
+        if (pl[k].n == 1) f |= REC_SINGLE;
+        if (pl[k].n > SCORE_LIGHT || nl[k].n > SCORE_LIGHT) f |= REC_HEAVY;
+        if (nl[k].ind) f |= REC_IND;
+        const int32_t cnt = nl[k].n < (int32_t)REC_COUNT ? nl[k].n : (int32_t)REC_COUNT;
+        r.y = (int32_t)(f | (uint32_t)cnt);
+        if (e[k] >= 0) {
+          r.x = x[k];
+          r.z = wz[k];
+          // slot of the term (see pull_slots); < 2^32 since E < 2^31
+          r.w = (int32_t)(uint32_t)(to_merge[k] ? (ull)G.E + (uint32_t)mp[k] : (ull)e[k]);
+        } else {
+          r.x = nl[k].beg;
+          r.z = 0;
+          r.w = -1;
+        }
+        S.rec[v] = r;
+        if (pl[k].n >= 2) {
+          S.pend[v] = pl[k].n;
+          S.mkey[v] = 0ull;
+        }
+        want = pl[k].n == 0;
+      }
+      list_ready<FWD>(S, nx, want, (int32_t)v, r);
+    }
   }
 }
 
@@ -675,11 +726,6 @@ __global__ __launch_bounds__(NT) void k_score_init(ScoreArgs S) {
 // stored values, and the next kernel (after the kernel boundary's release
 // and acquire) reads that one value everywhere.  Device-scope atomic stores
 // and loads would write through and read past the L2 at every access.
-// Structure passes take ST_ITEMS items per thread and round, their loads
-// issued before any store or atomic (which would otherwise make every load
-// wait for the previous item's store).
-constexpr int ST_ITEMS = 8;
-
 __global__ __launch_bounds__(NT) void k_owner(ScoreGraph G, int32_t *owner) {
   const long long stride = (long long)gridDim.x * NT * ST_ITEMS;
   for (long long e0 = (long long)blockIdx.x * NT * ST_ITEMS + threadIdx.x; e0 < G.E;
