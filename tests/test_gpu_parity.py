@@ -341,6 +341,22 @@ def test_heavy_states(comp):
     assert comp.stats()["heavy_states"] > 0
 
 
+def test_many_heavy_keys_in_one_generation(comp):
+    # the forward search lists 300 keys of 70 units each in one generation,
+    # more than the heavy list a workgroup keeps in LDS
+    rng = np.random.default_rng(5)
+    n, fan = 300, 70
+    arcsA = [(0, 1 + i, 1, 1, float(rng.standard_normal())) for i in range(n)]
+    arcsA += [(1 + i, n + 1, 1, 1 + lab, float(rng.standard_normal()))
+              for i in range(n) for lab in range(fan)]
+    arcsB = [(0, 0, 1 + lab, 1 + lab, float(rng.standard_normal())) for lab in range(fan)]
+    A = synth.from_arcs(n + 2, arcsA, start=[0], accept=[n + 1])
+    B = synth.from_arcs(1, arcsB, start=[0], accept=[0])
+    got, _ = check_pair(comp, A, B, "300 heavy keys in one generation")
+    assert got["num_arcs"] == n + n * fan
+    assert comp.stats()["heavy_states"] > n
+
+
 def test_lexicon_small_many_words(comp):
     spec = synth.LexSpec(T=40, C=8, W=3000, len_lo=1, len_hi=4)
     A, B, meta = synth.emissions_lexicon("lexicon-T100-W1000", 11, spec=spec)

@@ -99,6 +99,29 @@ def test_score_random_dags(comp, name, kw, seed):
     check_scores(comp, synth.random_dag(seed, **kw), f"dag {name} seed {seed}")
 
 
+def _layered_heavy(seed, width, fan):
+    """Start state 0 -> `width` states with `fan` out-arcs each -> `width`
+    merges with `fan` in-arcs each -> one accepting state.  Each middle
+    layer is `width` heavy states listed in one generation, in either
+    direction."""
+    rng = np.random.default_rng(seed)
+    L1 = [1 + i for i in range(width)]
+    L2 = [1 + width + i for i in range(width)]
+    F = 1 + 2 * width
+    ends = rng.permutation(np.repeat(L2, fan))
+    arcs = [(0, a, 1, 1, float(rng.standard_normal())) for a in L1]
+    arcs += [(a, int(ends[k * fan + j]), 1, 1, float(rng.standard_normal()))
+             for k, a in enumerate(L1) for j in range(fan)]
+    arcs += [(b, F, 1, 1, float(rng.standard_normal())) for b in L2]
+    return synth.from_arcs(F + 1, arcs, start=[0], accept=[F])
+
+
+@pytest.mark.parametrize("width", [65, 300])
+def test_score_many_heavy_states_in_one_generation(comp, width):
+    # more heavy states than one wavefront's lanes in a generation's list
+    check_scores(comp, _layered_heavy(width, width, 70), f"{width} heavy states per generation")
+
+
 @pytest.mark.parametrize("seed", range(40))
 def test_score_tiny_dags(comp, seed):
     rng = np.random.default_rng(seed)
