@@ -31,6 +31,10 @@
 //     heavy: the next generation gives every NT of its notified arcs a
 //     workgroup, which pulls the value cooperatively; then each thread walks
 //     on from one successor.
+//   * A walk settles the state it stops at only once every lane of its
+//     wavefront has stopped (walks differ in length), and in the workgroups
+//     of heavy states the arrivals at each merge are first gathered in LDS,
+//     so a merge is counted down once per workgroup.
 // Log-add is exact up to its final rounding and does not depend on the order
 // of its terms: the maximum m first, then every exp(x - m), which lies in
 // (0, 1], truncated to a multiple of 2^-64 and added as a 128-bit integer.
