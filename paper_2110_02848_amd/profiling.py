@@ -42,9 +42,10 @@ FAMILIES = {
     # scores of the composed graph (bench.py --task score)
     "score_gen": ("k_score_gen<true>", "k_score_gen<false>", "k_score_gen2("),
     "score_structure": ("k_owner(", "k_extra(", "k_merge_index(", "k_merge_place(",
-                        "k_score_init<", "k_score_rec<", "k_score_pending<", "k_score_seed<"),
+                        "k_score_init<"),
     "posterior": ("k_posterior(",),
-    "scatter": ("k_absmax(", "k_scatter(", "k_scatter_final("),
+    "scatter": ("k_absmax(", "k_bucket_count(", "k_bucket_place(", "k_scatter(",
+                "k_scatter_final("),
 }
 
 
