@@ -479,7 +479,8 @@ __device__ void settle_block(const ScoreArgs &S, const ScoreNext &nx, const Pend
     else if (slot < 0) slot = FWD ? S.G.E + S.mpos[p.e] : (long long)p.e;
     S.term[slot] = t;
     if (merge) {
-      uint32_t h = ((uint32_t)p.y * 2654435761u) >> 24;  // NT = 256 buckets
+      static_assert(NT == 256, "the table hash yields 8 bits");
+      uint32_t h = ((uint32_t)p.y * 2654435761u) >> 24;  // one of NT buckets
       for (;;) {
         const int32_t old = atomicCAS(&s_y[h], -1, p.y);
         if (old == -1 || old == p.y) break;
