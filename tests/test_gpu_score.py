@@ -258,6 +258,30 @@ def test_score_of_composed_lexicon_T100(comp, seed):
     assert abs(float(got["total"].item()) - closed) <= max(tol, 1e-9 * (1 + abs(closed)))
 
 
+@pytest.mark.parametrize("depth", [3, 1])
+def test_score_of_composed_lexicon_short_walks(comp, depth):
+    # walks from the heavy root states stop at the depth budget inside the
+    # words, so the single-dependency states they stop at are settled (and
+    # listed) together with the workgroup's merge arrivals
+    import torch
+    from paper_2110_02848_amd import gpu
+    spec = synth.LexSpec(T=30, C=8, W=400, len_lo=2, len_hi=6)
+    A, B, _ = synth.emissions_lexicon("lexicon-T100-W1000", 3, spec=spec)
+    Cd = _compose(comp, A, B)
+    C = oracle.compose(A, B)
+    ref = oracle.score(C)
+    tol = score_tol(C, ref)
+    comp.set_option(gpu.FST_OPT_CHAIN_DEPTH, depth)
+    try:
+        got = comp.score(Cd)
+        torch.cuda.synchronize()
+    finally:
+        comp.set_option(gpu.FST_OPT_CHAIN_DEPTH, 64)
+    assert_scores_close(got["alpha"].cpu().numpy(), ref["alpha"], tol, f"alpha depth {depth}")
+    assert_scores_close(got["beta"].cpu().numpy(), ref["beta"], tol, f"beta depth {depth}")
+    assert_scores_close([float(got["total"].item())], [ref["total"]], tol, f"total depth {depth}")
+
+
 def check_posterior(comp, Cd, C, ref, tag):
     import torch
     print(f"[posterior] {tag}", flush=True)
