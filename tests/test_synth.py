@@ -91,3 +91,27 @@ def test_random_dag_is_acyclic_and_seeded(seed):
     assert G["start"].sum() >= 1 and G["accept"].sum() >= 1
     indeg = np.bincount(G["dst"], minlength=G["num_states"])
     assert indeg.max() >= 400  # the hubs
+
+
+# SHA-256 (synth.graph_sha256: V, then every array's bytes) of seed 0 of each
+# workload, recorded when the generators were written; a change of a
+# generator (or of numpy's bit streams) changes what the parity tests and the
+# benchmark measure, and fails here first.
+PINNED_SHA256 = {
+    "random-64": ("9739bfcaedaefdd304b5b64f0ead6ccd44feb1ae38fee4e479f225b938c9c771",
+                  "f8333e7fb76986659071e44136119b3c833f80615ebbd64a2012ddfb9e7faa73"),
+    "random-1000": ("5fc3519ed38ad27a493131d7d9d701bc2a572d35c86679d9187503d8ebf45da3",
+                    "2916c55486526601e8c06d6108c00142b770ab6c0170215b72d49e82d3a227fc"),
+    "random-5000": ("62cb352049ccb454f49a18d99ba901d6c7b2ddd5e4fb3a96573cdcfda805c627",
+                    "5c0a5acd59838cc9461997f4a80fccf5c1cf93494ac30e56c4709921eb10431d"),
+    "lexicon-T100-W1000": ("b83bd4cf5ad77223ba3edc9a50dbe3125f6ab6f1032de17a70a77b07eb398a77",
+                           "38864ac5c8c2dc56ccb2d8e752122ff5ae4ce145a476d0481c9a289e42b370ad"),
+    "lexicon-T500-W10000": ("1f8e1478730c7c3eaba6b949ebbd56a6195e524704a1d129145043f3714cc7f4",
+                            "bd2698bacd9e84ac1528c35cb4a55b625f7d30623edd06b21c463c20424371d0"),
+}
+
+
+@pytest.mark.parametrize("name", list(PINNED_SHA256))
+def test_inputs_pinned(name):
+    A, B = synth.workload(name, 0)
+    assert (synth.graph_sha256(A), synth.graph_sha256(B)) == PINNED_SHA256[name]
