@@ -187,6 +187,7 @@ class Composer:
         h = ctypes.c_void_p()
         _check(self._lib.fst_ctx_create(self.device, ctypes.byref(h)), "fst_ctx_create")
         self._h = h
+        self.options = {}  # options set on this context (option -> value)
 
     def close(self):
         if getattr(self, "_h", None):
@@ -201,6 +202,7 @@ class Composer:
 
     def set_option(self, option, value):
         _check(self._lib.fst_ctx_set_option(self._h, option, int(value)), "fst_ctx_set_option")
+        self.options[option] = int(value)
 
     def run(self, A, B, stream=None):
         """Phase 1: search, trim, number and count.  Returns (V_C, E_C)."""
