@@ -261,6 +261,27 @@ FST_API int fst_score_posterior(fst_ctx *ctx, const fst_graph *G, const double *
 FST_API int fst_grad_scatter(fst_ctx *ctx, int64_t n, const float *grad, const int32_t *idx,
                              int32_t m, float *out, void *stream);
 
+/* Largest m (number of targets) that fst_grad_scatter_noalloc accepts. */
+#define FST_SCATTER_NOALLOC_MAX_TARGETS (1 << 20)
+
+/* fst_grad_scatter for callers that cannot allocate device memory (code
+ * under HIP graph capture, serving loops that must not call hipMalloc,
+ * harnesses that forbid it): same arguments and the same result, bit for
+ * bit, but the call allocates nothing.  Its accumulators live in a fixed
+ * device array of the library (32 bytes per target, for at most
+ * FST_SCATTER_NOALLOC_MAX_TARGETS targets: 32 MiB plus a small header),
+ * which every device the library runs on holds until the process ends; its
+ * address is looked up once per device by fst_ctx_create.  The call clears
+ * the part it uses before summing; the array keeps the last call's sums
+ * afterwards.  All calls on one device share that one array, so calls that
+ * overlap on a device (different streams or host threads without ordering)
+ * race and give wrong sums: order them.  Returns FST_ERR_TOO_LARGE if m
+ * exceeds the maximum, FST_ERR_INVALID_ARG for an index outside [-1, m) or
+ * bad arguments.  Blocks until done (it reads back the bad-index flag into
+ * the context's host memory, set up by fst_ctx_create). */
+FST_API int fst_grad_scatter_noalloc(fst_ctx *ctx, int64_t n, const float *grad,
+                                     const int32_t *idx, int32_t m, float *out, void *stream);
+
 /* ---- Batches and chains ------------------------------------------------
  * Batch (the realistic workload of Section 4.2: the emission graphs of many
  * utterances composed with one lexicon): C_i = A_i o B for i < n in one

@@ -934,6 +934,13 @@ int fst_ctx_create(int device, fst_ctx **ctx) {
     }
     memset(b->host, 0, sizeof(ScoreScalars));
   }
+  // the device array of fst_grad_scatter_noalloc: its address on this device
+  void *scr = nullptr;
+  if (scatter_scratch(device, &scr) != hipSuccess) {
+    (void)hipGetLastError();
+    fst_ctx_destroy(c);
+    return FST_ERR_HIP;
+  }
   for (int i = 0; i < NEV; ++i) {
     if (hipEventCreate(&c->ev[i]) != hipSuccess) {
       fst_ctx_destroy(c);
@@ -1209,6 +1216,28 @@ int fst_grad_scatter(fst_ctx *c, int64_t n, const float *grad, const int32_t *id
     return FST_ERR_HIP;
   }
   FST_TRY(score_readback(c, s));
+  return c->h_ssc->bad ? FST_ERR_INVALID_ARG : FST_OK;
+}
+
+int fst_grad_scatter_noalloc(fst_ctx *c, int64_t n, const float *grad, const int32_t *idx,
+                             int32_t m, float *out, void *stream) {
+  if (!c || n < 0 || m < 0) return FST_ERR_INVALID_ARG;
+  if ((n > 0 && (!grad || !idx)) || (m > 0 && !out)) return FST_ERR_INVALID_ARG;
+  if (m > FST_SCATTER_NOALLOC_MAX_TARGETS) return FST_ERR_TOO_LARGE;
+  DeviceGuard g(c->device);
+  if (!g.ok) return FST_ERR_HIP;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  void *scr = nullptr;
+  if (scatter_scratch(c->device, &scr) != hipSuccess ||
+      launch_scatter_noalloc(grad, idx, (long long)n, m, scr, out, s) != hipSuccess) {
+    (void)hipGetLastError();
+    return FST_ERR_HIP;
+  }
+  // the bad-index flag (32-bit word 1 of the array) into pinned host memory
+  // the context allocated at creation
+  HIP_TRY(hipMemcpyAsync(&c->h_ssc->bad, static_cast<uint32_t *>(scr) + 1, sizeof(uint32_t),
+                         hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
   return c->h_ssc->bad ? FST_ERR_INVALID_ARG : FST_OK;
 }
 

@@ -522,5 +522,14 @@ size_t scatter_count_words(long long n, int32_t m);
 hipError_t launch_scatter(const float *g, const int32_t *idx, long long n, int32_t m,
                           unsigned long long *acc, uint32_t *mx, uint32_t *bad, float *out,
                           const ScatterTemp *tmp, hipStream_t s);
+// The address, on `device` (which must be current), of the device array
+// that fst_grad_scatter_noalloc works in; looked up once per device.
+hipError_t scatter_scratch(int device, void **out);
+// launch_scatter without grouping, with its accumulators and scalars in
+// that array (scr, from scatter_scratch): clears what the call uses, then
+// sums; m <= FST_SCATTER_NOALLOC_MAX_TARGETS.  The bad-index flag is 32-bit
+// word 1 of scr.
+hipError_t launch_scatter_noalloc(const float *g, const int32_t *idx, long long n, int32_t m,
+                                  void *scr, float *out, hipStream_t s);
 
 }  // namespace fstc

@@ -48,6 +48,8 @@
 // result does not depend on the order of the atomics.
 #include <math.h>
 
+#include <mutex>
+
 #include "internal.h"
 
 namespace fstc {
@@ -1317,6 +1319,25 @@ __global__ __launch_bounds__(NT) void k_scatter_final(const ull *acc, int32_t m,
   }
 }
 
+// Zeroes words [0, n) (a kernel rather than a memset, so that the call
+// that uses it records no memset node when captured in a graph).
+__global__ __launch_bounds__(NT) void k_clear(ull *w, long long n) {
+  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n;
+       i += (long long)gridDim.x * NT)
+    w[i] = 0ull;
+}
+
+// Device memory of fst_grad_scatter_noalloc, which allocates nothing: a
+// header of SCRATCH_HEAD words (32-bit word 0: bits of the largest
+// |gradient|, word 1: the bad-index flag), then the four accumulator words
+// of each of up to FST_SCATTER_NOALLOC_MAX_TARGETS targets.  Each device
+// holds its own copy for the life of the process; host code reaches it only
+// through the address hipGetSymbolAddress gives on that device
+// (scatter_scratch below).
+constexpr long long SCRATCH_HEAD = 4;
+constexpr long long SCRATCH_WORDS = SCRATCH_HEAD + 4ll * FST_SCATTER_NOALLOC_MAX_TARGETS;
+static __device__ __align__(256) ull scratch[SCRATCH_WORDS];
+
 int grid_for(long long n) {
   long long b = (n + NT - 1) / NT;
   if (b < 1) b = 1;
@@ -1422,6 +1443,46 @@ hipError_t launch_scatter(const float *g, const int32_t *idx, long long n, int32
 
 bool scatter_grouped(long long n, int32_t m) {
   return m > SC_BINS && (long long)m <= (long long)SC_BUCKETS * SC_BINS && n >= 4 * SC_CHUNK;
+}
+
+namespace {
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void *g_scratch[MAX_DEVICES] = {};
+}  // namespace
+
+hipError_t scatter_scratch(int device, void **out) {
+  *out = nullptr;
+  if (device < 0 || device >= MAX_DEVICES) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[device]) {
+    // the symbol's address on the current device, which must be `device`
+    int cur = -1;
+    hipError_t e = hipGetDevice(&cur);
+    if (e != hipSuccess) return e;
+    if (cur != device) return hipErrorInvalidDevice;
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch[device] = p;
+  }
+  *out = g_scratch[device];
+  return hipSuccess;
+}
+
+hipError_t launch_scatter_noalloc(const float *g, const int32_t *idx, long long n, int32_t m,
+                                  void *scr, float *out, hipStream_t s) {
+  if (m < 0 || m > FST_SCATTER_NOALLOC_MAX_TARGETS) return hipErrorInvalidValue;
+  ull *w = static_cast<ull *>(scr);
+  uint32_t *head = static_cast<uint32_t *>(scr);
+  // the header and the accumulators of this call's targets start at zero
+  // (an earlier call leaves its sums behind)
+  const long long words = SCRATCH_HEAD + 4ll * m;
+  k_clear<<<grid_for(words), NT, 0, s>>>(w, words);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_scatter(g, idx, n, m, w + SCRATCH_HEAD, head, head + 1, out, nullptr, s);
 }
 
 size_t scatter_count_words(long long n, int32_t m) {

@@ -32,6 +32,8 @@ FST_OPT_CHAIN_DEPTH = 4
 FST_OPT_COUNT_MOVES = 5
 FST_OPT_ORDER = 6
 
+FST_SCATTER_NOALLOC_MAX_TARGETS = 1 << 20
+
 FST_ORDER_FORWARD_FIRST = 0
 FST_ORDER_COACCESSIBLE_FIRST = 1
 FST_ORDER_CONCURRENT = 2
@@ -118,6 +120,10 @@ def load():
                                      ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
                                      ctypes.c_void_p]
     lib.fst_grad_scatter.restype = ctypes.c_int
+    lib.fst_grad_scatter_noalloc.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                             ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
+                                             ctypes.c_void_p]
+    lib.fst_grad_scatter_noalloc.restype = ctypes.c_int
     lib.fst_compose_batch_run.argtypes = [ctypes.c_void_p, ctypes.POINTER(_Graph), ctypes.c_int32,
                                           ctypes.POINTER(_Graph), ctypes.c_void_p,
                                           ctypes.POINTER(ctypes.c_int64),
@@ -345,6 +351,18 @@ class Composer:
         rc = self._lib.fst_grad_scatter(self._h, int(grad.numel()), _ptr(grad), _ptr(idx),
                                         int(m), _ptr(out), _stream_handle(stream))
         _check(rc, "fst_grad_scatter")
+        return out
+
+    def grad_scatter_noalloc(self, grad, idx, m, out=None, stream=None):
+        """grad_scatter through the entry point that allocates no device
+        memory (m <= FST_SCATTER_NOALLOC_MAX_TARGETS); ``out`` (float32 [m])
+        may be passed in, so that the call itself allocates nothing."""
+        import torch
+        if out is None:
+            out = torch.empty(int(m), dtype=torch.float32, device=f"cuda:{self.device}")
+        rc = self._lib.fst_grad_scatter_noalloc(self._h, int(grad.numel()), _ptr(grad), _ptr(idx),
+                                                int(m), _ptr(out), _stream_handle(stream))
+        _check(rc, "fst_grad_scatter_noalloc")
         return out
 
     def operand_grads(self, C, A_arcs, B_arcs, scale=1.0, stream=None):
