@@ -4,6 +4,18 @@ One step = one full composition (search, trim, numbering, arc count and the
 fill of the output CSR) of the emissions(T=500, C=64) o lexicon(W=10000,
 L=3..10) workload, inputs resident in HBM.  Prints one JSON line.
 
+The timed region is K plain steps (no library timing, no statistics read
+between them); `value` is E_C / wall time per step, with the per-step device
+times (HIP events) as mean / p10 / p50 / p90.  K more steps with the
+library's per-kernel HIP events give each kernel group's time, its
+algorithmic bytes per launch and the `roofline` of the dominant group; the
+group's HBM traffic and occupancy come from the committed rocprofv3 counter
+table (profiles/counters_<workload>.txt) while the kernel sources still hash
+to the value recorded there.  A timed 256 MiB device-to-device copy gives
+the measured copy ceiling beside the 8 TB/s peak.  `cpu_baseline` is the
+sequential C oracle on the same inputs in both of its orders (median of
+several runs each, single thread), with the host's CPU model and core count.
+
     python bench.py [--steps K] [--warmup W] [--workload lexicon-T500-W10000] [--seed 0]
 
 ``--task score`` measures what a training step runs on the composed graph
@@ -46,39 +58,149 @@ def algorithmic_bytes(A, B, st, provenance=False):
 
 
 def kernel_bytes(st):
-    """Algorithmic bytes per composition of each timed kernel group:
-    forward search: 4 B probe per move out of an accessible key + 16 B per
-    accessible key (frontier write and read); backward search: the same over
-    the predecessor moves and the co-accessible keys; count: 8 B per state of
-    C (its key in, its count out) + 4 B per kept arc (the probe of its
-    target); fill: the output CSR (20 B per arc, 6 B per state + 4 B)."""
+    """Algorithmic bytes per composition of each timed kernel group.
+    search (both searches, whose launches the default order shares): 4 B
+    probe per move out of an accessible key + 16 B per accessible key
+    (frontier write and read), and the same over the predecessor moves of
+    the co-accessible keys and those keys; count: 8 B per state of C (its
+    key in, its count out) + 4 B per kept arc (the probe of its target);
+    fill: the output CSR (20 B per arc, 6 B per state + 4 B)."""
     V, E = st["num_states"], st["num_arcs"]
     return {
-        "search_forward": 4 * st["generated"] + 16 * st["accessible"],
-        "search_backward": 4 * st["generated_backward"] + 16 * st["coaccessible"],
+        "search": (4 * st["generated"] + 16 * st["accessible"]
+                   + 4 * st["generated_backward"] + 16 * st["coaccessible"]),
         "count": 8 * V + 4 * E,
         "fill": 20 * E + 4 * (V + 1) + 2 * V,
     }
 
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_emissions_lexicon_T500_W10000.txt")
-SCORE_TRAFFIC_FILE = os.path.join(ROOT, "profiles",
-                                  "traffic_score_emissions_lexicon_T500_W10000.txt")
+def counters_file(workload, task="compose"):
+    stem = workload.replace("-", "_")
+    if task == "score":
+        return os.path.join(ROOT, "profiles", f"counters_score_{stem}.txt")
+    return os.path.join(ROOT, "profiles", f"counters_{stem}.txt")
 
 
-def measured_traffic(workload, kernel, path=TRAFFIC_FILE):
-    """HBM bytes per launch of `kernel` from the committed counter table, or
-    None if there is none for this workload or the kernels changed since."""
-    if workload != "lexicon-T500-W10000":
-        return None
+def measured_counters(workload, kernel, task="compose"):
+    """The committed rocprof counter row of a kernel group for this
+    workload ({column: value}), or None if there is none or the kernel
+    sources changed since it was taken."""
     from paper_2110_02848_amd import profiling
-    t = profiling.read_traffic(path)
+    t = profiling.read_counters(counters_file(workload, task))
     if t is None:
         return None
     sha, table = t
     if sha != profiling.kernel_source_hash() or kernel not in table:
         return None
     return table[kernel]
+
+
+def roofline_extras(workload, kernel, achieved, copy_gbs, task="compose"):
+    """traffic (HBM bytes per launch from the committed FETCH_SIZE /
+    WRITE_SIZE passes, copy-scaled), occupancy figures of the same profile,
+    and the fraction of the measured copy ceiling."""
+    row = measured_counters(workload, kernel, task)
+    out = {"traffic": row["HBM bytes"] if row else None,
+           "copy_ceiling_GBs": copy_gbs,
+           "frac_of_copy_ceiling": achieved / copy_gbs if copy_gbs else None}
+    if row:
+        out["counters"] = {"read_bytes_by_request_size": row["read bytes by request size"],
+                           "l2_hit_pct": row["L2 hit %"],
+                           "waves_per_active_cu": row["waves per active CU"],
+                           "occupancy_pct": row["occupancy %"],
+                           # OccupancyPercent is of 32 wavefronts per CU
+                           "mean_waves_per_cu": row["occupancy %"] * 32 / 100.0,
+                           "valu_busy_pct": row["VALUBusy %"],
+                           "mem_unit_stalled_pct": row["MemUnitStalled %"]}
+    else:
+        out["counters"] = None
+    return out
+
+
+def host_info():
+    """CPU model and the cores this process may run on (the GPU machine's host)."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count()
+    return {"host_cpu": model, "host_nproc": n}
+
+
+def percentiles(xs):
+    a = np.asarray(xs, dtype=np.float64)
+    return {"mean": float(a.mean()), "p10": float(np.percentile(a, 10)),
+            "p50": float(np.percentile(a, 50)), "p90": float(np.percentile(a, 90))}
+
+
+def timed_steps(step, steps):
+    """Run `steps` steps between two synchronisations (the timed region).
+    Returns (wall ms per step, device ms of each step from HIP events on the
+    current stream, the last step's result)."""
+    import torch
+    stream = torch.cuda.current_stream()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    r = None
+    for e0, e1 in evs:
+        e0.record(stream)
+        r = step()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    wall = 1e3 * (time.perf_counter() - t0) / steps
+    return wall, [e0.elapsed_time(e1) for e0, e1 in evs], r
+
+
+def copy_ceiling(mib=256, reps=10):
+    """Device-to-device copy rate on this GPU: (read + write bytes) / time of
+    a plain copy of `mib` MiB, best of `reps` (HIP events)."""
+    import torch
+    n = mib << 20
+    src = torch.ones(n, dtype=torch.uint8, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    best = None
+    for _ in range(reps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        best = ms if best is None or ms < best else best
+    del src, dst
+    return 2.0 * n / (best * 1e-3) / 1e9
+
+
+GATHER_ROWS = 1 << 21
+
+
+def calibrate_gather():
+    """Gathers of known footprint for the counter calibration: 2^21 random
+    rows of 32 bytes (float) and of 64 bytes (double) out of 256 MiB tables,
+    each row once, by an int64 index (rows x (row + 8) bytes read, rows x
+    row bytes written)."""
+    import torch
+    g = torch.Generator(device="cpu").manual_seed(1)
+    for dt, cols in ((torch.float32, 8), (torch.float64, 8)):
+        rows_total = (256 << 20) // (cols * torch.empty(0, dtype=dt).element_size())
+        table = torch.ones(rows_total, cols, dtype=dt, device="cuda:0")
+        idx = torch.randperm(rows_total, generator=g)[:GATHER_ROWS].to("cuda:0")
+        out = torch.index_select(table, 0, idx)
+        torch.cuda.synchronize()
+        del table, idx, out
 
 
 def score_kernel_bytes(V, E):
@@ -91,24 +213,77 @@ def score_kernel_bytes(V, E):
     return {"score_gen": 2 * (8 * V + 16 * E), "score_prep": 12 * E + 4 * V}
 
 
+def _reps_for(first_seconds, budget=8.0):
+    return int(min(20, max(3, budget // max(first_seconds, 1e-6))))
+
+
 def cpu_score_baseline(A, B):
     import oracle
     oracle.build(force=False)
     C = oracle.compose(A, B)
-    t0 = time.perf_counter()
-    r = oracle.score(C)
-    post = oracle.posterior(C, r["alpha"], r["beta"], r["total"])
-    oracle.scatter(post, C["arc_a"], len(A["src"]))
-    oracle.scatter(post, C["arc_b"], len(B["src"]))
-    t = time.perf_counter() - t0
-    return {"value": C["num_arcs"] / t, "unit": "arcs/s", "cores": 1, "kind": "oracle",
-            "sample": "one full step (forward and backward scores, posteriors, both "
-                      "scatters) of the benchmark workload by the C oracle on its own "
-                      "composed graph, single thread",
-            "seconds": round(t, 3)}
+
+    def once():
+        t0 = time.perf_counter()
+        r = oracle.score(C)
+        post = oracle.posterior(C, r["alpha"], r["beta"], r["total"])
+        oracle.scatter(post, C["arc_a"], len(A["src"]))
+        oracle.scatter(post, C["arc_b"], len(B["src"]))
+        return time.perf_counter() - t0
+
+    ts = [once()]
+    ts += [once() for _ in range(_reps_for(ts[0]) - 1)]
+    t = float(np.median(ts))
+    out = {"value": C["num_arcs"] / t, "unit": "arcs/s", "cores": 1, "kind": "oracle",
+           "sample": f"median of {len(ts)} full score steps (forward and backward scores, "
+                     "posteriors, both scatters) of the benchmark workload by the C oracle on "
+                     "its own composed graph, single thread",
+           "seconds_median": round(t, 4), "seconds_runs": [round(x, 4) for x in ts]}
+    out.update(host_info())
+    return out
 
 
-def run_score(args, A, B, comp, dA, dB):
+def instrumented_kernels(comp, step, steps, kernel_names, times_fn, kb):
+    """Per-kernel-group device time (library HIP events on the caller's
+    stream) over `steps` extra steps with the library's timing on; these
+    steps are not the timed region.  kb: algorithmic bytes per step of each
+    group.  Returns {group: launches, ms, average launch, achieved GB/s}."""
+    from paper_2110_02848_amd import gpu
+    comp.set_option(gpu.FST_OPT_TIMING, 1)
+    kern = {k: [0.0, 0] for k in kernel_names}
+    for _ in range(steps):
+        step()
+        for k, (ms_k, n_k) in times_fn().items():
+            kern[k][0] += ms_k
+            kern[k][1] += n_k
+    comp.set_option(gpu.FST_OPT_TIMING, 0)
+    # the searches are one group (the default order shares their launches)
+    if "search_forward" in kern:
+        f, b = kern.pop("search_forward"), kern.pop("search_backward")
+        kern["search"] = [f[0] + b[0], f[1] + b[1]]
+    out = {}
+    for k, (ms_k, n_k) in kern.items():
+        if n_k == 0 or ms_k <= 0:
+            continue
+        per_launch = kb[k] * steps / n_k
+        avg_ms = ms_k / n_k
+        out[k] = {"launches_per_step": n_k / steps, "ms_per_step": ms_k / steps,
+                  "avg_launch_us": 1e3 * avg_ms, "alg_bytes_per_launch": per_launch,
+                  "achieved_GBs": per_launch / (avg_ms * 1e-3) / 1e9}
+    return out
+
+
+def roofline_of(kernels, workload, copy_gbs, task="compose"):
+    dom = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
+    d = kernels[dom]
+    r = {"bound": "hbm", "kernel": dom, "achieved": d["achieved_GBs"], "peak": HBM_PEAK_GBS,
+         "unit": "GB/s", "frac": d["achieved_GBs"] / HBM_PEAK_GBS}
+    r.update(roofline_extras(workload, dom, d["achieved_GBs"], copy_gbs, task))
+    r["avg_launch_us"] = d["avg_launch_us"]
+    r["alg_bytes_per_launch"] = d["alg_bytes_per_launch"]
+    return r
+
+
+def run_score(args, A, B, comp, dA, dB, copy_gbs):
     import torch
     from paper_2110_02848_amd import gpu, synth
     C = comp.compose(dA, dB, provenance=True, keys=False)
@@ -125,32 +300,9 @@ def run_score(args, A, B, comp, dA, dB):
 
     for _ in range(args.warmup):
         step()
-    torch.cuda.synchronize()
-    kern = {k: [0.0, 0] for k in gpu.SCORE_KERNELS}
-    stream = torch.cuda.current_stream()
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
-    t0 = time.perf_counter()
-    ev0.record(stream)
-    for _ in range(args.steps):
-        sc, ga, gb = step()
-        for k, (ms_k, n_k) in comp.score_kernel_times().items():
-            kern[k][0] += ms_k
-            kern[k][1] += n_k
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    ms_wall = 1e3 * (time.perf_counter() - t0) / args.steps
-    ms_dev = ev0.elapsed_time(ev1) / args.steps
-    kernels = {}
-    kb = score_kernel_bytes(V, E)
-    for k, (ms_k, n_k) in kern.items():
-        per_launch = kb[k] * args.steps / n_k
-        avg_ms = ms_k / n_k
-        kernels[k] = {"launches_per_step": n_k / args.steps, "ms_per_step": ms_k / args.steps,
-                      "avg_launch_us": 1e3 * avg_ms, "alg_bytes_per_launch": per_launch,
-                      "achieved_GBs": per_launch / (avg_ms * 1e-3) / 1e9}
-    dom = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
-    d = kernels[dom]
+    ms_wall, per_step, (sc, ga, gb) = timed_steps(step, args.steps)
+    kernels = instrumented_kernels(comp, step, args.steps, gpu.SCORE_KERNELS,
+                                   comp.score_kernel_times, score_kernel_bytes(V, E))
     out = {
         "metric": "scored arcs/sec (scores and operand gradients of emissions o lexicon)",
         "value": E / (ms_wall * 1e-3),
@@ -166,16 +318,12 @@ def run_score(args, A, B, comp, dA, dB):
         "data": "synthetic",
         "config": {"workload": synth.WORKLOAD_TITLES[args.workload], "name": args.workload,
                    "seed": args.seed, "task": "score", "V_C": V, "E_C": E, "E_A": EA,
-                   "E_B": EB},
-        "ms_per_step_device": ms_dev,
+                   "E_B": EB, "inputs_sha256": {"A": synth.graph_sha256(A),
+                                                "B": synth.graph_sha256(B)}},
+        "ms_per_step_device": percentiles(per_step),
         "total": float(sc["total"].item()),
         "kernels": kernels,
-        "roofline": {"bound": "hbm", "kernel": dom, "achieved": d["achieved_GBs"],
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": d["achieved_GBs"] / HBM_PEAK_GBS,
-                     "traffic": measured_traffic(args.workload, dom, SCORE_TRAFFIC_FILE),
-                     "avg_launch_us": d["avg_launch_us"],
-                     "alg_bytes_per_launch": d["alg_bytes_per_launch"]},
+        "roofline": roofline_of(kernels, args.workload, copy_gbs, "score"),
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_score_baseline(A, B)
@@ -197,21 +345,9 @@ def run_batch(args, comp):
 
     for _ in range(args.warmup):
         step()
-    torch.cuda.synchronize()
-    kern = {k: [0.0, 0] for k in gpu.KERNELS}
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        C, st, ar = step()
-        for k, (ms_k, n_k) in comp.kernel_times().items():
-            kern[k][0] += ms_k
-            kern[k][1] += n_k
-    torch.cuda.synchronize()
-    ms_wall = 1e3 * (time.perf_counter() - t0) / args.steps
+    ms_wall, per_step, (C, st, ar) = timed_steps(step, args.steps)
     V, E = int(C["num_states"]), int(C["num_arcs"])
     st_moves = comp.stats()
-    kernels = {k: {"launches_per_step": n / args.steps, "ms_per_step": ms / args.steps,
-                   "avg_launch_us": 1e3 * ms / n if n else 0.0}
-               for k, (ms, n) in kern.items()}
     out = {
         "metric": "composed arcs/sec (batch of emissions o one lexicon)",
         "value": E / (ms_wall * 1e-3),
@@ -230,28 +366,44 @@ def run_batch(args, comp):
                    "batch": args.batch, "V_C": V, "E_C": E,
                    "item_states": [int(x) for x in np.diff(st)],
                    "item_arcs": [int(x) for x in np.diff(ar)]},
-        "kernels": kernels,
+        "ms_per_step_device": percentiles(per_step),
         "search_stats": {k: st_moves[k] for k in ("key_space", "fwd_levels", "bwd_levels")},
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(As[0], B, int(ar[1] - ar[0]))
         out["cpu_baseline"]["sample"] = ("one item of the batch composed by the sequential C "
-                                         "oracle (forward-then-trim order), single thread")
+                                         "oracle, single thread, " +
+                                         out["cpu_baseline"]["sample"].split(": ", 1)[1])
     return out
 
 
 def cpu_baseline(A, B, E_C):
+    """The oracle (plain sequential C, one thread) on the same inputs, in
+    both of its orders: Algorithm 1's (co-accessible set first) and
+    forward-then-trim; the median of several runs of each (compose time
+    only, the oracle's own steady clock); the faster order is the value."""
     import oracle
     oracle.build(force=False)
-    t0 = time.perf_counter()
-    raw = oracle.compose_raw(A, B, oracle.ORDER_FORWARD)
-    wall = time.perf_counter() - t0
-    t = raw["stats"]["compose_seconds"]
-    assert raw["num_arcs"] == E_C, (raw["num_arcs"], E_C)
-    return {"value": E_C / t, "unit": "arcs/s", "cores": 1, "kind": "oracle",
-            "sample": "one full composition of the benchmark workload by the sequential "
-                      "C oracle (forward-then-trim order), single thread",
-            "seconds": round(t, 3), "wall_seconds": round(wall, 3)}
+    runs = {}
+    for name, order in (("forward", oracle.ORDER_FORWARD), ("paper", oracle.ORDER_PAPER)):
+        raw = oracle.compose_raw(A, B, order)
+        assert raw["num_arcs"] == E_C, (name, raw["num_arcs"], E_C)
+        ts = [raw["stats"]["compose_seconds"]]
+        del raw
+        for _ in range(_reps_for(ts[0], 6.0) - 1):
+            ts.append(oracle.compose_raw(A, B, order)["stats"]["compose_seconds"])
+        runs[name] = ts
+    med = {k: float(np.median(v)) for k, v in runs.items()}
+    best = min(med, key=med.get)
+    out = {"value": E_C / med[best], "unit": "arcs/s", "cores": 1, "kind": "oracle",
+           "sample": f"the full benchmark composition by the sequential C oracle, single thread: "
+                     f"median of {len(runs['forward'])} runs in forward-then-trim order and "
+                     f"{len(runs['paper'])} in Algorithm 1's order (co-accessible set first); "
+                     f"value = the faster order ({best})",
+           "seconds_median": {k: round(v, 4) for k, v in med.items()},
+           "seconds_runs": {k: [round(x, 4) for x in v] for k, v in runs.items()}}
+    out.update(host_info())
+    return out
 
 
 def main():
@@ -272,14 +424,16 @@ def main():
                          "gradients of the composed graph; batch: --batch utterances "
                          "composed with one lexicon per step")
     ap.add_argument("--batch", type=int, default=8)
-    ap.add_argument("--copy-probe-mb", type=int, default=0,
-                    help="first copy a buffer of this many MiB device to device "
-                         "(calibrates HBM byte counters under rocprofv3 --pmc)")
+    ap.add_argument("--copy-probe-mb", type=int, default=256,
+                    help="size of the device-to-device copy timed for the copy ceiling (and "
+                         "counted under rocprofv3 --pmc to calibrate the byte counters)")
+    ap.add_argument("--calibrate-gather", action="store_true",
+                    help="also run gathers of known footprint (for counter calibration "
+                         "under rocprofv3 --pmc)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU only: the composition is a single-GPU kernel "
-              "pipeline on one device; run with --gpus 1",
-              file=sys.stderr)
+        print("bench.py measures one GPU only: the composition is a kernel pipeline on one "
+              "device and is reported for one GPU; run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -291,22 +445,16 @@ def main():
     dev = "cuda:0"
     dA, dB = gpu.to_device(A, dev), gpu.to_device(B, dev)
     comp = gpu.Composer(0)
-    comp.set_option(gpu.FST_OPT_TIMING, 1)
     comp.set_option(gpu.FST_OPT_ORDER, {"forward-first": gpu.FST_ORDER_FORWARD_FIRST,
                                         "coaccessible-first": gpu.FST_ORDER_COACCESSIBLE_FIRST,
                                         "concurrent": gpu.FST_ORDER_CONCURRENT}[args.order])
-    stream = torch.cuda.current_stream()
 
-    if args.copy_probe_mb > 0:
-        n = args.copy_probe_mb << 20
-        src = torch.ones(n, dtype=torch.uint8, device=dev)
-        dst = torch.empty_like(src)
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+    copy_gbs = copy_ceiling(args.copy_probe_mb) if args.copy_probe_mb > 0 else None
+    if args.calibrate_gather:
+        calibrate_gather()
 
     if args.task in ("score", "batch"):
-        out = run_score(args, A, B, comp, dA, dB) if args.task == "score" else \
+        out = run_score(args, A, B, comp, dA, dB, copy_gbs) if args.task == "score" else \
             run_batch(args, comp)
         comp.close()
         print(json.dumps(out), flush=True)
@@ -327,55 +475,30 @@ def main():
     comp.set_option(gpu.FST_OPT_COUNT_MOVES, 0)
     for _ in range(args.warmup):
         step()
-    torch.cuda.synchronize()
-    phases = {k: 0.0 for k in gpu.PHASES}
-    kern = {k: [0.0, 0] for k in gpu.KERNELS}
-    t0 = time.perf_counter()
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
-    ev0.record(stream)
-    for _ in range(args.steps):
-        step()
-        for k, v in comp.phase_times().items():
-            phases[k] += v
-        for k, (ms_k, n_k) in comp.kernel_times().items():
-            kern[k][0] += ms_k
-            kern[k][1] += n_k
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms = ev0.elapsed_time(ev1) / args.steps
-    ms_wall = 1e3 * wall / args.steps
+    # the timed region: K plain compositions (no library timing, no reads
+    # of statistics between them)
+    ms_wall, per_step, _ = timed_steps(step, args.steps)
     st = comp.stats()
     st["generated"] = st_moves["generated"]
     st["generated_backward"] = st_moves["generated_backward"]
     E_C = st["num_arcs"]
-    phases = {k: v / args.steps for k, v in phases.items()}
 
+    # per-kernel and per-phase device times from K more steps with the
+    # library's timing on (not part of the timed region)
+    phases = {k: 0.0 for k in gpu.PHASES}
+
+    def timed_phases():
+        for k, v in comp.phase_times().items():
+            phases[k] += v
+        return comp.kernel_times()
+
+    kernels = instrumented_kernels(comp, step, args.steps, gpu.KERNELS, timed_phases,
+                                   kernel_bytes(st))
+    phases = {k: round(v / args.steps, 4) for k, v in phases.items()}
     alg = algorithmic_bytes(A, B, st)
-    kb = kernel_bytes(st)
-    if args.order == "concurrent" and kern["search_backward"][1] == 0:
-        # the searches ran side by side: one launch advances both
-        kb["search_forward"] += kb.pop("search_backward")
-    kernels = {}
-    for k, (ms_k, n_k) in kern.items():
-        if n_k == 0 or ms_k <= 0:
-            continue
-        per_launch = kb[k] * args.steps / n_k
-        avg_ms = ms_k / n_k
-        kernels[k] = {"launches_per_step": n_k / args.steps, "ms_per_step": ms_k / args.steps,
-                      "avg_launch_us": 1e3 * avg_ms, "alg_bytes_per_launch": per_launch,
-                      "achieved_GBs": per_launch / (avg_ms * 1e-3) / 1e9}
-    dom = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
-    d = kernels[dom]
-    roofline = {"bound": "hbm", "kernel": dom, "achieved": d["achieved_GBs"],
-                "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": d["achieved_GBs"] / HBM_PEAK_GBS,
-                "traffic": measured_traffic(args.workload, dom),
-                "avg_launch_us": d["avg_launch_us"],
-                "alg_bytes_per_launch": d["alg_bytes_per_launch"]}
     out = {
-        "metric": "composed arcs/sec (emissions o lexicon)",
+        "metric": "composed arcs/sec (emissions o lexicon)" if args.workload.startswith("lexicon")
+        else "composed arcs/sec (random transducer pair)",
         "value": E_C / (ms_wall * 1e-3),
         "unit": "arcs/s",
         "n_gpus": 1,
@@ -390,14 +513,15 @@ def main():
         "config": {"workload": synth.WORKLOAD_TITLES[args.workload], "name": args.workload,
                    "seed": args.seed, "order": args.order,
                    "V_A": A["num_states"], "E_A": len(A["src"]), "V_B": B["num_states"],
-                   "E_B": len(B["src"]), "V_C": st["num_states"], "E_C": E_C},
-        "ms_per_composition_device": ms,
-        "phases_ms": {k: round(v, 4) for k, v in phases.items()},
+                   "E_B": len(B["src"]), "V_C": st["num_states"], "E_C": E_C,
+                   "inputs_sha256": {"A": synth.graph_sha256(A), "B": synth.graph_sha256(B)}},
+        "ms_per_composition_device": percentiles(per_step),
+        "phases_ms": phases,
         "kernels": kernels,
         "search_stats": st,
         "algorithmic_bytes": alg,
         "hbm_roofline_fraction_whole": (alg["total"] / (HBM_PEAK_GBS * 1e9)) / (ms_wall * 1e-3),
-        "roofline": roofline,
+        "roofline": roofline_of(kernels, args.workload, copy_gbs),
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(A, B, E_C)

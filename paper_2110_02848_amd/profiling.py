@@ -1,23 +1,35 @@
-"""Short text summaries of rocprofv3 output, and the HBM traffic they record.
+"""Short text summaries of rocprofv3 output, and the figures bench.py reads
+back from them.
 
 Two summaries are kept with the library's measurements:
 
 * a kernel-time table from ``rocprofv3 --kernel-trace --stats`` (calls,
-  total and average duration of every kernel of a run);
-* an HBM traffic table from two ``rocprofv3 --pmc`` passes over the same
-  run, one collecting ``FETCH_SIZE`` and one ``WRITE_SIZE`` (KiB per
-  dispatch).  The run also copies a buffer of known size with a plain
-  device-to-device copy, and the counters of that copy give the factor that
-  turns counter readings into bytes.
+  total and average duration of every kernel of a run, and per kernel
+  group);
+* a counter table per kernel group from several ``rocprofv3 --pmc`` passes
+  over the same run (one CSV per pass, at most what one pass can hold):
+  - HBM bytes: ``FETCH_SIZE`` and ``WRITE_SIZE`` (KiB per dispatch), each
+    divided by what the same counter reads for a plain device-to-device copy
+    of known size (the run copies ``--copy-bytes`` first);
+  - the same read traffic from the L2-to-memory read requests counted by
+    size (``TCC_EA0_RDREQ{,_32B,_64B,_128B}_sum``), which needs no factor;
+  - a calibration of both methods on gathers of known footprint: random
+    rows of 32 and of 64 bytes (the size of the search's scattered record
+    reads) gathered by index (bench.py --calibrate-gather), so the copy
+    factor can be checked for scattered reads;
+  - occupancy and activity: mean resident wavefronts per active CU
+    (``MeanOccupancyPerActiveCU``), ``OccupancyPercent``, ``VALUBusy``,
+    ``MemUnitStalled``, wavefronts launched (``SQ_WAVES``), L2 hit rate
+    (``TCC_HIT_sum``, ``TCC_MISS_sum``).
 
 Usage (on a machine with the GPU, from the repository root)::
 
     python -m paper_2110_02848_amd.profiling stats STATS_CSV OUT.txt --command "..."
-    python -m paper_2110_02848_amd.profiling traffic FETCH_CSV WRITE_CSV OUT.txt \\
-        --copy-bytes N --command "..."
+    python -m paper_2110_02848_amd.profiling counters OUT.txt --copy-bytes N \\
+        --gather-rows R --command "..." PASS1.csv PASS2.csv ...
 
-``read_traffic`` parses a traffic table back (bench.py reports it only while
-the kernel sources still hash to the value recorded in the table).
+``read_counters`` parses a counter table back; bench.py reports its figures
+only while the device sources still hash to the value recorded in it.
 """
 from __future__ import annotations
 
@@ -31,12 +43,10 @@ from collections import defaultdict
 _HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(_HERE, "csrc")
 
-# kernel families, as timed by the library (enum fst_kernel) in the default
-# (concurrent) search order, where one timer covers every search launch:
-# both searches side by side (k_gen2), the forward search alone (its first
-# generations) and either search alone once the other has ended
+# Kernel groups.  The search groups every launch of a search generation:
+# both searches side by side (k_gen2) and either search alone.
 FAMILIES = {
-    "search_forward": ("k_gen<true>", "k_gen<false>", "k_gen2("),
+    "search": ("k_gen<true>", "k_gen<false>", "k_gen2("),
     "count": ("k_count(", "k_count_heavy("),
     "fill": ("k_fill(", "k_fill_light(", "k_fill_heavy("),
     # scores of the composed graph (bench.py --task score)
@@ -46,7 +56,19 @@ FAMILIES = {
     "posterior": ("k_posterior(",),
     "scatter": ("k_absmax(", "k_bucket_count(", "k_bucket_place(", "k_scatter(",
                 "k_scatter_final("),
+    # N-way composition
+    "search3": ("k3_expand(", "k3_expand2("),
 }
+
+# Counters of each pass (what one rocprofv3 pass can collect on gfx950).
+PASSES = (
+    ("FETCH_SIZE",),
+    ("WRITE_SIZE",),
+    ("TCC_EA0_RDREQ_sum", "TCC_EA0_RDREQ_32B_sum", "TCC_EA0_RDREQ_64B_sum",
+     "TCC_EA0_RDREQ_128B_sum"),
+    ("MeanOccupancyPerActiveCU", "VALUBusy", "SQ_WAVES", "MemUnitStalled"),
+    ("OccupancyPercent", "TCC_HIT_sum", "TCC_MISS_sum"),
+)
 
 
 def kernel_source_hash():
@@ -78,7 +100,8 @@ def stats_summary(stats_csv, command, top=20):
     rows = list(csv.DictReader(open(stats_csv)))
     rows.sort(key=lambda r: -float(r["TotalDurationNs"]))
     total = sum(float(r["TotalDurationNs"]) for r in rows)
-    out = ["# rocprofv3 kernel-time summary", f"command: {command}", "",
+    out = ["# rocprofv3 kernel-time summary", f"command: {command}",
+           f"kernel_source_sha256: {kernel_source_hash()}", "",
            "| kernel | calls | total ms | avg us | min us | max us | % |",
            "|---|---|---|---|---|---|---|"]
     for r in rows[:top]:
@@ -100,59 +123,118 @@ def stats_summary(stats_csv, command, top=20):
     return "\n".join(out) + "\n"
 
 
-def _per_dispatch(csv_path, counter):
-    """{dispatch id: (kernel name, grid size, value)} for one counter."""
+def _dispatches(csv_paths):
+    """{(pass index, dispatch id): {"name", "counters": {counter: value}}},
+    values summed over the rows of one dispatch (instances)."""
     d = {}
-    for r in csv.DictReader(open(csv_path)):
-        if r["Counter_Name"] != counter:
-            continue
-        key = r["Dispatch_Id"]
-        v = float(r["Counter_Value"])
-        if key in d:
-            d[key] = (d[key][0], d[key][1], d[key][2] + v)
-        else:
-            d[key] = (r["Kernel_Name"], int(r["Grid_Size"]), v)
+    for pi, path in enumerate(csv_paths):
+        for r in csv.DictReader(open(path)):
+            key = (pi, r["Dispatch_Id"])
+            e = d.setdefault(key, {"name": r["Kernel_Name"], "counters": defaultdict(float)})
+            e["counters"][r["Counter_Name"]] += float(r["Counter_Value"])
     return d
 
 
-def _copy_factor(d, copy_bytes):
-    copies = [(g, v) for (n, g, v) in d.values() if "copyBuffer" in n]
-    if not copies:
-        raise SystemExit("no copy kernel in the counter output")
-    g, v = max(copies)
-    return v * 1024.0 / copy_bytes
+def _read_bytes_by_size(c):
+    """Read bytes from the request counts by size; requests counted in
+    RDREQ but in none of the sized counters are taken as 64 bytes."""
+    n32 = c.get("TCC_EA0_RDREQ_32B_sum", 0.0)
+    n64 = c.get("TCC_EA0_RDREQ_64B_sum", 0.0)
+    n128 = c.get("TCC_EA0_RDREQ_128B_sum", 0.0)
+    other = max(0.0, c.get("TCC_EA0_RDREQ_sum", 0.0) - n32 - n64 - n128)
+    return 32 * n32 + 64 * (n64 + other) + 128 * n128
 
 
-def traffic_summary(fetch_csv, write_csv, copy_bytes, command):
-    fe = _per_dispatch(fetch_csv, "FETCH_SIZE")
-    wr = _per_dispatch(write_csv, "WRITE_SIZE")
-    ff, fw = _copy_factor(fe, copy_bytes), _copy_factor(wr, copy_bytes)
-    out = ["# rocprofv3 HBM traffic per dispatch (FETCH_SIZE and WRITE_SIZE passes)",
-           f"command: {command}",
+def _mean_by(dd, pred):
+    """Mean of every counter over the dispatches whose name satisfies pred
+    (each counter averaged over the dispatches of the pass that has it)."""
+    sums, counts = defaultdict(float), defaultdict(int)
+    for (pi, _), e in dd.items():
+        if pred(e["name"]):
+            for k, v in e["counters"].items():
+                sums[k] += v
+                counts[k] += 1
+    return {k: sums[k] / counts[k] for k in sums}, max(counts.values()) if counts else 0
+
+
+def counters_summary(csv_paths, copy_bytes, gather_rows, command):
+    dd = _dispatches(csv_paths)
+    # the copy: the largest copyBuffer dispatch of each pass
+    copy = {}
+    for (pi, _), e in dd.items():
+        if "copyBuffer" in e["name"]:
+            for k, v in e["counters"].items():
+                copy[k] = max(copy.get(k, 0.0), v)
+    ff = copy.get("FETCH_SIZE", 0.0) * 1024.0 / copy_bytes if copy_bytes else 0.0
+    fw = copy.get("WRITE_SIZE", 0.0) * 1024.0 / copy_bytes if copy_bytes else 0.0
+    copy_rd = _read_bytes_by_size(copy)
+    out = ["# rocprofv3 counters per dispatch, by kernel group", f"command: {command}",
            f"kernel_source_sha256: {kernel_source_hash()}",
            f"copy_bytes: {copy_bytes}",
            f"copy_fetch_factor: {ff:.4f}",
            f"copy_write_factor: {fw:.4f}",
-           "",
-           "Bytes = FETCH_SIZE KiB * 1024 / copy_fetch_factor + WRITE_SIZE KiB * 1024 / "
-           "copy_write_factor, per dispatch of the kernel group.",
-           "",
-           "| kernel group | dispatches | FETCH_SIZE KiB/dispatch | WRITE_SIZE KiB/dispatch | "
-           "HBM bytes/dispatch |",
-           "|---|---|---|---|---|"]
+           f"copy_read_bytes_by_request_size: {copy_rd:.0f}", ""]
+    # gathers of known footprint: rows of 32 bytes, then of 64 bytes (the
+    # first and the second gather dispatch of each pass), each row gathered
+    # once by an int64 index, the output written once
+    if gather_rows:
+        out += ["Gather calibration (random rows read once, int64 index read once, rows written "
+                "once):", "",
+                "| gather | known read bytes | FETCH_SIZE / copy factor | read bytes by request "
+                "size | known write bytes | WRITE_SIZE / copy factor |", "|---|---|---|---|---|---|"]
+        by_pass = defaultdict(list)
+        for (pi, did), e in dd.items():
+            nm = e["name"].lower()
+            if "gather" in nm or "index_select" in nm or "indexselect" in nm:
+                by_pass[pi].append((int(did), e["counters"]))
+        for gi, row in enumerate((32, 64)):
+            c = defaultdict(float)
+            for pi, lst in by_pass.items():
+                lst.sort(key=lambda t: t[0])
+                if gi < len(lst):
+                    for k, v in lst[gi][1].items():
+                        c[k] += v
+            if not c:
+                continue
+            known_rd = gather_rows * (row + 8)
+            known_wr = gather_rows * row
+            fs = c.get("FETCH_SIZE", 0.0) * 1024.0 / ff if ff else 0.0
+            ws = c.get("WRITE_SIZE", 0.0) * 1024.0 / fw if fw else 0.0
+            rb = _read_bytes_by_size(c)
+            out.append(f"| {row}-byte rows x {gather_rows} | {known_rd} | {fs:.0f} "
+                       f"({fs / known_rd:.3f} x) | {rb:.0f} ({rb / known_rd:.3f} x) | "
+                       f"{known_wr} | {ws:.0f} ({ws / known_wr:.3f} x) |")
+        out.append("")
+    out += ["HBM bytes = FETCH_SIZE KiB * 1024 / copy_fetch_factor + WRITE_SIZE KiB * 1024 / "
+            "copy_write_factor; read bytes by request size = 32 n32 + 64 n64 + 128 n128 "
+            "(L2-to-memory read requests); all per dispatch of the kernel group (mean).", "",
+            "| kernel group | dispatches | FETCH_SIZE KiB | WRITE_SIZE KiB | HBM bytes | "
+            "read bytes by request size | L2 hit % | waves per active CU | occupancy % | "
+            "VALUBusy % | MemUnitStalled % | wavefronts |",
+            "|---|---|---|---|---|---|---|---|---|---|---|---|"]
     for fam in FAMILIES:
-        fk = [v for (n, g, v) in fe.values() if family_of(n) == fam]
-        wk = [v for (n, g, v) in wr.values() if family_of(n) == fam]
-        if not fk or not wk:
+        c, n = _mean_by(dd, lambda nm, f=fam: family_of(nm) == f)
+        if not n:
             continue
-        mf, mw = sum(fk) / len(fk), sum(wk) / len(wk)
-        b = mf * 1024.0 / ff + mw * 1024.0 / fw
-        out.append(f"| {fam} | {len(fk)} | {mf:.1f} | {mw:.1f} | {b:.0f} |")
+        fk, wk = c.get("FETCH_SIZE", 0.0), c.get("WRITE_SIZE", 0.0)
+        hbm = (fk * 1024.0 / ff if ff else 0.0) + (wk * 1024.0 / fw if fw else 0.0)
+        hit, miss = c.get("TCC_HIT_sum", 0.0), c.get("TCC_MISS_sum", 0.0)
+        hr = 100.0 * hit / (hit + miss) if hit + miss else 0.0
+        out.append(f"| {fam} | {n} | {fk:.1f} | {wk:.1f} | {hbm:.0f} | "
+                   f"{_read_bytes_by_size(c):.0f} | {hr:.1f} | "
+                   f"{c.get('MeanOccupancyPerActiveCU', 0.0):.2f} | "
+                   f"{c.get('OccupancyPercent', 0.0):.1f} | {c.get('VALUBusy', 0.0):.1f} | "
+                   f"{c.get('MemUnitStalled', 0.0):.1f} | {c.get('SQ_WAVES', 0.0):.0f} |")
     return "\n".join(out) + "\n"
 
 
-def read_traffic(path):
-    """(kernel_source_sha256, {group: HBM bytes per dispatch}) or None."""
+COLUMNS = ("dispatches", "FETCH_SIZE KiB", "WRITE_SIZE KiB", "HBM bytes",
+           "read bytes by request size", "L2 hit %", "waves per active CU", "occupancy %",
+           "VALUBusy %", "MemUnitStalled %", "wavefronts")
+
+
+def read_counters(path):
+    """(kernel_source_sha256, {group: {column: value}}) or None."""
     if not os.path.exists(path):
         return None
     sha, table = None, {}
@@ -161,8 +243,8 @@ def read_traffic(path):
             sha = line.split(":", 1)[1].strip()
         elif line.startswith("| ") and not line.startswith("| kernel"):
             cells = [c.strip() for c in line.strip().strip("|").split("|")]
-            if len(cells) == 5 and cells[0] in FAMILIES:
-                table[cells[0]] = float(cells[4])
+            if len(cells) == 1 + len(COLUMNS) and cells[0] in FAMILIES:
+                table[cells[0]] = {k: float(v) for k, v in zip(COLUMNS, cells[1:])}
     return sha, table
 
 
@@ -173,17 +255,17 @@ def main():
     a.add_argument("stats_csv")
     a.add_argument("out")
     a.add_argument("--command", required=True)
-    b = sub.add_parser("traffic")
-    b.add_argument("fetch_csv")
-    b.add_argument("write_csv")
+    b = sub.add_parser("counters")
     b.add_argument("out")
+    b.add_argument("csvs", nargs="+")
     b.add_argument("--copy-bytes", type=int, required=True)
+    b.add_argument("--gather-rows", type=int, default=0)
     b.add_argument("--command", required=True)
     args = ap.parse_args()
     if args.cmd == "stats":
         text = stats_summary(args.stats_csv, args.command)
     else:
-        text = traffic_summary(args.fetch_csv, args.write_csv, args.copy_bytes, args.command)
+        text = counters_summary(args.csvs, args.copy_bytes, args.gather_rows, args.command)
     with open(args.out, "w") as f:
         f.write(text)
     print(text)
