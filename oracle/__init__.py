@@ -17,6 +17,12 @@ Algorithm 1 (Section 3.1) with the epsilon-sequencing filter described in
 
 Parity with the GPU path is checked on this canonical form.
 
+``compose3(A, B, D)`` (``compose3.c``) is the simultaneous composition of
+three transducers, C = A o B o D (the N-way composition the paper names as
+the next step), canonical in the same way: states by key (qa, qb, f1, qd,
+f2), arcs of a state by (a, b, d), the arcs of A, B and D they came from,
+with a missing arc sorting last.
+
 ``score(G)``, ``posterior(G, ...)`` and ``scatter(...)`` (``score.c``) give
 the log-semiring forward and backward scores of an acyclic graph, the arc
 posteriors that are the total score's gradient, and the scatter of per-arc
@@ -31,7 +37,7 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_SRCS = [os.path.join(_HERE, n) for n in ("oracle.c", "score.c")]
+_SRCS = [os.path.join(_HERE, n) for n in ("oracle.c", "score.c", "compose3.c")]
 _DEPS = _SRCS + [os.path.join(_HERE, "og.h")]
 _LIB = os.path.join(_HERE, "liboracle.so")
 
@@ -52,6 +58,13 @@ SMUT_MAX = 1
 SMUT_DROP_WEIGHT = 2
 SMUT_ALL_ACCEPT = 3
 SMUT_NO_START = 4
+
+# deliberate mistakes of the three-input oracle (tests of the pins only)
+MUT3_NONE = 0
+MUT3_NO_INNER_FILTER = 1
+MUT3_NO_OUTER_FILTER = 2
+MUT3_DROP_WD = 3
+MUT3_OUTER_LABEL = 4
 
 _ERRORS = {1: "invalid argument", 2: "out of memory", 3: "key space too large",
            4: "graph has a cycle"}
@@ -96,6 +109,19 @@ class _Result(ctypes.Structure):
                 ("compose_seconds", ctypes.c_double)]
 
 
+class _Result3(ctypes.Structure):
+    _fields_ = [("num_states", ctypes.c_int64), ("num_arcs", ctypes.c_int64),
+                ("key_a", ctypes.c_void_p), ("key_b", ctypes.c_void_p),
+                ("key_d", ctypes.c_void_p), ("key_fab", ctypes.c_void_p),
+                ("key_f", ctypes.c_void_p), ("start", ctypes.c_void_p),
+                ("accept", ctypes.c_void_p), ("arc_src", ctypes.c_void_p),
+                ("arc_dst", ctypes.c_void_p), ("arc_ilabel", ctypes.c_void_p),
+                ("arc_olabel", ctypes.c_void_p), ("arc_weight", ctypes.c_void_p),
+                ("arc_a", ctypes.c_void_p), ("arc_b", ctypes.c_void_p),
+                ("arc_d", ctypes.c_void_p), ("accessible", ctypes.c_int64),
+                ("generated", ctypes.c_int64), ("compose_seconds", ctypes.c_double)]
+
+
 _lib = None
 
 
@@ -110,6 +136,12 @@ def _load():
         lib.oracle_compose.restype = ctypes.c_int
         lib.oracle_free.argtypes = [ctypes.POINTER(_Result)]
         lib.oracle_free.restype = None
+        lib.oracle_compose3.argtypes = [ctypes.POINTER(_Graph), ctypes.POINTER(_Graph),
+                                        ctypes.POINTER(_Graph), ctypes.c_int,
+                                        ctypes.POINTER(_Result3)]
+        lib.oracle_compose3.restype = ctypes.c_int
+        lib.oracle_free3.argtypes = [ctypes.POINTER(_Result3)]
+        lib.oracle_free3.restype = None
         lib.oracle_in_csr.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
                                       ctypes.c_void_p, ctypes.c_void_p]
         lib.oracle_in_csr.restype = ctypes.c_int
@@ -235,6 +267,75 @@ def compose(A, B, order=ORDER_PAPER, mutation=MUT_NONE):
 
 RESULT_KEYS = ("arc_offset", "src", "dst", "ilabel", "olabel", "weight", "arc_a", "arc_b",
                "start", "accept", "key_a", "key_b", "key_f")
+
+
+def compose3_raw(A, B, D, mutation=MUT3_NONE):
+    """Run the three-input C oracle; states and arcs in discovery order."""
+    lib = _load()
+    keep = []
+    ga, gb, gd = _as_struct(A, keep), _as_struct(B, keep), _as_struct(D, keep)
+    res = _Result3()
+    rc = lib.oracle_compose3(ctypes.byref(ga), ctypes.byref(gb), ctypes.byref(gd), mutation,
+                             ctypes.byref(res))
+    if rc:
+        raise ValueError("oracle_compose3: " + _ERRORS.get(rc, str(rc)))
+    try:
+        V, E = int(res.num_states), int(res.num_arcs)
+        out = dict(
+            num_states=V, num_arcs=E,
+            key_a=_copy(res.key_a, V, np.int32), key_b=_copy(res.key_b, V, np.int32),
+            key_d=_copy(res.key_d, V, np.int32), key_fab=_copy(res.key_fab, V, np.uint8),
+            key_f=_copy(res.key_f, V, np.uint8), start=_copy(res.start, V, np.uint8),
+            accept=_copy(res.accept, V, np.uint8),
+            src=_copy(res.arc_src, E, np.int32), dst=_copy(res.arc_dst, E, np.int32),
+            ilabel=_copy(res.arc_ilabel, E, np.int32), olabel=_copy(res.arc_olabel, E, np.int32),
+            weight=_copy(res.arc_weight, E, np.float32),
+            arc_a=_copy(res.arc_a, E, np.int32), arc_b=_copy(res.arc_b, E, np.int32),
+            arc_d=_copy(res.arc_d, E, np.int32),
+            stats=dict(accessible=int(res.accessible), generated=int(res.generated),
+                       compose_seconds=float(res.compose_seconds)),
+        )
+    finally:
+        lib.oracle_free3(ctypes.byref(res))
+    return out
+
+
+def canonicalize3(raw):
+    """Renumber states by key (qa, qb, f1, qd, f2) and sort the arcs of each
+    state by (a, b, d), a missing arc (-1) last."""
+    V, E = raw["num_states"], raw["num_arcs"]
+    order = np.lexsort((raw["key_f"], raw["key_d"], raw["key_fab"], raw["key_b"], raw["key_a"]))
+    new_id = np.empty(V, np.int64)
+    new_id[order] = np.arange(V)
+    src = new_id[raw["src"]] if E else np.zeros(0, np.int64)
+    dst = new_id[raw["dst"]] if E else np.zeros(0, np.int64)
+    big = np.int64(1) << 40
+
+    def k(x):
+        x = x.astype(np.int64)
+        return np.where(x >= 0, x, big)
+
+    aorder = np.lexsort((k(raw["arc_d"]), k(raw["arc_b"]), k(raw["arc_a"]), src))
+    off = np.zeros(V + 1, np.int32)
+    if V:
+        off[1:] = np.cumsum(np.bincount(src, minlength=V))
+    out = dict(num_states=V, num_arcs=E, arc_offset=off,
+               src=src[aorder].astype(np.int32), dst=dst[aorder].astype(np.int32),
+               start=raw["start"][order], accept=raw["accept"][order], stats=raw["stats"])
+    for name in ("ilabel", "olabel", "weight", "arc_a", "arc_b", "arc_d"):
+        out[name] = raw[name][aorder]
+    for name in ("key_a", "key_b", "key_fab", "key_d", "key_f"):
+        out[name] = raw[name][order]
+    return out
+
+
+def compose3(A, B, D, mutation=MUT3_NONE):
+    """Canonical C = A o B o D, composed simultaneously (see compose3.c)."""
+    return canonicalize3(compose3_raw(A, B, D, mutation))
+
+
+RESULT3_KEYS = ("arc_offset", "src", "dst", "ilabel", "olabel", "weight", "arc_a", "arc_b",
+                "arc_d", "start", "accept", "key_a", "key_b", "key_fab", "key_d", "key_f")
 
 
 def _graph_of(G, keep):

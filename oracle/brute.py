@@ -190,3 +190,104 @@ def product_trim_keys(A, B):
                 stack.append(u)
     return fwd & bwd
 
+
+
+# --------------------------------------------------------------------------
+# three inputs: C = A o B o D (the N-way composition of Section 5)
+# --------------------------------------------------------------------------
+
+def path_triples(A, B, D, max_len):
+    """Map (pi_A, pi_B, pi_D) -> (x, w, weight) for every triple of
+    accepting paths with at most ``max_len`` arcs each whose middle strings
+    agree: out(pi_A) = in(pi_B) and out(pi_B) = in(pi_D)."""
+    pa = accepting_paths(A, max_len)
+    pb = accepting_paths(B, max_len)
+    pd = accepting_paths(D, max_len)
+    b_by_in = defaultdict(list)
+    for p in pb:
+        b_by_in[_strings(B, p, "in")].append(p)
+    d_by_in = defaultdict(list)
+    for p in pd:
+        d_by_in[_strings(D, p, "in")].append(p)
+    out = {}
+    for p in pa:
+        for q in b_by_in.get(_strings(A, p, "out"), ()):
+            for r in d_by_in.get(_strings(B, q, "out"), ()):
+                out[(p, q, r)] = (_strings(A, p, "in"), _strings(D, r, "out"),
+                                  _wsum(A, p) + _wsum(B, q) + _wsum(D, r))
+    return out
+
+
+def composed3_paths(C, max_len, max_proj):
+    """Accepting paths of a three-input composition C (length <= max_len)
+    whose projections onto A, B and D each have at most ``max_proj`` arcs:
+    a list of (pi_A, pi_B, pi_D, x, w, weight), the projections read from the
+    provenance arc_a, arc_b, arc_d and the keys of C's start state."""
+    outs = _out_arcs(C)
+    dst, acc = C["dst"], C["accept"]
+    prov = (C["arc_a"], C["arc_b"], C["arc_d"])
+    keys = (C["key_a"], C["key_b"], C["key_d"])
+    il, ol, w = C["ilabel"], C["olabel"], C["weight"]
+    res = []
+
+    def walk(s, q, path, n):
+        if acc[q]:
+            proj = tuple((int(keys[i][s]), tuple(int(prov[i][e]) for e in path if prov[i][e] >= 0))
+                         for i in range(3))
+            x = tuple(int(il[e]) for e in path if il[e] != 0)
+            z = tuple(int(ol[e]) for e in path if ol[e] != 0)
+            res.append(proj + (x, z, math.fsum(float(w[e]) for e in path)))
+        if len(path) == max_len:
+            return
+        for e in outs[q]:
+            m = [n[i] + (1 if prov[i][e] >= 0 else 0) for i in range(3)]
+            if max(m) > max_proj:
+                continue
+            path.append(e)
+            walk(s, int(dst[e]), path, m)
+            path.pop()
+
+    for s in range(C["num_states"]):
+        if C["start"][s]:
+            walk(s, s, [], [0, 0, 0])
+    return res
+
+
+def check3(A, B, D, C, max_len):
+    """Compare a three-input composition C against brute force: every
+    matching triple of accepting paths (each at most max_len arcs) is
+    realised by exactly one accepting path of C, with its strings and
+    weight, and nothing else is; and the per-(x, w) log-sum scores agree.
+    Returns a list of discrepancies."""
+    problems = []
+    triples = path_triples(A, B, D, max_len)
+    cpaths = composed3_paths(C, 3 * max_len, max_len)
+    seen = defaultdict(int)
+    for pa, pb, pd, x, z, w in cpaths:
+        k = (pa, pb, pd)
+        seen[k] += 1
+        ref = triples.get(k)
+        if ref is None:
+            problems.append(f"C path projects to a non-matching triple {k}")
+            continue
+        if (x, z) != (ref[0], ref[1]):
+            problems.append(f"strings differ for {k}: {(x, z)} vs {ref[:2]}")
+        tol = 1e-6 * (1.0 + sum(abs(float(A["weight"][e])) for e in pa[1])
+                      + sum(abs(float(B["weight"][e])) for e in pb[1])
+                      + sum(abs(float(D["weight"][e])) for e in pd[1]))
+        if abs(w - ref[2]) > tol:
+            problems.append(f"weight differs for {k}: {w} vs {ref[2]}")
+    for k, n in seen.items():
+        if n > 1:
+            problems.append(f"triple {k} realised by {n} paths of C")
+    for k in triples:
+        if k not in seen:
+            problems.append(f"triple {k} missing from C")
+    s_ref = scores(triples.values())
+    s_c = scores([(x, z, w) for _, _, _, x, z, w in cpaths])
+    for k in set(s_ref) | set(s_c):
+        if k not in s_ref or k not in s_c:
+            problems.append(f"(x, w) = {k} present on one side only")
+        elif abs(s_ref[k] - s_c[k]) > 1e-5 * (1 + abs(s_ref[k])):
+            problems.append(f"score of {k}: {s_c[k]} vs {s_ref[k]}")
+    return problems

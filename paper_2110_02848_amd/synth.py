@@ -316,6 +316,64 @@ def lexicon_batch(name, n, seed=0, spec=None, frames=None):
     return As, B, dict(tables=tables, spellings=spell, spec=spec)
 
 
+def word_grammar(rng, G, W, deg, p_backoff, p_accept):
+    """Word-level grammar acceptor over word ids 1..W (the third input of an
+    emissions o lexicon o grammar composition).  G states, state 0 start and
+    accepting, others accepting with probability p_accept.  Each state has
+    ``deg`` arcs w:w for distinct words drawn uniformly, to uniform
+    destinations; each state other than 0 has, with probability p_backoff,
+    an epsilon:epsilon backoff arc to state 0 (listed last).  A state's arc
+    weights are a float32 log-softmax of N(0, 1) logits drawn in float64
+    (over its word arcs and its backoff arc)."""
+    arcs = []
+    for s in range(G):
+        words = rng.choice(W, size=min(deg, W), replace=False) + 1
+        dsts = rng.integers(0, G, size=len(words))
+        back = s != 0 and rng.random() < p_backoff
+        z = rng.standard_normal(len(words) + (1 if back else 0))
+        m = z.max()
+        logp = (z - m - np.log(np.exp(z - m).sum())).astype(np.float32)
+        for i, (w, d) in enumerate(zip(words, dsts)):
+            arcs.append((s, int(d), int(w), int(w), float(logp[i])))
+        if back:
+            arcs.append((s, 0, EPS, EPS, float(logp[-1])))
+    acc = [0] + [s for s in range(1, G) if rng.random() < p_accept]
+    return from_arcs(G, arcs, start=[0], accept=acc)
+
+
+@dataclass(frozen=True)
+class GrammarSpec:
+    T: int
+    C: int
+    W: int
+    len_lo: int
+    len_hi: int
+    G: int
+    deg: int
+    p_backoff: float
+    p_accept: float
+
+
+GRAMMAR_SPECS = {
+    "grammar-T40-W300-G6": GrammarSpec(40, 12, 300, 2, 6, 6, 60, 0.5, 0.5),
+    "grammar-T100-W1000-G20": GrammarSpec(100, 28, 1000, 3, 8, 20, 200, 0.5, 0.3),
+}
+_STREAM.update({"grammar-T40-W300-G6": 6, "grammar-T100-W1000-G20": 7})
+
+
+def emissions_lexicon_grammar(name, seed=0, spec=None):
+    """A = emissions, B = lexicon, D = word grammar (so A o B o D maps token
+    strings to the word strings the grammar accepts).  Inputs are drawn from
+    SeedSequence([stream, seed]).spawn(3), one generator per graph."""
+    spec = spec or GRAMMAR_SPECS[name]
+    ra, rb, rd = [np.random.default_rng(s)
+                  for s in np.random.SeedSequence([_STREAM[name], int(seed)]).spawn(3)]
+    A, table = emissions(ra, spec.T, spec.C)
+    B, spell = lexicon(rb, spec.W, spec.C, spec.len_lo, spec.len_hi)
+    D = word_grammar(rd, spec.G, spec.W, spec.deg, spec.p_backoff, spec.p_accept)
+    return A, B, D, dict(table=table, spellings=spell, spec=spec)
+
+
 def workload(name, seed=0):
     """Inputs ``(A, B)`` of a named workload for a given seed."""
     if name in RANDOM_SPECS:
@@ -325,6 +383,12 @@ def workload(name, seed=0):
 
 
 WORKLOADS = tuple(RANDOM_SPECS) + tuple(LEX_SPECS)
+
+GRAMMAR_TITLES = {
+    "grammar-T40-W300-G6": "emissions(T=40,C=12) o lexicon(W=300,L=2..6) o grammar(G=6,deg=60)",
+    "grammar-T100-W1000-G20":
+        "emissions(T=100,C=28) o lexicon(W=1000,L=3..8) o grammar(G=20,deg=200)",
+}
 
 WORKLOAD_TITLES = {
     "random-64": "random pair V=64 d=4 K=16 p_eps=0.1 p_acc=0.1",

@@ -308,3 +308,130 @@ def bfs_levels(n, adj, seeds):
                 lvl[v] = lvl[u] + 1
                 q.append(v)
     return lvl
+
+
+# --------------------------------------------------------------------------
+# three inputs: C = A o B o D
+# --------------------------------------------------------------------------
+
+def eps_out_t(A, B, qa, qb, fab):
+    """Per key: whether the state (qa, qb, fab) of A o B has an arc with
+    output epsilon (an A-epsilon move when fab = 0, a B arc eps:eps, or a
+    matching pair whose B arc has output epsilon)."""
+    epsA = eps_out(A)
+    VB = B["num_states"]
+    bb_eps = np.zeros(VB, bool)
+    b_sets = [set() for _ in range(VB)]
+    for s, i, o in zip(B["src"], B["ilabel"], B["olabel"]):
+        if o == 0:
+            if i == 0:
+                bb_eps[s] = True
+            else:
+                b_sets[s].add(int(i))
+    a_sets = [set() for _ in range(A["num_states"])]
+    for s, o in zip(A["src"], A["olabel"]):
+        if o != 0:
+            a_sets[s].add(int(o))
+    out = np.zeros(len(qa), bool)
+    for i, (a, b, f) in enumerate(zip(qa, qb, fab)):
+        out[i] = ((f == 0 and epsA[a]) or bb_eps[b] or bool(a_sets[a] & b_sets[b]))
+    return out
+
+
+def check_invariants3(A, B, D, C):
+    """Return a list of violated invariants of a canonical three-input
+    composition C = A o B o D (keys (qa, qb, f1, qd, f2), provenance
+    arc_a, arc_b, arc_d)."""
+    errs = []
+    V, E = int(C["num_states"]), int(C["num_arcs"])
+    if V == 0:
+        return [] if E == 0 else ["arcs without states"]
+    ka, kb, kd = (C[k].astype(np.int64) for k in ("key_a", "key_b", "key_d"))
+    f1, f2 = C["key_fab"].astype(np.int64), C["key_f"].astype(np.int64)
+    VA, VB, VD = A["num_states"], B["num_states"], D["num_states"]
+    if min(ka.min(), kb.min(), kd.min()) < 0 or ka.max() >= VA or kb.max() >= VB \
+            or kd.max() >= VD:
+        return ["key out of range"]
+    key = (((ka * VB + kb) * 2 + f1) * VD + kd) * 2 + f2
+    if np.any(np.diff(key) <= 0):
+        errs.append("states not in strictly ascending key order")
+    epsA = eps_out(A)
+    epsT = eps_out_t(A, B, ka, kb, f1)
+    if np.any((f1 == 1) & ~epsA[ka]):
+        errs.append("inner filter bit set where A has no epsilon output")
+    if np.any((f2 == 1) & ~epsT):
+        errs.append("outer filter bit set where A o B has no epsilon output")
+    st = ((f1 == 0) & (f2 == 0) & (A["start"][ka] == 1) & (B["start"][kb] == 1)
+          & (D["start"][kd] == 1)).astype(np.uint8)
+    ac = ((A["accept"][ka] == 1) & (B["accept"][kb] == 1) & (D["accept"][kd] == 1)).astype(np.uint8)
+    if not np.array_equal(st, C["start"]):
+        errs.append("start flags differ from keys")
+    if not np.array_equal(ac, C["accept"]):
+        errs.append("accept flags differ from keys")
+    off = C["arc_offset"].astype(np.int64)
+    src, dst = C["src"].astype(np.int64), C["dst"].astype(np.int64)
+    if off[0] != 0 or off[-1] != E or np.any(np.diff(off) < 0):
+        errs.append("bad arc_offset")
+    elif not np.array_equal(np.repeat(np.arange(V), np.diff(off)), src):
+        errs.append("src inconsistent with arc_offset")
+    if E:
+        if dst.min() < 0 or dst.max() >= V:
+            return errs + ["dst out of range"]
+        a, b, d = (C[k].astype(np.int64) for k in ("arc_a", "arc_b", "arc_d"))
+        Ap, Bp, Dp = _padded(A), _padded(B), _padded(D)
+        aa, bb, dd = np.maximum(a, 0), np.maximum(b, 0), np.maximum(d, 0)
+        wA = Ap["weight"][aa].astype(np.float32)
+        wB = Bp["weight"][bb].astype(np.float32)
+        wD = Dp["weight"][dd].astype(np.float32)
+        w = _bits(C["weight"])
+        ha, hb, hd = a >= 0, b >= 0, d >= 0
+        il, ol = C["ilabel"], C["olabel"]
+        same = lambda x: x[src] == x[dst]
+        # the T-arc (A o B move) of an arc, when A or B moves
+        tm = ha & hb
+        t_ok = np.ones(E, bool)
+        t_ok &= ~tm | ((Ap["olabel"][aa] == Bp["ilabel"][bb]) & (Ap["olabel"][aa] != 0)
+                       & (ka[src] == Ap["src"][aa]) & (kb[src] == Bp["src"][bb])
+                       & (ka[dst] == Ap["dst"][aa]) & (kb[dst] == Bp["dst"][bb]) & (f1[dst] == 0))
+        ta = ha & ~hb
+        t_ok &= ~ta | ((Ap["olabel"][aa] == 0) & (f1[src] == 0) & (ka[src] == Ap["src"][aa])
+                       & (ka[dst] == Ap["dst"][aa]) & same(kb) & (f1[dst] == 0))
+        tb = ~ha & hb
+        t_ok &= ~tb | ((Bp["ilabel"][bb] == 0) & same(ka) & (kb[src] == Bp["src"][bb])
+                       & (kb[dst] == Bp["dst"][bb]) & (f1[dst] == epsA[ka[dst]]))
+        moves_t = ha | hb
+        t_in = np.where(ha, Ap["ilabel"][aa], 0)
+        t_out = np.where(hb, Bp["olabel"][bb], 0)
+        t_w = np.where(tm, wA + wB, np.where(ha, wA, wB)).astype(np.float32)
+        # the move of the key: T-arc with D arc (match), T-arc alone (output
+        # epsilon), or D arc alone (input epsilon)
+        m = moves_t & hd
+        ok = ~m | ((t_out != 0) & (Dp["ilabel"][dd] == t_out) & (kd[src] == Dp["src"][dd])
+                   & (kd[dst] == Dp["dst"][dd]) & (f2[dst] == 0) & (il == t_in)
+                   & (ol == Dp["olabel"][dd]) & (w == _bits(t_w + wD)))
+        te = moves_t & ~hd
+        ok &= ~te | ((t_out == 0) & (f2[src] == 0) & same(kd) & (f2[dst] == 0) & (il == t_in)
+                     & (ol == 0) & (w == _bits(t_w)))
+        de = ~moves_t & hd
+        ok &= ~de | ((Dp["ilabel"][dd] == 0) & same(ka) & same(kb) & same(f1)
+                     & (kd[src] == Dp["src"][dd]) & (kd[dst] == Dp["dst"][dd])
+                     & (f2[dst] == epsT[dst]) & (il == 0) & (ol == Dp["olabel"][dd])
+                     & (w == _bits(wD)))
+        ok &= ~moves_t | t_ok
+        ok &= moves_t | hd
+        if not np.all(ok):
+            errs.append(f"{int(np.sum(~ok))} arcs inconsistent with their provenance")
+        trip = np.stack([src, a, b, d], axis=1)
+        if len(np.unique(trip, axis=0)) != E:
+            errs.append("duplicate (src, arc_a, arc_b, arc_d)")
+        big = np.int64(1) << 40
+        order = np.lexsort((np.where(hd, d, big), np.where(hb, b, big), np.where(ha, a, big), src))
+        if not np.array_equal(order, np.arange(E)):
+            errs.append("arcs not in canonical order")
+    fwd = _reach(V, src, dst, np.flatnonzero(C["start"]))
+    bwd = _reach(V, dst, src, np.flatnonzero(C["accept"]))
+    if not fwd.all():
+        errs.append("inaccessible state")
+    if not bwd.all():
+        errs.append("non-coaccessible state")
+    return errs
