@@ -205,12 +205,18 @@ enum fst_kernel {
   FST_KERNEL_FILL = 3,
   FST_KERNEL_SCORE_GEN = 4,   /* fst_score: generation kernels (one launch
                                  advances every direction asked for)       */
-  FST_KERNEL_SCORE_PREP = 5   /* fst_score: in-arc structure of the graph   */
+  FST_KERNEL_SCORE_PREP = 5,  /* fst_score: in-arc structure of the graph   */
+  FST_KERNEL_SEARCH3 = 6,     /* fst_compose3_run: the level launches of the
+                                 forward and backward searches             */
+  FST_KERNEL_COMPACT3 = 7     /* fst_compose3_run + fill: in-arc grouping,
+                                 trim keys, sort and numbering, arc count,
+                                 fill                                      */
 };
 
 /* With FST_OPT_TIMING on: *ms = summed device time of the launches of
- * `kernel` in the last run + fill (kernels 0-3) or the last fst_score
- * (kernels 4-5), each bracketed by HIP events on the caller's stream, and
+ * `kernel` in the last run + fill (kernels 0-3), the last fst_score
+ * (kernels 4-5) or the last fst_compose3_run + fst_compose3_fill (kernels
+ * 6-7), each bracketed by HIP events on the caller's stream, and
  * *launches = how many there were.  Returns FST_ERR_STATE if timing was off
  * or no such call was timed, FST_ERR_INVALID_ARG for an unknown kernel. */
 FST_API int fst_compose_kernel_time(const fst_ctx *ctx, int kernel, float *ms, int64_t *launches);
@@ -310,6 +316,64 @@ FST_API int fst_compose_batch_run(fst_ctx *ctx, const fst_graph *A, int32_t n,
  * non-decreasing entries within the arrays.  Blocks until done. */
 FST_API int fst_segment_logsum(fst_ctx *ctx, const double *val, const uint8_t *flag, int32_t n,
                                const int64_t *bounds, double *totals, void *stream);
+
+/* ---- Three inputs at once ----------------------------------------------
+ * N-way composition (Section 5 names composing N inputs at once, instead
+ * of two, as the next step): C = A o B o D in one search, without building
+ * A o B.  Eq. (1) read for three inputs: C maps x to w with score log-sum,
+ * over all y and z, of exp(A(x, y) + B(y, z) + D(z, w)).  States of C are
+ * keys (qa, qb, f1, qd, f2): (qa, qb, f1) is a state of T = A o B whose
+ * arcs are the three moves of two-input composition (header comment above,
+ * filter bit f1), and the key composes T with D by the same three rules,
+ * filter bit f2:
+ *   match  : a T-arc t with output z != 0, an arc ed of qd with ilabel z
+ *            -> (dst t, dst ed, 0); label in(t):olabel(ed);
+ *            weight w(t) + w(ed) (a T-match weighs w(ea) + w(eb), so the
+ *            adds are (w(ea) + w(eb)) + w(ed), binary32, in that order)
+ *   T alone: only when f2 = 0; a T-arc t with output 0 -> (dst t, qd, 0);
+ *            label in(t):0; weight w(t)
+ *   D alone: an arc ed of qd with ilabel 0 -> ((qa, qb, f1), dst ed,
+ *            epsOutT(qa, qb, f1)); label 0:olabel(ed); weight w(ed)
+ * where epsOutT says whether the T-state has a T-arc with output 0.  Start
+ * keys are (sa, sb, 0, sd, 0); a key accepts iff its three states accept;
+ * C is trim.  Output is canonical: states in ascending key order (qa, qb,
+ * f1, qd, f2); the arcs of a state by (a, b, d), the arcs of A, B and D
+ * they came from, a missing arc sorting last.  Key bits: bits(V_A - 1) +
+ * bits(V_B - 1) + bits(V_D - 1) + 2 <= 62 (each at least 1), else
+ * FST_ERR_TOO_LARGE.  The workspace grows with the number of keys reached
+ * (a hash set of 8 bytes per slot, at most 3/4 full, grown and searched
+ * again when it fills). */
+typedef struct {
+  int32_t *arc_offset;
+  int32_t *src, *dst, *ilabel, *olabel;
+  float *weight;
+  uint8_t *start, *accept;
+  int32_t *key_a, *key_b;   /* optional [V_C] (NULL skips): the key of     */
+  uint8_t *key_fab;         /* each state, (key_a, key_b, key_fab, key_d,  */
+  int32_t *key_d;           /* key_f) = (qa, qb, f1, qd, f2)               */
+  uint8_t *key_f;
+  int32_t *arc_a, *arc_b, *arc_d; /* optional [E_C] provenance, -1 = none  */
+} fst_graph3_out;
+
+/* Phase 1 of C = A o B o D: validate the three graphs, search forward from
+ * the start keys and backward over the generated arcs, number the trim
+ * keys and count their arcs.  Blocks until *num_states and *num_arcs are
+ * known.  A, B and D must stay valid and unchanged until
+ * fst_compose3_fill's work has completed. */
+FST_API int fst_compose3_run(fst_ctx *ctx, const fst_graph *A, const fst_graph *B,
+                             const fst_graph *D, void *stream, int64_t *num_states,
+                             int64_t *num_arcs);
+
+/* Phase 2: write C into caller-allocated arrays sized from phase 1
+ * (asynchronous on `stream`). */
+FST_API int fst_compose3_fill(fst_ctx *ctx, const fst_graph3_out *C, void *stream);
+
+/* Statistics of the last successful fst_compose3_run: key_space = 2^(key
+ * bits), accessible = keys reached, coaccessible = num_states = V_C,
+ * generated = moves out of the accessible keys, fwd_levels and bwd_levels
+ * = levels of the two searches, num_arcs = E_C (heavy_states 0,
+ * generated_backward -1). */
+FST_API int fst_compose3_stats(const fst_ctx *ctx, fst_stats *out);
 
 /* Static string for a status code. */
 FST_API const char *fst_strerror(int code);

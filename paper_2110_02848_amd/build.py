@@ -15,7 +15,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libfstcompose.so")
-SOURCES = ["primitives.hip", "compose.hip", "score.hip", "api.cpp"]
+SOURCES = ["primitives.hip", "compose.hip", "compose3.hip", "score.hip", "api.cpp"]
 ARCH = "gfx950"
 
 

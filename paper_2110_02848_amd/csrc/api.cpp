@@ -32,8 +32,9 @@ struct DevBuf {
 };
 
 constexpr int NEV = 10;  // a begin and an end event per phase (enum in fst_compose_phase_times)
-constexpr int NKERNELS = 6;  // enum fst_kernel
-constexpr int NCOMPOSE_KERNELS = 4;  // kernels 0-3 time a composition, 4-5 a score
+constexpr int NKERNELS = 8;  // enum fst_kernel
+constexpr int NCOMPOSE_KERNELS = 4;  // kernels 0-3 time a composition, 4-5 a score,
+                                     // 6-7 a three-input composition
 
 // Per-direction working arrays of the score recursion.
 struct ScoreBufs {
@@ -67,6 +68,22 @@ struct fst_ctx {
       s_mpos;
   // batches: the union of the A graphs, item tables, segment sums
   DevBuf u_off, u_src, u_dst, u_il, u_ol, u_w, u_start, u_accept, u_items, seg;
+  // three-input composition
+  DevBuf t_scal, t_aPerm, t_aArc, t_aRec, t_bPerm, t_bArc, t_bRec, t_bLab, t_bW, t_dPerm,
+      t_dArc, t_dRec, t_dLab, t_dW, t_bflags, t_lists, t_tab, t_F, t_chunks, t_arcs, t_inoff,
+      t_cursor, t_insrc, t_coacc, t_keys0, t_keys1, t_slots0, t_slots1, t_idof, t_units, t_ucnt;
+  Scal3 *h_s3 = nullptr;
+  uint32_t h3_hint = 0;  // hash capacity the last three-input search needed
+  struct {
+    bool ready = false;
+    Problem3 P = {};
+    const unsigned long long *keys = nullptr;
+    const uint32_t *ustart = nullptr, *uoff = nullptr;
+    uint32_t n = 0, U = 0, narcs = 0;
+    fst_stats stats = {};
+    bool timed = false;
+  } c3;
+  bool have_times3 = false;
   Scalars *h_sc = nullptr;
   ScoreScalars *h_ssc = nullptr;
   ScoreBufs score_f, score_b;  // forward / backward recursion
@@ -800,6 +817,276 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   return FST_OK;
 }
 
+// ---------------------------------------------------------------------------
+// three inputs
+// ---------------------------------------------------------------------------
+
+int readback3(fst_ctx *c, hipStream_t s) {
+  HIP_TRY(hipMemcpyAsync(c->h_s3, c->t_scal.p, sizeof(Scal3), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  return FST_OK;
+}
+
+// One label-sorted out-view of g (side 0: by olabel, 1: by ilabel) into the
+// given buffers; lab/w (the other side's label and the weight in sorted
+// order) only when lab is given.
+int view3(fst_ctx *c, const DevGraph &g, int side, bool presorted, uint32_t maxlab, DevBuf &perm,
+          DevBuf &arc, DevBuf &rec, DevBuf *lab, DevBuf *w, View &v, hipStream_t s) {
+  FST_TRY(ensure(c, perm, (size_t)g.E * 4));
+  FST_TRY(ensure(c, arc, (size_t)g.E * 8));
+  FST_TRY(ensure(c, rec, (size_t)g.V * 2 * sizeof(int4)));
+  int32_t *olab = nullptr;
+  float *wv = nullptr;
+  if (lab) {
+    FST_TRY(ensure(c, *lab, (size_t)g.E * 4));
+    FST_TRY(ensure(c, *w, (size_t)g.E * 4));
+    olab = as<int32_t>(*lab);
+    wv = as<float>(*w);
+  }
+  HIP_TRY(sort_view(g, side, false, presorted, bitlen(maxlab), as<int4>(rec), as<int2>(arc),
+                    as<int32_t>(perm), olab, wv, nullptr, nullptr, as<unsigned long long>(c->k0),
+                    as<int32_t>(c->v0), as<unsigned long long>(c->k1), as<int32_t>(c->v1),
+                    c->sort_tmp.p, nullptr, s));
+  v = View{as<int4>(rec), as<int2>(arc), as<int32_t>(perm), nullptr, 0, olab, wv, nullptr};
+  return FST_OK;
+}
+
+// Levels of a three-input search in batches (4, 16, 32, 64, 64, ...) with
+// one read-back after each batch; *done tells whether it ended (false: a
+// capacity was exceeded).
+int levels3(fst_ctx *c, const Problem3 &P, const Search3 &S, bool forward, uint32_t grow_at,
+            bool *done, hipStream_t s) {
+  const KernelTimer t = timer(c, FST_KERNEL_SEARCH3);
+  int g = 0, batch = 4;
+  *done = false;
+  for (;;) {
+    t.begin(s);
+    for (int b = 0; b < batch; ++b, ++g) HIP_TRY(launch3_level(P, S, forward, g, s));
+    t.end(s);
+    FST_TRY(readback3(c, s));
+    FST_TRY(add_time(c, FST_KERNEL_SEARCH3, 2 * batch));
+    const Lvl3 &nx = c->h_s3->ring[g % 3];
+    if (c->h_s3->overflow || (unsigned long long)nx.fbase + nx.fcount > grow_at) return FST_OK;
+    if (nx.fcount == 0) break;
+    batch = batch == 4 ? 16 : (batch < 64 ? 2 * batch : 64);
+  }
+  *done = true;
+  return FST_OK;
+}
+
+int compose3_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, const fst_graph *D,
+                  hipStream_t s, int64_t *V_C, int64_t *E_C) {
+  FST_TRY(check_graph_args(A));
+  FST_TRY(check_graph_args(B));
+  FST_TRY(check_graph_args(D));
+  const DevGraph dA = dev_graph(A), dB = dev_graph(B), dD = dev_graph(D);
+  FST_TRY(ensure(c, c->t_scal, sizeof(Scal3)));
+  Scal3 *d3 = as<Scal3>(c->t_scal);
+  for (int k = 6; k < NKERNELS; ++k) {
+    c->kms[k] = 0.f;
+    c->klaunches[k] = 0;
+  }
+  HIP_TRY(hipMemsetAsync(d3, 0, sizeof(Scal3), s));
+  if (dA.V) HIP_TRY(launch_validate(dA, 0, &d3->errA, &d3->maxA, s));
+  if (dB.V) HIP_TRY(launch_validate(dB, 1, &d3->errB, &d3->maxB, s));
+  if (dD.V) HIP_TRY(launch_validate(dD, 1, &d3->errD, &d3->maxD, s));
+  FST_TRY(readback3(c, s));
+  const uint32_t info = 1u << 16;  // validation's "not in label order" note
+  const Scal3 v = *c->h_s3;
+  if ((v.errA & ~info) || (v.errB & ~info) || (v.errD & ~info)) return FST_ERR_INVALID_GRAPH;
+  c->c3.stats = fst_stats{};
+  if (dA.V == 0 || dB.V == 0 || dD.V == 0) {
+    c->c3.n = c->c3.U = c->c3.narcs = 0;
+    c->c3.ready = true;
+    return FST_OK;
+  }
+  if (dA.V > NBR_MASK || dB.V > NBR_MASK || dD.V > NBR_MASK) return FST_ERR_TOO_LARGE;
+  const int bA = bitlen((unsigned long long)(dA.V - 1)) > 0 ? bitlen((unsigned long long)(dA.V - 1)) : 1;
+  const int bB = bitlen((unsigned long long)(dB.V - 1)) > 0 ? bitlen((unsigned long long)(dB.V - 1)) : 1;
+  const int bD = bitlen((unsigned long long)(dD.V - 1)) > 0 ? bitlen((unsigned long long)(dD.V - 1)) : 1;
+  const int kbits = bA + bB + bD + 2;
+  if (kbits > 62) return FST_ERR_TOO_LARGE;
+  c->c3.stats.key_space = (int64_t)1 << kbits;
+
+  // label-sorted views
+  int32_t EA = dA.E, EB = dB.E, ED = dD.E;
+  const size_t Emax = (size_t)(EA > EB ? (EA > ED ? EA : ED) : (EB > ED ? EB : ED));
+  FST_TRY(ensure(c, c->k0, Emax * 8));
+  FST_TRY(ensure(c, c->k1, Emax * 8));
+  FST_TRY(ensure(c, c->v0, Emax * 4));
+  FST_TRY(ensure(c, c->v1, Emax * 4));
+  FST_TRY(ensure(c, c->sort_tmp, sort_temp_bytes(Emax)));
+  Problem3 P = {};
+  P.A = dA;
+  P.B = dB;
+  P.D = dD;
+  FST_TRY(view3(c, dA, 0, !(v.errA & info), v.maxA, c->t_aPerm, c->t_aArc, c->t_aRec, nullptr,
+                nullptr, P.aOut, s));
+  FST_TRY(view3(c, dB, 1, !(v.errB & info), v.maxB, c->t_bPerm, c->t_bArc, c->t_bRec,
+                &c->t_bLab, &c->t_bW, P.bOut, s));
+  FST_TRY(view3(c, dD, 1, !(v.errD & info), v.maxD, c->t_dPerm, c->t_dArc, c->t_dRec,
+                &c->t_dLab, &c->t_dW, P.dOut, s));
+  FST_TRY(ensure(c, c->t_bflags, (size_t)dB.V * 4));
+  HIP_TRY(hipMemsetAsync(c->t_bflags.p, 0, (size_t)dB.V * 4, s));
+  HIP_TRY(launch3_bflags(dB, as<uint32_t>(c->t_bflags), s));
+  P.bflags = as<uint32_t>(c->t_bflags);
+  P.shB = (uint32_t)bB;
+  P.shD = (uint32_t)bD;
+  FST_TRY(ensure(c, c->t_lists, ((size_t)dA.V + dB.V + dD.V) * 4 + 16));
+  int32_t *lists = as<int32_t>(c->t_lists);
+  uint32_t *counts = reinterpret_cast<uint32_t *>(lists + dA.V + dB.V + dD.V);
+
+  // forward search; a table that fills up (or lists that overflow) is
+  // grown four-fold and the search starts again
+  const KernelTimer tout = timer(c, FST_KERNEL_COMPACT3);
+  unsigned long long H = c->h3_hint ? c->h3_hint : (1ull << 20);
+  Search3 S = {};
+  for (;;) {
+    if (H > (1ull << 31)) return FST_ERR_TOO_LARGE;
+    const unsigned long long acap = 4 * H;
+    FST_TRY(ensure(c, c->t_tab, H * 8));
+    FST_TRY(ensure(c, c->t_F, H * 4));
+    FST_TRY(ensure(c, c->t_chunks, H * 8));
+    FST_TRY(ensure(c, c->t_arcs, acap * 8));
+    HIP_TRY(hipMemsetAsync(c->t_tab.p, 0xff, H * 8, s));
+    HIP_TRY(hipMemsetAsync(&d3->overflow, 0, offsetof(Scal3, ring) - offsetof(Scal3, overflow) +
+                                                 sizeof(d3->ring), s));
+    HIP_TRY(hipMemsetAsync(counts, 0, 3 * 4, s));
+    P.tab = as<unsigned long long>(c->t_tab);
+    P.hmask = (uint32_t)(H - 1);
+    S.F = as<uint32_t>(c->t_F);
+    S.fcap = (uint32_t)H;
+    S.chunks = as<uint2>(c->t_chunks);
+    S.ccap = (uint32_t)H;
+    S.arcs = as<uint2>(c->t_arcs);
+    S.acap = acap;
+    S.ring = d3->ring;
+    S.sc = d3;
+    HIP_TRY(launch3_starts(dA, dB, dD, lists, counts, s));
+    HIP_TRY(launch3_seed(P, S, lists, counts, s));
+    bool done = false;
+    // a table at most 3/4 full keeps probe sequences short
+    FST_TRY(levels3(c, P, S, true, (uint32_t)(H / 4 * 3), &done, s));
+    if (done) break;
+    H *= 4;
+  }
+  c->h3_hint = (uint32_t)H;
+  const Scal3 f = *c->h_s3;
+  c->c3.stats.fwd_levels = f.levels;
+  const unsigned long long nacc = f.ring[0].fbase > f.ring[1].fbase
+                                      ? (f.ring[0].fbase > f.ring[2].fbase ? f.ring[0].fbase
+                                                                           : f.ring[2].fbase)
+                                      : (f.ring[1].fbase > f.ring[2].fbase ? f.ring[1].fbase
+                                                                           : f.ring[2].fbase);
+  c->c3.stats.accessible = (int64_t)nacc;
+  const unsigned long long narcs = f.narcs;
+  c->c3.stats.generated = (int64_t)narcs;
+
+  // backward search over the generated arcs, grouped by target
+  tout.begin(s);
+  FST_TRY(ensure(c, c->t_inoff, (H + 1) * 4));
+  FST_TRY(ensure(c, c->t_cursor, H * 4));
+  FST_TRY(ensure(c, c->t_insrc, (narcs + 1) * 4));
+  FST_TRY(ensure(c, c->t_coacc, (H / 32 + 1) * 4));
+  FST_TRY(ensure(c, c->scan_tmp, scan_temp_bytes(H + 1)));
+  const unsigned long long ccap = H + narcs / 32 + 1;
+  if (ccap > 0xffffffffull) return FST_ERR_TOO_LARGE;
+  FST_TRY(ensure(c, c->t_chunks, ccap * 8));
+  uint32_t *inoff = as<uint32_t>(c->t_inoff);
+  HIP_TRY(hipMemsetAsync(inoff, 0, (H + 1) * 4, s));
+  HIP_TRY(launch3_in_arcs(S.arcs, narcs, inoff, nullptr, false, s));
+  HIP_TRY(scan_u32(inoff, inoff, H, true, &d3->total, c->scan_tmp.p, s));
+  HIP_TRY(hipMemcpyAsync(c->t_cursor.p, inoff, H * 4, hipMemcpyDeviceToDevice, s));
+  HIP_TRY(launch3_in_arcs(S.arcs, narcs, as<uint32_t>(c->t_cursor), as<uint32_t>(c->t_insrc),
+                          true, s));
+  HIP_TRY(hipMemsetAsync(c->t_coacc.p, 0, (H / 32 + 1) * 4, s));
+  HIP_TRY(hipMemsetAsync(&d3->overflow, 0, offsetof(Scal3, ring) - offsetof(Scal3, overflow) +
+                                               sizeof(d3->ring), s));
+  P.coacc = as<uint32_t>(c->t_coacc);
+  P.in_off = inoff;
+  P.in_src = as<uint32_t>(c->t_insrc);
+  S.chunks = as<uint2>(c->t_chunks);
+  S.ccap = (uint32_t)ccap;
+  tout.end(s);
+  HIP_TRY(launch3_seed_bwd(P, S, s));
+  bool done = false;
+  FST_TRY(levels3(c, P, S, false, 0xffffffffu, &done, s));
+  if (!done) return FST_ERR_TOO_LARGE;  // every list holds each slot at most once
+  c->c3.stats.bwd_levels = c->h_s3->levels;
+  FST_TRY(add_time(c, FST_KERNEL_COMPACT3, 1));
+
+  // trim keys, sorted: a state's id is its rank
+  tout.begin(s);
+  FST_TRY(ensure(c, c->t_keys0, (nacc + 1) * 8));
+  FST_TRY(ensure(c, c->t_keys1, (nacc + 1) * 8));
+  FST_TRY(ensure(c, c->t_slots0, (nacc + 1) * 4));
+  FST_TRY(ensure(c, c->t_slots1, (nacc + 1) * 4));
+  FST_TRY(ensure(c, c->sort_tmp, sort_temp_bytes(nacc + 1)));
+  HIP_TRY(hipMemsetAsync(&d3->ntrim, 0, 4, s));
+  HIP_TRY(launch3_collect(P, as<unsigned long long>(c->t_keys0), as<int32_t>(c->t_slots0),
+                          &d3->ntrim, (uint32_t)nacc, &d3->overflow, s));
+  tout.end(s);
+  FST_TRY(readback3(c, s));
+  FST_TRY(add_time(c, FST_KERNEL_COMPACT3, 1));
+  if (c->h_s3->overflow) return FST_ERR_TOO_LARGE;
+  const uint32_t n = c->h_s3->ntrim;
+  c->c3.stats.coaccessible = n;
+  c->c3.stats.num_states = n;
+  c->c3.stats.generated_backward = -1;
+  if (n == 0) {
+    c->c3.n = c->c3.U = c->c3.narcs = 0;
+    c->c3.ready = true;
+    return FST_OK;
+  }
+  tout.begin(s);
+  bool second = false;
+  HIP_TRY(radix_sort(as<unsigned long long>(c->t_keys0), as<int32_t>(c->t_slots0),
+                     as<unsigned long long>(c->t_keys1), as<int32_t>(c->t_slots1), n, kbits,
+                     c->sort_tmp.p, s, &second));
+  const unsigned long long *keys = as<unsigned long long>(second ? c->t_keys1 : c->t_keys0);
+  const int32_t *slots = as<int32_t>(second ? c->t_slots1 : c->t_slots0);
+  FST_TRY(ensure(c, c->t_idof, H * 4));
+  FST_TRY(ensure(c, c->t_units, ((size_t)n + 1) * 4));
+  FST_TRY(ensure(c, c->scan_tmp, scan_temp_bytes((size_t)n + 1)));
+  HIP_TRY(hipMemsetAsync(c->t_idof.p, 0xff, H * 4, s));
+  uint32_t *units = as<uint32_t>(c->t_units);
+  HIP_TRY(launch3_ids(P, keys, slots, n, as<int32_t>(c->t_idof), units, s));
+  P.id_of = as<int32_t>(c->t_idof);
+  HIP_TRY(scan_u32(units, units, n, true, &d3->total, c->scan_tmp.p, s));
+  tout.end(s);
+  FST_TRY(readback3(c, s));
+  FST_TRY(add_time(c, FST_KERNEL_COMPACT3, 1));
+  const unsigned long long U = c->h_s3->total;
+  if (U >= 0xffffffffull) return FST_ERR_TOO_LARGE;
+
+  // arcs kept by every work unit, scanned into positions
+  tout.begin(s);
+  FST_TRY(ensure(c, c->t_ucnt, (U + 1) * 4));
+  FST_TRY(ensure(c, c->scan_tmp, scan_temp_bytes(U + 1)));
+  uint32_t *ucnt = as<uint32_t>(c->t_ucnt);
+  HIP_TRY(launch3_count(P, keys, units, n, (uint32_t)U, ucnt, s));
+  HIP_TRY(scan_u32(ucnt, ucnt, U, true, &d3->total, c->scan_tmp.p, s));
+  tout.end(s);
+  FST_TRY(readback3(c, s));
+  FST_TRY(add_time(c, FST_KERNEL_COMPACT3, 1));
+  const unsigned long long E = c->h_s3->total;
+  if (E > (unsigned long long)INT32_MAX) return FST_ERR_TOO_LARGE;
+  c->c3.P = P;
+  c->c3.keys = keys;
+  c->c3.ustart = units;
+  c->c3.uoff = ucnt;
+  c->c3.n = n;
+  c->c3.U = (uint32_t)U;
+  c->c3.narcs = (uint32_t)E;
+  c->c3.stats.num_arcs = (int64_t)E;
+  c->c3.timed = c->timing;
+  c->have_times3 = c->timing;
+  c->c3.ready = true;
+  *V_C = n;
+  *E_C = (int64_t)E;
+  return FST_OK;
+}
+
 // Batch: validate every item, lay the items out as one disjoint union (state
 // and arc offsets shifted), compose the union with B, then find each item's
 // state and arc range in C.
@@ -926,6 +1213,11 @@ int fst_ctx_create(int device, fst_ctx **ctx) {
     return FST_ERR_NOMEM;
   }
   memset(c->h_ssc, 0, sizeof(ScoreScalars));
+  if (hipHostMalloc(reinterpret_cast<void **>(&c->h_s3), sizeof(Scal3), 0) != hipSuccess) {
+    fst_ctx_destroy(c);
+    return FST_ERR_NOMEM;
+  }
+  memset(c->h_s3, 0, sizeof(Scal3));
   for (ScoreBufs *b : {&c->score_f, &c->score_b}) {
     if (hipHostMalloc(reinterpret_cast<void **>(&b->host), sizeof(ScoreScalars), 0) !=
         hipSuccess) {
@@ -975,7 +1267,13 @@ void fst_ctx_destroy(fst_ctx *c) {
                     &c->s_acc,    &c->s_pg,     &c->s_pidx,  &c->s_bcnt,  &c->s_bscan,
                     &c->s_btotal, &c->s_mpos,   &c->u_off,   &c->u_src,   &c->u_dst,
                     &c->u_il,     &c->u_ol,     &c->u_w,     &c->u_start, &c->u_accept,
-                    &c->u_items,  &c->seg};
+                    &c->u_items,  &c->seg,    &c->t_scal,  &c->t_aPerm, &c->t_aArc,
+                    &c->t_aRec,   &c->t_bPerm,  &c->t_bArc,  &c->t_bRec,  &c->t_bLab,
+                    &c->t_bW,     &c->t_dPerm,  &c->t_dArc,  &c->t_dRec,  &c->t_dLab,
+                    &c->t_dW,     &c->t_bflags, &c->t_lists, &c->t_tab,   &c->t_F,
+                    &c->t_chunks, &c->t_arcs,   &c->t_inoff, &c->t_cursor, &c->t_insrc,
+                    &c->t_coacc,  &c->t_keys0,  &c->t_keys1, &c->t_slots0, &c->t_slots1,
+                    &c->t_idof,   &c->t_units,  &c->t_ucnt};
   for (DevBuf *b : bufs) release(*b);
   for (ScoreBufs *sb : {&c->score_f, &c->score_b}) {
     for (DevBuf *b : {&sb->sc, &sb->rec, &sb->term, &sb->mkey, &sb->pend, &sb->q, &sb->h,
@@ -989,6 +1287,7 @@ void fst_ctx_destroy(fst_ctx *c) {
     if (c->kev[i]) (void)hipEventDestroy(c->kev[i]);
   if (c->h_sc) (void)hipHostFree(c->h_sc);
   if (c->h_ssc) (void)hipHostFree(c->h_ssc);
+  if (c->h_s3) (void)hipHostFree(c->h_s3);
   delete c;
 }
 
@@ -1117,6 +1416,81 @@ int fst_compose_fill(fst_ctx *c, const fst_graph_out *C, void *stream) {
   return FST_OK;
 }
 
+int fst_compose3_run(fst_ctx *c, const fst_graph *A, const fst_graph *B, const fst_graph *D,
+                     void *stream, int64_t *num_states, int64_t *num_arcs) {
+  if (!c || !A || !B || !D || !num_states || !num_arcs) return FST_ERR_INVALID_ARG;
+  DeviceGuard g(c->device);
+  if (!g.ok) return FST_ERR_HIP;
+  c->c3.ready = false;
+  c->have_times3 = false;
+  *num_states = 0;
+  *num_arcs = 0;
+  int rc = compose3_impl(c, A, B, D, reinterpret_cast<hipStream_t>(stream), num_states,
+                         num_arcs);
+  if (rc != FST_OK) {
+    c->c3.ready = false;
+    *num_states = 0;
+    *num_arcs = 0;
+    (void)hipGetLastError();
+  }
+  return rc;
+}
+
+int fst_compose3_fill(fst_ctx *c, const fst_graph3_out *C, void *stream) {
+  if (!c || !C) return FST_ERR_INVALID_ARG;
+  if (!c->c3.ready) return FST_ERR_STATE;
+  if (!C->arc_offset) return FST_ERR_INVALID_ARG;
+  if (c->c3.n && (!C->start || !C->accept)) return FST_ERR_INVALID_ARG;
+  if (c->c3.narcs && (!C->src || !C->dst || !C->ilabel || !C->olabel || !C->weight))
+    return FST_ERR_INVALID_ARG;
+  DeviceGuard g(c->device);
+  if (!g.ok) return FST_ERR_HIP;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (c->c3.n == 0) {
+    HIP_TRY(hipMemsetAsync(C->arc_offset, 0, sizeof(int32_t), s));
+    return FST_OK;
+  }
+  OutGraph3 O;
+  O.arc_offset = C->arc_offset;
+  O.src = C->src;
+  O.dst = C->dst;
+  O.il = C->ilabel;
+  O.ol = C->olabel;
+  O.w = C->weight;
+  O.start = C->start;
+  O.accept = C->accept;
+  O.key_a = C->key_a;
+  O.key_b = C->key_b;
+  O.key_fab = C->key_fab;
+  O.key_d = C->key_d;
+  O.key_f = C->key_f;
+  O.arc_a = C->arc_a;
+  O.arc_b = C->arc_b;
+  O.arc_d = C->arc_d;
+  const KernelTimer t = c->c3.timed ? timer(c, FST_KERNEL_COMPACT3) : KernelTimer{};
+  t.begin(s);
+  hipError_t e = launch3_fill(c->c3.P, c->c3.keys, c->c3.ustart, c->c3.n, c->c3.U, c->c3.uoff,
+                              c->c3.narcs, O, s);
+  t.end(s);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return FST_ERR_HIP;
+  }
+  if (c->c3.timed) {
+    // the fill's launches join the time of the compaction kernels
+    HIP_TRY(hipEventSynchronize(c->kev[2 * FST_KERNEL_COMPACT3 + 1]));
+    FST_TRY(add_time(c, FST_KERNEL_COMPACT3, 2));
+  }
+  return FST_OK;
+}
+
+int fst_compose3_stats(const fst_ctx *c, fst_stats *out) {
+  if (!c || !out) return FST_ERR_INVALID_ARG;
+  if (!c->c3.ready) return FST_ERR_STATE;
+  *out = c->c3.stats;
+  return FST_OK;
+}
+
 int fst_compose_stats(const fst_ctx *c, fst_stats *out) {
   if (!c || !out) return FST_ERR_INVALID_ARG;
   if (!c->ready) return FST_ERR_STATE;
@@ -1140,7 +1514,10 @@ int fst_compose_phase_times(const fst_ctx *c, float *ms, int n) {
 
 int fst_compose_kernel_time(const fst_ctx *c, int kernel, float *ms, int64_t *launches) {
   if (!c || !ms || !launches || kernel < 0 || kernel >= NKERNELS) return FST_ERR_INVALID_ARG;
-  if (!(kernel < NCOMPOSE_KERNELS ? c->have_times : c->have_score_times)) return FST_ERR_STATE;
+  const bool have = kernel < NCOMPOSE_KERNELS ? c->have_times
+                    : kernel < 6                ? c->have_score_times
+                                                : c->have_times3;
+  if (!have) return FST_ERR_STATE;
   float t = c->kms[kernel];
   if (kernel == FST_KERNEL_FILL) {
     // the fill is asynchronous: its events are read here

@@ -1,0 +1,686 @@
+// Kernels of the simultaneous composition of three transducers, C = A o B o
+// D (the N-way composition the paper names as the next step after its
+// two-input one, Section 5), for gfx950.
+//
+// A state of C is a key (qa, qb, f1, qd, f2).  (qa, qb, f1) is a state of
+// T = A o B, read on the fly: its arcs are the two-input moves (a matching
+// pair of arcs of A and B; an A arc with output epsilon, only when f1 = 0;
+// a B arc with input epsilon, setting f1 = epsOutA(qa)).  The key composes
+// T with D by the same three rules with filter bit f2: a T-arc whose output
+// z is not epsilon with a D arc of input z; a T-arc with output epsilon
+// alone, only when f2 = 0; a D arc with input epsilon alone, setting f2 =
+// epsOutT(qa, qb, f1) (whether that T-state has an arc with output
+// epsilon).  Weights: a T-match is w(a) + w(b), a match with D adds w(d)
+// after it; single arcs copy their weight.
+//
+// The key space is the product of three state sets, far too large for a
+// bitmap, so keys are 64-bit, packed so that numeric order is (qa, qb, f1,
+// qd, f2) order, and deduplicated in an open-addressing hash set whose slot
+// index names the state during the search.  The search goes level by level:
+// one thread per frontier state, or, for a state with more than LIGHT3
+// units of work, one thread per chunk of LIGHT3 units (work units: the
+// state's arcs of A in index order, then its B arcs with input epsilon,
+// then its D arcs with input epsilon).  New keys are appended to the next
+// frontier and every generated arc (source slot, target slot) to an arc
+// list, one atomic per wavefront.  Co-accessibility runs backwards over
+// that arc list (in-arcs grouped by a count, a scan and a placement).  The
+// trim keys are sorted (radix sort of the 64-bit keys): a state's id is its
+// rank.  Count and fill give every work unit of every trim state one
+// thread; units enumerate in canonical (a, b, d) order (an A arc, its B
+// bucket by arc index, the D bucket of each B arc's output, by arc index;
+// then B arcs with input epsilon; then D arcs with input epsilon), so a
+// scan of the per-unit counts gives every arc's position.
+#include "internal.h"
+
+namespace fstc {
+
+namespace {
+
+typedef unsigned long long ull;
+
+constexpr ull EMPTY3 = ~0ull;
+constexpr uint32_t NO_SLOT = 0xFFFFFFFFu;
+constexpr uint32_t LIGHT3 = 32;   // work units one thread takes
+constexpr int PROBE_MAX = 4096;   // hash probes before the table counts as full
+constexpr uint32_t BF_EPS_EPS = 1u, BF_EPS_OUT = 2u;  // B state flags
+
+unsigned grid3(size_t n, unsigned cap = 4096) {
+  size_t g = (n + NT - 1) / NT;
+  if (g < 1) g = 1;
+  if (g > cap) g = cap;
+  return (unsigned)g;
+}
+
+// The state id in an arc record's neighbour field.
+__device__ __forceinline__ uint32_t nbr_of_arc(int32_t y) { return (uint32_t)(y & NBR_MASK); }
+
+__device__ __forceinline__ ull mix64(ull x) {
+  x ^= x >> 30;
+  x *= 0xbf58476d1ce4e5b9ull;
+  x ^= x >> 27;
+  x *= 0x94d049bb133111ebull;
+  x ^= x >> 31;
+  return x;
+}
+
+__device__ __forceinline__ ull pack3(const Problem3 &P, uint32_t qa, uint32_t qb, uint32_t f1,
+                                     uint32_t qd, uint32_t f2) {
+  return (((((ull)qa << P.shB | qb) << 1 | f1) << P.shD | qd) << 1) | f2;
+}
+
+struct Key3 {
+  uint32_t qa, qb, f1, qd, f2;
+};
+
+__device__ __forceinline__ Key3 unpack3(const Problem3 &P, ull k) {
+  Key3 s;
+  s.f2 = (uint32_t)(k & 1ull);
+  k >>= 1;
+  s.qd = (uint32_t)(k & ((1ull << P.shD) - 1ull));
+  k >>= P.shD;
+  s.f1 = (uint32_t)(k & 1ull);
+  k >>= 1;
+  s.qb = (uint32_t)(k & ((1ull << P.shB) - 1ull));
+  s.qa = (uint32_t)(k >> P.shB);
+  return s;
+}
+
+// Slot of key k: inserted if absent (fresh), NO_SLOT (and the overflow
+// flag) if PROBE_MAX slots in a row are taken.  A plain load first: a slot
+// never changes once set, so a stale EMPTY only sends the thread to the CAS.
+__device__ __forceinline__ uint32_t h_insert(const Problem3 &P, ull k, bool &fresh,
+                                             uint32_t *overflow) {
+  uint32_t h = (uint32_t)mix64(k) & P.hmask;
+  fresh = false;
+  for (int p = 0; p < PROBE_MAX; ++p) {
+    const ull cur = P.tab[h];
+    if (cur == k) return h;
+    if (cur == EMPTY3) {
+      const ull old = atomicCAS(P.tab + h, EMPTY3, k);
+      if (old == EMPTY3) {
+        fresh = true;
+        return h;
+      }
+      if (old == k) return h;
+    }
+    h = (h + 1) & P.hmask;
+  }
+  atomicOr(overflow, 1u);
+  return NO_SLOT;
+}
+
+// Slot of key k, or NO_SLOT if it is not in the set.
+__device__ __forceinline__ uint32_t h_find(const Problem3 &P, ull k) {
+  uint32_t h = (uint32_t)mix64(k) & P.hmask;
+  for (int p = 0; p < PROBE_MAX; ++p) {
+    const ull cur = P.tab[h];
+    if (cur == k) return h;
+    if (cur == EMPTY3) return NO_SLOT;
+    h = (h + 1) & P.hmask;
+  }
+  return NO_SLOT;
+}
+
+// Append x for every lane with `want`, one atomic per wavefront; false (and
+// the overflow flag) past the capacity.
+template <class T>
+__device__ __forceinline__ void wave_append(bool want, T x, T *list, ull cap, uint32_t *count,
+                                            uint32_t *overflow) {
+  const ull m = __ballot(want);
+  if (m == 0) return;
+  const int leader = __ffsll(m) - 1;
+  uint32_t base = 0;
+  if ((int)__lane_id() == leader) base = atomicAdd(count, (uint32_t)__popcll(m));
+  base = __shfl(base, leader, WAVE);
+  if (want) {
+    const ull pos = (ull)base + (ull)__popcll(m & __lanemask_lt());
+    if (pos < cap) list[pos] = x;
+    else atomicOr(overflow, 1u);
+  }
+}
+
+// A state's arc group in a label-sorted view: [begin, end), the first
+// `neps` arcs with label epsilon.
+struct Grp {
+  int32_t begin, neps, end, flags;
+};
+__device__ __forceinline__ Grp grp_of(const View &v, uint32_t q) {
+  const int4 r = v.srec[2 * (size_t)q];
+  return Grp{r.x, r.y, r.z, r.w};
+}
+
+// [lo, hi) of label lab among the non-epsilon arcs [lo, hi) of a group.
+__device__ __forceinline__ void bucket(const View &v, int32_t lo, int32_t hi, int32_t lab,
+                                       int32_t &r0, int32_t &r1) {
+  int32_t a = lo, b = hi;
+  while (a < b) {
+    const int32_t mid = a + ((b - a) >> 1);
+    if (v.arec[mid].x < lab) a = mid + 1; else b = mid;
+  }
+  r0 = a;
+  b = hi;
+  while (a < b) {
+    const int32_t mid = a + ((b - a) >> 1);
+    if (v.arec[mid].x <= lab) a = mid + 1; else b = mid;
+  }
+  r1 = a;
+}
+
+// epsOutT(qa, qb, f1): some T-arc out of (qa, qb, f1) has output epsilon.
+__device__ __forceinline__ uint32_t eps_out_t(const Problem3 &P, uint32_t qa, uint32_t qb,
+                                              uint32_t f1) {
+  const Grp ga = grp_of(P.aOut, qa);
+  if (f1 == 0 && ga.neps > 0) return 1u;
+  const uint32_t bf = P.bflags[qb];
+  if (bf & BF_EPS_EPS) return 1u;
+  if (!(bf & BF_EPS_OUT)) return 0u;
+  // a B arc with input y != eps and output eps, and an A arc with output y
+  const Grp gb = grp_of(P.bOut, qb);
+  for (int32_t p = gb.begin + gb.neps; p < gb.end; ++p) {
+    if (P.bOut.olab[p] != 0) continue;
+    int32_t r0, r1;
+    bucket(P.aOut, ga.begin + ga.neps, ga.end, P.bOut.arec[p].x, r0, r1);
+    if (r0 < r1) return 1u;
+  }
+  return 0u;
+}
+
+// The work units of a key: its A arcs, its B arcs with input epsilon, its
+// D arcs with input epsilon.
+struct Units3 {
+  Key3 k;
+  int32_t a0, na;     // A arcs [a0, a0 + na) in index order
+  Grp gb, gd;
+};
+__device__ __forceinline__ Units3 units_of(const Problem3 &P, ull key) {
+  Units3 u;
+  u.k = unpack3(P, key);
+  u.a0 = P.A.off[u.k.qa];
+  u.na = P.A.off[u.k.qa + 1] - u.a0;
+  u.gb = grp_of(P.bOut, u.k.qb);
+  u.gd = grp_of(P.dOut, u.k.qd);
+  return u;
+}
+__device__ __forceinline__ uint32_t nunits(const Units3 &u) {
+  return (uint32_t)u.na + (uint32_t)u.gb.neps + (uint32_t)u.gd.neps;
+}
+
+// Calls f(target key, ilabel, olabel, weight, a, b, d) for every move of
+// unit j of a key, in canonical (a, b, d) order (arc ids; -1 = none).
+template <class F>
+__device__ __forceinline__ void for_unit3(const Problem3 &P, const Units3 &u, uint32_t j, F &&f) {
+  const Key3 &k = u.k;
+  if (j < (uint32_t)u.na) {
+    const int32_t ea = u.a0 + (int32_t)j;
+    const int32_t y = P.A.ol[ea], ia = P.A.il[ea], da = P.A.dst[ea];
+    const float wa = P.A.w[ea];
+    if (y == 0) {
+      // T-epsA (f1 = 0), output epsilon: T alone (f2 = 0)
+      if (k.f1 == 0 && k.f2 == 0) f(pack3(P, da, k.qb, 0, k.qd, 0), ia, 0, wa, ea, -1, -1);
+      return;
+    }
+    int32_t b0, b1;
+    bucket(P.bOut, u.gb.begin + u.gb.neps, u.gb.end, y, b0, b1);
+    for (int32_t p = b0; p < b1; ++p) {
+      const int32_t eb = P.bOut.perm[p], z = P.bOut.olab[p];
+      const uint32_t db = nbr_of_arc(P.bOut.arec[p].y);
+      const float wt = wa + P.bOut.w[p];
+      if (z == 0) {
+        if (k.f2 == 0) f(pack3(P, da, db, 0, k.qd, 0), ia, 0, wt, ea, eb, -1);
+        continue;
+      }
+      int32_t d0, d1;
+      bucket(P.dOut, u.gd.begin + u.gd.neps, u.gd.end, z, d0, d1);
+      for (int32_t r = d0; r < d1; ++r)
+        f(pack3(P, da, db, 0, nbr_of_arc(P.dOut.arec[r].y), 0), ia, P.dOut.olab[r],
+          wt + P.dOut.w[r], ea, eb, P.dOut.perm[r]);
+    }
+    return;
+  }
+  j -= (uint32_t)u.na;
+  if (j < (uint32_t)u.gb.neps) {
+    // T-epsB: (qa, dst b, epsOutA(qa))
+    const int32_t p = u.gb.begin + (int32_t)j;
+    const int32_t eb = P.bOut.perm[p], z = P.bOut.olab[p];
+    const uint32_t db = nbr_of_arc(P.bOut.arec[p].y);
+    const uint32_t nf1 = (grp_of(P.aOut, k.qa).neps > 0) ? 1u : 0u;
+    const float wb = P.bOut.w[p];
+    if (z == 0) {
+      if (k.f2 == 0) f(pack3(P, k.qa, db, nf1, k.qd, 0), 0, 0, wb, -1, eb, -1);
+      return;
+    }
+    int32_t d0, d1;
+    bucket(P.dOut, u.gd.begin + u.gd.neps, u.gd.end, z, d0, d1);
+    for (int32_t r = d0; r < d1; ++r)
+      f(pack3(P, k.qa, db, nf1, nbr_of_arc(P.dOut.arec[r].y), 0), 0, P.dOut.olab[r],
+        wb + P.dOut.w[r], -1, eb, P.dOut.perm[r]);
+    return;
+  }
+  j -= (uint32_t)u.gb.neps;
+  // D alone (input epsilon): f2 = epsOutT of the key's T-state
+  const int32_t r = u.gd.begin + (int32_t)j;
+  const uint32_t nf2 = eps_out_t(P, k.qa, k.qb, k.f1);
+  f(pack3(P, k.qa, k.qb, k.f1, nbr_of_arc(P.dOut.arec[r].y), nf2), 0, P.dOut.olab[r],
+    P.dOut.w[r], -1, -1, P.dOut.perm[r]);
+}
+
+__device__ __forceinline__ bool key_accepts(const Problem3 &P, const Key3 &k) {
+  return P.A.accept[k.qa] && P.B.accept[k.qb] && P.D.accept[k.qd];
+}
+
+// ---------------------------------------------------------------------------
+// preprocessing
+// ---------------------------------------------------------------------------
+
+// B state flags: an arc eps:eps (BF_EPS_EPS), an arc y:eps with y != eps
+// (BF_EPS_OUT).
+__global__ __launch_bounds__(NT) void k3_bflags(DevGraph B, uint32_t *bflags) {
+  for (long long e = (long long)blockIdx.x * NT + threadIdx.x; e < B.E;
+       e += (long long)gridDim.x * NT) {
+    if (B.ol[e] != 0) continue;
+    atomicOr(bflags + B.src[e], B.il[e] == 0 ? BF_EPS_EPS : BF_EPS_OUT);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// forward search
+// ---------------------------------------------------------------------------
+
+// Start states of one graph into a list (count zeroed by the caller).
+__global__ __launch_bounds__(NT) void k3_starts(const uint8_t *flags, int V, int32_t *list,
+                                                uint32_t *count) {
+  for (long long v0 = (long long)blockIdx.x * NT; v0 < V; v0 += (long long)gridDim.x * NT) {
+    const long long v = v0 + threadIdx.x;
+    const bool want = v < V && flags[v] != 0;
+    const ull m = __ballot(want);
+    if (m == 0) continue;
+    const int leader = __ffsll(m) - 1;
+    uint32_t base = 0;
+    if ((int)__lane_id() == leader) base = atomicAdd(count, (uint32_t)__popcll(m));
+    base = __shfl(base, leader, WAVE);
+    if (want) list[base + __popcll(m & __lanemask_lt())] = (int32_t)v;
+  }
+}
+
+// Start keys (sa, sb, 0, sd, 0) for every triple of start states: lists of
+// A's, B's and D's start states at lists, lists + V_A, lists + V_A + V_B,
+// their counts in counts[0..2].
+__global__ __launch_bounds__(NT) void k3_seed(Problem3 P, Search3 S, const int32_t *lists,
+                                              const uint32_t *counts) {
+  const ull na = counts[0], nb = counts[1], nd = counts[2], n = na * nb * nd;
+  const int32_t *la = lists, *lb = lists + P.A.V, *ld = lists + P.A.V + P.B.V;
+  for (ull i0 = (ull)blockIdx.x * NT; i0 < n; i0 += (ull)gridDim.x * NT) {
+    const ull i = i0 + threadIdx.x;
+    bool push = false;
+    uint32_t slot = 0;
+    if (i < n) {
+      const uint32_t qa = (uint32_t)la[i / (nb * nd)], qb = (uint32_t)lb[(i / nd) % nb],
+                     qd = (uint32_t)ld[i % nd];
+      bool fresh;
+      slot = h_insert(P, pack3(P, qa, qb, 0, qd, 0), fresh, &S.sc->overflow);
+      push = fresh && slot != NO_SLOT;
+    }
+    wave_append<uint32_t>(push, slot, S.F, S.fcap, &S.ring[0].fcount, &S.sc->overflow);
+  }
+}
+
+// The moves of units [u0, u1) of the key in `slot`: every target is looked
+// up / inserted; new keys join the next frontier; every move is recorded as
+// an arc (source slot, target slot).
+__device__ __forceinline__ void expand_units(const Problem3 &P, const Search3 &S, uint32_t slot,
+                                             const Units3 &u, uint32_t u0, uint32_t u1, Lvl3 *nx,
+                                             uint32_t nbase) {
+  for (uint32_t j = u0; j < u1; ++j)
+    for_unit3(P, u, j, [&](ull t, int32_t, int32_t, float, int32_t, int32_t, int32_t) {
+      bool fresh;
+      const uint32_t ts = h_insert(P, t, fresh, &S.sc->overflow);
+      if (ts == NO_SLOT) return;
+      wave_append<uint2>(true, make_uint2(slot, ts), S.arcs, S.acap, &S.sc->narcs,
+                         &S.sc->overflow);
+      wave_append<uint32_t>(fresh, ts, S.F + nbase, (ull)S.fcap - nbase, &nx->fcount,
+                            &S.sc->overflow);
+    });
+}
+
+// Level l of the forward search: frontier entries [fbase, fbase + fcount)
+// of ring[l % 3]; light keys are expanded here, heavy ones cut into chunks
+// of LIGHT3 units for k3_fwd_chunks.  Block 0 publishes the next level's
+// frontier base and clears the ring slot of level l + 2.
+__global__ __launch_bounds__(NT) void k3_fwd(Problem3 P, Search3 S, int l) {
+  const Lvl3 cur = S.ring[l % 3];
+  Lvl3 *nx = &S.ring[(l + 1) % 3];
+  const uint32_t nbase = cur.fbase + cur.fcount;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    nx->fbase = nbase;
+    Lvl3 *done = &S.ring[(l + 2) % 3];
+    done->fcount = 0;
+    done->ccount = 0;
+    if (cur.fcount) S.sc->levels = (uint32_t)l + 1;
+  }
+  if (S.sc->overflow) return;
+  for (ull i = (ull)blockIdx.x * NT + threadIdx.x; i < cur.fcount; i += (ull)gridDim.x * NT) {
+    const uint32_t slot = S.F[cur.fbase + i];
+    const Units3 u = units_of(P, P.tab[slot]);
+    const uint32_t n = nunits(u);
+    if (n > LIGHT3) {
+      const uint32_t nc = (n + LIGHT3 - 1) / LIGHT3;
+      const uint32_t c0 = atomicAdd(&S.ring[l % 3].ccount, nc);
+      for (uint32_t c = 0; c < nc; ++c) {
+        if ((ull)c0 + c < S.ccap) S.chunks[c0 + c] = make_uint2((uint32_t)i, c * LIGHT3);
+        else atomicOr(&S.sc->overflow, 1u);
+      }
+      continue;
+    }
+    expand_units(P, S, slot, u, 0, n, nx, nbase);
+  }
+}
+
+__global__ __launch_bounds__(NT) void k3_fwd_chunks(Problem3 P, Search3 S, int l) {
+  const Lvl3 cur = S.ring[l % 3];
+  Lvl3 *nx = &S.ring[(l + 1) % 3];
+  const uint32_t nbase = cur.fbase + cur.fcount;
+  if (S.sc->overflow) return;
+  const uint32_t nch = cur.ccount < S.ccap ? cur.ccount : S.ccap;
+  for (ull i = (ull)blockIdx.x * NT + threadIdx.x; i < nch; i += (ull)gridDim.x * NT) {
+    const uint2 c = S.chunks[i];
+    const uint32_t slot = S.F[cur.fbase + c.x];
+    const Units3 u = units_of(P, P.tab[slot]);
+    const uint32_t n = nunits(u);
+    const uint32_t u1 = c.y + LIGHT3 < n ? c.y + LIGHT3 : n;
+    expand_units(P, S, slot, u, c.y, u1, nx, nbase);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// backward search over the recorded arcs
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(NT) void k3_indeg(const uint2 *arcs, ull narcs, uint32_t *indeg) {
+  for (ull e = (ull)blockIdx.x * NT + threadIdx.x; e < narcs; e += (ull)gridDim.x * NT)
+    atomicAdd(indeg + arcs[e].y, 1u);
+}
+
+__global__ __launch_bounds__(NT) void k3_place(const uint2 *arcs, ull narcs, uint32_t *cursor,
+                                               uint32_t *in_src) {
+  for (ull e = (ull)blockIdx.x * NT + threadIdx.x; e < narcs; e += (ull)gridDim.x * NT) {
+    const uint2 a = arcs[e];
+    in_src[atomicAdd(cursor + a.y, 1u)] = a.x;
+  }
+}
+
+__device__ __forceinline__ bool claim_bit(uint32_t *bm, uint32_t s) {
+  const uint32_t bit = 1u << (s & 31u);
+  if (bm[s >> 5] & bit) return false;
+  return (atomicOr(bm + (s >> 5), bit) & bit) == 0;
+}
+
+// Accepting keys seed the backward search (level 0 of its ring).
+__global__ __launch_bounds__(NT) void k3_seed_bwd(Problem3 P, Search3 S) {
+  const ull H = (ull)P.hmask + 1;
+  for (ull i0 = (ull)blockIdx.x * NT; i0 < H; i0 += (ull)gridDim.x * NT) {
+    const ull s = i0 + threadIdx.x;
+    bool push = false;
+    if (s < H) {
+      const ull k = P.tab[s];
+      if (k != EMPTY3 && key_accepts(P, unpack3(P, k))) {
+        atomicOr(P.coacc + (s >> 5), 1u << (s & 31u));
+        push = true;
+      }
+    }
+    wave_append<uint32_t>(push, (uint32_t)s, S.F, S.fcap, &S.ring[0].fcount, &S.sc->overflow);
+  }
+}
+
+__device__ __forceinline__ void bwd_range(const Problem3 &P, const Search3 &S, uint32_t p0,
+                                          uint32_t p1, Lvl3 *nx, uint32_t nbase) {
+  for (uint32_t p = p0; p < p1; ++p) {
+    const uint32_t u = P.in_src[p];
+    const bool fresh = claim_bit(P.coacc, u);
+    wave_append<uint32_t>(fresh, u, S.F + nbase, (ull)S.fcap - nbase, &nx->fcount,
+                          &S.sc->overflow);
+  }
+}
+
+__global__ __launch_bounds__(NT) void k3_bwd(Problem3 P, Search3 S, int l) {
+  const Lvl3 cur = S.ring[l % 3];
+  Lvl3 *nx = &S.ring[(l + 1) % 3];
+  const uint32_t nbase = cur.fbase + cur.fcount;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    nx->fbase = nbase;
+    Lvl3 *done = &S.ring[(l + 2) % 3];
+    done->fcount = 0;
+    done->ccount = 0;
+    if (cur.fcount) S.sc->levels = (uint32_t)l + 1;
+  }
+  if (S.sc->overflow) return;
+  for (ull i = (ull)blockIdx.x * NT + threadIdx.x; i < cur.fcount; i += (ull)gridDim.x * NT) {
+    const uint32_t v = S.F[cur.fbase + i];
+    const uint32_t p0 = P.in_off[v], p1 = P.in_off[v + 1];
+    if (p1 - p0 > LIGHT3) {
+      const uint32_t nc = (p1 - p0 + LIGHT3 - 1) / LIGHT3;
+      const uint32_t c0 = atomicAdd(&S.ring[l % 3].ccount, nc);
+      for (uint32_t c = 0; c < nc; ++c) {
+        if ((ull)c0 + c < S.ccap) S.chunks[c0 + c] = make_uint2((uint32_t)i, c * LIGHT3);
+        else atomicOr(&S.sc->overflow, 1u);
+      }
+      continue;
+    }
+    bwd_range(P, S, p0, p1, nx, nbase);
+  }
+}
+
+__global__ __launch_bounds__(NT) void k3_bwd_chunks(Problem3 P, Search3 S, int l) {
+  const Lvl3 cur = S.ring[l % 3];
+  Lvl3 *nx = &S.ring[(l + 1) % 3];
+  const uint32_t nbase = cur.fbase + cur.fcount;
+  if (S.sc->overflow) return;
+  const uint32_t nch = cur.ccount < S.ccap ? cur.ccount : S.ccap;
+  for (ull i = (ull)blockIdx.x * NT + threadIdx.x; i < nch; i += (ull)gridDim.x * NT) {
+    const uint2 c = S.chunks[i];
+    const uint32_t v = S.F[cur.fbase + c.x];
+    const uint32_t p0 = P.in_off[v] + c.y, pe = P.in_off[v + 1];
+    const uint32_t p1 = p0 + LIGHT3 < pe ? p0 + LIGHT3 : pe;
+    bwd_range(P, S, p0, p1, nx, nbase);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// trim, numbering, count, fill
+// ---------------------------------------------------------------------------
+
+// Trim keys (in the set and co-accessible) with their slots.
+__global__ __launch_bounds__(NT) void k3_collect(Problem3 P, ull *keys, int32_t *slots,
+                                                 uint32_t *count, uint32_t cap,
+                                                 uint32_t *overflow) {
+  const ull H = (ull)P.hmask + 1;
+  for (ull i0 = (ull)blockIdx.x * NT; i0 < H; i0 += (ull)gridDim.x * NT) {
+    const ull s = i0 + threadIdx.x;
+    ull k = EMPTY3;
+    bool want = false;
+    if (s < H) {
+      k = P.tab[s];
+      want = k != EMPTY3 && ((P.coacc[s >> 5] >> (s & 31u)) & 1u);
+    }
+    const ull m = __ballot(want);
+    if (m == 0) continue;
+    const int leader = __ffsll(m) - 1;
+    uint32_t base = 0;
+    if ((int)__lane_id() == leader) base = atomicAdd(count, (uint32_t)__popcll(m));
+    base = __shfl(base, leader, WAVE);
+    if (want) {
+      const uint32_t pos = base + (uint32_t)__popcll(m & __lanemask_lt());
+      if (pos < cap) {
+        keys[pos] = k;
+        slots[pos] = (int32_t)s;
+      } else {
+        atomicOr(overflow, 1u);
+      }
+    }
+  }
+}
+
+// id_of[slot] = rank of the slot's key among the trim keys; units of every
+// state of C.
+__global__ __launch_bounds__(NT) void k3_ids(Problem3 P, const ull *keys, const int32_t *slots,
+                                             uint32_t n, int32_t *id_of, uint32_t *units) {
+  for (ull i = (ull)blockIdx.x * NT + threadIdx.x; i < n; i += (ull)gridDim.x * NT) {
+    id_of[slots[i]] = (int32_t)i;
+    units[i] = nunits(units_of(P, keys[i]));
+  }
+}
+
+// The state of C owning unit u: the last i with ustart[i] <= u.
+__device__ __forceinline__ uint32_t state_of_unit(const uint32_t *ustart, uint32_t n, uint32_t u) {
+  uint32_t lo = 0, hi = n;  // ustart[lo] <= u < ustart[hi]
+  while (hi - lo > 1) {
+    const uint32_t mid = lo + ((hi - lo) >> 1);
+    if (ustart[mid] <= u) lo = mid; else hi = mid;
+  }
+  return lo;
+}
+
+__device__ __forceinline__ int32_t id_of_key(const Problem3 &P, ull t) {
+  const uint32_t s = h_find(P, t);
+  return s == NO_SLOT ? -1 : P.id_of[s];
+}
+
+__global__ __launch_bounds__(NT) void k3_count(Problem3 P, const ull *keys, const uint32_t *ustart,
+                                               uint32_t n, uint32_t U, uint32_t *ucnt) {
+  for (ull u = (ull)blockIdx.x * NT + threadIdx.x; u < U; u += (ull)gridDim.x * NT) {
+    const uint32_t i = state_of_unit(ustart, n, (uint32_t)u);
+    const Units3 st = units_of(P, keys[i]);
+    uint32_t c = 0;
+    for_unit3(P, st, (uint32_t)u - ustart[i],
+              [&](ull t, int32_t, int32_t, float, int32_t, int32_t, int32_t) {
+                c += id_of_key(P, t) >= 0 ? 1u : 0u;
+              });
+    ucnt[u] = c;
+  }
+}
+
+__global__ __launch_bounds__(NT) void k3_fill(Problem3 P, const ull *keys, const uint32_t *ustart,
+                                              uint32_t n, uint32_t U, const uint32_t *uoff,
+                                              OutGraph3 O) {
+  for (ull u = (ull)blockIdx.x * NT + threadIdx.x; u < U; u += (ull)gridDim.x * NT) {
+    const uint32_t i = state_of_unit(ustart, n, (uint32_t)u);
+    const Units3 st = units_of(P, keys[i]);
+    uint32_t pos = uoff[u];
+    for_unit3(P, st, (uint32_t)u - ustart[i],
+              [&](ull t, int32_t il, int32_t ol, float w, int32_t a, int32_t b, int32_t d) {
+                const int32_t id = id_of_key(P, t);
+                if (id < 0) return;
+                O.src[pos] = (int32_t)i;
+                O.dst[pos] = id;
+                O.il[pos] = il;
+                O.ol[pos] = ol;
+                O.w[pos] = w;
+                if (O.arc_a) O.arc_a[pos] = a;
+                if (O.arc_b) O.arc_b[pos] = b;
+                if (O.arc_d) O.arc_d[pos] = d;
+                ++pos;
+              });
+  }
+}
+
+__global__ __launch_bounds__(NT) void k3_fill_states(Problem3 P, const ull *keys,
+                                                     const uint32_t *ustart, uint32_t n,
+                                                     const uint32_t *uoff, uint32_t narcs,
+                                                     OutGraph3 O) {
+  for (ull i = (ull)blockIdx.x * NT + threadIdx.x; i <= n; i += (ull)gridDim.x * NT) {
+    if (i == n) {
+      O.arc_offset[n] = (int32_t)narcs;
+      continue;
+    }
+    const Key3 k = unpack3(P, keys[i]);
+    O.arc_offset[i] = (int32_t)uoff[ustart[i]];
+    O.start[i] = (k.f1 == 0 && k.f2 == 0 && P.A.start[k.qa] && P.B.start[k.qb] &&
+                  P.D.start[k.qd]) ? 1 : 0;
+    O.accept[i] = key_accepts(P, k) ? 1 : 0;
+    if (O.key_a) O.key_a[i] = (int32_t)k.qa;
+    if (O.key_b) O.key_b[i] = (int32_t)k.qb;
+    if (O.key_fab) O.key_fab[i] = (uint8_t)k.f1;
+    if (O.key_d) O.key_d[i] = (int32_t)k.qd;
+    if (O.key_f) O.key_f[i] = (uint8_t)k.f2;
+  }
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// launchers
+// ---------------------------------------------------------------------------
+
+hipError_t launch3_bflags(const DevGraph &B, uint32_t *bflags, hipStream_t s) {
+  if (B.E) k3_bflags<<<grid3((size_t)B.E), NT, 0, s>>>(B, bflags);
+  return hipGetLastError();
+}
+
+hipError_t launch3_starts(const DevGraph &A, const DevGraph &B, const DevGraph &D,
+                          int32_t *lists, uint32_t *counts, hipStream_t s) {
+  k3_starts<<<grid3((size_t)A.V, 1024), NT, 0, s>>>(A.start, A.V, lists, counts);
+  k3_starts<<<grid3((size_t)B.V, 1024), NT, 0, s>>>(B.start, B.V, lists + A.V, counts + 1);
+  k3_starts<<<grid3((size_t)D.V, 1024), NT, 0, s>>>(D.start, D.V, lists + A.V + B.V, counts + 2);
+  return hipGetLastError();
+}
+
+hipError_t launch3_seed(const Problem3 &P, const Search3 &S, const int32_t *lists,
+                        const uint32_t *counts, hipStream_t s) {
+  k3_seed<<<64, NT, 0, s>>>(P, S, lists, counts);
+  return hipGetLastError();
+}
+
+hipError_t launch3_level(const Problem3 &P, const Search3 &S, bool forward, int l,
+                         hipStream_t s) {
+  constexpr unsigned GRID = 1024;
+  if (forward) {
+    k3_fwd<<<GRID, NT, 0, s>>>(P, S, l);
+    k3_fwd_chunks<<<GRID, NT, 0, s>>>(P, S, l);
+  } else {
+    k3_bwd<<<GRID, NT, 0, s>>>(P, S, l);
+    k3_bwd_chunks<<<GRID, NT, 0, s>>>(P, S, l);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch3_in_arcs(const uint2 *arcs, unsigned long long narcs, uint32_t *indeg_or_cursor,
+                           uint32_t *in_src, bool place, hipStream_t s) {
+  if (!narcs) return hipSuccess;
+  if (place) k3_place<<<grid3((size_t)narcs), NT, 0, s>>>(arcs, narcs, indeg_or_cursor, in_src);
+  else k3_indeg<<<grid3((size_t)narcs), NT, 0, s>>>(arcs, narcs, indeg_or_cursor);
+  return hipGetLastError();
+}
+
+hipError_t launch3_seed_bwd(const Problem3 &P, const Search3 &S, hipStream_t s) {
+  k3_seed_bwd<<<grid3((size_t)P.hmask + 1, 8192), NT, 0, s>>>(P, S);
+  return hipGetLastError();
+}
+
+hipError_t launch3_collect(const Problem3 &P, unsigned long long *keys, int32_t *slots,
+                           uint32_t *count, uint32_t cap, uint32_t *overflow, hipStream_t s) {
+  k3_collect<<<grid3((size_t)P.hmask + 1, 8192), NT, 0, s>>>(P, keys, slots, count, cap,
+                                                             overflow);
+  return hipGetLastError();
+}
+
+hipError_t launch3_ids(const Problem3 &P, const unsigned long long *keys, const int32_t *slots,
+                       uint32_t n, int32_t *id_of, uint32_t *units, hipStream_t s) {
+  if (n) k3_ids<<<grid3(n), NT, 0, s>>>(P, keys, slots, n, id_of, units);
+  return hipGetLastError();
+}
+
+hipError_t launch3_count(const Problem3 &P, const unsigned long long *keys,
+                         const uint32_t *ustart, uint32_t n, uint32_t U, uint32_t *ucnt,
+                         hipStream_t s) {
+  if (U) k3_count<<<grid3(U, 8192), NT, 0, s>>>(P, keys, ustart, n, U, ucnt);
+  return hipGetLastError();
+}
+
+hipError_t launch3_fill(const Problem3 &P, const unsigned long long *keys, const uint32_t *ustart,
+                        uint32_t n, uint32_t U, const uint32_t *uoff, uint32_t narcs,
+                        const OutGraph3 &O, hipStream_t s) {
+  if (U) k3_fill<<<grid3(U, 8192), NT, 0, s>>>(P, keys, ustart, n, U, uoff, O);
+  k3_fill_states<<<grid3((size_t)n + 1, 8192), NT, 0, s>>>(P, keys, ustart, n, uoff, narcs, O);
+  return hipGetLastError();
+}
+
+}  // namespace fstc

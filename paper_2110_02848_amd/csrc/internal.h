@@ -185,6 +185,66 @@ struct SearchArgs {
 };
 
 // ---------------------------------------------------------------------------
+// Three inputs, C = A o B o D (compose3.hip)
+// ---------------------------------------------------------------------------
+
+// Everything the three-input kernels read, passed by value.  Keys are
+// ((((qa << shB | qb) << 1 | f1) << shD | qd) << 1 | f2), 64-bit; a key's
+// state is named by its slot in the hash set tab (hmask + 1 slots, empty =
+// all ones) until the numbering.
+struct Problem3 {
+  DevGraph A, B, D;
+  View aOut;  // A by (src, olabel): epsOutA and the output-label lookups of epsOutT
+  View bOut;  // B by (src, ilabel), with B's olabel and weight in sorted order
+  View dOut;  // D by (src, ilabel), with D's olabel and weight in sorted order
+  const uint32_t *bflags;  // per B state: an eps:eps arc (1), a y:eps arc, y != eps (2)
+  uint32_t shB, shD;
+  unsigned long long *tab;
+  uint32_t hmask;
+  uint32_t *coacc;          // co-accessible slots (bitmap)
+  const uint32_t *in_off;   // in-arcs of each slot: in_src[in_off[s] .. in_off[s + 1])
+  const uint32_t *in_src;
+  const int32_t *id_of;     // slot -> state id of C (-1: not trim)
+};
+
+// A level of a three-input search in a ring of three: its frontier entries
+// F[fbase, fbase + fcount) and the number of heavy-state chunks it listed.
+struct Lvl3 {
+  uint32_t fbase, fcount, ccount, pad;
+};
+
+// Device scalars of a three-input composition, read back by the host.
+struct Scal3 {
+  uint32_t errA, errB, errD, maxA, maxB, maxD;
+  uint32_t overflow, levels, narcs, ntrim;
+  unsigned long long total;  // scan totals
+  Lvl3 ring[3];
+};
+
+struct Search3 {
+  uint32_t *F;       // frontier slots, level after level
+  uint32_t fcap;
+  uint2 *chunks;     // (frontier index, first unit) of the chunks of heavy states
+  uint32_t ccap;
+  uint2 *arcs;       // generated arcs (source slot, target slot)
+  unsigned long long acap;
+  Lvl3 *ring;
+  Scal3 *sc;
+};
+
+// Output arrays of a three-input C.
+struct OutGraph3 {
+  int32_t *arc_offset, *src, *dst, *il, *ol;
+  float *w;
+  uint8_t *start, *accept;
+  int32_t *key_a, *key_b;
+  uint8_t *key_fab;
+  int32_t *key_d;
+  uint8_t *key_f;
+  int32_t *arc_a, *arc_b, *arc_d;
+};
+
+// ---------------------------------------------------------------------------
 // Scores of an acyclic graph (score.hip)
 // ---------------------------------------------------------------------------
 
@@ -474,6 +534,33 @@ hipError_t launch_item_ranges(const Problem &P, unsigned long long nkeys, int32_
                               const long long *qa_base, const uint32_t *cnt,
                               const uint32_t *btot, size_t per, uint32_t nstates,
                               uint32_t narcs, long long *out, hipStream_t s);
+
+// Three-input launchers (compose3.hip).
+hipError_t launch3_bflags(const DevGraph &B, uint32_t *bflags, hipStream_t s);
+// Start keys of every triple of start states (lists and counts from
+// launch3_starts) into level 0 of S.
+hipError_t launch3_starts(const DevGraph &A, const DevGraph &B, const DevGraph &D,
+                          int32_t *lists, uint32_t *counts, hipStream_t s);
+hipError_t launch3_seed(const Problem3 &P, const Search3 &S, const int32_t *lists,
+                        const uint32_t *counts, hipStream_t s);
+// Level l of the forward (or backward) search: two kernels.
+hipError_t launch3_level(const Problem3 &P, const Search3 &S, bool forward, int l,
+                         hipStream_t s);
+// In-arc counts of every slot (place = false: indeg_or_cursor counts), or
+// the placement of every arc's source (place = true: cursor = in_off).
+hipError_t launch3_in_arcs(const uint2 *arcs, unsigned long long narcs, uint32_t *indeg_or_cursor,
+                           uint32_t *in_src, bool place, hipStream_t s);
+hipError_t launch3_seed_bwd(const Problem3 &P, const Search3 &S, hipStream_t s);
+hipError_t launch3_collect(const Problem3 &P, unsigned long long *keys, int32_t *slots,
+                           uint32_t *count, uint32_t cap, uint32_t *overflow, hipStream_t s);
+hipError_t launch3_ids(const Problem3 &P, const unsigned long long *keys, const int32_t *slots,
+                       uint32_t n, int32_t *id_of, uint32_t *units, hipStream_t s);
+hipError_t launch3_count(const Problem3 &P, const unsigned long long *keys,
+                         const uint32_t *ustart, uint32_t n, uint32_t U, uint32_t *ucnt,
+                         hipStream_t s);
+hipError_t launch3_fill(const Problem3 &P, const unsigned long long *keys, const uint32_t *ustart,
+                        uint32_t n, uint32_t U, const uint32_t *uoff, uint32_t narcs,
+                        const OutGraph3 &O, hipStream_t s);
 
 // Score launchers (score.hip).
 // In-arc structure of G: owner (V words, all -1) and extra (V words, all 0)

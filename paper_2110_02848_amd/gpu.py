@@ -43,6 +43,7 @@ PHASES = ("preprocess", "forward", "backward", "count", "fill")
 # kernels timed one by one (enum fst_kernel): a composition's, then a score's
 KERNELS = ("search_forward", "search_backward", "count", "fill")
 SCORE_KERNELS = ("score_gen", "score_prep")
+KERNELS3 = ("search3", "compact3")
 
 
 class FstError(RuntimeError):
@@ -67,6 +68,12 @@ class _GraphOut(ctypes.Structure):
                 ("key_a", ctypes.c_void_p), ("key_b", ctypes.c_void_p),
                 ("key_f", ctypes.c_void_p), ("arc_a", ctypes.c_void_p),
                 ("arc_b", ctypes.c_void_p)]
+
+
+class _GraphOut3(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in (
+        "arc_offset", "src", "dst", "ilabel", "olabel", "weight", "start", "accept", "key_a",
+        "key_b", "key_fab", "key_d", "key_f", "arc_a", "arc_b", "arc_d")]
 
 
 class _Stats(ctypes.Structure):
@@ -134,6 +141,16 @@ def load():
                                        ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
                                        ctypes.c_void_p]
     lib.fst_segment_logsum.restype = ctypes.c_int
+    lib.fst_compose3_run.argtypes = [ctypes.c_void_p, ctypes.POINTER(_Graph),
+                                     ctypes.POINTER(_Graph), ctypes.POINTER(_Graph),
+                                     ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64),
+                                     ctypes.POINTER(ctypes.c_int64)]
+    lib.fst_compose3_run.restype = ctypes.c_int
+    lib.fst_compose3_fill.argtypes = [ctypes.c_void_p, ctypes.POINTER(_GraphOut3),
+                                      ctypes.c_void_p]
+    lib.fst_compose3_fill.restype = ctypes.c_int
+    lib.fst_compose3_stats.argtypes = [ctypes.c_void_p, ctypes.POINTER(_Stats)]
+    lib.fst_compose3_stats.restype = ctypes.c_int
     lib.fst_strerror.argtypes = [ctypes.c_int]
     lib.fst_strerror.restype = ctypes.c_char_p
     _lib = lib
@@ -313,6 +330,60 @@ class Composer:
             out[name] = (float(ms.value), int(n.value))
         return out
 
+
+    # ---- three inputs at once: C = A o B o D ----
+
+    def run3(self, A, B, D, stream=None):
+        """Phase 1 of C = A o B o D.  Returns (V_C, E_C)."""
+        ga, gb, gd = _graph_struct(A), _graph_struct(B), _graph_struct(D)
+        nv, ne = ctypes.c_int64(), ctypes.c_int64()
+        rc = self._lib.fst_compose3_run(self._h, ctypes.byref(ga), ctypes.byref(gb),
+                                        ctypes.byref(gd), _stream_handle(stream),
+                                        ctypes.byref(nv), ctypes.byref(ne))
+        _check(rc, "fst_compose3_run")
+        return int(nv.value), int(ne.value)
+
+    def alloc_output3(self, nv, ne, provenance=True, keys=True):
+        import torch
+        C = self.alloc_output(nv, ne, provenance=provenance, keys=keys)
+        dev = f"cuda:{self.device}"
+        if keys:
+            C.update(key_fab=torch.empty(nv, dtype=torch.uint8, device=dev),
+                     key_d=torch.empty(nv, dtype=torch.int32, device=dev))
+        if provenance:
+            C["arc_d"] = torch.empty(ne, dtype=torch.int32, device=dev)
+        return C
+
+    def fill3(self, C, stream=None):
+        o = _GraphOut3()
+        for k, _ in _GraphOut3._fields_:
+            setattr(o, k, _ptr(C.get(k)))
+        o.arc_offset = ctypes.c_void_p(C["arc_offset"].data_ptr())
+        _check(self._lib.fst_compose3_fill(self._h, ctypes.byref(o), _stream_handle(stream)),
+               "fst_compose3_fill")
+        return C
+
+    def compose3(self, A, B, D, provenance=True, keys=True, stream=None):
+        """C = A o B o D (composed at once) as a dict of device tensors."""
+        nv, ne = self.run3(A, B, D, stream)
+        C = self.alloc_output3(nv, ne, provenance, keys)
+        return self.fill3(C, stream)
+
+    def stats3(self):
+        st = _Stats()
+        _check(self._lib.fst_compose3_stats(self._h, ctypes.byref(st)), "fst_compose3_stats")
+        return {n: int(getattr(st, n)) for n, _ in _Stats._fields_}
+
+    def kernel_times3(self):
+        """{kernel: (ms, launches)} of the last timed fst_compose3_run + fill."""
+        out = {}
+        for i, name in enumerate(KERNELS3):
+            ms, n = ctypes.c_float(), ctypes.c_int64()
+            _check(self._lib.fst_compose_kernel_time(self._h, 6 + i, ctypes.byref(ms),
+                                                     ctypes.byref(n)),
+                   "fst_compose_kernel_time")
+            out[name] = (float(ms.value), int(n.value))
+        return out
 
     # ---- scores of an acyclic graph and their gradient ----
 
