@@ -76,6 +76,8 @@ def kernel_bytes(st):
 
 def counters_file(workload, task="compose"):
     stem = workload.replace("-", "_")
+    if task == "compose3":
+        return os.path.join(ROOT, "profiles", f"counters_compose3_{stem}.txt")
     if task == "score":
         return os.path.join(ROOT, "profiles", f"counters_score_{stem}.txt")
     return os.path.join(ROOT, "profiles", f"counters_{stem}.txt")
@@ -330,6 +332,90 @@ def run_score(args, A, B, comp, dA, dB, copy_gbs):
     return out
 
 
+def compose3_kernel_bytes(st):
+    """Algorithmic bytes per three-input composition of each timed group.
+    search3 (both searches): per generated move, the target key probed in
+    the hash set (8 B) and the arc recorded (8 B); per accessible key, the
+    key stored and read back (16 B) and its frontier entry written and read
+    (8 B); backward, per generated arc its source placed and read (8 B)
+    and the claim probe of that source (4 B), per co-accessible key its
+    frontier entry (8 B).  compact3: the grouping of the arcs by target (8 B
+    read twice per arc), the trim keys collected and radix-sorted (8 passes
+    of 12 B read and written per key), and count and fill: one hash probe
+    per candidate arc in each (16 B per kept arc) plus the output CSR (20 B
+    per arc, 6 B per state + 4 B)."""
+    V, E = st["num_states"], st["num_arcs"]
+    G, acc = st["generated"], st["accessible"]
+    return {"search3": 16 * G + 24 * acc + 12 * G + 8 * V,
+            "compact3": 16 * G + 8 * 24 * V + 16 * E + 20 * E + 6 * V + 4 * (V + 1)}
+
+
+def cpu_baseline3(A, B, D, E_C):
+    import oracle
+    oracle.build(force=False)
+    raw = oracle.compose3_raw(A, B, D)
+    assert raw["num_arcs"] == E_C, (raw["num_arcs"], E_C)
+    ts = [raw["stats"]["compose_seconds"]]
+    del raw
+    for _ in range(_reps_for(ts[0], 8.0) - 1):
+        ts.append(oracle.compose3_raw(A, B, D)["stats"]["compose_seconds"])
+    t = float(np.median(ts))
+    out = {"value": E_C / t, "unit": "arcs/s", "cores": 1, "kind": "oracle",
+           "sample": f"the full three-input composition of the benchmark workload by the "
+                     f"sequential C oracle (forward search, then trim), single thread: median "
+                     f"of {len(ts)} runs",
+           "seconds_median": round(t, 4), "seconds_runs": [round(x, 4) for x in ts]}
+    out.update(host_info())
+    return out
+
+
+def run_compose3(args, comp, copy_gbs):
+    from paper_2110_02848_amd import gpu, synth
+    name = args.workload if args.workload in synth.GRAMMAR_SPECS else "grammar-T100-W1000-G20"
+    A, B, D, _ = synth.emissions_lexicon_grammar(name, args.seed)
+    dA, dB, dD = gpu.to_device(A), gpu.to_device(B), gpu.to_device(D)
+
+    def step():
+        nv, ne = comp.run3(dA, dB, dD)
+        C = comp.alloc_output3(nv, ne, provenance=False, keys=False)
+        comp.fill3(C)
+        return C
+
+    step()  # sizes the hash set once (later runs start at the size found)
+    for _ in range(args.warmup):
+        step()
+    ms_wall, per_step, C = timed_steps(step, args.steps)
+    st = comp.stats3()
+    kernels = instrumented_kernels(comp, step, args.steps, gpu.KERNELS3, comp.kernel_times3,
+                                   compose3_kernel_bytes(st))
+    out = {
+        "metric": "composed arcs/sec (emissions o lexicon o grammar, three inputs at once)",
+        "value": st["num_arcs"] / (ms_wall * 1e-3),
+        "unit": "arcs/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_wall,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": synth.GRAMMAR_TITLES[name], "name": name, "seed": args.seed,
+                   "task": "compose3", "V_A": A["num_states"], "V_B": B["num_states"],
+                   "V_D": D["num_states"], "V_C": st["num_states"], "E_C": st["num_arcs"],
+                   "inputs_sha256": {"A": synth.graph_sha256(A), "B": synth.graph_sha256(B),
+                                     "D": synth.graph_sha256(D)}},
+        "ms_per_composition_device": percentiles(per_step),
+        "kernels": kernels,
+        "search_stats": st,
+        "roofline": roofline_of(kernels, name, copy_gbs, "compose3"),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline3(A, B, D, st["num_arcs"])
+    return out
+
+
 def run_batch(args, comp):
     import torch
     from paper_2110_02848_amd import gpu, synth
@@ -419,10 +505,12 @@ def main():
                     help="order of the two searches (Algorithm 1 computes the co-accessible "
                          "set first; concurrent, the default, runs both side by side); the "
                          "result is the same")
-    ap.add_argument("--task", choices=("compose", "score", "batch"), default="compose",
+    ap.add_argument("--task", choices=("compose", "score", "batch", "compose3"),
+                    default="compose",
                     help="compose: the composition itself; score: scores and operand "
                          "gradients of the composed graph; batch: --batch utterances "
-                         "composed with one lexicon per step")
+                         "composed with one lexicon per step; compose3: emissions o lexicon "
+                         "o grammar composed at once (three inputs)")
     ap.add_argument("--batch", type=int, default=8)
     ap.add_argument("--copy-probe-mb", type=int, default=256,
                     help="size of the device-to-device copy timed for the copy ceiling (and "
@@ -439,6 +527,15 @@ def main():
     import torch
     from paper_2110_02848_amd import gpu, synth
 
+    if args.task == "compose3":
+        comp = gpu.Composer(0)
+        copy_gbs = copy_ceiling(args.copy_probe_mb) if args.copy_probe_mb > 0 else None
+        if args.calibrate_gather:
+            calibrate_gather()
+        out = run_compose3(args, comp, copy_gbs)
+        comp.close()
+        print(json.dumps(out), flush=True)
+        return
     if args.workload not in synth.WORKLOADS:
         ap.error(f"--workload must be one of {', '.join(synth.WORKLOADS)}")
     A, B = synth.workload(args.workload, args.seed)

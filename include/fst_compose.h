@@ -337,8 +337,10 @@ FST_API int fst_segment_logsum(fst_ctx *ctx, const double *val, const uint8_t *f
  * where epsOutT says whether the T-state has a T-arc with output 0.  Start
  * keys are (sa, sb, 0, sd, 0); a key accepts iff its three states accept;
  * C is trim.  Output is canonical: states in ascending key order (qa, qb,
- * f1, qd, f2); the arcs of a state by (a, b, d), the arcs of A, B and D
- * they came from, a missing arc sorting last.  Key bits: bits(V_A - 1) +
+ * f1, qd, f2); the arcs of a state by (l, a, b, d), where l is the label
+ * the arcs of A and B were matched on (0 when they were not both used) and
+ * a, b, d are the arcs of A, B and D the arc came from, a missing arc
+ * sorting last.  Key bits: bits(V_A - 1) +
  * bits(V_B - 1) + bits(V_D - 1) + 2 <= 62 (each at least 1), else
  * FST_ERR_TOO_LARGE.  The workspace grows with the number of keys reached
  * (a hash set of 8 bytes per slot, at most 3/4 full, grown and searched
@@ -371,8 +373,9 @@ FST_API int fst_compose3_fill(fst_ctx *ctx, const fst_graph3_out *C, void *strea
 /* Statistics of the last successful fst_compose3_run: key_space = 2^(key
  * bits), accessible = keys reached, coaccessible = num_states = V_C,
  * generated = moves out of the accessible keys, fwd_levels and bwd_levels
- * = levels of the two searches, num_arcs = E_C (heavy_states 0,
- * generated_backward -1). */
+ * = levels of the two searches, num_arcs = E_C, heavy_states = states of
+ * C with more work units than one thread takes (one workgroup each in the
+ * count and the fill), generated_backward -1. */
 FST_API int fst_compose3_stats(const fst_ctx *ctx, fst_stats *out);
 
 /* Static string for a status code. */

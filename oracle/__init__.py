@@ -20,8 +20,10 @@ Parity with the GPU path is checked on this canonical form.
 ``compose3(A, B, D)`` (``compose3.c``) is the simultaneous composition of
 three transducers, C = A o B o D (the N-way composition the paper names as
 the next step), canonical in the same way: states by key (qa, qb, f1, qd,
-f2), arcs of a state by (a, b, d), the arcs of A, B and D they came from,
-with a missing arc sorting last.
+f2), arcs of a state by (l, a, b, d), where l is the label the arcs of A
+and B were matched on (0 when A or B did not move, or moved alone) and a,
+b, d are the arcs of A, B and D the arc came from, a missing arc (-1)
+sorting last.
 
 ``score(G)``, ``posterior(G, ...)`` and ``scatter(...)`` (``score.c``) give
 the log-semiring forward and backward scores of an acyclic graph, the arc
@@ -300,9 +302,10 @@ def compose3_raw(A, B, D, mutation=MUT3_NONE):
     return out
 
 
-def canonicalize3(raw):
+def canonicalize3(raw, A):
     """Renumber states by key (qa, qb, f1, qd, f2) and sort the arcs of each
-    state by (a, b, d), a missing arc (-1) last."""
+    state by (l, a, b, d): l = olabel of the arc of A when arcs of A and B
+    were matched, else 0; a missing arc (-1) last."""
     V, E = raw["num_states"], raw["num_arcs"]
     order = np.lexsort((raw["key_f"], raw["key_d"], raw["key_fab"], raw["key_b"], raw["key_a"]))
     new_id = np.empty(V, np.int64)
@@ -315,7 +318,11 @@ def canonicalize3(raw):
         x = x.astype(np.int64)
         return np.where(x >= 0, x, big)
 
-    aorder = np.lexsort((k(raw["arc_d"]), k(raw["arc_b"]), k(raw["arc_a"]), src))
+    a, b = raw["arc_a"].astype(np.int64), raw["arc_b"].astype(np.int64)
+    match = (a >= 0) & (b >= 0)
+    lab = np.zeros(E, np.int64)
+    lab[match] = np.asarray(A["olabel"], dtype=np.int64)[a[match]]
+    aorder = np.lexsort((k(raw["arc_d"]), k(raw["arc_b"]), k(raw["arc_a"]), lab, src))
     off = np.zeros(V + 1, np.int32)
     if V:
         off[1:] = np.cumsum(np.bincount(src, minlength=V))
@@ -331,7 +338,7 @@ def canonicalize3(raw):
 
 def compose3(A, B, D, mutation=MUT3_NONE):
     """Canonical C = A o B o D, composed simultaneously (see compose3.c)."""
-    return canonicalize3(compose3_raw(A, B, D, mutation))
+    return canonicalize3(compose3_raw(A, B, D, mutation), A)
 
 
 RESULT3_KEYS = ("arc_offset", "src", "dst", "ilabel", "olabel", "weight", "arc_a", "arc_b",

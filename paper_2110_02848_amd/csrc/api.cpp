@@ -71,14 +71,15 @@ struct fst_ctx {
   // three-input composition
   DevBuf t_scal, t_aPerm, t_aArc, t_aRec, t_bPerm, t_bArc, t_bRec, t_bLab, t_bW, t_dPerm,
       t_dArc, t_dRec, t_dLab, t_dW, t_bflags, t_lists, t_tab, t_F, t_chunks, t_arcs, t_inoff,
-      t_cursor, t_insrc, t_coacc, t_keys0, t_keys1, t_slots0, t_slots1, t_idof, t_units, t_ucnt;
+      t_cursor, t_insrc, t_coacc, t_keys0, t_keys1, t_slots0, t_slots1, t_idof, t_units, t_ucnt,
+      t_aLab, t_aW, t_heavy, t_aLut, t_bLut, t_dLut;
   Scal3 *h_s3 = nullptr;
   uint32_t h3_hint = 0;  // hash capacity the last three-input search needed
   struct {
     bool ready = false;
     Problem3 P = {};
     const unsigned long long *keys = nullptr;
-    const uint32_t *ustart = nullptr, *uoff = nullptr;
+    const uint32_t *ustart = nullptr, *uoff = nullptr, *heavy = nullptr, *nheavy = nullptr;
     uint32_t n = 0, U = 0, narcs = 0;
     fst_stats stats = {};
     bool timed = false;
@@ -831,7 +832,7 @@ int readback3(fst_ctx *c, hipStream_t s) {
 // given buffers; lab/w (the other side's label and the weight in sorted
 // order) only when lab is given.
 int view3(fst_ctx *c, const DevGraph &g, int side, bool presorted, uint32_t maxlab, DevBuf &perm,
-          DevBuf &arc, DevBuf &rec, DevBuf *lab, DevBuf *w, View &v, hipStream_t s) {
+          DevBuf &arc, DevBuf &rec, DevBuf *lab, DevBuf *w, DevBuf &lut, View &v, hipStream_t s) {
   FST_TRY(ensure(c, perm, (size_t)g.E * 4));
   FST_TRY(ensure(c, arc, (size_t)g.E * 8));
   FST_TRY(ensure(c, rec, (size_t)g.V * 2 * sizeof(int4)));
@@ -848,6 +849,13 @@ int view3(fst_ctx *c, const DevGraph &g, int side, bool presorted, uint32_t maxl
                     as<int32_t>(c->v0), as<unsigned long long>(c->k1), as<int32_t>(c->v1),
                     c->sort_tmp.p, nullptr, s));
   v = View{as<int4>(rec), as<int2>(arc), as<int32_t>(perm), nullptr, 0, olab, wv, nullptr};
+  // bucket table under the same budget as the two-input views
+  if (want_lut(c, g.V, g.E, maxlab)) {
+    FST_TRY(ensure(c, lut, lut_bytes(g.V, maxlab)));
+    v.lut = as<int4>(lut);
+    v.lstride = (int32_t)maxlab + 1;
+    HIP_TRY(launch3_lut(v, g.V, s));
+  }
   return FST_OK;
 }
 
@@ -920,12 +928,12 @@ int compose3_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, const fst_
   P.A = dA;
   P.B = dB;
   P.D = dD;
-  FST_TRY(view3(c, dA, 0, !(v.errA & info), v.maxA, c->t_aPerm, c->t_aArc, c->t_aRec, nullptr,
-                nullptr, P.aOut, s));
+  FST_TRY(view3(c, dA, 0, !(v.errA & info), v.maxA, c->t_aPerm, c->t_aArc, c->t_aRec,
+                &c->t_aLab, &c->t_aW, c->t_aLut, P.aOut, s));
   FST_TRY(view3(c, dB, 1, !(v.errB & info), v.maxB, c->t_bPerm, c->t_bArc, c->t_bRec,
-                &c->t_bLab, &c->t_bW, P.bOut, s));
+                &c->t_bLab, &c->t_bW, c->t_bLut, P.bOut, s));
   FST_TRY(view3(c, dD, 1, !(v.errD & info), v.maxD, c->t_dPerm, c->t_dArc, c->t_dRec,
-                &c->t_dLab, &c->t_dW, P.dOut, s));
+                &c->t_dLab, &c->t_dW, c->t_dLut, P.dOut, s));
   FST_TRY(ensure(c, c->t_bflags, (size_t)dB.V * 4));
   HIP_TRY(hipMemsetAsync(c->t_bflags.p, 0, (size_t)dB.V * 4, s));
   HIP_TRY(launch3_bflags(dB, as<uint32_t>(c->t_bflags), s));
@@ -1047,10 +1055,13 @@ int compose3_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, const fst_
   const int32_t *slots = as<int32_t>(second ? c->t_slots1 : c->t_slots0);
   FST_TRY(ensure(c, c->t_idof, H * 4));
   FST_TRY(ensure(c, c->t_units, ((size_t)n + 1) * 4));
+  FST_TRY(ensure(c, c->t_heavy, (size_t)n * 4));
   FST_TRY(ensure(c, c->scan_tmp, scan_temp_bytes((size_t)n + 1)));
   HIP_TRY(hipMemsetAsync(c->t_idof.p, 0xff, H * 4, s));
+  HIP_TRY(hipMemsetAsync(d3->nheavy, 0, sizeof(d3->nheavy), s));
   uint32_t *units = as<uint32_t>(c->t_units);
-  HIP_TRY(launch3_ids(P, keys, slots, n, as<int32_t>(c->t_idof), units, s));
+  HIP_TRY(launch3_ids(P, keys, slots, n, as<int32_t>(c->t_idof), units, as<uint32_t>(c->t_heavy),
+                      d3->nheavy, s));
   P.id_of = as<int32_t>(c->t_idof);
   HIP_TRY(scan_u32(units, units, n, true, &d3->total, c->scan_tmp.p, s));
   tout.end(s);
@@ -1064,7 +1075,7 @@ int compose3_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, const fst_
   FST_TRY(ensure(c, c->t_ucnt, (U + 1) * 4));
   FST_TRY(ensure(c, c->scan_tmp, scan_temp_bytes(U + 1)));
   uint32_t *ucnt = as<uint32_t>(c->t_ucnt);
-  HIP_TRY(launch3_count(P, keys, units, n, (uint32_t)U, ucnt, s));
+  HIP_TRY(launch3_count(P, keys, units, n, as<uint32_t>(c->t_heavy), d3->nheavy, ucnt, s));
   HIP_TRY(scan_u32(ucnt, ucnt, U, true, &d3->total, c->scan_tmp.p, s));
   tout.end(s);
   FST_TRY(readback3(c, s));
@@ -1075,6 +1086,9 @@ int compose3_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, const fst_
   c->c3.keys = keys;
   c->c3.ustart = units;
   c->c3.uoff = ucnt;
+  c->c3.heavy = as<uint32_t>(c->t_heavy);
+  c->c3.nheavy = d3->nheavy;
+  c->c3.stats.heavy_states = c->h_s3->nheavy[0];
   c->c3.n = n;
   c->c3.U = (uint32_t)U;
   c->c3.narcs = (uint32_t)E;
@@ -1273,7 +1287,8 @@ void fst_ctx_destroy(fst_ctx *c) {
                     &c->t_dW,     &c->t_bflags, &c->t_lists, &c->t_tab,   &c->t_F,
                     &c->t_chunks, &c->t_arcs,   &c->t_inoff, &c->t_cursor, &c->t_insrc,
                     &c->t_coacc,  &c->t_keys0,  &c->t_keys1, &c->t_slots0, &c->t_slots1,
-                    &c->t_idof,   &c->t_units,  &c->t_ucnt};
+                    &c->t_idof,   &c->t_units,  &c->t_ucnt,  &c->t_aLab,  &c->t_aW,
+                    &c->t_heavy,  &c->t_aLut,   &c->t_bLut,  &c->t_dLut};
   for (DevBuf *b : bufs) release(*b);
   for (ScoreBufs *sb : {&c->score_f, &c->score_b}) {
     for (DevBuf *b : {&sb->sc, &sb->rec, &sb->term, &sb->mkey, &sb->pend, &sb->q, &sb->h,
@@ -1469,8 +1484,8 @@ int fst_compose3_fill(fst_ctx *c, const fst_graph3_out *C, void *stream) {
   O.arc_d = C->arc_d;
   const KernelTimer t = c->c3.timed ? timer(c, FST_KERNEL_COMPACT3) : KernelTimer{};
   t.begin(s);
-  hipError_t e = launch3_fill(c->c3.P, c->c3.keys, c->c3.ustart, c->c3.n, c->c3.U, c->c3.uoff,
-                              c->c3.narcs, O, s);
+  hipError_t e = launch3_fill(c->c3.P, c->c3.keys, c->c3.ustart, c->c3.n, c->c3.heavy,
+                              c->c3.nheavy, c->c3.uoff, c->c3.narcs, O, s);
   t.end(s);
   if (e != hipSuccess) {
     (void)hipGetLastError();

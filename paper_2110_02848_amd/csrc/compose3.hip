@@ -16,20 +16,29 @@
 // The key space is the product of three state sets, far too large for a
 // bitmap, so keys are 64-bit, packed so that numeric order is (qa, qb, f1,
 // qd, f2) order, and deduplicated in an open-addressing hash set whose slot
-// index names the state during the search.  The search goes level by level:
-// one thread per frontier state, or, for a state with more than LIGHT3
-// units of work, one thread per chunk of LIGHT3 units (work units: the
-// state's arcs of A in index order, then its B arcs with input epsilon,
-// then its D arcs with input epsilon).  New keys are appended to the next
-// frontier and every generated arc (source slot, target slot) to an arc
-// list, one atomic per wavefront.  Co-accessibility runs backwards over
-// that arc list (in-arcs grouped by a count, a scan and a placement).  The
-// trim keys are sorted (radix sort of the 64-bit keys): a state's id is its
-// rank.  Count and fill give every work unit of every trim state one
-// thread; units enumerate in canonical (a, b, d) order (an A arc, its B
-// bucket by arc index, the D bucket of each B arc's output, by arc index;
-// then B arcs with input epsilon; then D arcs with input epsilon), so a
-// scan of the per-unit counts gives every arc's position.
+// index names the state during the search.
+//
+// Work units of a key, in canonical order: its A arcs with output epsilon
+// (only when f1 = f2 = 0), its B arcs with input epsilon, its D arcs with
+// input epsilon, then one unit per non-epsilon arc of whichever of A and B
+// has fewer: the unit of the first arc of a label joins the label's arcs
+// of A (outer, by arc index) with those of B (inner), each T-arc with the D
+// bucket of its output; later arcs of the same label do nothing.  So the
+// moves come out in canonical (l, a, b, d) order (l the label A and B were
+// matched on, 0 for the epsilon units; a missing arc last) and a key whose
+// B state has one arc (a lexicon word) has one unit however many arcs its
+// A state has.
+//
+// The search goes level by level: one thread per frontier key with at most
+// LIGHT3 units, one thread per chunk of LIGHT3 units of the others.  New
+// keys are appended to the next frontier and every generated arc (source
+// slot, target slot) to an arc list, one atomic per wavefront.
+// Co-accessibility runs backwards over that arc list (in-arcs grouped by a
+// count, a scan and a placement).  The trim keys are sorted (radix sort of
+// the 64-bit keys): a state's id is its rank.  Count and fill give a state
+// with at most LIGHT3 units one thread and a heavier one a workgroup (its
+// threads take its units in turn); per-unit counts are scanned into every
+// unit's first arc position.
 #include "internal.h"
 
 namespace fstc {
@@ -40,7 +49,7 @@ typedef unsigned long long ull;
 
 constexpr ull EMPTY3 = ~0ull;
 constexpr uint32_t NO_SLOT = 0xFFFFFFFFu;
-constexpr uint32_t LIGHT3 = 32;   // work units one thread takes
+constexpr uint32_t LIGHT3 = 8;    // work units one thread takes
 constexpr int PROBE_MAX = 4096;   // hash probes before the table counts as full
 constexpr uint32_t BF_EPS_EPS = 1u, BF_EPS_OUT = 2u;  // B state flags
 
@@ -149,9 +158,21 @@ __device__ __forceinline__ Grp grp_of(const View &v, uint32_t q) {
   return Grp{r.x, r.y, r.z, r.w};
 }
 
-// [lo, hi) of label lab among the non-epsilon arcs [lo, hi) of a group.
-__device__ __forceinline__ void bucket(const View &v, int32_t lo, int32_t hi, int32_t lab,
-                                       int32_t &r0, int32_t &r1) {
+// [lo, hi) of label lab among the non-epsilon arcs [lo, hi) of group q:
+// one load from the view's bucket table when it has one, else a binary
+// search.
+__device__ __forceinline__ void bucket(const View &v, uint32_t q, int32_t lo, int32_t hi,
+                                       int32_t lab, int32_t &r0, int32_t &r1) {
+  if (v.lut) {
+    if ((uint32_t)lab < (uint32_t)v.lstride) {
+      const int4 b = v.lut[(size_t)q * (uint32_t)v.lstride + (uint32_t)lab];
+      r0 = b.x;
+      r1 = b.y;
+    } else {
+      r0 = r1 = hi;
+    }
+    return;
+  }
   int32_t a = lo, b = hi;
   while (a < b) {
     const int32_t mid = a + ((b - a) >> 1);
@@ -179,89 +200,106 @@ __device__ __forceinline__ uint32_t eps_out_t(const Problem3 &P, uint32_t qa, ui
   for (int32_t p = gb.begin + gb.neps; p < gb.end; ++p) {
     if (P.bOut.olab[p] != 0) continue;
     int32_t r0, r1;
-    bucket(P.aOut, ga.begin + ga.neps, ga.end, P.bOut.arec[p].x, r0, r1);
+    bucket(P.aOut, qa, ga.begin + ga.neps, ga.end, P.bOut.arec[p].x, r0, r1);
     if (r0 < r1) return 1u;
   }
   return 0u;
 }
 
-// The work units of a key: its A arcs, its B arcs with input epsilon, its
-// D arcs with input epsilon.
+// The work units of a key (see the file comment).
 struct Units3 {
   Key3 k;
-  int32_t a0, na;     // A arcs [a0, a0 + na) in index order
-  Grp gb, gd;
+  Grp ga, gb, gd;
+  uint32_t nae;      // A-epsilon units (0 unless f1 = f2 = 0)
+  uint32_t nm;       // matching units: non-epsilon arcs of the smaller side
+  bool joinA;        // the matching units walk A's arcs (else B's)
 };
 __device__ __forceinline__ Units3 units_of(const Problem3 &P, ull key) {
   Units3 u;
   u.k = unpack3(P, key);
-  u.a0 = P.A.off[u.k.qa];
-  u.na = P.A.off[u.k.qa + 1] - u.a0;
+  u.ga = grp_of(P.aOut, u.k.qa);
   u.gb = grp_of(P.bOut, u.k.qb);
   u.gd = grp_of(P.dOut, u.k.qd);
+  u.nae = (u.k.f1 == 0 && u.k.f2 == 0) ? (uint32_t)u.ga.neps : 0u;
+  const uint32_t na = (uint32_t)(u.ga.end - u.ga.begin - u.ga.neps);
+  const uint32_t nb = (uint32_t)(u.gb.end - u.gb.begin - u.gb.neps);
+  u.joinA = na <= nb;
+  u.nm = (na && nb) ? (u.joinA ? na : nb) : 0u;
   return u;
 }
 __device__ __forceinline__ uint32_t nunits(const Units3 &u) {
-  return (uint32_t)u.na + (uint32_t)u.gb.neps + (uint32_t)u.gd.neps;
+  return u.nae + (uint32_t)u.gb.neps + (uint32_t)u.gd.neps + u.nm;
+}
+
+// A T-arc (B's arc at position p of its view, A's arc id ea or -1, target
+// (ta, tb, tf1), input label il, weight wt) composed with D: alone when
+// its output is epsilon (f2 = 0 only), else with the D bucket of its output.
+template <class F>
+__device__ __forceinline__ void t_with_d(const Problem3 &P, const Units3 &u, int32_t p, int32_t ea,
+                                         uint32_t ta, uint32_t tf1, int32_t il, float wt, F &&f) {
+  const int32_t eb = P.bOut.perm[p], z = P.bOut.olab[p];
+  const uint32_t tb = nbr_of_arc(P.bOut.arec[p].y);
+  if (z == 0) {
+    if (u.k.f2 == 0) f(pack3(P, ta, tb, tf1, u.k.qd, 0), il, 0, wt, ea, eb, -1);
+    return;
+  }
+  int32_t d0, d1;
+  bucket(P.dOut, u.k.qd, u.gd.begin + u.gd.neps, u.gd.end, z, d0, d1);
+  for (int32_t r = d0; r < d1; ++r)
+    f(pack3(P, ta, tb, tf1, nbr_of_arc(P.dOut.arec[r].y), 0), il, P.dOut.olab[r],
+      wt + P.dOut.w[r], ea, eb, P.dOut.perm[r]);
 }
 
 // Calls f(target key, ilabel, olabel, weight, a, b, d) for every move of
-// unit j of a key, in canonical (a, b, d) order (arc ids; -1 = none).
+// unit j of a key, in canonical order (arc ids; -1 = none).
 template <class F>
 __device__ __forceinline__ void for_unit3(const Problem3 &P, const Units3 &u, uint32_t j, F &&f) {
   const Key3 &k = u.k;
-  if (j < (uint32_t)u.na) {
-    const int32_t ea = u.a0 + (int32_t)j;
-    const int32_t y = P.A.ol[ea], ia = P.A.il[ea], da = P.A.dst[ea];
-    const float wa = P.A.w[ea];
-    if (y == 0) {
-      // T-epsA (f1 = 0), output epsilon: T alone (f2 = 0)
-      if (k.f1 == 0 && k.f2 == 0) f(pack3(P, da, k.qb, 0, k.qd, 0), ia, 0, wa, ea, -1, -1);
-      return;
-    }
-    int32_t b0, b1;
-    bucket(P.bOut, u.gb.begin + u.gb.neps, u.gb.end, y, b0, b1);
-    for (int32_t p = b0; p < b1; ++p) {
-      const int32_t eb = P.bOut.perm[p], z = P.bOut.olab[p];
-      const uint32_t db = nbr_of_arc(P.bOut.arec[p].y);
-      const float wt = wa + P.bOut.w[p];
-      if (z == 0) {
-        if (k.f2 == 0) f(pack3(P, da, db, 0, k.qd, 0), ia, 0, wt, ea, eb, -1);
-        continue;
-      }
-      int32_t d0, d1;
-      bucket(P.dOut, u.gd.begin + u.gd.neps, u.gd.end, z, d0, d1);
-      for (int32_t r = d0; r < d1; ++r)
-        f(pack3(P, da, db, 0, nbr_of_arc(P.dOut.arec[r].y), 0), ia, P.dOut.olab[r],
-          wt + P.dOut.w[r], ea, eb, P.dOut.perm[r]);
-    }
+  if (j < u.nae) {
+    // A alone (output epsilon; f1 = f2 = 0): T-arc alone as well
+    const int32_t p = u.ga.begin + (int32_t)j;
+    f(pack3(P, nbr_of_arc(P.aOut.arec[p].y), k.qb, 0, k.qd, 0), P.aOut.olab[p], 0,
+      P.aOut.w[p], P.aOut.perm[p], -1, -1);
     return;
   }
-  j -= (uint32_t)u.na;
+  j -= u.nae;
   if (j < (uint32_t)u.gb.neps) {
-    // T-epsB: (qa, dst b, epsOutA(qa))
+    // B alone (input epsilon): T-state (qa, dst b, epsOutA(qa))
     const int32_t p = u.gb.begin + (int32_t)j;
-    const int32_t eb = P.bOut.perm[p], z = P.bOut.olab[p];
-    const uint32_t db = nbr_of_arc(P.bOut.arec[p].y);
-    const uint32_t nf1 = (grp_of(P.aOut, k.qa).neps > 0) ? 1u : 0u;
-    const float wb = P.bOut.w[p];
-    if (z == 0) {
-      if (k.f2 == 0) f(pack3(P, k.qa, db, nf1, k.qd, 0), 0, 0, wb, -1, eb, -1);
-      return;
-    }
-    int32_t d0, d1;
-    bucket(P.dOut, u.gd.begin + u.gd.neps, u.gd.end, z, d0, d1);
-    for (int32_t r = d0; r < d1; ++r)
-      f(pack3(P, k.qa, db, nf1, nbr_of_arc(P.dOut.arec[r].y), 0), 0, P.dOut.olab[r],
-        wb + P.dOut.w[r], -1, eb, P.dOut.perm[r]);
+    t_with_d(P, u, p, -1, k.qa, u.ga.neps > 0 ? 1u : 0u, 0, P.bOut.w[p], f);
     return;
   }
   j -= (uint32_t)u.gb.neps;
-  // D alone (input epsilon): f2 = epsOutT of the key's T-state
-  const int32_t r = u.gd.begin + (int32_t)j;
-  const uint32_t nf2 = eps_out_t(P, k.qa, k.qb, k.f1);
-  f(pack3(P, k.qa, k.qb, k.f1, nbr_of_arc(P.dOut.arec[r].y), nf2), 0, P.dOut.olab[r],
-    P.dOut.w[r], -1, -1, P.dOut.perm[r]);
+  if (j < (uint32_t)u.gd.neps) {
+    // D alone (input epsilon): f2 = epsOutT of the key's T-state
+    const int32_t r = u.gd.begin + (int32_t)j;
+    const uint32_t nf2 = eps_out_t(P, k.qa, k.qb, k.f1);
+    f(pack3(P, k.qa, k.qb, k.f1, nbr_of_arc(P.dOut.arec[r].y), nf2), 0, P.dOut.olab[r],
+      P.dOut.w[r], -1, -1, P.dOut.perm[r]);
+    return;
+  }
+  j -= (uint32_t)u.gd.neps;
+  // matching unit: the j-th non-epsilon arc of the smaller side; only the
+  // first arc of a label does the label's join
+  const View &side = u.joinA ? P.aOut : P.bOut;
+  const Grp &g = u.joinA ? u.ga : u.gb;
+  const int32_t p = g.begin + g.neps + (int32_t)j;
+  const int32_t lab = side.arec[p].x;
+  if (p > g.begin + g.neps && side.arec[p - 1].x == lab) return;
+  int32_t a0, a1, b0, b1;
+  if (u.joinA) {
+    bucket(P.aOut, k.qa, p, u.ga.end, lab, a0, a1);
+    bucket(P.bOut, k.qb, u.gb.begin + u.gb.neps, u.gb.end, lab, b0, b1);
+  } else {
+    bucket(P.bOut, k.qb, p, u.gb.end, lab, b0, b1);
+    bucket(P.aOut, k.qa, u.ga.begin + u.ga.neps, u.ga.end, lab, a0, a1);
+  }
+  for (int32_t pa = a0; pa < a1; ++pa) {
+    const int32_t ea = P.aOut.perm[pa], ia = P.aOut.olab[pa];
+    const uint32_t ta = nbr_of_arc(P.aOut.arec[pa].y);
+    const float wa = P.aOut.w[pa];
+    for (int32_t pb = b0; pb < b1; ++pb) t_with_d(P, u, pb, ea, ta, 0, ia, wa + P.bOut.w[pb], f);
+  }
 }
 
 __device__ __forceinline__ bool key_accepts(const Problem3 &P, const Key3 &k) {
@@ -279,6 +317,31 @@ __global__ __launch_bounds__(NT) void k3_bflags(DevGraph B, uint32_t *bflags) {
        e += (long long)gridDim.x * NT) {
     if (B.ol[e] != 0) continue;
     atomicOr(bflags + B.src[e], B.il[e] == 0 ? BF_EPS_EPS : BF_EPS_OUT);
+  }
+}
+
+// Bucket table of a view: lut[v * stride + l] = {first position of label
+// l in group v, first position past it, 0, 0}.
+__global__ __launch_bounds__(NT) void k3_lut(View v, long long nstates) {
+  const long long n = nstates * v.lstride;
+  int4 *lut = const_cast<int4 *>(v.lut);
+  for (long long x = (long long)blockIdx.x * NT + threadIdx.x; x < n;
+       x += (long long)gridDim.x * NT) {
+    const uint32_t q = (uint32_t)(x / v.lstride);
+    const int32_t l = (int32_t)(x % v.lstride);
+    const int4 r = v.srec[2 * (size_t)q];
+    int32_t a = r.x, b = r.z;
+    while (a < b) {
+      const int32_t mid = a + ((b - a) >> 1);
+      if (v.arec[mid].x < l) a = mid + 1; else b = mid;
+    }
+    const int32_t lo = a;
+    b = r.z;
+    while (a < b) {
+      const int32_t mid = a + ((b - a) >> 1);
+      if (v.arec[mid].x <= l) a = mid + 1; else b = mid;
+    }
+    lut[x] = make_int4(lo, a, 0, 0);
   }
 }
 
@@ -488,55 +551,68 @@ __global__ __launch_bounds__(NT) void k3_bwd_chunks(Problem3 P, Search3 S, int l
 // trim, numbering, count, fill
 // ---------------------------------------------------------------------------
 
-// Trim keys (in the set and co-accessible) with their slots.
+// Trim keys (in the set and co-accessible) with their slots.  Each
+// workgroup takes COL_ITEMS x NT consecutive slots per round and appends
+// its keys with one atomic (a workgroup scan places them).
+constexpr int COL_ITEMS = 8;
+
 __global__ __launch_bounds__(NT) void k3_collect(Problem3 P, ull *keys, int32_t *slots,
                                                  uint32_t *count, uint32_t cap,
                                                  uint32_t *overflow) {
+  __shared__ uint32_t s_w[NWAVES];
+  __shared__ uint32_t s_base;
   const ull H = (ull)P.hmask + 1;
-  for (ull i0 = (ull)blockIdx.x * NT; i0 < H; i0 += (ull)gridDim.x * NT) {
-    const ull s = i0 + threadIdx.x;
-    ull k = EMPTY3;
-    bool want = false;
-    if (s < H) {
-      k = P.tab[s];
-      want = k != EMPTY3 && ((P.coacc[s >> 5] >> (s & 31u)) & 1u);
-    }
-    const ull m = __ballot(want);
-    if (m == 0) continue;
-    const int leader = __ffsll(m) - 1;
-    uint32_t base = 0;
-    if ((int)__lane_id() == leader) base = atomicAdd(count, (uint32_t)__popcll(m));
-    base = __shfl(base, leader, WAVE);
-    if (want) {
-      const uint32_t pos = base + (uint32_t)__popcll(m & __lanemask_lt());
-      if (pos < cap) {
-        keys[pos] = k;
-        slots[pos] = (int32_t)s;
-      } else {
-        atomicOr(overflow, 1u);
+  const ull tile = (ull)NT * COL_ITEMS;
+  for (ull b0 = (ull)blockIdx.x * tile; b0 < H; b0 += (ull)gridDim.x * tile) {
+    ull kv[COL_ITEMS];
+    uint32_t want = 0, c = 0;
+#pragma unroll
+    for (int r = 0; r < COL_ITEMS; ++r) {
+      const ull sl = b0 + (ull)threadIdx.x * COL_ITEMS + r;
+      kv[r] = EMPTY3;
+      if (sl < H) {
+        kv[r] = P.tab[sl];
+        if (kv[r] != EMPTY3 && ((P.coacc[sl >> 5] >> (sl & 31u)) & 1u)) {
+          want |= 1u << r;
+          ++c;
+        }
       }
     }
+    uint32_t total;
+    const uint32_t off = block_excl_scan<uint32_t>(c, s_w, total);
+    if (threadIdx.x == 0) s_base = total ? atomicAdd(count, total) : 0u;
+    __syncthreads();
+    uint32_t pos = s_base + off;
+#pragma unroll
+    for (int r = 0; r < COL_ITEMS; ++r)
+      if (want & (1u << r)) {
+        if (pos < cap) {
+          keys[pos] = kv[r];
+          slots[pos] = (int32_t)(b0 + (ull)threadIdx.x * COL_ITEMS + r);
+        } else {
+          atomicOr(overflow, 1u);
+        }
+        ++pos;
+      }
+    __syncthreads();  // s_base is rewritten next round
   }
 }
 
 // id_of[slot] = rank of the slot's key among the trim keys; units of every
-// state of C.
+// state of C; states with more than LIGHT3 units listed as heavy.
 __global__ __launch_bounds__(NT) void k3_ids(Problem3 P, const ull *keys, const int32_t *slots,
-                                             uint32_t n, int32_t *id_of, uint32_t *units) {
-  for (ull i = (ull)blockIdx.x * NT + threadIdx.x; i < n; i += (ull)gridDim.x * NT) {
-    id_of[slots[i]] = (int32_t)i;
-    units[i] = nunits(units_of(P, keys[i]));
+                                             uint32_t n, int32_t *id_of, uint32_t *units,
+                                             uint32_t *heavy, uint32_t *nheavy) {
+  for (ull i0 = (ull)blockIdx.x * NT; i0 < n; i0 += (ull)gridDim.x * NT) {
+    const ull i = i0 + threadIdx.x;
+    uint32_t nu = 0;
+    if (i < n) {
+      id_of[slots[i]] = (int32_t)i;
+      nu = nunits(units_of(P, keys[i]));
+      units[i] = nu;
+    }
+    wave_append<uint32_t>(nu > LIGHT3, (uint32_t)i, heavy, n, nheavy, nheavy + 1);
   }
-}
-
-// The state of C owning unit u: the last i with ustart[i] <= u.
-__device__ __forceinline__ uint32_t state_of_unit(const uint32_t *ustart, uint32_t n, uint32_t u) {
-  uint32_t lo = 0, hi = n;  // ustart[lo] <= u < ustart[hi]
-  while (hi - lo > 1) {
-    const uint32_t mid = lo + ((hi - lo) >> 1);
-    if (ustart[mid] <= u) lo = mid; else hi = mid;
-  }
-  return lo;
 }
 
 __device__ __forceinline__ int32_t id_of_key(const Problem3 &P, ull t) {
@@ -544,41 +620,64 @@ __device__ __forceinline__ int32_t id_of_key(const Problem3 &P, ull t) {
   return s == NO_SLOT ? -1 : P.id_of[s];
 }
 
-__global__ __launch_bounds__(NT) void k3_count(Problem3 P, const ull *keys, const uint32_t *ustart,
-                                               uint32_t n, uint32_t U, uint32_t *ucnt) {
-  for (ull u = (ull)blockIdx.x * NT + threadIdx.x; u < U; u += (ull)gridDim.x * NT) {
-    const uint32_t i = state_of_unit(ustart, n, (uint32_t)u);
+// Kept arcs of unit j of state i, written from position pos (FILL) or
+// counted.
+template <bool FILL>
+__device__ __forceinline__ uint32_t out_unit(const Problem3 &P, const Units3 &st, uint32_t i,
+                                             uint32_t j, uint32_t pos, const OutGraph3 &O) {
+  uint32_t c = 0;
+  for_unit3(P, st, j, [&](ull t, int32_t il, int32_t ol, float w, int32_t a, int32_t b, int32_t d) {
+    const int32_t id = id_of_key(P, t);
+    if (id < 0) return;
+    if (FILL) {
+      const uint32_t q = pos + c;
+      O.src[q] = (int32_t)i;
+      O.dst[q] = id;
+      O.il[q] = il;
+      O.ol[q] = ol;
+      O.w[q] = w;
+      if (O.arc_a) O.arc_a[q] = a;
+      if (O.arc_b) O.arc_b[q] = b;
+      if (O.arc_d) O.arc_d[q] = d;
+    }
+    ++c;
+  });
+  return c;
+}
+
+// Light states: one thread each, every unit in turn (counts per unit, or
+// the arcs at each unit's position).
+template <bool FILL>
+__global__ __launch_bounds__(NT) void k3_out_light(Problem3 P, const ull *keys,
+                                                   const uint32_t *ustart, uint32_t n,
+                                                   uint32_t *ucnt, const uint32_t *uoff,
+                                                   OutGraph3 O) {
+  for (ull i = (ull)blockIdx.x * NT + threadIdx.x; i < n; i += (ull)gridDim.x * NT) {
+    const uint32_t u0 = ustart[i], nu = ustart[i + 1] - u0;
+    if (nu > LIGHT3) continue;
     const Units3 st = units_of(P, keys[i]);
-    uint32_t c = 0;
-    for_unit3(P, st, (uint32_t)u - ustart[i],
-              [&](ull t, int32_t, int32_t, float, int32_t, int32_t, int32_t) {
-                c += id_of_key(P, t) >= 0 ? 1u : 0u;
-              });
-    ucnt[u] = c;
+    for (uint32_t j = 0; j < nu; ++j) {
+      const uint32_t c = out_unit<FILL>(P, st, (uint32_t)i, j, FILL ? uoff[u0 + j] : 0u, O);
+      if (!FILL) ucnt[u0 + j] = c;
+    }
   }
 }
 
-__global__ __launch_bounds__(NT) void k3_fill(Problem3 P, const ull *keys, const uint32_t *ustart,
-                                              uint32_t n, uint32_t U, const uint32_t *uoff,
-                                              OutGraph3 O) {
-  for (ull u = (ull)blockIdx.x * NT + threadIdx.x; u < U; u += (ull)gridDim.x * NT) {
-    const uint32_t i = state_of_unit(ustart, n, (uint32_t)u);
+// Heavy states: one workgroup each, its threads taking the units in turn.
+template <bool FILL>
+__global__ __launch_bounds__(NT) void k3_out_heavy(Problem3 P, const ull *keys,
+                                                   const uint32_t *ustart, const uint32_t *heavy,
+                                                   const uint32_t *nheavy, uint32_t *ucnt,
+                                                   const uint32_t *uoff, OutGraph3 O) {
+  const uint32_t nh = *nheavy;
+  for (uint32_t h = blockIdx.x; h < nh; h += gridDim.x) {
+    const uint32_t i = heavy[h];
+    const uint32_t u0 = ustart[i], nu = ustart[i + 1] - u0;
     const Units3 st = units_of(P, keys[i]);
-    uint32_t pos = uoff[u];
-    for_unit3(P, st, (uint32_t)u - ustart[i],
-              [&](ull t, int32_t il, int32_t ol, float w, int32_t a, int32_t b, int32_t d) {
-                const int32_t id = id_of_key(P, t);
-                if (id < 0) return;
-                O.src[pos] = (int32_t)i;
-                O.dst[pos] = id;
-                O.il[pos] = il;
-                O.ol[pos] = ol;
-                O.w[pos] = w;
-                if (O.arc_a) O.arc_a[pos] = a;
-                if (O.arc_b) O.arc_b[pos] = b;
-                if (O.arc_d) O.arc_d[pos] = d;
-                ++pos;
-              });
+    for (uint32_t j = threadIdx.x; j < nu; j += NT) {
+      const uint32_t c = out_unit<FILL>(P, st, i, j, FILL ? uoff[u0 + j] : 0u, O);
+      if (!FILL) ucnt[u0 + j] = c;
+    }
   }
 }
 
@@ -650,6 +749,12 @@ hipError_t launch3_in_arcs(const uint2 *arcs, unsigned long long narcs, uint32_t
   return hipGetLastError();
 }
 
+hipError_t launch3_lut(const View &v, long long nstates, hipStream_t s) {
+  const long long n = nstates * v.lstride;
+  if (n > 0) k3_lut<<<grid3((size_t)n, 8192), NT, 0, s>>>(v, nstates);
+  return hipGetLastError();
+}
+
 hipError_t launch3_seed_bwd(const Problem3 &P, const Search3 &S, hipStream_t s) {
   k3_seed_bwd<<<grid3((size_t)P.hmask + 1, 8192), NT, 0, s>>>(P, S);
   return hipGetLastError();
@@ -657,28 +762,37 @@ hipError_t launch3_seed_bwd(const Problem3 &P, const Search3 &S, hipStream_t s) 
 
 hipError_t launch3_collect(const Problem3 &P, unsigned long long *keys, int32_t *slots,
                            uint32_t *count, uint32_t cap, uint32_t *overflow, hipStream_t s) {
-  k3_collect<<<grid3((size_t)P.hmask + 1, 8192), NT, 0, s>>>(P, keys, slots, count, cap,
-                                                             overflow);
+  const size_t tiles = ((size_t)P.hmask + 1 + (size_t)NT * COL_ITEMS - 1) / ((size_t)NT * COL_ITEMS);
+  k3_collect<<<(unsigned)(tiles < 4096 ? tiles : 4096), NT, 0, s>>>(P, keys, slots, count, cap,
+                                                                   overflow);
   return hipGetLastError();
 }
 
 hipError_t launch3_ids(const Problem3 &P, const unsigned long long *keys, const int32_t *slots,
-                       uint32_t n, int32_t *id_of, uint32_t *units, hipStream_t s) {
-  if (n) k3_ids<<<grid3(n), NT, 0, s>>>(P, keys, slots, n, id_of, units);
+                       uint32_t n, int32_t *id_of, uint32_t *units, uint32_t *heavy,
+                       uint32_t *nheavy, hipStream_t s) {
+  if (n) k3_ids<<<grid3(n), NT, 0, s>>>(P, keys, slots, n, id_of, units, heavy, nheavy);
   return hipGetLastError();
 }
 
 hipError_t launch3_count(const Problem3 &P, const unsigned long long *keys,
-                         const uint32_t *ustart, uint32_t n, uint32_t U, uint32_t *ucnt,
-                         hipStream_t s) {
-  if (U) k3_count<<<grid3(U, 8192), NT, 0, s>>>(P, keys, ustart, n, U, ucnt);
+                         const uint32_t *ustart, uint32_t n, const uint32_t *heavy,
+                         const uint32_t *nheavy, uint32_t *ucnt, hipStream_t s) {
+  if (!n) return hipSuccess;
+  const OutGraph3 none = {};
+  k3_out_light<false><<<grid3(n, 16384), NT, 0, s>>>(P, keys, ustart, n, ucnt, nullptr, none);
+  k3_out_heavy<false><<<1024, NT, 0, s>>>(P, keys, ustart, heavy, nheavy, ucnt, nullptr, none);
   return hipGetLastError();
 }
 
 hipError_t launch3_fill(const Problem3 &P, const unsigned long long *keys, const uint32_t *ustart,
-                        uint32_t n, uint32_t U, const uint32_t *uoff, uint32_t narcs,
-                        const OutGraph3 &O, hipStream_t s) {
-  if (U) k3_fill<<<grid3(U, 8192), NT, 0, s>>>(P, keys, ustart, n, U, uoff, O);
+                        uint32_t n, const uint32_t *heavy, const uint32_t *nheavy,
+                        const uint32_t *uoff, uint32_t narcs, const OutGraph3 &O,
+                        hipStream_t s) {
+  if (n) {
+    k3_out_light<true><<<grid3(n, 16384), NT, 0, s>>>(P, keys, ustart, n, nullptr, uoff, O);
+    k3_out_heavy<true><<<1024, NT, 0, s>>>(P, keys, ustart, heavy, nheavy, nullptr, uoff, O);
+  }
   k3_fill_states<<<grid3((size_t)n + 1, 8192), NT, 0, s>>>(P, keys, ustart, n, uoff, narcs, O);
   return hipGetLastError();
 }

@@ -194,7 +194,7 @@ struct SearchArgs {
 // all ones) until the numbering.
 struct Problem3 {
   DevGraph A, B, D;
-  View aOut;  // A by (src, olabel): epsOutA and the output-label lookups of epsOutT
+  View aOut;  // A by (src, olabel), with A's ilabel and weight in sorted order
   View bOut;  // B by (src, ilabel), with B's olabel and weight in sorted order
   View dOut;  // D by (src, ilabel), with D's olabel and weight in sorted order
   const uint32_t *bflags;  // per B state: an eps:eps arc (1), a y:eps arc, y != eps (2)
@@ -217,6 +217,7 @@ struct Lvl3 {
 struct Scal3 {
   uint32_t errA, errB, errD, maxA, maxB, maxD;
   uint32_t overflow, levels, narcs, ntrim;
+  uint32_t nheavy[2];        // heavy states of C (and an overflow word)
   unsigned long long total;  // scan totals
   Lvl3 ring[3];
 };
@@ -537,6 +538,9 @@ hipError_t launch_item_ranges(const Problem &P, unsigned long long nkeys, int32_
 
 // Three-input launchers (compose3.hip).
 hipError_t launch3_bflags(const DevGraph &B, uint32_t *bflags, hipStream_t s);
+// Bucket table of a view (v.lut with v.lstride labels per state) from its
+// records and arcs.
+hipError_t launch3_lut(const View &v, long long nstates, hipStream_t s);
 // Start keys of every triple of start states (lists and counts from
 // launch3_starts) into level 0 of S.
 hipError_t launch3_starts(const DevGraph &A, const DevGraph &B, const DevGraph &D,
@@ -553,14 +557,20 @@ hipError_t launch3_in_arcs(const uint2 *arcs, unsigned long long narcs, uint32_t
 hipError_t launch3_seed_bwd(const Problem3 &P, const Search3 &S, hipStream_t s);
 hipError_t launch3_collect(const Problem3 &P, unsigned long long *keys, int32_t *slots,
                            uint32_t *count, uint32_t cap, uint32_t *overflow, hipStream_t s);
+// id_of (slot -> state id), units per state, heavy states (more units
+// than one thread takes; count in nheavy[0], nheavy[1] an overflow word).
 hipError_t launch3_ids(const Problem3 &P, const unsigned long long *keys, const int32_t *slots,
-                       uint32_t n, int32_t *id_of, uint32_t *units, hipStream_t s);
+                       uint32_t n, int32_t *id_of, uint32_t *units, uint32_t *heavy,
+                       uint32_t *nheavy, hipStream_t s);
+// Kept arcs per work unit (ustart: n + 1 unit offsets per state).
 hipError_t launch3_count(const Problem3 &P, const unsigned long long *keys,
-                         const uint32_t *ustart, uint32_t n, uint32_t U, uint32_t *ucnt,
-                         hipStream_t s);
+                         const uint32_t *ustart, uint32_t n, const uint32_t *heavy,
+                         const uint32_t *nheavy, uint32_t *ucnt, hipStream_t s);
+// Write C (uoff: U + 1 arc offsets per unit).
 hipError_t launch3_fill(const Problem3 &P, const unsigned long long *keys, const uint32_t *ustart,
-                        uint32_t n, uint32_t U, const uint32_t *uoff, uint32_t narcs,
-                        const OutGraph3 &O, hipStream_t s);
+                        uint32_t n, const uint32_t *heavy, const uint32_t *nheavy,
+                        const uint32_t *uoff, uint32_t narcs, const OutGraph3 &O,
+                        hipStream_t s);
 
 // Score launchers (score.hip).
 // In-arc structure of G: owner (V words, all -1) and extra (V words, all 0)

@@ -56,8 +56,10 @@ FAMILIES = {
     "posterior": ("k_posterior(",),
     "scatter": ("k_absmax(", "k_bucket_count(", "k_bucket_place(", "k_scatter(",
                 "k_scatter_final("),
-    # N-way composition
-    "search3": ("k3_expand(", "k3_expand2("),
+    # three inputs at once (bench.py --task compose3)
+    "search3": ("k3_fwd(", "k3_fwd_chunks(", "k3_bwd(", "k3_bwd_chunks("),
+    "compact3": ("k3_indeg(", "k3_place(", "k3_seed_bwd(", "k3_collect(", "k3_ids(",
+                 "k3_count(", "k3_fill(", "k3_fill_states("),
 }
 
 # Counters of each pass (what one rocprofv3 pass can collect on gfx950).

@@ -425,7 +425,9 @@ def check_invariants3(A, B, D, C):
         if len(np.unique(trip, axis=0)) != E:
             errs.append("duplicate (src, arc_a, arc_b, arc_d)")
         big = np.int64(1) << 40
-        order = np.lexsort((np.where(hd, d, big), np.where(hb, b, big), np.where(ha, a, big), src))
+        lab = np.where(tm, Ap["olabel"][aa].astype(np.int64), 0)
+        order = np.lexsort((np.where(hd, d, big), np.where(hb, b, big), np.where(ha, a, big),
+                            lab, src))
         if not np.array_equal(order, np.arange(E)):
             errs.append("arcs not in canonical order")
     fwd = _reach(V, src, dst, np.flatnonzero(C["start"]))

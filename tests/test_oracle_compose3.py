@@ -80,7 +80,7 @@ def chained3(A, B, D):
                src=CD["src"], dst=CD["dst"], ilabel=CD["ilabel"], olabel=CD["olabel"],
                weight=CD["weight"], arc_a=pad(AB["arc_a"])[aa], arc_b=pad(AB["arc_b"])[aa],
                arc_d=CD["arc_b"], stats={})
-    return oracle.canonicalize3(raw)
+    return oracle.canonicalize3(raw, A)
 
 
 def _no_eps_input(g):
