@@ -74,8 +74,9 @@ enum fst_status {
  *   ilabel[E], olabel[E]  labels >= 0, 0 = epsilon
  *   weight[E]        binary32 log weights (any value, not checked)
  *   start[V], accept[V]   0 or 1; any number of start states
- * Every run validates these rules and returns FST_ERR_INVALID_GRAPH on a
- * violation.  Pointers may be NULL only when the array is empty. */
+ * Every run validates these rules (unless FST_OPT_VALIDATE is 0) and
+ * returns FST_ERR_INVALID_GRAPH on a violation.  Pointers may be NULL only
+ * when the array is empty. */
 typedef struct {
   int32_t num_states, num_arcs;
   const int32_t *arc_offset;
@@ -154,14 +155,20 @@ FST_API void fst_ctx_destroy(fst_ctx *ctx);
  * the forward search has ended and held back while its frontier is far
  * wider than the forward one (kernel FST_KERNEL_SEARCH_FORWARD then times
  * the launches that advance either search, and FST_KERNEL_SEARCH_BACKWARD
- * has none). */
+ * has none).  FST_OPT_VALIDATE (default 1) checks every input graph's
+ * structure as described at fst_graph; 0 is for callers that vouch for
+ * their graphs: the checks are skipped (the composition still reads the
+ * largest label, the label order and the accepting states; a score reads
+ * nothing before it starts), and a graph that breaks the rules then gives
+ * unspecified results, which may include reads outside its arrays. */
 enum fst_option {
   FST_OPT_MAX_WORKSPACE = 1,
   FST_OPT_TIMING = 2,
   FST_OPT_LABEL_BUCKETS = 3,
   FST_OPT_CHAIN_DEPTH = 4,
   FST_OPT_COUNT_MOVES = 5,
-  FST_OPT_ORDER = 6
+  FST_OPT_ORDER = 6,
+  FST_OPT_VALIDATE = 7
 };
 enum fst_order {
   FST_ORDER_FORWARD_FIRST = 0,

@@ -161,6 +161,47 @@ __global__ __launch_bounds__(NT) void k_validate(DevGraph g, int side, uint32_t 
   }
 }
 
+// What the composition needs from a graph whose structure the caller
+// vouches for (validation switched off): the largest matched label, whether
+// the arcs of every state are in label order (an arc and the one before it
+// with the same source), and the number of accepting states; no checks.
+__global__ __launch_bounds__(NT) void k_label_facts(DevGraph g, int side, uint32_t *err,
+                                                    uint32_t *maxlab, uint32_t *nacc) {
+  uint32_t bits = 0, mx = 0, na = 0;
+  const long long V = g.V, E = g.E;
+  const long long n = V > E ? V : E;
+  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n;
+       i += (long long)gridDim.x * NT) {
+    if (i < V && nacc) na += g.accept[i] == 1 ? 1u : 0u;
+    if (i < E && side != 2) {
+      const int32_t lab = side == 0 ? g.ol[i] : g.il[i];
+      if (lab > 0 && (uint32_t)lab > mx) mx = (uint32_t)lab;
+      if (i > 0 && g.src[i - 1] == g.src[i] && (side == 0 ? g.ol[i - 1] : g.il[i - 1]) > lab)
+        bits |= INFO_UNSORTED;
+    }
+  }
+  __shared__ uint32_t s_bits[NWAVES], s_mx[NWAVES], s_na[NWAVES];
+  bits = wave_or(bits);
+  mx = wave_max(mx);
+  na = wave_sum(na);
+  if (__lane_id() == 0) {
+    s_bits[threadIdx.x / WAVE] = bits;
+    s_mx[threadIdx.x / WAVE] = mx;
+    s_na[threadIdx.x / WAVE] = na;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < NWAVES; ++w) {
+      bits |= s_bits[w];
+      mx = s_mx[w] > mx ? s_mx[w] : mx;
+      na += s_na[w];
+    }
+    if (bits) atomicOr(err, bits);
+    if (mx) atomicMax(maxlab, mx);
+    if (na && nacc) atomicAdd(nacc, na);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // label-sorted views
 // ---------------------------------------------------------------------------
@@ -1841,9 +1882,10 @@ __global__ __launch_bounds__(NT) void k_item_ranges(Problem P, ull nkeys, int32_
 // launchers
 // ---------------------------------------------------------------------------
 hipError_t launch_validate(const DevGraph &g, int side, uint32_t *err, uint32_t *maxlab,
-                           hipStream_t s, uint32_t *nacc) {
+                           hipStream_t s, uint32_t *nacc, bool check) {
   size_t n = (size_t)(g.V + 1 > g.E ? g.V + 1 : g.E);
-  k_validate<<<grid_for(n, 2048), NT, 0, s>>>(g, side, err, maxlab, nacc);
+  if (check) k_validate<<<grid_for(n, 2048), NT, 0, s>>>(g, side, err, maxlab, nacc);
+  else k_label_facts<<<grid_for(n, 2048), NT, 0, s>>>(g, side, err, maxlab, nacc);
   return hipGetLastError();
 }
 

@@ -430,8 +430,9 @@ hipError_t radix_sort(unsigned long long *k0, int32_t *v0, unsigned long long *k
 // side 0 (A: matched label = olabel) or 1 (B: ilabel), its labels, the
 // largest matched label and whether the arcs are in label order; side 2
 // checks the structure only.  *nacc (if given) += number of accepting states.
+// check = false skips the checks and only gathers the label facts and nacc.
 hipError_t launch_validate(const DevGraph &g, int side, uint32_t *err, uint32_t *maxlab,
-                           hipStream_t s, uint32_t *nacc = nullptr);
+                           hipStream_t s, uint32_t *nacc = nullptr, bool check = true);
 // Views are built in two steps.  sort_view: sort the arcs of a view (side
 // 0: A by olabel, side 1: B by ilabel; by_dst selects in-views, for which
 // `off_tmp` (V+1 words) receives the group offsets; an out-view of an input

@@ -85,3 +85,26 @@ def test_options_never_change_the_result(composers, order, buckets, depth):
         got, _ = check_pair(comp, A, B, tag, ref=ref)
         if case[0] in ("hubs", "long-words", "random-64"):
             assert not fsthelp.check_invariants(A, B, got), tag
+
+
+def test_validation_off_same_result(composers):
+    """FST_OPT_VALIDATE = 0 (the caller vouches for its graphs): the same
+    result on valid inputs, compositions and scores."""
+    from paper_2110_02848_amd import gpu
+    import torch
+    c = gpu.Composer(0)
+    c.set_option(gpu.FST_OPT_VALIDATE, 0)
+    try:
+        for case in [("random-64", 0), ("random-1000", 1), ("lexicon-T100-W1000", 0),
+                     ("hubs", 0)] + [("tiny", s) for s in range(4)]:
+            A, B, ref = _inputs(case)
+            check_pair(c, A, B, f"{case} validation off", ref=ref)
+        A, B, ref = _inputs(("lexicon-T100-W1000", 0))
+        C = c.compose(gpu.to_device(A), gpu.to_device(B))
+        s_off = c.score(C)["total"].item()
+        c.set_option(gpu.FST_OPT_VALIDATE, 1)
+        s_on = c.score(C)["total"].item()
+        torch.cuda.synchronize()
+        assert s_off == s_on
+    finally:
+        c.close()
