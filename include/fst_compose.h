@@ -160,7 +160,12 @@ FST_API void fst_ctx_destroy(fst_ctx *ctx);
  * their graphs: the checks are skipped (the composition still reads the
  * largest label, the label order and the accepting states; a score reads
  * nothing before it starts), and a graph that breaks the rules then gives
- * unspecified results, which may include reads outside its arrays. */
+ * unspecified results, which may include reads outside its arrays.
+ * FST_OPT_LIST_CAPACITY (entries, 0 = default 2^22) is the first size of
+ * the search's work lists (frontier, heavy and accepting keys); a search
+ * that overflows them runs again with four times the size (never more than
+ * 2 V_A V_B), and the context keeps the size that sufficed for later calls;
+ * the result is the same. */
 enum fst_option {
   FST_OPT_MAX_WORKSPACE = 1,
   FST_OPT_TIMING = 2,
@@ -168,7 +173,8 @@ enum fst_option {
   FST_OPT_CHAIN_DEPTH = 4,
   FST_OPT_COUNT_MOVES = 5,
   FST_OPT_ORDER = 6,
-  FST_OPT_VALIDATE = 7
+  FST_OPT_VALIDATE = 7,
+  FST_OPT_LIST_CAPACITY = 8
 };
 enum fst_order {
   FST_ORDER_FORWARD_FIRST = 0,

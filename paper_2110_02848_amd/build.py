@@ -32,6 +32,9 @@ def compile_flags():
         "-fno-gpu-flush-denormals-to-zero", "-ffp-contract=off", "-fno-fast-math",
         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
         "-fvisibility=hidden", "-Wall", "-Wno-unused-function", "-Wno-unused-command-line-argument",
+        # a lambda's local that shadows a variable of the enclosing function
+        # leaves the outer one unset: an error, not a warning
+        "-Werror=shadow-uncaptured-local",
         "-I", INCLUDE, "-I", CSRC,
     ]
 

@@ -76,6 +76,8 @@ struct fst_ctx {
       t_aLab, t_aW, t_heavy, t_aLut, t_bLut, t_dLut;
   Scal3 *h_s3 = nullptr;
   uint32_t h3_hint = 0;  // hash capacity the last three-input search needed
+  unsigned long long list_hint = 0;  // search list capacity the last run needed
+  unsigned long long list_start = 1ull << 22;  // FST_OPT_LIST_CAPACITY
   struct {
     bool ready = false;
     Problem3 P = {};
@@ -617,162 +619,189 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   HIP_TRY(finish_views(J, s));
 
   // ---- search state ----
-  // every list holds at most one entry per key: 2 V_A V_B bounds the keys
-  // (f = 1 only where epsOutA), without waiting for a count of those states
-  const unsigned long long capll = 2ull * (unsigned long long)VA * (unsigned long long)VB;
-  const uint32_t cap = (uint32_t)(capll < nkeys ? capll : nkeys);  // <= nkeys < 2^32
   const size_t nwords = (size_t)((nkeys + 31) / 32);  // key-order bitmaps
   const size_t snwords = (size_t)(nsbits / 32);          // search bitmaps
-  FST_TRY(ensure(c, c->vis, snwords * 4));
-  FST_TRY(ensure(c, c->coacc, snwords * 4));
-  FST_TRY(ensure(c, c->trim, nwords * 4));
-  FST_TRY(ensure(c, c->wbase, nwords * 4));
-  FST_TRY(ensure(c, c->fq, (size_t)cap * 4));
-  FST_TRY(ensure(c, c->bq, (size_t)cap * 4));
-  FST_TRY(ensure(c, c->heavy, (size_t)cap * 4));
-  FST_TRY(ensure(c, c->hoff, (size_t)cap * 4));
-  if (c->order == FST_ORDER_CONCURRENT) {
-    FST_TRY(ensure(c, c->heavy2, (size_t)cap * 4));
-    FST_TRY(ensure(c, c->hoff2, (size_t)cap * 4));
-  }
-  FST_TRY(ensure(c, c->lists, ((size_t)VA + VB + 2) * 4));
-  size_t scan_n = nwords > (size_t)cap + 1 ? nwords : (size_t)cap + 1;
-  FST_TRY(ensure(c, c->scan_tmp, scan_temp_bytes(scan_n)));
-  HIP_TRY(hipMemsetAsync(c->vis.p, 0, snwords * 4, s));
-  HIP_TRY(hipMemsetAsync(c->coacc.p, 0, snwords * 4, s));
+  // Every list holds at most one entry per key, so 2 V_A V_B (f = 1 only
+  // where epsOutA) bounds them; what a search pushes (frontier and heavy
+  // keys, the accepting keys it meets) is far less when its threads follow
+  // keys depth-first.  The lists start at FST_OPT_LIST_CAPACITY entries
+  // (2^22 by default), or the size the last call needed, and the searches
+  // run again with four times as much when one overflows.
+  const unsigned long long capll = 2ull * (unsigned long long)VA * (unsigned long long)VB;
+  const unsigned long long cap_full = capll < nkeys ? capll : nkeys;  // <= nkeys < 2^32
+  unsigned long long cap_try = c->list_hint ? c->list_hint : c->list_start;
+  uint32_t *wbase = nullptr;
+  for (;;) {
+    const uint32_t cap = (uint32_t)(cap_try < cap_full ? cap_try : cap_full);
+    auto searches = [&]() -> int {
+    FST_TRY(ensure(c, c->vis, snwords * 4));
+    FST_TRY(ensure(c, c->coacc, snwords * 4));
+    FST_TRY(ensure(c, c->trim, nwords * 4));
+    FST_TRY(ensure(c, c->wbase, nwords * 4));
+    FST_TRY(ensure(c, c->fq, (size_t)cap * 4));
+    FST_TRY(ensure(c, c->bq, (size_t)cap * 4));
+    FST_TRY(ensure(c, c->heavy, (size_t)cap * 4));
+    FST_TRY(ensure(c, c->hoff, (size_t)cap * 4));
+    if (c->order == FST_ORDER_CONCURRENT) {
+      FST_TRY(ensure(c, c->heavy2, (size_t)cap * 4));
+      FST_TRY(ensure(c, c->hoff2, (size_t)cap * 4));
+    }
+    FST_TRY(ensure(c, c->lists, ((size_t)VA + VB + 2) * 4));
+    size_t scan_n = nwords > (size_t)cap + 1 ? nwords : (size_t)cap + 1;
+    FST_TRY(ensure(c, c->scan_tmp, scan_temp_bytes(scan_n)));
+    HIP_TRY(hipMemsetAsync(c->vis.p, 0, snwords * 4, s));
+    HIP_TRY(hipMemsetAsync(c->coacc.p, 0, snwords * 4, s));
 
-  Problem &P = c->P;
-  P = Problem{};
-  P.A = dA;
-  P.B = dB;
-  P.aOut = views[0];
-  P.bOut = views[1];
-  P.aIn = views[2];
-  P.bIn = views[3];
-  P.shiftB = shiftB;
-  P.maskB = (1u << shiftB) - 1u;
-  P.rowA = (uint32_t)rowA;
-  P.chain_max = c->chain_depth;
-  P.mark_accept = 1;
-  P.vis = as<uint32_t>(c->vis);
-  P.coacc = as<uint32_t>(c->coacc);
-  P.trim = as<uint32_t>(c->trim);
-  P.wbase = as<uint32_t>(c->wbase);
+    Problem &P = c->P;
+    P = Problem{};
+    P.A = dA;
+    P.B = dB;
+    P.aOut = views[0];
+    P.bOut = views[1];
+    P.aIn = views[2];
+    P.bIn = views[3];
+    P.shiftB = shiftB;
+    P.maskB = (1u << shiftB) - 1u;
+    P.rowA = (uint32_t)rowA;
+    P.chain_max = c->chain_depth;
+    P.mark_accept = 1;
+    P.vis = as<uint32_t>(c->vis);
+    P.coacc = as<uint32_t>(c->coacc);
+    P.trim = as<uint32_t>(c->trim);
+    P.wbase = as<uint32_t>(c->wbase);
 
-  // ---- the two searches ----
-  int32_t *la = as<int32_t>(c->lists), *lb = la + VA;
-  uint32_t *cnts = reinterpret_cast<uint32_t *>(lb + VB);
-  uint32_t *fq = as<uint32_t>(c->fq), *bq = as<uint32_t>(c->bq);
-  SearchArgs S;
-  S.Q = fq;
-  S.heavy = as<uint32_t>(c->heavy);
-  S.hoff = as<uint32_t>(c->hoff);
-  S.acc = bq;
-  S.cap = cap;
-  S.sc = d_sc;
-  S.G = d_sc->G;
-  S.gens = &d_sc->gens;
-  uint32_t *wbase = as<uint32_t>(c->wbase);
-  phase_end(c, PH_PRE, s);
-  if (c->order == FST_ORDER_CONCURRENT) {
-    // The forward search's first generations run alone (listing accepting
-    // keys as in the forward-first order).  If it has ended by then, the
-    // backward search follows as in that order; otherwise a backward search
-    // from every accepting pair runs beside the rest of it.
-    // With few accepting pairs the backward search starts at once (its
-    // seeds cannot outnumber much of the forward work).
-    const int FIRST =
-        (unsigned long long)c->h_sc->naccA * c->h_sc->naccB <= FEW_ACCEPTING_PAIRS ? 0 : 4;
-    P.restrict_fwd = 0;
-    P.restrict_bwd = 0;
-    phase_begin(c, PH_FWD, s);
-    // the generation slots are still zero from the run's first memset
-    HIP_TRY(hipMemsetAsync(cnts, 0, 8, s));
-    HIP_TRY(launch_seed_forward(P, S, la, cnts, lb, cnts + 1, s));
-    const KernelTimer tf = timer(c, FST_KERNEL_SEARCH_FORWARD);
-    tf.begin(s);
-    for (int g = 0; g < FIRST; ++g) HIP_TRY(launch_generation(P, S, true, g, s));
-    tf.end(s);
-    FST_TRY(readback(c, s));
-    FST_TRY(add_time(c, FST_KERNEL_SEARCH_FORWARD, FIRST));
-    if (c->h_sc->overflow) return FST_ERR_TOO_LARGE;
-    const GenSlot &nf = c->h_sc->G[FIRST % 3];
-    if (nf.qcount == 0 && (uint32_t)nf.hpack == 0) {
-      c->stats.fwd_levels = c->h_sc->gens;
+    // ---- the two searches ----
+    int32_t *la = as<int32_t>(c->lists), *lb = la + VA;
+    uint32_t *cnts = reinterpret_cast<uint32_t *>(lb + VB);
+    uint32_t *fq = as<uint32_t>(c->fq), *bq = as<uint32_t>(c->bq);
+    SearchArgs S;
+    S.Q = fq;
+    S.heavy = as<uint32_t>(c->heavy);
+    S.hoff = as<uint32_t>(c->hoff);
+    S.acc = bq;
+    S.cap = cap;
+    S.sc = d_sc;
+    S.G = d_sc->G;
+    S.gens = &d_sc->gens;
+    wbase = as<uint32_t>(c->wbase);
+    phase_end(c, PH_PRE, s);
+    if (c->order == FST_ORDER_CONCURRENT) {
+      // The forward search's first generations run alone (listing accepting
+      // keys as in the forward-first order).  If it has ended by then, the
+      // backward search follows as in that order; otherwise a backward search
+      // from every accepting pair runs beside the rest of it.
+      // With few accepting pairs the backward search starts at once (its
+      // seeds cannot outnumber much of the forward work).
+      const int FIRST =
+          (unsigned long long)c->h_sc->naccA * c->h_sc->naccB <= FEW_ACCEPTING_PAIRS ? 0 : 4;
+      P.restrict_fwd = 0;
+      P.restrict_bwd = 0;
+      phase_begin(c, PH_FWD, s);
+      // the generation slots are still zero from the run's first memset
+      HIP_TRY(hipMemsetAsync(cnts, 0, 8, s));
+      HIP_TRY(launch_seed_forward(P, S, la, cnts, lb, cnts + 1, s));
+      const KernelTimer tf = timer(c, FST_KERNEL_SEARCH_FORWARD);
+      tf.begin(s);
+      for (int g = 0; g < FIRST; ++g) HIP_TRY(launch_generation(P, S, true, g, s));
+      tf.end(s);
+      FST_TRY(readback(c, s));
+      FST_TRY(add_time(c, FST_KERNEL_SEARCH_FORWARD, FIRST));
+      if (c->h_sc->overflow) return FST_ERR_TOO_LARGE;
+      const GenSlot &nf = c->h_sc->G[FIRST % 3];
+      if (nf.qcount == 0 && (uint32_t)nf.hpack == 0) {
+        c->stats.fwd_levels = c->h_sc->gens;
+        HIP_TRY(launch_popcount(P.vis, snwords, &d_sc->naccessible, s));
+        if (c->count_moves) HIP_TRY(launch_count_moves(P, snwords, true, &d_sc->generated, s));
+        phase_end(c, PH_FWD, s);
+        phase_begin(c, PH_BWD, s);
+        P.restrict_bwd = 1;
+        HIP_TRY(hipMemsetAsync(d_sc->G, 0, sizeof(d_sc->G), s));
+        HIP_TRY(launch_seed_backward(P, S, bq, s));
+        FST_TRY(search(c, S, false, &c->stats.bwd_levels, s));
+        HIP_TRY(launch_trim(P, (uint32_t)VA, as<uint32_t>(c->trim), wbase, s));
+        phase_end(c, PH_BWD, s);
+      } else {
+        P.mark_accept = 0;  // the backward seeds below are every accepting pair
+        SearchArgs SB = S;
+        SB.Q = bq;  // the forward search's list of accepting keys is not needed
+        SB.heavy = as<uint32_t>(c->heavy2);
+        SB.hoff = as<uint32_t>(c->hoff2);
+        SB.acc = nullptr;
+        SB.G = d_sc->G2;
+        SB.gens = &d_sc->gens2;
+        HIP_TRY(hipMemsetAsync(cnts, 0, 8, s));
+        HIP_TRY(launch_seed_backward_all(P, SB, la, cnts, lb, cnts + 1, s));
+        FST_TRY(search_concurrent(c, P, S, SB, FIRST, s));
+        HIP_TRY(launch_popcount(P.vis, snwords, &d_sc->naccessible, s));
+        if (c->count_moves) HIP_TRY(launch_count_moves(P, snwords, true, &d_sc->generated, s));
+        phase_end(c, PH_FWD, s);
+        // the backward phase is the final intersection only
+        phase_begin(c, PH_BWD, s);
+        HIP_TRY(launch_trim(P, (uint32_t)VA, as<uint32_t>(c->trim), wbase, s));
+        phase_end(c, PH_BWD, s);
+      }
+    } else if (c->order == FST_ORDER_COACCESSIBLE_FIRST) {
+      // Algorithm 1's order: the co-accessible set over all key pairs first,
+      // from every accepting pair, then the forward search inside it
+      P.restrict_fwd = 1;
+      P.restrict_bwd = 0;
+      phase_begin(c, PH_BWD, s);
+      HIP_TRY(hipMemsetAsync(cnts, 0, 8, s));
+      HIP_TRY(hipMemsetAsync(d_sc->G, 0, sizeof(d_sc->G), s));
+      HIP_TRY(launch_seed_backward_all(P, S, la, cnts, lb, cnts + 1, s));
+      FST_TRY(search(c, S, false, &c->stats.bwd_levels, s));
+      phase_end(c, PH_BWD, s);
+      phase_begin(c, PH_FWD, s);
+      HIP_TRY(hipMemsetAsync(cnts, 0, 8, s));
+      HIP_TRY(hipMemsetAsync(d_sc->G, 0, sizeof(d_sc->G), s));
+      HIP_TRY(launch_seed_forward(P, S, la, cnts, lb, cnts + 1, s));
+      FST_TRY(search(c, S, true, &c->stats.fwd_levels, s));
+      HIP_TRY(launch_popcount(P.vis, snwords, &d_sc->naccessible, s));
+      if (c->count_moves) HIP_TRY(launch_count_moves(P, snwords, true, &d_sc->generated, s));
+      HIP_TRY(launch_trim(P, (uint32_t)VA, as<uint32_t>(c->trim), wbase, s));
+      phase_end(c, PH_FWD, s);
+    } else {
+      P.restrict_fwd = 0;
+      P.restrict_bwd = 1;
+      phase_begin(c, PH_FWD, s);
+      HIP_TRY(hipMemsetAsync(cnts, 0, 8, s));
+      HIP_TRY(hipMemsetAsync(d_sc->G, 0, sizeof(d_sc->G), s));
+      HIP_TRY(launch_seed_forward(P, S, la, cnts, lb, cnts + 1, s));
+      FST_TRY(search(c, S, true, &c->stats.fwd_levels, s));
       HIP_TRY(launch_popcount(P.vis, snwords, &d_sc->naccessible, s));
       if (c->count_moves) HIP_TRY(launch_count_moves(P, snwords, true, &d_sc->generated, s));
       phase_end(c, PH_FWD, s);
+
+      // backward search, seeded by the accepting keys listed in bq
       phase_begin(c, PH_BWD, s);
-      P.restrict_bwd = 1;
       HIP_TRY(hipMemsetAsync(d_sc->G, 0, sizeof(d_sc->G), s));
       HIP_TRY(launch_seed_backward(P, S, bq, s));
       FST_TRY(search(c, S, false, &c->stats.bwd_levels, s));
-      HIP_TRY(launch_trim(P, (uint32_t)VA, as<uint32_t>(c->trim), wbase, s));
-      phase_end(c, PH_BWD, s);
-    } else {
-      P.mark_accept = 0;  // the backward seeds below are every accepting pair
-      SearchArgs SB = S;
-      SB.Q = bq;  // the forward search's list of accepting keys is not needed
-      SB.heavy = as<uint32_t>(c->heavy2);
-      SB.hoff = as<uint32_t>(c->hoff2);
-      SB.acc = nullptr;
-      SB.G = d_sc->G2;
-      SB.gens = &d_sc->gens2;
-      HIP_TRY(hipMemsetAsync(cnts, 0, 8, s));
-      HIP_TRY(launch_seed_backward_all(P, SB, la, cnts, lb, cnts + 1, s));
-      FST_TRY(search_concurrent(c, P, S, SB, FIRST, s));
-      HIP_TRY(launch_popcount(P.vis, snwords, &d_sc->naccessible, s));
-      if (c->count_moves) HIP_TRY(launch_count_moves(P, snwords, true, &d_sc->generated, s));
-      phase_end(c, PH_FWD, s);
-      // the backward phase is the final intersection only
-      phase_begin(c, PH_BWD, s);
+      // the backward search may set co-accessible bits of keys it never
+      // expands (not accessible); the trim set is what remains after masking
+      // them, and the same pass counts the trim keys of every bitmap word
       HIP_TRY(launch_trim(P, (uint32_t)VA, as<uint32_t>(c->trim), wbase, s));
       phase_end(c, PH_BWD, s);
     }
-  } else if (c->order == FST_ORDER_COACCESSIBLE_FIRST) {
-    // Algorithm 1's order: the co-accessible set over all key pairs first,
-    // from every accepting pair, then the forward search inside it
-    P.restrict_fwd = 1;
-    P.restrict_bwd = 0;
-    phase_begin(c, PH_BWD, s);
-    HIP_TRY(hipMemsetAsync(cnts, 0, 8, s));
-    HIP_TRY(hipMemsetAsync(d_sc->G, 0, sizeof(d_sc->G), s));
-    HIP_TRY(launch_seed_backward_all(P, S, la, cnts, lb, cnts + 1, s));
-    FST_TRY(search(c, S, false, &c->stats.bwd_levels, s));
-    phase_end(c, PH_BWD, s);
-    phase_begin(c, PH_FWD, s);
-    HIP_TRY(hipMemsetAsync(cnts, 0, 8, s));
-    HIP_TRY(hipMemsetAsync(d_sc->G, 0, sizeof(d_sc->G), s));
-    HIP_TRY(launch_seed_forward(P, S, la, cnts, lb, cnts + 1, s));
-    FST_TRY(search(c, S, true, &c->stats.fwd_levels, s));
-    HIP_TRY(launch_popcount(P.vis, snwords, &d_sc->naccessible, s));
-    if (c->count_moves) HIP_TRY(launch_count_moves(P, snwords, true, &d_sc->generated, s));
-    HIP_TRY(launch_trim(P, (uint32_t)VA, as<uint32_t>(c->trim), wbase, s));
-    phase_end(c, PH_FWD, s);
-  } else {
-    P.restrict_fwd = 0;
-    P.restrict_bwd = 1;
-    phase_begin(c, PH_FWD, s);
-    HIP_TRY(hipMemsetAsync(cnts, 0, 8, s));
-    HIP_TRY(hipMemsetAsync(d_sc->G, 0, sizeof(d_sc->G), s));
-    HIP_TRY(launch_seed_forward(P, S, la, cnts, lb, cnts + 1, s));
-    FST_TRY(search(c, S, true, &c->stats.fwd_levels, s));
-    HIP_TRY(launch_popcount(P.vis, snwords, &d_sc->naccessible, s));
-    if (c->count_moves) HIP_TRY(launch_count_moves(P, snwords, true, &d_sc->generated, s));
-    phase_end(c, PH_FWD, s);
+    if (c->count_moves) HIP_TRY(launch_count_moves(P, nwords, false, &d_sc->generated_bwd, s));
 
-    // backward search, seeded by the accepting keys listed in bq
-    phase_begin(c, PH_BWD, s);
-    HIP_TRY(hipMemsetAsync(d_sc->G, 0, sizeof(d_sc->G), s));
-    HIP_TRY(launch_seed_backward(P, S, bq, s));
-    FST_TRY(search(c, S, false, &c->stats.bwd_levels, s));
-    // the backward search may set co-accessible bits of keys it never
-    // expands (not accessible); the trim set is what remains after masking
-    // them, and the same pass counts the trim keys of every bitmap word
-    HIP_TRY(launch_trim(P, (uint32_t)VA, as<uint32_t>(c->trim), wbase, s));
-    phase_end(c, PH_BWD, s);
+      return FST_OK;
+    };
+    const int rc = searches();
+    if (rc == FST_ERR_TOO_LARGE && c->h_sc->overflow && (unsigned long long)cap < cap_full) {
+      cap_try = 4ull * cap;
+      // the search scalars start again from zero (validation's stay)
+      HIP_TRY(hipMemsetAsync(&d_sc->tail2, 0, sizeof(uint32_t), s));
+      HIP_TRY(hipMemsetAsync(&d_sc->heavy, 0,
+                             offsetof(Scalars, gens2) + sizeof(uint32_t) -
+                                 offsetof(Scalars, heavy), s));
+      continue;
+    }
+    FST_TRY(rc);
+    c->list_hint = cap;
+    break;
   }
-  if (c->count_moves) HIP_TRY(launch_count_moves(P, nwords, false, &d_sc->generated_bwd, s));
+  if (!wbase) return FST_ERR_HIP;  // the searches set it; never launch on a null buffer
 
   // ---- numbering and arc counts ----
   phase_begin(c, PH_COUNT, s);
@@ -781,8 +810,13 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   const unsigned long long nst = c->h_sc->total;
   if (nst > (unsigned long long)INT32_MAX) return FST_ERR_TOO_LARGE;
   const uint32_t nstates = (uint32_t)nst;
-  uint32_t *key_of = fq;   // the forward queue is free now (nstates <= cap)
-  uint32_t *heavy = bq;    // so is the backward queue
+  // the search lists are free now: the forward queue takes the key of
+  // every state, the backward queue the heavy states
+  FST_TRY(ensure(c, c->fq, ((size_t)nstates + 1) * 4));
+  FST_TRY(ensure(c, c->bq, ((size_t)nstates + 1) * 4));
+  uint32_t *key_of = as<uint32_t>(c->fq);
+  uint32_t *heavy = as<uint32_t>(c->bq);
+  const Problem &P = c->P;
   HIP_TRY(launch_key_of_id(P.trim, wbase, nwords, key_of, s));
   FST_TRY(ensure(c, c->cnt, ((size_t)nstates + 1) * 4));
   FST_TRY(ensure(c, c->btot, (OUT_CHUNKS + 1) * 4));
@@ -1334,6 +1368,11 @@ int fst_ctx_set_option(fst_ctx *c, int option, int64_t value) {
           value != FST_ORDER_CONCURRENT)
         return FST_ERR_INVALID_ARG;
       c->order = (int)value;
+      return FST_OK;
+    case FST_OPT_LIST_CAPACITY:
+      if (value < 0 || value > (1ll << 32)) return FST_ERR_INVALID_ARG;
+      c->list_start = value ? (unsigned long long)value : (1ull << 22);
+      c->list_hint = 0;
       return FST_OK;
     case FST_OPT_VALIDATE:
       c->validate = value != 0;

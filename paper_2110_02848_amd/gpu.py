@@ -32,6 +32,7 @@ FST_OPT_CHAIN_DEPTH = 4
 FST_OPT_COUNT_MOVES = 5
 FST_OPT_ORDER = 6
 FST_OPT_VALIDATE = 7
+FST_OPT_LIST_CAPACITY = 8
 
 FST_SCATTER_NOALLOC_MAX_TARGETS = 1 << 20
 

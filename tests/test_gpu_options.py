@@ -108,3 +108,25 @@ def test_validation_off_same_result(composers):
         assert s_off == s_on
     finally:
         c.close()
+
+
+@pytest.mark.parametrize("order", ORDERS)
+def test_search_lists_grow(composers, order):
+    """Search lists far too small at first (FST_OPT_LIST_CAPACITY = 256):
+    every search overflows them, grows them four-fold and runs again, with
+    the same result; the next call starts at the size that sufficed."""
+    from paper_2110_02848_amd import gpu
+    c = gpu.Composer(0)
+    try:
+        c.set_option(gpu.FST_OPT_ORDER, {"forward-first": gpu.FST_ORDER_FORWARD_FIRST,
+                                         "coaccessible-first": gpu.FST_ORDER_COACCESSIBLE_FIRST,
+                                         "concurrent": gpu.FST_ORDER_CONCURRENT}[order])
+        c.set_option(gpu.FST_OPT_COUNT_MOVES, 1)
+        for case in [("random-1000", 1), ("lexicon-T100-W1000", 0), ("hubs", 0),
+                     ("random-64", 1)]:
+            c.set_option(gpu.FST_OPT_LIST_CAPACITY, 256)
+            A, B, ref = _inputs(case)
+            check_pair(c, A, B, f"{case} lists from 256 entries, {order}", ref=ref)
+            check_pair(c, A, B, f"{case} again, {order}", ref=ref)
+    finally:
+        c.close()
