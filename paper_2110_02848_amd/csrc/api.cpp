@@ -913,8 +913,13 @@ int levels3(fst_ctx *c, const Problem3 &P, const Search3 &S, bool forward, uint3
     FST_TRY(readback3(c, s));
     FST_TRY(add_time(c, FST_KERNEL_SEARCH3, 2 * batch));
     const Lvl3 &nx = c->h_s3->ring[g % 3];
-    if (c->h_s3->overflow || (unsigned long long)nx.fbase + nx.fcount > grow_at) return FST_OK;
-    if (nx.fcount == 0) break;
+    // keys in the set: those of the frontiers and those walks went on to
+    if (c->h_s3->overflow ||
+        (unsigned long long)nx.fbase + nx.fcount + c->h_s3->ncont > grow_at)
+      return FST_OK;
+    // walks that reach a heavy key leave it as a chunk of the next level:
+    // a level can hold chunks and no frontier
+    if (nx.fcount == 0 && nx.ccount == 0) break;
     batch = batch == 4 ? 16 : (batch < 64 ? 2 * batch : 64);
   }
   *done = true;
@@ -993,7 +998,7 @@ int compose3_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, const fst_
     const unsigned long long acap = 4 * H;
     FST_TRY(ensure(c, c->t_tab, H * 8));
     FST_TRY(ensure(c, c->t_F, H * 4));
-    FST_TRY(ensure(c, c->t_chunks, H * 8));
+    FST_TRY(ensure(c, c->t_chunks, 2 * H * 8));
     FST_TRY(ensure(c, c->t_arcs, acap * 8));
     HIP_TRY(hipMemsetAsync(c->t_tab.p, 0xff, H * 8, s));
     HIP_TRY(hipMemsetAsync(&d3->overflow, 0, offsetof(Scal3, ring) - offsetof(Scal3, overflow) +
@@ -1020,11 +1025,12 @@ int compose3_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, const fst_
   c->h3_hint = (uint32_t)H;
   const Scal3 f = *c->h_s3;
   c->c3.stats.fwd_levels = f.levels;
-  const unsigned long long nacc = f.ring[0].fbase > f.ring[1].fbase
-                                      ? (f.ring[0].fbase > f.ring[2].fbase ? f.ring[0].fbase
-                                                                           : f.ring[2].fbase)
-                                      : (f.ring[1].fbase > f.ring[2].fbase ? f.ring[1].fbase
-                                                                           : f.ring[2].fbase);
+  const unsigned long long nacc = (f.ring[0].fbase > f.ring[1].fbase
+                                       ? (f.ring[0].fbase > f.ring[2].fbase ? f.ring[0].fbase
+                                                                            : f.ring[2].fbase)
+                                       : (f.ring[1].fbase > f.ring[2].fbase ? f.ring[1].fbase
+                                                                            : f.ring[2].fbase)) +
+                                  (unsigned long long)f.ncont;
   c->c3.stats.accessible = (int64_t)nacc;
   const unsigned long long narcs = f.narcs;
   c->c3.stats.generated = (int64_t)narcs;
@@ -1036,9 +1042,10 @@ int compose3_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, const fst_
   FST_TRY(ensure(c, c->t_insrc, (narcs + 1) * 4));
   FST_TRY(ensure(c, c->t_coacc, (H / 32 + 1) * 4));
   FST_TRY(ensure(c, c->scan_tmp, scan_temp_bytes(H + 1)));
-  const unsigned long long ccap = H + narcs / 32 + 1;
+  // chunks of LIGHT3 = 8 in-arcs: a key is chunked at most once
+  const unsigned long long ccap = H + narcs / 8 + 1;
   if (ccap > 0xffffffffull) return FST_ERR_TOO_LARGE;
-  FST_TRY(ensure(c, c->t_chunks, ccap * 8));
+  FST_TRY(ensure(c, c->t_chunks, 2 * ccap * 8));
   uint32_t *inoff = as<uint32_t>(c->t_inoff);
   HIP_TRY(hipMemsetAsync(inoff, 0, (H + 1) * 4, s));
   HIP_TRY(launch3_in_arcs(S.arcs, narcs, inoff, nullptr, false, s));

@@ -29,10 +29,13 @@
 // B state has one arc (a lexicon word) has one unit however many arcs its
 // A state has.
 //
-// The search goes level by level: one thread per frontier key with at most
-// LIGHT3 units, one thread per chunk of LIGHT3 units of the others.  New
-// keys are appended to the next frontier and every generated arc (source
-// slot, target slot) to an arc list, one atomic per wavefront.
+// The search goes level by level.  A thread takes a frontier key (or a
+// chunk of LIGHT3 units of a heavy key), expands it and goes on depth-first
+// with the first new key it reached (up to CHAIN3 keys), so a word of a
+// lexicon is one thread's walk; other new keys join the next frontier, and
+// heavy keys met on a walk are cut into chunks.  Every generated arc
+// (source slot, target slot) is appended to an arc list, and new keys to
+// the next frontier, one atomic per wavefront.
 // Co-accessibility runs backwards over that arc list (in-arcs grouped by a
 // count, a scan and a placement).  The trim keys are sorted (radix sort of
 // the 64-bit keys): a state's id is its rank.  Count and fill give a state
@@ -387,12 +390,46 @@ __global__ __launch_bounds__(NT) void k3_seed(Problem3 P, Search3 S, const int32
   }
 }
 
+// Keys one search thread may expand depth-first, one after the other,
+// before it hands new keys to the next level.
+constexpr int CHAIN3 = 64;
+
+// The chunk list of level l: levels of even and odd number use the two
+// halves of the chunk array (ccap entries each), so a level's chunks are
+// read while the next level's are written.
+__device__ __forceinline__ uint2 *chunks_of(const Search3 &S, int l) {
+  return S.chunks + (size_t)(l & 1) * S.ccap;
+}
+
+// Sum of v over the wave into *counter (one atomic); every lane of the
+// wave takes part.
+__device__ __forceinline__ void wave_add(uint32_t v, uint32_t *counter) {
+#pragma unroll
+  for (int o = WAVE / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, WAVE);
+  if (__lane_id() == 0 && v) atomicAdd(counter, v);
+}
+
+// Chunks of LIGHT3 units of a heavy key into level l's chunk list (counter
+// lv = the level's ring slot).
+__device__ __forceinline__ void push_chunks(const Search3 &S, Lvl3 *lv, int l, uint32_t slot,
+                                            uint32_t n) {
+  uint2 *list = chunks_of(S, l);
+  const uint32_t nc = (n + LIGHT3 - 1) / LIGHT3;
+  const uint32_t c0 = atomicAdd(&lv->ccount, nc);
+  for (uint32_t c = 0; c < nc; ++c) {
+    if ((ull)c0 + c < S.ccap) list[c0 + c] = make_uint2(slot, c * LIGHT3);
+    else atomicOr(&S.sc->overflow, 1u);
+  }
+}
+
 // The moves of units [u0, u1) of the key in `slot`: every target is looked
-// up / inserted; new keys join the next frontier; every move is recorded as
-// an arc (source slot, target slot).
+// up / inserted and every move recorded as an arc (source slot, target
+// slot).  The first new key becomes *cont when the thread may go on
+// depth-first (cont not null and none taken yet); other new keys join the
+// next frontier.
 __device__ __forceinline__ void expand_units(const Problem3 &P, const Search3 &S, uint32_t slot,
                                              const Units3 &u, uint32_t u0, uint32_t u1, Lvl3 *nx,
-                                             uint32_t nbase) {
+                                             uint32_t nbase, uint32_t *cont) {
   for (uint32_t j = u0; j < u1; ++j)
     for_unit3(P, u, j, [&](ull t, int32_t, int32_t, float, int32_t, int32_t, int32_t) {
       bool fresh;
@@ -400,15 +437,43 @@ __device__ __forceinline__ void expand_units(const Problem3 &P, const Search3 &S
       if (ts == NO_SLOT) return;
       wave_append<uint2>(true, make_uint2(slot, ts), S.arcs, S.acap, &S.sc->narcs,
                          &S.sc->overflow);
-      wave_append<uint32_t>(fresh, ts, S.F + nbase, (ull)S.fcap - nbase, &nx->fcount,
+      bool push = fresh;
+      if (fresh && cont && *cont == NO_SLOT) {
+        *cont = ts;
+        push = false;
+      }
+      wave_append<uint32_t>(push, ts, S.F + nbase, (ull)S.fcap - nbase, &nx->fcount,
                             &S.sc->overflow);
     });
 }
 
+// A thread's depth-first walk from the key in `slot`: a light key is
+// expanded at once and the walk goes on with the first new key it reached
+// (up to CHAIN3 keys); a heavy key is cut into chunks for the chunk list
+// `heavy_to`.  Every other new key joins the next frontier.  Returns the
+// number of keys the walk went on to.
+__device__ __forceinline__ uint32_t walk_fwd(const Problem3 &P, const Search3 &S, uint32_t slot,
+                                             Lvl3 *nx, uint32_t nbase, Lvl3 *heavy_to,
+                                             int heavy_l) {
+  for (int depth = 0; depth < CHAIN3; ++depth) {
+    const Units3 u = units_of(P, P.tab[slot]);
+    const uint32_t n = nunits(u);
+    if (n > LIGHT3) {
+      push_chunks(S, heavy_to, heavy_l, slot, n);
+      return (uint32_t)depth;
+    }
+    uint32_t cont = NO_SLOT;
+    expand_units(P, S, slot, u, 0, n, nx, nbase, depth + 1 < CHAIN3 ? &cont : nullptr);
+    if (cont == NO_SLOT) return (uint32_t)depth;
+    slot = cont;
+  }
+  return CHAIN3 - 1;
+}
+
 // Level l of the forward search: frontier entries [fbase, fbase + fcount)
-// of ring[l % 3]; light keys are expanded here, heavy ones cut into chunks
-// of LIGHT3 units for k3_fwd_chunks.  Block 0 publishes the next level's
-// frontier base and clears the ring slot of level l + 2.
+// of ring[l % 3], each the start of a depth-first walk; heavy keys met go to
+// this level's chunks (k3_fwd_chunks, next).  Block 0 publishes the next
+// level's frontier base and clears the ring slot of level l + 2.
 __global__ __launch_bounds__(NT) void k3_fwd(Problem3 P, Search3 S, int l) {
   const Lvl3 cur = S.ring[l % 3];
   Lvl3 *nx = &S.ring[(l + 1) % 3];
@@ -418,40 +483,35 @@ __global__ __launch_bounds__(NT) void k3_fwd(Problem3 P, Search3 S, int l) {
     Lvl3 *done = &S.ring[(l + 2) % 3];
     done->fcount = 0;
     done->ccount = 0;
-    if (cur.fcount) S.sc->levels = (uint32_t)l + 1;
+    if (cur.fcount || cur.ccount) S.sc->levels = (uint32_t)l + 1;
   }
-  if (S.sc->overflow) return;
-  for (ull i = (ull)blockIdx.x * NT + threadIdx.x; i < cur.fcount; i += (ull)gridDim.x * NT) {
-    const uint32_t slot = S.F[cur.fbase + i];
-    const Units3 u = units_of(P, P.tab[slot]);
-    const uint32_t n = nunits(u);
-    if (n > LIGHT3) {
-      const uint32_t nc = (n + LIGHT3 - 1) / LIGHT3;
-      const uint32_t c0 = atomicAdd(&S.ring[l % 3].ccount, nc);
-      for (uint32_t c = 0; c < nc; ++c) {
-        if ((ull)c0 + c < S.ccap) S.chunks[c0 + c] = make_uint2((uint32_t)i, c * LIGHT3);
-        else atomicOr(&S.sc->overflow, 1u);
-      }
-      continue;
-    }
-    expand_units(P, S, slot, u, 0, n, nx, nbase);
-  }
+  uint32_t went = 0;
+  if (!S.sc->overflow)
+    for (ull i = (ull)blockIdx.x * NT + threadIdx.x; i < cur.fcount; i += (ull)gridDim.x * NT)
+      went += walk_fwd(P, S, S.F[cur.fbase + i], nx, nbase, &S.ring[l % 3], l);
+  wave_add(went, &S.sc->ncont);
 }
 
+// The chunks of level l: LIGHT3 units each, then a depth-first walk from
+// the first new key; heavy keys met on the walk go to the next level's
+// chunks.
 __global__ __launch_bounds__(NT) void k3_fwd_chunks(Problem3 P, Search3 S, int l) {
   const Lvl3 cur = S.ring[l % 3];
   Lvl3 *nx = &S.ring[(l + 1) % 3];
   const uint32_t nbase = cur.fbase + cur.fcount;
-  if (S.sc->overflow) return;
-  const uint32_t nch = cur.ccount < S.ccap ? cur.ccount : S.ccap;
+  const uint32_t nch = S.sc->overflow ? 0 : (cur.ccount < S.ccap ? cur.ccount : S.ccap);
+  const uint2 *list = chunks_of(S, l);
+  uint32_t went = 0;
   for (ull i = (ull)blockIdx.x * NT + threadIdx.x; i < nch; i += (ull)gridDim.x * NT) {
-    const uint2 c = S.chunks[i];
-    const uint32_t slot = S.F[cur.fbase + c.x];
-    const Units3 u = units_of(P, P.tab[slot]);
+    const uint2 c = list[i];
+    const Units3 u = units_of(P, P.tab[c.x]);
     const uint32_t n = nunits(u);
     const uint32_t u1 = c.y + LIGHT3 < n ? c.y + LIGHT3 : n;
-    expand_units(P, S, slot, u, c.y, u1, nx, nbase);
+    uint32_t cont = NO_SLOT;
+    expand_units(P, S, c.x, u, c.y, u1, nx, nbase, &cont);
+    if (cont != NO_SLOT) went += 1 + walk_fwd(P, S, cont, nx, nbase, nx, l + 1);
   }
+  wave_add(went, &S.sc->ncont);
 }
 
 // ---------------------------------------------------------------------------
@@ -494,14 +554,39 @@ __global__ __launch_bounds__(NT) void k3_seed_bwd(Problem3 P, Search3 S) {
   }
 }
 
+// Sources of in-arcs [p0, p1): each one claimed becomes *cont (the first,
+// when allowed) or joins the next frontier.
 __device__ __forceinline__ void bwd_range(const Problem3 &P, const Search3 &S, uint32_t p0,
-                                          uint32_t p1, Lvl3 *nx, uint32_t nbase) {
+                                          uint32_t p1, Lvl3 *nx, uint32_t nbase,
+                                          uint32_t *cont) {
   for (uint32_t p = p0; p < p1; ++p) {
     const uint32_t u = P.in_src[p];
-    const bool fresh = claim_bit(P.coacc, u);
-    wave_append<uint32_t>(fresh, u, S.F + nbase, (ull)S.fcap - nbase, &nx->fcount,
+    bool push = claim_bit(P.coacc, u);
+    if (push && cont && *cont == NO_SLOT) {
+      *cont = u;
+      push = false;
+    }
+    wave_append<uint32_t>(push, u, S.F + nbase, (ull)S.fcap - nbase, &nx->fcount,
                           &S.sc->overflow);
   }
+}
+
+// Depth-first backward walk from slot v (as walk_fwd, over in-arcs).
+__device__ __forceinline__ uint32_t walk_bwd(const Problem3 &P, const Search3 &S, uint32_t v,
+                                             Lvl3 *nx, uint32_t nbase, Lvl3 *heavy_to,
+                                             int heavy_l) {
+  for (int depth = 0; depth < CHAIN3; ++depth) {
+    const uint32_t p0 = P.in_off[v], p1 = P.in_off[v + 1];
+    if (p1 - p0 > LIGHT3) {
+      push_chunks(S, heavy_to, heavy_l, v, p1 - p0);
+      return (uint32_t)depth;
+    }
+    uint32_t cont = NO_SLOT;
+    bwd_range(P, S, p0, p1, nx, nbase, depth + 1 < CHAIN3 ? &cont : nullptr);
+    if (cont == NO_SLOT) return (uint32_t)depth;
+    v = cont;
+  }
+  return CHAIN3 - 1;
 }
 
 __global__ __launch_bounds__(NT) void k3_bwd(Problem3 P, Search3 S, int l) {
@@ -513,38 +598,31 @@ __global__ __launch_bounds__(NT) void k3_bwd(Problem3 P, Search3 S, int l) {
     Lvl3 *done = &S.ring[(l + 2) % 3];
     done->fcount = 0;
     done->ccount = 0;
-    if (cur.fcount) S.sc->levels = (uint32_t)l + 1;
+    if (cur.fcount || cur.ccount) S.sc->levels = (uint32_t)l + 1;
   }
-  if (S.sc->overflow) return;
-  for (ull i = (ull)blockIdx.x * NT + threadIdx.x; i < cur.fcount; i += (ull)gridDim.x * NT) {
-    const uint32_t v = S.F[cur.fbase + i];
-    const uint32_t p0 = P.in_off[v], p1 = P.in_off[v + 1];
-    if (p1 - p0 > LIGHT3) {
-      const uint32_t nc = (p1 - p0 + LIGHT3 - 1) / LIGHT3;
-      const uint32_t c0 = atomicAdd(&S.ring[l % 3].ccount, nc);
-      for (uint32_t c = 0; c < nc; ++c) {
-        if ((ull)c0 + c < S.ccap) S.chunks[c0 + c] = make_uint2((uint32_t)i, c * LIGHT3);
-        else atomicOr(&S.sc->overflow, 1u);
-      }
-      continue;
-    }
-    bwd_range(P, S, p0, p1, nx, nbase);
-  }
+  uint32_t went = 0;
+  if (!S.sc->overflow)
+    for (ull i = (ull)blockIdx.x * NT + threadIdx.x; i < cur.fcount; i += (ull)gridDim.x * NT)
+      went += walk_bwd(P, S, S.F[cur.fbase + i], nx, nbase, &S.ring[l % 3], l);
+  wave_add(went, &S.sc->ncont);
 }
 
 __global__ __launch_bounds__(NT) void k3_bwd_chunks(Problem3 P, Search3 S, int l) {
   const Lvl3 cur = S.ring[l % 3];
   Lvl3 *nx = &S.ring[(l + 1) % 3];
   const uint32_t nbase = cur.fbase + cur.fcount;
-  if (S.sc->overflow) return;
-  const uint32_t nch = cur.ccount < S.ccap ? cur.ccount : S.ccap;
+  const uint32_t nch = S.sc->overflow ? 0 : (cur.ccount < S.ccap ? cur.ccount : S.ccap);
+  const uint2 *list = chunks_of(S, l);
+  uint32_t went = 0;
   for (ull i = (ull)blockIdx.x * NT + threadIdx.x; i < nch; i += (ull)gridDim.x * NT) {
-    const uint2 c = S.chunks[i];
-    const uint32_t v = S.F[cur.fbase + c.x];
-    const uint32_t p0 = P.in_off[v] + c.y, pe = P.in_off[v + 1];
+    const uint2 c = list[i];
+    const uint32_t p0 = P.in_off[c.x] + c.y, pe = P.in_off[c.x + 1];
     const uint32_t p1 = p0 + LIGHT3 < pe ? p0 + LIGHT3 : pe;
-    bwd_range(P, S, p0, p1, nx, nbase);
+    uint32_t cont = NO_SLOT;
+    bwd_range(P, S, p0, p1, nx, nbase, &cont);
+    if (cont != NO_SLOT) went += 1 + walk_bwd(P, S, cont, nx, nbase, nx, l + 1);
   }
+  wave_add(went, &S.sc->ncont);
 }
 
 // ---------------------------------------------------------------------------

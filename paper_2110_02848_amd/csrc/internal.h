@@ -217,6 +217,7 @@ struct Lvl3 {
 struct Scal3 {
   uint32_t errA, errB, errD, maxA, maxB, maxD;
   uint32_t overflow, levels, narcs, ntrim;
+  uint32_t ncont, pad;       // keys a search walk went on to (not in the frontier)
   uint32_t nheavy[2];        // heavy states of C (and an overflow word)
   unsigned long long total;  // scan totals
   Lvl3 ring[3];
@@ -225,8 +226,8 @@ struct Scal3 {
 struct Search3 {
   uint32_t *F;       // frontier slots, level after level
   uint32_t fcap;
-  uint2 *chunks;     // (frontier index, first unit) of the chunks of heavy states
-  uint32_t ccap;
+  uint2 *chunks;     // (slot, first unit) of the chunks of heavy keys: two
+  uint32_t ccap;     // lists of ccap entries (levels of even / odd number)
   uint2 *arcs;       // generated arcs (source slot, target slot)
   unsigned long long acap;
   Lvl3 *ring;
