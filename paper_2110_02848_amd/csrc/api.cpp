@@ -76,7 +76,9 @@ struct fst_ctx {
       t_aLab, t_aW, t_heavy, t_aLut, t_bLut, t_dLut;
   Scal3 *h_s3 = nullptr;
   uint32_t h3_hint = 0;  // hash capacity the last three-input search needed
+  int lv3_hint[2] = {0, 0};  // levels the last three-input searches took (bwd, fwd)
   unsigned long long list_hint = 0;  // search list capacity the last run needed
+  int gen_hint = 0;  // launches the last concurrent search took
   unsigned long long list_start = 1ull << 22;  // FST_OPT_LIST_CAPACITY
   struct {
     bool ready = false;
@@ -101,7 +103,7 @@ struct fst_ctx {
   Problem P = {};
   uint32_t nstates = 0, narcs = 0, nheavy = 0;
   unsigned long long nkeys = 0;
-  size_t out_per = NT;  // states per workgroup in the output passes
+  size_t out_words = 0;  // trim words the output passes cover
   fst_stats stats = {};
 };
 
@@ -208,7 +210,8 @@ void phase_end(fst_ctx *c, int ph, hipStream_t s) {
 }
 
 int finish_empty(fst_ctx *c, int64_t *V_C, int64_t *E_C) {
-  c->P = Problem{};
+  c->P = Problem{};  // no trim bitmap: the fill must not read one
+  c->out_words = 0;
   c->nstates = 0;
   c->narcs = 0;
   c->nheavy = 0;
@@ -452,10 +455,13 @@ int search_concurrent(fst_ctx *c, Problem P, const SearchArgs &SF, const SearchA
                       hipStream_t s) {
   const KernelTimer t = timer(c, FST_KERNEL_SEARCH_FORWARD);
   int gf = g0, gb = 0;  // each search numbers its own generations
-  bool fdone = false, bdone = false, pause = false;
+  bool fdone = false, bdone = false, pause = false, first = true;
   for (;;) {
-    // the one search left after the other ends is usually near its end too
-    const int batch = fdone || bdone ? 8 : 16;
+    // the one search left after the other ends is usually near its end too;
+    // the first batch covers as many launches as the last search took
+    int batch = fdone || bdone ? 8 : 16;
+    if (first && c->gen_hint > batch) batch = c->gen_hint < 256 ? c->gen_hint : 256;
+    first = false;
     t.begin(s);
     for (int b = 0; b < batch; ++b) {
       if (!fdone && !bdone && !pause) HIP_TRY(launch_generation2(P, SF, SB, gf++, gb++, s));
@@ -481,6 +487,9 @@ int search_concurrent(fst_ctx *c, Problem P, const SearchArgs &SF, const SearchA
   }
   c->stats.fwd_levels = c->h_sc->gens;
   c->stats.bwd_levels = c->h_sc->gens2;
+  // launches that found work (both searches side by side from g0 on)
+  const int fl = (int)c->h_sc->gens - g0, bl = (int)c->h_sc->gens2;
+  c->gen_hint = fl > bl ? fl : bl;
   return FST_OK;
 }
 
@@ -810,29 +819,31 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   const unsigned long long nst = c->h_sc->total;
   if (nst > (unsigned long long)INT32_MAX) return FST_ERR_TOO_LARGE;
   const uint32_t nstates = (uint32_t)nst;
-  // the search lists are free now: the forward queue takes the key of
-  // every state, the backward queue the heavy states
+  // the search lists are free now: the forward queue takes the counts of
+  // 255 arcs or more, the backward queue the heavy states (id, key)
   FST_TRY(ensure(c, c->fq, ((size_t)nstates + 1) * 4));
-  FST_TRY(ensure(c, c->bq, ((size_t)nstates + 1) * 4));
-  uint32_t *key_of = as<uint32_t>(c->fq);
-  uint32_t *heavy = as<uint32_t>(c->bq);
+  FST_TRY(ensure(c, c->bq, ((size_t)nstates + 1) * 8));
+  uint32_t *cnt32 = as<uint32_t>(c->fq);
+  uint2 *heavy = as<uint2>(c->bq);
   const Problem &P = c->P;
-  HIP_TRY(launch_key_of_id(P.trim, wbase, nwords, key_of, s));
-  FST_TRY(ensure(c, c->cnt, ((size_t)nstates + 1) * 4));
-  FST_TRY(ensure(c, c->btot, (OUT_CHUNKS + 1) * 4));
-  uint32_t *cnt = as<uint32_t>(c->cnt), *btot = as<uint32_t>(c->btot);
-  const size_t per = out_chunk(nstates);
+  const size_t nchunks = out_chunks(nwords);
+  FST_TRY(ensure(c, c->cnt, (size_t)nstates + 1));
+  FST_TRY(ensure(c, c->btot, (nchunks + 1) * 4));
+  FST_TRY(ensure(c, c->scan_tmp, scan_temp_bytes(nchunks + 1)));
+  uint8_t *cnt8 = as<uint8_t>(c->cnt);
+  uint32_t *btot = as<uint32_t>(c->btot);
   HIP_TRY(hipMemsetAsync(&d_sc->heavy, 0, sizeof(uint32_t), s));
   HIP_TRY(hipMemsetAsync(&d_sc->total, 0, sizeof(unsigned long long), s));
   const KernelTimer tc = timer(c, FST_KERNEL_COUNT);
   tc.begin(s);
-  HIP_TRY(launch_count(P, key_of, nstates, per, cnt, btot, heavy, d_sc, s));
-  HIP_TRY(launch_count_heavy(P, key_of, heavy, &d_sc->heavy, per, cnt, btot, s));
+  if (nstates) {
+    HIP_TRY(launch_count(P, nwords, cnt8, cnt32, btot, heavy, d_sc, s));
+    HIP_TRY(launch_count_heavy(P, heavy, &d_sc->heavy, cnt8, cnt32, btot, s));
+  }
   tc.end(s);
   // exclusive arc offset of every chunk; the total is E_C
   if (nstates)
-    HIP_TRY(scan_u32(btot, btot, out_chunks(nstates, per), false, &d_sc->total, c->scan_tmp.p,
-                     s));
+    HIP_TRY(scan_u32(btot, btot, nchunks, false, &d_sc->total, c->scan_tmp.p, s));
   phase_end(c, PH_COUNT, s);
   FST_TRY(readback(c, s));
   const unsigned long long narcs = c->h_sc->total;
@@ -840,7 +851,7 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
   FST_TRY(add_time(c, FST_KERNEL_COUNT, nstates ? 2 : 1));
 
   c->nstates = nstates;
-  c->out_per = per;
+  c->out_words = nwords;
   c->narcs = (uint32_t)narcs;
   c->nheavy = c->h_sc->heavy;
   c->stats.accessible = (int64_t)c->h_sc->naccessible;
@@ -898,13 +909,15 @@ int view3(fst_ctx *c, const DevGraph &g, int side, bool presorted, uint32_t maxl
   return FST_OK;
 }
 
-// Levels of a three-input search in batches (4, 16, 32, 64, 64, ...) with
-// one read-back after each batch; *done tells whether it ended (false: a
-// capacity was exceeded).
+// Levels of a three-input search in batches with one read-back after each
+// batch; *done tells whether it ended (false: a capacity was exceeded).
+// The first batch is as many levels as the last search in this direction
+// took (at least 4), then 16, 32, 64, 64, ...
 int levels3(fst_ctx *c, const Problem3 &P, const Search3 &S, bool forward, uint32_t grow_at,
             bool *done, hipStream_t s) {
   const KernelTimer t = timer(c, FST_KERNEL_SEARCH3);
-  int g = 0, batch = 4;
+  int &hint = c->lv3_hint[forward ? 1 : 0];
+  int g = 0, batch = hint > 4 ? (hint < 256 ? hint : 256) : 4;
   *done = false;
   for (;;) {
     t.begin(s);
@@ -920,8 +933,9 @@ int levels3(fst_ctx *c, const Problem3 &P, const Search3 &S, bool forward, uint3
     // walks that reach a heavy key leave it as a chunk of the next level:
     // a level can hold chunks and no frontier
     if (nx.fcount == 0 && nx.ccount == 0) break;
-    batch = batch == 4 ? 16 : (batch < 64 ? 2 * batch : 64);
+    batch = batch < 16 ? 16 : (batch < 64 ? 2 * batch : 64);
   }
+  hint = (int)c->h_s3->levels;
   *done = true;
   return FST_OK;
 }
@@ -1231,8 +1245,8 @@ int batch_impl(fst_ctx *c, const fst_graph *A, int32_t n, const fst_graph *B, hi
   long long *dq = as<long long>(c->u_items), *dout = dq + (n + 1);
   HIP_TRY(hipMemcpyAsync(dq, h.data(), ((size_t)n + 1) * sizeof(long long),
                          hipMemcpyHostToDevice, s));
-  HIP_TRY(launch_item_ranges(c->P, c->nkeys, n, dq, as<uint32_t>(c->cnt), as<uint32_t>(c->btot),
-                             c->out_per, c->nstates, c->narcs, dout, s));
+  HIP_TRY(launch_item_ranges(c->P, c->nkeys, n, dq, as<uint8_t>(c->cnt), as<uint32_t>(c->fq),
+                             as<uint32_t>(c->btot), c->nstates, c->narcs, dout, s));
   HIP_TRY(hipMemcpyAsync(h.data() + (n + 1), dout, 2 * ((size_t)n + 1) * sizeof(long long),
                          hipMemcpyDeviceToHost, s));
   HIP_TRY(hipStreamSynchronize(s));
@@ -1470,9 +1484,11 @@ int fst_compose_fill(fst_ctx *c, const fst_graph_out *C, void *stream) {
   phase_begin(c, PH_FILL, s);
   const KernelTimer tf = c->timed_run ? timer(c, FST_KERNEL_FILL) : KernelTimer{};
   tf.begin(s);
-  hipError_t e = launch_fill(c->P, as<uint32_t>(c->fq), c->nstates, c->out_per,
-                             as<uint32_t>(c->cnt), as<uint32_t>(c->btot), as<uint32_t>(c->bq),
-                             c->nheavy, c->narcs, O, s);
+  // with no states the fill only writes arc_offset[0] (and reads no bitmap)
+  hipError_t e = launch_fill(c->P, c->nstates ? c->out_words : 0, as<uint8_t>(c->cnt),
+                             as<uint32_t>(c->fq),
+                             as<uint32_t>(c->btot), as<uint2>(c->bq), c->nheavy, c->nstates,
+                             c->narcs, O, s);
   tf.end(s);
   // one launch: offsets, flags and arcs of every state
   c->klaunches[FST_KERNEL_FILL] = c->timed_run ? 1 : 0;

@@ -1375,39 +1375,74 @@ __global__ __launch_bounds__(NT) void k_trim(Problem P, uint32_t VA, uint32_t nt
   }
 }
 
-// The chunk of `per` items of this wavefront: [begin, end).
-__device__ __forceinline__ void wave_chunk(ull n, ull per, ull &chunk, ull &begin, ull &end,
-                                           unsigned block = blockIdx.x) {
-  chunk = (ull)block * NWAVES + threadIdx.x / WAVE;
-  begin = chunk * per;
-  end = begin + per < n ? begin + per : n;
-  if (begin > end) begin = end;
+// The trim words of output chunk c (trim words [OUT_WORDS c, OUT_WORDS c +
+// OUT_WORDS), one per lane): lane l holds its word and the number of keys
+// in the chunk's words before it; every lane holds the chunk's key count.  State ids are ranks in key order, so the chunk's
+// i-th key is state wbase[first word] + i.
+struct TrimChunk {
+  uint32_t word, before, count;
+  ull w0;  // the chunk's first word
+};
+
+__device__ __forceinline__ TrimChunk trim_chunk(const Problem &P, ull chunk, ull nwords) {
+  static_assert(OUT_WORDS <= WAVE && (OUT_WORDS & (OUT_WORDS - 1)) == 0,
+                "at most one trim word per lane, a power of two");
+  TrimChunk t;
+  t.w0 = chunk * OUT_WORDS;
+  const ull w = t.w0 + __lane_id();
+  t.word = __lane_id() < OUT_WORDS && w < nwords ? P.trim[w] : 0u;
+  const uint32_t p = (uint32_t)__popc(t.word);
+  const uint32_t incl = wave_incl_scan(p);
+  t.before = incl - p;
+  t.count = __shfl(incl, WAVE - 1, WAVE);
+  return t;
 }
 
-// key_of[id] = the id-th trim key.  One workgroup per NT bitmap words (one
-// word per thread): a workgroup scan of the words' popcounts places each
-// word's keys in an LDS list, which the workgroup then writes out
-// contiguously from the prefix of its first word.
-__global__ __launch_bounds__(NT) void k_key_of_id(const uint32_t *__restrict__ bm,
-                                                  const uint32_t *__restrict__ wbase,
-                                                  ull nwords, uint32_t *__restrict__ key_of) {
-  __shared__ uint32_t s_keys[NT * 32];
-  __shared__ uint32_t s_w[NWAVES];
-  for (ull w0 = (ull)blockIdx.x * NT; w0 < nwords; w0 += (ull)gridDim.x * NT) {
-    const ull w = w0 + threadIdx.x;
-    uint32_t m = w < nwords ? bm[w] : 0u;
-    const uint32_t base = wbase[w0];
-    uint32_t total;
-    uint32_t o = block_excl_scan<uint32_t>((uint32_t)__popc(m), s_w, total);
-    while (m) {
-      const uint32_t b = (uint32_t)__ffs(m) - 1u;
-      s_keys[o++] = (uint32_t)(w * 32u) + b;
-      m &= m - 1u;
-    }
-    __syncthreads();
-    for (uint32_t i = threadIdx.x; i < total; i += NT) key_of[base + i] = s_keys[i];
-    __syncthreads();  // the list is read before the next chunk overwrites it
+// The chunk's trim keys in order, as offsets from its first bit (< 2^16),
+// in the wavefront's LDS list: each lane writes its word's keys from its
+// prefix on.  The list is read by other lanes of the same wavefront only
+// (LDS operations of a wavefront complete in order).
+__device__ __forceinline__ void trim_expand(const TrimChunk &t, uint16_t *list) {
+  static_assert(OUT_WORDS * 32 <= 65536, "offsets fit 16 bits");
+  uint32_t m = t.word, o = t.before;
+  const uint32_t base = __lane_id() * 32u;
+  while (m) {
+    list[o++] = (uint16_t)(base + (uint32_t)__ffs(m) - 1u);
+    m &= m - 1u;
   }
+  __builtin_amdgcn_wave_barrier();
+}
+
+__device__ __forceinline__ uint32_t trim_key_at(const TrimChunk &t, const uint16_t *list,
+                                                uint32_t i) {
+  return i < t.count ? (uint32_t)(t.w0 * 32u) + list[i] : 0u;
+}
+
+// Kept-arc count of state id: one byte per state; 255 says the count is in
+// cnt32 (only such states have an entry there).
+__device__ __forceinline__ uint32_t count_of(const uint8_t *__restrict__ cnt8,
+                                             const uint32_t *__restrict__ cnt32, ull id) {
+  const uint32_t c = cnt8[id];
+  return c == 255u ? cnt32[id] : c;
+}
+
+__device__ __forceinline__ void put_count(uint8_t *__restrict__ cnt8, uint32_t *__restrict__ cnt32,
+                                          ull id, uint32_t c) {
+  cnt8[id] = (uint8_t)(c < 255u ? c : 255u);
+  if (c >= 255u) cnt32[id] = c;
+}
+
+// Arcs of the states of chunk c before state `id` (a state of that chunk,
+// or the first state after it): summed by the whole workgroup, valid in
+// thread 0.
+__device__ __forceinline__ uint32_t chunk_arcs_before(const Problem &P, ull chunk, ull id,
+                                                      const uint8_t *__restrict__ cnt8,
+                                                      const uint32_t *__restrict__ cnt32,
+                                                      uint32_t *s_w) {
+  const ull first = P.wbase[chunk * OUT_WORDS];
+  uint32_t part = 0;
+  for (ull j = first + threadIdx.x; j < id; j += NT) part += count_of(cnt8, cnt32, j);
+  return block_sum(part, s_w);
 }
 
 __device__ __forceinline__ uint32_t new_id(const Problem &P, uint32_t k) {
@@ -1686,23 +1721,30 @@ __device__ uint32_t heavy_state(const Problem &P, uint32_t id, uint32_t key, uin
   return run;
 }
 
-__global__ __launch_bounds__(NT) void k_count(Problem P, const uint32_t *__restrict__ key_of,
-                                              uint32_t n, ull per, uint32_t *__restrict__ cnt,
+// Kept-arc counts, one output chunk per wavefront: put_count for light
+// states (0 for now for heavy ones, which are listed with their keys), and
+// btot[chunk] = the chunk's light total.
+__global__ __launch_bounds__(NT) void k_count(Problem P, ull nwords, ull nchunks,
+                                              uint8_t *__restrict__ cnt8,
+                                              uint32_t *__restrict__ cnt32,
                                               uint32_t *__restrict__ btot,
-                                              uint32_t *__restrict__ heavy, Scalars *sc,
-                                              uint32_t nchunks) {
-  ull chunk, begin, end;
-  wave_chunk(n, per, chunk, begin, end);
+                                              uint2 *__restrict__ heavy, Scalars *sc) {
+  const ull chunk = (ull)blockIdx.x * NWAVES + threadIdx.x / WAVE;
+  if (chunk >= nchunks) return;  // the whole wavefront
+  __shared__ uint16_t s_keys[NWAVES][OUT_WORDS * 32];
+  uint16_t *list = s_keys[threadIdx.x / WAVE];
+  const TrimChunk t = trim_chunk(P, chunk, nwords);
+  const uint32_t first = t.count ? P.wbase[t.w0] : 0u;
+  trim_expand(t, list);
   uint32_t sum = 0;
-  // each iteration loads the next one's key (one round trip fewer on the
-  // chain of dependent loads)
-  uint32_t k_next = begin + __lane_id() < end ? key_of[begin + __lane_id()] : 0u;
-  for (ull base = begin; base < end; base += WAVE) {
-    const ull id = base + __lane_id();
-    const uint32_t key = k_next;
-    if (id + WAVE < end) k_next = key_of[id + WAVE];
+  // each round reads the next round's keys before its own loads
+  uint32_t key_next = trim_key_at(t, list, __lane_id());
+  for (uint32_t i0 = 0; i0 < t.count; i0 += WAVE) {
+    const uint32_t i = i0 + __lane_id();
+    const uint32_t key = key_next;
+    key_next = trim_key_at(t, list, i + WAVE);
     bool hv = false;
-    if (id < end) {
+    if (i < t.count) {
       const Fwd s = fwd_info(P, key);
       uint32_t c = 0;
       if (out_units(s) > LIGHT_UNITS) {
@@ -1712,7 +1754,7 @@ __global__ __launch_bounds__(NT) void k_count(Problem P, const uint32_t *__restr
           c += test_bit(P.trim, d) ? 1u : 0u;
         });
       }
-      cnt[id] = c;
+      put_count(cnt8, cnt32, (ull)first + i, c);
       sum += c;
     }
     unsigned long long m = __ballot(hv);
@@ -1721,56 +1763,71 @@ __global__ __launch_bounds__(NT) void k_count(Problem P, const uint32_t *__restr
       uint32_t hb = 0;
       if ((int)__lane_id() == leader) hb = atomicAdd(&sc->heavy, (uint32_t)__popcll(m));
       hb = __shfl(hb, leader, WAVE);
-      if (hv) heavy[hb + __popcll(m & __lanemask_lt())] = (uint32_t)id;
+      if (hv) heavy[hb + __popcll(m & __lanemask_lt())] = make_uint2(first + i, key);
     }
   }
   sum = wave_sum(sum);
-  if (__lane_id() == 0 && chunk < nchunks) btot[chunk] = sum;
+  if (__lane_id() == 0) btot[chunk] = sum;
 }
 
-__global__ __launch_bounds__(NT) void k_count_heavy(Problem P, const uint32_t *__restrict__ key_of,
-                                                    const uint32_t *__restrict__ heavy,
-                                                    const uint32_t *__restrict__ nheavy_p, ull per,
-                                                    uint32_t *__restrict__ cnt,
+// Counts of the heavy states (one workgroup each), added to their chunk's
+// btot.
+__global__ __launch_bounds__(NT) void k_count_heavy(Problem P, const uint2 *__restrict__ heavy,
+                                                    const uint32_t *__restrict__ nheavy_p,
+                                                    uint8_t *__restrict__ cnt8,
+                                                    uint32_t *__restrict__ cnt32,
                                                     uint32_t *__restrict__ btot) {
   __shared__ uint32_t s_w[NWAVES];
   const uint32_t nheavy = *nheavy_p;
   OutGraph none = {};
   for (uint32_t h = blockIdx.x; h < nheavy; h += gridDim.x) {
-    const uint32_t id = heavy[h];
-    uint32_t c = heavy_state<false>(P, id, key_of[id], 0, none, s_w);
+    const uint2 hk = heavy[h];
+    uint32_t c = heavy_state<false>(P, hk.x, hk.y, 0, none, s_w);
     if (threadIdx.x == 0) {
-      cnt[id] = c;
-      atomicAdd(btot + id / per, c);
+      put_count(cnt8, cnt32, hk.x, c);
+      atomicAdd(btot + (hk.y >> 5) / OUT_WORDS, c);
     }
   }
 }
 
-// One thread per state of C, one contiguous chunk per wavefront: the state's
-// arc offset (chunk base + wavefront scan of the counts), flags and key, and
-// the arcs of a light state (heavy states are written by the workgroups of
-// k_fill set aside for them).
-__device__ __forceinline__ void fill_light(const Problem &P, const uint32_t *__restrict__ key_of,
-                                           uint32_t n, ull per, const uint32_t *__restrict__ cnt,
+// One thread per state of C, one output chunk per wavefront: the state's
+// arc offset (chunk offset + wavefront scan of the counts), flags and key,
+// and the arcs of a light state (heavy states are written by the
+// workgroups of k_fill set aside for them).
+__device__ __forceinline__ void fill_light(const Problem &P, ull nwords, ull nchunks,
+                                           const uint8_t *__restrict__ cnt8,
+                                           const uint32_t *__restrict__ cnt32,
                                            const uint32_t *__restrict__ btot,
                                            const OutGraph &O, unsigned block) {
-  ull chunk, begin, end;
-  wave_chunk(n, per, chunk, begin, end, block);
-  uint32_t run = begin < end ? btot[chunk] : 0u;
-  // each iteration loads the next one's count and key (one round trip
-  // fewer on the chain of dependent loads)
-  uint32_t c_next = 0, k_next = 0;
-  if (begin + __lane_id() < end) {
-    c_next = cnt[begin + __lane_id()];
-    k_next = key_of[begin + __lane_id()];
+  const ull chunk = (ull)block * NWAVES + threadIdx.x / WAVE;
+  if (chunk >= nchunks) return;  // the whole wavefront
+  __shared__ uint16_t s_keys[NWAVES][OUT_WORDS * 32];
+  uint16_t *list = s_keys[threadIdx.x / WAVE];
+  const TrimChunk t = trim_chunk(P, chunk, nwords);
+  if (!t.count) return;
+  const uint32_t first = P.wbase[t.w0], end = first + t.count;
+  uint32_t run = btot[chunk];
+  trim_expand(t, list);
+  // rounds cover ids [64 k, 64 k + 64), so that the state outputs of a
+  // round (offsets, flags) fill whole aligned segments; lanes outside the
+  // chunk are idle
+  const uint32_t a0 = first & ~(uint32_t)(WAVE - 1);
+  uint32_t c_next = 0, key_next = 0;
+  {
+    const uint32_t id = a0 + __lane_id();
+    if (id >= first && id < end) {
+      c_next = count_of(cnt8, cnt32, id);
+      key_next = trim_key_at(t, list, id - first);
+    }
   }
-  for (ull base = begin; base < end; base += WAVE) {
-    const ull id = base + __lane_id();
-    const bool valid = id < end;
-    const uint32_t c = c_next, key = k_next;
-    if (id + WAVE < end) {
-      c_next = cnt[id + WAVE];
-      k_next = key_of[id + WAVE];
+  for (uint32_t g0 = a0; g0 < end; g0 += WAVE) {
+    const uint32_t id = g0 + __lane_id();
+    const bool valid = id >= first && id < end;
+    const uint32_t c = c_next, key = key_next;
+    const uint32_t nid = id + WAVE;
+    if (nid >= first && nid < end) {
+      c_next = count_of(cnt8, cnt32, nid);
+      key_next = trim_key_at(t, list, nid - first);
     }
     const uint32_t incl = wave_incl_scan(c);
     uint32_t pos = run + incl - c;
@@ -1784,13 +1841,12 @@ __device__ __forceinline__ void fill_light(const Problem &P, const uint32_t *__r
     if (O.key_b) out_store(O.key_b + id, (int32_t)s.qb);
     if (O.key_f) out_store(O.key_f + id, (uint8_t)s.f);
     if (out_units(s) > LIGHT_UNITS) continue;
-    const uint32_t sid = (uint32_t)id;
     const Move m = single_move(P, s);
     if (m.fast) {
-      if (m.has) put_move(O, P, pos, sid, m);
+      if (m.has) put_move(O, P, pos, id, m);
     } else {
       enum_general(P, s, [&](uint32_t d, int32_t il, int32_t ol, float w, int32_t pa, int32_t pb) {
-        if (put_arc(O, P, pos, sid, d, il, ol, w, pa, pb)) ++pos;
+        if (put_arc(O, P, pos, id, d, il, ol, w, pa, pb)) ++pos;
       });
     }
   }
@@ -1801,30 +1857,29 @@ __device__ __forceinline__ void fill_light(const Problem &P, const uint32_t *__r
 // light chunks, so the heavy states' workgroup loops run under the light
 // work.  A heavy state's first arc position is its chunk's offset plus the
 // counts of the chunk's earlier states, summed by its workgroup.
-__global__ __launch_bounds__(NT) void k_fill(Problem P, const uint32_t *__restrict__ key_of,
-                                             uint32_t n, ull per, const uint32_t *__restrict__ cnt,
-                                             const uint32_t *__restrict__ btot, uint32_t narcs,
-                                             const uint32_t *__restrict__ heavy, uint32_t nheavy,
-                                             unsigned hb, OutGraph O) {
+__global__ __launch_bounds__(NT) void k_fill(Problem P, ull nwords, ull nchunks,
+                                             const uint8_t *__restrict__ cnt8,
+                                             const uint32_t *__restrict__ cnt32,
+                                             const uint32_t *__restrict__ btot, uint32_t nstates,
+                                             uint32_t narcs, const uint2 *__restrict__ heavy,
+                                             uint32_t nheavy, unsigned hb, OutGraph O) {
   if (blockIdx.x < hb) {
     __shared__ uint32_t s_w[NWAVES];
     __shared__ uint32_t s_pos;
     for (uint32_t h = blockIdx.x; h < nheavy; h += hb) {
-      const uint32_t id = heavy[h];
-      const ull chunk = id / per;
-      uint32_t part = 0;
-      for (ull j = chunk * per + threadIdx.x; j < id; j += NT) part += cnt[j];
-      const uint32_t before = block_sum(part, s_w);  // valid in thread 0
+      const uint2 hk = heavy[h];
+      const ull chunk = (hk.y >> 5) / OUT_WORDS;
+      const uint32_t before = chunk_arcs_before(P, chunk, hk.x, cnt8, cnt32, s_w);
       if (threadIdx.x == 0) s_pos = btot[chunk] + before;
       __syncthreads();
-      heavy_state<true>(P, id, key_of[id], s_pos, O, s_w);
+      heavy_state<true>(P, hk.x, hk.y, s_pos, O, s_w);
       __syncthreads();  // s_pos and s_w are reused by the next heavy state
     }
     return;
   }
   const unsigned block = blockIdx.x - hb;
-  fill_light(P, key_of, n, per, cnt, btot, O, block);
-  if (block == gridDim.x - hb - 1 && threadIdx.x == 0) O.arc_offset[n] = (int32_t)narcs;
+  fill_light(P, nwords, nchunks, cnt8, cnt32, btot, O, block);
+  if (block == gridDim.x - hb - 1 && threadIdx.x == 0) O.arc_offset[nstates] = (int32_t)narcs;
 }
 
 // ---------------------------------------------------------------------------
@@ -1855,22 +1910,23 @@ __global__ __launch_bounds__(NT) void k_union_copy(DevGraph a, long long vbase, 
 // the item), for i <= n.
 __global__ __launch_bounds__(NT) void k_item_ranges(Problem P, ull nkeys, int32_t n,
                                                     const long long *__restrict__ qa_base,
-                                                    const uint32_t *__restrict__ cnt,
-                                                    const uint32_t *__restrict__ btot, ull per,
+                                                    const uint8_t *__restrict__ cnt8,
+                                                    const uint32_t *__restrict__ cnt32,
+                                                    const uint32_t *__restrict__ btot,
                                                     uint32_t nstates, uint32_t narcs,
                                                     long long *__restrict__ out) {
-  __shared__ ull s_w[NWAVES];
+  __shared__ uint32_t s_w[NWAVES];
   for (int i = blockIdx.x; i <= n; i += gridDim.x) {
     const ull K = (ull)qa_base[i] << (P.shiftB + 1);
     const uint32_t st = K >= nkeys ? nstates : new_id(P, (uint32_t)K);
-    ull part = 0;
-    const ull c = st / per;
-    if (st < nstates)
-      for (ull j = c * per + threadIdx.x; j < st; j += NT) part += cnt[j];
-    const ull before = block_sum(part, s_w);  // valid in thread 0
+    // the item's first state is the first trim key >= K: a state of K's
+    // chunk, or the first state after it
+    const ull chunk = (K >> 5) / OUT_WORDS;
+    uint32_t before = 0;
+    if (st < nstates) before = chunk_arcs_before(P, chunk, st, cnt8, cnt32, s_w);
     if (threadIdx.x == 0) {
       out[i] = st;
-      out[n + 1 + i] = st < nstates ? (long long)(btot[c] + before) : (long long)narcs;
+      out[n + 1 + i] = st < nstates ? (long long)(btot[chunk] + before) : (long long)narcs;
     }
     __syncthreads();  // s_w is reused by the next item
   }
@@ -2032,35 +2088,30 @@ hipError_t launch_trim(const Problem &P, uint32_t VA, uint32_t *trim, uint32_t *
   return hipGetLastError();
 }
 
-hipError_t launch_key_of_id(const uint32_t *bm, const uint32_t *wbase, size_t nwords,
-                            uint32_t *key_of, hipStream_t s) {
-  if (!nwords) return hipSuccess;
-  k_key_of_id<<<grid_for(nwords, 16384), NT, 0, s>>>(bm, wbase, nwords, key_of);
+hipError_t launch_count(const Problem &P, size_t nwords, uint8_t *cnt8, uint32_t *cnt32,
+                        uint32_t *btot, uint2 *heavy, Scalars *sc, hipStream_t s) {
+  const size_t nchunks = out_chunks(nwords);
+  if (!nchunks) return hipSuccess;
+  if (!P.trim || !P.wbase) return hipErrorInvalidValue;  // no trim bitmap to expand
+  k_count<<<out_grid(nchunks), NT, 0, s>>>(P, nwords, nchunks, cnt8, cnt32, btot, heavy, sc);
   return hipGetLastError();
 }
 
-hipError_t launch_count(const Problem &P, const uint32_t *key_of, uint32_t nstates, size_t per,
-                        uint32_t *cnt, uint32_t *btot, uint32_t *heavy, Scalars *sc,
-                        hipStream_t s) {
-  if (!nstates) return hipSuccess;
-  k_count<<<out_grid(nstates, per), NT, 0, s>>>(P, key_of, nstates, per, cnt, btot, heavy, sc,
-                                                out_chunks(nstates, per));
+hipError_t launch_count_heavy(const Problem &P, const uint2 *heavy, const uint32_t *nheavy_dev,
+                              uint8_t *cnt8, uint32_t *cnt32, uint32_t *btot, hipStream_t s) {
+  k_count_heavy<<<1024, NT, 0, s>>>(P, heavy, nheavy_dev, cnt8, cnt32, btot);
   return hipGetLastError();
 }
 
-hipError_t launch_count_heavy(const Problem &P, const uint32_t *key_of, const uint32_t *heavy,
-                              const uint32_t *nheavy_dev, size_t per, uint32_t *cnt,
-                              uint32_t *btot, hipStream_t s) {
-  k_count_heavy<<<1024, NT, 0, s>>>(P, key_of, heavy, nheavy_dev, per, cnt, btot);
-  return hipGetLastError();
-}
-
-hipError_t launch_fill(const Problem &P, const uint32_t *key_of, uint32_t nstates, size_t per,
-                       const uint32_t *cnt, const uint32_t *btot, const uint32_t *heavy,
-                       uint32_t nheavy, uint32_t narcs, const OutGraph &O, hipStream_t s) {
+hipError_t launch_fill(const Problem &P, size_t nwords, const uint8_t *cnt8,
+                       const uint32_t *cnt32, const uint32_t *btot, const uint2 *heavy,
+                       uint32_t nheavy, uint32_t nstates, uint32_t narcs, const OutGraph &O,
+                       hipStream_t s) {
+  const size_t nchunks = out_chunks(nwords);
+  if (nchunks && (!P.trim || !P.wbase)) return hipErrorInvalidValue;  // no trim bitmap
   const unsigned hb = nheavy < 4096 ? nheavy : 4096;
-  k_fill<<<hb + out_grid(nstates, per), NT, 0, s>>>(P, key_of, nstates, per, cnt, btot, narcs,
-                                                    heavy, nheavy, hb, O);
+  k_fill<<<hb + out_grid(nchunks), NT, 0, s>>>(P, nwords, nchunks, cnt8, cnt32, btot, nstates,
+                                               narcs, heavy, nheavy, hb, O);
   return hipGetLastError();
 }
 
@@ -2072,11 +2123,11 @@ hipError_t launch_union_copy(const DevGraph &a, long long vbase, long long ebase
 }
 
 hipError_t launch_item_ranges(const Problem &P, unsigned long long nkeys, int32_t n,
-                              const long long *qa_base, const uint32_t *cnt,
-                              const uint32_t *btot, size_t per, uint32_t nstates,
+                              const long long *qa_base, const uint8_t *cnt8,
+                              const uint32_t *cnt32, const uint32_t *btot, uint32_t nstates,
                               uint32_t narcs, long long *out, hipStream_t s) {
   const unsigned g = (unsigned)(n + 1 < 4096 ? n + 1 : 4096);
-  k_item_ranges<<<g, NT, 0, s>>>(P, nkeys, n, qa_base, cnt, btot, per, nstates, narcs, out);
+  k_item_ranges<<<g, NT, 0, s>>>(P, nkeys, n, qa_base, cnt8, cnt32, btot, nstates, narcs, out);
   return hipGetLastError();
 }
 

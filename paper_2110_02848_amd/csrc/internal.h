@@ -18,22 +18,15 @@ constexpr uint32_t LIGHT_SEARCH = 64;  // search: a key with more units is split
 constexpr int CHAIN_MAX = 64;          // search: default depth-first budget per thread
 constexpr uint32_t NO_KEY = 0xFFFFFFFFu;
 
-// The output passes give every wavefront one contiguous chunk of states (a
-// multiple of WAVE; at most OUT_CHUNKS chunks), so the arcs a wavefront
+// The output passes give every wavefront one chunk of OUT_WORDS consecutive
+// trim words (its states are consecutive ids), so the arcs a wavefront
 // writes are contiguous and its offsets need only wavefront scans.  Every
 // workgroup covers NWAVES consecutive chunks.
-constexpr size_t OUT_CHUNKS = 262144;
-inline size_t out_chunk(size_t n) {
-  size_t per = (n + OUT_CHUNKS - 1) / OUT_CHUNKS;
-  per = (per + WAVE - 1) / WAVE * WAVE;
-  return per ? per : (size_t)WAVE;
-}
-inline unsigned out_chunks(size_t n, size_t per) {
-  const size_t g = (n + per - 1) / per;
+constexpr size_t OUT_WORDS = 16;
+inline size_t out_chunks(size_t nwords) { return (nwords + OUT_WORDS - 1) / OUT_WORDS; }
+inline unsigned out_grid(size_t nchunks) {
+  const size_t g = (nchunks + NWAVES - 1) / NWAVES;
   return (unsigned)(g ? g : 1);
-}
-inline unsigned out_grid(size_t n, size_t per) {
-  return (out_chunks(n, per) + NWAVES - 1) / NWAVES;
 }
 
 // ---------------------------------------------------------------------------
@@ -510,22 +503,20 @@ hipError_t launch_popcount(const uint32_t *bm, size_t nwords, unsigned long long
 // Needs shiftB >= 4 (a trim word then holds keys of one A state).
 hipError_t launch_trim(const Problem &P, uint32_t VA, uint32_t *trim, uint32_t *cnt,
                        hipStream_t s);
-hipError_t launch_key_of_id(const uint32_t *bm, const uint32_t *wbase, size_t nwords,
-                            uint32_t *key_of, hipStream_t s);
-// Kept-arc count of every state of C (chunks of `per` states per
-// wavefront): cnt[id] for light states, heavy state ids listed in `heavy`
-// (count in Scalars::heavy), btot[chunk] = the chunk's light total.
-hipError_t launch_count(const Problem &P, const uint32_t *key_of, uint32_t nstates, size_t per,
-                        uint32_t *cnt, uint32_t *btot, uint32_t *heavy, Scalars *sc,
-                        hipStream_t s);
-// Counts of the heavy states (cnt[id], added to their chunk's btot).
-hipError_t launch_count_heavy(const Problem &P, const uint32_t *key_of, const uint32_t *heavy,
-                              const uint32_t *nheavy_dev, size_t per, uint32_t *cnt,
-                              uint32_t *btot, hipStream_t s);
+// Kept-arc count of every state of C, one chunk of OUT_WORDS trim words per
+// wavefront: cnt8[id] (255: the count is in cnt32[id]) for light states,
+// heavy states listed in `heavy` as (id, key) (their number in
+// Scalars::heavy), btot[chunk] = the chunk's light total.
+hipError_t launch_count(const Problem &P, size_t nwords, uint8_t *cnt8, uint32_t *cnt32,
+                        uint32_t *btot, uint2 *heavy, Scalars *sc, hipStream_t s);
+// Counts of the heavy states (cnt8 / cnt32, added to their chunk's btot).
+hipError_t launch_count_heavy(const Problem &P, const uint2 *heavy, const uint32_t *nheavy_dev,
+                              uint8_t *cnt8, uint32_t *cnt32, uint32_t *btot, hipStream_t s);
 // Write C: btot holds the exclusive arc offset of every chunk.
-hipError_t launch_fill(const Problem &P, const uint32_t *key_of, uint32_t nstates, size_t per,
-                       const uint32_t *cnt, const uint32_t *btot, const uint32_t *heavy,
-                       uint32_t nheavy, uint32_t narcs, const OutGraph &O, hipStream_t s);
+hipError_t launch_fill(const Problem &P, size_t nwords, const uint8_t *cnt8,
+                       const uint32_t *cnt32, const uint32_t *btot, const uint2 *heavy,
+                       uint32_t nheavy, uint32_t nstates, uint32_t narcs, const OutGraph &O,
+                       hipStream_t s);
 
 // Batches (compose.hip): copy item graph a into the union arrays at state
 // offset vbase and arc offset ebase (off, src, dst shifted); and, after a
@@ -534,8 +525,8 @@ hipError_t launch_fill(const Problem &P, const uint32_t *key_of, uint32_t nstate
 hipError_t launch_union_copy(const DevGraph &a, long long vbase, long long ebase, int32_t *off,
                              int32_t *src, int32_t *dst, hipStream_t s);
 hipError_t launch_item_ranges(const Problem &P, unsigned long long nkeys, int32_t n,
-                              const long long *qa_base, const uint32_t *cnt,
-                              const uint32_t *btot, size_t per, uint32_t nstates,
+                              const long long *qa_base, const uint8_t *cnt8,
+                              const uint32_t *cnt32, const uint32_t *btot, uint32_t nstates,
                               uint32_t narcs, long long *out, hipStream_t s);
 
 // Three-input launchers (compose3.hip).

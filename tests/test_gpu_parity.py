@@ -477,6 +477,10 @@ def test_rounding_cases(comp):
 def test_degenerate_inputs(comp):
     E0 = synth.empty_graph()
     A, B = synth.workload("random-64", 0)
+    # a composition with states first: the empty runs after it must not
+    # reuse its output layout (their fill writes arc_offset[0] only)
+    got, _ = check_pair(comp, A, B, "non-empty before empty inputs")
+    assert got["num_states"] > 0
     for X, Y, tag in ((E0, E0, "empty/empty"), (E0, A, "empty/A"), (A, E0, "A/empty")):
         got, _ = check_pair(comp, X, Y, tag)
         assert got["num_states"] == 0 and got["arc_offset"].tolist() == [0]
