@@ -356,7 +356,7 @@ FST_API int fst_segment_logsum(fst_ctx *ctx, const double *val, const uint8_t *f
  * sorting last.  Key bits: bits(V_A - 1) +
  * bits(V_B - 1) + bits(V_D - 1) + 2 <= 62 (each at least 1), else
  * FST_ERR_TOO_LARGE.  The workspace grows with the number of keys reached
- * (a hash set of 8 bytes per slot, at most 3/4 full, grown and searched
+ * (a hash set of 8 bytes per slot, at most half full, grown and searched
  * again when it fills). */
 typedef struct {
   int32_t *arc_offset;

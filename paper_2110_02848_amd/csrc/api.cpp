@@ -1031,8 +1031,9 @@ int compose3_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, const fst_
     HIP_TRY(launch3_starts(dA, dB, dD, lists, counts, s));
     HIP_TRY(launch3_seed(P, S, lists, counts, s));
     bool done = false;
-    // a table at most 3/4 full keeps probe sequences short
-    FST_TRY(levels3(c, P, S, true, (uint32_t)(H / 4 * 3), &done, s));
+    // a table at most half full keeps probe sequences short (most keys sit
+    // in the first group of four slots they probe)
+    FST_TRY(levels3(c, P, S, true, (uint32_t)(H / 2), &done, s));
     if (done) break;
     H *= 4;
   }
@@ -1056,8 +1057,8 @@ int compose3_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, const fst_
   FST_TRY(ensure(c, c->t_insrc, (narcs + 1) * 4));
   FST_TRY(ensure(c, c->t_coacc, (H / 32 + 1) * 4));
   FST_TRY(ensure(c, c->scan_tmp, scan_temp_bytes(H + 1)));
-  // chunks of LIGHT3 = 8 in-arcs: a key is chunked at most once
-  const unsigned long long ccap = H + narcs / 8 + 1;
+  // chunks of CHUNK3 in-arcs: a key is chunked at most once
+  const unsigned long long ccap = H + narcs / CHUNK3 + 1;
   if (ccap > 0xffffffffull) return FST_ERR_TOO_LARGE;
   FST_TRY(ensure(c, c->t_chunks, 2 * ccap * 8));
   uint32_t *inoff = as<uint32_t>(c->t_inoff);

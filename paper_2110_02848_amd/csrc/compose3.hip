@@ -30,7 +30,8 @@
 // A state has.
 //
 // The search goes level by level.  A thread takes a frontier key (or a
-// chunk of LIGHT3 units of a heavy key), expands it and goes on depth-first
+// chunk of CHUNK3 units of a key with more than WALK3), expands it and goes
+// on depth-first
 // with the first new key it reached (up to CHAIN3 keys), so a word of a
 // lexicon is one thread's walk; other new keys join the next frontier, and
 // heavy keys met on a walk are cut into chunks.  Every generated arc
@@ -52,7 +53,8 @@ typedef unsigned long long ull;
 
 constexpr ull EMPTY3 = ~0ull;
 constexpr uint32_t NO_SLOT = 0xFFFFFFFFu;
-constexpr uint32_t LIGHT3 = 8;    // work units one thread takes
+constexpr uint32_t LIGHT3 = 8;    // output: units of a state one thread writes
+constexpr uint32_t WALK3 = 8;     // search: units of a key a walk expands in place
 constexpr int PROBE_MAX = 4096;   // hash probes before the table counts as full
 constexpr uint32_t BF_EPS_EPS = 1u, BF_EPS_OUT = 2u;  // B state flags
 
@@ -97,25 +99,44 @@ __device__ __forceinline__ Key3 unpack3(const Problem3 &P, ull k) {
   return s;
 }
 
+// The set is probed in aligned groups of four slots (32 bytes, one cache
+// line sector), group after group from the key's hash: a key sits in the
+// first group of its sequence with a free slot when it was inserted.
+constexpr uint32_t HGROUP = 4;
+
+__device__ __forceinline__ void load_group(const Problem3 &P, uint32_t h, ull g[HGROUP]) {
+  const ulonglong2 *q = reinterpret_cast<const ulonglong2 *>(P.tab + h);
+  const ulonglong2 a = q[0], b = q[1];
+  g[0] = a.x;
+  g[1] = a.y;
+  g[2] = b.x;
+  g[3] = b.y;
+}
+
 // Slot of key k: inserted if absent (fresh), NO_SLOT (and the overflow
-// flag) if PROBE_MAX slots in a row are taken.  A plain load first: a slot
+// flag) if PROBE_MAX slots in a row are taken.  Plain loads first: a slot
 // never changes once set, so a stale EMPTY only sends the thread to the CAS.
 __device__ __forceinline__ uint32_t h_insert(const Problem3 &P, ull k, bool &fresh,
                                              uint32_t *overflow) {
-  uint32_t h = (uint32_t)mix64(k) & P.hmask;
+  uint32_t h = (uint32_t)mix64(k) & P.hmask & ~(HGROUP - 1u);
   fresh = false;
-  for (int p = 0; p < PROBE_MAX; ++p) {
-    const ull cur = P.tab[h];
-    if (cur == k) return h;
-    if (cur == EMPTY3) {
-      const ull old = atomicCAS(P.tab + h, EMPTY3, k);
+  for (int p = 0; p < PROBE_MAX; p += HGROUP) {
+    ull g[HGROUP];
+    load_group(P, h, g);
+#pragma unroll
+    for (uint32_t j = 0; j < HGROUP; ++j)
+      if (g[j] == k) return h + j;
+#pragma unroll
+    for (uint32_t j = 0; j < HGROUP; ++j) {
+      if (g[j] != EMPTY3) continue;
+      const ull old = atomicCAS(P.tab + h + j, EMPTY3, k);
       if (old == EMPTY3) {
         fresh = true;
-        return h;
+        return h + j;
       }
-      if (old == k) return h;
+      if (old == k) return h + j;
     }
-    h = (h + 1) & P.hmask;
+    h = (h + HGROUP) & P.hmask;
   }
   atomicOr(overflow, 1u);
   return NO_SLOT;
@@ -123,12 +144,18 @@ __device__ __forceinline__ uint32_t h_insert(const Problem3 &P, ull k, bool &fre
 
 // Slot of key k, or NO_SLOT if it is not in the set.
 __device__ __forceinline__ uint32_t h_find(const Problem3 &P, ull k) {
-  uint32_t h = (uint32_t)mix64(k) & P.hmask;
-  for (int p = 0; p < PROBE_MAX; ++p) {
-    const ull cur = P.tab[h];
-    if (cur == k) return h;
-    if (cur == EMPTY3) return NO_SLOT;
-    h = (h + 1) & P.hmask;
+  uint32_t h = (uint32_t)mix64(k) & P.hmask & ~(HGROUP - 1u);
+  for (int p = 0; p < PROBE_MAX; p += HGROUP) {
+    ull g[HGROUP];
+    load_group(P, h, g);
+    bool empty = false;
+#pragma unroll
+    for (uint32_t j = 0; j < HGROUP; ++j) {
+      if (g[j] == k) return h + j;
+      empty = empty || g[j] == EMPTY3;
+    }
+    if (empty) return NO_SLOT;
+    h = (h + HGROUP) & P.hmask;
   }
   return NO_SLOT;
 }
@@ -409,27 +436,27 @@ __device__ __forceinline__ void wave_add(uint32_t v, uint32_t *counter) {
   if (__lane_id() == 0 && v) atomicAdd(counter, v);
 }
 
-// Chunks of LIGHT3 units of a heavy key into level l's chunk list (counter
+// Chunks of CHUNK3 units of a heavy key into level l's chunk list (counter
 // lv = the level's ring slot).
 __device__ __forceinline__ void push_chunks(const Search3 &S, Lvl3 *lv, int l, uint32_t slot,
                                             uint32_t n) {
   uint2 *list = chunks_of(S, l);
-  const uint32_t nc = (n + LIGHT3 - 1) / LIGHT3;
+  const uint32_t nc = (n + CHUNK3 - 1) / CHUNK3;
   const uint32_t c0 = atomicAdd(&lv->ccount, nc);
   for (uint32_t c = 0; c < nc; ++c) {
-    if ((ull)c0 + c < S.ccap) list[c0 + c] = make_uint2(slot, c * LIGHT3);
+    if ((ull)c0 + c < S.ccap) list[c0 + c] = make_uint2(slot, c * CHUNK3);
     else atomicOr(&S.sc->overflow, 1u);
   }
 }
 
 // The moves of units [u0, u1) of the key in `slot`: every target is looked
 // up / inserted and every move recorded as an arc (source slot, target
-// slot).  The first new key becomes *cont when the thread may go on
-// depth-first (cont not null and none taken yet); other new keys join the
-// next frontier.
+// slot).  The first new key becomes *cont (its key *cont_key) when the
+// thread may go on depth-first (cont not null and none taken yet); other
+// new keys join the next frontier.
 __device__ __forceinline__ void expand_units(const Problem3 &P, const Search3 &S, uint32_t slot,
                                              const Units3 &u, uint32_t u0, uint32_t u1, Lvl3 *nx,
-                                             uint32_t nbase, uint32_t *cont) {
+                                             uint32_t nbase, uint32_t *cont, ull *cont_key) {
   for (uint32_t j = u0; j < u1; ++j)
     for_unit3(P, u, j, [&](ull t, int32_t, int32_t, float, int32_t, int32_t, int32_t) {
       bool fresh;
@@ -440,6 +467,7 @@ __device__ __forceinline__ void expand_units(const Problem3 &P, const Search3 &S
       bool push = fresh;
       if (fresh && cont && *cont == NO_SLOT) {
         *cont = ts;
+        *cont_key = t;
         push = false;
       }
       wave_append<uint32_t>(push, ts, S.F + nbase, (ull)S.fcap - nbase, &nx->fcount,
@@ -447,25 +475,28 @@ __device__ __forceinline__ void expand_units(const Problem3 &P, const Search3 &S
     });
 }
 
-// A thread's depth-first walk from the key in `slot`: a light key is
-// expanded at once and the walk goes on with the first new key it reached
-// (up to CHAIN3 keys); a heavy key is cut into chunks for the chunk list
-// `heavy_to`.  Every other new key joins the next frontier.  Returns the
-// number of keys the walk went on to.
+// A thread's depth-first walk from `key` (in `slot`): a key with at most
+// WALK3 units is expanded at once and the walk goes on with the first new
+// key it reached (up to CHAIN3 keys); a heavier key is cut into chunks for
+// the chunk list `heavy_to`.  Every other new key joins the next frontier.
+// Returns the number of keys the walk went on to.
 __device__ __forceinline__ uint32_t walk_fwd(const Problem3 &P, const Search3 &S, uint32_t slot,
-                                             Lvl3 *nx, uint32_t nbase, Lvl3 *heavy_to,
+                                             ull key, Lvl3 *nx, uint32_t nbase, Lvl3 *heavy_to,
                                              int heavy_l) {
   for (int depth = 0; depth < CHAIN3; ++depth) {
-    const Units3 u = units_of(P, P.tab[slot]);
+    const Units3 u = units_of(P, key);
     const uint32_t n = nunits(u);
-    if (n > LIGHT3) {
+    if (n > WALK3) {
       push_chunks(S, heavy_to, heavy_l, slot, n);
       return (uint32_t)depth;
     }
     uint32_t cont = NO_SLOT;
-    expand_units(P, S, slot, u, 0, n, nx, nbase, depth + 1 < CHAIN3 ? &cont : nullptr);
+    ull cont_key = 0;
+    expand_units(P, S, slot, u, 0, n, nx, nbase, depth + 1 < CHAIN3 ? &cont : nullptr,
+                 &cont_key);
     if (cont == NO_SLOT) return (uint32_t)depth;
     slot = cont;
+    key = cont_key;
   }
   return CHAIN3 - 1;
 }
@@ -487,12 +518,14 @@ __global__ __launch_bounds__(NT) void k3_fwd(Problem3 P, Search3 S, int l) {
   }
   uint32_t went = 0;
   if (!S.sc->overflow)
-    for (ull i = (ull)blockIdx.x * NT + threadIdx.x; i < cur.fcount; i += (ull)gridDim.x * NT)
-      went += walk_fwd(P, S, S.F[cur.fbase + i], nx, nbase, &S.ring[l % 3], l);
+    for (ull i = (ull)blockIdx.x * NT + threadIdx.x; i < cur.fcount; i += (ull)gridDim.x * NT) {
+      const uint32_t slot = S.F[cur.fbase + i];
+      went += walk_fwd(P, S, slot, P.tab[slot], nx, nbase, &S.ring[l % 3], l);
+    }
   wave_add(went, &S.sc->ncont);
 }
 
-// The chunks of level l: LIGHT3 units each, then a depth-first walk from
+// The chunks of level l: CHUNK3 units each, then a depth-first walk from
 // the first new key; heavy keys met on the walk go to the next level's
 // chunks.
 __global__ __launch_bounds__(NT) void k3_fwd_chunks(Problem3 P, Search3 S, int l) {
@@ -506,10 +539,11 @@ __global__ __launch_bounds__(NT) void k3_fwd_chunks(Problem3 P, Search3 S, int l
     const uint2 c = list[i];
     const Units3 u = units_of(P, P.tab[c.x]);
     const uint32_t n = nunits(u);
-    const uint32_t u1 = c.y + LIGHT3 < n ? c.y + LIGHT3 : n;
+    const uint32_t u1 = c.y + CHUNK3 < n ? c.y + CHUNK3 : n;
     uint32_t cont = NO_SLOT;
-    expand_units(P, S, c.x, u, c.y, u1, nx, nbase, &cont);
-    if (cont != NO_SLOT) went += 1 + walk_fwd(P, S, cont, nx, nbase, nx, l + 1);
+    ull cont_key = 0;
+    expand_units(P, S, c.x, u, c.y, u1, nx, nbase, &cont, &cont_key);
+    if (cont != NO_SLOT) went += 1 + walk_fwd(P, S, cont, cont_key, nx, nbase, nx, l + 1);
   }
   wave_add(went, &S.sc->ncont);
 }
@@ -577,7 +611,7 @@ __device__ __forceinline__ uint32_t walk_bwd(const Problem3 &P, const Search3 &S
                                              int heavy_l) {
   for (int depth = 0; depth < CHAIN3; ++depth) {
     const uint32_t p0 = P.in_off[v], p1 = P.in_off[v + 1];
-    if (p1 - p0 > LIGHT3) {
+    if (p1 - p0 > WALK3) {
       push_chunks(S, heavy_to, heavy_l, v, p1 - p0);
       return (uint32_t)depth;
     }
@@ -617,7 +651,7 @@ __global__ __launch_bounds__(NT) void k3_bwd_chunks(Problem3 P, Search3 S, int l
   for (ull i = (ull)blockIdx.x * NT + threadIdx.x; i < nch; i += (ull)gridDim.x * NT) {
     const uint2 c = list[i];
     const uint32_t p0 = P.in_off[c.x] + c.y, pe = P.in_off[c.x + 1];
-    const uint32_t p1 = p0 + LIGHT3 < pe ? p0 + LIGHT3 : pe;
+    const uint32_t p1 = p0 + CHUNK3 < pe ? p0 + CHUNK3 : pe;
     uint32_t cont = NO_SLOT;
     bwd_range(P, S, p0, p1, nx, nbase, &cont);
     if (cont != NO_SLOT) went += 1 + walk_bwd(P, S, cont, nx, nbase, nx, l + 1);

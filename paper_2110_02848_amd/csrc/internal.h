@@ -200,6 +200,10 @@ struct Problem3 {
   const int32_t *id_of;     // slot -> state id of C (-1: not trim)
 };
 
+// Units (forward) or in-arcs (backward) of a heavy key that one search
+// thread of a three-input search takes.
+constexpr uint32_t CHUNK3 = 8;
+
 // A level of a three-input search in a ring of three: its frontier entries
 // F[fbase, fbase + fcount) and the number of heavy-state chunks it listed.
 struct Lvl3 {
