@@ -62,15 +62,16 @@ def kernel_bytes(st):
     search (both searches, whose launches the default order shares): 4 B
     probe per move out of an accessible key + 16 B per accessible key
     (frontier write and read), and the same over the predecessor moves of
-    the co-accessible keys and those keys; count: 8 B per state of C (its
-    key in, its count out) + 4 B per kept arc (the probe of its target);
-    fill: the output CSR (20 B per arc, 6 B per state + 4 B)."""
+    the co-accessible keys and those keys; count: 1 B per state of C (its
+    count out; keys come from the trim bitmap, 1 bit each) + 4 B per kept
+    arc (the probe of its target); fill: the output CSR (20 B per arc, 6 B
+    per state + 4 B) and each state's count (1 B)."""
     V, E = st["num_states"], st["num_arcs"]
     return {
         "search": (4 * st["generated"] + 16 * st["accessible"]
                    + 4 * st["generated_backward"] + 16 * st["coaccessible"]),
-        "count": 8 * V + 4 * E,
-        "fill": 20 * E + 4 * (V + 1) + 2 * V,
+        "count": V + 4 * E,
+        "fill": 20 * E + 4 * (V + 1) + 2 * V + V,
     }
 
 
