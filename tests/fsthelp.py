@@ -437,3 +437,31 @@ def check_invariants3(A, B, D, C):
     if not bwd.all():
         errs.append("non-coaccessible state")
     return errs
+
+
+def wide_fanout_pair(rng, fan=(300, 255, 254), n_mid=300, n_gap=5):
+    """A pair whose start keys are light states (one work unit) with many
+    kept arcs: A's start states (its last states, after n_gap isolated ones)
+    have fan[i] arcs with output 1 to the middle states 1..fan[i], each of
+    which reaches the accepting state 0 by an arc with output 2; B reads
+    1 then 2.  The start key (s, 0) joins its one B arc with A's 1-bucket:
+    fan[i] arcs of C from one state (255 and more take the output passes'
+    wide-count path).  With n_mid + n_gap + 1 = 306 the start states sit at
+    rows 306.. and a batch item's first state follows them in the same
+    output chunk of 16 trim words (B has three states: one row per word)."""
+    f32 = lambda: float(np.float32(rng.standard_normal()))
+    arcs = [(k, 0, 8, 2, f32()) for k in range(1, n_mid + 1)]
+    first = n_mid + n_gap + 1
+    starts = []
+    for i, n in enumerate(fan):
+        s = first + i
+        starts.append(s)
+        arcs += [(s, k, 7, 1, f32()) for k in range(1, n + 1)]
+    A = synth_from_arcs(first + len(fan), arcs, start=starts, accept=[0])
+    B = synth_from_arcs(3, [(0, 1, 1, 5, f32()), (1, 2, 2, 6, f32())], start=[0], accept=[2])
+    return A, B
+
+
+def synth_from_arcs(V, arcs, start, accept):
+    from paper_2110_02848_amd import synth
+    return synth.from_arcs(V, arcs, start=start, accept=accept)

@@ -190,6 +190,20 @@ def test_chain_of_three(comp, seed):
     assert not errs, errs[:5]
 
 
+def test_batch_item_after_wide_states(comp):
+    """Items whose first state follows, in the same output chunk, the
+    previous item's start states of 300, 255 and 254 arcs: each item's first
+    arc counts them (wide counts) and every item equals the oracle's."""
+    rng = np.random.default_rng(32)
+    As, B = [], None
+    for _ in range(3):
+        A, B0 = fsthelp.wide_fanout_pair(rng)
+        As.append(A)
+        B = B if B is not None else B0
+    C, st, ar = check_batch(comp, As, B, "items after wide states")
+    assert int(ar[1]) == 1109 and int(ar[2]) == 2 * 1109
+
+
 def test_batch_full_size_lexicon(comp):
     """Four full-size utterances (T = 500, 10,000-word lexicon) in one pass:
     every item's state and arc counts equal the closed form from the word

@@ -474,6 +474,16 @@ def test_rounding_cases(comp):
         check_pair(comp, A, B, f"rounding {wa} {wb}")
 
 
+def test_light_states_with_wide_fanout(comp):
+    """Start keys with one work unit each and 300, 255 and 254 kept arcs:
+    the counts of 255 and more take the wide-count path of count and fill,
+    and the offsets of every later state include them."""
+    A, B = fsthelp.wide_fanout_pair(np.random.default_rng(31))
+    got, _ = check_pair(comp, A, B, "wide fan-out of light states")
+    deg = np.diff(got["arc_offset"].astype(np.int64))
+    assert sorted(deg.tolist())[-3:] == [254, 255, 300]
+
+
 def test_degenerate_inputs(comp):
     E0 = synth.empty_graph()
     A, B = synth.workload("random-64", 0)
