@@ -313,7 +313,15 @@ FST_API int fst_grad_scatter_noalloc(fst_ctx *ctx, int64_t n, const float *grad,
  * arc_offset) for item-local values; key_a and arc_a index the union of the
  * A_i (subtract the states / arcs of the items before i).  item_states and
  * item_arcs are host arrays of n + 1 entries, filled on success (the last
- * entries are V_C and E_C).  Limits as for one A, applied to the union.
+ * entries are V_C and E_C).  Items are composed in parts: consecutive
+ * items whose union fits the key space of one composition (an item that
+ * does not fit alone gives FST_ERR_TOO_LARGE); most batches are one part,
+ * one search.  With several parts the run searches each part in turn, and
+ * fst_compose_fill searches every part but the last again before writing
+ * it, so that fill blocks until done; the A_i and B must stay valid and
+ * unchanged until the fill has completed (a part that comes out with other
+ * sizes gives FST_ERR_STATE).  fst_compose_stats then reports sums over the
+ * parts (levels: the largest).  V_C and E_C are at most INT32_MAX.
  * Chains (N-way composition): C has the input layout, so A o B o D is two
  * calls (compose, then compose C with D). */
 FST_API int fst_compose_batch_run(fst_ctx *ctx, const fst_graph *A, int32_t n,

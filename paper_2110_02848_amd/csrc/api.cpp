@@ -105,6 +105,22 @@ struct fst_ctx {
   unsigned long long nkeys = 0;
   size_t out_words = 0;  // trim words the output passes cover
   fst_stats stats = {};
+
+  // A batch composed in parts: consecutive items whose key space fits 32
+  // bits each; the context holds the search state of part cur_part, and the
+  // fill searches every other part again.  Empty for a plain composition or
+  // a batch of one part.
+  struct BatchPart {
+    int32_t i0, i1;                  // items [i0, i1)
+    long long vbase, ebase;          // first state and arc of the part in C
+    long long abase, aebase;         // first state and arc of its items in the union of A
+    long long V, E;                  // its states and arcs
+  };
+  std::vector<BatchPart> parts;
+  std::vector<fst_graph> batch_A;
+  fst_graph batch_B = {};
+  int cur_part = -1;
+  fst_stats batch_stats = {};
 };
 
 namespace {
@@ -1165,27 +1181,14 @@ int compose3_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, const fst_
 // Batch: validate every item, lay the items out as one disjoint union (state
 // and arc offsets shifted), compose the union with B, then find each item's
 // state and arc range in C.
-int batch_impl(fst_ctx *c, const fst_graph *A, int32_t n, const fst_graph *B, hipStream_t s,
-               int64_t *V_C, int64_t *E_C, int64_t *item_states, int64_t *item_arcs) {
+// The disjoint union of items A[0 .. n) in the context's union arrays, as
+// one graph U (state and arc ids of item i shifted by the items before it).
+int build_union(fst_ctx *c, const fst_graph *A, int32_t n, hipStream_t s, fst_graph *U) {
   long long VA = 0, EA = 0;
   for (int32_t i = 0; i < n; ++i) {
-    FST_TRY(check_graph_args(&A[i]));
     VA += A[i].num_states;
     EA += A[i].num_arcs;
   }
-  if (VA > NBR_MASK || EA > INT32_MAX) return FST_ERR_TOO_LARGE;
-  // each item on its own first: an arc of one item must not name a state
-  // of another once the union shifts its ids
-  FST_TRY(ensure(c, c->scal, sizeof(Scalars)));
-  Scalars *d_sc = as<Scalars>(c->scal);
-  HIP_TRY(hipMemsetAsync(d_sc, 0, sizeof(Scalars), s));
-  for (int32_t i = 0; i < n; ++i)
-    if (A[i].num_states > 0)
-      HIP_TRY(launch_validate(dev_graph(&A[i]), 0, &d_sc->errA, &d_sc->maxLabA, s, nullptr,
-                              c->validate));
-  FST_TRY(readback(c, s));
-  if (c->h_sc->errA & ~(1u << 16)) return FST_ERR_INVALID_GRAPH;
-
   FST_TRY(ensure(c, c->u_off, ((size_t)VA + 1) * 4));
   FST_TRY(ensure(c, c->u_src, (size_t)EA * 4));
   FST_TRY(ensure(c, c->u_dst, (size_t)EA * 4));
@@ -1194,7 +1197,6 @@ int batch_impl(fst_ctx *c, const fst_graph *A, int32_t n, const fst_graph *B, hi
   FST_TRY(ensure(c, c->u_w, (size_t)EA * 4));
   FST_TRY(ensure(c, c->u_start, (size_t)VA));
   FST_TRY(ensure(c, c->u_accept, (size_t)VA));
-  FST_TRY(ensure(c, c->u_items, ((size_t)n + 1) * 3 * sizeof(long long)));
   int32_t *off = as<int32_t>(c->u_off);
   HIP_TRY(hipMemsetAsync(off, 0, 4, s));  // the offsets of an empty union
   long long vb = 0, eb = 0;
@@ -1218,31 +1220,42 @@ int batch_impl(fst_ctx *c, const fst_graph *A, int32_t n, const fst_graph *B, hi
     vb += a.V;
     eb += a.E;
   }
-  fst_graph U = {};
-  U.num_states = (int32_t)VA;
-  U.num_arcs = (int32_t)EA;
-  U.arc_offset = off;
-  U.src = as<int32_t>(c->u_src);
-  U.dst = as<int32_t>(c->u_dst);
-  U.ilabel = as<int32_t>(c->u_il);
-  U.olabel = as<int32_t>(c->u_ol);
-  U.weight = as<float>(c->u_w);
-  U.start = as<uint8_t>(c->u_start);
-  U.accept = as<uint8_t>(c->u_accept);
-  FST_TRY(run_impl(c, &U, B, s, V_C, E_C));
+  *U = fst_graph{};
+  U->num_states = (int32_t)VA;
+  U->num_arcs = (int32_t)EA;
+  U->arc_offset = off;
+  U->src = as<int32_t>(c->u_src);
+  U->dst = as<int32_t>(c->u_dst);
+  U->ilabel = as<int32_t>(c->u_il);
+  U->olabel = as<int32_t>(c->u_ol);
+  U->weight = as<float>(c->u_w);
+  U->start = as<uint8_t>(c->u_start);
+  U->accept = as<uint8_t>(c->u_accept);
+  return FST_OK;
+}
 
-  // item ranges: qa_base[0..n] (first state of A of each item, then VA)
+// Items [i0, i1) composed with B as one union: run, then the first state and
+// arc of every item in that run's C (st[i - i0], ar[i - i0]; the last
+// entries are the run's V_C and E_C).
+int run_items(fst_ctx *c, const fst_graph *A, int32_t i0, int32_t i1, const fst_graph *B,
+              hipStream_t s, int64_t *V_C, int64_t *E_C, long long *st, long long *ar) {
+  const int32_t n = i1 - i0;
+  fst_graph U;
+  FST_TRY(build_union(c, A + i0, n, s, &U));
+  FST_TRY(run_impl(c, &U, B, s, V_C, E_C));
+  if (c->nstates == 0) {
+    for (int32_t i = 0; i <= n; ++i) st[i] = ar[i] = 0;
+    return FST_OK;
+  }
+  // qa_base[0..n] (first state of A of each item, then the union's V_A)
   std::vector<long long> h(3 * ((size_t)n + 1), 0);
   long long acc = 0;
   for (int32_t i = 0; i < n; ++i) {
     h[i] = acc;
-    acc += A[i].num_states;
+    acc += A[i0 + i].num_states;
   }
   h[n] = acc;
-  if (c->nstates == 0) {
-    for (int32_t i = 0; i <= n; ++i) item_states[i] = item_arcs[i] = 0;
-    return FST_OK;
-  }
+  FST_TRY(ensure(c, c->u_items, ((size_t)n + 1) * 3 * sizeof(long long)));
   long long *dq = as<long long>(c->u_items), *dout = dq + (n + 1);
   HIP_TRY(hipMemcpyAsync(dq, h.data(), ((size_t)n + 1) * sizeof(long long),
                          hipMemcpyHostToDevice, s));
@@ -1252,9 +1265,175 @@ int batch_impl(fst_ctx *c, const fst_graph *A, int32_t n, const fst_graph *B, hi
                          hipMemcpyDeviceToHost, s));
   HIP_TRY(hipStreamSynchronize(s));
   for (int32_t i = 0; i <= n; ++i) {
-    item_states[i] = h[(n + 1) + i];
-    item_arcs[i] = h[2 * (n + 1) + i];
+    st[i] = h[(n + 1) + i];
+    ar[i] = h[2 * (n + 1) + i];
   }
+  return FST_OK;
+}
+
+void add_stats(fst_stats &t, const fst_stats &p) {
+  t.key_space += p.key_space;
+  t.accessible += p.accessible;
+  t.coaccessible += p.coaccessible;
+  t.generated = t.generated < 0 || p.generated < 0 ? -1 : t.generated + p.generated;
+  t.generated_backward = t.generated_backward < 0 || p.generated_backward < 0
+                             ? -1
+                             : t.generated_backward + p.generated_backward;
+  t.fwd_levels = t.fwd_levels > p.fwd_levels ? t.fwd_levels : p.fwd_levels;
+  t.bwd_levels = t.bwd_levels > p.bwd_levels ? t.bwd_levels : p.bwd_levels;
+  t.heavy_states += p.heavy_states;
+  t.num_states += p.num_states;
+  t.num_arcs += p.num_arcs;
+}
+
+int batch_impl(fst_ctx *c, const fst_graph *A, int32_t n, const fst_graph *B, hipStream_t s,
+               int64_t *V_C, int64_t *E_C, int64_t *item_states, int64_t *item_arcs) {
+  c->parts.clear();
+  c->batch_A.clear();
+  c->cur_part = -1;
+  long long VA = 0, EA = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    FST_TRY(check_graph_args(&A[i]));
+    VA += A[i].num_states;
+    EA += A[i].num_arcs;
+  }
+  FST_TRY(check_graph_args(B));
+  if (EA > INT32_MAX) return FST_ERR_TOO_LARGE;
+  // each item on its own first: an arc of one item must not name a state
+  // of another once the union shifts its ids
+  FST_TRY(ensure(c, c->scal, sizeof(Scalars)));
+  Scalars *d_sc = as<Scalars>(c->scal);
+  HIP_TRY(hipMemsetAsync(d_sc, 0, sizeof(Scalars), s));
+  for (int32_t i = 0; i < n; ++i)
+    if (A[i].num_states > 0)
+      HIP_TRY(launch_validate(dev_graph(&A[i]), 0, &d_sc->errA, &d_sc->maxLabA, s, nullptr,
+                              c->validate));
+  FST_TRY(readback(c, s));
+  if (c->h_sc->errA & ~(1u << 16)) return FST_ERR_INVALID_GRAPH;
+
+  // Parts: consecutive items whose union has a key space below 2^32 (with
+  // its A states rounded up to 64 for the search layout, as the run checks)
+  unsigned long long max_rows = ~0ull;
+  if (B->num_states > 0) {
+    const int bitsB = bitlen((unsigned long long)(B->num_states - 1));
+    const uint32_t shiftB = (uint32_t)(bitsB > 4 ? bitsB : 4);
+    max_rows = (((1ull << 32) - 1) >> (shiftB + 1)) / 64 * 64;
+    if (max_rows > NBR_MASK) max_rows = NBR_MASK;
+  }
+  std::vector<std::pair<int32_t, int32_t>> ranges;
+  {
+    int32_t i0 = 0;
+    unsigned long long rows = 0;
+    for (int32_t i = 0; i < n; ++i) {
+      const unsigned long long v = (unsigned long long)A[i].num_states;
+      if (v > max_rows) return FST_ERR_TOO_LARGE;  // one item alone is too large
+      if (rows + v > max_rows && i > i0) {
+        ranges.emplace_back(i0, i);
+        i0 = i;
+        rows = 0;
+      }
+      rows += v;
+    }
+    ranges.emplace_back(i0, n);
+  }
+
+  std::vector<long long> st((size_t)n + 1), ar((size_t)n + 1);
+  if (ranges.size() == 1) {
+    if (VA > NBR_MASK) return FST_ERR_TOO_LARGE;
+    FST_TRY(run_items(c, A, 0, n, B, s, V_C, E_C, st.data(), ar.data()));
+    for (int32_t i = 0; i <= n; ++i) {
+      item_states[i] = st[i];
+      item_arcs[i] = ar[i];
+    }
+    return FST_OK;
+  }
+
+  // several parts: each run in turn; C is the parts' results one after the
+  // other (item order), ids shifted by the parts before
+  fst_stats total = {};
+  total.generated = total.generated_backward = 0;
+  long long vbase = 0, ebase = 0, abase = 0, aebase = 0;
+  for (size_t p = 0; p < ranges.size(); ++p) {
+    const int32_t i0 = ranges[p].first, i1 = ranges[p].second;
+    int64_t Vp = 0, Ep = 0;
+    FST_TRY(run_items(c, A, i0, i1, B, s, &Vp, &Ep, st.data(), ar.data()));
+    for (int32_t i = i0; i < i1; ++i) {
+      item_states[i] = vbase + st[i - i0];
+      item_arcs[i] = ebase + ar[i - i0];
+    }
+    long long va = 0, ea = 0;
+    for (int32_t i = i0; i < i1; ++i) {
+      va += A[i].num_states;
+      ea += A[i].num_arcs;
+    }
+    c->parts.push_back(fst_ctx::BatchPart{i0, i1, vbase, ebase, abase, aebase, Vp, Ep});
+    add_stats(total, c->stats);
+    vbase += Vp;
+    ebase += Ep;
+    abase += va;
+    aebase += ea;
+    if (vbase > INT32_MAX || ebase > INT32_MAX) {
+      c->parts.clear();
+      return FST_ERR_TOO_LARGE;
+    }
+  }
+  item_states[n] = vbase;
+  item_arcs[n] = ebase;
+  *V_C = vbase;
+  *E_C = ebase;
+  c->batch_A.assign(A, A + n);
+  c->batch_B = *B;
+  c->cur_part = (int)ranges.size() - 1;
+  c->batch_stats = total;
+  c->stats = total;
+  c->timed_run = false;
+  return FST_OK;
+}
+
+// The fill of a batch in parts: the part whose search state the context
+// holds first, then every other part searched again (same sizes, or the
+// inputs changed: FST_ERR_STATE), each written at its place in C.
+int fill_parts(fst_ctx *c, const fst_graph_out *C, hipStream_t s) {
+  std::vector<int> order;
+  order.push_back(c->cur_part);
+  for (int p = 0; p < (int)c->parts.size(); ++p)
+    if (p != c->cur_part) order.push_back(p);
+  for (int p : order) {
+    const fst_ctx::BatchPart &part = c->parts[(size_t)p];
+    if (p != c->cur_part) {
+      int64_t Vp = 0, Ep = 0;
+      std::vector<long long> st((size_t)(part.i1 - part.i0) + 1), ar(st.size());
+      c->cur_part = -1;
+      FST_TRY(run_items(c, c->batch_A.data(), part.i0, part.i1, &c->batch_B, s, &Vp, &Ep,
+                        st.data(), ar.data()));
+      c->cur_part = p;
+      if (Vp != part.V || Ep != part.E) return FST_ERR_STATE;
+    }
+    const long long vb = part.vbase, eb = part.ebase;
+    OutGraph O = {};
+    O.arc_offset = C->arc_offset + vb;
+    O.src = C->src ? C->src + eb : nullptr;
+    O.dst = C->dst ? C->dst + eb : nullptr;
+    O.il = C->ilabel ? C->ilabel + eb : nullptr;
+    O.ol = C->olabel ? C->olabel + eb : nullptr;
+    O.w = C->weight ? C->weight + eb : nullptr;
+    O.start = C->start ? C->start + vb : nullptr;
+    O.accept = C->accept ? C->accept + vb : nullptr;
+    O.key_a = C->key_a ? C->key_a + vb : nullptr;
+    O.key_b = C->key_b ? C->key_b + vb : nullptr;
+    O.key_f = C->key_f ? C->key_f + vb : nullptr;
+    O.arc_a = C->arc_a ? C->arc_a + eb : nullptr;
+    O.arc_b = C->arc_b ? C->arc_b + eb : nullptr;
+    O.vbase = (int32_t)vb;
+    O.ebase = (int32_t)eb;
+    O.abase = (int32_t)part.abase;
+    O.aebase = (int32_t)part.aebase;
+    HIP_TRY(launch_fill(c->P, c->nstates ? c->out_words : 0, as<uint8_t>(c->cnt),
+                        as<uint32_t>(c->fq), as<uint32_t>(c->btot), as<uint2>(c->bq), c->nheavy,
+                        c->nstates, c->narcs, O, s));
+  }
+  c->stats = c->batch_stats;
+  c->timed_run = false;
   return FST_OK;
 }
 
@@ -1416,6 +1595,7 @@ int fst_compose_run(fst_ctx *c, const fst_graph *A, const fst_graph *B, void *st
   c->ready = false;
   c->have_times = false;
   c->timed_run = false;
+  c->parts.clear();
   *num_states = 0;
   *num_arcs = 0;
   int rc = run_impl(c, A, B, reinterpret_cast<hipStream_t>(stream), num_states, num_arcs);
@@ -1450,6 +1630,7 @@ int fst_compose_batch_run(fst_ctx *c, const fst_graph *A, int32_t n, const fst_g
   }
   if (rc != FST_OK) {
     c->ready = false;
+    c->parts.clear();
     *num_states = 0;
     *num_arcs = 0;
     for (int32_t i = 0; i <= n; ++i) item_states[i] = item_arcs[i] = 0;
@@ -1461,14 +1642,32 @@ int fst_compose_batch_run(fst_ctx *c, const fst_graph *A, int32_t n, const fst_g
 int fst_compose_fill(fst_ctx *c, const fst_graph_out *C, void *stream) {
   if (!c || !C) return FST_ERR_INVALID_ARG;
   if (!c->ready) return FST_ERR_STATE;
+  const bool parts = !c->parts.empty();
+  const long long nst = parts ? c->batch_stats.num_states : c->nstates;
+  const long long nar = parts ? c->batch_stats.num_arcs : c->narcs;
   if (!C->arc_offset) return FST_ERR_INVALID_ARG;
-  if (c->nstates && (!C->start || !C->accept)) return FST_ERR_INVALID_ARG;
-  if (c->narcs && (!C->src || !C->dst || !C->ilabel || !C->olabel || !C->weight))
+  if (nst && (!C->start || !C->accept)) return FST_ERR_INVALID_ARG;
+  if (nar && (!C->src || !C->dst || !C->ilabel || !C->olabel || !C->weight))
     return FST_ERR_INVALID_ARG;
   DeviceGuard g(c->device);
   if (!g.ok) return FST_ERR_HIP;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  OutGraph O;
+  if (parts) {
+    int rc = FST_OK;
+    try {
+      rc = fill_parts(c, C, s);
+    } catch (const std::bad_alloc &) {
+      rc = FST_ERR_NOMEM;
+    }
+    if (rc != FST_OK) {
+      c->ready = false;
+      c->parts.clear();
+      (void)hipGetLastError();
+    }
+    c->have_times = false;
+    return rc;
+  }
+  OutGraph O = {};
   O.arc_offset = C->arc_offset;
   O.src = C->src;
   O.dst = C->dst;

@@ -1612,12 +1612,12 @@ __device__ __forceinline__ bool put_arc(const OutGraph &O, const Problem &P, uin
                                         uint32_t id, uint32_t dk, int32_t il, int32_t ol,
                                         float w, int32_t pa, int32_t pb) {
   const uint32_t tw = P.trim[dk >> 5], base = P.wbase[dk >> 5];
-  const int32_t ida = O.arc_a && pa >= 0 ? P.aOut.perm[pa] : -1;
+  const int32_t ida = O.arc_a && pa >= 0 ? P.aOut.perm[pa] + O.aebase : -1;
   const int32_t idb = O.arc_b && pb >= 0 ? P.bOut.perm[pb] : -1;
   const uint32_t below = tw & ((1u << (dk & 31u)) - 1u);
   if (!((tw >> (dk & 31u)) & 1u)) return false;
-  out_store(O.src + pos, (int32_t)id);
-  out_store(O.dst + pos, (int32_t)(base + (uint32_t)__popc(below)));
+  out_store(O.src + pos, (int32_t)id + O.vbase);
+  out_store(O.dst + pos, (int32_t)(base + (uint32_t)__popc(below)) + O.vbase);
   out_store(O.il + pos, il);
   out_store(O.ol + pos, ol);
   out_store(O.w + pos, w);
@@ -1632,13 +1632,13 @@ __device__ __forceinline__ void put_move(const OutGraph &O, const Problem &P, ui
                                          uint32_t id, Move m) {
   const uint32_t dk = m.d;
   const uint32_t tw = P.trim[dk >> 5], base = P.wbase[dk >> 5];
-  const int32_t ida = O.arc_a && m.pa >= 0 ? P.aOut.perm[m.pa] : -1;
+  const int32_t ida = O.arc_a && m.pa >= 0 ? P.aOut.perm[m.pa] + O.aebase : -1;
   const int32_t idb = O.arc_b && m.pb >= 0 ? P.bOut.perm[m.pb] : -1;
   move_labels(P, m);
   const uint32_t below = tw & ((1u << (dk & 31u)) - 1u);
   if (!((tw >> (dk & 31u)) & 1u)) return;
-  out_store(O.src + pos, (int32_t)id);
-  out_store(O.dst + pos, (int32_t)(base + (uint32_t)__popc(below)));
+  out_store(O.src + pos, (int32_t)id + O.vbase);
+  out_store(O.dst + pos, (int32_t)(base + (uint32_t)__popc(below)) + O.vbase);
   out_store(O.il + pos, m.il);
   out_store(O.ol + pos, m.ol);
   out_store(O.w + pos, m.w);
@@ -1834,10 +1834,10 @@ __device__ __forceinline__ void fill_light(const Problem &P, ull nwords, ull nch
     run += __shfl(incl, WAVE - 1, WAVE);
     if (!valid) continue;
     const Fwd s = fwd_info(P, key);
-    out_store(O.arc_offset + id, (int32_t)pos);
+    out_store(O.arc_offset + id, (int32_t)pos + O.ebase);
     out_store(O.accept + id, (uint8_t)(s.accept ? 1 : 0));
     out_store(O.start + id, (uint8_t)(s.start ? 1 : 0));
-    if (O.key_a) out_store(O.key_a + id, (int32_t)s.qa);
+    if (O.key_a) out_store(O.key_a + id, (int32_t)s.qa + O.abase);
     if (O.key_b) out_store(O.key_b + id, (int32_t)s.qb);
     if (O.key_f) out_store(O.key_f + id, (uint8_t)s.f);
     if (out_units(s) > LIGHT_UNITS) continue;
@@ -1879,7 +1879,8 @@ __global__ __launch_bounds__(NT) void k_fill(Problem P, ull nwords, ull nchunks,
   }
   const unsigned block = blockIdx.x - hb;
   fill_light(P, nwords, nchunks, cnt8, cnt32, btot, O, block);
-  if (block == gridDim.x - hb - 1 && threadIdx.x == 0) O.arc_offset[nstates] = (int32_t)narcs;
+  if (block == gridDim.x - hb - 1 && threadIdx.x == 0)
+    O.arc_offset[nstates] = (int32_t)narcs + O.ebase;
 }
 
 // ---------------------------------------------------------------------------

@@ -124,7 +124,9 @@ struct Problem {
   const uint32_t *wbase;  // exclusive popcount prefix of trim words
 };
 
-// Output arrays of C.
+// Output arrays of C.  The arrays may start inside a larger C (one part of
+// a batch): written ids then add vbase (states), ebase (arc offsets), abase
+// (key_a, A states) and aebase (arc_a, A arcs); all 0 otherwise.
 struct OutGraph {
   int32_t *arc_offset, *src, *dst, *il, *ol;
   float *w;
@@ -132,6 +134,7 @@ struct OutGraph {
   int32_t *key_a, *key_b;
   uint8_t *key_f;
   int32_t *arc_a, *arc_b;
+  int32_t vbase, ebase, abase, aebase;
 };
 
 // Work of one search generation, kept in one of three rotating slots

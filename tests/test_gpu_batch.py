@@ -52,14 +52,15 @@ def item_slice(C, st, ar, i, As):
         key_b=C["key_b"][s0:s1], key_f=C["key_f"][s0:s1])
 
 
-def check_batch(comp, As, B, tag):
+def check_batch(comp, As, B, tag, ref_B=None):
+    """ref_B: the B the oracle composes each item with (default B)."""
     print(f"[batch] {tag}", flush=True)
     C, st, ar = gpu_batch(comp, As, B)
     assert st[0] == 0 and ar[0] == 0
     assert st[-1] == C["num_states"] and ar[-1] == C["num_arcs"]
     assert np.all(np.diff(st) >= 0) and np.all(np.diff(ar) >= 0)
     for i, A in enumerate(As):
-        ref = oracle.compose(A, B)
+        ref = oracle.compose(A, B if ref_B is None else ref_B)
         got = item_slice(C, st, ar, i, As)
         errs = fsthelp.compare_results(got, ref)
         assert not errs, (tag, i, errs[:5])
@@ -202,6 +203,52 @@ def test_batch_item_after_wide_states(comp):
         B = B if B is not None else B0
     C, st, ar = check_batch(comp, As, B, "items after wide states")
     assert int(ar[1]) == 1109 and int(ar[2]) == 2 * 1109
+
+
+def padded(B, extra):
+    """B with `extra` isolated states appended (no arcs, neither start nor
+    accepting): the same compositions over a larger key space."""
+    g = dict(B)
+    g["num_states"] = int(B["num_states"]) + extra
+    g["arc_offset"] = np.concatenate(
+        [B["arc_offset"], np.full(extra, B["arc_offset"][-1], np.int32)])
+    g["start"] = np.concatenate([B["start"], np.zeros(extra, np.uint8)])
+    g["accept"] = np.concatenate([B["accept"], np.zeros(extra, np.uint8)])
+    return g
+
+
+def test_batch_in_parts(comp):
+    """A batch whose union needs more than 2^32 keys: B padded with 2^21
+    isolated states has 2^23 keys per A state, so at most 448 A states fit
+    one search and the five items (151 + 201, 121 + 251, 91 A states) are
+    composed in three parts.  Every item equals the oracle's A_i o B (the
+    oracle composes with B without the padding, which no key reaches: the
+    same states, keys and arcs), with the ids, key_a and arc_a of the whole
+    batch; a second fill writes the same C; the statistics are the sums."""
+    import torch
+    from paper_2110_02848_amd import gpu
+    spec = synth.LexSpec(T=0, C=6, W=40, len_lo=2, len_hi=5)
+    As, B, _ = synth.lexicon_batch("lexicon-T100-W1000", 5, 0, spec=spec,
+                                   frames=[150, 200, 120, 250, 90])
+    Bbig = padded(B, 1 << 21)
+    C, st, ar = check_batch(comp, As, Bbig, "batch in three parts", ref_B=B)
+    assert C["num_states"] > 0 and int(st[-1]) == C["num_states"]
+    stats = comp.stats()
+    assert stats["num_states"] == C["num_states"] and stats["num_arcs"] == C["num_arcs"]
+    # the inputs stay allocated until the fills are done: the fill of a batch
+    # in parts searches its parts again
+    dAs, dB = [gpu.to_device(A) for A in As], gpu.to_device(Bbig)
+    nv, ne, st2, ar2 = comp.run_batch(dAs, dB)
+    assert (list(st2), list(ar2)) == (list(st), list(ar))
+    C1 = comp.fill(comp.alloc_output(nv, ne))
+    C2 = comp.fill(comp.alloc_output(nv, ne))
+    torch.cuda.synchronize()
+    g1, g2 = gpu.to_numpy(C1), gpu.to_numpy(C2)
+    assert not fsthelp.compare_results(g1, g2)
+    assert not fsthelp.compare_results(g1, C)
+    del dAs, dB
+    # a plain composition after it is a plain composition again
+    check_batch(comp, [As[0]], B, "one part after parts")
 
 
 def test_batch_full_size_lexicon(comp):
