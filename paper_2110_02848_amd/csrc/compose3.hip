@@ -552,17 +552,30 @@ __global__ __launch_bounds__(NT) void k3_fwd_chunks(Problem3 P, Search3 S, int l
 // backward search over the recorded arcs
 // ---------------------------------------------------------------------------
 
-__global__ __launch_bounds__(NT) void k3_indeg(const uint2 *arcs, ull narcs, uint32_t *indeg) {
-  for (ull e = (ull)blockIdx.x * NT + threadIdx.x; e < narcs; e += (ull)gridDim.x * NT)
-    atomicAdd(indeg + arcs[e].y, 1u);
-}
-
-__global__ __launch_bounds__(NT) void k3_place(const uint2 *arcs, ull narcs, uint32_t *cursor,
-                                               uint32_t *in_src) {
+// In-arcs grouped by target without atomics: the arcs as (target, source)
+// pairs, sorted by target (a radix sort); then each run of one target marks
+// its first position (run start) and, at its last, its length (the target's
+// in-degree); a scan of the in-degrees gives the offsets, and the sorted
+// sources are the in-arc lists.
+__global__ __launch_bounds__(NT) void k3_arc_keys(const uint2 *arcs, ull narcs, ull *key,
+                                                  int32_t *src) {
   for (ull e = (ull)blockIdx.x * NT + threadIdx.x; e < narcs; e += (ull)gridDim.x * NT) {
     const uint2 a = arcs[e];
-    in_src[atomicAdd(cursor + a.y, 1u)] = a.x;
+    key[e] = a.y;
+    src[e] = (int32_t)a.x;
   }
+}
+
+__global__ __launch_bounds__(NT) void k3_run_starts(const ull *key, ull narcs,
+                                                    uint32_t *first) {
+  for (ull e = (ull)blockIdx.x * NT + threadIdx.x; e < narcs; e += (ull)gridDim.x * NT)
+    if (e == 0 || key[e] != key[e - 1]) first[key[e]] = (uint32_t)e;
+}
+
+__global__ __launch_bounds__(NT) void k3_run_ends(const ull *key, ull narcs,
+                                                  const uint32_t *first, uint32_t *indeg) {
+  for (ull e = (ull)blockIdx.x * NT + threadIdx.x; e < narcs; e += (ull)gridDim.x * NT)
+    if (e + 1 == narcs || key[e] != key[e + 1]) indeg[key[e]] = (uint32_t)(e + 1) - first[key[e]];
 }
 
 __device__ __forceinline__ bool claim_bit(uint32_t *bm, uint32_t s) {
@@ -853,11 +866,18 @@ hipError_t launch3_level(const Problem3 &P, const Search3 &S, bool forward, int 
   return hipGetLastError();
 }
 
-hipError_t launch3_in_arcs(const uint2 *arcs, unsigned long long narcs, uint32_t *indeg_or_cursor,
-                           uint32_t *in_src, bool place, hipStream_t s) {
+hipError_t launch3_arc_keys(const uint2 *arcs, unsigned long long narcs, unsigned long long *key,
+                            int32_t *src, hipStream_t s) {
   if (!narcs) return hipSuccess;
-  if (place) k3_place<<<grid3((size_t)narcs), NT, 0, s>>>(arcs, narcs, indeg_or_cursor, in_src);
-  else k3_indeg<<<grid3((size_t)narcs), NT, 0, s>>>(arcs, narcs, indeg_or_cursor);
+  k3_arc_keys<<<grid3((size_t)narcs), NT, 0, s>>>(arcs, narcs, key, src);
+  return hipGetLastError();
+}
+
+hipError_t launch3_in_degrees(const unsigned long long *key, unsigned long long narcs,
+                              uint32_t *first, uint32_t *indeg, hipStream_t s) {
+  if (!narcs) return hipSuccess;
+  k3_run_starts<<<grid3((size_t)narcs), NT, 0, s>>>(key, narcs, first);
+  k3_run_ends<<<grid3((size_t)narcs), NT, 0, s>>>(key, narcs, first, indeg);
   return hipGetLastError();
 }
 

@@ -550,10 +550,13 @@ hipError_t launch3_seed(const Problem3 &P, const Search3 &S, const int32_t *list
 // Level l of the forward (or backward) search: two kernels.
 hipError_t launch3_level(const Problem3 &P, const Search3 &S, bool forward, int l,
                          hipStream_t s);
-// In-arc counts of every slot (place = false: indeg_or_cursor counts), or
-// the placement of every arc's source (place = true: cursor = in_off).
-hipError_t launch3_in_arcs(const uint2 *arcs, unsigned long long narcs, uint32_t *indeg_or_cursor,
-                           uint32_t *in_src, bool place, hipStream_t s);
+// The generated arcs as (target, source) pairs for a sort by target; then,
+// over the sorted targets, every target's in-degree (indeg, zeroed by the
+// caller; first: H scratch entries).
+hipError_t launch3_arc_keys(const uint2 *arcs, unsigned long long narcs, unsigned long long *key,
+                            int32_t *src, hipStream_t s);
+hipError_t launch3_in_degrees(const unsigned long long *key, unsigned long long narcs,
+                              uint32_t *first, uint32_t *indeg, hipStream_t s);
 hipError_t launch3_seed_bwd(const Problem3 &P, const Search3 &S, hipStream_t s);
 hipError_t launch3_collect(const Problem3 &P, unsigned long long *keys, int32_t *slots,
                            uint32_t *count, uint32_t cap, uint32_t *overflow, hipStream_t s);

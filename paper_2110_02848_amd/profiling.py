@@ -58,8 +58,8 @@ FAMILIES = {
                 "k_scatter_final("),
     # three inputs at once (bench.py --task compose3)
     "search3": ("k3_fwd(", "k3_fwd_chunks(", "k3_bwd(", "k3_bwd_chunks("),
-    "compact3": ("k3_indeg(", "k3_place(", "k3_seed_bwd(", "k3_collect(", "k3_ids(",
-                 "k3_count(", "k3_fill(", "k3_fill_states("),
+    "compact3": ("k3_arc_keys(", "k3_run_starts(", "k3_run_ends(", "k3_seed_bwd(", "k3_collect(", "k3_ids(",
+                 "k3_out_light<", "k3_out_heavy<", "k3_fill_states("),
 }
 
 # Counters of each pass (what one rocprofv3 pass can collect on gfx950).
