@@ -72,7 +72,7 @@ struct fst_ctx {
   // three-input composition
   DevBuf t_scal, t_aPerm, t_aArc, t_aRec, t_bPerm, t_bArc, t_bRec, t_bLab, t_bW, t_dPerm,
       t_dArc, t_dRec, t_dLab, t_dW, t_bflags, t_lists, t_tab, t_F, t_chunks, t_arcs, t_inoff,
-      t_cursor, t_coacc, t_keys0, t_keys1, t_slots0, t_slots1, t_idof, t_units, t_ucnt,
+      t_first, t_coacc, t_keys0, t_keys1, t_slots0, t_slots1, t_idof, t_units, t_ucnt,
       t_aLab, t_aW, t_heavy, t_aLut, t_bLut, t_dLut;
   Scal3 *h_s3 = nullptr;
   uint32_t h3_hint = 0;  // hash capacity the last three-input search needed
@@ -1069,7 +1069,7 @@ int compose3_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, const fst_
   // backward search over the generated arcs, grouped by target (sorted)
   tout.begin(s);
   FST_TRY(ensure(c, c->t_inoff, (H + 1) * 4));
-  FST_TRY(ensure(c, c->t_cursor, H * 4));
+  FST_TRY(ensure(c, c->t_first, H * 4));
   FST_TRY(ensure(c, c->k0, (narcs + 1) * 8));
   FST_TRY(ensure(c, c->k1, (narcs + 1) * 8));
   FST_TRY(ensure(c, c->v0, (narcs + 1) * 4));
@@ -1090,7 +1090,7 @@ int compose3_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, const fst_
                        as<unsigned long long>(c->k1), as<int32_t>(c->v1), narcs,
                        bitlen(H - 1) > 0 ? bitlen(H - 1) : 1, c->sort_tmp.p, s, &in_second));
   const unsigned long long *tkey = as<unsigned long long>(in_second ? c->k1 : c->k0);
-  HIP_TRY(launch3_in_degrees(tkey, narcs, as<uint32_t>(c->t_cursor), inoff, s));
+  HIP_TRY(launch3_in_degrees(tkey, narcs, as<uint32_t>(c->t_first), inoff, s));
   HIP_TRY(scan_u32(inoff, inoff, H, true, &d3->total, c->scan_tmp.p, s));
   HIP_TRY(hipMemsetAsync(c->t_coacc.p, 0, (H / 32 + 1) * 4, s));
   HIP_TRY(hipMemsetAsync(&d3->overflow, 0, offsetof(Scal3, ring) - offsetof(Scal3, overflow) +
@@ -1535,7 +1535,7 @@ void fst_ctx_destroy(fst_ctx *c) {
                     &c->t_aRec,   &c->t_bPerm,  &c->t_bArc,  &c->t_bRec,  &c->t_bLab,
                     &c->t_bW,     &c->t_dPerm,  &c->t_dArc,  &c->t_dRec,  &c->t_dLab,
                     &c->t_dW,     &c->t_bflags, &c->t_lists, &c->t_tab,   &c->t_F,
-                    &c->t_chunks, &c->t_arcs,   &c->t_inoff, &c->t_cursor,
+                    &c->t_chunks, &c->t_arcs,   &c->t_inoff, &c->t_first,
                     &c->t_coacc,  &c->t_keys0,  &c->t_keys1, &c->t_slots0, &c->t_slots1,
                     &c->t_idof,   &c->t_units,  &c->t_ucnt,  &c->t_aLab,  &c->t_aW,
                     &c->t_heavy,  &c->t_aLut,   &c->t_bLut,  &c->t_dLut};

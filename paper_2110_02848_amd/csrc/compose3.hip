@@ -38,7 +38,7 @@
 // (source slot, target slot) is appended to an arc list, and new keys to
 // the next frontier, one atomic per wavefront.
 // Co-accessibility runs backwards over that arc list (in-arcs grouped by a
-// count, a scan and a placement).  The trim keys are sorted (radix sort of
+// radix sort of the arcs by target, their run boundaries and a scan).  The trim keys are sorted (radix sort of
 // the 64-bit keys): a state's id is its rank.  Count and fill give a state
 // with at most LIGHT3 units one thread and a heavier one a workgroup (its
 // threads take its units in turn); per-unit counts are scanned into every
