@@ -604,8 +604,13 @@ __device__ void gen_body(const ScoreArgs &S, int g, unsigned bid, unsigned nb) {
     if (next >= 0) walk_from<FWD>(S, nx, next, next_rec, next_val, 1, fin, &pd);
     settle_block<FWD>(S, nx, pd);
   }
+  // light states start at the workgroups with the fewest heavy units (the
+  // heavy units went to workgroups 0, 1, ... in turn), so walks cut short
+  // by the depth budget resume beside the heavy work, not behind it
   const ull n = cur.qcount;
-  for (ull i = (ull)bid * NT + threadIdx.x; i < n; i += (ull)nb * NT) {
+  const unsigned hrem = (unsigned)(HB % nb);
+  const unsigned lb = bid >= hrem ? bid - hrem : bid + nb - hrem;
+  for (ull i = (ull)lb * NT + threadIdx.x; i < n; i += (ull)nb * NT) {
     const int32_t v = S.Q[cur.qbase + (uint32_t)i];
     const int4 rv = S.rec[v];
     const double x =
