@@ -73,7 +73,7 @@ struct fst_ctx {
   DevBuf t_scal, t_aPerm, t_aArc, t_aRec, t_bPerm, t_bArc, t_bRec, t_bLab, t_bW, t_dPerm,
       t_dArc, t_dRec, t_dLab, t_dW, t_bflags, t_lists, t_tab, t_F, t_chunks, t_arcs, t_inoff,
       t_first, t_coacc, t_keys0, t_keys1, t_slots0, t_slots1, t_idof, t_units, t_ucnt,
-      t_aLab, t_aW, t_heavy, t_aLut, t_bLut, t_dLut;
+      t_aLab, t_aW, t_heavy, t_aLut, t_bLut, t_dLut, t_bChain;
   Scal3 *h_s3 = nullptr;
   uint32_t h3_hint = 0;  // hash capacity the last three-input search needed
   int lv3_hint[2] = {0, 0};  // levels the last three-input searches took (bwd, fwd)
@@ -1008,6 +1008,13 @@ int compose3_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, const fst_
                 &c->t_bLab, &c->t_bW, c->t_bLut, P.bOut, s));
   FST_TRY(view3(c, dD, 1, !(v.errD & info), v.maxD, c->t_dPerm, c->t_dArc, c->t_dRec,
                 &c->t_dLab, &c->t_dW, c->t_dLut, P.dOut, s));
+  // chain records of B for the search's chain jumps (which look up A's
+  // buckets: only with A's bucket table)
+  if (P.aOut.lut) {
+    FST_TRY(ensure(c, c->t_bChain, (size_t)dB.V * CHAIN_INT4 * sizeof(int4)));
+    P.bOut.chain = as<int4>(c->t_bChain);
+    HIP_TRY(launch3_chains(P.bOut, dB.V, as<int4>(c->t_bChain), s));
+  }
   FST_TRY(ensure(c, c->t_bflags, (size_t)dB.V * 4));
   HIP_TRY(hipMemsetAsync(c->t_bflags.p, 0, (size_t)dB.V * 4, s));
   HIP_TRY(launch3_bflags(dB, as<uint32_t>(c->t_bflags), s));
@@ -1538,7 +1545,7 @@ void fst_ctx_destroy(fst_ctx *c) {
                     &c->t_chunks, &c->t_arcs,   &c->t_inoff, &c->t_first,
                     &c->t_coacc,  &c->t_keys0,  &c->t_keys1, &c->t_slots0, &c->t_slots1,
                     &c->t_idof,   &c->t_units,  &c->t_ucnt,  &c->t_aLab,  &c->t_aW,
-                    &c->t_heavy,  &c->t_aLut,   &c->t_bLut,  &c->t_dLut};
+                    &c->t_heavy,  &c->t_aLut,   &c->t_bLut,  &c->t_dLut, &c->t_bChain};
   for (DevBuf *b : bufs) release(*b);
   for (ScoreBufs *sb : {&c->score_f, &c->score_b}) {
     for (DevBuf *b : {&sb->sc, &sb->rec, &sb->term, &sb->mkey, &sb->pend, &sb->q, &sb->h,

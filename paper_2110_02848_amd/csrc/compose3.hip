@@ -351,7 +351,8 @@ __global__ __launch_bounds__(NT) void k3_bflags(DevGraph B, uint32_t *bflags) {
 }
 
 // Bucket table of a view: lut[v * stride + l] = {first position of label
-// l in group v, first position past it, 0, 0}.
+// l in group v, first position past it, the first arc's neighbour field
+// (0 for an empty bucket), 0}.
 __global__ __launch_bounds__(NT) void k3_lut(View v, long long nstates) {
   const long long n = nstates * v.lstride;
   int4 *lut = const_cast<int4 *>(v.lut);
@@ -371,7 +372,40 @@ __global__ __launch_bounds__(NT) void k3_lut(View v, long long nstates) {
       const int32_t mid = a + ((b - a) >> 1);
       if (v.arec[mid].x <= l) a = mid + 1; else b = mid;
     }
-    lut[x] = make_int4(lo, a, 0, 0);
+    lut[x] = make_int4(lo, a, lo < a ? v.arec[lo].y : 0, 0);
+  }
+}
+
+// Chain records of B's out-view for the chain jumps of the search: per
+// state, up to CHAIN_STEPS steps {n, l0, s0, l1, s1, ...} (CHAIN_INT4
+// int4), where step i follows the only arc of the state reached after i
+// steps, an arc with input label l_i != epsilon and output epsilon, to s_i.
+__global__ __launch_bounds__(NT) void k3_chains(View v, long long nstates, int4 *chain) {
+  for (long long q = (long long)blockIdx.x * NT + threadIdx.x; q < nstates;
+       q += (long long)gridDim.x * NT) {
+    int32_t w[4 * CHAIN_INT4] = {};
+    int n = 0;
+    uint32_t cur = (uint32_t)q;
+#pragma unroll
+    for (int k = 0; k < CHAIN_STEPS; ++k) {
+      if (n == k) {
+        const int4 r = v.srec[2 * (size_t)cur];
+        const bool one = r.z - r.x == 1;
+        const int2 a = one ? v.arec[r.x] : make_int2(0, 0);
+        const int32_t ol = one ? v.olab[r.x] : 1;
+        if (one && a.x != 0 && ol == 0) {
+          w[1 + 2 * k] = a.x;
+          w[2 + 2 * k] = (int32_t)nbr_of_arc(a.y);
+          cur = nbr_of_arc(a.y);
+          n = k + 1;
+        }
+      }
+    }
+    w[0] = n;
+    int4 *c = chain + CHAIN_INT4 * q;
+#pragma unroll
+    for (int k = 0; k < CHAIN_INT4; ++k)
+      c[k] = make_int4(w[4 * k], w[4 * k + 1], w[4 * k + 2], w[4 * k + 3]);
   }
 }
 
@@ -475,30 +509,256 @@ __device__ __forceinline__ void expand_units(const Problem3 &P, const Search3 &S
     });
 }
 
+// Chain jumps.  A key (qa, qb, f1, qd, 0) whose matching move joins the
+// one arc of qb (input l != epsilon, output epsilon) with the one arc of
+// label l out of qa reaches (qa', qb', 0, qd, 0); along the chain record of
+// qb such moves follow each other as long as every key reached again has
+// that one matching move (no epsilon output at its A state, one arc of the
+// next label).  Beside it a key has at most one more move, the epsilon arc
+// of qd when qd has one (a grammar's backoff): it reaches the side key (qa,
+// qb, f1, d', 1), since the matching move is a T-arc with output epsilon.
+// Hop 0's A bucket is looked up first; the buckets of the later hops (with
+// the epsilon counts of their A states) are then loaded together at A
+// states guessed to continue hop 0's step, and verified in order (a hop
+// whose guessed state was wrong ends the jump).  The keys reached, then the
+// side keys, are inserted together (their groups loaded, then one CAS
+// each; a key that loses its slot takes the general insert).  The moves of
+// the keys this thread inserted, and of the key it started from, are
+// recorded as arcs with one atomic; a key another thread inserted is
+// expanded by that thread, which records its moves.  New side keys join the
+// next frontier.
+constexpr int JUMP3 = 8;  // hops per jump
+
+struct Jump3 {
+  bool done;       // the jump was taken (else the key is expanded as usual)
+  int hops;        // keys reached
+  uint32_t fresh;  // of them, inserted by this thread
+  uint32_t last;   // slot of the last key reached if this thread inserted it, else NO_SLOT
+  ull last_key;
+};
+
+// Slots of keys key[i], i < n, inserted if absent (fr[i]): all groups
+// loaded, then one CAS per key at the first free slot of its group; a key
+// whose group is full or whose slot another key took goes through h_insert.
+// ts[i] = NO_SLOT (and the overflow flag) when the table is full.
+__device__ __forceinline__ void insert_batch(const Problem3 &P, const Search3 &S,
+                                             const ull key[JUMP3], int n,
+                                             uint32_t ts[JUMP3], bool fr[JUMP3]) {
+  uint32_t h[JUMP3], pick[JUMP3];
+  // pick[i]: HGROUP + j when slot j of the first group holds the key, j
+  // when it is the group's first free slot, 2 HGROUP when neither
+#pragma unroll
+  for (int i = 0; i < JUMP3; ++i) {
+    h[i] = (uint32_t)mix64(key[i]) & P.hmask & ~(HGROUP - 1u);
+    pick[i] = 2 * HGROUP;
+    if (i < n) {
+      ull g[HGROUP];
+      load_group(P, h[i], g);
+#pragma unroll
+      for (int j = HGROUP - 1; j >= 0; --j)
+        if (g[j] == EMPTY3) pick[i] = (uint32_t)j;
+#pragma unroll
+      for (int j = HGROUP - 1; j >= 0; --j)
+        if (g[j] == key[i]) pick[i] = HGROUP + (uint32_t)j;
+    }
+  }
+  ull old[JUMP3];
+#pragma unroll
+  for (int i = 0; i < JUMP3; ++i) {
+    old[i] = 0;
+    if (i < n && pick[i] < HGROUP) old[i] = atomicCAS(P.tab + h[i] + pick[i], EMPTY3, key[i]);
+  }
+#pragma unroll
+  for (int i = 0; i < JUMP3; ++i) {
+    ts[i] = NO_SLOT;
+    fr[i] = false;
+    if (i < n) {
+      if (pick[i] >= HGROUP && pick[i] < 2 * HGROUP) {
+        ts[i] = h[i] + pick[i] - HGROUP;
+      } else if (pick[i] < HGROUP && old[i] == EMPTY3) {
+        ts[i] = h[i] + pick[i];
+        fr[i] = true;
+      } else if (pick[i] < HGROUP && old[i] == key[i]) {
+        ts[i] = h[i] + pick[i];
+      } else {
+        ts[i] = h_insert(P, key[i], fr[i], &S.sc->overflow);
+      }
+    }
+  }
+}
+
+__device__ __forceinline__ Jump3 jump3(const Problem3 &P, const Search3 &S, uint32_t slot,
+                                       const Units3 &u, int max_hops, Lvl3 *nx,
+                                       uint32_t nbase) {
+  Jump3 r;
+  r.done = false;
+  const Key3 &k = u.k;
+  if (!P.bOut.chain || !P.aOut.lut || max_hops < 1) return r;
+  if (k.f2 != 0 || u.nae != 0 || u.gb.neps != 0 || u.gd.neps > 1 ||
+      u.gb.end - u.gb.begin != 1)
+    return r;
+  const int4 *cr = P.bOut.chain + CHAIN_INT4 * (size_t)k.qb;
+  int32_t cw[4 * CHAIN_INT4];
+#pragma unroll
+  for (int q = 0; q < CHAIN_INT4; ++q) {
+    const int4 c = cr[q];
+    cw[4 * q] = c.x;
+    cw[4 * q + 1] = c.y;
+    cw[4 * q + 2] = c.z;
+    cw[4 * q + 3] = c.w;
+  }
+  // the target of qd's epsilon arc, if it has one
+  const bool side = u.gd.neps == 1;
+  const uint32_t dd = side ? nbr_of_arc(P.dOut.arec[u.gd.begin].y) : 0u;
+  int n = cw[0];
+  if (n > max_hops) n = max_hops;
+  if (n > JUMP3) n = JUMP3;
+  const uint32_t stride = (uint32_t)P.aOut.lstride, VA = (uint32_t)P.A.V;
+  if (n < 1 || (uint32_t)cw[1] >= stride) return r;
+  const int4 *lut = P.aOut.lut;
+  const int4 b0 = lut[(size_t)k.qa * stride + (uint32_t)cw[1]];
+  if (b0.y - b0.x != 1) return r;
+  uint32_t qa[JUMP3 + 1];  // A state of the key reached after i hops, i <= m
+  qa[0] = k.qa;
+  qa[1] = nbr_of_arc(b0.z);
+  const uint32_t step = qa[1] - qa[0];  // modulo 2^32
+  int4 bk[JUMP3];
+  int32_t ek[JUMP3];
+#pragma unroll
+  for (int i = 1; i < JUMP3; ++i) {
+    const uint32_t g = qa[0] + (uint32_t)i * step;
+    const uint32_t lab = (uint32_t)cw[1 + 2 * i];
+    bk[i] = make_int4(0, 0, 0, 0);
+    ek[i] = 1;
+    if (i < n && g < VA && lab < stride) {
+      bk[i] = lut[(size_t)g * stride + lab];
+      ek[i] = P.aOut.srec[2 * (size_t)g].y;
+    }
+  }
+  int m = 1;  // hops taken
+#pragma unroll
+  for (int i = 1; i < JUMP3; ++i)
+    if (m == i && i < n && qa[0] + (uint32_t)i * step == qa[i] && bk[i].y - bk[i].x == 1 &&
+        ek[i] == 0) {
+      qa[i + 1] = nbr_of_arc(bk[i].z);
+      m = i + 1;
+    }
+  // the keys reached, (qa[i + 1], s_i, 0, qd, 0) for i < m
+  ull key[JUMP3];
+#pragma unroll
+  for (int i = 0; i < JUMP3; ++i)
+    key[i] = pack3(P, qa[i + 1 <= m ? i + 1 : m], (uint32_t)cw[2 + 2 * i], 0, k.qd, 0);
+  uint32_t ts[JUMP3];
+  bool fr[JUMP3];
+  insert_batch(P, S, key, m, ts, fr);
+  // the side keys of the hops' sources, (qa[i], s_(i-1) (qb for i = 0),
+  // f1 of the source, d', 1) for i < m
+  ull skey[JUMP3];
+  uint32_t sts[JUMP3];
+  bool sfr[JUMP3];
+#pragma unroll
+  for (int i = 0; i < JUMP3; ++i)
+    skey[i] = pack3(P, qa[i <= m ? i : m], i == 0 ? k.qb : (uint32_t)cw[2 * i],
+                    i == 0 ? k.f1 : 0u, dd, 1);
+  insert_batch(P, S, skey, side ? m : 0, sts, sfr);
+  r.done = true;
+  r.hops = m;
+  r.fresh = 0;
+  r.last = NO_SLOT;
+  r.last_key = 0;
+  bool full = false;
+#pragma unroll
+  for (int i = 0; i < JUMP3; ++i)
+    if (i < m) {
+      full = full || ts[i] == NO_SLOT || (side && sts[i] == NO_SLOT);
+      r.fresh += fr[i] ? 1u : 0u;
+    }
+  if (full) return r;  // the table is full: the search starts again
+  // the moves of the hops' sources this thread owns: the start key, and
+  // the keys it inserted before the last
+  bool own[JUMP3];
+  uint32_t nown = 0, nside = 0;
+#pragma unroll
+  for (int i = 0; i < JUMP3; ++i) {
+    own[i] = i < m && (i == 0 || fr[i - 1]);
+    nown += own[i] ? 1u : 0u;
+    nside += (i < m && side && sfr[i]) ? 1u : 0u;
+  }
+  const uint32_t per = side ? 2u : 1u;
+  const ull base = atomicAdd(&S.sc->narcs, nown * per);
+  uint32_t o = 0;
+#pragma unroll
+  for (int i = 0; i < JUMP3; ++i)
+    if (own[i]) {
+      const uint32_t src = i == 0 ? slot : ts[i - 1];
+      if (base + o + per <= S.acap) {
+        S.arcs[base + o] = make_uint2(src, ts[i]);
+        if (side) S.arcs[base + o + 1] = make_uint2(src, sts[i]);
+      } else {
+        atomicOr(&S.sc->overflow, 1u);
+      }
+      o += per;
+    }
+  // new side keys join the next frontier
+  if (nside) {
+    const uint32_t fb = atomicAdd(&nx->fcount, nside);
+    uint32_t q = 0;
+#pragma unroll
+    for (int i = 0; i < JUMP3; ++i)
+      if (i < m && side && sfr[i]) {
+        const ull pos = (ull)fb + q;
+        if (pos < (ull)S.fcap - nbase) S.F[nbase + pos] = sts[i];
+        else atomicOr(&S.sc->overflow, 1u);
+        ++q;
+      }
+  }
+  // the last key goes on the walk if this thread inserted it
+#pragma unroll
+  for (int i = 0; i < JUMP3; ++i)
+    if (i + 1 == m && fr[i]) {
+      r.last_key = key[i];
+      r.last = ts[i];
+    }
+  return r;
+}
+
 // A thread's depth-first walk from `key` (in `slot`): a key with at most
-// WALK3 units is expanded at once and the walk goes on with the first new
-// key it reached (up to CHAIN3 keys); a heavier key is cut into chunks for
-// the chunk list `heavy_to`.  Every other new key joins the next frontier.
-// Returns the number of keys the walk went on to.
+// WALK3 units is expanded at once (a chain of one-move keys by a jump) and
+// the walk goes on with the first new key it reached (up to CHAIN3 keys); a
+// heavier key is cut into chunks for the chunk list `heavy_to`.  Every
+// other new key joins the next frontier.  Returns the number of keys the
+// walk inserted and did not put in a frontier.
 __device__ __forceinline__ uint32_t walk_fwd(const Problem3 &P, const Search3 &S, uint32_t slot,
                                              ull key, Lvl3 *nx, uint32_t nbase, Lvl3 *heavy_to,
                                              int heavy_l) {
+  uint32_t went = 0;
   for (int depth = 0; depth < CHAIN3; ++depth) {
     const Units3 u = units_of(P, key);
     const uint32_t n = nunits(u);
     if (n > WALK3) {
       push_chunks(S, heavy_to, heavy_l, slot, n);
-      return (uint32_t)depth;
+      return went;
+    }
+    // the key reached last must still be expanded within the budget
+    const Jump3 j = jump3(P, S, slot, u, CHAIN3 - 1 - depth, nx, nbase);
+    if (j.done) {
+      went += j.fresh;
+      if (j.last == NO_SLOT) return went;
+      depth += j.hops - 1;
+      slot = j.last;
+      key = j.last_key;
+      continue;
     }
     uint32_t cont = NO_SLOT;
     ull cont_key = 0;
     expand_units(P, S, slot, u, 0, n, nx, nbase, depth + 1 < CHAIN3 ? &cont : nullptr,
                  &cont_key);
-    if (cont == NO_SLOT) return (uint32_t)depth;
+    if (cont == NO_SLOT) return went;
+    ++went;
     slot = cont;
     key = cont_key;
   }
-  return CHAIN3 - 1;
+  return went;
 }
 
 // Level l of the forward search: frontier entries [fbase, fbase + fcount)
@@ -878,6 +1138,11 @@ hipError_t launch3_in_degrees(const unsigned long long *key, unsigned long long 
   if (!narcs) return hipSuccess;
   k3_run_starts<<<grid3((size_t)narcs), NT, 0, s>>>(key, narcs, first);
   k3_run_ends<<<grid3((size_t)narcs), NT, 0, s>>>(key, narcs, first, indeg);
+  return hipGetLastError();
+}
+
+hipError_t launch3_chains(const View &v, long long nstates, int4 *chain, hipStream_t s) {
+  if (nstates > 0) k3_chains<<<grid3((size_t)nstates), NT, 0, s>>>(v, nstates, chain);
   return hipGetLastError();
 }
 

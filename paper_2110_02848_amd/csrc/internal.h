@@ -541,6 +541,9 @@ hipError_t launch3_bflags(const DevGraph &B, uint32_t *bflags, hipStream_t s);
 // Bucket table of a view (v.lut with v.lstride labels per state) from its
 // records and arcs.
 hipError_t launch3_lut(const View &v, long long nstates, hipStream_t s);
+// Chain records (CHAIN_INT4 int4 per state) of B's out-view for the chain
+// jumps of the forward search.
+hipError_t launch3_chains(const View &v, long long nstates, int4 *chain, hipStream_t s);
 // Start keys of every triple of start states (lists and counts from
 // launch3_starts) into level 0 of S.
 hipError_t launch3_starts(const DevGraph &A, const DevGraph &B, const DevGraph &D,

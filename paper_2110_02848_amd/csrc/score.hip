@@ -402,12 +402,14 @@ __device__ __forceinline__ void walk_from(const ScoreArgs &S, const ScoreNext &n
   Pending p;
   p.y = -1;
   for (;;) {
-    S.val[v] = x;
-    ++fin;
     const int32_t nd = rec_count(rv);
     if (nd == 1) {
       const int32_t y = rv.x;
       const int4 ry = S.rec[y];
+      // v's value is stored after the load of y's record is issued (a wait
+      // for a load also waits for every store issued before it)
+      S.val[v] = x;
+      ++fin;
       const float w = __int_as_float(rv.z);
       const uint32_t fy = rec_flags(ry);
       if ((fy & REC_SINGLE) && !(fy & REC_HEAVY) && depth + 1 < S.chain) {
@@ -428,6 +430,8 @@ __device__ __forceinline__ void walk_from(const ScoreArgs &S, const ScoreNext &n
       p.x = x;
       break;
     }
+    S.val[v] = x;
+    ++fin;
     int32_t next = -1;
     double next_val = 0.0;
     int4 next_rec = rv;
