@@ -465,3 +465,14 @@ def wide_fanout_pair(rng, fan=(300, 255, 254), n_mid=300, n_gap=5):
 def synth_from_arcs(V, arcs, start, accept):
     from paper_2110_02848_amd import synth
     return synth.from_arcs(V, arcs, start=start, accept=accept)
+
+
+def renumber(g, perm):
+    """The same graph with state s renamed perm[s] (arcs keep their order
+    within a state)."""
+    perm = np.asarray(perm, dtype=np.int64)
+    arcs = [(int(perm[s]), int(perm[d]), int(i), int(o), float(w))
+            for s, d, i, o, w in zip(g["src"], g["dst"], g["ilabel"], g["olabel"], g["weight"])]
+    return synth_from_arcs(g["num_states"], arcs,
+                           start=[int(perm[v]) for v in np.flatnonzero(g["start"])],
+                           accept=[int(perm[v]) for v in np.flatnonzero(g["accept"])])

@@ -101,6 +101,28 @@ def test_hub_states_and_epsilon_inputs_everywhere(comp):
     assert not fsthelp.check_invariants3(A, B, D, got)
 
 
+@pytest.mark.parametrize("mode", ["plain", "A shuffled", "A reversed", "B shuffled"])
+def test_chain_jumps(comp, mode):
+    """Words longer than one chain jump (9 to 14 letters), a backoff at
+    every grammar state but the start (every hop has a side move), and
+    renumbered emissions or lexicon states (the jump's guessed A states
+    miss and it ends early, or B's chains are scattered).  Besides the
+    result, the accessible and generated counts equal the oracle's: every
+    move is recorded exactly once."""
+    spec = synth.GrammarSpec(30, 6, 120, 9, 14, 4, 60, 1.0, 0.5)
+    A, B, D, _ = synth.emissions_lexicon_grammar("grammar-T40-W300-G6", 5, spec=spec)
+    rng = np.random.default_rng([913, len(mode)])
+    if mode == "A shuffled":
+        A = fsthelp.renumber(A, rng.permutation(A["num_states"]))
+    if mode == "A reversed":
+        A = fsthelp.renumber(A, np.arange(A["num_states"])[::-1])
+    if mode == "B shuffled":
+        B = fsthelp.renumber(B, rng.permutation(B["num_states"]))
+    got = check3(comp, A, B, D, f"chain jumps ({mode})")
+    assert got["num_states"] > 0
+    assert not fsthelp.check_invariants3(A, B, D, got)
+
+
 def test_equal_to_chained_when_d_has_no_epsilon_input(comp):
     import test_oracle_compose3 as t3
     rng = np.random.default_rng(912)

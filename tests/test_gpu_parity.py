@@ -270,17 +270,6 @@ def test_chain_jump_conditions(comp, seed):
     assert not fsthelp.check_invariants(A, B, got)
 
 
-def _renumber(g, perm):
-    """The same graph with state s renamed perm[s] (arcs keep their order
-    within a state)."""
-    perm = np.asarray(perm, dtype=np.int64)
-    arcs = [(int(perm[s]), int(perm[d]), int(i), int(o), float(w))
-            for s, d, i, o, w in zip(g["src"], g["dst"], g["ilabel"], g["olabel"], g["weight"])]
-    return synth.from_arcs(g["num_states"], arcs,
-                           start=[int(perm[v]) for v in np.flatnonzero(g["start"])],
-                           accept=[int(perm[v]) for v in np.flatnonzero(g["accept"])])
-
-
 @pytest.mark.parametrize("mode", ["A shuffled", "A reversed", "B shuffled", "both shuffled"])
 @pytest.mark.parametrize("seed", range(2))
 def test_renumbered_states(comp, mode, seed):
@@ -293,11 +282,11 @@ def test_renumbered_states(comp, mode, seed):
     A, B, _ = synth.emissions_lexicon("lexicon-T100-W1000", seed, spec=spec)
     rng = np.random.default_rng([17, seed])
     if mode in ("A shuffled", "both shuffled"):
-        A = _renumber(A, rng.permutation(A["num_states"]))
+        A = fsthelp.renumber(A, rng.permutation(A["num_states"]))
     if mode == "A reversed":
-        A = _renumber(A, np.arange(A["num_states"])[::-1])
+        A = fsthelp.renumber(A, np.arange(A["num_states"])[::-1])
     if mode in ("B shuffled", "both shuffled"):
-        B = _renumber(B, rng.permutation(B["num_states"]))
+        B = fsthelp.renumber(B, rng.permutation(B["num_states"]))
     got, _ = check_pair(comp, A, B, f"renumbered states ({mode}) seed {seed}")
     assert got["num_arcs"] > 0
     assert not fsthelp.check_invariants(A, B, got)
