@@ -1026,7 +1026,8 @@ int compose3_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, const fst_
   uint32_t *counts = reinterpret_cast<uint32_t *>(lists + dA.V + dB.V + dD.V);
 
   // forward search; a table that fills up (or lists that overflow) is
-  // grown four-fold and the search starts again
+  // grown two-fold and the search starts again (the later passes scan the
+  // whole table: a smaller one pays off more than the longer first call)
   const KernelTimer tout = timer(c, FST_KERNEL_COMPACT3);
   unsigned long long H = c->h3_hint ? c->h3_hint : (1ull << 20);
   Search3 S = {};
@@ -1058,7 +1059,7 @@ int compose3_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, const fst_
     // in the first group of four slots they probe)
     FST_TRY(levels3(c, P, S, true, (uint32_t)(H / 2), &done, s));
     if (done) break;
-    H *= 4;
+    H *= 2;
   }
   c->h3_hint = (uint32_t)H;
   const Scal3 f = *c->h_s3;
