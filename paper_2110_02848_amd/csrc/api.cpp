@@ -729,11 +729,17 @@ int run_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, hipStream_t s, 
       tf.begin(s);
       for (int g = 0; g < FIRST; ++g) HIP_TRY(launch_generation(P, S, true, g, s));
       tf.end(s);
-      FST_TRY(readback(c, s));
-      FST_TRY(add_time(c, FST_KERNEL_SEARCH_FORWARD, FIRST));
-      if (c->h_sc->overflow) return FST_ERR_TOO_LARGE;
-      const GenSlot &nf = c->h_sc->G[FIRST % 3];
-      if (nf.qcount == 0 && (uint32_t)nf.hpack == 0) {
+      // with no generation run alone there is nothing to read back yet (an
+      // empty forward search ends in the concurrent loop as well)
+      bool fwd_over = false;
+      if (FIRST > 0) {
+        FST_TRY(readback(c, s));
+        FST_TRY(add_time(c, FST_KERNEL_SEARCH_FORWARD, FIRST));
+        if (c->h_sc->overflow) return FST_ERR_TOO_LARGE;
+        const GenSlot &nf = c->h_sc->G[FIRST % 3];
+        fwd_over = nf.qcount == 0 && (uint32_t)nf.hpack == 0;
+      }
+      if (fwd_over) {
         c->stats.fwd_levels = c->h_sc->gens;
         HIP_TRY(launch_popcount(P.vis, snwords, &d_sc->naccessible, s));
         if (c->count_moves) HIP_TRY(launch_count_moves(P, snwords, true, &d_sc->generated, s));
