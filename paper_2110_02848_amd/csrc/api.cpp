@@ -73,7 +73,7 @@ struct fst_ctx {
   DevBuf t_scal, t_aPerm, t_aArc, t_aRec, t_bPerm, t_bArc, t_bRec, t_bLab, t_bW, t_dPerm,
       t_dArc, t_dRec, t_dLab, t_dW, t_bflags, t_lists, t_tab, t_F, t_chunks, t_arcs, t_inoff,
       t_first, t_coacc, t_keys0, t_keys1, t_slots0, t_slots1, t_idof, t_units, t_ucnt,
-      t_aLab, t_aW, t_heavy, t_aLut, t_bLut, t_dLut, t_bChain;
+      t_aLab, t_aW, t_heavy, t_aLut, t_bLut, t_dLut, t_bChain, t_segs, t_segof;
   Scal3 *h_s3 = nullptr;
   uint32_t h3_hint = 0;  // hash capacity the last three-input search needed
   int lv3_hint[2] = {0, 0};  // levels the last three-input searches took (bwd, fwd)
@@ -1057,6 +1057,18 @@ int compose3_impl(fst_ctx *c, const fst_graph *A, const fst_graph *B, const fst_
     S.arcs = as<uint2>(c->t_arcs);
     S.acap = acap;
     S.ring = d3->ring;
+    // chain segments of the jumps for the backward search (a quarter of the
+    // table's size, below 2^28 so that seg_of packs the index with the
+    // length; jumps past that record none)
+    if (P.bOut.chain) {
+      const unsigned long long scap = H / 4 < (1ull << 28) ? H / 4 : (1ull << 28) - 1;
+      FST_TRY(ensure(c, c->t_segof, H * 4));
+      FST_TRY(ensure(c, c->t_segs, scap * 32));
+      HIP_TRY(hipMemsetAsync(c->t_segof.p, 0xff, H * 4, s));
+      S.segs = as<uint32_t>(c->t_segs);
+      S.seg_of = as<uint32_t>(c->t_segof);
+      S.scap = (uint32_t)scap;
+    }
     S.sc = d3;
     HIP_TRY(launch3_starts(dA, dB, dD, lists, counts, s));
     HIP_TRY(launch3_seed(P, S, lists, counts, s));
@@ -1552,7 +1564,8 @@ void fst_ctx_destroy(fst_ctx *c) {
                     &c->t_chunks, &c->t_arcs,   &c->t_inoff, &c->t_first,
                     &c->t_coacc,  &c->t_keys0,  &c->t_keys1, &c->t_slots0, &c->t_slots1,
                     &c->t_idof,   &c->t_units,  &c->t_ucnt,  &c->t_aLab,  &c->t_aW,
-                    &c->t_heavy,  &c->t_aLut,   &c->t_bLut,  &c->t_dLut, &c->t_bChain};
+                    &c->t_heavy,  &c->t_aLut,   &c->t_bLut,  &c->t_dLut, &c->t_bChain,
+                    &c->t_segs,   &c->t_segof};
   for (DevBuf *b : bufs) release(*b);
   for (ScoreBufs *sb : {&c->score_f, &c->score_b}) {
     for (DevBuf *b : {&sb->sc, &sb->rec, &sb->term, &sb->mkey, &sb->pend, &sb->q, &sb->h,

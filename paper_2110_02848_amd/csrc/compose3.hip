@@ -643,6 +643,9 @@ __device__ __forceinline__ Jump3 jump3(const Problem3 &P, const Search3 &S, uint
       qa[i + 1] = nbr_of_arc(bk[i].z);
       m = i + 1;
     }
+  // a segment of the keys that lead to the last one (its slot taken now,
+  // so the atomic returns during the inserts)
+  const uint32_t sidx = (S.segs && m >= 2) ? atomicAdd(&S.sc->nseg, 1u) : NO_SLOT;
   // the keys reached, (qa[i + 1], s_i, 0, qd, 0) for i < m
   ull key[JUMP3];
 #pragma unroll
@@ -699,6 +702,15 @@ __device__ __forceinline__ Jump3 jump3(const Problem3 &P, const Search3 &S, uint
       }
       o += per;
     }
+  if (sidx < S.scap) {
+    uint32_t *sg = S.segs + 8 * (size_t)sidx;
+#pragma unroll
+    for (int i = 0; i < JUMP3; ++i)
+      if (i < m) sg[i] = i == 0 ? slot : ts[i - 1];
+#pragma unroll
+    for (int i = 0; i < JUMP3; ++i)
+      if (i + 1 == m) S.seg_of[ts[i]] = sidx << 4 | (uint32_t)m;
+  }
   // new side keys join the next frontier
   if (nside) {
     const uint32_t fb = atomicAdd(&nx->fcount, nside);
@@ -878,22 +890,74 @@ __device__ __forceinline__ void bwd_range(const Problem3 &P, const Search3 &S, u
   }
 }
 
-// Depth-first backward walk from slot v (as walk_fwd, over in-arcs).
+// A slot into the next frontier (one atomic).
+__device__ __forceinline__ void push_one(const Search3 &S, Lvl3 *nx, uint32_t nbase, uint32_t u) {
+  const uint32_t pos = atomicAdd(&nx->fcount, 1u);
+  if ((ull)pos < (ull)S.fcap - nbase) S.F[nbase + pos] = u;
+  else atomicOr(&S.sc->overflow, 1u);
+}
+
+// The keys of chain segment sg (see Search3), which lead to a key found
+// co-accessible, are claimed together (their bitmap words loaded, then one
+// atomic each for the unclaimed).  A newly claimed key other than the first
+// that has in-arcs besides the one from its predecessor on the segment
+// joins the next frontier (its in-arcs are walked from there); the first
+// key, if newly claimed, is returned to walk on from (cont allowed) or
+// joins the next frontier.  *went counts the claimed keys not put in a
+// frontier.
+__device__ __forceinline__ uint32_t claim_segment(const Problem3 &P, const Search3 &S,
+                                                  uint32_t sg, Lvl3 *nx, uint32_t nbase,
+                                                  bool cont, uint32_t *went) {
+  const uint32_t n = sg & 15u;
+  const uint32_t *seg = S.segs + 8 * (size_t)(sg >> 4);
+  uint32_t u[JUMP3], w[JUMP3];
+#pragma unroll
+  for (int j = 0; j < JUMP3; ++j) u[j] = (uint32_t)j < n ? seg[j] : 0u;
+#pragma unroll
+  for (int j = 0; j < JUMP3; ++j) w[j] = (uint32_t)j < n ? P.coacc[u[j] >> 5] : ~0u;
+  bool fr[JUMP3];
+#pragma unroll
+  for (int j = 0; j < JUMP3; ++j) {
+    const uint32_t bit = 1u << (u[j] & 31u);
+    fr[j] = (uint32_t)j < n && !(w[j] & bit) && (atomicOr(P.coacc + (u[j] >> 5), bit) & bit) == 0;
+  }
+  uint32_t d[JUMP3];
+#pragma unroll
+  for (int j = 1; j < JUMP3; ++j) d[j] = fr[j] ? P.in_off[u[j] + 1] - P.in_off[u[j]] : 1u;
+#pragma unroll
+  for (int j = 1; j < JUMP3; ++j)
+    if (fr[j]) {
+      if (d[j] != 1u) push_one(S, nx, nbase, u[j]);
+      else ++*went;
+    }
+  if (!fr[0]) return NO_SLOT;
+  if (cont) return u[0];
+  push_one(S, nx, nbase, u[0]);
+  return NO_SLOT;
+}
+
+// Depth-first backward walk from slot v (as walk_fwd, over in-arcs; a key
+// that ends a chain segment has the segment's keys claimed first).
 __device__ __forceinline__ uint32_t walk_bwd(const Problem3 &P, const Search3 &S, uint32_t v,
                                              Lvl3 *nx, uint32_t nbase, Lvl3 *heavy_to,
                                              int heavy_l) {
+  uint32_t went = 0;
   for (int depth = 0; depth < CHAIN3; ++depth) {
     const uint32_t p0 = P.in_off[v], p1 = P.in_off[v + 1];
-    if (p1 - p0 > WALK3) {
-      push_chunks(S, heavy_to, heavy_l, v, p1 - p0);
-      return (uint32_t)depth;
-    }
+    const uint32_t sg = S.seg_of ? S.seg_of[v] : NO_SLOT;
     uint32_t cont = NO_SLOT;
+    if (sg != NO_SLOT) cont = claim_segment(P, S, sg, nx, nbase, depth + 1 < CHAIN3, &went);
+    if (p1 - p0 > WALK3) {
+      if (cont != NO_SLOT) push_one(S, nx, nbase, cont);
+      push_chunks(S, heavy_to, heavy_l, v, p1 - p0);
+      return went;
+    }
     bwd_range(P, S, p0, p1, nx, nbase, depth + 1 < CHAIN3 ? &cont : nullptr);
-    if (cont == NO_SLOT) return (uint32_t)depth;
+    if (cont == NO_SLOT) return went;
+    ++went;
     v = cont;
   }
-  return CHAIN3 - 1;
+  return went;
 }
 
 __global__ __launch_bounds__(NT) void k3_bwd(Problem3 P, Search3 S, int l) {

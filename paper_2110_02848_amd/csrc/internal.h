@@ -217,7 +217,8 @@ struct Lvl3 {
 struct Scal3 {
   uint32_t errA, errB, errD, maxA, maxB, maxD;
   uint32_t overflow, levels, narcs, ntrim;
-  uint32_t ncont, pad;       // keys a search walk went on to (not in the frontier)
+  uint32_t ncont;            // keys a search walk went on to (not in the frontier)
+  uint32_t nseg;             // chain segments the forward jumps recorded
   uint32_t nheavy[2];        // heavy states of C (and an overflow word)
   unsigned long long total;  // scan totals
   Lvl3 ring[3];
@@ -232,6 +233,13 @@ struct Search3 {
   unsigned long long acap;
   Lvl3 *ring;
   Scal3 *sc;
+  // Chain segments (optional, null to go without): a forward jump from key
+  // k_0 over k_1 .. k_m records the slots of k_0 .. k_(m-1) as segment i
+  // (segs[8 i .. 8 i + m)) and seg_of[slot of k_m] = i << 4 | m, so the
+  // backward search claims the keys leading to k_m together.
+  uint32_t *segs;
+  uint32_t *seg_of;
+  uint32_t scap;
 };
 
 // Output arrays of a three-input C.
