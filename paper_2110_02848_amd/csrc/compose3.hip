@@ -537,12 +537,13 @@ struct Jump3 {
   ull last_key;
 };
 
-// Slots of keys key[i], i < n, inserted if absent (fr[i]): all groups
-// loaded, then one CAS per key at the first free slot of its group; a key
-// whose group is full or whose slot another key took goes through h_insert.
-// ts[i] = NO_SLOT (and the overflow flag) when the table is full.
+// Slots of keys key[i], i in the mask `valid`, inserted if absent (fr[i]):
+// all groups loaded, then one CAS per key at the first free slot of its
+// group; a key whose group is full or whose slot another key took goes
+// through h_insert.  ts[i] = NO_SLOT (and the overflow flag) when the table
+// is full.
 __device__ __forceinline__ void insert_batch(const Problem3 &P, const Search3 &S,
-                                             const ull key[JUMP3], int n,
+                                             const ull key[JUMP3], uint32_t valid,
                                              uint32_t ts[JUMP3], bool fr[JUMP3]) {
   uint32_t h[JUMP3], pick[JUMP3];
   // pick[i]: HGROUP + j when slot j of the first group holds the key, j
@@ -551,7 +552,7 @@ __device__ __forceinline__ void insert_batch(const Problem3 &P, const Search3 &S
   for (int i = 0; i < JUMP3; ++i) {
     h[i] = (uint32_t)mix64(key[i]) & P.hmask & ~(HGROUP - 1u);
     pick[i] = 2 * HGROUP;
-    if (i < n) {
+    if ((valid >> i) & 1u) {
       ull g[HGROUP];
       load_group(P, h[i], g);
 #pragma unroll
@@ -566,13 +567,14 @@ __device__ __forceinline__ void insert_batch(const Problem3 &P, const Search3 &S
 #pragma unroll
   for (int i = 0; i < JUMP3; ++i) {
     old[i] = 0;
-    if (i < n && pick[i] < HGROUP) old[i] = atomicCAS(P.tab + h[i] + pick[i], EMPTY3, key[i]);
+    if (((valid >> i) & 1u) && pick[i] < HGROUP)
+      old[i] = atomicCAS(P.tab + h[i] + pick[i], EMPTY3, key[i]);
   }
 #pragma unroll
   for (int i = 0; i < JUMP3; ++i) {
     ts[i] = NO_SLOT;
     fr[i] = false;
-    if (i < n) {
+    if ((valid >> i) & 1u) {
       if (pick[i] >= HGROUP && pick[i] < 2 * HGROUP) {
         ts[i] = h[i] + pick[i] - HGROUP;
       } else if (pick[i] < HGROUP && old[i] == EMPTY3) {
@@ -653,7 +655,7 @@ __device__ __forceinline__ Jump3 jump3(const Problem3 &P, const Search3 &S, uint
     key[i] = pack3(P, qa[i + 1 <= m ? i + 1 : m], (uint32_t)cw[2 + 2 * i], 0, k.qd, 0);
   uint32_t ts[JUMP3];
   bool fr[JUMP3];
-  insert_batch(P, S, key, m, ts, fr);
+  insert_batch(P, S, key, (1u << m) - 1u, ts, fr);
   // the side keys of the hops' sources, (qa[i], s_(i-1) (qb for i = 0),
   // f1 of the source, d', 1) for i < m
   ull skey[JUMP3];
@@ -663,7 +665,7 @@ __device__ __forceinline__ Jump3 jump3(const Problem3 &P, const Search3 &S, uint
   for (int i = 0; i < JUMP3; ++i)
     skey[i] = pack3(P, qa[i <= m ? i : m], i == 0 ? k.qb : (uint32_t)cw[2 * i],
                     i == 0 ? k.f1 : 0u, dd, 1);
-  insert_batch(P, S, skey, side ? m : 0, sts, sfr);
+  insert_batch(P, S, skey, side ? (1u << m) - 1u : 0u, sts, sfr);
   r.done = true;
   r.hops = m;
   r.fresh = 0;
@@ -797,6 +799,112 @@ __global__ __launch_bounds__(NT) void k3_fwd(Problem3 P, Search3 S, int l) {
   wave_add(went, &S.sc->ncont);
 }
 
+// Units [u0, u1) of the key in `slot` when they are all arcs of its B
+// state with input epsilon (a lexicon root's word entries), each with at
+// most one D arc for its output (or none needed): their arc records, D
+// buckets and targets are loaded together and the targets inserted
+// together, the moves recorded with one atomic; the first new target
+// becomes *cont, the others join the next frontier.  Returns false (nothing
+// done) when the units do not have that shape.
+__device__ __forceinline__ bool expand_beps(const Problem3 &P, const Search3 &S, uint32_t slot,
+                                            const Units3 &u, uint32_t u0, uint32_t u1,
+                                            Lvl3 *nx, uint32_t nbase, uint32_t *cont,
+                                            ull *cont_key) {
+  static_assert(CHUNK3 <= JUMP3, "a chunk's units fit one batch");
+  const Key3 &k = u.k;
+  if (!P.dOut.lut || u1 - u0 > (uint32_t)JUMP3 || u0 < u.nae ||
+      u1 > u.nae + (uint32_t)u.gb.neps)
+    return false;
+  const uint32_t tf1 = u.ga.neps > 0 ? 1u : 0u;  // epsOutA(qa)
+  const uint32_t dstride = (uint32_t)P.dOut.lstride;
+  int32_t z[JUMP3];
+  uint32_t tb[JUMP3];
+#pragma unroll
+  for (int i = 0; i < JUMP3; ++i) {
+    z[i] = 0;
+    tb[i] = 0;
+    if (u0 + (uint32_t)i < u1) {
+      const int32_t p = u.gb.begin + (int32_t)(u0 - u.nae) + i;
+      z[i] = P.bOut.olab[p];
+      tb[i] = nbr_of_arc(P.bOut.arec[p].y);
+    }
+  }
+  int4 db[JUMP3];
+#pragma unroll
+  for (int i = 0; i < JUMP3; ++i) {
+    db[i] = make_int4(0, 0, 0, 0);
+    if (u0 + (uint32_t)i < u1 && z[i] != 0 && (uint32_t)z[i] < dstride)
+      db[i] = P.dOut.lut[(size_t)k.qd * dstride + (uint32_t)z[i]];
+  }
+  // a unit with several D arcs for its output takes the general path
+  uint32_t valid = 0;
+  ull key[JUMP3];
+#pragma unroll
+  for (int i = 0; i < JUMP3; ++i) {
+    key[i] = 0;
+    if (u0 + (uint32_t)i >= u1) continue;
+    if (z[i] == 0) {
+      if (k.f2 == 0) {  // a T-arc with output epsilon, alone
+        key[i] = pack3(P, k.qa, tb[i], tf1, k.qd, 0);
+        valid |= 1u << i;
+      }
+    } else if (db[i].y - db[i].x == 1) {
+      key[i] = pack3(P, k.qa, tb[i], tf1, nbr_of_arc(db[i].z), 0);
+      valid |= 1u << i;
+    } else if (db[i].y - db[i].x > 1) {
+      return false;
+    }
+  }
+  uint32_t ts[JUMP3];
+  bool fr[JUMP3];
+  insert_batch(P, S, key, valid, ts, fr);
+  uint32_t nv = 0, nnew = 0;
+  bool full = false;
+#pragma unroll
+  for (int i = 0; i < JUMP3; ++i)
+    if ((valid >> i) & 1u) {
+      ++nv;
+      full = full || ts[i] == NO_SLOT;
+    }
+  if (full) return true;  // the table is full: the search starts again
+  if (nv) {
+    const ull base = atomicAdd(&S.sc->narcs, nv);
+    uint32_t o = 0;
+#pragma unroll
+    for (int i = 0; i < JUMP3; ++i)
+      if ((valid >> i) & 1u) {
+        if (base + o < S.acap) S.arcs[base + o] = make_uint2(slot, ts[i]);
+        else atomicOr(&S.sc->overflow, 1u);
+        ++o;
+      }
+  }
+  // the first new target goes on the walk, the others to the next frontier
+#pragma unroll
+  for (int i = 0; i < JUMP3; ++i)
+    if (((valid >> i) & 1u) && fr[i]) {
+      if (*cont == NO_SLOT) {
+        *cont = ts[i];
+        *cont_key = key[i];
+        fr[i] = false;
+      } else {
+        ++nnew;
+      }
+    }
+  if (nnew) {
+    const uint32_t fb = atomicAdd(&nx->fcount, nnew);
+    uint32_t q = 0;
+#pragma unroll
+    for (int i = 0; i < JUMP3; ++i)
+      if (((valid >> i) & 1u) && fr[i]) {
+        const ull pos = (ull)fb + q;
+        if (pos < (ull)S.fcap - nbase) S.F[nbase + pos] = ts[i];
+        else atomicOr(&S.sc->overflow, 1u);
+        ++q;
+      }
+  }
+  return true;
+}
+
 // The chunks of level l: CHUNK3 units each, then a depth-first walk from
 // the first new key; heavy keys met on the walk go to the next level's
 // chunks.
@@ -814,7 +922,8 @@ __global__ __launch_bounds__(NT) void k3_fwd_chunks(Problem3 P, Search3 S, int l
     const uint32_t u1 = c.y + CHUNK3 < n ? c.y + CHUNK3 : n;
     uint32_t cont = NO_SLOT;
     ull cont_key = 0;
-    expand_units(P, S, c.x, u, c.y, u1, nx, nbase, &cont, &cont_key);
+    if (!expand_beps(P, S, c.x, u, c.y, u1, nx, nbase, &cont, &cont_key))
+      expand_units(P, S, c.x, u, c.y, u1, nx, nbase, &cont, &cont_key);
     if (cont != NO_SLOT) went += 1 + walk_fwd(P, S, cont, cont_key, nx, nbase, nx, l + 1);
   }
   wave_add(went, &S.sc->ncont);
