@@ -132,6 +132,30 @@ def test_equal_to_chained_when_d_has_no_epsilon_input(comp):
     check3(comp, A, B, D, "chained reference", ref=t3.chained3(A, B, D))
 
 
+def _compose3_np(comp, A, B, D):
+    import torch
+    from paper_2110_02848_amd import gpu
+    C = comp.compose3(gpu.to_device(A), gpu.to_device(B), gpu.to_device(D))
+    torch.cuda.synchronize()
+    return gpu.to_numpy(C), comp.stats3()
+
+
+def test_repeatable_and_context_reuse(comp):
+    """The result does not depend on the schedule of the concurrent inserts,
+    jumps and segment claims: the same inputs composed again, after another
+    composition and with the hash set at the size the last call left, give
+    the same arrays bit for bit and the same counts."""
+    A, B, D, _ = synth.emissions_lexicon_grammar("grammar-T40-W300-G6", 1)
+    print("[parity3] repeatable grammar-T40-W300-G6 seed 1", flush=True)
+    r1, s1 = _compose3_np(comp, A, B, D)
+    _compose3_np(comp, *_tiny_triple(7))
+    for _ in range(3):
+        r2, s2 = _compose3_np(comp, A, B, D)
+        assert not fsthelp.compare_results(r1, r2, oracle.RESULT3_KEYS)
+        for k in ("num_states", "num_arcs", "accessible", "coaccessible", "generated"):
+            assert s1[k] == s2[k], (k, s1[k], s2[k])
+
+
 def test_degenerate_and_errors(comp):
     import torch
     from paper_2110_02848_amd import gpu
