@@ -36,9 +36,13 @@
 // lexicon is one thread's walk; other new keys join the next frontier, and
 // heavy keys met on a walk are cut into chunks.  Every generated arc
 // (source slot, target slot) is appended to an arc list, and new keys to
-// the next frontier, one atomic per wavefront.
+// the next frontier, one atomic per wavefront.  Keys with one move along a
+// chain of B (a word's letters) are crossed by a chain jump that inserts
+// the keys it reaches together, and a lexicon root's chunk of word entries
+// is expanded in one batch (see jump3 and expand_beps).
 // Co-accessibility runs backwards over that arc list (in-arcs grouped by a
-// radix sort of the arcs by target, their run boundaries and a scan).  The trim keys are sorted (radix sort of
+// radix sort of the arcs by target, their run boundaries and a scan); the
+// keys of a jump's chain segment are claimed together.  The trim keys are sorted (radix sort of
 // the 64-bit keys): a state's id is its rank.  Count and fill give a state
 // with at most LIGHT3 units one thread and a heavier one a workgroup (its
 // threads take its units in turn); per-unit counts are scanned into every
