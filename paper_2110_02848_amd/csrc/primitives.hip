@@ -142,13 +142,25 @@ __global__ __launch_bounds__(NT) void k_radix_scatter(const ull *__restrict__ ki
     s_run[tid] = gofs[(size_t)tid * nb + blockIdx.x];
   }
   const size_t base = (size_t)blockIdx.x * NT * items;
+  // each round loads the next round's key and value before its own work
+  ull key_next = 0ull;
+  int32_t val_next = 0;
+  if (base + tid < n) {
+    key_next = kin[base + tid];
+    val_next = vin[base + tid];
+  }
   for (int r = 0; r < items; ++r) {
 #pragma unroll
     for (int w = 0; w < NWAVES; ++w) s_wc[w][tid] = 0;
-    __syncthreads();
     const size_t i = base + (size_t)r * NT + tid;
     const bool valid = i < n;
-    ull key = valid ? kin[i] : 0ull;
+    const ull key = key_next;
+    const int32_t val = val_next;
+    if (r + 1 < items && i + NT < n) {
+      key_next = kin[i + NT];
+      val_next = vin[i + NT];
+    }
+    __syncthreads();
     uint32_t d = (uint32_t)(key >> shift) & 255u;
     unsigned long long m = __ballot(valid);
 #pragma unroll
@@ -163,7 +175,7 @@ __global__ __launch_bounds__(NT) void k_radix_scatter(const ull *__restrict__ ki
       uint32_t pos = s_run[d] + rank;
       for (unsigned w = 0; w < wid; ++w) pos += s_wc[w][d];
       kout[pos] = key;
-      vout[pos] = vin[i];
+      vout[pos] = val;
     }
     __syncthreads();
     uint32_t add = 0;
