@@ -59,7 +59,7 @@ constexpr ull EMPTY3 = ~0ull;
 constexpr uint32_t NO_SLOT = 0xFFFFFFFFu;
 constexpr uint32_t LIGHT3 = 8;    // output: units of a state one thread writes
 constexpr uint32_t WALK3 = 8;     // search: units of a key a walk expands in place
-constexpr int PROBE_MAX = 4096;   // hash probes before the table counts as full
+constexpr int PROBE_MAX = 256;    // hash probes before the table counts as full
 constexpr uint32_t BF_EPS_EPS = 1u, BF_EPS_OUT = 2u;  // B state flags
 
 unsigned grid3(size_t n, unsigned cap = 4096) {
