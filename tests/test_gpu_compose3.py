@@ -132,6 +132,27 @@ def test_equal_to_chained_when_d_has_no_epsilon_input(comp):
     check3(comp, A, B, D, "chained reference", ref=t3.chained3(A, B, D))
 
 
+@pytest.mark.parametrize("buckets", [0, 1])
+def test_bucket_tables_off_and_on(buckets):
+    """With FST_OPT_LABEL_BUCKETS = 0 the label buckets are binary searches
+    and there are no chain records, so no chain jumps, batched root chunks
+    or segment claims: the general paths alone give the same result (and
+    with 1, the same inputs through the fast paths)."""
+    import torch
+    from paper_2110_02848_amd import gpu
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    c = gpu.Composer(0)
+    c.set_option(gpu.FST_OPT_LABEL_BUCKETS, buckets)
+    A, B, D, _ = synth.emissions_lexicon_grammar("grammar-T40-W300-G6", 2)
+    check3(c, A, B, D, f"grammar-T40-W300-G6 seed 2, buckets {buckets}")
+    spec = synth.GrammarSpec(30, 6, 120, 9, 14, 4, 60, 1.0, 0.5)
+    A, B, D, _ = synth.emissions_lexicon_grammar("grammar-T40-W300-G6", 5, spec=spec)
+    check3(c, A, B, D, f"long words, buckets {buckets}")
+    for seed in range(8):
+        check3(c, *_tiny_triple(seed), f"tiny triple seed {seed}, buckets {buckets}")
+    c.close()
+
+
 def _compose3_np(comp, A, B, D):
     import torch
     from paper_2110_02848_amd import gpu
