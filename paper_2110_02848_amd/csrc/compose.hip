@@ -2072,7 +2072,8 @@ hipError_t launch_count_moves(const Problem &P, size_t nwords, bool forward,
 hipError_t launch_popcount(const uint32_t *bm, size_t nwords, unsigned long long *out,
                            hipStream_t s) {
   if (!nwords) return hipSuccess;
-  k_popcount<<<grid_for(nwords / 4 + 1, 2048), NT, 0, s>>>(bm, nwords, out);
+  // few workgroups: each adds its sum with one atomic on the same counter
+  k_popcount<<<grid_for(nwords / 4 + 1, 256), NT, 0, s>>>(bm, nwords, out);
   return hipGetLastError();
 }
 

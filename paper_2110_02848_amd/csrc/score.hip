@@ -924,12 +924,30 @@ __global__ __launch_bounds__(NT) void k_merge_place(ScoreGraph G, const int32_t 
 // ---------------------------------------------------------------------------
 
 
+// Calls f(v) for every v < V with flag[v] set: sixteen flags per load when
+// the flags are 16-byte aligned (flagged states are few: accepting or start
+// states), one byte per load for the rest.
+template <class F>
+__device__ __forceinline__ void for_flagged(const uint8_t *flag, int32_t V, F &&f) {
+  const long long stride = (long long)gridDim.x * NT;
+  const long long n16 = ((uintptr_t)flag & 15) ? 0 : (long long)V / 16;
+  const uint4 *f16 = reinterpret_cast<const uint4 *>(flag);
+  for (long long w = (long long)blockIdx.x * NT + threadIdx.x; w < n16; w += stride) {
+    const uint4 q = f16[w];
+    if (!(q.x | q.y | q.z | q.w)) continue;
+    const uint32_t word[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+    for (int j = 0; j < 16; ++j)
+      if ((word[j >> 2] >> (8 * (j & 3))) & 0xffu) f(16 * w + j);
+  }
+  for (long long v = 16 * n16 + (long long)blockIdx.x * NT + threadIdx.x; v < V; v += stride)
+    if (flag[v]) f(v);
+}
+
 __global__ __launch_bounds__(NT) void k_total_max(const double *val, const uint8_t *flag,
                                                   int32_t V, ScoreScalars *sc) {
   double m = -INFINITY;
-  for (long long v = (long long)blockIdx.x * NT + threadIdx.x; v < V;
-       v += (long long)gridDim.x * NT)
-    if (flag[v]) m = fmax(m, val[v]);
+  for_flagged(flag, V, [&](long long v) { m = fmax(m, val[v]); });
   m = block_fmax(m);
   if (threadIdx.x == 0 && m != -INFINITY) atomicMax(&sc->zmax, order_key(m));
 }
@@ -940,9 +958,7 @@ __global__ __launch_bounds__(NT) void k_total_sum(const double *val, const uint8
   const double M = from_order_key(sc->zmax);
   if (M == INFINITY) return;
   ull lo = 0, hi = 0;
-  for (long long v = (long long)blockIdx.x * NT + threadIdx.x; v < V;
-       v += (long long)gridDim.x * NT)
-    if (flag[v]) acc_add(lo, hi, exp(val[v] - M));
+  for_flagged(flag, V, [&](long long v) { acc_add(lo, hi, exp(val[v] - M)); });
   block_sum128(lo, hi);
   if (threadIdx.x == 0 && (lo | hi)) {
     const ull old = atomicAdd(&sc->zlo, lo);
@@ -1393,8 +1409,8 @@ hipError_t launch_score_generation(const ScoreArgs *F, const ScoreArgs *B, int g
 
 hipError_t launch_score_total(const double *val, const uint8_t *flag, int32_t V,
                               ScoreScalars *sc, double *total, hipStream_t s) {
-  k_total_max<<<grid_for(V), NT, 0, s>>>(val, flag, V, sc);
-  k_total_sum<<<grid_for(V), NT, 0, s>>>(val, flag, V, sc);
+  k_total_max<<<grid_for((long long)V / 16 + 1), NT, 0, s>>>(val, flag, V, sc);
+  k_total_sum<<<grid_for((long long)V / 16 + 1), NT, 0, s>>>(val, flag, V, sc);
   k_total_final<<<1, 1, 0, s>>>(sc, total);
   return hipGetLastError();
 }
@@ -1424,7 +1440,8 @@ hipError_t launch_scatter(const float *g, const int32_t *idx, long long n, int32
                           uint32_t *mx, uint32_t *bad, float *out, const ScatterTemp *tmp,
                           hipStream_t s) {
   if (n > 0) {
-    k_absmax<<<grid_for(n / 4 + 1), NT, 0, s>>>(g, n, mx);
+    // few workgroups: each ends with one atomic on the same word
+    k_absmax<<<grid_for(n / 4 + 1) < 512 ? grid_for(n / 4 + 1) : 512, NT, 0, s>>>(g, n, mx);
     const int32_t nbk = (int32_t)((m + SC_BINS - 1) / SC_BINS);
     if (tmp && scatter_grouped(n, m)) {
       const long long nblk = (n + 8 * NT - 1) / (8 * NT) < SC_BLOCKS ? (n + 8 * NT - 1) / (8 * NT)
