@@ -340,6 +340,22 @@ __device__ __forceinline__ T wave_incl_scan(T x) {
   return x;
 }
 
+// The same for 32-bit values with DPP moves instead of LDS shuffles: adds
+// of the values shifted by 1, 2, 4 and 8 lanes inside each row of 16 lanes
+// (lanes shifted in from outside the row add 0), then of row 0's and row
+// 2's last lane to rows 1 and 3, then of lane 31 to rows 2 and 3.
+template <>
+__device__ __forceinline__ uint32_t wave_incl_scan<uint32_t>(uint32_t x) {
+  static_assert(WAVE == 64, "four rows of 16 lanes");
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, true);   // row_shr:1
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, true);   // row_shr:2
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, true);   // row_shr:4
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, true);   // row_shr:8
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false);  // row_bcast:31
+  return x;
+}
+
 // Exclusive scan over the NT threads of a workgroup.  Every thread must call
 // it (it contains barriers).  s_wsum needs NWAVES entries.
 template <typename T>
