@@ -366,7 +366,8 @@ __global__ __launch_bounds__(NT) void k_mark_arcs(ViewJobs J) {
   }
 }
 
-// Second state record: the first epsilon and first non-epsilon arcs.
+// Second state record: the first epsilon and first non-epsilon arcs; and
+// FLAG_DISTINCT in the first.
 __global__ __launch_bounds__(NT) void k_state_inline(ViewJobs J) {
   for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < J.vbegin[4];
        i += (long long)gridDim.x * NT) {
@@ -376,6 +377,20 @@ __global__ __launch_bounds__(NT) void k_state_inline(ViewJobs J) {
     const int4 r = b.srec[2 * v];
     const int2 first_ne = r.x + r.y < r.z ? b.arec[r.x + r.y] : make_int2(0, 0);
     b.srec[2 * v + 1] = make_int4(r.y > 0 ? b.arec[r.x].y : 0, first_ne.x, first_ne.y, 0);
+    // labels are sorted inside the group: distinct unless two neighbours are
+    // equal (eight arcs per round, loaded together)
+    bool d = r.z - r.x - r.y <= DISTINCT_SCAN_MAX;
+    int32_t last = -1;  // label before the round (none: -1, labels are >= 0)
+    for (int32_t k0 = r.x + r.y; d && k0 < r.z; k0 += 8) {
+      int32_t l[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) l[q] = k0 + q < r.z ? b.arec[k0 + q].x : -1 - q;
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        if ((q ? l[q - 1] : last) == l[q]) d = false;
+      last = l[7];
+    }
+    if (d) b.srec[2 * v] = make_int4(r.x, r.y, r.z, r.w | (int32_t)FLAG_DISTINCT);
   }
 }
 
@@ -1452,6 +1467,21 @@ __device__ __forceinline__ uint32_t new_id(const Problem &P, uint32_t k) {
 
 __device__ __forceinline__ uint32_t out_units(const Fwd &s) { return s.eA + (uint32_t)s.be + s.mU; }
 
+// A state of C (a trim key) that does not accept and has exactly one move:
+// one epsilon move and no matching unit, or one non-epsilon arc on the
+// smaller side whose label bucket on the other side holds at most one arc
+// (that side's labels are distinct).  Its one move is a kept arc: a trim key
+// that does not accept reaches an accepting key through some move, whose
+// target is then co-accessible and, reached from an accessible key,
+// accessible.  So its count is 1, known from its records alone.
+__device__ __forceinline__ bool lone_move(const Fwd &s) {
+  if (s.accept) return false;
+  const uint32_t neps = s.eA + (uint32_t)s.be;
+  if (neps == 1 && s.mU == 0) return true;
+  if (neps != 0 || s.mU != 1) return false;
+  return ((s.nA <= s.nB ? s.flB : s.flA) & (int32_t)FLAG_DISTINCT) != 0;
+}
+
 // The move of a state that has a single candidate: one epsilon arc and no
 // matching unit, or no epsilon arc and one non-epsilon arc on the smaller
 // side whose label bucket on the other side holds at most one arc.  Lanes of
@@ -1749,6 +1779,8 @@ __global__ __launch_bounds__(NT) void k_count(Problem P, ull nwords, ull nchunks
       uint32_t c = 0;
       if (out_units(s) > LIGHT_UNITS) {
         hv = true;
+      } else if (lone_move(s)) {
+        c = 1;
       } else {
         enum_light(P, s, [&](uint32_t d, int32_t, int32_t, float, int32_t, int32_t) {
           c += test_bit(P.trim, d) ? 1u : 0u;

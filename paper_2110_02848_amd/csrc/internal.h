@@ -66,6 +66,10 @@ struct DevGraph {
 //   with distinct non-epsilon output labels).  A key whose two states are
 //   both marked is reached once by a search in that direction, so it needs
 //   no claim.
+//   FLAG_DISTINCT marks a state whose non-epsilon arcs in the view all have
+//   different labels (checked for groups of at most DISTINCT_SCAN_MAX
+//   non-epsilon arcs; larger groups are left unmarked), so any label bucket
+//   of the state holds at most one arc.
 //   chain (views of B, optional): per state, up to CHAIN_STEPS steps of its
 //   single-arc path in the view: {n, l0, s0, l1, s1, ..., l10, s10} as
 //   CHAIN_INT4 int4, where step i follows the only arc (label l_i, non-epsilon) of the
@@ -94,7 +98,9 @@ struct View {
 constexpr int CHAIN_STEPS = 11;
 constexpr int CHAIN_INT4 = (1 + 2 * CHAIN_STEPS + 3) / 4;  // int4 per chain record
 
-constexpr uint32_t FLAG_ACCEPT = 1u, FLAG_EPS_OUT = 2u, FLAG_START = 4u, FLAG_UNIQ = 8u;
+constexpr uint32_t FLAG_ACCEPT = 1u, FLAG_EPS_OUT = 2u, FLAG_START = 4u, FLAG_UNIQ = 8u,
+                   FLAG_DISTINCT = 16u;
+constexpr int32_t DISTINCT_SCAN_MAX = 256;
 constexpr int32_t NBR_MASK = 0x3fffffff;            // state ids < 2^30
 constexpr int32_t NBR_UNIQ = 0x40000000;
 constexpr int32_t NBR_EPS = (int32_t)0x80000000u;

@@ -227,6 +227,20 @@ def test_unique_move_corner_cases(comp):
         assert not fsthelp.check_invariants(X, Y, got)
 
 
+def test_accepting_states_with_one_move(comp):
+    # keys of C with exactly one move whose target is a dead end: (1, 1) by
+    # a matching pair (B's one arc, A's labels distinct), (2, 1) by an A
+    # epsilon arc.  Both accept, so they are kept with no kept arc; the
+    # keys before them have one kept arc each.
+    A = synth.from_arcs(4, [(0, 1, 1, 1, 0.5), (1, 3, 2, 2, 0.25), (1, 2, 3, 3, 1.0),
+                            (2, 3, 4, 0, 2.0), (0, 2, 6, 6, 0.75)], start=[0], accept=[1, 2])
+    B = synth.from_arcs(3, [(0, 1, 1, 5, 0.5), (1, 2, 2, 6, 0.0), (0, 1, 6, 8, 1.5)],
+                        start=[0], accept=[1])
+    got, _ = check_pair(comp, A, B, "accepting one-move keys")
+    assert (got["num_states"], got["num_arcs"]) == (3, 2)
+    assert not fsthelp.check_invariants(A, B, got)
+
+
 def _sparse_emissions(rng, T, C, p_tok, p_dup, p_acc):
     """Linear acceptor where each frame has a random subset of tokens, some
     tokens twice (buckets of two arcs), and some extra accepting frames."""
