@@ -1751,6 +1751,31 @@ __device__ uint32_t heavy_state(const Problem &P, uint32_t id, uint32_t key, uin
   return run;
 }
 
+// The kept-arc count of a heavy state (the same moves as heavy_state): each
+// thread counts its share of the moves, one block sum at the end; valid in
+// thread 0.  Every thread of the workgroup must call it.
+__device__ uint32_t heavy_count(const Problem &P, uint32_t key, uint32_t *s_w) {
+  const Fwd s = fwd_info<false>(P, key);
+  const uint32_t sh = P.shiftB;
+  uint32_t kept = 0;
+#pragma unroll 4
+  for (uint32_t i = threadIdx.x; i < s.eA; i += NT)
+    kept += test_bit(P.trim, make_key(nbr_of(P.aOut.arec[s.aS + (int32_t)i].y), s.qb, 0u, sh));
+#pragma unroll 4
+  for (uint32_t i = threadIdx.x; i < (uint32_t)s.be; i += NT)
+    kept += test_bit(P.trim, make_key(s.qa, nbr_of(P.bOut.arec[s.bS + (int32_t)i].y), s.epsA, sh));
+  if (s.mU)
+    for (uint32_t i = threadIdx.x; i < s.nA; i += NT) {
+      const int2 ar = P.aOut.arec[s.aS + s.ae + (int32_t)i];
+      const uint32_t da = nbr_of(ar.y);
+      int32_t lo, hi;
+      label_range(P.bOut, s.qb, s.bS + s.be, s.bE, ar.x, lo, hi);
+      for (int32_t pb = lo; pb < hi; ++pb)
+        kept += test_bit(P.trim, make_key(da, nbr_of(P.bOut.arec[pb].y), 0u, sh));
+    }
+  return block_sum(kept, s_w);
+}
+
 // Kept-arc counts, one output chunk per wavefront: put_count for light
 // states (0 for now for heavy ones, which are listed with their keys), and
 // btot[chunk] = the chunk's light total.
@@ -1811,14 +1836,14 @@ __global__ __launch_bounds__(NT) void k_count_heavy(Problem P, const uint2 *__re
                                                     uint32_t *__restrict__ btot) {
   __shared__ uint32_t s_w[NWAVES];
   const uint32_t nheavy = *nheavy_p;
-  OutGraph none = {};
   for (uint32_t h = blockIdx.x; h < nheavy; h += gridDim.x) {
     const uint2 hk = heavy[h];
-    uint32_t c = heavy_state<false>(P, hk.x, hk.y, 0, none, s_w);
+    const uint32_t c = heavy_count(P, hk.y, s_w);
     if (threadIdx.x == 0) {
       put_count(cnt8, cnt32, hk.x, c);
       atomicAdd(btot + (hk.y >> 5) / OUT_WORDS, c);
     }
+    __syncthreads();  // s_w is read by thread 0 before the next state's sum
   }
 }
 
