@@ -419,6 +419,44 @@ def tiny_random(rng, V, max_degree, n_sym, p_eps, p_accept=0.4, n_start=1):
     return from_arcs(V, arcs, start=starts, accept=acc)
 
 
+def random_cyclic(seed, V, degree=3, mass=0.5, n_start=2, p_accept=0.2, hubs=0,
+                  hub_degree=0):
+    """Seeded random graph with cycles whose path sums converge (inputs of
+    the cyclic-score tests).
+
+    Every state gets ``degree`` out-arcs to uniform destinations (self-loops
+    and parallel arcs allowed); ``hubs`` states (drawn at random) also get
+    ``hub_degree`` in-arcs from random states.  A state's out-arc weights are
+    log(mass * p) for p a softmax of N(0, 1) draws over its arcs, rounded to
+    binary32, so the probabilities of a state's arcs add to about ``mass``
+    (< 1: the spectral radius of the arc matrix stays below 1).  Labels are
+    1.  ``n_start`` distinct start states; accepting states at rate p_accept,
+    at least one."""
+    rng = np.random.default_rng(np.random.SeedSequence([11, int(seed)]))
+    src = np.repeat(np.arange(V, dtype=np.int64), degree)
+    dst = rng.integers(0, V, size=V * degree)
+    if hubs and hub_degree:
+        hub = rng.choice(V, size=hubs, replace=False)
+        src = np.concatenate([src, rng.integers(0, V, size=hubs * hub_degree)])
+        dst = np.concatenate([dst, np.repeat(hub, hub_degree)])
+    z = rng.standard_normal(len(src))
+    order = np.argsort(src, kind="stable")
+    src, dst, z = src[order], dst[order], z[order]
+    w = np.empty(len(src))
+    for v in range(V):
+        lo, hi = np.searchsorted(src, [v, v + 1])
+        if hi > lo:
+            e = np.exp(z[lo:hi] - z[lo:hi].max())
+            w[lo:hi] = np.log(mass * e / e.sum())
+    w = w.astype(np.float32)
+    starts = rng.choice(V, size=min(n_start, V), replace=False)
+    acc = np.flatnonzero(rng.random(V) < p_accept)
+    if len(acc) == 0:
+        acc = np.array([int(rng.integers(0, V))])
+    arcs = [(int(a), int(b), 1, 1, float(c)) for a, b, c in zip(src, dst, w)]
+    return from_arcs(V, arcs, start=sorted(int(x) for x in starts), accept=acc.tolist())
+
+
 def random_dag(seed, V, mean_out=2.0, window=16, hubs=0, hub_degree=0, p_global=0.1,
                n_start=2, p_accept=0.05, p_parallel=0.05):
     """Seeded random acyclic graph (inputs of the score tests and benchmark).
