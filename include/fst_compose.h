@@ -63,7 +63,8 @@ enum fst_status {
   FST_ERR_NOMEM = 4,         /* device allocation failed or over the cap     */
   FST_ERR_HIP = 5,           /* a HIP runtime call failed                    */
   FST_ERR_STATE = 6,         /* fill without a successful run               */
-  FST_ERR_CYCLIC = 7         /* fst_score on a graph with a cycle            */
+  FST_ERR_CYCLIC = 7,        /* fst_score on a graph with a cycle            */
+  FST_ERR_NOT_CONVERGED = 8  /* fst_score_cyclic: sweeps did not settle      */
 };
 
 /* Read-only transducer view (device memory, caller-owned).
@@ -259,6 +260,32 @@ FST_API int fst_compose_kernel_time(const fst_ctx *ctx, int kernel, float *ms, i
  * fault).  G must stay valid until the work has completed. */
 FST_API int fst_score(fst_ctx *ctx, const fst_graph *G, double *alpha, double *beta,
                       double *total, void *stream);
+
+/* The same scores (alpha, beta, total: the sums over all paths) of a graph
+ * that may have cycles, where a state can have infinitely many paths; the
+ * sums are finite when the spectral radius of the matrix of arc
+ * probabilities, M[u][v] = sum of exp(w(e)) over the arcs from u to v, is
+ * below 1 over the states that lie on such paths (the Neumann series
+ * sum_k M^k of the probability domain).  Shortest distance is among the
+ * operations the paper leaves to future work (Section 5); here it is
+ * relaxed by Jacobi sweeps of both recursions from every value at -inf:
+ * sweep k gives each state the exact log-add of fst_score over the
+ * previous sweep's values (its pull list's terms and its empty path), so
+ * after k sweeps the values are the sums over the paths of at most k - 1
+ * arcs, rising monotonically.  The sweeps stop at the first sweep in which
+ * no value rose by more than `tol` (log domain, >= 0; 0 waits for a sweep
+ * that changes no value upwards); *sweeps (if not NULL) receives its
+ * number.  On a graph without cycles the sweeps reach fst_score's values
+ * bit for bit after at most (longest path + 2) sweeps.  Each sweep reads
+ * every state's in-arcs and out-arcs once (one thread per state, so a state
+ * with many arcs is summed by one thread), in batches of up to 64 sweeps
+ * between read-backs.  Arguments, validation and outputs as in fst_score;
+ * returns FST_ERR_NOT_CONVERGED (outputs: the last sweep's values) if no
+ * sweep settled within max_sweeps (>= 0) sweeps, as when the sums diverge;
+ * FST_ERR_INVALID_ARG for a negative max_sweeps or tol. */
+FST_API int fst_score_cyclic(fst_ctx *ctx, const fst_graph *G, double *alpha, double *beta,
+                             double *total, int32_t max_sweeps, double tol, int32_t *sweeps,
+                             void *stream);
 
 /* Arc posteriors times `scale`: grad[e] = scale * exp(alpha[src e] + w(e) +
  * beta[dst e] - *total), the derivative of scale * total by w(e) (0 for every

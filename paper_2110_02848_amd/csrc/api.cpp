@@ -66,7 +66,7 @@ struct fst_ctx {
   // score workspace
   DevBuf s_pg, s_pidx, s_bcnt, s_bscan, s_btotal;  // grouped scatter
   DevBuf s_sc, s_owner, s_extra, s_inref, s_mbeg, s_mlen, s_mcur, s_marc, s_val, s_acc,
-      s_mpos;
+      s_mpos, s_sweep;
   // batches: the union of the A graphs, item tables, segment sums
   DevBuf u_off, u_src, u_dst, u_il, u_ol, u_w, u_start, u_accept, u_items, seg;
   // three-input composition
@@ -379,6 +379,42 @@ int score_total(fst_ctx *c, const double *val, const uint8_t *flag, int32_t V, d
   return FST_OK;
 }
 
+// G with its in-arc structure (single in-arcs, and the in-arc lists of
+// merges), built into the context's buffers.
+int score_structure(fst_ctx *c, const DevGraph &d, ScoreGraph &SG, hipStream_t s) {
+  const int32_t V = d.V;
+  const size_t E = (size_t)d.E;
+  FST_TRY(ensure(c, c->s_owner, (size_t)V * 4));
+  FST_TRY(ensure(c, c->s_extra, (size_t)V * 4));
+  FST_TRY(ensure(c, c->s_inref, (size_t)V * 4));
+  FST_TRY(ensure(c, c->s_mbeg, (size_t)V * 4));
+  FST_TRY(ensure(c, c->s_mlen, (size_t)V * 4));
+  FST_TRY(ensure(c, c->s_mcur, (size_t)V * 4));
+  FST_TRY(ensure(c, c->s_marc, E * 4));
+  FST_TRY(ensure(c, c->s_mpos, E * 4));
+  SG = ScoreGraph{};
+  SG.V = V;
+  SG.E = (long long)E;
+  SG.off = d.off;
+  SG.src = d.src;
+  SG.dst = d.dst;
+  SG.w = d.w;
+  SG.start = d.start;
+  SG.accept = d.accept;
+  SG.inref = as<int32_t>(c->s_inref);
+  SG.mbeg = as<int32_t>(c->s_mbeg);
+  SG.mlen = as<int32_t>(c->s_mlen);
+  SG.marc = as<int32_t>(c->s_marc);
+  HIP_TRY(hipMemsetAsync(c->s_owner.p, 0xff, (size_t)V * 4, s));
+  HIP_TRY(hipMemsetAsync(c->s_extra.p, 0, (size_t)V * 4, s));
+  HIP_TRY(launch_score_structure(SG, as<int32_t>(c->s_owner), as<int32_t>(c->s_extra),
+                                 as<int32_t>(c->s_inref), as<int32_t>(c->s_mbeg),
+                                 as<int32_t>(c->s_mlen), as<int32_t>(c->s_mcur),
+                                 as<int32_t>(c->s_marc), as<int32_t>(c->s_mpos),
+                                 as<ScoreScalars>(c->s_sc), s));
+  return FST_OK;
+}
+
 int score_impl(fst_ctx *c, const fst_graph *G, double *alpha, double *beta, double *total,
                hipStream_t s) {
   FST_TRY(check_graph_args(G));
@@ -401,37 +437,11 @@ int score_impl(fst_ctx *c, const fst_graph *G, double *alpha, double *beta, doub
   }
   const KernelTimer tp = timer(c, FST_KERNEL_SCORE_PREP);
   tp.begin(s);
-  FST_TRY(ensure(c, c->s_owner, (size_t)V * 4));
-  FST_TRY(ensure(c, c->s_extra, (size_t)V * 4));
-  FST_TRY(ensure(c, c->s_inref, (size_t)V * 4));
-  FST_TRY(ensure(c, c->s_mbeg, (size_t)V * 4));
-  FST_TRY(ensure(c, c->s_mlen, (size_t)V * 4));
-  FST_TRY(ensure(c, c->s_mcur, (size_t)V * 4));
-  FST_TRY(ensure(c, c->s_marc, E * 4));
-  FST_TRY(ensure(c, c->s_mpos, E * 4));
   if (fwd && !alpha) FST_TRY(ensure(c, c->s_val, (size_t)V * 8));
   if (fwd) FST_TRY(score_bufs(c, c->score_f, V, E));
   if (beta) FST_TRY(score_bufs(c, c->score_b, V, E));
-
   ScoreGraph SG = {};
-  SG.V = V;
-  SG.E = (long long)E;
-  SG.off = d.off;
-  SG.src = d.src;
-  SG.dst = d.dst;
-  SG.w = d.w;
-  SG.start = d.start;
-  SG.accept = d.accept;
-  SG.inref = as<int32_t>(c->s_inref);
-  SG.mbeg = as<int32_t>(c->s_mbeg);
-  SG.mlen = as<int32_t>(c->s_mlen);
-  SG.marc = as<int32_t>(c->s_marc);
-  HIP_TRY(hipMemsetAsync(c->s_owner.p, 0xff, (size_t)V * 4, s));
-  HIP_TRY(hipMemsetAsync(c->s_extra.p, 0, (size_t)V * 4, s));
-  HIP_TRY(launch_score_structure(SG, as<int32_t>(c->s_owner), as<int32_t>(c->s_extra),
-                                 as<int32_t>(c->s_inref), as<int32_t>(c->s_mbeg),
-                                 as<int32_t>(c->s_mlen), as<int32_t>(c->s_mcur),
-                                 as<int32_t>(c->s_marc), as<int32_t>(c->s_mpos), dsc, s));
+  FST_TRY(score_structure(c, d, SG, s));
   tp.end(s);
   ScoreArgs SF = {}, SB = {};
   if (fwd) SF = score_args(c, c->score_f, SG, alpha ? alpha : as<double>(c->s_val));
@@ -443,6 +453,86 @@ int score_impl(fst_ctx *c, const fst_graph *G, double *alpha, double *beta, doub
   else FST_TRY(score_total(c, beta, d.start, V, total, s));
   c->have_score_times = c->timing;
   return FST_OK;
+}
+
+// Relaxation sweeps of both recursions (graphs with cycles), from every
+// value at -inf, in batches with one read-back of the batch's rises each,
+// until a sweep in which no value rose by more than tol.  The values after
+// the batch's last sweep are returned (later sweeps of a batch rise no
+// more than tol either, up to rounding).
+int score_cyclic_impl(fst_ctx *c, const fst_graph *G, double *alpha, double *beta,
+                      double *total, int32_t max_sweeps, double tol, int32_t *sweeps,
+                      hipStream_t s) {
+  FST_TRY(check_graph_args(G));
+  if (max_sweeps < 0 || !(tol >= 0.0)) return FST_ERR_INVALID_ARG;
+  const DevGraph d = dev_graph(G);
+  FST_TRY(ensure(c, c->s_sc, sizeof(ScoreScalars)));
+  for (int k = NCOMPOSE_KERNELS; k < NKERNELS; ++k) {
+    c->kms[k] = 0.f;
+    c->klaunches[k] = 0;
+  }
+  if (sweeps) *sweeps = 0;
+  FST_TRY(score_validate(c, d, s));
+  const int32_t V = d.V;
+  ScoreScalars *dsc = as<ScoreScalars>(c->s_sc);
+  const bool fwd = alpha != nullptr || beta == nullptr, bwd = beta != nullptr;
+  if (V == 0) {
+    HIP_TRY(hipMemsetAsync(&dsc->zmax, 0, 3 * sizeof(unsigned long long), s));
+    HIP_TRY(launch_score_total(nullptr, nullptr, 0, dsc, total, s));
+    return FST_OK;
+  }
+  const KernelTimer tp = timer(c, FST_KERNEL_SCORE_PREP);
+  tp.begin(s);
+  ScoreGraph SG = {};
+  FST_TRY(score_structure(c, d, SG, s));
+  FST_TRY(ensure(c, c->s_sweep, (size_t)V * 4 * sizeof(double)));
+  double *a[2] = {as<double>(c->s_sweep), as<double>(c->s_sweep) + V};
+  double *b[2] = {a[1] + V, a[1] + 2 * (size_t)V};
+  if (fwd) HIP_TRY(launch_fill_f64(a[0], V, -INFINITY, s));
+  if (bwd) HIP_TRY(launch_fill_f64(b[0], V, -INFINITY, s));
+  tp.end(s);
+  const KernelTimer t = timer(c, FST_KERNEL_SCORE_GEN);
+  int k = 0, batch = 8;
+  bool done = false;
+  while (!done && k < max_sweeps) {
+    const int n = batch < max_sweeps - k ? batch : max_sweeps - k;
+    HIP_TRY(hipMemsetAsync(dsc->rise, 0, (size_t)n * sizeof(unsigned long long), s));
+    t.begin(s);
+    for (int j = 0; j < n; ++j) {
+      const int x = (k + j) & 1, y = x ^ 1;
+      HIP_TRY(launch_sweep(SG, a[x], fwd ? a[y] : nullptr, b[x], bwd ? b[y] : nullptr,
+                           &dsc->rise[j], s));
+    }
+    t.end(s);
+    HIP_TRY(hipMemcpyAsync(c->h_ssc->rise, dsc->rise, (size_t)n * sizeof(unsigned long long),
+                           hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    FST_TRY(add_time(c, FST_KERNEL_SCORE_GEN, n));
+    for (int j = 0; j < n && !done; ++j) {
+      // the order key of a rise >= +0.0 is its bit pattern with the top bit set
+      const unsigned long long key = c->h_ssc->rise[j] & ~(1ull << 63);
+      double r;
+      memcpy(&r, &key, sizeof r);
+      if (r <= tol) {
+        done = true;
+        if (sweeps) *sweeps = k + j + 1;
+      }
+    }
+    k += n;
+    batch = 2 * batch < SWEEP_BATCH ? 2 * batch : SWEEP_BATCH;
+  }
+  if (c->timing) {
+    HIP_TRY(hipStreamSynchronize(s));  // the structure's events (no sweep may have run)
+    FST_TRY(add_time(c, FST_KERNEL_SCORE_PREP, 1));
+  }
+  // the last sweep wrote buffer k mod 2 (the values so far when none ran)
+  const double *fa = a[k & 1], *fb = b[k & 1];
+  if (alpha) HIP_TRY(hipMemcpyAsync(alpha, fa, (size_t)V * 8, hipMemcpyDeviceToDevice, s));
+  if (beta) HIP_TRY(hipMemcpyAsync(beta, fb, (size_t)V * 8, hipMemcpyDeviceToDevice, s));
+  if (fwd) FST_TRY(score_total(c, fa, d.accept, V, total, s));
+  else FST_TRY(score_total(c, fb, d.start, V, total, s));
+  c->have_score_times = c->timing;
+  return done ? FST_OK : FST_ERR_NOT_CONVERGED;
 }
 
 ScoreGraph plain_score_graph(const DevGraph &d) {
@@ -1555,7 +1645,7 @@ void fst_ctx_destroy(fst_ctx *c) {
                     &c->bInChain, &c->s_sc,     &c->s_owner, &c->s_extra, &c->s_inref,
                     &c->s_mbeg,   &c->s_mlen,   &c->s_mcur,  &c->s_marc,  &c->s_val,
                     &c->s_acc,    &c->s_pg,     &c->s_pidx,  &c->s_bcnt,  &c->s_bscan,
-                    &c->s_btotal, &c->s_mpos,   &c->u_off,   &c->u_src,   &c->u_dst,
+                    &c->s_btotal, &c->s_mpos,   &c->s_sweep, &c->u_off,   &c->u_src,   &c->u_dst,
                     &c->u_il,     &c->u_ol,     &c->u_w,     &c->u_start, &c->u_accept,
                     &c->u_items,  &c->seg,    &c->t_scal,  &c->t_aPerm, &c->t_aArc,
                     &c->t_aRec,   &c->t_bPerm,  &c->t_bArc,  &c->t_bRec,  &c->t_bLab,
@@ -1864,6 +1954,19 @@ int fst_score(fst_ctx *c, const fst_graph *G, double *alpha, double *beta, doubl
   return rc;
 }
 
+int fst_score_cyclic(fst_ctx *c, const fst_graph *G, double *alpha, double *beta,
+                     double *total, int32_t max_sweeps, double tol, int32_t *sweeps,
+                     void *stream) {
+  if (!c || !G || !total) return FST_ERR_INVALID_ARG;
+  DeviceGuard g(c->device);
+  if (!g.ok) return FST_ERR_HIP;
+  c->have_score_times = false;
+  int rc = score_cyclic_impl(c, G, alpha, beta, total, max_sweeps, tol, sweeps,
+                             reinterpret_cast<hipStream_t>(stream));
+  if (rc != FST_OK && rc != FST_ERR_NOT_CONVERGED) (void)hipGetLastError();
+  return rc;
+}
+
 int fst_score_posterior(fst_ctx *c, const fst_graph *G, const double *alpha, const double *beta,
                         const double *total, float scale, float *grad, void *stream) {
   if (!c || !G || !total) return FST_ERR_INVALID_ARG;
@@ -1981,6 +2084,7 @@ const char *fst_strerror(int code) {
     case FST_ERR_HIP: return "HIP runtime error";
     case FST_ERR_STATE: return "no successful fst_compose_run to fill from";
     case FST_ERR_CYCLIC: return "graph has a cycle (scores need an acyclic graph)";
+    case FST_ERR_NOT_CONVERGED: return "relaxation sweeps did not converge (path sums may diverge)";
     default: return "unknown error";
   }
 }

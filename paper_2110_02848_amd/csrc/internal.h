@@ -277,6 +277,9 @@ struct ScoreGraph {
   const int32_t *mbeg, *mlen, *marc;
 };
 
+// Relaxation sweeps of a score queued between two read-backs, at most.
+constexpr int SWEEP_BATCH = 64;
+
 // Device scalars of a score computation, read back by the host.
 struct ScoreScalars {
   uint32_t err, maxlab;      // validation
@@ -287,6 +290,7 @@ struct ScoreScalars {
   unsigned long long zmax, zlo, zhi;  // total: order key of the maximum, 128-bit sum
   uint32_t absmax, pad;         // scatter: bits of the largest |gradient|
   GenSlot G[3];
+  unsigned long long rise[SWEEP_BATCH];  // sweeps: order key of each sweep's largest rise
 };
 
 // One direction of the score recursion (forward: alpha from in-arcs;
@@ -622,6 +626,14 @@ hipError_t launch_score_seed(const ScoreArgs &S, bool forward, hipStream_t s);
 // Generation g of the forward (F) and / or backward (B) recursion: one kernel.
 hipError_t launch_score_generation(const ScoreArgs *F, const ScoreArgs *B, int g,
                                    hipStream_t s);
+// One relaxation sweep of the score recursions (graphs with cycles): ya[v]
+// = forward value of v from the previous values xa, yb[v] = backward value
+// from xb (a null output skips that direction; G needs the in-arc
+// structure); *incr = max(*incr, order key of the largest rise of a value).
+hipError_t launch_sweep(const ScoreGraph &G, const double *xa, double *ya, const double *xb,
+                        double *yb, unsigned long long *incr, hipStream_t s);
+// p[0 .. n) = x.
+hipError_t launch_fill_f64(double *p, long long n, double x, hipStream_t s);
 // *total = log-add of val[v] over the states with flag[v] (sc->zmax, zlo,
 // zhi zeroed).
 hipError_t launch_score_total(const double *val, const uint8_t *flag, int32_t V,

@@ -59,6 +59,9 @@ typedef unsigned long long ull;
 
 constexpr int32_t SCORE_LIGHT = 64;  // arcs a single thread pulls or notifies
 constexpr unsigned SCORE_GRID = 1024;
+// Workgroups of a relaxation sweep at most (each ends with one atomic on the
+// sweep's rise word).
+constexpr long long SWEEP_GRID = 512;
 // Structure passes take ST_ITEMS items per thread and round, their loads
 // issued before any store or atomic (which would otherwise make every load
 // wait for the previous item's store).
@@ -734,6 +737,83 @@ __global__ __launch_bounds__(NT) void k_score_init(ScoreArgs S) {
 }
 
 // ---------------------------------------------------------------------------
+// relaxation sweeps (graphs with cycles)
+// ---------------------------------------------------------------------------
+
+// The value of state v from the values x of the previous sweep: the exact
+// log-add of thread_pull over the terms x[other end] + w(e) of v's pull list
+// and, for a start (forward) or accepting (backward) state, its empty
+// path's 0.  The terms are formed twice (their maximum first).  Since every
+// step is the recursion's own, the sweeps reach on a graph without cycles
+// the recursion's values bit for bit.
+template <bool FWD>
+__device__ double sweep_value(const ScoreGraph &G, const double *x, int32_t v, bool init) {
+  const AList l = pull_list<FWD>(G, v);
+  auto term = [&](int32_t j) -> double {
+    const int32_t e = arc_at(G, l, j);
+    return x[FWD ? G.src[e] : G.dst[e]] + (double)G.w[e];
+  };
+  if (l.n == 1 && !init) return term(0);
+  double m = init ? 0.0 : -INFINITY;
+  for (int32_t j = 0; j < l.n; ++j) m = fmax(m, term(j));
+  if (m == -INFINITY || m == INFINITY) return m;
+  ull lo = 0, hi = 0;
+  if (init) acc_add(lo, hi, exp(0.0 - m));
+  for (int32_t j = 0; j < l.n; ++j) acc_add(lo, hi, exp(term(j) - m));
+  return acc_finish(m, lo, hi);
+}
+
+// How much a value rose in a sweep (0 if it did not; a value that leaves
+// -inf rises by +inf).
+__device__ __forceinline__ double rise(double before, double after) {
+  if (!(after > before)) return 0.0;
+  return before == -INFINITY ? INFINITY : after - before;
+}
+
+// One Jacobi sweep of both recursions over every state: ya = sweep of xa
+// (forward), yb = sweep of xb (backward); a direction whose output is null
+// is skipped.  *incr = max(*incr, order key of the largest rise), one
+// atomic per workgroup.
+__global__ __launch_bounds__(NT) void k_sweep(ScoreGraph G, const double *xa, double *ya,
+                                              const double *xb, double *yb, ull *incr) {
+  __shared__ ull s_m[NWAVES];
+  ull mk = 0;
+  for (long long v = (long long)blockIdx.x * NT + threadIdx.x; v < G.V;
+       v += (long long)gridDim.x * NT) {
+    double r = 0.0;
+    if (ya) {
+      const double a = sweep_value<true>(G, xa, (int32_t)v, G.start[v] != 0);
+      r = fmax(r, rise(xa[v], a));
+      ya[v] = a;
+    }
+    if (yb) {
+      const double b = sweep_value<false>(G, xb, (int32_t)v, G.accept[v] != 0);
+      r = fmax(r, rise(xb[v], b));
+      yb[v] = b;
+    }
+    const ull k = order_key(r);
+    mk = k > mk ? k : mk;
+  }
+#pragma unroll
+  for (int o = WAVE / 2; o > 0; o >>= 1) {
+    const ull t = __shfl_xor(mk, o);
+    mk = t > mk ? t : mk;
+  }
+  if (__lane_id() == 0) s_m[threadIdx.x / WAVE] = mk;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < NWAVES; ++w) mk = s_m[w] > mk ? s_m[w] : mk;
+    atomicMax(incr, mk);
+  }
+}
+
+__global__ __launch_bounds__(NT) void k_fill_f64(double *p, long long n, double x) {
+  for (long long i = (long long)blockIdx.x * NT + threadIdx.x; i < n;
+       i += (long long)gridDim.x * NT)
+    p[i] = x;
+}
+
+// ---------------------------------------------------------------------------
 // in-arc structure
 // ---------------------------------------------------------------------------
 
@@ -1404,6 +1484,20 @@ hipError_t launch_score_generation(const ScoreArgs *F, const ScoreArgs *B, int g
   if (F && B) k_score_gen2<<<2 * SCORE_GRID, NT, 0, s>>>(*F, *B, g);
   else if (F) k_score_gen<true><<<SCORE_GRID, NT, 0, s>>>(*F, g);
   else if (B) k_score_gen<false><<<SCORE_GRID, NT, 0, s>>>(*B, g);
+  return hipGetLastError();
+}
+
+hipError_t launch_sweep(const ScoreGraph &G, const double *xa, double *ya, const double *xb,
+                        double *yb, unsigned long long *incr, hipStream_t s) {
+  if (G.V == 0) return hipSuccess;
+  const long long b = ((long long)G.V + NT - 1) / NT;
+  k_sweep<<<(unsigned)(b < SWEEP_GRID ? b : SWEEP_GRID), NT, 0, s>>>(G, xa, ya, xb, yb, incr);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_f64(double *p, long long n, double x, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  k_fill_f64<<<grid_for(n), NT, 0, s>>>(p, n, x);
   return hipGetLastError();
 }
 

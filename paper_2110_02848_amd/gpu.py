@@ -24,6 +24,7 @@ FST_ERR_NOMEM = 4
 FST_ERR_HIP = 5
 FST_ERR_STATE = 6
 FST_ERR_CYCLIC = 7
+FST_ERR_NOT_CONVERGED = 8
 
 FST_OPT_MAX_WORKSPACE = 1
 FST_OPT_TIMING = 2
@@ -121,6 +122,11 @@ def load():
     lib.fst_score.argtypes = [ctypes.c_void_p, ctypes.POINTER(_Graph), ctypes.c_void_p,
                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     lib.fst_score.restype = ctypes.c_int
+    lib.fst_score_cyclic.argtypes = [ctypes.c_void_p, ctypes.POINTER(_Graph), ctypes.c_void_p,
+                                     ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                     ctypes.c_double, ctypes.POINTER(ctypes.c_int32),
+                                     ctypes.c_void_p]
+    lib.fst_score_cyclic.restype = ctypes.c_int
     lib.fst_score_posterior.argtypes = [ctypes.c_void_p, ctypes.POINTER(_Graph),
                                         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                         ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p]
@@ -404,6 +410,25 @@ class Composer:
                                  ctypes.c_void_p(total.data_ptr()), _stream_handle(stream))
         _check(rc, "fst_score")
         return dict(alpha=a, beta=b, total=total)
+
+    def score_cyclic(self, G, alpha=True, beta=True, max_sweeps=10000, tol=0.0, stream=None):
+        """The same scores of a graph that may have cycles, by relaxation
+        sweeps: dict(alpha, beta, total as in ``score``, sweeps: the number
+        of sweeps until none raised a value by more than ``tol``).  Raises
+        FstError(FST_ERR_NOT_CONVERGED) if that took more than max_sweeps."""
+        import torch
+        dev = f"cuda:{self.device}"
+        V = int(G["num_states"])
+        a = torch.empty(V, dtype=torch.float64, device=dev) if alpha else None
+        b = torch.empty(V, dtype=torch.float64, device=dev) if beta else None
+        total = torch.empty(1, dtype=torch.float64, device=dev)
+        n = ctypes.c_int32(0)
+        g = _graph_struct(G)
+        rc = self._lib.fst_score_cyclic(self._h, ctypes.byref(g), _ptr(a), _ptr(b),
+                                        ctypes.c_void_p(total.data_ptr()), int(max_sweeps),
+                                        float(tol), ctypes.byref(n), _stream_handle(stream))
+        _check(rc, "fst_score_cyclic")
+        return dict(alpha=a, beta=b, total=total, sweeps=int(n.value))
 
     def posterior(self, G, alpha, beta, total, scale=1.0, stream=None):
         """scale * d total / d w for every arc (float32 [E] tensor)."""
