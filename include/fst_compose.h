@@ -278,8 +278,8 @@ FST_API int fst_score(fst_ctx *ctx, const fst_graph *G, double *alpha, double *b
  * number.  On a graph without cycles the sweeps reach fst_score's values
  * bit for bit after at most (longest path + 2) sweeps.  Each sweep reads
  * every state's in-arcs and out-arcs once (one thread per state, so a state
- * with many arcs is summed by one thread), in batches of up to 64 sweeps
- * between read-backs.  Arguments, validation and outputs as in fst_score;
+ * with many arcs is summed by one thread), in batches of 8 to 64 sweeps
+ * between read-backs (a quarter of the sweeps so far).  Arguments, validation and outputs as in fst_score;
  * returns FST_ERR_NOT_CONVERGED (outputs: the last sweep's values) if no
  * sweep settled within max_sweeps (>= 0) sweeps, as when the sums diverge;
  * FST_ERR_INVALID_ARG for a negative max_sweeps or tol. */

@@ -457,9 +457,11 @@ int score_impl(fst_ctx *c, const fst_graph *G, double *alpha, double *beta, doub
 
 // Relaxation sweeps of both recursions (graphs with cycles), from every
 // value at -inf, in batches with one read-back of the batch's rises each,
-// until a sweep in which no value rose by more than tol.  The values after
-// the batch's last sweep are returned (later sweeps of a batch rise no
-// more than tol either, up to rounding).
+// until a sweep in which no value rose by more than tol.  A batch is a
+// quarter of the sweeps done so far (8 to SWEEP_BATCH), so the sweeps run
+// past the one that settled stay within about a quarter of the total.  The
+// values after the batch's last sweep are returned (later sweeps of a
+// batch rise no more than tol either, up to rounding).
 int score_cyclic_impl(fst_ctx *c, const fst_graph *G, double *alpha, double *beta,
                       double *total, int32_t max_sweeps, double tol, int32_t *sweeps,
                       hipStream_t s) {
@@ -492,9 +494,10 @@ int score_cyclic_impl(fst_ctx *c, const fst_graph *G, double *alpha, double *bet
   if (bwd) HIP_TRY(launch_fill_f64(b[0], V, -INFINITY, s));
   tp.end(s);
   const KernelTimer t = timer(c, FST_KERNEL_SCORE_GEN);
-  int k = 0, batch = 8;
+  int k = 0;
   bool done = false;
   while (!done && k < max_sweeps) {
+    const int batch = k / 4 < 8 ? 8 : (k / 4 > SWEEP_BATCH ? SWEEP_BATCH : k / 4);
     const int n = batch < max_sweeps - k ? batch : max_sweeps - k;
     HIP_TRY(hipMemsetAsync(dsc->rise, 0, (size_t)n * sizeof(unsigned long long), s));
     t.begin(s);
@@ -519,7 +522,6 @@ int score_cyclic_impl(fst_ctx *c, const fst_graph *G, double *alpha, double *bet
       }
     }
     k += n;
-    batch = 2 * batch < SWEEP_BATCH ? 2 * batch : SWEEP_BATCH;
   }
   if (c->timing) {
     HIP_TRY(hipStreamSynchronize(s));  // the structure's events (no sweep may have run)
