@@ -255,7 +255,8 @@ FST_API int fst_compose_kernel_time(const fst_ctx *ctx, int kernel, float *ms, i
  * beta over start states).  G's structure is validated as in
  * fst_compose_run (labels are not read: scores do not depend on them).  Queued on
  * `stream`; blocks on small readbacks as the recursion advances.  Returns
- * FST_ERR_CYCLIC (outputs undefined) if G has a cycle.  Weights must be
+ * FST_ERR_CYCLIC (outputs undefined) if G has a cycle (fst_score_cyclic
+ * below takes such graphs).  Weights must be
  * finite (an infinite or NaN weight gives unspecified values, never a
  * fault).  G must stay valid until the work has completed. */
 FST_API int fst_score(fst_ctx *ctx, const fst_graph *G, double *alpha, double *beta,
