@@ -275,6 +275,10 @@ struct ScoreGraph {
   const uint8_t *start, *accept;
   const int32_t *inref;
   const int32_t *mbeg, *mlen, *marc;
+  // relaxation sweeps only: the source and weight of the arc at each merge
+  // list position (msrc[p] = src[marc[p]], mw[p] = w[marc[p]]), else null
+  const int32_t *msrc;
+  const float *mw;
 };
 
 // Relaxation sweeps of a score queued between two read-backs, at most.
@@ -634,6 +638,10 @@ hipError_t launch_sweep(const ScoreGraph &G, const double *xa, double *ya, const
                         double *yb, unsigned long long *incr, hipStream_t s);
 // p[0 .. n) = x.
 hipError_t launch_fill_f64(double *p, long long n, double x, hipStream_t s);
+// msrc[p] = src[marc[p]], mw[p] = w[marc[p]] for the merge list positions
+// p < sc->mtotal (at most E).
+hipError_t launch_merge_gather(const ScoreGraph &G, const ScoreScalars *sc, int32_t *msrc,
+                               float *mw, hipStream_t s);
 // *total = log-add of val[v] over the states with flag[v] (sc->zmax, zlo,
 // zhi zeroed).
 hipError_t launch_score_total(const double *val, const uint8_t *flag, int32_t V,

@@ -749,8 +749,10 @@ __global__ __launch_bounds__(NT) void k_score_init(ScoreArgs S) {
 template <bool FWD>
 __device__ double sweep_value(const ScoreGraph &G, const double *x, int32_t v, bool init) {
   const AList l = pull_list<FWD>(G, v);
+  // a merge's in-arcs are read from the copies aligned with its list
   auto term = [&](int32_t j) -> double {
-    const int32_t e = arc_at(G, l, j);
+    if (FWD && l.ind) return x[G.msrc[l.beg + j]] + (double)G.mw[l.beg + j];
+    const int32_t e = l.beg + j;
     return x[FWD ? G.src[e] : G.dst[e]] + (double)G.w[e];
   };
   if (l.n == 1 && !init) return term(0);
@@ -804,6 +806,17 @@ __global__ __launch_bounds__(NT) void k_sweep(ScoreGraph G, const double *xa, do
   if (threadIdx.x == 0) {
     for (int w = 1; w < NWAVES; ++w) mk = s_m[w] > mk ? s_m[w] : mk;
     atomicMax(incr, mk);
+  }
+}
+
+__global__ __launch_bounds__(NT) void k_merge_gather(ScoreGraph G, const ScoreScalars *sc,
+                                                     int32_t *msrc, float *mw) {
+  const long long n = (long long)sc->mtotal;
+  for (long long p = (long long)blockIdx.x * NT + threadIdx.x; p < n && p < G.E;
+       p += (long long)gridDim.x * NT) {
+    const int32_t e = G.marc[p];
+    msrc[p] = G.src[e];
+    mw[p] = G.w[e];
   }
 }
 
@@ -1492,6 +1505,13 @@ hipError_t launch_sweep(const ScoreGraph &G, const double *xa, double *ya, const
   if (G.V == 0) return hipSuccess;
   const long long b = ((long long)G.V + NT - 1) / NT;
   k_sweep<<<(unsigned)(b < SWEEP_GRID ? b : SWEEP_GRID), NT, 0, s>>>(G, xa, ya, xb, yb, incr);
+  return hipGetLastError();
+}
+
+hipError_t launch_merge_gather(const ScoreGraph &G, const ScoreScalars *sc, int32_t *msrc,
+                               float *mw, hipStream_t s) {
+  if (G.E == 0) return hipSuccess;
+  k_merge_gather<<<grid_for(G.E), NT, 0, s>>>(G, sc, msrc, mw);
   return hipGetLastError();
 }
 
