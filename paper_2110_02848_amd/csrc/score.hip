@@ -62,6 +62,8 @@ constexpr unsigned SCORE_GRID = 1024;
 // Workgroups of a relaxation sweep at most (each ends with one atomic on the
 // sweep's rise word).
 constexpr long long SWEEP_GRID = 512;
+// Pull lists of at most this many terms are loaded once into registers.
+constexpr int SWEEP_REGS = 8;
 // Structure passes take ST_ITEMS items per thread and round, their loads
 // issued before any store or atomic (which would otherwise make every load
 // wait for the previous item's store).
@@ -757,9 +759,24 @@ __device__ double sweep_value(const ScoreGraph &G, const double *x, int32_t v, b
   };
   if (l.n == 1 && !init) return term(0);
   double m = init ? 0.0 : -INFINITY;
+  ull lo = 0, hi = 0;
+  if (l.n <= SWEEP_REGS) {
+    // few terms: each loaded once, kept in registers
+    double t[SWEEP_REGS];
+#pragma unroll
+    for (int j = 0; j < SWEEP_REGS; ++j) {
+      t[j] = j < l.n ? term(j) : -INFINITY;
+      m = fmax(m, t[j]);
+    }
+    if (m == -INFINITY || m == INFINITY) return m;
+    if (init) acc_add(lo, hi, exp(0.0 - m));
+#pragma unroll
+    for (int j = 0; j < SWEEP_REGS; ++j)
+      if (j < l.n) acc_add(lo, hi, exp(t[j] - m));
+    return acc_finish(m, lo, hi);
+  }
   for (int32_t j = 0; j < l.n; ++j) m = fmax(m, term(j));
   if (m == -INFINITY || m == INFINITY) return m;
-  ull lo = 0, hi = 0;
   if (init) acc_add(lo, hi, exp(0.0 - m));
   for (int32_t j = 0; j < l.n; ++j) acc_add(lo, hi, exp(term(j) - m));
   return acc_finish(m, lo, hi);
