@@ -290,9 +290,10 @@ FST_API int fst_score_cyclic(fst_ctx *ctx, const fst_graph *G, double *alpha, do
 
 /* Arc posteriors times `scale`: grad[e] = scale * exp(alpha[src e] + w(e) +
  * beta[dst e] - *total), the derivative of scale * total by w(e) (0 for every
- * arc when *total is -inf).  alpha, beta, total come from fst_score on the
- * same G; grad has E floats (device).  G is validated.  Asynchronous after
- * the validation readback. */
+ * arc when *total is -inf).  alpha, beta, total come from fst_score or
+ * fst_score_cyclic on the same G (with cycles, an arc's posterior is its
+ * expected number of uses and can exceed 1); grad has E floats (device).
+ * G is validated.  Asynchronous after the validation readback. */
 FST_API int fst_score_posterior(fst_ctx *ctx, const fst_graph *G, const double *alpha,
                                 const double *beta, const double *total, float scale,
                                 float *grad, void *stream);

@@ -83,8 +83,13 @@ def score_cyclic(G):
     """dict(alpha[V], beta[V], total) of a graph that may have cycles;
     raises DivergeError when its path sums do not converge."""
     V, src, dst, w = _arcs(G)
-    start = np.asarray(G["start"], np.uint8) != 0
-    accept = np.asarray(G["accept"], np.uint8) != 0
+    return scores_of(V, src, dst, w, np.asarray(G["start"], np.uint8) != 0,
+                     np.asarray(G["accept"], np.uint8) != 0)
+
+
+def scores_of(V, src, dst, w, start, accept):
+    """The same from arc arrays with float64 weights w (arc e from src[e]
+    to dst[e]) and boolean start / accept arrays."""
     alpha = np.full(V, -np.inf)
     beta = np.full(V, -np.inf)
     acc = _reach(V, src, dst, start)

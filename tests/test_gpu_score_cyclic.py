@@ -168,3 +168,24 @@ def test_empty_and_unreachable(comp):
     with pytest.raises(gpu.FstError) as e:
         _run(comp, dict(G, start=np.array([1, 0, 1, 0], np.uint8)), max_sweeps=200)
     assert e.value.code == gpu.FST_ERR_NOT_CONVERGED
+
+
+def test_posteriors_of_a_cyclic_graph(comp):
+    """fst_score_posterior with fst_score_cyclic's scores: each arc's
+    expected number of uses (above 1 on cycles), the total's gradient
+    (pinned by finite differences on the CPU), against the oracle's scores
+    (float32 results of float64 arithmetic: 1e-6 relative covers the float32
+    rounding and the scores' error passed through exp)."""
+    import torch
+    from paper_2110_02848_amd import gpu
+    G = synth.random_cyclic(9, 500, degree=3, mass=0.6, hubs=2, hub_degree=40)
+    dG = gpu.to_device(G)
+    r = comp.score_cyclic(dG)
+    grad = comp.posterior(dG, r["alpha"], r["beta"], r["total"])
+    torch.cuda.synchronize()
+    grad = grad.cpu().numpy().astype(np.float64)
+    ref = cyclic.score_cyclic(G)
+    V, src, dst, w = cyclic._arcs(G)
+    want = np.exp(ref["alpha"][src] + w + ref["beta"][dst] - ref["total"])
+    assert np.allclose(grad, want, rtol=1e-6, atol=0.0)
+    assert want.max() > 0.0

@@ -154,3 +154,31 @@ def test_generator_sums_converge():
         G = synth.random_cyclic(seed, 200, hubs=2, hub_degree=60)
         r = cyclic.score_cyclic(G)
         assert math.isfinite(r["total"])
+
+
+def test_posterior_is_the_gradient_of_the_total():
+    """d total / d w(e) = exp(alpha[src e] + w(e) + beta[dst e] - total), the
+    expected number of uses of arc e (above 1 on a cycle), against central
+    finite differences of the oracle's total in float64 weights."""
+    # a random graph, and a cycle of mass 0.9 that paths go round 9 times on
+    # average (0 -> 1 -> 0, exit 1 -> 2): arc 0 -> 1 is taken 10 times, the
+    # back arc 9 times, the exit once
+    cyc = _g(3, [(0, 1, _w(math.log(0.95))), (1, 0, _w(math.log(0.9 / 0.95))),
+                 (1, 2, _w(-1.0))], [0], [2])
+    for G, most in ((synth.random_cyclic(5, 12, degree=3, mass=0.7, p_accept=0.3), None),
+                    (cyc, [10.0, 9.0, 1.0])):
+        V, src, dst, w = cyclic._arcs(G)
+        start = np.asarray(G["start"]) != 0
+        accept = np.asarray(G["accept"]) != 0
+        r = cyclic.scores_of(V, src, dst, w, start, accept)
+        post = np.exp(r["alpha"][src] + w + r["beta"][dst] - r["total"])
+        h = 1e-6
+        for e in range(len(w)):
+            wp, wm = w.copy(), w.copy()
+            wp[e] += h
+            wm[e] -= h
+            fd = (cyclic.scores_of(V, src, dst, wp, start, accept)["total"]
+                  - cyclic.scores_of(V, src, dst, wm, start, accept)["total"]) / (2 * h)
+            assert abs(fd - post[e]) < 1e-6 * max(1.0, post[e]), (e, fd, post[e])
+        if most is not None:
+            assert np.allclose(post, most, rtol=1e-6, atol=0), post
