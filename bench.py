@@ -26,6 +26,11 @@ as the library's own output, with FST_OPT_VALIDATE off).
 
 ``--task batch --batch N`` composes N utterances (emissions of T=500 frames,
 different seeds) with the one lexicon in a single pass per step.
+
+``--task score_cyclic`` measures the scores of a graph with cycles
+(fst_score_cyclic: relaxation sweeps until no value rises): one step = both
+scores of a seeded random graph of 10^6 states with 3 out-arcs each (arc
+probabilities adding to 1/2 per state), inputs resident in HBM.
 """
 from __future__ import annotations
 
@@ -422,6 +427,63 @@ def run_compose3(args, comp, copy_gbs):
     return out
 
 
+CYCLIC_V, CYCLIC_DEGREE = 1_000_000, 3
+
+
+def run_score_cyclic(args, comp, copy_gbs):
+    import torch
+    from paper_2110_02848_amd import gpu, synth
+    G = synth.random_cyclic(args.seed, CYCLIC_V, degree=CYCLIC_DEGREE, mass=0.5)
+    V, E = int(G["num_states"]), len(G["src"])
+    dG = gpu.to_device(G)
+
+    def step():
+        return comp.score_cyclic(dG)
+
+    for _ in range(args.warmup):
+        step()
+    ms_wall, per_step, r = timed_steps(step, args.steps)
+    # algorithmic bytes of one sweep: per direction, per arc its neighbour,
+    # weight and the neighbour's value (16 B); per state its list bounds and
+    # flag, its value read and written (25 B).  Once per call, the in-arc
+    # structure (arc targets read three times, owner and merge positions
+    # written: 32 B per arc, 16 B per state), the merge lists' source and
+    # weight copies (20 B per arc) and the two value buffers set to -inf
+    # (16 B per state)
+    comp.set_option(gpu.FST_OPT_TIMING, 1)
+    step()
+    torch.cuda.synchronize()
+    runs = comp.score_kernel_times()["score_gen"][1]
+    comp.set_option(gpu.FST_OPT_TIMING, 0)
+    kb = {"score_gen": runs * 2 * (16 * E + 25 * V), "score_prep": 52 * E + 32 * V}
+    kernels = instrumented_kernels(comp, step, args.steps, gpu.SCORE_KERNELS,
+                                   comp.score_kernel_times, kb)
+    name = f"cyclic-V{V}-d{CYCLIC_DEGREE}"
+    return {
+        "metric": "scored arcs/sec (both scores of a graph with cycles, relaxation sweeps)",
+        "value": E / (ms_wall * 1e-3),
+        "unit": "arcs/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_wall,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {"workload": f"random graph with cycles, V={V}, {CYCLIC_DEGREE} arcs per state, "
+                               "arc probabilities 1/2 per state", "name": name,
+                   "seed": args.seed, "task": "score_cyclic", "V": V, "E": E,
+                   "sweeps_to_settle": r["sweeps"], "sweeps_run": runs,
+                   "inputs_sha256": synth.graph_sha256(G)},
+        "ms_per_step_device": percentiles(per_step),
+        "total": float(r["total"].item()),
+        "kernels": kernels,
+        "roofline": roofline_of(kernels, name, copy_gbs, "score_cyclic"),
+    }
+
+
 def run_batch(args, comp):
     import torch
     from paper_2110_02848_amd import gpu, synth
@@ -511,12 +573,13 @@ def main():
                     help="order of the two searches (Algorithm 1 computes the co-accessible "
                          "set first; concurrent, the default, runs both side by side); the "
                          "result is the same")
-    ap.add_argument("--task", choices=("compose", "score", "batch", "compose3"),
+    ap.add_argument("--task", choices=("compose", "score", "batch", "compose3", "score_cyclic"),
                     default="compose",
                     help="compose: the composition itself; score: scores and operand "
                          "gradients of the composed graph; batch: --batch utterances "
                          "composed with one lexicon per step; compose3: emissions o lexicon "
-                         "o grammar composed at once (three inputs)")
+                         "o grammar composed at once (three inputs); score_cyclic: scores "
+                         "of a random graph with cycles")
     ap.add_argument("--batch", type=int, default=8)
     ap.add_argument("--copy-probe-mb", type=int, default=256,
                     help="size of the device-to-device copy timed for the copy ceiling (and "
@@ -533,12 +596,13 @@ def main():
     import torch
     from paper_2110_02848_amd import gpu, synth
 
-    if args.task == "compose3":
+    if args.task in ("compose3", "score_cyclic"):
         comp = gpu.Composer(0)
         copy_gbs = copy_ceiling(args.copy_probe_mb) if args.copy_probe_mb > 0 else None
         if args.calibrate_gather:
             calibrate_gather()
-        out = run_compose3(args, comp, copy_gbs)
+        out = (run_compose3 if args.task == "compose3" else run_score_cyclic)(args, comp,
+                                                                               copy_gbs)
         comp.close()
         print(json.dumps(out), flush=True)
         return

@@ -422,16 +422,17 @@ def tiny_random(rng, V, max_degree, n_sym, p_eps, p_accept=0.4, n_start=1):
 def random_cyclic(seed, V, degree=3, mass=0.5, n_start=2, p_accept=0.2, hubs=0,
                   hub_degree=0):
     """Seeded random graph with cycles whose path sums converge (inputs of
-    the cyclic-score tests).
+    the cyclic-score tests and benchmark).
 
-    Every state gets ``degree`` out-arcs to uniform destinations (self-loops
-    and parallel arcs allowed); ``hubs`` states (drawn at random) also get
-    ``hub_degree`` in-arcs from random states.  A state's out-arc weights are
-    log(mass * p) for p a softmax of N(0, 1) draws over its arcs, rounded to
-    binary32, so the probabilities of a state's arcs add to about ``mass``
-    (< 1: the spectral radius of the arc matrix stays below 1).  Labels are
-    1.  ``n_start`` distinct start states; accepting states at rate p_accept,
-    at least one."""
+    Every state gets ``degree`` (>= 1) out-arcs to uniform destinations
+    (self-loops and parallel arcs allowed); ``hubs`` states (drawn at random)
+    also get ``hub_degree`` in-arcs from random states.  A state's out-arc
+    weights are log(mass * p) for p a softmax of N(0, 1) draws over its
+    arcs, rounded to binary32, so the probabilities of a state's arcs add to
+    about ``mass`` (< 1: the spectral radius of the arc matrix stays below
+    1).  Labels are 1.  ``n_start`` distinct start states; accepting states
+    at rate p_accept, at least one."""
+    assert degree >= 1
     rng = np.random.default_rng(np.random.SeedSequence([11, int(seed)]))
     src = np.repeat(np.arange(V, dtype=np.int64), degree)
     dst = rng.integers(0, V, size=V * degree)
@@ -442,19 +443,19 @@ def random_cyclic(seed, V, degree=3, mass=0.5, n_start=2, p_accept=0.2, hubs=0,
     z = rng.standard_normal(len(src))
     order = np.argsort(src, kind="stable")
     src, dst, z = src[order], dst[order], z[order]
-    w = np.empty(len(src))
-    for v in range(V):
-        lo, hi = np.searchsorted(src, [v, v + 1])
-        if hi > lo:
-            e = np.exp(z[lo:hi] - z[lo:hi].max())
-            w[lo:hi] = np.log(mass * e / e.sum())
-    w = w.astype(np.float32)
-    starts = rng.choice(V, size=min(n_start, V), replace=False)
-    acc = np.flatnonzero(rng.random(V) < p_accept)
-    if len(acc) == 0:
-        acc = np.array([int(rng.integers(0, V))])
-    arcs = [(int(a), int(b), 1, 1, float(c)) for a, b, c in zip(src, dst, w)]
-    return from_arcs(V, arcs, start=sorted(int(x) for x in starts), accept=acc.tolist())
+    first = np.searchsorted(src, np.arange(V))  # every state has an arc
+    e = np.exp(z - np.maximum.reduceat(z, first)[src])
+    w = np.log(mass * e / np.add.reduceat(e, first)[src]).astype(np.float32)
+    start = np.zeros(V, np.uint8)
+    start[rng.choice(V, size=min(n_start, V), replace=False)] = 1
+    accept = (rng.random(V) < p_accept).astype(np.uint8)
+    if not accept.any():
+        accept[int(rng.integers(0, V))] = 1
+    E = len(src)
+    off = np.searchsorted(src, np.arange(V + 1)).astype(np.int32)
+    return dict(num_states=V, arc_offset=off, src=src.astype(np.int32),
+                dst=dst.astype(np.int32), ilabel=np.ones(E, np.int32),
+                olabel=np.ones(E, np.int32), weight=w, start=start, accept=accept)
 
 
 def random_dag(seed, V, mean_out=2.0, window=16, hubs=0, hub_degree=0, p_global=0.1,
