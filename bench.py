@@ -446,16 +446,15 @@ def run_score_cyclic(args, comp, copy_gbs):
     # algorithmic bytes of one sweep: per direction, per arc its neighbour,
     # weight and the neighbour's value (16 B); per state its list bounds and
     # flag, its value read and written (25 B).  Once per call, the in-arc
-    # structure (arc targets read three times, owner and merge positions
-    # written: 32 B per arc, 16 B per state), the merge lists' source and
-    # weight copies (20 B per arc) and the two value buffers set to -inf
-    # (16 B per state)
+    # CSR (targets read twice, sources and weights read and written: 24 B
+    # per arc, plus the cursors; the counts and offsets, 16 B per state) and
+    # the two value buffers set to -inf (16 B per state)
     comp.set_option(gpu.FST_OPT_TIMING, 1)
     step()
     torch.cuda.synchronize()
     runs = comp.score_kernel_times()["score_gen"][1]
     comp.set_option(gpu.FST_OPT_TIMING, 0)
-    kb = {"score_gen": runs * 2 * (16 * E + 25 * V), "score_prep": 52 * E + 32 * V}
+    kb = {"score_gen": runs * 2 * (16 * E + 25 * V), "score_prep": 28 * E + 32 * V}
     kernels = instrumented_kernels(comp, step, args.steps, gpu.SCORE_KERNELS,
                                    comp.score_kernel_times, kb)
     name = f"cyclic-V{V}-d{CYCLIC_DEGREE}"

@@ -66,7 +66,7 @@ struct fst_ctx {
   // score workspace
   DevBuf s_pg, s_pidx, s_bcnt, s_bscan, s_btotal;  // grouped scatter
   DevBuf s_sc, s_owner, s_extra, s_inref, s_mbeg, s_mlen, s_mcur, s_marc, s_val, s_acc,
-      s_mpos, s_sweep, s_msrc, s_mw;
+      s_mpos, s_sweep, s_ioff, s_isrc, s_iw;
   // batches: the union of the A graphs, item tables, segment sums
   DevBuf u_off, u_src, u_dst, u_il, u_ol, u_w, u_start, u_accept, u_items, seg;
   // three-input composition
@@ -462,6 +462,8 @@ int score_impl(fst_ctx *c, const fst_graph *G, double *alpha, double *beta, doub
 // past the one that settled stay within about a quarter of the total.  The
 // values after the batch's last sweep are returned (later sweeps of a
 // batch rise no more than tol either, up to rounding).
+ScoreGraph plain_score_graph(const DevGraph &d);
+
 int score_cyclic_impl(fst_ctx *c, const fst_graph *G, double *alpha, double *beta,
                       double *total, int32_t max_sweeps, double tol, int32_t *sweeps,
                       hipStream_t s) {
@@ -485,13 +487,17 @@ int score_cyclic_impl(fst_ctx *c, const fst_graph *G, double *alpha, double *bet
   }
   const KernelTimer tp = timer(c, FST_KERNEL_SCORE_PREP);
   tp.begin(s);
-  ScoreGraph SG = {};
-  FST_TRY(score_structure(c, d, SG, s));
-  FST_TRY(ensure(c, c->s_msrc, (size_t)d.E * 4));
-  FST_TRY(ensure(c, c->s_mw, (size_t)d.E * 4));
-  SG.msrc = as<int32_t>(c->s_msrc);
-  SG.mw = as<float>(c->s_mw);
-  HIP_TRY(launch_merge_gather(SG, dsc, as<int32_t>(c->s_msrc), as<float>(c->s_mw), s));
+  ScoreGraph SG = plain_score_graph(d);
+  FST_TRY(ensure(c, c->s_ioff, ((size_t)V + 1) * 4));
+  FST_TRY(ensure(c, c->s_isrc, (size_t)d.E * 4));
+  FST_TRY(ensure(c, c->s_iw, (size_t)d.E * 4));
+  FST_TRY(ensure(c, c->s_inref, (size_t)V * 4));  // the placing cursors
+  FST_TRY(ensure(c, c->scan_tmp, scan_temp_bytes((size_t)V + 1)));
+  SG.ioff = as<int32_t>(c->s_ioff);
+  SG.isrc = as<int32_t>(c->s_isrc);
+  SG.iw = as<float>(c->s_iw);
+  HIP_TRY(launch_in_csr(SG, as<int32_t>(c->s_ioff), as<int32_t>(c->s_isrc), as<float>(c->s_iw),
+                        as<int32_t>(c->s_inref), c->scan_tmp.p, &dsc->mtotal, s));
   FST_TRY(ensure(c, c->s_sweep, (size_t)V * 4 * sizeof(double)));
   double *a[2] = {as<double>(c->s_sweep), as<double>(c->s_sweep) + V};
   double *b[2] = {a[1] + V, a[1] + 2 * (size_t)V};
@@ -1652,7 +1658,7 @@ void fst_ctx_destroy(fst_ctx *c) {
                     &c->bInChain, &c->s_sc,     &c->s_owner, &c->s_extra, &c->s_inref,
                     &c->s_mbeg,   &c->s_mlen,   &c->s_mcur,  &c->s_marc,  &c->s_val,
                     &c->s_acc,    &c->s_pg,     &c->s_pidx,  &c->s_bcnt,  &c->s_bscan,
-                    &c->s_btotal, &c->s_mpos,   &c->s_sweep, &c->s_msrc, &c->s_mw, &c->u_off,   &c->u_src,   &c->u_dst,
+                    &c->s_btotal, &c->s_mpos,   &c->s_sweep, &c->s_ioff, &c->s_isrc, &c->s_iw, &c->u_off,   &c->u_src,   &c->u_dst,
                     &c->u_il,     &c->u_ol,     &c->u_w,     &c->u_start, &c->u_accept,
                     &c->u_items,  &c->seg,    &c->t_scal,  &c->t_aPerm, &c->t_aArc,
                     &c->t_aRec,   &c->t_bPerm,  &c->t_bArc,  &c->t_bRec,  &c->t_bLab,

@@ -275,10 +275,11 @@ struct ScoreGraph {
   const uint8_t *start, *accept;
   const int32_t *inref;
   const int32_t *mbeg, *mlen, *marc;
-  // relaxation sweeps only: the source and weight of the arc at each merge
-  // list position (msrc[p] = src[marc[p]], mw[p] = w[marc[p]]), else null
-  const int32_t *msrc;
-  const float *mw;
+  // relaxation sweeps only (else null): the in-arcs as a CSR by target,
+  // the in-arcs of v at [ioff[v], ioff[v + 1]) with their sources isrc and
+  // weights iw (in no particular order)
+  const int32_t *ioff, *isrc;
+  const float *iw;
 };
 
 // Relaxation sweeps of a score queued between two read-backs, at most.
@@ -638,10 +639,12 @@ hipError_t launch_sweep(const ScoreGraph &G, const double *xa, double *ya, const
                         double *yb, unsigned long long *incr, hipStream_t s);
 // p[0 .. n) = x.
 hipError_t launch_fill_f64(double *p, long long n, double x, hipStream_t s);
-// msrc[p] = src[marc[p]], mw[p] = w[marc[p]] for the merge list positions
-// p < sc->mtotal (at most E).
-hipError_t launch_merge_gather(const ScoreGraph &G, const ScoreScalars *sc, int32_t *msrc,
-                               float *mw, hipStream_t s);
+// The in-arc CSR of G for the sweeps (counting by target, a scan, then
+// each arc placed with an atomic cursor): ioff (V + 1 words), isrc and iw (E
+// each), cur (V words of scratch); scan_temp of scan_temp_bytes(V) bytes.
+hipError_t launch_in_csr(const ScoreGraph &G, int32_t *ioff, int32_t *isrc, float *iw,
+                         int32_t *cur, void *scan_temp, unsigned long long *total_dev,
+                         hipStream_t s);
 // *total = log-add of val[v] over the states with flag[v] (sc->zmax, zlo,
 // zhi zeroed).
 hipError_t launch_score_total(const double *val, const uint8_t *flag, int32_t V,

@@ -750,12 +750,12 @@ __global__ __launch_bounds__(NT) void k_score_init(ScoreArgs S) {
 // the recursion's values bit for bit.
 template <bool FWD>
 __device__ double sweep_value(const ScoreGraph &G, const double *x, int32_t v, bool init) {
-  const AList l = pull_list<FWD>(G, v);
-  // a merge's in-arcs are read from the copies aligned with its list
+  // forward: the in-arc CSR; backward: the out-arcs
+  const int32_t b = FWD ? G.ioff[v] : G.off[v];
+  const AList l = AList{b, (FWD ? G.ioff[v + 1] : G.off[v + 1]) - b, false};
   auto term = [&](int32_t j) -> double {
-    if (FWD && l.ind) return x[G.msrc[l.beg + j]] + (double)G.mw[l.beg + j];
-    const int32_t e = l.beg + j;
-    return x[FWD ? G.src[e] : G.dst[e]] + (double)G.w[e];
+    const int32_t p = l.beg + j;
+    return FWD ? x[G.isrc[p]] + (double)G.iw[p] : x[G.dst[p]] + (double)G.w[p];
   };
   if (l.n == 1 && !init) return term(0);
   double m = init ? 0.0 : -INFINITY;
@@ -826,14 +826,22 @@ __global__ __launch_bounds__(NT) void k_sweep(ScoreGraph G, const double *xa, do
   }
 }
 
-__global__ __launch_bounds__(NT) void k_merge_gather(ScoreGraph G, const ScoreScalars *sc,
-                                                     int32_t *msrc, float *mw) {
-  const long long n = (long long)sc->mtotal;
-  for (long long p = (long long)blockIdx.x * NT + threadIdx.x; p < n && p < G.E;
-       p += (long long)gridDim.x * NT) {
-    const int32_t e = G.marc[p];
-    msrc[p] = G.src[e];
-    mw[p] = G.w[e];
+// In-arc CSR: the in-degrees (one atomic per arc), then, after a scan,
+// every arc placed at its target's cursor.
+__global__ __launch_bounds__(NT) void k_in_count(ScoreGraph G, int32_t *cnt) {
+  for (long long e = (long long)blockIdx.x * NT + threadIdx.x; e < G.E;
+       e += (long long)gridDim.x * NT)
+    atomicAdd(cnt + G.dst[e], 1);
+}
+
+__global__ __launch_bounds__(NT) void k_in_place(ScoreGraph G, const int32_t *ioff,
+                                                 int32_t *cur, int32_t *isrc, float *iw) {
+  for (long long e = (long long)blockIdx.x * NT + threadIdx.x; e < G.E;
+       e += (long long)gridDim.x * NT) {
+    const int32_t d = G.dst[e];
+    const int32_t p = ioff[d] + atomicAdd(cur + d, 1);
+    isrc[p] = G.src[e];
+    iw[p] = G.w[e];
   }
 }
 
@@ -1525,10 +1533,21 @@ hipError_t launch_sweep(const ScoreGraph &G, const double *xa, double *ya, const
   return hipGetLastError();
 }
 
-hipError_t launch_merge_gather(const ScoreGraph &G, const ScoreScalars *sc, int32_t *msrc,
-                               float *mw, hipStream_t s) {
-  if (G.E == 0) return hipSuccess;
-  k_merge_gather<<<grid_for(G.E), NT, 0, s>>>(G, sc, msrc, mw);
+hipError_t launch_in_csr(const ScoreGraph &G, int32_t *ioff, int32_t *isrc, float *iw,
+                         int32_t *cur, void *scan_temp, unsigned long long *total_dev,
+                         hipStream_t s) {
+  hipError_t e = hipMemsetAsync(ioff, 0, ((size_t)G.V + 1) * 4, s);
+  if (e != hipSuccess) return e;
+  if ((e = hipMemsetAsync(cur, 0, (size_t)G.V * 4, s)) != hipSuccess) return e;
+  if (G.E) {
+    k_in_count<<<grid_for(G.E), NT, 0, s>>>(G, ioff);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  // ioff[v] = in-arcs of the states before v; ioff[V] = E
+  e = scan_u32(reinterpret_cast<const uint32_t *>(ioff), reinterpret_cast<uint32_t *>(ioff),
+               (size_t)G.V, true, total_dev, scan_temp, s);
+  if (e != hipSuccess || G.E == 0) return e;
+  k_in_place<<<grid_for(G.E), NT, 0, s>>>(G, ioff, cur, isrc, iw);
   return hipGetLastError();
 }
 
