@@ -115,3 +115,18 @@ PINNED_SHA256 = {
 def test_inputs_pinned(name):
     A, B = synth.workload(name, 0)
     assert (synth.graph_sha256(A), synth.graph_sha256(B)) == PINNED_SHA256[name]
+
+
+def test_cyclic_inputs_pinned_and_convergent():
+    """The graph with cycles that ``bench.py --task score_cyclic`` scores
+    (seed 0, 10^6 states, 3 arcs each): its SHA-256 as recorded when the
+    generator was written, and every state's arc probabilities adding to
+    the requested mass (so the path sums converge)."""
+    G = synth.random_cyclic(0, 1_000_000, degree=3, mass=0.5)
+    assert synth.graph_sha256(G) == \
+        "4f0ee4bf88467a1ca7e86c20062626b47b37d508699aad64ba4b4d4a3a513baf"
+    small = synth.random_cyclic(1, 500, degree=3, mass=0.5, hubs=2, hub_degree=40)
+    p = np.exp(small["weight"].astype(np.float64))
+    mass = np.add.reduceat(p, small["arc_offset"][:-1])
+    assert np.allclose(mass, 0.5, rtol=1e-6)
+    assert np.all(np.diff(small["arc_offset"]) >= 3)
