@@ -189,3 +189,28 @@ def test_posteriors_of_a_cyclic_graph(comp):
     want = np.exp(ref["alpha"][src] + w + ref["beta"][dst] - ref["total"])
     assert np.allclose(grad, want, rtol=1e-6, atol=0.0)
     assert want.max() > 0.0
+
+
+def test_equals_fst_score_bitwise_on_composed_lexicon(comp):
+    """C = emissions(T=100) o lexicon(W=1000): 0.59 M states, roots with
+    about 10^3 in-arcs (pull lists longer than the register path); the
+    sweeps reach fst_score's values bit for bit, with validation off and
+    timing on (as a training loop scoring its own output would run)."""
+    import torch
+    from paper_2110_02848_amd import gpu
+    A, B = synth.workload("lexicon-T100-W1000", 0)
+    C = comp.compose(gpu.to_device(A), gpu.to_device(B), provenance=False, keys=False)
+    torch.cuda.synchronize()
+    comp.set_option(gpu.FST_OPT_VALIDATE, 0)
+    comp.set_option(gpu.FST_OPT_TIMING, 1)
+    try:
+        ref = comp.score(C)
+        got = comp.score_cyclic(C)
+        torch.cuda.synchronize()
+        times = comp.score_kernel_times()
+    finally:
+        comp.set_option(gpu.FST_OPT_VALIDATE, 1)
+        comp.set_option(gpu.FST_OPT_TIMING, 0)
+    for k in ("alpha", "beta", "total"):
+        assert torch.equal(got[k], ref[k]), k
+    assert times["score_gen"][1] >= got["sweeps"] > 100
