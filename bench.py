@@ -127,7 +127,7 @@ def roofline_extras(workload, kernel, achieved, copy_gbs, task="compose"):
 
 
 def host_info():
-    """CPU model and the cores this process may run on (the GPU machine's host)."""
+    """CPU model and the cores this process may run on (the host of the measured GPU)."""
     model = None
     try:
         with open("/proc/cpuinfo") as f:
